@@ -1,0 +1,164 @@
+/*
+ * phsa.h - C ABI of libphsa, the MI355X (gfx950) implementation of PHSA,
+ * Punctuation-aware Hybrid Sparse Attention (arXiv 2601.02819).
+ *
+ * The method (the paper's Section 3.2 and Algorithm 1):
+ *   1. cut the keys into T = Lk / m blocks of m tokens (Eq. 3);
+ *   2. give every block a representative key M = lambda*M0 + (1-lambda)*Mp,
+ *      where M0 is the mean of the block's keys (Eq. 6) and Mp the mean of
+ *      the keys at punctuation tokens (Eq. 7), M = M0 when the block has no
+ *      punctuation (Eq. 8 and the fallback under Eq. 7);
+ *   3. score every causal block against each query, q.M / sqrt(d) (Eq. 8),
+ *      keep the forced init blocks and the local window, and add the top-k
+ *      remaining blocks (Algorithm 1, block selection);
+ *   4. run exact softmax attention over only the selected blocks (Eq. 10-11).
+ *
+ * Conventions shared by every entry point
+ *   - All tensor pointers are DEVICE pointers; the caller owns every buffer,
+ *     including the workspace.  The library never allocates device memory and
+ *     never synchronises; all work is enqueued on `stream` (a hipStream_t, or
+ *     NULL for the default stream) and the call returns immediately.
+ *   - Layouts are contiguous row-major:
+ *       Q, O, dO, dQ     [B, Lq, Hq, d]       (dtype)
+ *       K, V, dK, dV     [B, Lk, Hkv, d]      (dtype)
+ *       punct            [B, Lk]              uint8, 1 = punctuation token
+ *       K_comp           [B, Hkv, T, d]       float32, T = Lk / m
+ *       sel              [B, Hkv, Lq, Ksel]   int32, ascending block ids,
+ *                                             padded at the end with -1
+ *       LSE              [B, Hq, Lq]          float32, natural log of
+ *                                             sum_j exp(scale * q.k_j)
+ *     with Ksel = n_init_blocks + window / block_size + 1 + top_k.
+ *   - Query row i sits at sequence position (Lk - Lq) + i: prefill has
+ *     Lq = Lk, a decode step has Lq = 1 at position Lk - 1.
+ *   - Query head h reads key/value head h / (Hq / Hkv) (grouped-query
+ *     attention).  Selection is shared by the Hq / Hkv heads of a group: a
+ *     block's group score is the sum over those heads of q_h.M / sqrt(d).
+ *   - Ties in the top-k are broken towards the lower block index.
+ *   - Validation runs on the host before anything is enqueued.  On an error
+ *     nothing is launched and no output is written.  PHSA_ERR_HIP reports a
+ *     failed launch; faults inside kernels surface at the caller's next
+ *     synchronisation of the stream.
+ *   - No C++ exception crosses this interface.
+ */
+#ifndef PHSA_H
+#define PHSA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PHSA_OK = 0,
+  PHSA_ERR_INVALID_ARG = 1, /* a scalar parameter is out of range (lambda, top_k, ...) */
+  PHSA_ERR_SHAPE = 2,       /* inconsistent sizes (Lk % m, Hq % Hkv, Lq > Lk, ...) */
+  PHSA_ERR_DTYPE = 3,       /* dtype is not PHSA_BF16 / PHSA_FP32 */
+  PHSA_ERR_NULL = 4,        /* a required pointer is NULL */
+  PHSA_ERR_WORKSPACE = 5,   /* ws_bytes < phsa_workspace_size(params, op) or ws is NULL */
+  PHSA_ERR_UNSUPPORTED = 6, /* valid for the method but outside what the kernels implement */
+  PHSA_ERR_HIP = 7          /* a HIP launch failed */
+} phsa_status;
+
+typedef enum { PHSA_BF16 = 0, PHSA_FP32 = 1 } phsa_dtype;
+
+/* Operation ids for phsa_workspace_size / phsa_validate. */
+typedef enum {
+  PHSA_OP_COMPRESS = 0,
+  PHSA_OP_SELECT = 1,
+  PHSA_OP_ATTN_FWD = 2,
+  PHSA_OP_ATTN_BWD = 3,
+  PHSA_OP_FORWARD = 4,
+  PHSA_OP_DECODE = 5
+} phsa_op;
+
+/* Problem description (Algorithm 1's inputs plus the tensor geometry). */
+typedef struct {
+  int32_t batch;         /* B  >= 1 */
+  int32_t seqlen_q;      /* Lq >= 1, Lq <= Lk */
+  int32_t seqlen_k;      /* Lk, a multiple of block_size (Eq. 3 with no tail) */
+  int32_t n_heads_q;     /* Hq, a multiple of n_heads_kv */
+  int32_t n_heads_kv;    /* Hkv >= 1 */
+  int32_t head_dim;      /* d; the kernels implement 64 and 128 */
+  int32_t block_size;    /* m, tokens per key block (Eq. 3); the kernels implement 64 */
+  int32_t top_k;         /* k, free picks after the forced blocks are excluded */
+  int32_t n_init_blocks; /* n_init, blocks 0..n_init-1 always kept (clipped to causal) */
+  int32_t window;        /* w, local window in tokens, a multiple of block_size;
+                            blocks max(0, cur - w/m) .. cur are always kept */
+  float lambda;          /* gate of Eq. 8, in [0, 1] */
+  float softmax_scale;   /* <= 0 selects 1 / sqrt(head_dim) (Eq. 2, 8, 11) */
+  int32_t dtype;         /* phsa_dtype of Q, K, V, O, dO, dQ, dK, dV */
+} phsa_params;
+
+/* Number of index slots per (query row, KV head): n_init + w/m + 1 + top_k. */
+int32_t phsa_ksel(const phsa_params *p);
+
+/* Host-only validation of `p` for operation `op` (no GPU access). */
+phsa_status phsa_validate(const phsa_params *p, int32_t op);
+
+/* Workspace bytes `op` needs for `p` (0 if none, or if `p` is invalid). */
+size_t phsa_workspace_size(const phsa_params *p, int32_t op);
+
+/* Static, human-readable name of a status code. */
+const char *phsa_status_string(phsa_status s);
+
+/* Block representatives (Eq. 6-8, Algorithm 1 representative-token step).
+ * Reads K [B, Lk, Hkv, d] and punct [B, Lk]; writes K_comp [B, Hkv, T, d]
+ * (float32, sums accumulated in float32).  Uses seqlen_k, not seqlen_q. */
+phsa_status phsa_compress(const phsa_params *p, const void *K, const uint8_t *punct, float *K_comp,
+                          void *stream);
+
+/* Relevance scoring and block selection (Eq. 8, Algorithm 1 scoring and
+ * selection).  Reads Q and K_comp; writes sel [B, Hkv, Lq, Ksel].  Scores
+ * are computed in float32 from float32 K_comp.  No workspace is needed
+ * (ws may be NULL when phsa_workspace_size(p, PHSA_OP_SELECT) is 0). */
+phsa_status phsa_select(const phsa_params *p, const void *Q, const float *K_comp, int32_t *sel,
+                        void *ws, size_t ws_bytes, void *stream);
+
+/* Sparse attention forward (Eq. 10-11, Algorithm 1 attention step) over the
+ * blocks listed in sel, with the token-level causal mask j <= position(i).
+ * Writes O [B, Lq, Hq, d] (dtype) and LSE [B, Hq, Lq].  sel rows must be
+ * ascending, duplicate-free, within 0..cur of their row, and -1 padded. */
+phsa_status phsa_attn_fwd(const phsa_params *p, const void *Q, const void *K, const void *V,
+                          const int32_t *sel, void *O, float *LSE, void *ws, size_t ws_bytes,
+                          void *stream);
+
+/* Sparse attention backward with sel held fixed (the top-k is piecewise
+ * constant, so K_comp, lambda and the mask receive no gradient).  Reads the
+ * forward tensors, dO and LSE; writes dQ [B, Lq, Hq, d] and dK, dV
+ * [B, Lk, Hkv, d] (dtype; float32 accumulation).  dK/dV sum over the heads
+ * of each group; keys that no query selected get zero gradient. */
+phsa_status phsa_attn_bwd(const phsa_params *p, const void *Q, const void *K, const void *V,
+                          const void *O, const void *dO, const float *LSE, const int32_t *sel,
+                          void *dQ, void *dK, void *dV, void *ws, size_t ws_bytes, void *stream);
+
+/* Whole forward: phsa_compress, phsa_select, phsa_attn_fwd in one call.
+ * Writes K_comp, sel, O and LSE. */
+phsa_status phsa_forward(const phsa_params *p, const void *Q, const void *K, const void *V,
+                         const uint8_t *punct, float *K_comp, int32_t *sel, void *O, float *LSE,
+                         void *ws, size_t ws_bytes, void *stream);
+
+/* One decode step (generation with a block KV cache): Lq must be 1, the
+ * query sits at position Lk - 1.  K_comp [B, Hkv, T, d] holds the cache's
+ * block representatives (from phsa_compress).  Writes sel [B, Hkv, 1, Ksel],
+ * O [B, 1, Hq, d] and LSE [B, Hq, 1]. */
+phsa_status phsa_decode(const phsa_params *p, const void *Q, const void *K_cache,
+                        const void *V_cache, const float *K_comp, int32_t *sel, void *O,
+                        float *LSE, void *ws, size_t ws_bytes, void *stream);
+
+/* Profiling aid (off by default, not thread-safe): while enabled, every
+ * kernel launch is bracketed by a pair of HIP events on its stream.
+ * phsa_timing_collect synchronises those events and returns, for the kernel
+ * named `name`, the summed duration in milliseconds and the launch count;
+ * it returns the number of distinct kernel names recorded.  phsa_timing_reset
+ * drops every record.  Event objects are created on first enable. */
+phsa_status phsa_timing_enable(int32_t enable);
+int32_t phsa_timing_collect(const char *name, double *total_ms, int64_t *count);
+void phsa_timing_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PHSA_H */

@@ -1,0 +1,371 @@
+// C ABI of libphsa: host-side validation, workspace layout and dispatch.
+// Nothing here allocates device memory; every kernel goes on the caller's stream.
+#include <math.h>
+#include <string.h>
+
+#include <exception>
+#include <vector>
+
+#include "../../include/phsa.h"
+#include "launch.h"
+
+namespace phsa {
+
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+// Carves the inverted-index workspace starting at `base` (NULL = size only).
+size_t index_layout(const Geom &g, char *base, IndexWs *ix) {
+  IndexWs w{};
+  const int64_t R = (int64_t)g.B * g.Hkv;
+  const int64_t nbgt = R * g.T;
+  w.W = (g.Lq + kIndexTile - 1) / kIndexTile;
+  w.unit_tokens = 64 * (64 / g.G);  // 64 chunks of 64 MFMA rows
+  w.nnz_max = R * g.Lq * g.ksel;
+  w.units_max = nbgt + (w.nnz_max + w.unit_tokens - 1) / w.unit_tokens;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char *p = base ? base + off : nullptr;
+    off += align_up(bytes);
+    return p;
+  };
+  w.cntw = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * R * w.W * g.T));
+  w.cnt = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * nbgt));
+  w.off = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (nbgt + 1)));
+  w.uoff = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (nbgt + 1)));
+  w.totals = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * 4));
+  w.tok = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * w.nnz_max));
+  w.units = reinterpret_cast<int2 *>(take(sizeof(int2) * w.units_max));
+  if (ix) *ix = w;
+  return off;
+}
+
+struct FwdWs {
+  IndexWs ix;
+  void *opart;
+  float2 *ml;
+};
+struct BwdWs {
+  IndexWs ix;
+  float *Dvec;
+  void *dqpart;
+  float *dkvpart;
+};
+
+size_t elem_bytes(const Geom &g) { return g.dtype == PHSA_BF16 ? 2 : 4; }
+
+size_t fwd_layout(const Geom &g, char *base, FwdWs *ws) {
+  if (g.dtype == PHSA_FP32) return 0;
+  FwdWs w{};
+  size_t off = index_layout(g, base, &w.ix);
+  const int64_t slots = (int64_t)g.B * g.Hkv * g.Lq * g.ksel * g.G;
+  w.opart = base ? base + off : nullptr;
+  off += align_up(slots * g.d * elem_bytes(g));
+  w.ml = base ? reinterpret_cast<float2 *>(base + off) : nullptr;
+  off += align_up(slots * sizeof(float2));
+  if (ws) *ws = w;
+  return off;
+}
+
+size_t bwd_layout(const Geom &g, char *base, BwdWs *ws) {
+  BwdWs w{};
+  size_t off = 0;
+  if (g.dtype == PHSA_BF16) off = index_layout(g, base, &w.ix);
+  w.Dvec = base ? reinterpret_cast<float *>(base + off) : nullptr;
+  off += align_up(sizeof(float) * (size_t)g.B * g.Hq * g.Lq);
+  if (g.dtype == PHSA_BF16) {
+    const int64_t slots = (int64_t)g.B * g.Hkv * g.Lq * g.ksel * g.G;
+    w.dqpart = base ? base + off : nullptr;
+    off += align_up(slots * g.d * elem_bytes(g));
+    w.dkvpart = base ? reinterpret_cast<float *>(base + off) : nullptr;
+    off += align_up(sizeof(float) * (size_t)w.ix.units_max * 2 * 64 * g.d);
+  }
+  if (ws) *ws = w;
+  return off;
+}
+
+size_t decode_layout(const Geom &g) {
+  return align_up(sizeof(float) * (size_t)g.B * g.Hkv * g.ksel * g.G * (g.d + 2));
+}
+
+bool is_attention_op(int op) {
+  return op == PHSA_OP_ATTN_FWD || op == PHSA_OP_ATTN_BWD || op == PHSA_OP_FORWARD || op == PHSA_OP_DECODE;
+}
+
+phsa_status validate(const phsa_params *p, int op, Geom *out) {
+  if (!p) return PHSA_ERR_NULL;
+  if (op < PHSA_OP_COMPRESS || op > PHSA_OP_DECODE) return PHSA_ERR_INVALID_ARG;
+  if (p->dtype != PHSA_BF16 && p->dtype != PHSA_FP32) return PHSA_ERR_DTYPE;
+  if (p->batch < 1 || p->seqlen_q < 1 || p->seqlen_k < 1 || p->n_heads_q < 1 || p->n_heads_kv < 1 ||
+      p->head_dim < 1 || p->block_size < 1)
+    return PHSA_ERR_SHAPE;
+  if (p->n_heads_q % p->n_heads_kv != 0) return PHSA_ERR_SHAPE;
+  if (p->seqlen_k % p->block_size != 0) return PHSA_ERR_SHAPE;
+  if (p->seqlen_q > p->seqlen_k) return PHSA_ERR_SHAPE;
+  if (op == PHSA_OP_DECODE && p->seqlen_q != 1) return PHSA_ERR_SHAPE;
+  if (p->top_k < 0 || p->n_init_blocks < 0 || p->window < 0 || p->window % p->block_size != 0)
+    return PHSA_ERR_INVALID_ARG;
+  if (!(p->lambda >= 0.f && p->lambda <= 1.f)) return PHSA_ERR_INVALID_ARG;
+  if (!isfinite(p->softmax_scale)) return PHSA_ERR_INVALID_ARG;
+  // What the kernels implement.
+  if (p->head_dim != 64 && p->head_dim != 128) return PHSA_ERR_UNSUPPORTED;
+  const int64_t T = p->seqlen_k / p->block_size;
+  const int64_t ksel = (int64_t)p->n_init_blocks + p->window / p->block_size + 1 + p->top_k;
+  const int G = p->n_heads_q / p->n_heads_kv;
+  if (ksel > 64 || p->top_k > 32) return PHSA_ERR_UNSUPPORTED;
+  if (T > 2048 || p->seqlen_q >= (1 << 25)) return PHSA_ERR_UNSUPPORTED;
+  if (p->batch > 65535 || p->n_heads_q > 65535) return PHSA_ERR_UNSUPPORTED;
+  if (is_attention_op(op)) {
+    if (p->block_size != 64) return PHSA_ERR_UNSUPPORTED;
+    if (G != 1 && G != 2 && G != 4 && G != 8) return PHSA_ERR_UNSUPPORTED;
+    const int64_t nnz = (int64_t)p->batch * p->n_heads_kv * p->seqlen_q * ksel;
+    if (nnz >= ((int64_t)1 << 31) / 2) return PHSA_ERR_UNSUPPORTED;
+  }
+  if (out) {
+    Geom g{};
+    g.B = p->batch;
+    g.Lq = p->seqlen_q;
+    g.Lk = p->seqlen_k;
+    g.Hq = p->n_heads_q;
+    g.Hkv = p->n_heads_kv;
+    g.G = G;
+    g.d = p->head_dim;
+    g.m = p->block_size;
+    g.T = (int)T;
+    g.top_k = p->top_k;
+    g.n_init = p->n_init_blocks;
+    g.window = p->window;
+    g.ksel = (int)ksel;
+    g.q_pos0 = p->seqlen_k - p->seqlen_q;
+    g.lambda = p->lambda;
+    g.scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.f / sqrtf((float)p->head_dim);
+    g.dtype = p->dtype;
+    *out = g;
+  }
+  return PHSA_OK;
+}
+
+size_t workspace_bytes(const Geom &g, int op) {
+  switch (op) {
+    case PHSA_OP_ATTN_FWD:
+    case PHSA_OP_FORWARD: return fwd_layout(g, nullptr, nullptr);
+    case PHSA_OP_ATTN_BWD: return bwd_layout(g, nullptr, nullptr);
+    case PHSA_OP_DECODE: return decode_layout(g);
+    default: return 0;
+  }
+}
+
+phsa_status check_ws(const Geom &g, int op, const void *ws, size_t ws_bytes) {
+  const size_t need = workspace_bytes(g, op);
+  if (need == 0) return PHSA_OK;
+  if (!ws || ws_bytes < need) return PHSA_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0) return PHSA_ERR_WORKSPACE;
+  return PHSA_OK;
+}
+
+phsa_status from_hip(hipError_t e) { return e == hipSuccess ? PHSA_OK : PHSA_ERR_HIP; }
+
+// ---------------------------------------------------------------- timing
+struct TimingRec {
+  const char *name;
+  hipEvent_t a, b;
+};
+bool g_timing = false;
+std::vector<TimingRec> g_recs;
+std::vector<std::pair<hipEvent_t, hipEvent_t>> g_pool;
+TimingRec g_open{nullptr, nullptr, nullptr};
+
+}  // namespace
+
+void timing_begin(const char *name, hipStream_t s) {
+  if (!g_timing) return;
+  std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
+  if (!g_pool.empty()) {
+    ev = g_pool.back();
+    g_pool.pop_back();
+  } else if (hipEventCreate(&ev.first) != hipSuccess || hipEventCreate(&ev.second) != hipSuccess) {
+    return;
+  }
+  g_open = TimingRec{name, ev.first, ev.second};
+  (void)hipEventRecord(ev.first, s);
+}
+
+void timing_end(hipStream_t s) {
+  if (!g_timing || !g_open.name) return;
+  (void)hipEventRecord(g_open.b, s);
+  g_recs.push_back(g_open);
+  g_open = TimingRec{nullptr, nullptr, nullptr};
+}
+
+}  // namespace phsa
+
+using namespace phsa;
+
+#define PHSA_GUARD(body)            \
+  try {                             \
+    body                            \
+  } catch (const std::exception &) { \
+    return PHSA_ERR_HIP;            \
+  } catch (...) {                   \
+    return PHSA_ERR_HIP;            \
+  }
+
+extern "C" {
+
+int32_t phsa_ksel(const phsa_params *p) {
+  if (!p || p->block_size < 1) return 0;
+  return p->n_init_blocks + p->window / p->block_size + 1 + p->top_k;
+}
+
+phsa_status phsa_validate(const phsa_params *p, int32_t op) { return validate(p, op, nullptr); }
+
+size_t phsa_workspace_size(const phsa_params *p, int32_t op) {
+  Geom g;
+  if (validate(p, op, &g) != PHSA_OK) return 0;
+  return workspace_bytes(g, op);
+}
+
+const char *phsa_status_string(phsa_status s) {
+  switch (s) {
+    case PHSA_OK: return "ok";
+    case PHSA_ERR_INVALID_ARG: return "invalid argument";
+    case PHSA_ERR_SHAPE: return "inconsistent shape";
+    case PHSA_ERR_DTYPE: return "unknown dtype";
+    case PHSA_ERR_NULL: return "null pointer";
+    case PHSA_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+    case PHSA_ERR_UNSUPPORTED: return "configuration not implemented by the kernels";
+    case PHSA_ERR_HIP: return "HIP launch failure";
+  }
+  return "unknown status";
+}
+
+phsa_status phsa_compress(const phsa_params *p, const void *K, const uint8_t *punct, float *K_comp, void *stream) {
+  PHSA_GUARD({
+    Geom g;
+    phsa_status st = validate(p, PHSA_OP_COMPRESS, &g);
+    if (st != PHSA_OK) return st;
+    if (!K || !punct || !K_comp) return PHSA_ERR_NULL;
+    return from_hip(launch_compress(g, K, punct, K_comp, static_cast<hipStream_t>(stream)));
+  })
+}
+
+phsa_status phsa_select(const phsa_params *p, const void *Q, const float *K_comp, int32_t *sel, void *ws,
+                        size_t ws_bytes, void *stream) {
+  PHSA_GUARD({
+    Geom g;
+    phsa_status st = validate(p, PHSA_OP_SELECT, &g);
+    if (st != PHSA_OK) return st;
+    if (!Q || !K_comp || !sel) return PHSA_ERR_NULL;
+    if ((st = check_ws(g, PHSA_OP_SELECT, ws, ws_bytes)) != PHSA_OK) return st;
+    return from_hip(launch_select(g, Q, K_comp, sel, static_cast<hipStream_t>(stream)));
+  })
+}
+
+phsa_status phsa_attn_fwd(const phsa_params *p, const void *Q, const void *K, const void *V, const int32_t *sel,
+                          void *O, float *LSE, void *ws, size_t ws_bytes, void *stream) {
+  PHSA_GUARD({
+    Geom g;
+    phsa_status st = validate(p, PHSA_OP_ATTN_FWD, &g);
+    if (st != PHSA_OK) return st;
+    if (!Q || !K || !V || !sel || !O || !LSE) return PHSA_ERR_NULL;
+    if ((st = check_ws(g, PHSA_OP_ATTN_FWD, ws, ws_bytes)) != PHSA_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (g.dtype == PHSA_FP32)
+      return from_hip(launch_attn_fwd_fp32(g, static_cast<const float *>(Q), static_cast<const float *>(K),
+                                           static_cast<const float *>(V), sel, static_cast<float *>(O), LSE, s));
+    FwdWs w;
+    fwd_layout(g, static_cast<char *>(ws), &w);
+    return from_hip(launch_attn_fwd(g, Q, K, V, sel, O, LSE, w.ix, w.opart, w.ml, s));
+  })
+}
+
+phsa_status phsa_attn_bwd(const phsa_params *p, const void *Q, const void *K, const void *V, const void *O,
+                          const void *dO, const float *LSE, const int32_t *sel, void *dQ, void *dK, void *dV, void *ws,
+                          size_t ws_bytes, void *stream) {
+  PHSA_GUARD({
+    Geom g;
+    phsa_status st = validate(p, PHSA_OP_ATTN_BWD, &g);
+    if (st != PHSA_OK) return st;
+    if (!Q || !K || !V || !O || !dO || !LSE || !sel || !dQ || !dK || !dV) return PHSA_ERR_NULL;
+    if ((st = check_ws(g, PHSA_OP_ATTN_BWD, ws, ws_bytes)) != PHSA_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    BwdWs w;
+    bwd_layout(g, static_cast<char *>(ws), &w);
+    if (g.dtype == PHSA_FP32)
+      return from_hip(launch_attn_bwd_fp32(g, static_cast<const float *>(Q), static_cast<const float *>(K),
+                                           static_cast<const float *>(V), static_cast<const float *>(O),
+                                           static_cast<const float *>(dO), LSE, sel, static_cast<float *>(dQ),
+                                           static_cast<float *>(dK), static_cast<float *>(dV), w.Dvec, s));
+    return from_hip(launch_attn_bwd(g, Q, K, V, O, dO, LSE, sel, dQ, dK, dV, w.ix, w.Dvec, w.dqpart, w.dkvpart, s));
+  })
+}
+
+phsa_status phsa_forward(const phsa_params *p, const void *Q, const void *K, const void *V, const uint8_t *punct,
+                         float *K_comp, int32_t *sel, void *O, float *LSE, void *ws, size_t ws_bytes, void *stream) {
+  PHSA_GUARD({
+    Geom g;
+    phsa_status st = validate(p, PHSA_OP_FORWARD, &g);
+    if (st != PHSA_OK) return st;
+    if (!Q || !K || !V || !punct || !K_comp || !sel || !O || !LSE) return PHSA_ERR_NULL;
+    if ((st = check_ws(g, PHSA_OP_FORWARD, ws, ws_bytes)) != PHSA_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = launch_compress(g, K, punct, K_comp, s);
+    if (e == hipSuccess) e = launch_select(g, Q, K_comp, sel, s);
+    if (e != hipSuccess) return PHSA_ERR_HIP;
+    if (g.dtype == PHSA_FP32)
+      return from_hip(launch_attn_fwd_fp32(g, static_cast<const float *>(Q), static_cast<const float *>(K),
+                                           static_cast<const float *>(V), sel, static_cast<float *>(O), LSE, s));
+    FwdWs w;
+    fwd_layout(g, static_cast<char *>(ws), &w);
+    return from_hip(launch_attn_fwd(g, Q, K, V, sel, O, LSE, w.ix, w.opart, w.ml, s));
+  })
+}
+
+phsa_status phsa_decode(const phsa_params *p, const void *Q, const void *K_cache, const void *V_cache,
+                        const float *K_comp, int32_t *sel, void *O, float *LSE, void *ws, size_t ws_bytes,
+                        void *stream) {
+  PHSA_GUARD({
+    Geom g;
+    phsa_status st = validate(p, PHSA_OP_DECODE, &g);
+    if (st != PHSA_OK) return st;
+    if (!Q || !K_cache || !V_cache || !K_comp || !sel || !O || !LSE) return PHSA_ERR_NULL;
+    if ((st = check_ws(g, PHSA_OP_DECODE, ws, ws_bytes)) != PHSA_OK) return st;
+    return from_hip(launch_decode(g, Q, K_cache, V_cache, K_comp, sel, O, LSE, static_cast<float *>(ws),
+                                  static_cast<hipStream_t>(stream)));
+  })
+}
+
+phsa_status phsa_timing_enable(int32_t enable) {
+  g_timing = enable != 0;
+  return PHSA_OK;
+}
+
+int32_t phsa_timing_collect(const char *name, double *total_ms, int64_t *count) {
+  double tot = 0.0;
+  int64_t n = 0;
+  std::vector<const char *> names;
+  for (const TimingRec &r : g_recs) {
+    bool seen = false;
+    for (const char *x : names) seen = seen || strcmp(x, r.name) == 0;
+    if (!seen) names.push_back(r.name);
+    if (name && strcmp(name, r.name) == 0) {
+      float ms = 0.f;
+      if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+        tot += ms;
+        ++n;
+      }
+    }
+  }
+  if (total_ms) *total_ms = tot;
+  if (count) *count = n;
+  return (int32_t)names.size();
+}
+
+void phsa_timing_reset(void) {
+  for (const TimingRec &r : g_recs) g_pool.emplace_back(r.a, r.b);
+  g_recs.clear();
+}
+
+}  // extern "C"

@@ -1,0 +1,150 @@
+// Inverted selection index: for every (b, g, block t) the ascending list of
+// query rows whose selection contains t (the transpose of sel), plus a table
+// of attention work units (a unit = one block and up to unit_tokens entries of
+// its list).  This lets the attention kernels run key-block-major: one K/V
+// tile is loaded once and meets every query row that selected it.
+//
+// Entries are (row << 6) | slot, where slot is the position of t in the row's
+// sel vector, so results can be written per (row, slot) without searching.
+//
+// Four integer-only passes, all deterministic (no order depends on timing):
+//   count : per 256-row tile, an LDS bitmap [T][256 bits] of who selected
+//           what; popcounts give per-tile counts cntw[bg][w][t].
+//   scan1 : per (bg, t), exclusive prefix over tiles -> cntw, total -> cnt.
+//   scan2 : one workgroup scans cnt into list offsets and unit offsets and
+//           writes the unit table.
+//   fill  : rebuilds the tile bitmap; an entry's place in its list is
+//           tile offset + number of lower rows in the tile that chose t.
+#include "common.h"
+#include "launch.h"
+
+namespace phsa {
+
+__device__ __forceinline__ bool slot_valid(int t, int cur, int T) { return t >= 0 && t <= cur && t < T; }
+
+__device__ void build_tile_bitmap(uint32_t *bm, const int32_t *sel, const Geom &gm, int bg, int w) {
+  const int tid = threadIdx.x;
+  for (int x = tid; x < gm.T * 8; x += 256) bm[x] = 0u;
+  __syncthreads();
+  const int i = w * kIndexTile + tid;
+  if (i < gm.Lq) {
+    const int cur = (gm.q_pos0 + i) / gm.m;
+    const int32_t *row = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
+    for (int s = 0; s < gm.ksel; ++s) {
+      const int t = row[s];
+      if (slot_valid(t, cur, gm.T)) atomicOr(&bm[t * 8 + (tid >> 5)], 1u << (tid & 31));
+    }
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(256) void index_count_kernel(const int32_t *__restrict__ sel, Geom gm, IndexWs ix) {
+  extern __shared__ uint32_t bm[];
+  const int w = blockIdx.x, bg = blockIdx.y;
+  build_tile_bitmap(bm, sel, gm, bg, w);
+  int32_t *dst = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
+  for (int t = threadIdx.x; t < gm.T; t += 256) {
+    int c = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) c += __popc(bm[t * 8 + k]);
+    dst[t] = c;
+  }
+}
+
+__global__ __launch_bounds__(256) void index_scan_tiles_kernel(Geom gm, IndexWs ix, int nbgt) {
+  const int x = blockIdx.x * 256 + threadIdx.x;
+  if (x >= nbgt) return;
+  const int bg = x / gm.T, t = x % gm.T;
+  int32_t *col = ix.cntw + (int64_t)bg * ix.W * gm.T + t;
+  int run = 0;
+  for (int w = 0; w < ix.W; ++w) {
+    const int c = col[(int64_t)w * gm.T];
+    col[(int64_t)w * gm.T] = run;
+    run += c;
+  }
+  ix.cnt[x] = run;
+}
+
+// Single workgroup of 1024 threads: exclusive scans of list lengths and of
+// units per list, then the unit table.
+__global__ __launch_bounds__(1024) void index_scan_lists_kernel(Geom gm, IndexWs ix, int nbgt) {
+  __shared__ int s_a[1024], s_b[1024];
+  const int tid = threadIdx.x;
+  const int per = (nbgt + 1023) / 1024;
+  const int lo = min(nbgt, tid * per), hi = min(nbgt, lo + per);
+  const int U = ix.unit_tokens;
+  int sa = 0, sb = 0;
+  for (int x = lo; x < hi; ++x) {
+    const int c = ix.cnt[x];
+    sa += c;
+    sb += (c + U - 1) / U;
+  }
+  s_a[tid] = sa;
+  s_b[tid] = sb;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {  // inclusive Hillis-Steele scan
+    const int va = tid >= o ? s_a[tid - o] : 0;
+    const int vb = tid >= o ? s_b[tid - o] : 0;
+    __syncthreads();
+    s_a[tid] += va;
+    s_b[tid] += vb;
+    __syncthreads();
+  }
+  int ra = s_a[tid] - sa, rb = s_b[tid] - sb;
+  for (int x = lo; x < hi; ++x) {
+    const int c = ix.cnt[x];
+    const int nu = (c + U - 1) / U;
+    ix.off[x] = ra;
+    ix.uoff[x] = rb;
+    for (int u = 0; u < nu; ++u) ix.units[rb + u] = make_int2(x, u * U);
+    ra += c;
+    rb += nu;
+  }
+  if (tid == 1023) {
+    ix.off[nbgt] = s_a[1023];
+    ix.uoff[nbgt] = s_b[1023];
+    ix.totals[0] = s_a[1023];
+    ix.totals[1] = s_b[1023];
+  }
+}
+
+__global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restrict__ sel, Geom gm, IndexWs ix) {
+  extern __shared__ uint32_t bm[];
+  const int w = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x;
+  build_tile_bitmap(bm, sel, gm, bg, w);
+  const int i = w * kIndexTile + tid;
+  if (i >= gm.Lq) return;
+  const int cur = (gm.q_pos0 + i) / gm.m;
+  const int32_t *row = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
+  const int32_t *tile_off = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
+  const int word = tid >> 5;
+  const uint32_t below = (1u << (tid & 31)) - 1u;
+  for (int s = 0; s < gm.ksel; ++s) {
+    const int t = row[s];
+    if (!slot_valid(t, cur, gm.T)) continue;
+    int rank = __popc(bm[t * 8 + word] & below);
+    for (int k = 0; k < word; ++k) rank += __popc(bm[t * 8 + k]);
+    const int64_t pos = (int64_t)ix.off[bg * gm.T + t] + tile_off[t] + rank;
+    ix.tok[pos] = (i << 6) | s;
+  }
+}
+
+hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &ix, hipStream_t s) {
+  const int nbgt = g.B * g.Hkv * g.T;
+  const size_t lds = (size_t)g.T * 8 * sizeof(uint32_t);
+  timing_begin("phsa_index_count", s);
+  hipLaunchKernelGGL(index_count_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds, s, sel, g, ix);
+  timing_end(s);
+  timing_begin("phsa_index_scan_tiles", s);
+  hipLaunchKernelGGL(index_scan_tiles_kernel, dim3((nbgt + 255) / 256), dim3(256), 0, s, g, ix, nbgt);
+  timing_end(s);
+  timing_begin("phsa_index_scan_lists", s);
+  hipLaunchKernelGGL(index_scan_lists_kernel, dim3(1), dim3(1024), 0, s, g, ix, nbgt);
+  timing_end(s);
+  timing_begin("phsa_index_fill", s);
+  hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds, s, sel, g, ix);
+  timing_end(s);
+  return hipGetLastError();
+}
+
+}  // namespace phsa

@@ -1,0 +1,59 @@
+// Internal launchers: one per kernel family.  The C ABI (api.hip) validates
+// every argument before calling any of these; launchers only enqueue work.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace phsa {
+
+// Geometry resolved once by the ABI layer.
+struct Geom {
+  int B, Lq, Lk, Hq, Hkv, G, d, m, T;
+  int top_k, n_init, window, ksel;
+  int q_pos0;         // position of query row 0 = Lk - Lq
+  float lambda;
+  float scale;        // softmax scale
+  int dtype;          // 0 bf16, 1 fp32
+};
+
+// Index (inverted selection) workspace, carved out of the caller's buffer.
+struct IndexWs {
+  int W;              // query tiles of kIndexTile rows
+  int unit_tokens;    // list entries per attention work unit
+  int64_t units_max;  // upper bound on the number of work units
+  int64_t nnz_max;    // upper bound on list entries
+  int32_t *cntw;      // [B*Hkv, W, T]  per-tile counts, then per-tile list offsets
+  int32_t *cnt;       // [B*Hkv*T]      list length per (b, g, t)
+  int32_t *off;       // [B*Hkv*T + 1]  list start per (b, g, t)
+  int32_t *uoff;      // [B*Hkv*T + 1]  first work unit per (b, g, t)
+  int32_t *totals;    // [4]            nnz, n_units
+  int32_t *tok;       // [nnz_max]      (query row << 6) | slot, ascending row per list
+  int2 *units;        // [units_max]    (b*Hkv*T + g*T + t, first list entry)
+};
+
+constexpr int kIndexTile = 256;  // query rows per index-building workgroup
+
+// Kernel timing hooks (no-ops unless phsa_timing_enable(1)).
+void timing_begin(const char *name, hipStream_t s);
+void timing_end(hipStream_t s);
+
+hipError_t launch_compress(const Geom &g, const void *K, const uint8_t *punct, float *Kc, hipStream_t s);
+hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t *sel, hipStream_t s);
+hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &ix, hipStream_t s);
+hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel,
+                           void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s);
+hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
+                           const void *dO, const float *LSE, const int32_t *sel, void *dQ, void *dK, void *dV,
+                           const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart, hipStream_t s);
+hipError_t launch_bwd_pre(const Geom &g, const void *O, const void *dO, float *Dvec, hipStream_t s);
+hipError_t launch_attn_fwd_fp32(const Geom &g, const float *Q, const float *K, const float *V,
+                                const int32_t *sel, float *O, float *LSE, hipStream_t s);
+hipError_t launch_attn_bwd_fp32(const Geom &g, const float *Q, const float *K, const float *V,
+                                const float *O, const float *dO, const float *LSE, const int32_t *sel,
+                                float *dQ, float *dK, float *dV, float *Dvec, hipStream_t s);
+hipError_t launch_decode(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc,
+                         int32_t *sel, void *O, float *LSE, float *part, hipStream_t s);
+
+}  // namespace phsa

@@ -1,0 +1,247 @@
+"""Thin ctypes binding over libphsa (see include/phsa.h).
+
+Argument marshalling only: every step of PHSA runs in the HIP kernels of
+``libphsa.so``.  torch supplies device memory and the current HIP stream.
+If the library has not been built this module raises; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libphsa.so")
+
+OK, ERR_INVALID_ARG, ERR_SHAPE, ERR_DTYPE, ERR_NULL, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP = range(8)
+BF16, FP32 = 0, 1
+OP_COMPRESS, OP_SELECT, OP_ATTN_FWD, OP_ATTN_BWD, OP_FORWARD, OP_DECODE = range(6)
+
+EXPORTS = (
+    "phsa_ksel", "phsa_validate", "phsa_workspace_size", "phsa_status_string", "phsa_compress",
+    "phsa_select", "phsa_attn_fwd", "phsa_attn_bwd", "phsa_forward", "phsa_decode",
+    "phsa_timing_enable", "phsa_timing_collect", "phsa_timing_reset",
+)
+
+
+class Params(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32), ("seqlen_q", ctypes.c_int32), ("seqlen_k", ctypes.c_int32),
+        ("n_heads_q", ctypes.c_int32), ("n_heads_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32), ("top_k", ctypes.c_int32), ("n_init_blocks", ctypes.c_int32),
+        ("window", ctypes.c_int32), ("lam", ctypes.c_float), ("softmax_scale", ctypes.c_float),
+        ("dtype", ctypes.c_int32),
+    ]
+
+
+class PHSAError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libphsa.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2601_02819_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, PP = ctypes.POINTER(Params), ctypes.c_void_p
+        sig = {
+            "phsa_ksel": (ctypes.c_int32, [P]),
+            "phsa_validate": (ctypes.c_int, [P, ctypes.c_int32]),
+            "phsa_workspace_size": (ctypes.c_size_t, [P, ctypes.c_int32]),
+            "phsa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+            "phsa_compress": (ctypes.c_int, [P, PP, PP, PP, PP]),
+            "phsa_select": (ctypes.c_int, [P, PP, PP, PP, PP, ctypes.c_size_t, PP]),
+            "phsa_attn_fwd": (ctypes.c_int, [P, PP, PP, PP, PP, PP, PP, PP, ctypes.c_size_t, PP]),
+            "phsa_attn_bwd": (ctypes.c_int, [P] + [PP] * 11 + [ctypes.c_size_t, PP]),
+            "phsa_forward": (ctypes.c_int, [P] + [PP] * 9 + [ctypes.c_size_t, PP]),
+            "phsa_decode": (ctypes.c_int, [P] + [PP] * 8 + [ctypes.c_size_t, PP]),
+            "phsa_timing_enable": (ctypes.c_int, [ctypes.c_int32]),
+            "phsa_timing_collect": (ctypes.c_int32, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                                     ctypes.POINTER(ctypes.c_int64)]),
+            "phsa_timing_reset": (None, []),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().phsa_status_string(int(status)).decode()
+
+
+@dataclasses.dataclass(frozen=True)
+class Config:
+    """Algorithm 1 hyperparameters (block size m, top-k, n_init, window w, gate lambda)."""
+    block_size: int = 64
+    top_k: int = 12
+    n_init_blocks: int = 1
+    window: int = 0
+    lam: float = 0.5
+    softmax_scale: float = 0.0   # <= 0: 1 / sqrt(head_dim)
+
+    @property
+    def ksel(self) -> int:
+        return self.n_init_blocks + self.window // self.block_size + 1 + self.top_k
+
+
+def make_params(cfg: Config, batch: int, seqlen_q: int, seqlen_k: int, n_heads_q: int, n_heads_kv: int,
+                head_dim: int, dtype) -> Params:
+    code = BF16 if dtype in (torch.bfloat16, BF16) else FP32 if dtype in (torch.float32, FP32) else 99
+    return Params(batch, seqlen_q, seqlen_k, n_heads_q, n_heads_kv, head_dim, cfg.block_size, cfg.top_k,
+                  cfg.n_init_blocks, cfg.window, cfg.lam, cfg.softmax_scale, code)
+
+
+def workspace_size(p: Params, op: int) -> int:
+    return int(lib().phsa_workspace_size(ctypes.byref(p), op))
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _check(st: int, where: str):
+    if st != OK:
+        raise PHSAError(st, where)
+
+
+def _dev(*ts):
+    for t in ts:
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous device tensors")
+
+
+def _workspace(p: Params, op: int, ws: Optional[torch.Tensor], device) -> Optional[torch.Tensor]:
+    need = workspace_size(p, op)
+    if need == 0:
+        return ws
+    if ws is not None and ws.numel() >= need:
+        return ws
+    return torch.empty(need, dtype=torch.uint8, device=device)
+
+
+def compress(k: torch.Tensor, punct: torch.Tensor, cfg: Config) -> torch.Tensor:
+    """K [B, Lk, Hkv, d], punct uint8 [B, Lk] -> K_comp float32 [B, Hkv, T, d]."""
+    _dev(k, punct)
+    B, Lk, Hkv, d = k.shape
+    p = make_params(cfg, B, Lk, Lk, Hkv, Hkv, d, k.dtype)
+    kc = torch.empty(B, Hkv, Lk // cfg.block_size, d, dtype=torch.float32, device=k.device)
+    _check(lib().phsa_compress(ctypes.byref(p), _ptr(k), _ptr(punct), _ptr(kc), _stream()), "phsa_compress")
+    return kc
+
+
+def select(q: torch.Tensor, kc: torch.Tensor, seqlen_k: int, cfg: Config) -> torch.Tensor:
+    """Q [B, Lq, Hq, d], K_comp [B, Hkv, T, d] -> sel int32 [B, Hkv, Lq, Ksel]."""
+    _dev(q, kc)
+    B, Lq, Hq, d = q.shape
+    Hkv = kc.shape[1]
+    p = make_params(cfg, B, Lq, seqlen_k, Hq, Hkv, d, q.dtype)
+    sel = torch.empty(B, Hkv, Lq, cfg.ksel, dtype=torch.int32, device=q.device)
+    _check(lib().phsa_select(ctypes.byref(p), _ptr(q), _ptr(kc), _ptr(sel), None, 0, _stream()), "phsa_select")
+    return sel
+
+
+def attn_fwd(q, k, v, sel, cfg: Config, ws: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Sparse attention forward -> (O [B, Lq, Hq, d], LSE float32 [B, Hq, Lq])."""
+    _dev(q, k, v, sel)
+    B, Lq, Hq, d = q.shape
+    Lk, Hkv = k.shape[1], k.shape[2]
+    p = make_params(cfg, B, Lq, Lk, Hq, Hkv, d, q.dtype)
+    o = torch.empty_like(q)
+    lse = torch.empty(B, Hq, Lq, dtype=torch.float32, device=q.device)
+    w = _workspace(p, OP_ATTN_FWD, ws, q.device)
+    _check(lib().phsa_attn_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(sel), _ptr(o), _ptr(lse), _ptr(w),
+                               w.numel() if w is not None else 0, _stream()), "phsa_attn_fwd")
+    return o, lse
+
+
+def attn_bwd(q, k, v, o, do, lse, sel, cfg: Config, ws: Optional[torch.Tensor] = None):
+    """Sparse attention backward (selection fixed) -> (dQ, dK, dV)."""
+    _dev(q, k, v, o, do, lse, sel)
+    B, Lq, Hq, d = q.shape
+    Lk, Hkv = k.shape[1], k.shape[2]
+    p = make_params(cfg, B, Lq, Lk, Hq, Hkv, d, q.dtype)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    w = _workspace(p, OP_ATTN_BWD, ws, q.device)
+    _check(lib().phsa_attn_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(sel),
+                               _ptr(dq), _ptr(dk), _ptr(dv), _ptr(w), w.numel() if w is not None else 0, _stream()),
+           "phsa_attn_bwd")
+    return dq, dk, dv
+
+
+def forward(q, k, v, punct, cfg: Config, ws: Optional[torch.Tensor] = None):
+    """compress + select + sparse attention -> (K_comp, sel, O, LSE)."""
+    _dev(q, k, v, punct)
+    B, Lq, Hq, d = q.shape
+    Lk, Hkv = k.shape[1], k.shape[2]
+    p = make_params(cfg, B, Lq, Lk, Hq, Hkv, d, q.dtype)
+    kc = torch.empty(B, Hkv, Lk // cfg.block_size, d, dtype=torch.float32, device=q.device)
+    sel = torch.empty(B, Hkv, Lq, cfg.ksel, dtype=torch.int32, device=q.device)
+    o = torch.empty_like(q)
+    lse = torch.empty(B, Hq, Lq, dtype=torch.float32, device=q.device)
+    w = _workspace(p, OP_FORWARD, ws, q.device)
+    _check(lib().phsa_forward(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(punct), _ptr(kc), _ptr(sel), _ptr(o),
+                              _ptr(lse), _ptr(w), w.numel() if w is not None else 0, _stream()), "phsa_forward")
+    return kc, sel, o, lse
+
+
+def decode(q, k_cache, v_cache, kc, cfg: Config, ws: Optional[torch.Tensor] = None):
+    """One decode step: q [B, 1, Hq, d] at position Lk - 1 -> (sel, O, LSE)."""
+    _dev(q, k_cache, v_cache, kc)
+    B, Lq, Hq, d = q.shape
+    Lk, Hkv = k_cache.shape[1], k_cache.shape[2]
+    p = make_params(cfg, B, Lq, Lk, Hq, Hkv, d, q.dtype)
+    sel = torch.empty(B, Hkv, Lq, cfg.ksel, dtype=torch.int32, device=q.device)
+    o = torch.empty_like(q)
+    lse = torch.empty(B, Hq, Lq, dtype=torch.float32, device=q.device)
+    w = _workspace(p, OP_DECODE, ws, q.device)
+    _check(lib().phsa_decode(ctypes.byref(p), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kc), _ptr(sel), _ptr(o),
+                             _ptr(lse), _ptr(w), w.numel() if w is not None else 0, _stream()), "phsa_decode")
+    return sel, o, lse
+
+
+class SparseAttention(torch.autograd.Function):
+    """Autograd wrapper: forward = phsa_attn_fwd, backward = phsa_attn_bwd (selection fixed)."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, sel, cfg: Config):
+        o, lse = attn_fwd(q, k, v, sel, cfg)
+        ctx.save_for_backward(q, k, v, o, lse, sel)
+        ctx.cfg = cfg
+        return o
+
+    @staticmethod
+    def backward(ctx, do):
+        q, k, v, o, lse, sel = ctx.saved_tensors
+        dq, dk, dv = attn_bwd(q, k, v, o, do.contiguous(), lse, sel, ctx.cfg)
+        return dq, dk, dv, None, None
+
+
+def timing_enable(on: bool = True) -> None:
+    lib().phsa_timing_enable(1 if on else 0)
+
+
+def timing_collect(name: str) -> Tuple[float, int]:
+    ms, n = ctypes.c_double(0.0), ctypes.c_int64(0)
+    lib().phsa_timing_collect(name.encode(), ctypes.byref(ms), ctypes.byref(n))
+    return ms.value, n.value
+
+
+def timing_reset() -> None:
+    lib().phsa_timing_reset()

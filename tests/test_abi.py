@@ -1,0 +1,100 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the header
+declares, and rejects bad arguments on the host before anything is launched."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2601_02819_amd import phsa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "phsa.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(phsa_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == sorted(phsa.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(phsa.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def _p(**kw):
+    base = dict(batch=1, seqlen_q=1024, seqlen_k=1024, n_heads_q=2, n_heads_kv=1, head_dim=64, block_size=64,
+                top_k=2, n_init_blocks=1, window=0, lam=0.5, softmax_scale=0.0, dtype=phsa.BF16)
+    base.update(kw)
+    return phsa.Params(*[base[f] for f, _ in phsa.Params._fields_])
+
+
+@pytest.mark.parametrize("kw,op,code", [
+    ({}, phsa.OP_ATTN_FWD, phsa.OK),
+    ({"dtype": phsa.FP32}, phsa.OP_ATTN_BWD, phsa.OK),
+    ({"dtype": 7}, phsa.OP_COMPRESS, phsa.ERR_DTYPE),
+    ({"seqlen_k": 1000}, phsa.OP_COMPRESS, phsa.ERR_SHAPE),             # Lk % m != 0
+    ({"n_heads_q": 3, "n_heads_kv": 2}, phsa.OP_SELECT, phsa.ERR_SHAPE),  # Hq % Hkv != 0
+    ({"seqlen_q": 2048}, phsa.OP_SELECT, phsa.ERR_SHAPE),               # Lq > Lk
+    ({"batch": 0}, phsa.OP_SELECT, phsa.ERR_SHAPE),
+    ({"window": 10}, phsa.OP_SELECT, phsa.ERR_INVALID_ARG),             # w % m != 0
+    ({"top_k": -1}, phsa.OP_SELECT, phsa.ERR_INVALID_ARG),
+    ({"lam": 1.5}, phsa.OP_COMPRESS, phsa.ERR_INVALID_ARG),
+    ({"lam": float("nan")}, phsa.OP_COMPRESS, phsa.ERR_INVALID_ARG),
+    ({"softmax_scale": float("inf")}, phsa.OP_SELECT, phsa.ERR_INVALID_ARG),
+    ({"head_dim": 96}, phsa.OP_SELECT, phsa.ERR_UNSUPPORTED),
+    ({"top_k": 40}, phsa.OP_SELECT, phsa.ERR_UNSUPPORTED),
+    ({"block_size": 32}, phsa.OP_ATTN_FWD, phsa.ERR_UNSUPPORTED),
+    ({"block_size": 32}, phsa.OP_SELECT, phsa.OK),
+    ({"n_heads_q": 6, "n_heads_kv": 2}, phsa.OP_ATTN_FWD, phsa.ERR_UNSUPPORTED),   # G = 3
+    ({"seqlen_q": 2}, phsa.OP_DECODE, phsa.ERR_SHAPE),
+    ({"seqlen_q": 1}, phsa.OP_DECODE, phsa.OK),
+    ({}, 17, phsa.ERR_INVALID_ARG),
+])
+def test_validate(kw, op, code):
+    assert phsa.lib().phsa_validate(ctypes.byref(_p(**kw)), op) == code
+
+
+def test_ksel_and_workspace():
+    L = phsa.lib()
+    p = _p(n_init_blocks=2, window=128, top_k=5)
+    assert L.phsa_ksel(ctypes.byref(p)) == 2 + 2 + 1 + 5
+    assert phsa.workspace_size(_p(), phsa.OP_COMPRESS) == 0
+    assert phsa.workspace_size(_p(), phsa.OP_SELECT) == 0
+    fwd = phsa.workspace_size(_p(), phsa.OP_ATTN_FWD)
+    assert fwd > 0 and fwd % 256 == 0
+    assert phsa.workspace_size(_p(batch=2), phsa.OP_ATTN_FWD) > fwd
+    assert phsa.workspace_size(_p(dtype=phsa.FP32), phsa.OP_ATTN_FWD) == 0
+    assert phsa.workspace_size(_p(seqlen_q=1), phsa.OP_DECODE) > 0
+    assert phsa.workspace_size(_p(head_dim=96), phsa.OP_ATTN_FWD) == 0     # invalid -> 0
+    assert L.phsa_validate(None, phsa.OP_SELECT) == phsa.ERR_NULL
+
+
+def test_entry_points_reject_before_launch():
+    """Every error return happens on the host: no device pointer is touched."""
+    L = phsa.lib()
+    bogus = ctypes.c_void_p(0x1000)
+    good = _p()
+    bad = _p(seqlen_k=1000)
+    assert L.phsa_compress(ctypes.byref(bad), bogus, bogus, bogus, None) == phsa.ERR_SHAPE
+    assert L.phsa_compress(ctypes.byref(good), None, bogus, bogus, None) == phsa.ERR_NULL
+    assert L.phsa_select(ctypes.byref(good), bogus, None, bogus, None, 0, None) == phsa.ERR_NULL
+    assert L.phsa_attn_fwd(ctypes.byref(good), bogus, bogus, bogus, bogus, bogus, bogus, None, 0,
+                           None) == phsa.ERR_WORKSPACE
+    assert L.phsa_attn_fwd(ctypes.byref(good), bogus, bogus, bogus, bogus, bogus, bogus, bogus, 16,
+                           None) == phsa.ERR_WORKSPACE
+    assert L.phsa_attn_bwd(ctypes.byref(_p(dtype=5)), *([bogus] * 11), 0, None) == phsa.ERR_DTYPE
+    assert L.phsa_forward(ctypes.byref(good), *([bogus] * 8), None, 0, None) == phsa.ERR_WORKSPACE
+    assert L.phsa_decode(ctypes.byref(good), *([bogus] * 7), None, 0, None) == phsa.ERR_SHAPE  # Lq != 1
+
+
+def test_status_strings():
+    for s in range(8):
+        assert isinstance(phsa.status_string(s), str) and phsa.status_string(s)
+    assert phsa.status_string(99) == "unknown status"

@@ -1,0 +1,144 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times, on outputs the oracle computes one by one: sampled query rows
+(selection, O, LSE, dQ) and sampled key blocks (dK, dV)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2601_02819_amd import phsa
+from paper_2601_02819_amd.inputs import WORKLOADS
+from tests.gpu_common import (GRAD_REL_L2, O_TOL, cfg_of, check_sel, device_inputs, log, oracle_inputs, rel_l2,
+                              to_np)
+
+pytestmark = pytest.mark.gpu
+
+
+def sample_rows(B, L, m, n_random, seed):
+    rng = np.random.default_rng(seed)
+    fixed = [0, 1, m - 1, m, 2 * m + 5, L // 2, L - m - 1, L - m, L - 2, L - 1]
+    rows = []
+    for b in range(B):
+        rows += [b * L + i for i in fixed]
+        rows += [b * L + int(i) for i in rng.integers(0, L, n_random)]
+    return np.array(sorted(set(rows)), dtype=np.int64)
+
+
+def check_rows(wl, h, kc_ref, sel_g, o, lse, rows):
+    scale = wl.head_dim ** -0.5
+    L, Hkv = wl.seqlen_q, wl.n_heads_kv
+    sel_r, kth, gap = oracle.select(h["q"], kc_ref, wl.block_size, wl.top_k, wl.n_init_blocks, wl.window, scale,
+                                    wl.seqlen_k, rows=rows)
+    b_idx, i_idx = rows // L, rows % L
+    gpu_rows = sel_g[b_idx, :, i_idx]                      # [n, Hkv, Ksel]
+    exempt = check_sel(gpu_rows, sel_r, kth, gap,
+                       lambda idx: oracle.score_row(h["q"], kc_ref, wl.block_size, scale, wl.seqlen_k,
+                                                    int(b_idx[idx[0]]), int(i_idx[idx[0]]), idx[1]))
+    o_r, lse_r = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, wl.block_size, scale, rows=rows)
+    tol = O_TOL[wl.dtype]
+    np.testing.assert_allclose(to_np(o)[b_idx, i_idx], o_r, atol=tol, rtol=0)
+    np.testing.assert_allclose(to_np(lse)[b_idx, :, i_idx], lse_r, atol=tol, rtol=0)
+    log(f"[fullsize] {wl.name}: {rows.size} rows x {Hkv} groups checked, {exempt} exempt")
+
+
+def test_prefill_32k_sampled():
+    wl = WORKLOADS["prefill_32k"]
+    log(f"[fullsize] {wl.name}: generating inputs")
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 0, with_grad_out=False)
+    kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg)
+    torch.cuda.synchronize()
+    h = oracle_inputs(host)
+    kc_ref = oracle.compress(h["k"], h["punct"], wl.block_size, wl.lam)
+    np.testing.assert_allclose(to_np(kc), kc_ref, atol=1e-5, rtol=1e-5)
+    sel_g = sel.cpu().numpy()
+    # every row: structural invariants of the selection
+    L, m = wl.seqlen_q, wl.block_size
+    cur = np.arange(L) // m
+    assert (sel_g[..., 0] == 0).all()
+    valid = sel_g >= 0
+    assert (np.where(valid, sel_g, -1).max(-1) == cur).all()
+    assert (np.diff(np.where(valid, sel_g, 1 << 30), axis=-1) > 0).all()
+    assert (valid.sum(-1) == np.minimum(cur + 1, wl.ksel)).all()
+    check_rows(wl, h, kc_ref, sel_g, o, lse, sample_rows(1, L, m, 150, 0))
+
+
+def test_train_32k_sampled():
+    """The benchmark's training workload (4 x 32k tokens): forward + backward on the GPU,
+    oracle on sampled rows (dQ) and sampled key blocks (dK, dV)."""
+    wl = WORKLOADS["train_32k"]
+    log(f"[fullsize] {wl.name}: generating inputs")
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 0, with_grad_out=True)
+    kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg)
+    dq, dk, dv = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg)
+    torch.cuda.synchronize()
+    log(f"[fullsize] {wl.name}: GPU done, running the oracle on samples")
+    h = oracle_inputs(host)
+    del host
+    kc_ref = oracle.compress(h["k"], h["punct"], wl.block_size, wl.lam)
+    sel_g = sel.cpu().numpy()
+    B, L, m, T = wl.batch, wl.seqlen_q, wl.block_size, wl.n_blocks
+    rows = sample_rows(B, L, m, 24, 1)
+    check_rows(wl, h, kc_ref, sel_g, o, lse, rows)
+    scale = wl.head_dim ** -0.5
+    dq_r, _, _ = oracle.attn_bwd(h["q"], h["k"], h["v"], h["do"], sel_g, m, scale, rows=rows, want_dkv=False)
+    dq_g = to_np(dq)[rows // L, rows % L]
+    e_dq = rel_l2(dq_g, dq_r)
+    # sampled blocks (b, g, t): late blocks keep the oracle's per-row work small
+    Hkv = wl.n_heads_kv
+    picks = [(0, 0, T - 1), (1, 3, 300), (2, 5, 100), (3, 7, 20), (0, 6, T - 2)]
+    blocks = np.array([(b * Hkv + g) * T + t for b, g, t in picks], dtype=np.int64)
+    _, dk_r, dv_r = oracle.attn_bwd(h["q"], h["k"], h["v"], h["do"], sel_g, m, scale, blocks=blocks, want_dq=False)
+    dk_c, dv_c = to_np(dk), to_np(dv)
+    dk_g = np.stack([dk_c[b, t * m:(t + 1) * m, g] for b, g, t in picks])
+    dv_g = np.stack([dv_c[b, t * m:(t + 1) * m, g] for b, g, t in picks])
+    e_dk, e_dv = rel_l2(dk_g, dk_r), rel_l2(dv_g, dv_r)
+    log(f"[fullsize] {wl.name}: grad rel-L2 dQ {e_dq:.2e} dK {e_dk:.2e} dV {e_dv:.2e}")
+    assert max(e_dq, e_dk, e_dv) < GRAD_REL_L2[wl.dtype]
+
+
+def test_decode_32k():
+    """64 sequences x one query against a 32k cache: every output checked."""
+    wl = WORKLOADS["decode_32k"]
+    log(f"[fullsize] {wl.name}: generating inputs")
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 0, with_grad_out=False)
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    sel, o, lse = phsa.decode(dev["q"], dev["k"], dev["v"], kc, cfg)
+    torch.cuda.synchronize()
+    h = oracle_inputs(host)
+    scale = wl.head_dim ** -0.5
+    kc_ref = oracle.compress(h["k"], h["punct"], wl.block_size, wl.lam)
+    np.testing.assert_allclose(to_np(kc), kc_ref, atol=1e-5, rtol=1e-5)
+    sel_ref, kth, gap = oracle.select(h["q"], kc_ref, wl.block_size, wl.top_k, wl.n_init_blocks, wl.window, scale,
+                                      wl.seqlen_k)
+    sel_g = sel.cpu().numpy()
+    exempt = check_sel(sel_g, sel_ref, kth, gap,
+                       lambda idx: oracle.score_row(h["q"], kc_ref, wl.block_size, scale, wl.seqlen_k, idx[0], idx[2],
+                                                    idx[1]))
+    o_r, lse_r = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, wl.block_size, scale)
+    np.testing.assert_allclose(to_np(o), o_r, atol=O_TOL[wl.dtype], rtol=0)
+    np.testing.assert_allclose(to_np(lse), lse_r, atol=O_TOL[wl.dtype], rtol=0)
+    log(f"[fullsize] {wl.name}: all {sel_g.shape[0] * sel_g.shape[1]} rows checked, {exempt} exempt")
+
+
+@pytest.mark.parametrize("L,window,n_init,top_k", [(4096, 0, 1, 12), (2048, 256, 2, 5), (192, 0, 1, 12)])
+def test_decode_variants(L, window, n_init, top_k):
+    """Decode against short caches, local windows, several init blocks, fewer candidates than k."""
+    wl = WORKLOADS["decode_32k"].replace(batch=8, seqlen_k=L, window=window, n_init_blocks=n_init, top_k=top_k)
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 2, with_grad_out=False)
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    sel, o, lse = phsa.decode(dev["q"], dev["k"], dev["v"], kc, cfg)
+    torch.cuda.synchronize()
+    h = oracle_inputs(host)
+    scale = wl.head_dim ** -0.5
+    kc_ref = oracle.compress(h["k"], h["punct"], wl.block_size, wl.lam)
+    sel_ref, kth, gap = oracle.select(h["q"], kc_ref, wl.block_size, top_k, n_init, window, scale, L)
+    sel_g = sel.cpu().numpy()
+    check_sel(sel_g, sel_ref, kth, gap,
+              lambda idx: oracle.score_row(h["q"], kc_ref, wl.block_size, scale, L, idx[0], idx[2], idx[1]))
+    o_r, lse_r = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, wl.block_size, scale)
+    np.testing.assert_allclose(to_np(o), o_r, atol=O_TOL[wl.dtype], rtol=0)
+    np.testing.assert_allclose(to_np(lse), lse_r, atol=O_TOL[wl.dtype], rtol=0)

@@ -1,0 +1,177 @@
+"""GPU parity: the HIP path through the C ABI against the oracle, on seeded inputs.
+
+Bars: K_comp within 1e-5; selected blocks equal except rows the oracle's top-k
+boundary gap exempts (< 1e-4); O and LSE within 2e-2 absolute (bf16) / 1e-4
+(fp32), evaluated by the oracle on the GPU's own selection; dQ/dK/dV within
+5e-2 relative L2 (bf16) / 1e-4 (fp32).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2601_02819_amd import phsa
+from paper_2601_02819_amd.inputs import WORKLOADS, Workload
+from tests.gpu_common import (GRAD_REL_L2, O_TOL, cfg_of, check_sel, device_inputs, log, oracle_inputs, rel_l2,
+                              to_np)
+
+pytestmark = pytest.mark.gpu
+
+
+def small(name, B, L, Hq, Hkv, d, top_k, n_init, window, dtype="bf16", **kw):
+    return Workload(name, B, L, L, Hq, Hkv, d, 64, top_k, n_init, window, dtype, **kw)
+
+
+SMALL = [
+    small("ragged320", 1, 320, 2, 1, 64, 2, 1, 0),
+    small("g2_win", 2, 1024, 4, 2, 128, 3, 1, 64),
+    small("g8_init2", 1, 1024, 8, 1, 128, 5, 2, 128),
+    small("g1_d64", 1, 768, 4, 4, 64, 4, 1, 0),
+    small("g4_k14", 1, 2048, 16, 4, 128, 14, 1, 0),
+    small("topk0", 1, 512, 2, 1, 128, 0, 1, 0),
+    small("k32_init3", 1, 4096, 2, 1, 128, 32, 3, 192),
+    small("one_block", 1, 64, 2, 1, 128, 4, 1, 0),
+    small("fp32_g2", 1, 1024, 4, 2, 128, 3, 1, 64, dtype="fp32"),
+    WORKLOADS["tiny_fp32"],
+]
+
+
+def run_full(wl: Workload, seed: int = 0, bwd: bool = True):
+    log(f"[parity] {wl.name} seed={seed} B={wl.batch} L={wl.seqlen_k} Hq={wl.n_heads_q} Hkv={wl.n_heads_kv} "
+        f"d={wl.head_dim} k={wl.top_k} init={wl.n_init_blocks} w={wl.window} {wl.dtype}")
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, seed, with_grad_out=bwd)
+    h = oracle_inputs(host)
+    scale = wl.head_dim ** -0.5
+    Lk = wl.seqlen_k
+
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    sel = phsa.select(dev["q"], kc, Lk, cfg)
+    o, lse = phsa.attn_fwd(dev["q"], dev["k"], dev["v"], sel, cfg)
+    torch.cuda.synchronize()
+
+    kc_ref = oracle.compress(h["k"], h["punct"], wl.block_size, wl.lam)
+    np.testing.assert_allclose(to_np(kc), kc_ref, atol=1e-5, rtol=1e-5)
+
+    sel_ref, kth, gap = oracle.select(h["q"], kc_ref, wl.block_size, wl.top_k, wl.n_init_blocks, wl.window, scale, Lk)
+    sel_g = sel.cpu().numpy()
+    exempt = check_sel(sel_g, sel_ref, kth, gap,
+                       lambda idx: oracle.score_row(h["q"], kc_ref, wl.block_size, scale, Lk, idx[0], idx[2], idx[1]))
+    log(f"[parity] {wl.name}: selection equal on all but {exempt} exempt rows of {sel_g.shape[0] * sel_g.shape[1] * sel_g.shape[2]}")
+
+    o_ref, lse_ref = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, wl.block_size, scale)
+    tol = O_TOL[wl.dtype]
+    np.testing.assert_allclose(to_np(o), o_ref, atol=tol, rtol=0)
+    np.testing.assert_allclose(to_np(lse), lse_ref, atol=tol, rtol=0)
+
+    if bwd:
+        dq, dk, dv = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg)
+        torch.cuda.synchronize()
+        dq_r, dk_r, dv_r = oracle.attn_bwd(h["q"], h["k"], h["v"], h["do"], sel_g, wl.block_size, scale)
+        gt = GRAD_REL_L2[wl.dtype]
+        errs = (rel_l2(to_np(dq), dq_r), rel_l2(to_np(dk), dk_r), rel_l2(to_np(dv), dv_r))
+        log(f"[parity] {wl.name}: grad rel-L2 dQ {errs[0]:.2e} dK {errs[1]:.2e} dV {errs[2]:.2e}")
+        assert max(errs) < gt, errs
+    return exempt
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=[w.name for w in SMALL])
+def test_small_full(wl):
+    run_full(wl, seed=1)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_prefill_8k_full(seed):
+    """8k-token prefill, sentence-like punctuation, every row checked (backward on a sample below)."""
+    run_full(WORKLOADS["prefill_8k"], seed=seed, bwd=False)
+
+
+@pytest.mark.parametrize("lam", [0.0, 0.25, 1.0])
+def test_lambda_sweep(lam):
+    run_full(small("lam", 1, 1024, 4, 2, 128, 4, 1, 0, lam=lam, punct_p=0.2), seed=3)
+
+
+def test_zero_mask_is_mean_pooling():
+    """No punctuation: the GPU's representatives are the block means."""
+    wl = small("nopunct", 1, 1024, 4, 2, 128, 4, 1, 0, punct_p=0.0)
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 4, with_grad_out=False)
+    assert int(dev["punct"].sum()) == 0
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    mean = host["k"].float().reshape(1, 16, 64, 2, 128).mean(2).permute(0, 2, 1, 3)
+    np.testing.assert_allclose(to_np(kc), mean.numpy(), atol=1e-5)
+
+
+@pytest.mark.parametrize("m,d,dtype", [(16, 64, "bf16"), (32, 128, "bf16"), (64, 128, "fp32"), (128, 64, "bf16")])
+def test_compress_select_block_sizes(m, d, dtype):
+    """compress and select support any block size; attention kernels use m = 64."""
+    wl = Workload("m", 2, 1024, 1024, 4, 2, d, m, 5, 2, 2 * m, dtype)
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 5, with_grad_out=False)
+    h = oracle_inputs(host)
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    sel = phsa.select(dev["q"], kc, 1024, cfg)
+    torch.cuda.synchronize()
+    kc_ref = oracle.compress(h["k"], h["punct"], m, wl.lam)
+    np.testing.assert_allclose(to_np(kc), kc_ref, atol=1e-5, rtol=1e-5)
+    scale = d ** -0.5
+    sel_ref, kth, gap = oracle.select(h["q"], kc_ref, m, 5, 2, 2 * m, scale, 1024)
+    check_sel(sel.cpu().numpy(), sel_ref, kth, gap,
+              lambda idx: oracle.score_row(h["q"], kc_ref, m, scale, 1024, idx[0], idx[2], idx[1]))
+
+
+def test_forward_entry_point_matches_steps():
+    """phsa_forward (one call) equals compress + select + attn_fwd bit for bit."""
+    wl = small("fwd1", 2, 1024, 4, 2, 128, 3, 1, 64)
+    cfg = cfg_of(wl)
+    _, dev = device_inputs(wl, 6, with_grad_out=False)
+    kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg)
+    kc2 = phsa.compress(dev["k"], dev["punct"], cfg)
+    sel2 = phsa.select(dev["q"], kc2, 1024, cfg)
+    o2, lse2 = phsa.attn_fwd(dev["q"], dev["k"], dev["v"], sel2, cfg)
+    assert torch.equal(kc, kc2) and torch.equal(sel, sel2) and torch.equal(o, o2) and torch.equal(lse, lse2)
+
+
+def test_all_blocks_is_dense_attention():
+    """top-k covering every block: the GPU result is dense causal attention (torch SDPA, float32 CPU)."""
+    wl = small("dense", 1, 1024, 4, 2, 128, 15, 1, 0)
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 7, with_grad_out=False)
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    sel = phsa.select(dev["q"], kc, 1024, cfg)
+    o, lse = phsa.attn_fwd(dev["q"], dev["k"], dev["v"], sel, cfg)
+    torch.cuda.synchronize()
+    assert (sel.cpu()[..., :].max(-1).values == torch.arange(1024) // 64).all()
+    q = host["q"].float().transpose(1, 2)
+    k = host["k"].float().transpose(1, 2).repeat_interleave(2, 1)
+    v = host["v"].float().transpose(1, 2).repeat_interleave(2, 1)
+    ref = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True).transpose(1, 2)
+    np.testing.assert_allclose(to_np(o), ref.numpy(), atol=2e-2)
+
+
+def test_determinism():
+    """Forward, selection and backward are bitwise repeatable (no order depends on timing)."""
+    wl = small("det", 2, 2048, 8, 4, 128, 6, 1, 64)
+    cfg = cfg_of(wl)
+    _, dev = device_inputs(wl, 8, with_grad_out=True)
+    outs = []
+    for _ in range(2):
+        kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg)
+        dq, dk, dv = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg)
+        outs.append([x.clone() for x in (kc, sel, o, lse, dq, dk, dv)])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+def test_autograd_wrapper():
+    wl = small("ag", 1, 512, 4, 2, 64, 3, 1, 0)
+    cfg = cfg_of(wl)
+    _, dev = device_inputs(wl, 9, with_grad_out=True)
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    sel = phsa.select(dev["q"], kc, 512, cfg)
+    q, k, v = (dev[n].clone().requires_grad_(True) for n in ("q", "k", "v"))
+    out = phsa.SparseAttention.apply(q, k, v, sel, cfg)
+    out.backward(dev["do"])
+    o, lse = phsa.attn_fwd(dev["q"], dev["k"], dev["v"], sel, cfg)
+    dq, dk, dv = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg)
+    assert torch.equal(out, o) and torch.equal(q.grad, dq) and torch.equal(k.grad, dk) and torch.equal(v.grad, dv)
