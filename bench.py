@@ -1,0 +1,234 @@
+"""PHSA hot-path benchmark on one MI355X.
+
+A step is one training pass of PHSA attention over the 32k-token workload
+(batch 4 x 32768 tokens, 16 query / 8 KV heads, head dim 128, 64-token
+blocks, 14 blocks per query = 97.3% sparsity): block compression, scoring +
+top-k selection, the inverted index, sparse attention forward and backward.
+Inputs are seeded synthetic tensors already resident in HBM.
+
+The JSON line reports whole-step selected-block TFLOP/s (4*d*m FLOPs per
+(query row, head, selected block) forward, 2.5x that backward), per-kernel
+times from HIP events recorded on the launch stream inside the timed region,
+the roofline of the dominant kernel, a decode-step measurement, and the fp64
+CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2601_02819_amd import phsa  # noqa: E402
+from paper_2601_02819_amd.inputs import WORKLOADS, make_inputs  # noqa: E402
+
+METRIC = "PHSA fwd+bwd ms & selected-block TFLOP/s at L=32k, 97.3% sparsity; % MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def cfg_of(wl):
+    return phsa.Config(block_size=wl.block_size, top_k=wl.top_k, n_init_blocks=wl.n_init_blocks, window=wl.window,
+                       lam=wl.lam)
+
+
+def selected_blocks(sel: torch.Tensor, seqlen_k: int, block: int) -> int:
+    """Sum over (b, g, query row) of the number of valid selected blocks."""
+    Lq = sel.shape[2]
+    cur = ((seqlen_k - Lq + torch.arange(Lq, device=sel.device)) // block).view(1, 1, Lq, 1)
+    return int(((sel >= 0) & (sel <= cur)).sum().item())
+
+
+def kernel_stats(names):
+    out = {}
+    for n in names:
+        ms, cnt = phsa.timing_collect(n)
+        if cnt:
+            out[n] = {"total_ms": ms, "launches": cnt, "avg_ms": ms / cnt}
+    return out
+
+
+KERNELS = ["phsa_compress", "phsa_select", "phsa_index_count", "phsa_index_scan_tiles", "phsa_index_scan_lists",
+           "phsa_index_fill", "phsa_attn_fwd_sparse", "phsa_attn_fwd_combine", "phsa_attn_bwd_pre",
+           "phsa_attn_bwd_sparse", "phsa_attn_bwd_dkv_finalize", "phsa_attn_bwd_dq_combine"]
+
+
+def bench_train(steps: int, warmup: int, seed: int):
+    wl = WORKLOADS["train_32k"]
+    cfg = cfg_of(wl)
+    host = make_inputs(wl, seed, with_grad_out=True)
+    dev = {k: v.cuda() for k, v in host.items()}
+    B, L, Hq, Hkv, d, m, T = wl.batch, wl.seqlen_q, wl.n_heads_q, wl.n_heads_kv, wl.head_dim, wl.block_size, wl.n_blocks
+    G = Hq // Hkv
+    p = phsa.make_params(cfg, B, L, L, Hq, Hkv, d, torch.bfloat16)
+    ws_f = torch.empty(phsa.workspace_size(p, phsa.OP_FORWARD), dtype=torch.uint8, device="cuda")
+    ws_b = torch.empty(phsa.workspace_size(p, phsa.OP_ATTN_BWD), dtype=torch.uint8, device="cuda")
+
+    def step():
+        kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg, ws=ws_f)
+        dq, dk, dv = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg, ws=ws_b)
+        return sel
+
+    for _ in range(warmup):
+        sel = step()
+    torch.cuda.synchronize()
+    nsel = selected_blocks(sel, L, m)
+    phsa.timing_reset()
+    phsa.timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    phsa.timing_enable(False)
+    ks = kernel_stats(KERNELS)
+    phsa.timing_reset()
+    ms_step = (t1 - t0) * 1e3 / steps
+
+    fwd_flop = 4.0 * d * m * nsel * G
+    bwd_flop = 2.5 * fwd_flop
+    bytes_compress = B * L * Hkv * d * 2 + B * L + B * Hkv * T * d * 4
+    bytes_select = B * L * Hq * d * 2 + B * Hkv * T * d * 4 + B * Hkv * L * wl.ksel * 4
+    work = {"phsa_attn_fwd_sparse": ("TFLOP/s", fwd_flop / 1e12), "phsa_attn_bwd_sparse": ("TFLOP/s", bwd_flop / 1e12),
+            "phsa_compress": ("GB/s", bytes_compress / 1e9), "phsa_select": ("GB/s", bytes_select / 1e9)}
+    for n, (unit, amount) in work.items():
+        if n in ks:
+            rate = amount / (ks[n]["avg_ms"] / 1e3)
+            peak = PEAK_BF16_TFLOPS if unit == "TFLOP/s" else PEAK_HBM_GBS
+            ks[n].update(rate=rate, unit=unit, frac=rate / peak)
+    dom = max(ks, key=lambda n: ks[n]["total_ms"])
+    return {
+        "ms_per_step": ms_step,
+        "value": (fwd_flop + bwd_flop) / 1e12 / (ms_step / 1e3),
+        "fwd_flop": fwd_flop, "bwd_flop": bwd_flop, "selected_blocks": nsel,
+        # the paper's convention: active tokens of the last query over the sequence length
+        "sparsity_last_query": 1.0 - wl.ksel * m / L,
+        "sparsity_causal_mean": 1.0 - nsel * m / (B * Hkv * L * (L + 1) / 2),
+        "kernels": ks, "dominant": dom, "host": host,
+    }
+
+
+def bench_decode(iters: int, seed: int):
+    wl = WORKLOADS["decode_32k"]
+    cfg = cfg_of(wl)
+    host = make_inputs(wl, seed, with_grad_out=False)
+    dev = {k: v.cuda() for k, v in host.items()}
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)      # block cache representatives, untimed
+    p = phsa.make_params(cfg, wl.batch, 1, wl.seqlen_k, wl.n_heads_q, wl.n_heads_kv, wl.head_dim, torch.bfloat16)
+    ws = torch.empty(phsa.workspace_size(p, phsa.OP_DECODE), dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        sel, o, lse = phsa.decode(dev["q"], dev["k"], dev["v"], kc, cfg, ws=ws)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(iters):
+        sel, o, lse = phsa.decode(dev["q"], dev["k"], dev["v"], kc, cfg, ws=ws)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / iters
+    nsel = selected_blocks(sel, wl.seqlen_k, wl.block_size)
+    B, Hq, Hkv, d, T, m = wl.batch, wl.n_heads_q, wl.n_heads_kv, wl.head_dim, wl.n_blocks, wl.block_size
+    nbytes = B * Hkv * T * d * 4 + nsel * m * d * 2 * 2 + 2 * B * Hq * d * 2 + B * Hkv * wl.ksel * 4
+    return {"workload": "decode_32k: 64 sequences x 1 query vs a 32768-token cache, 16/8 heads, d 128, 14 blocks",
+            "ms_per_step": ms, "algorithmic_bytes": nbytes, "GB_per_s": nbytes / 1e9 / (ms / 1e3),
+            "frac_hbm_peak": nbytes / 1e9 / (ms / 1e3) / PEAK_HBM_GBS}
+
+
+def cpu_baseline(host, wl, prefix: int):
+    """The fp64 oracle on a causal prefix of batch 0 (all heads): a complete PHSA
+    sub-problem, timed end to end (compress, select, forward, backward)."""
+    import oracle
+
+    oracle.build()
+    q = host["q"][:1, :prefix].float().numpy()
+    k = host["k"][:1, :prefix].float().numpy()
+    v = host["v"][:1, :prefix].float().numpy()
+    do = host["do"][:1, :prefix].float().numpy()
+    punct = host["punct"][:1, :prefix].numpy()
+    d, m = wl.head_dim, wl.block_size
+    scale = d ** -0.5
+    t0 = time.perf_counter()
+    kc = oracle.compress(k, punct, m, wl.lam)
+    sel, _, _ = oracle.select(q, kc, m, wl.top_k, wl.n_init_blocks, wl.window, scale, prefix)
+    oracle.attn_fwd(q, k, v, sel, m, scale)
+    oracle.attn_bwd(q, k, v, do, sel, m, scale)
+    dt = time.perf_counter() - t0
+    cur = (np.arange(prefix) // m)[None, None, :, None]
+    nsel = int(((sel >= 0) & (sel <= cur)).sum())
+    G = wl.n_heads_q // wl.n_heads_kv
+    flop = 4.0 * d * m * nsel * G * 3.5
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": flop / 1e12 / dt, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "seconds": dt,
+            "sample": f"batch 0, query/key tokens 0..{prefix - 1} (a causal prefix, a complete PHSA sub-problem) "
+                      f"of the 4x32768 training workload, all 16/8 heads; fp64 compress+select+forward+backward; "
+                      f"FLOPs counted with the same selected-block convention"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-prefix", type=int, default=8192)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="measured HBM traffic of the dominant kernel (from rocprofv3 counters)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the PHSA path shards by (batch, KV head) with no exchange, "
+              "and multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    phsa.lib()
+
+    tr = bench_train(args.steps, args.warmup, args.seed)
+    dom = tr["dominant"]
+    dk = tr["kernels"][dom]
+    traffic = None
+    if os.path.exists(args.traffic):
+        try:
+            tinfo = json.load(open(args.traffic))
+            if tinfo.get("kernel") == dom:
+                traffic = tinfo.get("bytes_per_launch")
+        except (OSError, ValueError):
+            traffic = None
+    roofline = {"bound": "mfma" if dk.get("unit") == "TFLOP/s" else "hbm", "kernel": dom,
+                "achieved": dk.get("rate"), "peak": PEAK_BF16_TFLOPS if dk.get("unit") == "TFLOP/s" else PEAK_HBM_GBS,
+                "unit": dk.get("unit"), "frac": dk.get("frac"), "traffic": traffic,
+                "avg_ms": dk["avg_ms"]}
+    result = {
+        "metric": METRIC, "value": tr["value"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": tr["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "train_32k: PHSA fwd+bwd, batch 4 x 32768 tokens, 16 query / 8 KV heads, head dim 128, "
+                               "block 64, 1 init + 1 local + 12 top-k blocks (97.3% sparse)",
+                   "batch": 4, "seq_len": 32768, "heads_q": 16, "heads_kv": 8, "head_dim": 128, "block": 64,
+                   "blocks_per_query": 14, "sparsity_last_query": tr["sparsity_last_query"],
+                   "sparsity_causal_mean": tr["sparsity_causal_mean"]},
+        "selected_block_gflop": {"fwd": tr["fwd_flop"] / 1e9, "bwd": tr["bwd_flop"] / 1e9},
+        "frac_mfma_peak_step": tr["value"] / PEAK_BF16_TFLOPS,
+        "roofline": roofline,
+        "kernels": tr["kernels"],
+    }
+    if not args.no_decode:
+        result["decode"] = bench_decode(20, args.seed)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(tr["host"], WORKLOADS["train_32k"], args.cpu_prefix)
+    print(json.dumps(result))
+
+
+if __name__ == "__main__":
+    main()

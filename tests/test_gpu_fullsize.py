@@ -58,7 +58,7 @@ def test_prefill_32k_sampled():
     assert (sel_g[..., 0] == 0).all()
     valid = sel_g >= 0
     assert (np.where(valid, sel_g, -1).max(-1) == cur).all()
-    assert (np.diff(np.where(valid, sel_g, 1 << 30), axis=-1) > 0).all()
+    assert (np.diff(np.where(valid, sel_g, (1 << 30) + np.arange(wl.ksel)), axis=-1) > 0).all()
     assert (valid.sum(-1) == np.minimum(cur + 1, wl.ksel)).all()
     check_rows(wl, h, kc_ref, sel_g, o, lse, sample_rows(1, L, m, 150, 0))
 
