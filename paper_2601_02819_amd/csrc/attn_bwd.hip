@@ -9,17 +9,23 @@
 // the block of key j and are causally allowed to see j.
 //
 // Like the forward, the main kernel is key-block-major over the inverted
-// index.  A work unit keeps K_t and V_t in LDS and its 64 x d dK_t / dV_t
-// accumulators in registers (wave w owns keys 16w..16w+15), and streams the
-// unit's query rows through in chunks of 64 MFMA rows.  Per chunk, per wave:
-//   S^T  = K_w Q^T,  dP^T = V_w dO^T          (keys x rows; 16x16x32 MFMA)
-//   P^T, dS^T elementwise from LSE and D
-//   dV_w += P^T dO,  dK_w += dS^T Q           (rows contracted; transposed Q, dO tiles)
-//   dQ_rows = dS K_t                          (keys contracted over all 4 waves)
-// dQ leaves as one bf16 partial per (row, slot), summed by a per-row kernel.
-// dK/dV leave directly (bf16) when the unit covers its whole block, else as
-// float32 partials that a per-block kernel sums; blocks nobody selected get
-// zeros from that kernel too.
+// index.  A work unit keeps K_t in LDS, the B operands of its own 16 keys in
+// registers (wave w owns keys 16w..16w+15) and their dK^T / dV^T
+// accumulators in registers, and streams the unit's query rows through in
+// chunks of 64 MFMA rows; the next chunk's gathered Q / dO rows are fetched
+// into registers while the current chunk computes.  Per chunk, per wave:
+//   S = Q K_w^T,  dP = dO V_w^T           (64 rows x 16 keys)
+//   P, dS elementwise from LSE and D
+//   dV_w^T += dO^T P,  dK_w^T += Q^T dS   (features x 16 keys; rows contracted)
+//   dQ^T = K_t^T dS^T                     (features x 16 rows; all 64 keys)
+// The S / dP accumulator layout is reused directly as the row-contracted
+// operand (row tiles {4q..4q+3} and {16+4q..16+4q+3}); dO^T, Q^T and K_t^T
+// come from the row-major tiles through transposing LDS loads, and dS
+// reaches the other waves through one [key][row] LDS tile.  dQ leaves as one
+// bf16 partial per (row, slot), summed by a per-row kernel.  dK/dV leave
+// directly (bf16) when the unit covers its whole block, else as float32
+// partials that a per-block kernel sums; blocks nobody selected get zeros
+// from that kernel too.
 #include <math.h>
 
 #include "common.h"
@@ -59,23 +65,20 @@ __global__ __launch_bounds__(256) void attn_bwd_sparse_kernel(
     const bf16_t *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dvec, Geom gm, IndexWs ix,
     bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dK, bf16_t *__restrict__ dV, float *__restrict__ dkvpart) {
   constexpr int CT = 64 / G;
-  constexpr int KP = D + 8;   // row-major tiles [64][KP]
-  constexpr int RP = 64 + 8;  // transposed tiles [D][RP] and P/dS tiles [.][RP]
+  constexpr int KP = D + 8;          // pitch of row-major [row][d] tiles
+  constexpr int RP = 64 + 8;         // pitch of the [key][row] dS tile
   constexpr int VPR = D / 8;
+  constexpr int NV = 64 * VPR / 256;
+  constexpr int KB = D / 32;
   constexpr int NT = D / 16;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Kt[D * RP];
   __shared__ __attribute__((aligned(16))) bf16_t Qs[64 * KP];
   __shared__ __attribute__((aligned(16))) bf16_t dOs[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Qt[D * RP];
-  __shared__ __attribute__((aligned(16))) bf16_t dOt[D * RP];
-  __shared__ __attribute__((aligned(16))) bf16_t PTs[4][16 * RP];
-  __shared__ __attribute__((aligned(16))) bf16_t dSTs[4][16 * RP];
-  __shared__ __attribute__((aligned(16))) bf16_t dSs[64 * RP];
-  __shared__ float lse_s[64], dd_s[64];
-  __shared__ int pos_s[64];
-  __shared__ int ent[CT];
+  __shared__ __attribute__((aligned(16))) bf16_t dSt[64 * RP];
+  __shared__ __attribute__((aligned(16))) float lse_s[64];
+  __shared__ __attribute__((aligned(16))) float dd_s[64];
+  __shared__ __attribute__((aligned(16))) int pos_s[64];
+  __shared__ int ent_s[64];
 
   const int u = blockIdx.x;
   if (u >= ix.totals[1]) return;
@@ -89,165 +92,176 @@ __global__ __launch_bounds__(256) void attn_bwd_sparse_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
   const int32_t *list = ix.tok + ix.off[bgt] + e0;
+  const int64_t krow0 = ((int64_t)b * gm.Lk + (int64_t)t * 64) * gm.Hkv + g;  // global row of key 0
 
   for (int x = tid; x < 64 * VPR; x += 256) {
     const int kk = x / VPR, c = (x % VPR) * 8;
-    const int64_t grow = ((int64_t)b * gm.Lk + (int64_t)t * 64 + kk) * gm.Hkv + g;
-    const uint4 kv = *reinterpret_cast<const uint4 *>(K + grow * D + c);
-    *reinterpret_cast<uint4 *>(&Ks[kk * KP + c]) = kv;
-    *reinterpret_cast<uint4 *>(&Vs[kk * KP + c]) = *reinterpret_cast<const uint4 *>(V + grow * D + c);
-    const bf16_t *ke = reinterpret_cast<const bf16_t *>(&kv);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) Kt[(c + e) * RP + kk] = ke[e];
+    *reinterpret_cast<uint4 *>(&Ks[kk * KP + c]) =
+        *reinterpret_cast<const uint4 *>(K + (krow0 + (int64_t)kk * gm.Hkv) * D + c);
   }
-
-  f32x4 dk[NT], dv[NT];
+  // B operands of S = Q K^T and dP = dO V^T for this wave's keys 16w..16w+15
+  bf16x8 kf[KB], vf[KB];
+  {
+    const int64_t r = (krow0 + (int64_t)(wave * 16 + l16) * gm.Hkv) * D;
 #pragma unroll
-  for (int n = 0; n < NT; ++n) dk[n] = dv[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const float sl2 = gm.scale * kLog2e;
-  const int key_base = t * 64 + wave * 16 + q4 * 4;  // key of accumulator element r is key_base + r
+    for (int kb = 0; kb < KB; ++kb) {
+      kf[kb] = load_bf16x8(K + r + kb * 32 + kq);
+      vf[kb] = load_bf16x8(V + r + kb * 32 + kq);
+    }
+  }
+  // dK^T / dV^T accumulators: lane (q, j) holds feature 16nt + 4q + r of key 16w + j
+  f32x4 dkt[NT], dvt[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) dkt[n] = dvt[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int c0 = 0; c0 < n_ent; c0 += CT) {
+  uint4 pq[NV], pd[NV];
+  int pe[NV];
+  float plse = 0.f, pdd = 0.f;
+  int ppos = -1;
+  auto prefetch = [&](int c0) {
     const int ntok = min(CT, n_ent - c0);
-    __syncthreads();
-    if (tid < CT) ent[tid] = tid < ntok ? list[c0 + tid] : -1;
-    __syncthreads();
-    for (int x = tid; x < 64 * VPR; x += 256) {
-      const int r = x / VPR, c = (x % VPR) * 8;
-      const int e = ent[r / G];
-      uint4 qv = make_uint4(0u, 0u, 0u, 0u), dv4 = make_uint4(0u, 0u, 0u, 0u);
-      if (e >= 0) {
-        const int64_t src = (((int64_t)b * gm.Lq + (e >> 6)) * gm.Hq + g * G + (r % G)) * D + c;
-        qv = *reinterpret_cast<const uint4 *>(Q + src);
-        dv4 = *reinterpret_cast<const uint4 *>(dO + src);
-      }
-      *reinterpret_cast<uint4 *>(&Qs[r * KP + c]) = qv;
-      *reinterpret_cast<uint4 *>(&dOs[r * KP + c]) = dv4;
-      const bf16_t *qe = reinterpret_cast<const bf16_t *>(&qv);
-      const bf16_t *de = reinterpret_cast<const bf16_t *>(&dv4);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        Qt[(c + k) * RP + r] = qe[k];
-        dOt[(c + k) * RP + r] = de[k];
+    for (int k = 0; k < NV; ++k) {
+      const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
+      const int tk = r / G;
+      pe[k] = tk < ntok ? list[c0 + tk] : -1;
+      pq[k] = pd[k] = make_uint4(0u, 0u, 0u, 0u);
+      if (pe[k] >= 0) {
+        const int64_t src = (((int64_t)b * gm.Lq + (pe[k] >> 6)) * gm.Hq + g * G + r % G) * D + c;
+        pq[k] = *reinterpret_cast<const uint4 *>(Q + src);
+        pd[k] = *reinterpret_cast<const uint4 *>(dO + src);
       }
     }
     if (tid < 64) {
-      const int e = ent[tid / G];
+      const int tk = tid / G;
+      const int e = tk < ntok ? list[c0 + tk] : -1;
       if (e >= 0) {
-        const int i = e >> 6, h = g * G + tid % G;
-        lse_s[tid] = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + i] * kLog2e;
-        dd_s[tid] = Dvec[((int64_t)b * gm.Hq + h) * gm.Lq + i];
-        pos_s[tid] = gm.q_pos0 + i;
+        const int i = e >> 6;
+        const int64_t li = ((int64_t)b * gm.Hq + g * G + tid % G) * gm.Lq + i;
+        plse = LSE[li] * kLog2e;
+        pdd = Dvec[li];
+        ppos = gm.q_pos0 + i;
       } else {
-        lse_s[tid] = 0.f;
-        dd_s[tid] = 0.f;
-        pos_s[tid] = -1;
+        plse = 0.f;
+        pdd = 0.f;
+        ppos = -1;
       }
+    }
+  };
+  prefetch(0);
+
+  const float sl2 = gm.scale * kLog2e;
+  const int key = t * 64 + wave * 16 + l16;  // the key whose S column this lane holds
+
+  for (int c0 = 0; c0 < n_ent; c0 += CT) {
+    __syncthreads();  // previous chunk is done with Qs, dOs, dSt and the row tables
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
+      *reinterpret_cast<uint4 *>(&Qs[r * KP + c]) = pq[k];
+      *reinterpret_cast<uint4 *>(&dOs[r * KP + c]) = pd[k];
+      if (c == 0 && r % G == 0) ent_s[r / G] = pe[k];
+    }
+    if (tid < 64) {
+      lse_s[tid] = plse;
+      dd_s[tid] = pdd;
+      pos_s[tid] = ppos;
     }
     __syncthreads();
+    if (c0 + CT < n_ent) prefetch(c0 + CT);
 
-    // S^T and dP^T: this wave's 16 keys x 64 rows
-    f32x4 st[4], dpt[4];
+    // S and dP: 64 rows (4 tiles) x this wave's 16 keys; lane (q, j) holds rows 16mt + 4q + r of key j
+    f32x4 s[4], dp[4];
 #pragma unroll
-    for (int n = 0; n < 4; ++n) st[n] = dpt[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int krow = wave * 16 + l16;
+    for (int mt = 0; mt < 4; ++mt) s[mt] = dp[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < D; kb += 32) {
-      const bf16x8 ak = load_bf16x8(&Ks[krow * KP + kb + kq]);
-      const bf16x8 av = load_bf16x8(&Vs[krow * KP + kb + kq]);
+    for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
-      for (int n = 0; n < 4; ++n) {
-        st[n] = mfma16x16x32(ak, load_bf16x8(&Qs[(n * 16 + l16) * KP + kb + kq]), st[n]);
-        dpt[n] = mfma16x16x32(av, load_bf16x8(&dOs[(n * 16 + l16) * KP + kb + kq]), dpt[n]);
+      for (int mt = 0; mt < 4; ++mt) {
+        s[mt] = mfma16x16x32(load_bf16x8(&Qs[(mt * 16 + l16) * KP + kb * 32 + kq]), kf[kb], s[mt]);
+        dp[mt] = mfma16x16x32(load_bf16x8(&dOs[(mt * 16 + l16) * KP + kb * 32 + kq]), vf[kb], dp[mt]);
       }
     }
-    // elementwise: lane holds rows n*16 + l16, keys key_base + r
+    // P and dS; dS also goes to LDS as [key][row] for the dQ product
 #pragma unroll
-    for (int n = 0; n < 4; ++n) {
-      const int row = n * 16 + l16;
-      const float lse2 = lse_s[row], dd = dd_s[row];
-      const int pos = pos_s[row];
+    for (int mt = 0; mt < 4; ++mt) {
+      const int r0 = mt * 16 + q4 * 4;
+      const float4 lse4 = *reinterpret_cast<const float4 *>(&lse_s[r0]);
+      const float4 dd4 = *reinterpret_cast<const float4 *>(&dd_s[r0]);
+      const int4 pos4 = *reinterpret_cast<const int4 *>(&pos_s[r0]);
+      const float lsev[4] = {lse4.x, lse4.y, lse4.z, lse4.w};
+      const float ddv[4] = {dd4.x, dd4.y, dd4.z, dd4.w};
+      const int posv[4] = {pos4.x, pos4.y, pos4.z, pos4.w};
       bf16_t dsq[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = (key_base + r) <= pos ? exp2f(st[n][r] * sl2 - lse2) : 0.f;
-        const float ds = p * (dpt[n][r] - dd);
-        PTs[wave][(q4 * 4 + r) * RP + row] = f32_to_bf16(p);
+        const float p = key <= posv[r] ? exp2f(s[mt][r] * sl2 - lsev[r]) : 0.f;
+        const float ds = p * (dp[mt][r] - ddv[r]);
+        s[mt][r] = p;
+        dp[mt][r] = ds;
         dsq[r] = f32_to_bf16(ds);
-        dSTs[wave][(q4 * 4 + r) * RP + row] = dsq[r];
       }
-      *reinterpret_cast<uint2 *>(&dSs[row * RP + wave * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(dsq);
+      *reinterpret_cast<uint2 *>(&dSt[(wave * 16 + l16) * RP + r0]) = *reinterpret_cast<const uint2 *>(dsq);
     }
-    __syncthreads();
+    // rows {4q..4q+3} and {16+4q..16+4q+3} (+32) as the K-operand of the row contractions
+    const bf16x8 pb0 = pack_bf16x8(s[0], s[1]), pb1 = pack_bf16x8(s[2], s[3]);
+    const bf16x8 sb0 = pack_bf16x8(dp[0], dp[1]), sb1 = pack_bf16x8(dp[2], dp[3]);
+    // dV^T += dO^T P,  dK^T += Q^T dS   (feature tiles x this wave's keys)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      dvt[nt] = mfma16x16x32(lds_col8(dOs, KP, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, dvt[nt]);
+      dvt[nt] = mfma16x16x32(lds_col8(dOs, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, dvt[nt]);
+      dkt[nt] = mfma16x16x32(lds_col8(Qs, KP, q4 * 4, 16 + q4 * 4, nt * 16, l16), sb0, dkt[nt]);
+      dkt[nt] = mfma16x16x32(lds_col8(Qs, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dkt[nt]);
+    }
+    __syncthreads();  // dSt complete
 
-    // dV += P^T dO, dK += dS^T Q (contract over the 64 chunk rows)
+    // dQ^T = K^T dS^T for chunk rows 16w..16w+15 (all 64 keys)
+    const int row = wave * 16 + l16;
+    const int e = ent_s[row / G];
+    f32x4 dqt[NT];
 #pragma unroll
-    for (int kb = 0; kb < 64; kb += 32) {
-      const bf16x8 ap = load_bf16x8(&PTs[wave][l16 * RP + kb + kq]);
-      const bf16x8 as = load_bf16x8(&dSTs[wave][l16 * RP + kb + kq]);
+    for (int nt = 0; nt < NT; ++nt) dqt[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        dv[n] = mfma16x16x32(ap, load_bf16x8(&dOt[(n * 16 + l16) * RP + kb + kq]), dv[n]);
-        dk[n] = mfma16x16x32(as, load_bf16x8(&Qt[(n * 16 + l16) * RP + kb + kq]), dk[n]);
+    for (int kb = 0; kb < 2; ++kb) {
+      const bf16x8 bs = lds_col8(dSt, RP, kb * 32 + kq, kb * 32 + kq + 4, wave * 16, l16);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        dqt[nt] = mfma16x16x32(lds_col8(Ks, KP, kb * 32 + kq, kb * 32 + kq + 4, nt * 16, l16), bs, dqt[nt]);
+    }
+    if (e >= 0) {
+      bf16_t *dst =
+          dqpart + ((((int64_t)bg * gm.Lq + (e >> 6)) * gm.ksel + (e & 63)) * G + row % G) * D + q4 * 4;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const bf16_t o4[4] = {f32_to_bf16(dqt[nt][0] * gm.scale), f32_to_bf16(dqt[nt][1] * gm.scale),
+                              f32_to_bf16(dqt[nt][2] * gm.scale), f32_to_bf16(dqt[nt][3] * gm.scale)};
+        *reinterpret_cast<uint2 *>(dst + nt * 16) = *reinterpret_cast<const uint2 *>(o4);
       }
-    }
-    // dQ for rows 16w..16w+15 = dS (rows x 64 keys) K (64 keys x D)
-    f32x4 dq[NT];
-#pragma unroll
-    for (int n = 0; n < NT; ++n) dq[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < 64; kb += 32) {
-      const bf16x8 a = load_bf16x8(&dSs[(wave * 16 + l16) * RP + kb + kq]);
-#pragma unroll
-      for (int n = 0; n < NT; ++n) dq[n] = mfma16x16x32(a, load_bf16x8(&Kt[(n * 16 + l16) * RP + kb + kq]), dq[n]);
-    }
-    // stage scaled dQ rows of this wave in Qs (all reads of Qs are done) and write them out
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = wave * 16 + q4 * 4 + r;
-#pragma unroll
-      for (int n = 0; n < NT; ++n) Qs[row * KP + n * 16 + l16] = f32_to_bf16(dq[n][r] * gm.scale);
-    }
-    __syncthreads();
-    for (int x = lane; x < 16 * VPR; x += 64) {
-      const int row = wave * 16 + x / VPR, c = (x % VPR) * 8;
-      const int e = ent[row / G];
-      if (e >= 0)
-        *reinterpret_cast<uint4 *>(dqpart + ((((int64_t)bg * gm.Lq + (e >> 6)) * gm.ksel + (e & 63)) * G + row % G) * D + c) =
-            *reinterpret_cast<const uint4 *>(&Qs[row * KP + c]);
     }
   }
 
-  // dK (scaled) / dV of this wave's 16 keys.
+  // this wave's keys: lane (q, j) holds features 16nt + 4q .. +3 of key 16w + j
+  const int kk = wave * 16 + l16;
   if (whole_block) {
-    __syncthreads();
+    const int64_t dst = (krow0 + (int64_t)kk * gm.Hkv) * D + q4 * 4;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int kk = wave * 16 + q4 * 4 + r;
-#pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        Ks[kk * KP + n * 16 + l16] = f32_to_bf16(dk[n][r] * gm.scale);
-        Vs[kk * KP + n * 16 + l16] = f32_to_bf16(dv[n][r]);
-      }
-    }
-    __syncthreads();
-    for (int x = tid; x < 64 * VPR; x += 256) {
-      const int kk = x / VPR, c = (x % VPR) * 8;
-      const int64_t grow = ((int64_t)b * gm.Lk + (int64_t)t * 64 + kk) * gm.Hkv + g;
-      *reinterpret_cast<uint4 *>(dK + grow * D + c) = *reinterpret_cast<const uint4 *>(&Ks[kk * KP + c]);
-      *reinterpret_cast<uint4 *>(dV + grow * D + c) = *reinterpret_cast<const uint4 *>(&Vs[kk * KP + c]);
+    for (int nt = 0; nt < NT; ++nt) {
+      const bf16_t k4[4] = {f32_to_bf16(dkt[nt][0] * gm.scale), f32_to_bf16(dkt[nt][1] * gm.scale),
+                            f32_to_bf16(dkt[nt][2] * gm.scale), f32_to_bf16(dkt[nt][3] * gm.scale)};
+      const bf16_t v4[4] = {f32_to_bf16(dvt[nt][0]), f32_to_bf16(dvt[nt][1]), f32_to_bf16(dvt[nt][2]),
+                            f32_to_bf16(dvt[nt][3])};
+      *reinterpret_cast<uint2 *>(dK + dst + nt * 16) = *reinterpret_cast<const uint2 *>(k4);
+      *reinterpret_cast<uint2 *>(dV + dst + nt * 16) = *reinterpret_cast<const uint2 *>(v4);
     }
   } else {
-    float *pk = dkvpart + (int64_t)u * 2 * 64 * D;
+    float *pk = dkvpart + (int64_t)u * 2 * 64 * D + kk * D + q4 * 4;
     float *pv = pk + 64 * D;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int kk = wave * 16 + q4 * 4 + r;
-#pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        pk[kk * D + n * 16 + l16] = dk[n][r] * gm.scale;
-        pv[kk * D + n * 16 + l16] = dv[n][r];
-      }
+    for (int nt = 0; nt < NT; ++nt) {
+      *reinterpret_cast<float4 *>(pk + nt * 16) =
+          make_float4(dkt[nt][0] * gm.scale, dkt[nt][1] * gm.scale, dkt[nt][2] * gm.scale, dkt[nt][3] * gm.scale);
+      *reinterpret_cast<float4 *>(pv + nt * 16) = make_float4(dvt[nt][0], dvt[nt][1], dvt[nt][2], dvt[nt][3]);
     }
   }
 }

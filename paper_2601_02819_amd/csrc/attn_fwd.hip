@@ -3,19 +3,25 @@
 // Work is key-block-major.  Every query row selects its own blocks, so the
 // only operand that many rows share is a key/value block.  A workgroup takes
 // one work unit = one (b, g, t) block plus up to unit_tokens entries of the
-// list of rows that selected it, keeps K_t (row-major) and V_t (transposed)
-// in LDS for the whole unit, and streams the rows through it in chunks of
-// 64 MFMA rows (64 / G tokens x G heads of the group):
+// list of rows that selected it, keeps K_t and V_t in LDS for the whole unit,
+// and streams the rows through it in chunks of 64 MFMA rows (64 / G tokens x
+// the G heads of the group); wave w owns chunk rows 16w..16w+15:
 //
-//   S = Q_chunk K_t^T            16x16x32 bf16 MFMA, fp32 accumulate
-//   m = rowmax(S), P = exp(S - m), l = rowsum(P)   (token-level causal mask)
-//   O_part = (P V_t) / l          16x16x32 bf16 MFMA
+//   S^T = K_t Q_w^T                    (64 keys x 16 rows, 16x16x32 bf16 MFMA)
+//   m = rowmax, P = 2^(S - m), l = rowsum(P)      (token-level causal mask)
+//   O^T = V_t^T P^T                    (d x 16 rows)
 //
-// and writes, per (row, slot), the partial output O_part (bf16) and its
-// (m, l) pair (log2 units).  A second kernel merges the at most Ksel
-// partials of each row into the exact softmax over the union:
-//   M = max_s m_s,  L = sum_s l_s 2^(m_s - M),  O = sum_s (l_s 2^(m_s - M) / L) O_part_s,
-//   LSE = (M + log2 L) ln 2.
+// The S^T accumulator layout (lane (q, j) holds keys 4q + r of row j) is used
+// directly as the P^T operand of the second product, pairing key tiles
+// {4q..4q+3} and {16+4q..16+4q+3}; V_t^T is read with transposing LDS loads
+// over the same key set, so P never goes through LDS.  O^T leaves each lane
+// with 4 consecutive features of one row (8-byte stores).  The next chunk's
+// query rows are gathered into registers while the current one computes.
+//
+// Output per (row, slot): the unnormalised partial O (bf16) and (m, l) in
+// log2 units.  A second kernel merges the at most Ksel partials of each row:
+//   M = max_s m_s,  w_s = 2^(m_s - M),  O = sum_s w_s O_s / sum_s w_s l_s,
+//   LSE = (M + log2 sum_s w_s l_s) ln 2.
 #include <math.h>
 
 #include "common.h"
@@ -30,15 +36,16 @@ __global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__re
                                                               const bf16_t *__restrict__ K,
                                                               const bf16_t *__restrict__ V, Geom gm, IndexWs ix,
                                                               bf16_t *__restrict__ opart, float2 *__restrict__ ml) {
-  constexpr int CT = 64 / G;   // query tokens per chunk
-  constexpr int KP = D + 8;    // padded LDS row (elements) of K and Q tiles
-  constexpr int VP = 64 + 8;   // padded LDS row of the transposed V tile and of P
-  constexpr int VPR = D / 8;   // 16-byte vectors per row
+  constexpr int CT = 64 / G;         // query tokens per chunk
+  constexpr int KP = D + 8;          // LDS row pitch (elements)
+  constexpr int VPR = D / 8;         // 16-byte vectors per row
+  constexpr int NV = 64 * VPR / 256; // gathered vectors per thread per chunk
+  constexpr int KB = D / 32;
+  constexpr int NT = D / 16;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[D * VP];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KP];
   __shared__ __attribute__((aligned(16))) bf16_t Qs[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Ps[4][16 * VP];
-  __shared__ int ent[CT];
+  __shared__ int ent_s[64];
 
   const int u = blockIdx.x;
   if (u >= ix.totals[1]) return;
@@ -55,100 +62,99 @@ __global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__re
     const int kk = x / VPR, c = (x % VPR) * 8;
     const int64_t grow = ((int64_t)b * gm.Lk + (int64_t)t * 64 + kk) * gm.Hkv + g;
     *reinterpret_cast<uint4 *>(&Ks[kk * KP + c]) = *reinterpret_cast<const uint4 *>(K + grow * D + c);
-    const uint4 vv = *reinterpret_cast<const uint4 *>(V + grow * D + c);
-    const bf16_t *ve = reinterpret_cast<const bf16_t *>(&vv);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) Vt[(c + e) * VP + kk] = ve[e];
+    *reinterpret_cast<uint4 *>(&Vs[kk * KP + c]) = *reinterpret_cast<const uint4 *>(V + grow * D + c);
   }
+
+  // gather of one chunk's rows: thread handles vectors tid + 256 k (row = v / VPR)
+  uint4 pf[NV];
+  int pe[NV];
+  auto prefetch = [&](int c0) {
+    const int ntok = min(CT, n_ent - c0);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
+      const int tk = r / G;
+      pe[k] = tk < ntok ? list[c0 + tk] : -1;
+      pf[k] = make_uint4(0u, 0u, 0u, 0u);
+      if (pe[k] >= 0)
+        pf[k] = *reinterpret_cast<const uint4 *>(Q + (((int64_t)b * gm.Lq + (pe[k] >> 6)) * gm.Hq + g * G + r % G) * D + c);
+    }
+  };
+  prefetch(0);
+
   const float sl2 = gm.scale * kLog2e;
   const int key0 = t * 64;
+  const int row = wave * 16 + l16;  // the chunk row whose S^T column this lane holds
 
   for (int c0 = 0; c0 < n_ent; c0 += CT) {
-    const int ntok = min(CT, n_ent - c0);
-    __syncthreads();
-    if (tid < CT) ent[tid] = tid < ntok ? list[c0 + tid] : -1;
-    __syncthreads();
-    for (int x = tid; x < 64 * VPR; x += 256) {
-      const int r = x / VPR, c = (x % VPR) * 8;
-      const int e = ent[r / G];
-      uint4 qv = make_uint4(0u, 0u, 0u, 0u);
-      if (e >= 0)
-        qv = *reinterpret_cast<const uint4 *>(Q + (((int64_t)b * gm.Lq + (e >> 6)) * gm.Hq + g * G + (r % G)) * D + c);
-      *reinterpret_cast<uint4 *>(&Qs[r * KP + c]) = qv;
+    __syncthreads();  // previous chunk is done with Qs / ent_s
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
+      *reinterpret_cast<uint4 *>(&Qs[r * KP + c]) = pf[k];
+      if (c == 0 && r % G == 0) ent_s[r / G] = pe[k];
     }
     __syncthreads();
+    if (c0 + CT < n_ent) prefetch(c0 + CT);
 
-    // S for this wave's 16 rows x 64 keys
-    f32x4 s[4];
+    // S^T: 64 keys (4 tiles) x this wave's 16 rows
+    f32x4 st[4];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) s[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int arow = wave * 16 + l16;
+    for (int kt = 0; kt < 4; ++kt) st[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < D; kb += 32) {
-      const bf16x8 a = load_bf16x8(&Qs[arow * KP + kb + kq]);
+    for (int kb = 0; kb < KB; ++kb) {
+      const bf16x8 bq = load_bf16x8(&Qs[row * KP + kb * 32 + kq]);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) s[nt] = mfma16x16x32(a, load_bf16x8(&Ks[(nt * 16 + l16) * KP + kb + kq]), s[nt]);
+      for (int kt = 0; kt < 4; ++kt)
+        st[kt] = mfma16x16x32(load_bf16x8(&Ks[(kt * 16 + l16) * KP + kb * 32 + kq]), bq, st[kt]);
     }
-
-    float mrow[4], lrow[4];
+    const int e = ent_s[row / G];
+    const int pos = e >= 0 ? gm.q_pos0 + (e >> 6) : -1;
+    float mx = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = wave * 16 + q4 * 4 + r;
-      const int e = ent[row / G];
-      const int pos = e >= 0 ? gm.q_pos0 + (e >> 6) : -1;
-      float mx = -INFINITY;
+    for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const int key = key0 + nt * 16 + l16;
-        const float v = key <= pos ? s[nt][r] * sl2 : -INFINITY;
-        s[nt][r] = v;
+      for (int r = 0; r < 4; ++r) {
+        const float v = (key0 + kt * 16 + q4 * 4 + r) <= pos ? st[kt][r] * sl2 : -INFINITY;
+        st[kt][r] = v;
         mx = fmaxf(mx, v);
       }
-      mx = max16(mx);
-      if (mx == -INFINITY) mx = 0.f;
-      float l = 0.f;
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    if (mx == -INFINITY) mx = 0.f;
+    float l = 0.f;
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const float p = exp2f(s[nt][r] - mx);
-        s[nt][r] = p;
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = exp2f(st[kt][r] - mx);
+        st[kt][r] = p;
         l += p;
       }
-      mrow[r] = mx;
-      lrow[r] = sum16(l);
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) Ps[wave][(q4 * 4 + r) * VP + nt * 16 + l16] = f32_to_bf16(s[nt][r]);
-    __syncthreads();
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const bf16x8 pb0 = pack_bf16x8(st[0], st[1]);  // keys {4q..4q+3} and {16+4q..16+4q+3}
+    const bf16x8 pb1 = pack_bf16x8(st[2], st[3]);  // keys 32 + the same
 
-    f32x4 o[D / 16];
+    // O^T = V^T P^T: d tiles x this wave's 16 rows
+    f32x4 ot[NT];
 #pragma unroll
-    for (int nt = 0; nt < D / 16; ++nt) o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < 64; kb += 32) {
-      const bf16x8 a = load_bf16x8(&Ps[wave][l16 * VP + kb + kq]);
-#pragma unroll
-      for (int nt = 0; nt < D / 16; ++nt) o[nt] = mfma16x16x32(a, load_bf16x8(&Vt[(nt * 16 + l16) * VP + kb + kq]), o[nt]);
+    for (int nt = 0; nt < NT; ++nt) {
+      ot[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      ot[nt] = mfma16x16x32(lds_col8(Vs, KP, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, ot[nt]);
+      ot[nt] = mfma16x16x32(lds_col8(Vs, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, ot[nt]);
     }
-
+    if (e >= 0) {
+      const int64_t slot = ((int64_t)bg * gm.Lq + (e >> 6)) * gm.ksel + (e & 63);
+      const int hh = row % G;
+      if (q4 == 0) ml[slot * G + hh] = make_float2(mx, l);
+      bf16_t *dst = opart + (slot * G + hh) * D + q4 * 4;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = wave * 16 + q4 * 4 + r;
-      const int e = ent[row / G];
-      if (l16 == 0 && e >= 0)
-        ml[(((int64_t)bg * gm.Lq + (e >> 6)) * gm.ksel + (e & 63)) * G + row % G] = make_float2(mrow[r], lrow[r]);
-      const float inv = lrow[r] > 0.f ? 1.f / lrow[r] : 0.f;
-#pragma unroll
-      for (int nt = 0; nt < D / 16; ++nt) Qs[row * KP + nt * 16 + l16] = f32_to_bf16(o[nt][r] * inv);
-    }
-    __syncthreads();
-    for (int x = lane; x < 16 * VPR; x += 64) {
-      const int row = wave * 16 + x / VPR, c = (x % VPR) * 8;
-      const int e = ent[row / G];
-      if (e >= 0)
-        *reinterpret_cast<uint4 *>(opart + ((((int64_t)bg * gm.Lq + (e >> 6)) * gm.ksel + (e & 63)) * G + row % G) * D + c) =
-            *reinterpret_cast<const uint4 *>(&Qs[row * KP + c]);
+      for (int nt = 0; nt < NT; ++nt) {
+        const bf16_t o4[4] = {f32_to_bf16(ot[nt][0]), f32_to_bf16(ot[nt][1]), f32_to_bf16(ot[nt][2]),
+                              f32_to_bf16(ot[nt][3])};
+        *reinterpret_cast<uint2 *>(dst + nt * 16) = *reinterpret_cast<const uint2 *>(o4);
+      }
     }
   }
 }
@@ -176,8 +182,8 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
     for (uint64_t v = valid; v; v &= v - 1) {
       const int64_t sl = base + __ffsll((long long)v) - 1;
       const float2 q = ml[sl * G + hh];
-      const float w = q.y * exp2f(q.x - M);
-      L += w;
+      const float w = exp2f(q.x - M);
+      L += w * q.y;
       const uint2 raw = *reinterpret_cast<const uint2 *>(opart + (sl * G + hh) * D + c);
       const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
       acc0 = fmaf(w, bf16_to_f32(pv[0]), acc0);

@@ -69,4 +69,35 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
+
+// Column reads from a row-major bf16 LDS tile X (row pitch `pitch` elements)
+// with the gfx950 transposing LDS load (ds_read_b64_tr_b16).  Within each
+// 16-lane group the instruction hands lane j element (j % 4) of the 8 bytes
+// addressed by lane 4e + j / 4, e = 0..3; giving lane i the address of
+// X[r0 + i / 4][c0 + 4 (i % 4)] therefore delivers X[r0 + e][c0 + j] to lane j.
+// r0 and c0 may differ between the four groups.  Rows must be 8-byte aligned.
+__device__ __forceinline__ v4i16 lds_col4(const bf16_t *X, int pitch, int r0, int c0, int l16) {
+  const bf16_t *p = X + (r0 + (l16 >> 2)) * pitch + c0 + 4 * (l16 & 3);
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)p);
+}
+
+// 8-element column fragment: lane j gets X[r0 + 0..3][c0 + j] then X[r1 + 0..3][c0 + j].
+__device__ __forceinline__ bf16x8 lds_col8(const bf16_t *X, int pitch, int r0, int r1, int c0, int l16) {
+  const v4i16 a = lds_col4(X, pitch, r0, c0, l16);
+  const v4i16 b = lds_col4(X, pitch, r1, c0, l16);
+  const v8i16 c = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return __builtin_bit_cast(bf16x8, c);
+}
+
+// Packs two 4-element float groups into a bf16 MFMA operand (elements 0..3, then 4..7).
+__device__ __forceinline__ bf16x8 pack_bf16x8(const f32x4 &a, const f32x4 &b) {
+  const v8i16 c = {(short)f32_to_bf16(a[0]), (short)f32_to_bf16(a[1]), (short)f32_to_bf16(a[2]),
+                   (short)f32_to_bf16(a[3]), (short)f32_to_bf16(b[0]), (short)f32_to_bf16(b[1]),
+                   (short)f32_to_bf16(b[2]), (short)f32_to_bf16(b[3])};
+  return __builtin_bit_cast(bf16x8, c);
+}
+
 }  // namespace phsa
