@@ -9,9 +9,8 @@
 // the block of key j and are causally allowed to see j.
 //
 // Like the forward, the main kernel is key-block-major over the inverted
-// index.  A work unit keeps K_t in LDS, the B operands of its own 16 keys in
-// registers (wave w owns keys 16w..16w+15) and their dK^T / dV^T
-// accumulators in registers, and streams the unit's query rows through in
+// index.  A work unit keeps K_t and V_t in LDS (wave w owns keys
+// 16w..16w+15) and the dK^T / dV^T accumulators of its keys in registers, and streams the unit's query rows through in
 // chunks of 64 MFMA rows; the next chunk's gathered Q / dO rows are fetched
 // into registers while the current chunk computes.  Per chunk, per wave:
 //   S = Q K_w^T,  dP = dO V_w^T           (64 rows x 16 keys)
@@ -60,7 +59,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const T *__restrict__ O, c
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(256) void attn_bwd_sparse_kernel(
+__global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     const bf16_t *__restrict__ Q, const bf16_t *__restrict__ K, const bf16_t *__restrict__ V,
     const bf16_t *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dvec, Geom gm, IndexWs ix,
     bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dK, bf16_t *__restrict__ dV, float *__restrict__ dkvpart) {
@@ -72,6 +71,7 @@ __global__ __launch_bounds__(256) void attn_bwd_sparse_kernel(
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KP];
   __shared__ __attribute__((aligned(16))) bf16_t Qs[64 * KP];
   __shared__ __attribute__((aligned(16))) bf16_t dOs[64 * KP];
   __shared__ __attribute__((aligned(16))) bf16_t dSt[64 * RP];
@@ -96,35 +96,37 @@ __global__ __launch_bounds__(256) void attn_bwd_sparse_kernel(
 
   for (int x = tid; x < 64 * VPR; x += 256) {
     const int kk = x / VPR, c = (x % VPR) * 8;
-    *reinterpret_cast<uint4 *>(&Ks[kk * KP + c]) =
-        *reinterpret_cast<const uint4 *>(K + (krow0 + (int64_t)kk * gm.Hkv) * D + c);
-  }
-  // B operands of S = Q K^T and dP = dO V^T for this wave's keys 16w..16w+15
-  bf16x8 kf[KB], vf[KB];
-  {
-    const int64_t r = (krow0 + (int64_t)(wave * 16 + l16) * gm.Hkv) * D;
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      kf[kb] = load_bf16x8(K + r + kb * 32 + kq);
-      vf[kb] = load_bf16x8(V + r + kb * 32 + kq);
-    }
+    const int64_t src = (krow0 + (int64_t)kk * gm.Hkv) * D + c;
+    *reinterpret_cast<uint4 *>(&Ks[kk * KP + c]) = *reinterpret_cast<const uint4 *>(K + src);
+    *reinterpret_cast<uint4 *>(&Vs[kk * KP + c]) = *reinterpret_cast<const uint4 *>(V + src);
   }
   // dK^T / dV^T accumulators: lane (q, j) holds feature 16nt + 4q + r of key 16w + j
   f32x4 dkt[NT], dvt[NT];
 #pragma unroll
   for (int n = 0; n < NT; ++n) dkt[n] = dvt[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // Row gather, pipelined two deep: the list entries of chunk c + 2 are read
+  // while the rows of chunk c + 1 are fetched, which is while chunk c computes.
+  int ne[NV], nrow = -1;               // list entries of the next chunk to fetch
   uint4 pq[NV], pd[NV];
   int pe[NV];
   float plse = 0.f, pdd = 0.f;
   int ppos = -1;
-  auto prefetch = [&](int c0) {
+  auto load_entries = [&](int c0) {
     const int ntok = min(CT, n_ent - c0);
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
+      const int tk = ((tid + 256 * k) / VPR) / G;
+      ne[k] = (c0 < n_ent && tk < ntok) ? list[c0 + tk] : -1;
+    }
+    const int tk = tid / G;
+    nrow = (tid < 64 && c0 < n_ent && tk < ntok) ? list[c0 + tk] : -1;
+  };
+  auto fetch_rows = [&]() {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
       const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
-      const int tk = r / G;
-      pe[k] = tk < ntok ? list[c0 + tk] : -1;
+      pe[k] = ne[k];
       pq[k] = pd[k] = make_uint4(0u, 0u, 0u, 0u);
       if (pe[k] >= 0) {
         const int64_t src = (((int64_t)b * gm.Lq + (pe[k] >> 6)) * gm.Hq + g * G + r % G) * D + c;
@@ -133,10 +135,8 @@ __global__ __launch_bounds__(256) void attn_bwd_sparse_kernel(
       }
     }
     if (tid < 64) {
-      const int tk = tid / G;
-      const int e = tk < ntok ? list[c0 + tk] : -1;
-      if (e >= 0) {
-        const int i = e >> 6;
+      if (nrow >= 0) {
+        const int i = nrow >> 6;
         const int64_t li = ((int64_t)b * gm.Hq + g * G + tid % G) * gm.Lq + i;
         plse = LSE[li] * kLog2e;
         pdd = Dvec[li];
@@ -148,7 +148,9 @@ __global__ __launch_bounds__(256) void attn_bwd_sparse_kernel(
       }
     }
   };
-  prefetch(0);
+  load_entries(0);
+  fetch_rows();
+  load_entries(CT);
 
   const float sl2 = gm.scale * kLog2e;
   const int key = t * 64 + wave * 16 + l16;  // the key whose S column this lane holds
@@ -168,7 +170,10 @@ __global__ __launch_bounds__(256) void attn_bwd_sparse_kernel(
       pos_s[tid] = ppos;
     }
     __syncthreads();
-    if (c0 + CT < n_ent) prefetch(c0 + CT);
+    if (c0 + CT < n_ent) {
+      fetch_rows();
+      load_entries(c0 + 2 * CT);
+    }
 
     // S and dP: 64 rows (4 tiles) x this wave's 16 keys; lane (q, j) holds rows 16mt + 4q + r of key j
     f32x4 s[4], dp[4];
@@ -176,10 +181,12 @@ __global__ __launch_bounds__(256) void attn_bwd_sparse_kernel(
     for (int mt = 0; mt < 4; ++mt) s[mt] = dp[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
+      const bf16x8 kf = load_bf16x8(&Ks[(wave * 16 + l16) * KP + kb * 32 + kq]);
+      const bf16x8 vf = load_bf16x8(&Vs[(wave * 16 + l16) * KP + kb * 32 + kq]);
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
-        s[mt] = mfma16x16x32(load_bf16x8(&Qs[(mt * 16 + l16) * KP + kb * 32 + kq]), kf[kb], s[mt]);
-        dp[mt] = mfma16x16x32(load_bf16x8(&dOs[(mt * 16 + l16) * KP + kb * 32 + kq]), vf[kb], dp[mt]);
+        s[mt] = mfma16x16x32(load_bf16x8(&Qs[(mt * 16 + l16) * KP + kb * 32 + kq]), kf, s[mt]);
+        dp[mt] = mfma16x16x32(load_bf16x8(&dOs[(mt * 16 + l16) * KP + kb * 32 + kq]), vf, dp[mt]);
       }
     }
     // P and dS; dS also goes to LDS as [key][row] for the dQ product
@@ -288,11 +295,13 @@ __global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restri
   }
 }
 
-// One wave per (b, g, query row): dQ = sum over valid slots of the partials.
+// One wave per (b, g, query row): dQ = sum over valid slots of the partials
+// (unrolled over a prefix of valid slots, the well-formed case; else a bit-walk).
 template <int D, int G>
 __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restrict__ sel,
                                                          const bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dQ,
                                                          Geom gm) {
+  constexpr int U = 8;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t x = (int64_t)blockIdx.x * 4 + wave;
   if (x >= (int64_t)gm.B * gm.Hkv * gm.Lq) return;
@@ -301,20 +310,40 @@ __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restri
   const int cur = (gm.q_pos0 + i) / gm.m;
   const int tl = lane < gm.ksel ? sel[x * gm.ksel + lane] : -1;
   const uint64_t valid = __ballot(slot_ok_b(tl, cur, gm.T));
+  const int nv = __popcll(valid);
+  const bool prefix = valid == (nv == 64 ? ~0ull : ((1ull << nv) - 1));
   const int64_t base = x * gm.ksel;
   for (int e = lane * 4; e < G * D; e += 256) {
     const int hh = e / D, c = e - hh * D;
     float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-    for (uint64_t v = valid; v; v &= v - 1) {
-      const int64_t sl = base + __ffsll((long long)v) - 1;
-      const uint2 raw = *reinterpret_cast<const uint2 *>(dqpart + (sl * G + hh) * D + c);
-      const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
-      a0 += bf16_to_f32(pv[0]);
-      a1 += bf16_to_f32(pv[1]);
-      a2 += bf16_to_f32(pv[2]);
-      a3 += bf16_to_f32(pv[3]);
+    if (prefix) {
+      for (int k0 = 0; k0 < nv; k0 += U) {
+        uint2 raw[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k)
+          raw[k] = k0 + k < nv ? *reinterpret_cast<const uint2 *>(dqpart + ((base + k0 + k) * G + hh) * D + c)
+                               : make_uint2(0u, 0u);
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw[k]);
+          a0 += bf16_to_f32(pv[0]);
+          a1 += bf16_to_f32(pv[1]);
+          a2 += bf16_to_f32(pv[2]);
+          a3 += bf16_to_f32(pv[3]);
+        }
+      }
+    } else {
+      for (uint64_t v = valid; v; v &= v - 1) {
+        const int64_t sl = base + __ffsll((long long)v) - 1;
+        const uint2 raw = *reinterpret_cast<const uint2 *>(dqpart + (sl * G + hh) * D + c);
+        const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
+        a0 += bf16_to_f32(pv[0]);
+        a1 += bf16_to_f32(pv[1]);
+        a2 += bf16_to_f32(pv[2]);
+        a3 += bf16_to_f32(pv[3]);
+      }
     }
-    bf16_t outv[4] = {f32_to_bf16(a0), f32_to_bf16(a1), f32_to_bf16(a2), f32_to_bf16(a3)};
+    const bf16_t outv[4] = {f32_to_bf16(a0), f32_to_bf16(a1), f32_to_bf16(a2), f32_to_bf16(a3)};
     *reinterpret_cast<uint2 *>(dQ + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + hh) * D + c) =
         *reinterpret_cast<const uint2 *>(outv);
   }

@@ -65,22 +65,33 @@ __global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__re
     *reinterpret_cast<uint4 *>(&Vs[kk * KP + c]) = *reinterpret_cast<const uint4 *>(V + grow * D + c);
   }
 
-  // gather of one chunk's rows: thread handles vectors tid + 256 k (row = v / VPR)
+  // Row gather, pipelined two deep: the list entries of chunk c + 2 are read
+  // while the rows of chunk c + 1 are fetched, which is while chunk c computes.
+  // Thread handles 16-byte vectors tid + 256 k (row = v / VPR).
+  int ne[NV];
   uint4 pf[NV];
   int pe[NV];
-  auto prefetch = [&](int c0) {
+  auto load_entries = [&](int c0) {
     const int ntok = min(CT, n_ent - c0);
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
+      const int tk = ((tid + 256 * k) / VPR) / G;
+      ne[k] = (c0 < n_ent && tk < ntok) ? list[c0 + tk] : -1;
+    }
+  };
+  auto fetch_rows = [&]() {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
       const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
-      const int tk = r / G;
-      pe[k] = tk < ntok ? list[c0 + tk] : -1;
+      pe[k] = ne[k];
       pf[k] = make_uint4(0u, 0u, 0u, 0u);
       if (pe[k] >= 0)
         pf[k] = *reinterpret_cast<const uint4 *>(Q + (((int64_t)b * gm.Lq + (pe[k] >> 6)) * gm.Hq + g * G + r % G) * D + c);
     }
   };
-  prefetch(0);
+  load_entries(0);
+  fetch_rows();
+  load_entries(CT);
 
   const float sl2 = gm.scale * kLog2e;
   const int key0 = t * 64;
@@ -95,7 +106,10 @@ __global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__re
       if (c == 0 && r % G == 0) ent_s[r / G] = pe[k];
     }
     __syncthreads();
-    if (c0 + CT < n_ent) prefetch(c0 + CT);
+    if (c0 + CT < n_ent) {
+      fetch_rows();
+      load_entries(c0 + 2 * CT);
+    }
 
     // S^T: 64 keys (4 tiles) x this wave's 16 rows
     f32x4 st[4];
@@ -159,12 +173,16 @@ __global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__re
   }
 }
 
-// One wave per (b, g, query row): merge the row's per-slot partials.
+// One wave per (b, g, query row): merge the row's per-slot partials.  For a
+// well-formed selection the valid slots are a prefix 0..n-1; that case runs
+// with the slot loop unrolled so all partial loads are in flight together.
+// Any other valid-slot pattern takes the general bit-walk.
 template <int D, int G>
 __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__restrict__ sel,
                                                                const bf16_t *__restrict__ opart,
                                                                const float2 *__restrict__ ml, bf16_t *__restrict__ O,
                                                                float *__restrict__ LSE, Geom gm) {
+  constexpr int U = 8;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t x = (int64_t)blockIdx.x * 4 + wave;  // bg * Lq + i
   if (x >= (int64_t)gm.B * gm.Hkv * gm.Lq) return;
@@ -173,27 +191,58 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
   const int cur = (gm.q_pos0 + i) / gm.m;
   const int tl = lane < gm.ksel ? sel[x * gm.ksel + lane] : -1;
   const uint64_t valid = __ballot(slot_ok(tl, cur, gm.T));
+  const int nv = __popcll(valid);
+  const bool prefix = valid == (nv == 64 ? ~0ull : ((1ull << nv) - 1));
   const int64_t base = x * gm.ksel;
   for (int e = lane * 4; e < G * D; e += 256) {
     const int hh = e / D, c = e - hh * D;
-    float M = -INFINITY;
-    for (uint64_t v = valid; v; v &= v - 1) M = fmaxf(M, ml[(base + __ffsll((long long)v) - 1) * G + hh].x);
-    float L = 0.f, acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, acc3 = 0.f;
-    for (uint64_t v = valid; v; v &= v - 1) {
-      const int64_t sl = base + __ffsll((long long)v) - 1;
-      const float2 q = ml[sl * G + hh];
-      const float w = exp2f(q.x - M);
-      L += w * q.y;
-      const uint2 raw = *reinterpret_cast<const uint2 *>(opart + (sl * G + hh) * D + c);
-      const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
-      acc0 = fmaf(w, bf16_to_f32(pv[0]), acc0);
-      acc1 = fmaf(w, bf16_to_f32(pv[1]), acc1);
-      acc2 = fmaf(w, bf16_to_f32(pv[2]), acc2);
-      acc3 = fmaf(w, bf16_to_f32(pv[3]), acc3);
+    float M = -INFINITY, L = 0.f, acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, acc3 = 0.f;
+    if (prefix) {
+      for (int k0 = 0; k0 < nv; k0 += U) {
+        float2 q[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) q[k] = k0 + k < nv ? ml[(base + k0 + k) * G + hh] : make_float2(-INFINITY, 0.f);
+#pragma unroll
+        for (int k = 0; k < U; ++k) M = fmaxf(M, q[k].x);
+      }
+      for (int k0 = 0; k0 < nv; k0 += U) {
+        float2 q[U];
+        uint2 raw[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          const bool ok = k0 + k < nv;
+          q[k] = ok ? ml[(base + k0 + k) * G + hh] : make_float2(-INFINITY, 0.f);
+          raw[k] = ok ? *reinterpret_cast<const uint2 *>(opart + ((base + k0 + k) * G + hh) * D + c) : make_uint2(0u, 0u);
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          const float w = exp2f(q[k].x - M);
+          L = fmaf(w, q[k].y, L);
+          const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw[k]);
+          acc0 = fmaf(w, bf16_to_f32(pv[0]), acc0);
+          acc1 = fmaf(w, bf16_to_f32(pv[1]), acc1);
+          acc2 = fmaf(w, bf16_to_f32(pv[2]), acc2);
+          acc3 = fmaf(w, bf16_to_f32(pv[3]), acc3);
+        }
+      }
+    } else {
+      for (uint64_t v = valid; v; v &= v - 1) M = fmaxf(M, ml[(base + __ffsll((long long)v) - 1) * G + hh].x);
+      for (uint64_t v = valid; v; v &= v - 1) {
+        const int64_t sl = base + __ffsll((long long)v) - 1;
+        const float2 q = ml[sl * G + hh];
+        const float w = exp2f(q.x - M);
+        L = fmaf(w, q.y, L);
+        const uint2 raw = *reinterpret_cast<const uint2 *>(opart + (sl * G + hh) * D + c);
+        const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
+        acc0 = fmaf(w, bf16_to_f32(pv[0]), acc0);
+        acc1 = fmaf(w, bf16_to_f32(pv[1]), acc1);
+        acc2 = fmaf(w, bf16_to_f32(pv[2]), acc2);
+        acc3 = fmaf(w, bf16_to_f32(pv[3]), acc3);
+      }
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
-    bf16_t outv[4] = {f32_to_bf16(acc0 * inv), f32_to_bf16(acc1 * inv), f32_to_bf16(acc2 * inv),
-                      f32_to_bf16(acc3 * inv)};
+    const bf16_t outv[4] = {f32_to_bf16(acc0 * inv), f32_to_bf16(acc1 * inv), f32_to_bf16(acc2 * inv),
+                            f32_to_bf16(acc3 * inv)};
     *reinterpret_cast<uint2 *>(O + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + hh) * D + c) =
         *reinterpret_cast<const uint2 *>(outv);
     if (c == 0) LSE[((int64_t)b * gm.Hq + g * G + hh) * gm.Lq + i] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
