@@ -34,28 +34,33 @@ namespace phsa {
 
 __device__ __forceinline__ bool slot_ok_b(int t, int cur, int T) { return t >= 0 && t <= cur && t < T; }
 
-// D = rowsum(dO * O) per (b, h, i), float32.
+// D = rowsum(dO * O) per (b, h, i), float32.  TPR threads cover one row with
+// 16-byte loads (coalesced), then reduce with lane shuffles.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(const T *__restrict__ O, const T *__restrict__ dO,
                                                       float *__restrict__ Dvec, Geom gm) {
-  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (b, i, h)
-  if (x >= (int64_t)gm.B * gm.Lq * gm.Hq) return;
-  const int h = (int)(x % gm.Hq);
-  const int64_t bi = x / gm.Hq;
-  const int i = (int)(bi % gm.Lq), b = (int)(bi / gm.Lq);
-  const T *o = O + x * D;
-  const T *d = dO + x * D;
-  float acc = 0.f;
   constexpr int V = 16 / sizeof(T);
-  for (int c = 0; c < D; c += V) {
-    const uint4 ro = *reinterpret_cast<const uint4 *>(o + c);
-    const uint4 rd = *reinterpret_cast<const uint4 *>(d + c);
+  constexpr int TPR = D / V;           // threads per row (8..32)
+  const int64_t x = ((int64_t)blockIdx.x * 256 + threadIdx.x) / TPR;  // row (b, i, h)
+  const int c = (threadIdx.x % TPR) * V;
+  const bool ok = x < (int64_t)gm.B * gm.Lq * gm.Hq;
+  float acc = 0.f;
+  if (ok) {
+    const uint4 ro = *reinterpret_cast<const uint4 *>(O + x * D + c);
+    const uint4 rd = *reinterpret_cast<const uint4 *>(dO + x * D + c);
     const T *po = reinterpret_cast<const T *>(&ro);
     const T *pd = reinterpret_cast<const T *>(&rd);
 #pragma unroll
     for (int e = 0; e < V; ++e) acc = fmaf(to_f32<T>(po[e]), to_f32<T>(pd[e]), acc);
   }
-  Dvec[((int64_t)b * gm.Hq + h) * gm.Lq + i] = acc;
+#pragma unroll
+  for (int o = 1; o < TPR; o <<= 1) acc += __shfl_xor(acc, o, 64);
+  if (ok && c == 0) {
+    const int h = (int)(x % gm.Hq);
+    const int64_t bi = x / gm.Hq;
+    const int i = (int)(bi % gm.Lq), b = (int)(bi / gm.Lq);
+    Dvec[((int64_t)b * gm.Hq + h) * gm.Lq + i] = acc;
+  }
 }
 
 template <int D, int G>
@@ -385,7 +390,7 @@ static hipError_t launch_bwd_d(const Geom &g, const void *Q, const void *K, cons
 
 template <typename T, int D>
 static void launch_pre(const Geom &g, const void *O, const void *dO, float *Dvec, hipStream_t s) {
-  const int64_t n = (int64_t)g.B * g.Lq * g.Hq;
+  const int64_t n = (int64_t)g.B * g.Lq * g.Hq * (D / (16 / sizeof(T)));  // threads
   timing_begin("phsa_attn_bwd_pre", s);
   hipLaunchKernelGGL((bwd_pre_kernel<T, D>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
                      static_cast<const T *>(O), static_cast<const T *>(dO), Dvec, g);

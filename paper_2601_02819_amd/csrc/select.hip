@@ -181,7 +181,7 @@ __global__ __launch_bounds__(256) void select_kernel(const T *__restrict__ Q, co
 // buffer, and the row's four threads insert every fourth of them into their
 // lists (compare/select only, no memory traffic).  After the last chunk the
 // four lists are merged.
-template <int D, int KMAX>
+template <int D, int G, int KMAX>
 __global__ __launch_bounds__(256) void select_mfma_kernel(const bf16_t *__restrict__ Q, const float *__restrict__ Kc,
                                                           int32_t *__restrict__ sel, Geom gm) {
   constexpr int CH = 64;
@@ -204,23 +204,28 @@ __global__ __launch_bounds__(256) void select_mfma_kernel(const bf16_t *__restri
   const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg % gm.Hkv;
   const int i0 = blockIdx.x * 64;
 
-  // A operand: split query-head sums of row 16w + l16
+  // A operand: split query-head sums of row 16w + l16 (all loads issued together)
   bf16x8 ah[KB], al[KB];
   {
     const int ia = i0 + wave * 16 + l16;
+    uint4 raw[G][KB];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+        raw[hh][kb] = ia < gm.Lq ? *reinterpret_cast<const uint4 *>(
+                                       Q + (((int64_t)b * gm.Lq + ia) * gm.Hq + g * G + hh) * D + kb * 32 + kq)
+                                 : make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
       float qs[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) qs[e] = 0.f;
-      if (ia < gm.Lq) {
-        for (int hh = 0; hh < gm.G; ++hh) {
-          const uint4 raw = *reinterpret_cast<const uint4 *>(
-              Q + (((int64_t)b * gm.Lq + ia) * gm.Hq + g * gm.G + hh) * D + kb * 32 + kq);
-          const bf16_t *v = reinterpret_cast<const bf16_t *>(&raw);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) qs[e] += bf16_to_f32(v[e]);
-        }
+      for (int hh = 0; hh < G; ++hh) {
+        const bf16_t *v = reinterpret_cast<const bf16_t *>(&raw[hh][kb]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qs[e] += bf16_to_f32(v[e]);
       }
       bf16_t hi[8], lo[8];
 #pragma unroll
@@ -255,14 +260,27 @@ __global__ __launch_bounds__(256) void select_mfma_kernel(const bf16_t *__restri
   const int t_end = gm.top_k > 0 ? max(0, (gm.q_pos0 + last_i) / gm.m - gm.window / gm.m) : 0;
   const float *kc_bg = Kc + (int64_t)bg * gm.T * D;
 
-  for (int t0 = gm.n_init; t0 < t_end; t0 += CH) {
+  // representative chunks: the next chunk's float32 rows are fetched into
+  // registers while the current chunk is scored
+  constexpr int NM = CH * D / (256 * 4);
+  float4 mreg[NM];
+  auto fetch_chunk = [&](int t0) {
     const int nblk = min(CH, gm.T - t0);
+#pragma unroll
+    for (int k = 0; k < NM; ++k) {
+      const int e = (tid + 256 * k) * 4, row = e / D, c = e % D;
+      mreg[k] = row < nblk ? *reinterpret_cast<const float4 *>(kc_bg + (int64_t)(t0 + row) * D + c)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  if (gm.n_init < t_end) fetch_chunk(gm.n_init);
+
+  for (int t0 = gm.n_init; t0 < t_end; t0 += CH) {
     __syncthreads();
-    for (int e = tid * 4; e < CH * D; e += 256 * 4) {
-      const int row = e / D, c = e % D;
-      float4 m4 = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (row < nblk) m4 = *reinterpret_cast<const float4 *>(kc_bg + (int64_t)(t0 + row) * D + c);
-      const float mv[4] = {m4.x, m4.y, m4.z, m4.w};
+#pragma unroll
+    for (int k = 0; k < NM; ++k) {
+      const int e = (tid + 256 * k) * 4, row = e / D, c = e % D;
+      const float mv[4] = {mreg[k].x, mreg[k].y, mreg[k].z, mreg[k].w};
       bf16_t hi[4], lo[4];
 #pragma unroll
       for (int x = 0; x < 4; ++x) {
@@ -273,6 +291,7 @@ __global__ __launch_bounds__(256) void select_mfma_kernel(const bf16_t *__restri
       *reinterpret_cast<uint2 *>(&Ml[row * MP + c]) = *reinterpret_cast<const uint2 *>(lo);
     }
     __syncthreads();
+    if (t0 + CH < t_end) fetch_chunk(t0 + CH);
 
     f32x4 acc[4];
 #pragma unroll
@@ -423,22 +442,35 @@ static hipError_t launch_select_t(const Geom &g, const void *Q, const float *Kc,
   return hipGetLastError();
 }
 
-template <int D>
+template <int D, int G>
 static hipError_t launch_select_mfma(const Geom &g, const void *Q, const float *Kc, int32_t *sel, hipStream_t s) {
   dim3 grid((g.Lq + 63) / 64, g.B * g.Hkv);
   const bf16_t *q = static_cast<const bf16_t *>(Q);
   timing_begin("phsa_select", s);
-  if (g.top_k <= 16)
-    hipLaunchKernelGGL((select_mfma_kernel<D, 16>), grid, dim3(256), 0, s, q, Kc, sel, g);
+  if (g.top_k <= 8)
+    hipLaunchKernelGGL((select_mfma_kernel<D, G, 8>), grid, dim3(256), 0, s, q, Kc, sel, g);
+  else if (g.top_k <= 16)
+    hipLaunchKernelGGL((select_mfma_kernel<D, G, 16>), grid, dim3(256), 0, s, q, Kc, sel, g);
   else
-    hipLaunchKernelGGL((select_mfma_kernel<D, 32>), grid, dim3(256), 0, s, q, Kc, sel, g);
+    hipLaunchKernelGGL((select_mfma_kernel<D, G, 32>), grid, dim3(256), 0, s, q, Kc, sel, g);
   timing_end(s);
   return hipGetLastError();
 }
 
+template <int D>
+static hipError_t launch_select_mfma_d(const Geom &g, const void *Q, const float *Kc, int32_t *sel, hipStream_t s) {
+  switch (g.G) {
+    case 1: return launch_select_mfma<D, 1>(g, Q, Kc, sel, s);
+    case 2: return launch_select_mfma<D, 2>(g, Q, Kc, sel, s);
+    case 4: return launch_select_mfma<D, 4>(g, Q, Kc, sel, s);
+    case 8: return launch_select_mfma<D, 8>(g, Q, Kc, sel, s);
+    default: return launch_select_t<bf16_t, D>(g, Q, Kc, sel, s);
+  }
+}
+
 hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t *sel, hipStream_t s) {
   if (g.dtype == 0)
-    return g.d == 128 ? launch_select_mfma<128>(g, Q, Kc, sel, s) : launch_select_mfma<64>(g, Q, Kc, sel, s);
+    return g.d == 128 ? launch_select_mfma_d<128>(g, Q, Kc, sel, s) : launch_select_mfma_d<64>(g, Q, Kc, sel, s);
   return g.d == 128 ? launch_select_t<float, 128>(g, Q, Kc, sel, s) : launch_select_t<float, 64>(g, Q, Kc, sel, s);
 }
 
