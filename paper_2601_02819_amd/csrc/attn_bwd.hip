@@ -34,7 +34,8 @@ namespace phsa {
 
 __device__ __forceinline__ bool slot_ok_b(int t, int cur, int T) { return t >= 0 && t <= cur && t < T; }
 
-// D = rowsum(dO * O) per (b, h, i), float32.  TPR threads cover one row with
+// D = rowsum(dO * O) per (b, i, h), float32, stored [B, Lq, Hq] (workspace
+// layout).  TPR threads cover one row with
 // 16-byte loads (coalesced), then reduce with lane shuffles.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(const T *__restrict__ O, const T *__restrict__ dO,
@@ -55,12 +56,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const T *__restrict__ O, c
   }
 #pragma unroll
   for (int o = 1; o < TPR; o <<= 1) acc += __shfl_xor(acc, o, 64);
-  if (ok && c == 0) {
-    const int h = (int)(x % gm.Hq);
-    const int64_t bi = x / gm.Hq;
-    const int i = (int)(bi % gm.Lq), b = (int)(bi / gm.Lq);
-    Dvec[((int64_t)b * gm.Hq + h) * gm.Lq + i] = acc;
-  }
+  if (ok && c == 0) Dvec[x] = acc;  // [B, Lq, Hq], the row order of O
 }
 
 template <int D, int G>
@@ -142,9 +138,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     if (tid < 64) {
       if (nrow >= 0) {
         const int i = nrow >> 6;
-        const int64_t li = ((int64_t)b * gm.Hq + g * G + tid % G) * gm.Lq + i;
-        plse = LSE[li] * kLog2e;
-        pdd = Dvec[li];
+        const int h = g * G + tid % G;
+        plse = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + i] * kLog2e;
+        pdd = Dvec[((int64_t)b * gm.Lq + i) * gm.Hq + h];
         ppos = gm.q_pos0 + i;
       } else {
         plse = 0.f;
@@ -278,7 +274,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   }
 }
 
-// Per (b, g, t): sum float32 partials of multi-unit blocks; zero unselected blocks.
+// Per (b, g, t): sum float32 partials of multi-unit blocks; zero unselected
+// blocks.  Each block's 2 x 64 x d outputs are split over kFinSplit
+// workgroups; each thread owns 4 consecutive features (16-byte loads).
+constexpr int kFinSplit = 16;
 template <int D>
 __global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restrict__ dkvpart, bf16_t *__restrict__ dK,
                                                            bf16_t *__restrict__ dV, Geom gm, IndexWs ix) {
@@ -287,70 +286,79 @@ __global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restri
   if (u1 - u0 == 1) return;  // written by the sparse kernel
   const int bg = bgt / gm.T, t = bgt - bg * gm.T;
   const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
-  for (int x = threadIdx.x; x < 64 * D; x += 256) {
+  constexpr int PER = 64 * D / kFinSplit;  // elements of dK (and of dV) per workgroup
+  for (int x = blockIdx.y * PER + threadIdx.x * 4; x < (blockIdx.y + 1) * PER; x += 256 * 4) {
     const int kk = x / D, c = x - kk * D;
-    float sk = 0.f, sv = 0.f;
+    float4 sk = make_float4(0.f, 0.f, 0.f, 0.f), sv = sk;
     for (int u = u0; u < u1; ++u) {
-      sk += dkvpart[(int64_t)u * 2 * 64 * D + x];
-      sv += dkvpart[(int64_t)u * 2 * 64 * D + 64 * D + x];
+      const float4 a = *reinterpret_cast<const float4 *>(dkvpart + (int64_t)u * 2 * 64 * D + x);
+      const float4 v = *reinterpret_cast<const float4 *>(dkvpart + (int64_t)u * 2 * 64 * D + 64 * D + x);
+      sk.x += a.x; sk.y += a.y; sk.z += a.z; sk.w += a.w;
+      sv.x += v.x; sv.y += v.y; sv.z += v.z; sv.w += v.w;
     }
     const int64_t dst = (((int64_t)b * gm.Lk + (int64_t)t * 64 + kk) * gm.Hkv + g) * D + c;
-    dK[dst] = f32_to_bf16(sk);
-    dV[dst] = f32_to_bf16(sv);
+    const bf16_t k4[4] = {f32_to_bf16(sk.x), f32_to_bf16(sk.y), f32_to_bf16(sk.z), f32_to_bf16(sk.w)};
+    const bf16_t v4[4] = {f32_to_bf16(sv.x), f32_to_bf16(sv.y), f32_to_bf16(sv.z), f32_to_bf16(sv.w)};
+    *reinterpret_cast<uint2 *>(dK + dst) = *reinterpret_cast<const uint2 *>(k4);
+    *reinterpret_cast<uint2 *>(dV + dst) = *reinterpret_cast<const uint2 *>(v4);
   }
 }
 
-// One wave per (b, g, query row): dQ = sum over valid slots of the partials
-// (unrolled over a prefix of valid slots, the well-formed case; else a bit-walk).
+// dQ = sum over a row's valid slots of the partials.  Half a wave per
+// (b, g, query row), 8 features per lane (16-byte loads); the slot loop is
+// unrolled over a prefix of valid slots (the well-formed case), else a bit-walk.
 template <int D, int G>
 __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restrict__ sel,
                                                          const bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dQ,
                                                          Geom gm) {
   constexpr int U = 8;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t x = (int64_t)blockIdx.x * 4 + wave;
-  if (x >= (int64_t)gm.B * gm.Hkv * gm.Lq) return;
-  const int bg = (int)(x / gm.Lq), i = (int)(x - (int64_t)bg * gm.Lq);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
+  const int64_t x = ((int64_t)blockIdx.x * 4 + wave) * 2 + half;
+  const bool row_ok = x < (int64_t)gm.B * gm.Hkv * gm.Lq;
+  const int64_t xr = row_ok ? x : 0;
+  const int bg = (int)(xr / gm.Lq), i = (int)(xr - (int64_t)bg * gm.Lq);
   const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   const int cur = (gm.q_pos0 + i) / gm.m;
-  const int tl = lane < gm.ksel ? sel[x * gm.ksel + lane] : -1;
-  const uint64_t valid = __ballot(slot_ok_b(tl, cur, gm.T));
+  // valid slots of this half's row (Ksel <= 64): lane l32 tests slots l32 and l32 + 32
+  const int ta = (row_ok && l32 < gm.ksel) ? sel[xr * gm.ksel + l32] : -1;
+  const int tb = (row_ok && l32 + 32 < gm.ksel) ? sel[xr * gm.ksel + l32 + 32] : -1;
+  const uint64_t ba = __ballot(slot_ok_b(ta, cur, gm.T)), bb = __ballot(slot_ok_b(tb, cur, gm.T));
+  const uint64_t valid = ((ba >> (32 * half)) & 0xffffffffull) | (((bb >> (32 * half)) & 0xffffffffull) << 32);
   const int nv = __popcll(valid);
   const bool prefix = valid == (nv == 64 ? ~0ull : ((1ull << nv) - 1));
-  const int64_t base = x * gm.ksel;
-  for (int e = lane * 4; e < G * D; e += 256) {
+  const int64_t base = xr * gm.ksel;
+  if (!row_ok) return;
+  for (int e = l32 * 8; e < G * D; e += 256) {
     const int hh = e / D, c = e - hh * D;
-    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    float a[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) a[k] = 0.f;
+    auto add = [&](const uint4 &raw) {
+      const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) a[k] += bf16_to_f32(pv[k]);
+    };
     if (prefix) {
       for (int k0 = 0; k0 < nv; k0 += U) {
-        uint2 raw[U];
+        uint4 raw[U];
 #pragma unroll
         for (int k = 0; k < U; ++k)
-          raw[k] = k0 + k < nv ? *reinterpret_cast<const uint2 *>(dqpart + ((base + k0 + k) * G + hh) * D + c)
-                               : make_uint2(0u, 0u);
+          raw[k] = k0 + k < nv ? *reinterpret_cast<const uint4 *>(dqpart + ((base + k0 + k) * G + hh) * D + c)
+                               : make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
-          const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw[k]);
-          a0 += bf16_to_f32(pv[0]);
-          a1 += bf16_to_f32(pv[1]);
-          a2 += bf16_to_f32(pv[2]);
-          a3 += bf16_to_f32(pv[3]);
-        }
+        for (int k = 0; k < U; ++k) add(raw[k]);
       }
     } else {
       for (uint64_t v = valid; v; v &= v - 1) {
         const int64_t sl = base + __ffsll((long long)v) - 1;
-        const uint2 raw = *reinterpret_cast<const uint2 *>(dqpart + (sl * G + hh) * D + c);
-        const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
-        a0 += bf16_to_f32(pv[0]);
-        a1 += bf16_to_f32(pv[1]);
-        a2 += bf16_to_f32(pv[2]);
-        a3 += bf16_to_f32(pv[3]);
+        add(*reinterpret_cast<const uint4 *>(dqpart + (sl * G + hh) * D + c));
       }
     }
-    const bf16_t outv[4] = {f32_to_bf16(a0), f32_to_bf16(a1), f32_to_bf16(a2), f32_to_bf16(a3)};
-    *reinterpret_cast<uint2 *>(dQ + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + hh) * D + c) =
-        *reinterpret_cast<const uint2 *>(outv);
+    bf16_t outv[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) outv[k] = f32_to_bf16(a[k]);
+    *reinterpret_cast<uint4 *>(dQ + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + hh) * D + c) =
+        *reinterpret_cast<const uint4 *>(outv);
   }
 }
 
@@ -365,12 +373,12 @@ static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, cons
                      static_cast<bf16_t *>(dK), static_cast<bf16_t *>(dV), dkvpart);
   timing_end(s);
   timing_begin("phsa_attn_bwd_dkv_finalize", s);
-  hipLaunchKernelGGL((dkv_finalize_kernel<D>), dim3(g.B * g.Hkv * g.T), dim3(256), 0, s, dkvpart,
+  hipLaunchKernelGGL((dkv_finalize_kernel<D>), dim3(g.B * g.Hkv * g.T, kFinSplit), dim3(256), 0, s, dkvpart,
                      static_cast<bf16_t *>(dK), static_cast<bf16_t *>(dV), g, ix);
   timing_end(s);
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_attn_bwd_dq_combine", s);
-  hipLaunchKernelGGL((dq_combine_kernel<D, G>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, sel,
+  hipLaunchKernelGGL((dq_combine_kernel<D, G>), dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s, sel,
                      static_cast<const bf16_t *>(dqpart), static_cast<bf16_t *>(dQ), g);
   timing_end(s);
   return hipGetLastError();

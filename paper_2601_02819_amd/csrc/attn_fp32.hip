@@ -96,7 +96,7 @@ __global__ __launch_bounds__(64) void attn_bwd_fp32_kernel(const float *__restri
     dos[c] = dO[qrow + c];
   }
   const float lse = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + i];
-  const float dd = Dvec[((int64_t)b * gm.Hq + h) * gm.Lq + i];
+  const float dd = Dvec[((int64_t)b * gm.Lq + i) * gm.Hq + h];
   __syncthreads();
   float dq[NC];
 #pragma unroll

@@ -173,56 +173,63 @@ __global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__re
   }
 }
 
-// One wave per (b, g, query row): merge the row's per-slot partials.  For a
-// well-formed selection the valid slots are a prefix 0..n-1; that case runs
-// with the slot loop unrolled so all partial loads are in flight together.
-// Any other valid-slot pattern takes the general bit-walk.
+// Merge of a row's per-slot partials.  Half a wave per (b, g, query row), 8
+// features per lane (16-byte loads).  For a well-formed selection the valid
+// slots are a prefix 0..n-1; that case runs with the slot loop unrolled so
+// all partial loads are in flight together.  Other patterns take a bit-walk.
 template <int D, int G>
 __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__restrict__ sel,
                                                                const bf16_t *__restrict__ opart,
                                                                const float2 *__restrict__ ml, bf16_t *__restrict__ O,
                                                                float *__restrict__ LSE, Geom gm) {
   constexpr int U = 8;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t x = (int64_t)blockIdx.x * 4 + wave;  // bg * Lq + i
-  if (x >= (int64_t)gm.B * gm.Hkv * gm.Lq) return;
-  const int bg = (int)(x / gm.Lq), i = (int)(x - (int64_t)bg * gm.Lq);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
+  const int64_t x = ((int64_t)blockIdx.x * 4 + wave) * 2 + half;  // bg * Lq + i
+  const bool row_ok = x < (int64_t)gm.B * gm.Hkv * gm.Lq;
+  const int64_t xr = row_ok ? x : 0;
+  const int bg = (int)(xr / gm.Lq), i = (int)(xr - (int64_t)bg * gm.Lq);
   const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   const int cur = (gm.q_pos0 + i) / gm.m;
-  const int tl = lane < gm.ksel ? sel[x * gm.ksel + lane] : -1;
-  const uint64_t valid = __ballot(slot_ok(tl, cur, gm.T));
+  // valid slots of this half's row (Ksel <= 64): lane l32 tests slots l32 and l32 + 32
+  const int ta = (row_ok && l32 < gm.ksel) ? sel[xr * gm.ksel + l32] : -1;
+  const int tb = (row_ok && l32 + 32 < gm.ksel) ? sel[xr * gm.ksel + l32 + 32] : -1;
+  const uint64_t ba = __ballot(slot_ok(ta, cur, gm.T)), bb = __ballot(slot_ok(tb, cur, gm.T));
+  const uint64_t valid = ((ba >> (32 * half)) & 0xffffffffull) | (((bb >> (32 * half)) & 0xffffffffull) << 32);
   const int nv = __popcll(valid);
   const bool prefix = valid == (nv == 64 ? ~0ull : ((1ull << nv) - 1));
-  const int64_t base = x * gm.ksel;
-  for (int e = lane * 4; e < G * D; e += 256) {
+  const int64_t base = xr * gm.ksel;
+  if (!row_ok) return;
+  for (int e = l32 * 8; e < G * D; e += 256) {
     const int hh = e / D, c = e - hh * D;
-    float M = -INFINITY, L = 0.f, acc0 = 0.f, acc1 = 0.f, acc2 = 0.f, acc3 = 0.f;
+    float M = -INFINITY, L = 0.f, a[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) a[k] = 0.f;
+    auto add = [&](float w, const uint4 &raw) {
+      const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) a[k] = fmaf(w, bf16_to_f32(pv[k]), a[k]);
+    };
     if (prefix) {
       for (int k0 = 0; k0 < nv; k0 += U) {
-        float2 q[U];
 #pragma unroll
-        for (int k = 0; k < U; ++k) q[k] = k0 + k < nv ? ml[(base + k0 + k) * G + hh] : make_float2(-INFINITY, 0.f);
-#pragma unroll
-        for (int k = 0; k < U; ++k) M = fmaxf(M, q[k].x);
+        for (int k = 0; k < U; ++k)
+          if (k0 + k < nv) M = fmaxf(M, ml[(base + k0 + k) * G + hh].x);
       }
       for (int k0 = 0; k0 < nv; k0 += U) {
         float2 q[U];
-        uint2 raw[U];
+        uint4 raw[U];
 #pragma unroll
         for (int k = 0; k < U; ++k) {
           const bool ok = k0 + k < nv;
           q[k] = ok ? ml[(base + k0 + k) * G + hh] : make_float2(-INFINITY, 0.f);
-          raw[k] = ok ? *reinterpret_cast<const uint2 *>(opart + ((base + k0 + k) * G + hh) * D + c) : make_uint2(0u, 0u);
+          raw[k] = ok ? *reinterpret_cast<const uint4 *>(opart + ((base + k0 + k) * G + hh) * D + c)
+                      : make_uint4(0u, 0u, 0u, 0u);
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
           const float w = exp2f(q[k].x - M);
           L = fmaf(w, q[k].y, L);
-          const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw[k]);
-          acc0 = fmaf(w, bf16_to_f32(pv[0]), acc0);
-          acc1 = fmaf(w, bf16_to_f32(pv[1]), acc1);
-          acc2 = fmaf(w, bf16_to_f32(pv[2]), acc2);
-          acc3 = fmaf(w, bf16_to_f32(pv[3]), acc3);
+          add(w, raw[k]);
         }
       }
     } else {
@@ -232,19 +239,15 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
         const float2 q = ml[sl * G + hh];
         const float w = exp2f(q.x - M);
         L = fmaf(w, q.y, L);
-        const uint2 raw = *reinterpret_cast<const uint2 *>(opart + (sl * G + hh) * D + c);
-        const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
-        acc0 = fmaf(w, bf16_to_f32(pv[0]), acc0);
-        acc1 = fmaf(w, bf16_to_f32(pv[1]), acc1);
-        acc2 = fmaf(w, bf16_to_f32(pv[2]), acc2);
-        acc3 = fmaf(w, bf16_to_f32(pv[3]), acc3);
+        add(w, *reinterpret_cast<const uint4 *>(opart + (sl * G + hh) * D + c));
       }
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
-    const bf16_t outv[4] = {f32_to_bf16(acc0 * inv), f32_to_bf16(acc1 * inv), f32_to_bf16(acc2 * inv),
-                            f32_to_bf16(acc3 * inv)};
-    *reinterpret_cast<uint2 *>(O + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + hh) * D + c) =
-        *reinterpret_cast<const uint2 *>(outv);
+    bf16_t outv[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) outv[k] = f32_to_bf16(a[k] * inv);
+    *reinterpret_cast<uint4 *>(O + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + hh) * D + c) =
+        *reinterpret_cast<const uint4 *>(outv);
     if (c == 0) LSE[((int64_t)b * gm.Hq + g * G + hh) * gm.Lq + i] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
   }
 }
@@ -259,7 +262,7 @@ static hipError_t launch_fwd_t(const Geom &g, const void *Q, const void *K, cons
   timing_end(s);
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_attn_fwd_combine", s);
-  hipLaunchKernelGGL((attn_fwd_combine_kernel<D, G>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, sel,
+  hipLaunchKernelGGL((attn_fwd_combine_kernel<D, G>), dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s, sel,
                      static_cast<const bf16_t *>(opart), ml, static_cast<bf16_t *>(O), LSE, g);
   timing_end(s);
   return hipGetLastError();
