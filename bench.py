@@ -30,6 +30,56 @@ from paper_2601_02819_amd import phsa  # noqa: E402
 from paper_2601_02819_amd.inputs import WORKLOADS, make_inputs  # noqa: E402
 
 METRIC = "PHSA fwd+bwd ms & selected-block TFLOP/s at L=32k, 97.3% sparsity; % MFMA peak"
+CSRC = os.path.join(ROOT, "paper_2601_02819_amd", "csrc")
+# kernel name in the timing hooks -> its source file (the traffic record is void once that changes)
+KERNEL_SOURCE = {"phsa_attn_bwd_sparse": "attn_bwd.hip", "phsa_attn_fwd_sparse": "attn_fwd.hip",
+                 "phsa_select": "select.hip", "phsa_compress": "compress.hip"}
+# rocprofv3 kernel-name fragment of each timed kernel
+KERNEL_SYMBOL = {"phsa_attn_bwd_sparse": "attn_bwd_sparse_kernel", "phsa_attn_fwd_sparse": "attn_fwd_sparse_kernel",
+                 "phsa_select": "select_mfma_kernel", "phsa_compress": "compress_kernel"}
+
+
+def source_hash(kernel: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in (KERNEL_SOURCE[kernel], "common.h", "launch.h"):
+        h.update(open(os.path.join(CSRC, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def summarize_traffic(fetch_csv: str, write_csv: str, copy_mb: int, out_json: str) -> None:
+    """Turns two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; KiB per dispatch) into
+    calibrated HBM bytes per launch: each counter is scaled by what it reads for the
+    plain elementwise copy of copy_mb MiB that --calib-copy-mb runs first."""
+    import csv
+    import statistics
+
+    def per_kernel(path):
+        d = {}
+        for r in csv.DictReader(open(path)):
+            d.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return d
+
+    fd, wd = per_kernel(fetch_csv), per_kernel(write_csv)
+    copy_kib = copy_mb * 1024.0
+    cal = [n for n in fd if "MulFunctor" in n or "mul" in n.split("(")[0].lower()]
+    big = [n for n in cal if max(fd[n]) > 0.25 * copy_kib]
+    if not big:
+        raise SystemExit("calibration copy kernel not found in " + fetch_csv)
+    fetch_factor = copy_kib / max(fd[big[0]])
+    write_factor = copy_kib / max(wd[big[0]])
+    rec = {"calibration_kernel": big[0].split("(")[0], "copy_mib": copy_mb,
+           "fetch_factor": fetch_factor, "write_factor": write_factor, "kernels": {}}
+    for k, sym in KERNEL_SYMBOL.items():
+        names = [n for n in fd if sym in n]
+        if not names:
+            continue
+        f = statistics.median(fd[names[0]]) * 1024 * fetch_factor
+        w = statistics.median(wd[names[0]]) * 1024 * write_factor
+        rec["kernels"][k] = {"symbol": names[0].split("(")[0], "fetch_bytes": f, "write_bytes": w,
+                             "bytes_per_launch": f + w, "source_hash": source_hash(k)}
+    json.dump(rec, open(out_json, "w"), indent=1)
+    print(json.dumps(rec, indent=1))
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 
@@ -187,7 +237,13 @@ def main():
                          "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM traffic of the dominant kernel (from rocprofv3 counters)")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write --traffic from two rocprofv3 --pmc counter_collection.csv files and exit")
     args = ap.parse_args()
+    if args.summarize_traffic:
+        summarize_traffic(args.summarize_traffic[0], args.summarize_traffic[1], args.calib_copy_mb or 1024,
+                          args.traffic)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the PHSA path shards by (batch, KV head) with no exchange, "
               "and multi-GPU runs are not part of this build.", file=sys.stderr)
@@ -197,10 +253,11 @@ def main():
         sys.exit(2)
     phsa.lib()
     if args.calib_copy_mb > 0:
+        # plain elementwise copy (reads N bytes, writes N bytes) for counter calibration
         n = args.calib_copy_mb * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         del src, dst
 
@@ -210,10 +267,10 @@ def main():
     traffic = None
     if os.path.exists(args.traffic):
         try:
-            tinfo = json.load(open(args.traffic))
-            if tinfo.get("kernel") == dom:
-                traffic = tinfo.get("bytes_per_launch")
-        except (OSError, ValueError):
+            tk = json.load(open(args.traffic)).get("kernels", {}).get(dom)
+            if tk and tk.get("source_hash") == source_hash(dom):
+                traffic = tk["bytes_per_launch"]
+        except (OSError, ValueError, KeyError):
             traffic = None
     roofline = {"bound": "mfma" if dk.get("unit") == "TFLOP/s" else "hbm", "kernel": dom,
                 "achieved": dk.get("rate"), "peak": PEAK_BF16_TFLOPS if dk.get("unit") == "TFLOP/s" else PEAK_HBM_GBS,

@@ -343,8 +343,7 @@ __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restri
         uint4 raw[U];
 #pragma unroll
         for (int k = 0; k < U; ++k)
-          raw[k] = k0 + k < nv ? *reinterpret_cast<const uint4 *>(dqpart + ((base + k0 + k) * G + hh) * D + c)
-                               : make_uint4(0u, 0u, 0u, 0u);
+          raw[k] = k0 + k < nv ? ld_stream16(dqpart + ((base + k0 + k) * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
         for (int k = 0; k < U; ++k) add(raw[k]);
       }

@@ -222,8 +222,7 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
         for (int k = 0; k < U; ++k) {
           const bool ok = k0 + k < nv;
           q[k] = ok ? ml[(base + k0 + k) * G + hh] : make_float2(-INFINITY, 0.f);
-          raw[k] = ok ? *reinterpret_cast<const uint4 *>(opart + ((base + k0 + k) * G + hh) * D + c)
-                      : make_uint4(0u, 0u, 0u, 0u);
+          raw[k] = ok ? ld_stream16(opart + ((base + k0 + k) * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {

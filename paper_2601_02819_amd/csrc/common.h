@@ -43,6 +43,13 @@ __device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8 &a, const bf16x8 &b, 
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// 16-byte load of data that is read once (bypasses cache retention).
+__device__ __forceinline__ uint4 ld_stream16(const bf16_t *p) {
+  const uint32_t *q = reinterpret_cast<const uint32_t *>(p);
+  return make_uint4(__builtin_nontemporal_load(q), __builtin_nontemporal_load(q + 1),
+                    __builtin_nontemporal_load(q + 2), __builtin_nontemporal_load(q + 3));
+}
+
 __device__ __forceinline__ bf16x8 load_bf16x8(const bf16_t *p) {  // 16-byte aligned
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(p));
 }

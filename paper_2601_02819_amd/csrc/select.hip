@@ -191,8 +191,10 @@ __global__ __launch_bounds__(256) void select_mfma_kernel(const bf16_t *__restri
   constexpr int LIST_BYTES = 4 * 64 * KMAX * 8;
   constexpr int BUF = TILE_BYTES > LIST_BYTES ? TILE_BYTES : LIST_BYTES;
   __shared__ __attribute__((aligned(16))) unsigned char smem[BUF];
-  __shared__ float nb_s[64][CH];
-  __shared__ int nb_t[64][CH];
+  // candidate buffers, one row per query row; rows padded by one word so that the
+  // merge threads (lane = row) do not all hit the same LDS bank
+  __shared__ float nb_s[64][CH + 1];
+  __shared__ int nb_t[64][CH + 1];
   __shared__ int nnew[64];
   __shared__ float bar_s[4][64];
   __shared__ int bar_t[4][64];
