@@ -3,20 +3,24 @@
 // Work is key-block-major.  Every query row selects its own blocks, so the
 // only operand that many rows share is a key/value block.  A workgroup takes
 // one work unit = one (b, g, t) block plus up to unit_tokens entries of the
-// list of rows that selected it, keeps K_t and V_t in LDS for the whole unit,
-// and streams the rows through it in chunks of 64 MFMA rows (64 / G tokens x
-// the G heads of the group); wave w owns chunk rows 16w..16w+15:
+// list of rows that selected it and keeps K_t and V_t in LDS.  Each wave then
+// works through the unit on its own, in wave chunks of 16 MFMA rows (16 / G
+// tokens x the G heads of the group), chunks w, w + 4, ...:
 //
-//   S^T = K_t Q_w^T                    (64 keys x 16 rows, 16x16x32 bf16 MFMA)
+//   S^T = K_t Q^T                      (64 keys x 16 rows, 16x16x32 bf16 MFMA)
 //   m = rowmax, P = 2^(S - m), l = rowsum(P)      (token-level causal mask)
 //   O^T = V_t^T P^T                    (d x 16 rows)
 //
-// The S^T accumulator layout (lane (q, j) holds keys 4q + r of row j) is used
-// directly as the P^T operand of the second product, pairing key tiles
-// {4q..4q+3} and {16+4q..16+4q+3}; V_t^T is read with transposing LDS loads
-// over the same key set, so P never goes through LDS.  O^T leaves each lane
-// with 4 consecutive features of one row (8-byte stores).  The next chunk's
-// query rows are gathered into registers while the current one computes.
+// The gathered query rows go straight from global memory into registers in
+// the B-operand layout of S^T (lane (q, j) holds features 32kb + 8q .. +7 of
+// row j), so there is no shared query tile and no barrier after the K/V
+// load; each wave fetches its next chunk's rows while it computes the current
+// one, with the list entries read one chunk further ahead.  The S^T
+// accumulator layout (lane (q, j) holds keys 4q + r of row j) is used directly
+// as the P^T operand of the second product, pairing key tiles {4q..4q+3} and
+// {16+4q..16+4q+3}; V_t^T is read with transposing LDS loads over the same
+// key set, so P never goes through LDS.  O^T leaves each lane with 4
+// consecutive features of one row (8-byte stores).
 //
 // Output per (row, slot): the unnormalised partial O (bf16) and (m, l) in
 // log2 units.  A second kernel merges the at most Ksel partials of each row:
@@ -32,20 +36,17 @@ namespace phsa {
 __device__ __forceinline__ bool slot_ok(int t, int cur, int T) { return t >= 0 && t <= cur && t < T; }
 
 template <int D, int G>
-__global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__restrict__ Q,
+__global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *__restrict__ Q,
                                                               const bf16_t *__restrict__ K,
                                                               const bf16_t *__restrict__ V, Geom gm, IndexWs ix,
                                                               bf16_t *__restrict__ opart, float2 *__restrict__ ml) {
-  constexpr int CT = 64 / G;         // query tokens per chunk
+  constexpr int TW = 16 / G;         // query tokens per wave chunk
   constexpr int KP = D + 8;          // LDS row pitch (elements)
   constexpr int VPR = D / 8;         // 16-byte vectors per row
-  constexpr int NV = 64 * VPR / 256; // gathered vectors per thread per chunk
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[64 * KP];
-  __shared__ int ent_s[64];
 
   const int u = blockIdx.x;
   if (u >= ix.totals[1]) return;
@@ -64,66 +65,42 @@ __global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__re
     *reinterpret_cast<uint4 *>(&Ks[kk * KP + c]) = *reinterpret_cast<const uint4 *>(K + grow * D + c);
     *reinterpret_cast<uint4 *>(&Vs[kk * KP + c]) = *reinterpret_cast<const uint4 *>(V + grow * D + c);
   }
+  __syncthreads();
 
-  // Row gather, pipelined two deep: the list entries of chunk c + 2 are read
-  // while the rows of chunk c + 1 are fetched, which is while chunk c computes.
-  // Thread handles 16-byte vectors tid + 256 k (row = v / VPR).
-  int ne[NV];
-  uint4 pf[NV];
-  int pe[NV];
-  auto load_entries = [&](int c0) {
-    const int ntok = min(CT, n_ent - c0);
-#pragma unroll
-    for (int k = 0; k < NV; ++k) {
-      const int tk = ((tid + 256 * k) / VPR) / G;
-      ne[k] = (c0 < n_ent && tk < ntok) ? list[c0 + tk] : -1;
-    }
+  // lane (q, j) works on row j = l16 of the wave chunk: token j / G, head j % G
+  const int hh = l16 % G;
+  const int nch = (n_ent + TW - 1) / TW;
+  auto entry = [&](int c) {
+    const int tk = c * TW + l16 / G;
+    return (c < nch && tk < n_ent) ? list[tk] : -1;
   };
-  auto fetch_rows = [&]() {
+  auto fetch = [&](int e, bf16x8 (&qf)[KB]) {
 #pragma unroll
-    for (int k = 0; k < NV; ++k) {
-      const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
-      pe[k] = ne[k];
-      pf[k] = make_uint4(0u, 0u, 0u, 0u);
-      if (pe[k] >= 0)
-        pf[k] = *reinterpret_cast<const uint4 *>(Q + (((int64_t)b * gm.Lq + (pe[k] >> 6)) * gm.Hq + g * G + r % G) * D + c);
-    }
+    for (int kb = 0; kb < KB; ++kb)
+      qf[kb] = e >= 0 ? load_bf16x8(Q + (((int64_t)b * gm.Lq + (e >> 6)) * gm.Hq + g * G + hh) * D + kb * 32 + kq)
+                      : __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
   };
-  load_entries(0);
-  fetch_rows();
-  load_entries(CT);
 
   const float sl2 = gm.scale * kLog2e;
   const int key0 = t * 64;
-  const int row = wave * 16 + l16;  // the chunk row whose S^T column this lane holds
+  int e_cur = entry(wave), e_nxt = entry(wave + 4);
+  bf16x8 qf[KB], qn[KB];
+  fetch(e_cur, qf);
 
-  for (int c0 = 0; c0 < n_ent; c0 += CT) {
-    __syncthreads();  // previous chunk is done with Qs / ent_s
-#pragma unroll
-    for (int k = 0; k < NV; ++k) {
-      const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
-      *reinterpret_cast<uint4 *>(&Qs[r * KP + c]) = pf[k];
-      if (c == 0 && r % G == 0) ent_s[r / G] = pe[k];
-    }
-    __syncthreads();
-    if (c0 + CT < n_ent) {
-      fetch_rows();
-      load_entries(c0 + 2 * CT);
-    }
+  for (int c = wave; c < nch; c += 4) {
+    // next chunk's rows (and the entries of the one after) are in flight during this one
+    const int e_nn = entry(c + 8);
+    fetch(e_nxt, qn);
 
-    // S^T: 64 keys (4 tiles) x this wave's 16 rows
     f32x4 st[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) st[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      const bf16x8 bq = load_bf16x8(&Qs[row * KP + kb * 32 + kq]);
+    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
-        st[kt] = mfma16x16x32(load_bf16x8(&Ks[(kt * 16 + l16) * KP + kb * 32 + kq]), bq, st[kt]);
-    }
-    const int e = ent_s[row / G];
-    const int pos = e >= 0 ? gm.q_pos0 + (e >> 6) : -1;
+        st[kt] = mfma16x16x32(load_bf16x8(&Ks[(kt * 16 + l16) * KP + kb * 32 + kq]), qf[kb], st[kt]);
+    const int pos = e_cur >= 0 ? gm.q_pos0 + (e_cur >> 6) : -1;
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
@@ -150,7 +127,6 @@ __global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__re
     const bf16x8 pb0 = pack_bf16x8(st[0], st[1]);  // keys {4q..4q+3} and {16+4q..16+4q+3}
     const bf16x8 pb1 = pack_bf16x8(st[2], st[3]);  // keys 32 + the same
 
-    // O^T = V^T P^T: d tiles x this wave's 16 rows
     f32x4 ot[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -158,9 +134,8 @@ __global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__re
       ot[nt] = mfma16x16x32(lds_col8(Vs, KP, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, ot[nt]);
       ot[nt] = mfma16x16x32(lds_col8(Vs, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, ot[nt]);
     }
-    if (e >= 0) {
-      const int64_t slot = ((int64_t)bg * gm.Lq + (e >> 6)) * gm.ksel + (e & 63);
-      const int hh = row % G;
+    if (e_cur >= 0) {
+      const int64_t slot = ((int64_t)bg * gm.Lq + (e_cur >> 6)) * gm.ksel + (e_cur & 63);
       if (q4 == 0) ml[slot * G + hh] = make_float2(mx, l);
       bf16_t *dst = opart + (slot * G + hh) * D + q4 * 4;
 #pragma unroll
@@ -170,6 +145,10 @@ __global__ __launch_bounds__(256) void attn_fwd_sparse_kernel(const bf16_t *__re
         *reinterpret_cast<uint2 *>(dst + nt * 16) = *reinterpret_cast<const uint2 *>(o4);
       }
     }
+    e_cur = e_nxt;
+    e_nxt = e_nn;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) qf[kb] = qn[kb];
   }
 }
 
