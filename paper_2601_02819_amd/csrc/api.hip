@@ -37,6 +37,7 @@ size_t index_layout(const Geom &g, char *base, IndexWs *ix) {
   w.uoff = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (nbgt + 1)));
   w.totals = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * 4));
   w.tok = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * w.nnz_max));
+  w.pmap = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * w.nnz_max));
   w.units = reinterpret_cast<int2 *>(take(sizeof(int2) * w.units_max));
   if (ix) *ix = w;
   return off;
@@ -60,7 +61,7 @@ size_t fwd_layout(const Geom &g, char *base, FwdWs *ws) {
   if (g.dtype == PHSA_FP32) return 0;
   FwdWs w{};
   size_t off = index_layout(g, base, &w.ix);
-  const int64_t slots = (int64_t)g.B * g.Hkv * g.Lq * g.ksel * g.G;
+  const int64_t slots = w.ix.nnz_max * g.G;  // partials in list order, one per (entry, head)
   w.opart = base ? base + off : nullptr;
   off += align_up(slots * g.d * elem_bytes(g));
   w.ml = base ? reinterpret_cast<float2 *>(base + off) : nullptr;
@@ -76,7 +77,7 @@ size_t bwd_layout(const Geom &g, char *base, BwdWs *ws) {
   w.Dvec = base ? reinterpret_cast<float *>(base + off) : nullptr;
   off += align_up(sizeof(float) * (size_t)g.B * g.Hq * g.Lq);
   if (g.dtype == PHSA_BF16) {
-    const int64_t slots = (int64_t)g.B * g.Hkv * g.Lq * g.ksel * g.G;
+    const int64_t slots = w.ix.nnz_max * g.G;
     w.dqpart = base ? base + off : nullptr;
     off += align_up(slots * g.d * elem_bytes(g));
     w.dkvpart = base ? reinterpret_cast<float *>(base + off) : nullptr;

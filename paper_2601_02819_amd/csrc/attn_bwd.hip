@@ -21,7 +21,8 @@
 // operand (row tiles {4q..4q+3} and {16+4q..16+4q+3}); dO^T, Q^T and K_t^T
 // come from the row-major tiles through transposing LDS loads, and dS
 // reaches the other waves through one [key][row] LDS tile.  dQ leaves as one
-// bf16 partial per (row, slot), summed by a per-row kernel.  dK/dV leave
+// bf16 partial per list entry, stored in list order (a unit writes one
+// contiguous run), and a per-row kernel sums a row's partials.  dK/dV leave
 // directly (bf16) when the unit covers its whole block, else as float32
 // partials that a per-block kernel sums; blocks nobody selected get zeros
 // from that kernel too.
@@ -226,7 +227,6 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
 
     // dQ^T = K^T dS^T for chunk rows 16w..16w+15 (all 64 keys)
     const int row = wave * 16 + l16;
-    const int e = ent_s[row / G];
     f32x4 dqt[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) dqt[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -237,14 +237,25 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       for (int nt = 0; nt < NT; ++nt)
         dqt[nt] = mfma16x16x32(lds_col8(Ks, KP, kb * 32 + kq, kb * 32 + kq + 4, nt * 16, l16), bs, dqt[nt]);
     }
-    if (e >= 0) {
-      bf16_t *dst =
-          dqpart + ((((int64_t)bg * gm.Lq + (e >> 6)) * gm.ksel + (e & 63)) * G + row % G) * D + q4 * 4;
+    // The wave's 16 dQ rows (chunk rows 16w..16w+15) are one contiguous run of
+    // the list-ordered partial buffer: stage them in this wave's rows of Qs
+    // (free after the dK product) and write full 16-byte lanes.
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const bf16_t o4[4] = {f32_to_bf16(dqt[nt][0] * gm.scale), f32_to_bf16(dqt[nt][1] * gm.scale),
-                              f32_to_bf16(dqt[nt][2] * gm.scale), f32_to_bf16(dqt[nt][3] * gm.scale)};
-        *reinterpret_cast<uint2 *>(dst + nt * 16) = *reinterpret_cast<const uint2 *>(o4);
+    for (int nt = 0; nt < NT; ++nt) {
+      const bf16_t o4[4] = {f32_to_bf16(dqt[nt][0] * gm.scale), f32_to_bf16(dqt[nt][1] * gm.scale),
+                            f32_to_bf16(dqt[nt][2] * gm.scale), f32_to_bf16(dqt[nt][3] * gm.scale)};
+      *reinterpret_cast<uint2 *>(&Qs[row * KP + nt * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(o4);
+    }
+    wave_lds_sync();
+    {
+      const int64_t run0 = ((int64_t)ix.off[bgt] + e0 + c0) * G + wave * 16;  // first row of this wave
+      const int nrows = min(CT, n_ent - c0) * G - wave * 16;                // valid rows of this wave
+#pragma unroll
+      for (int k = 0; k < 16 * VPR / 64; ++k) {
+        const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
+        if (r < nrows)
+          *reinterpret_cast<uint4 *>(dqpart + (run0 + r) * D + cc) =
+              *reinterpret_cast<const uint4 *>(&Qs[(wave * 16 + r) * KP + cc]);
       }
     }
   }
@@ -309,6 +320,7 @@ __global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restri
 // unrolled over a prefix of valid slots (the well-formed case), else a bit-walk.
 template <int D, int G>
 __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restrict__ sel,
+                                                         const int32_t *__restrict__ pmap,
                                                          const bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dQ,
                                                          Geom gm) {
   constexpr int U = 8;
@@ -340,16 +352,19 @@ __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restri
     };
     if (prefix) {
       for (int k0 = 0; k0 < nv; k0 += U) {
+        int pk[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) pk[k] = k0 + k < nv ? pmap[base + k0 + k] : 0;
         uint4 raw[U];
 #pragma unroll
         for (int k = 0; k < U; ++k)
-          raw[k] = k0 + k < nv ? ld_stream16(dqpart + ((base + k0 + k) * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
+          raw[k] = k0 + k < nv ? ld_stream16(dqpart + ((int64_t)pk[k] * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
         for (int k = 0; k < U; ++k) add(raw[k]);
       }
     } else {
       for (uint64_t v = valid; v; v &= v - 1) {
-        const int64_t sl = base + __ffsll((long long)v) - 1;
+        const int64_t sl = pmap[base + __ffsll((long long)v) - 1];
         add(*reinterpret_cast<const uint4 *>(dqpart + (sl * G + hh) * D + c));
       }
     }
@@ -378,7 +393,7 @@ static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, cons
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_attn_bwd_dq_combine", s);
   hipLaunchKernelGGL((dq_combine_kernel<D, G>), dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s, sel,
-                     static_cast<const bf16_t *>(dqpart), static_cast<bf16_t *>(dQ), g);
+                     ix.pmap, static_cast<const bf16_t *>(dqpart), static_cast<bf16_t *>(dQ), g);
   timing_end(s);
   return hipGetLastError();
 }

@@ -22,7 +22,8 @@
 // key set, so P never goes through LDS.  O^T leaves each lane with 4
 // consecutive features of one row (8-byte stores).
 //
-// Output per (row, slot): the unnormalised partial O (bf16) and (m, l) in
+// Output per list entry (row, slot), stored in list order so that a unit
+// writes one contiguous run: the unnormalised partial O (bf16) and (m, l) in
 // log2 units.  A second kernel merges the at most Ksel partials of each row:
 //   M = max_s m_s,  w_s = 2^(m_s - M),  O = sum_s w_s O_s / sum_s w_s l_s,
 //   LSE = (M + log2 sum_s w_s l_s) ln 2.
@@ -45,8 +46,10 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
   constexpr int VPR = D / 8;         // 16-byte vectors per row
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
+  constexpr int SP = D + 8;          // pitch of the per-wave output staging rows
   __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Os[4][16 * SP];  // per-wave partial rows
 
   const int u = blockIdx.x;
   if (u >= ix.totals[1]) return;
@@ -134,17 +137,27 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
       ot[nt] = mfma16x16x32(lds_col8(Vs, KP, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, ot[nt]);
       ot[nt] = mfma16x16x32(lds_col8(Vs, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, ot[nt]);
     }
-    if (e_cur >= 0) {
-      const int64_t slot = ((int64_t)bg * gm.Lq + (e_cur >> 6)) * gm.ksel + (e_cur & 63);
-      if (q4 == 0) ml[slot * G + hh] = make_float2(mx, l);
-      bf16_t *dst = opart + (slot * G + hh) * D + q4 * 4;
+    // The chunk's 16 partial rows are one contiguous run of the list-ordered
+    // partial buffer (entries c*TW.., heads inner): stage them in LDS and write
+    // full 16-byte lanes.
+    const int64_t run0 = (int64_t)ix.off[bgt] + e0 + c * TW;  // list position of the chunk's first entry
+    if (e_cur >= 0 && q4 == 0) ml[(run0 + l16 / G) * G + hh] = make_float2(mx, l);
+    bf16_t *os = Os[wave];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const bf16_t o4[4] = {f32_to_bf16(ot[nt][0]), f32_to_bf16(ot[nt][1]), f32_to_bf16(ot[nt][2]),
-                              f32_to_bf16(ot[nt][3])};
-        *reinterpret_cast<uint2 *>(dst + nt * 16) = *reinterpret_cast<const uint2 *>(o4);
-      }
+    for (int nt = 0; nt < NT; ++nt) {
+      const bf16_t o4[4] = {f32_to_bf16(ot[nt][0]), f32_to_bf16(ot[nt][1]), f32_to_bf16(ot[nt][2]),
+                            f32_to_bf16(ot[nt][3])};
+      *reinterpret_cast<uint2 *>(&os[l16 * SP + nt * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(o4);
     }
+    wave_lds_sync();
+    const int nrows = min(TW, n_ent - c * TW) * G;  // valid rows of this chunk
+#pragma unroll
+    for (int k = 0; k < 16 * D / 8 / 64; ++k) {
+      const int v = lane + 64 * k, r = v / (D / 8), cc = (v % (D / 8)) * 8;
+      if (r < nrows)
+        *reinterpret_cast<uint4 *>(opart + (run0 * G + r) * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
+    }
+    wave_lds_sync();
     e_cur = e_nxt;
     e_nxt = e_nn;
 #pragma unroll
@@ -158,6 +171,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
 // all partial loads are in flight together.  Other patterns take a bit-walk.
 template <int D, int G>
 __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__restrict__ sel,
+                                                               const int32_t *__restrict__ pmap,
                                                                const bf16_t *__restrict__ opart,
                                                                const float2 *__restrict__ ml, bf16_t *__restrict__ O,
                                                                float *__restrict__ LSE, Geom gm) {
@@ -190,18 +204,24 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
     };
     if (prefix) {
       for (int k0 = 0; k0 < nv; k0 += U) {
+        int pk[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) pk[k] = k0 + k < nv ? pmap[base + k0 + k] : 0;
 #pragma unroll
         for (int k = 0; k < U; ++k)
-          if (k0 + k < nv) M = fmaxf(M, ml[(base + k0 + k) * G + hh].x);
+          if (k0 + k < nv) M = fmaxf(M, ml[(int64_t)pk[k] * G + hh].x);
       }
       for (int k0 = 0; k0 < nv; k0 += U) {
+        int pk[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) pk[k] = k0 + k < nv ? pmap[base + k0 + k] : 0;
         float2 q[U];
         uint4 raw[U];
 #pragma unroll
         for (int k = 0; k < U; ++k) {
           const bool ok = k0 + k < nv;
-          q[k] = ok ? ml[(base + k0 + k) * G + hh] : make_float2(-INFINITY, 0.f);
-          raw[k] = ok ? ld_stream16(opart + ((base + k0 + k) * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
+          q[k] = ok ? ml[(int64_t)pk[k] * G + hh] : make_float2(-INFINITY, 0.f);
+          raw[k] = ok ? ld_stream16(opart + ((int64_t)pk[k] * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
@@ -211,9 +231,10 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
         }
       }
     } else {
-      for (uint64_t v = valid; v; v &= v - 1) M = fmaxf(M, ml[(base + __ffsll((long long)v) - 1) * G + hh].x);
+      for (uint64_t v = valid; v; v &= v - 1)
+        M = fmaxf(M, ml[(int64_t)pmap[base + __ffsll((long long)v) - 1] * G + hh].x);
       for (uint64_t v = valid; v; v &= v - 1) {
-        const int64_t sl = base + __ffsll((long long)v) - 1;
+        const int64_t sl = pmap[base + __ffsll((long long)v) - 1];
         const float2 q = ml[sl * G + hh];
         const float w = exp2f(q.x - M);
         L = fmaf(w, q.y, L);
@@ -241,7 +262,7 @@ static hipError_t launch_fwd_t(const Geom &g, const void *Q, const void *K, cons
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_attn_fwd_combine", s);
   hipLaunchKernelGGL((attn_fwd_combine_kernel<D, G>), dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s, sel,
-                     static_cast<const bf16_t *>(opart), ml, static_cast<bf16_t *>(O), LSE, g);
+                     ix.pmap, static_cast<const bf16_t *>(opart), ml, static_cast<bf16_t *>(O), LSE, g);
   timing_end(s);
   return hipGetLastError();
 }

@@ -99,6 +99,15 @@ __device__ __forceinline__ bf16x8 lds_col8(const bf16_t *X, int pitch, int r0, i
   return __builtin_bit_cast(bf16x8, c);
 }
 
+// Orders a wave's LDS writes before its following LDS reads of other lanes'
+// data.  A wave's LDS instructions execute in order, so this only has to stop
+// the compiler from moving the accesses across it.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Packs two 4-element float groups into a bf16 MFMA operand (elements 0..3, then 4..7).
 __device__ __forceinline__ bf16x8 pack_bf16x8(const f32x4 &a, const f32x4 &b) {
   const v8i16 c = {(short)f32_to_bf16(a[0]), (short)f32_to_bf16(a[1]), (short)f32_to_bf16(a[2]),

@@ -5,7 +5,9 @@
 // tile is loaded once and meets every query row that selected it.
 //
 // Entries are (row << 6) | slot, where slot is the position of t in the row's
-// sel vector, so results can be written per (row, slot) without searching.
+// sel vector.  The attention kernels store per-entry partial results in list
+// order (contiguous per work unit); pmap[(row, slot)] = list position lets the
+// per-row merges find them.
 //
 // Four integer-only passes, all deterministic (no order depends on timing):
 //   count : per 256-row tile, an LDS bitmap [T][256 bits] of who selected
@@ -126,6 +128,7 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
     for (int k = 0; k < word; ++k) rank += __popc(bm[t * 8 + k]);
     const int64_t pos = (int64_t)ix.off[bg * gm.T + t] + tile_off[t] + rank;
     ix.tok[pos] = (i << 6) | s;
+    ix.pmap[((int64_t)bg * gm.Lq + i) * gm.ksel + s] = (int32_t)pos;
   }
 }
 

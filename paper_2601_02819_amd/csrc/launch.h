@@ -30,6 +30,8 @@ struct IndexWs {
   int32_t *uoff;      // [B*Hkv*T + 1]  first work unit per (b, g, t)
   int32_t *totals;    // [4]            nnz, n_units
   int32_t *tok;       // [nnz_max]      (query row << 6) | slot, ascending row per list
+  int32_t *pmap;      // [B*Hkv*Lq*Ksel] list position of each valid (row, slot); partials are
+                      //                 stored in list order and the merges gather through this map
   int2 *units;        // [units_max]    (b*Hkv*T + g*T + t, first list entry)
 };
 
