@@ -118,12 +118,13 @@ def bench_train(steps: int, warmup: int, seed: int):
     B, L, Hq, Hkv, d, m, T = wl.batch, wl.seqlen_q, wl.n_heads_q, wl.n_heads_kv, wl.head_dim, wl.block_size, wl.n_blocks
     G = Hq // Hkv
     p = phsa.make_params(cfg, B, L, L, Hq, Hkv, d, torch.bfloat16)
-    ws_f = torch.empty(phsa.workspace_size(p, phsa.OP_FORWARD), dtype=torch.uint8, device="cuda")
-    ws_b = torch.empty(phsa.workspace_size(p, phsa.OP_ATTN_BWD), dtype=torch.uint8, device="cuda")
+    # one workspace for both passes: the backward reuses the forward's inverted index
+    ws = torch.empty(max(phsa.workspace_size(p, phsa.OP_FORWARD), phsa.workspace_size(p, phsa.OP_ATTN_BWD)),
+                     dtype=torch.uint8, device="cuda")
 
     def step():
-        kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg, ws=ws_f)
-        dq, dk, dv = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg, ws=ws_b)
+        kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg, ws=ws)
+        dq, dk, dv = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg, ws=ws, reuse_index=True)
         return sel
 
     for _ in range(warmup):

@@ -89,7 +89,19 @@ typedef struct {
   float lambda;          /* gate of Eq. 8, in [0, 1] */
   float softmax_scale;   /* <= 0 selects 1 / sqrt(head_dim) (Eq. 2, 8, 11) */
   int32_t dtype;         /* phsa_dtype of Q, K, V, O, dO, dQ, dK, dV */
+  int32_t flags;         /* bitwise OR of phsa_flag values, 0 for none */
 } phsa_params;
+
+/* phsa_params.flags */
+typedef enum {
+  /* phsa_attn_bwd only: `ws` is the workspace a preceding phsa_attn_fwd or
+   * phsa_forward call used with the same params and the same sel, and it has
+   * not been modified since.  The inverted selection index that call built
+   * (the first part of the workspace) is reused instead of rebuilt; the rest of
+   * the workspace is overwritten.  ws_bytes must still cover
+   * phsa_workspace_size(p, PHSA_OP_ATTN_BWD). */
+  PHSA_FLAG_REUSE_INDEX = 1
+} phsa_flag;
 
 /* Number of index slots per (query row, KV head): n_init + w/m + 1 + top_k. */
 int32_t phsa_ksel(const phsa_params *p);

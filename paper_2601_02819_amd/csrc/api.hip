@@ -108,6 +108,7 @@ phsa_status validate(const phsa_params *p, int op, Geom *out) {
   if (op == PHSA_OP_DECODE && p->seqlen_q != 1) return PHSA_ERR_SHAPE;
   if (p->top_k < 0 || p->n_init_blocks < 0 || p->window < 0 || p->window % p->block_size != 0)
     return PHSA_ERR_INVALID_ARG;
+  if ((p->flags & ~PHSA_FLAG_REUSE_INDEX) != 0) return PHSA_ERR_INVALID_ARG;
   if (!(p->lambda >= 0.f && p->lambda <= 1.f)) return PHSA_ERR_INVALID_ARG;
   if (!isfinite(p->softmax_scale)) return PHSA_ERR_INVALID_ARG;
   // What the kernels implement.
@@ -299,7 +300,9 @@ phsa_status phsa_attn_bwd(const phsa_params *p, const void *Q, const void *K, co
                                            static_cast<const float *>(V), static_cast<const float *>(O),
                                            static_cast<const float *>(dO), LSE, sel, static_cast<float *>(dQ),
                                            static_cast<float *>(dK), static_cast<float *>(dV), w.Dvec, s));
-    return from_hip(launch_attn_bwd(g, Q, K, V, O, dO, LSE, sel, dQ, dK, dV, w.ix, w.Dvec, w.dqpart, w.dkvpart, s));
+    const bool reuse = (p->flags & PHSA_FLAG_REUSE_INDEX) != 0;
+    return from_hip(
+        launch_attn_bwd(g, Q, K, V, O, dO, LSE, sel, dQ, dK, dV, w.ix, w.Dvec, w.dqpart, w.dkvpart, reuse, s));
   })
 }
 

@@ -112,24 +112,33 @@ __global__ __launch_bounds__(1024) void index_scan_lists_kernel(Geom gm, IndexWs
 
 __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restrict__ sel, Geom gm, IndexWs ix) {
   extern __shared__ uint32_t bm[];
+  int32_t *pm = reinterpret_cast<int32_t *>(bm + gm.T * 8);  // [kIndexTile][ksel] staged position map
   const int w = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x;
   build_tile_bitmap(bm, sel, gm, bg, w);
   const int i = w * kIndexTile + tid;
-  if (i >= gm.Lq) return;
-  const int cur = (gm.q_pos0 + i) / gm.m;
-  const int32_t *row = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
-  const int32_t *tile_off = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
-  const int word = tid >> 5;
-  const uint32_t below = (1u << (tid & 31)) - 1u;
-  for (int s = 0; s < gm.ksel; ++s) {
-    const int t = row[s];
-    if (!slot_valid(t, cur, gm.T)) continue;
-    int rank = __popc(bm[t * 8 + word] & below);
-    for (int k = 0; k < word; ++k) rank += __popc(bm[t * 8 + k]);
-    const int64_t pos = (int64_t)ix.off[bg * gm.T + t] + tile_off[t] + rank;
-    ix.tok[pos] = (i << 6) | s;
-    ix.pmap[((int64_t)bg * gm.Lq + i) * gm.ksel + s] = (int32_t)pos;
+  if (i < gm.Lq) {
+    const int cur = (gm.q_pos0 + i) / gm.m;
+    const int32_t *row = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
+    const int32_t *tile_off = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
+    const int word = tid >> 5;
+    const uint32_t below = (1u << (tid & 31)) - 1u;
+    for (int s = 0; s < gm.ksel; ++s) {
+      const int t = row[s];
+      int32_t pos = -1;
+      if (slot_valid(t, cur, gm.T)) {
+        int rank = __popc(bm[t * 8 + word] & below);
+        for (int k = 0; k < word; ++k) rank += __popc(bm[t * 8 + k]);
+        pos = ix.off[bg * gm.T + t] + tile_off[t] + rank;
+        ix.tok[pos] = (i << 6) | s;
+      }
+      pm[tid * gm.ksel + s] = pos;
+    }
   }
+  __syncthreads();
+  // the tile's rows are consecutive, so their position-map rows form one contiguous run
+  const int nrow = min(kIndexTile, gm.Lq - w * kIndexTile);
+  int32_t *dst = ix.pmap + ((int64_t)bg * gm.Lq + (int64_t)w * kIndexTile) * gm.ksel;
+  for (int x = tid; x < nrow * gm.ksel; x += 256) dst[x] = pm[x];
 }
 
 hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &ix, hipStream_t s) {
@@ -145,7 +154,8 @@ hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &
   hipLaunchKernelGGL(index_scan_lists_kernel, dim3(1), dim3(1024), 0, s, g, ix, nbgt);
   timing_end(s);
   timing_begin("phsa_index_fill", s);
-  hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds, s, sel, g, ix);
+  hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds + (size_t)kIndexTile * g.ksel * 4,
+                     s, sel, g, ix);
   timing_end(s);
   return hipGetLastError();
 }

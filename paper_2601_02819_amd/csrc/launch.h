@@ -48,7 +48,8 @@ hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const vo
                            void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s);
 hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
                            const void *dO, const float *LSE, const int32_t *sel, void *dQ, void *dK, void *dV,
-                           const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart, hipStream_t s);
+                           const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart, bool reuse_index,
+                           hipStream_t s);
 hipError_t launch_bwd_pre(const Geom &g, const void *O, const void *dO, float *Dvec, hipStream_t s);
 hipError_t launch_attn_fwd_fp32(const Geom &g, const float *Q, const float *K, const float *V,
                                 const int32_t *sel, float *O, float *LSE, hipStream_t s);

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libphsa.so")
 OK, ERR_INVALID_ARG, ERR_SHAPE, ERR_DTYPE, ERR_NULL, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP = range(8)
 BF16, FP32 = 0, 1
 OP_COMPRESS, OP_SELECT, OP_ATTN_FWD, OP_ATTN_BWD, OP_FORWARD, OP_DECODE = range(6)
+FLAG_REUSE_INDEX = 1
 
 EXPORTS = (
     "phsa_ksel", "phsa_validate", "phsa_workspace_size", "phsa_status_string", "phsa_compress",
@@ -33,7 +34,7 @@ class Params(ctypes.Structure):
         ("n_heads_q", ctypes.c_int32), ("n_heads_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
         ("block_size", ctypes.c_int32), ("top_k", ctypes.c_int32), ("n_init_blocks", ctypes.c_int32),
         ("window", ctypes.c_int32), ("lam", ctypes.c_float), ("softmax_scale", ctypes.c_float),
-        ("dtype", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("flags", ctypes.c_int32),
     ]
 
 
@@ -98,10 +99,10 @@ class Config:
 
 
 def make_params(cfg: Config, batch: int, seqlen_q: int, seqlen_k: int, n_heads_q: int, n_heads_kv: int,
-                head_dim: int, dtype) -> Params:
+                head_dim: int, dtype, flags: int = 0) -> Params:
     code = BF16 if dtype in (torch.bfloat16, BF16) else FP32 if dtype in (torch.float32, FP32) else 99
     return Params(batch, seqlen_q, seqlen_k, n_heads_q, n_heads_kv, head_dim, cfg.block_size, cfg.top_k,
-                  cfg.n_init_blocks, cfg.window, cfg.lam, cfg.softmax_scale, code)
+                  cfg.n_init_blocks, cfg.window, cfg.lam, cfg.softmax_scale, code, flags)
 
 
 def workspace_size(p: Params, op: int) -> int:
@@ -171,12 +172,17 @@ def attn_fwd(q, k, v, sel, cfg: Config, ws: Optional[torch.Tensor] = None) -> Tu
     return o, lse
 
 
-def attn_bwd(q, k, v, o, do, lse, sel, cfg: Config, ws: Optional[torch.Tensor] = None):
-    """Sparse attention backward (selection fixed) -> (dQ, dK, dV)."""
+def attn_bwd(q, k, v, o, do, lse, sel, cfg: Config, ws: Optional[torch.Tensor] = None, reuse_index: bool = False):
+    """Sparse attention backward (selection fixed) -> (dQ, dK, dV).
+
+    reuse_index=True: `ws` is the workspace of the forward call that produced
+    o/lse from the same sel, and its inverted index is reused."""
     _dev(q, k, v, o, do, lse, sel)
     B, Lq, Hq, d = q.shape
     Lk, Hkv = k.shape[1], k.shape[2]
-    p = make_params(cfg, B, Lq, Lk, Hq, Hkv, d, q.dtype)
+    p = make_params(cfg, B, Lq, Lk, Hq, Hkv, d, q.dtype, FLAG_REUSE_INDEX if reuse_index else 0)
+    if reuse_index and (ws is None or ws.numel() < workspace_size(p, OP_ATTN_BWD)):
+        raise ValueError("reuse_index needs the forward's workspace, sized for the backward")
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     w = _workspace(p, OP_ATTN_BWD, ws, q.device)
     _check(lib().phsa_attn_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(sel),
@@ -217,19 +223,27 @@ def decode(q, k_cache, v_cache, kc, cfg: Config, ws: Optional[torch.Tensor] = No
 
 
 class SparseAttention(torch.autograd.Function):
-    """Autograd wrapper: forward = phsa_attn_fwd, backward = phsa_attn_bwd (selection fixed)."""
+    """Autograd wrapper: forward = phsa_attn_fwd, backward = phsa_attn_bwd (selection fixed).
+
+    The forward's workspace, sized for both passes, is kept for the backward,
+    which then reuses the inverted selection index instead of rebuilding it."""
 
     @staticmethod
     def forward(ctx, q, k, v, sel, cfg: Config):
-        o, lse = attn_fwd(q, k, v, sel, cfg)
+        B, Lq, Hq, d = q.shape
+        p = make_params(cfg, B, Lq, k.shape[1], Hq, k.shape[2], d, q.dtype)
+        need = max(workspace_size(p, OP_ATTN_FWD), workspace_size(p, OP_ATTN_BWD))
+        ws = torch.empty(need, dtype=torch.uint8, device=q.device) if need else None
+        o, lse = attn_fwd(q, k, v, sel, cfg, ws)
         ctx.save_for_backward(q, k, v, o, lse, sel)
-        ctx.cfg = cfg
+        ctx.cfg, ctx.ws = cfg, ws
         return o
 
     @staticmethod
     def backward(ctx, do):
         q, k, v, o, lse, sel = ctx.saved_tensors
-        dq, dk, dv = attn_bwd(q, k, v, o, do.contiguous(), lse, sel, ctx.cfg)
+        dq, dk, dv = attn_bwd(q, k, v, o, do.contiguous(), lse, sel, ctx.cfg, ctx.ws, reuse_index=ctx.ws is not None)
+        ctx.ws = None
         return dq, dk, dv, None, None
 
 

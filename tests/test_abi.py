@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 def _p(**kw):
     base = dict(batch=1, seqlen_q=1024, seqlen_k=1024, n_heads_q=2, n_heads_kv=1, head_dim=64, block_size=64,
-                top_k=2, n_init_blocks=1, window=0, lam=0.5, softmax_scale=0.0, dtype=phsa.BF16)
+                top_k=2, n_init_blocks=1, window=0, lam=0.5, softmax_scale=0.0, dtype=phsa.BF16, flags=0)
     base.update(kw)
     return phsa.Params(*[base[f] for f, _ in phsa.Params._fields_])
 
@@ -56,6 +56,8 @@ def _p(**kw):
     ({"seqlen_q": 2}, phsa.OP_DECODE, phsa.ERR_SHAPE),
     ({"seqlen_q": 1}, phsa.OP_DECODE, phsa.OK),
     ({}, 17, phsa.ERR_INVALID_ARG),
+    ({"flags": phsa.FLAG_REUSE_INDEX}, phsa.OP_ATTN_BWD, phsa.OK),
+    ({"flags": 2}, phsa.OP_ATTN_BWD, phsa.ERR_INVALID_ARG),                 # unknown flag bit
 ])
 def test_validate(kw, op, code):
     assert phsa.lib().phsa_validate(ctypes.byref(_p(**kw)), op) == code

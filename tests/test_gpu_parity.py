@@ -175,3 +175,19 @@ def test_autograd_wrapper():
     o, lse = phsa.attn_fwd(dev["q"], dev["k"], dev["v"], sel, cfg)
     dq, dk, dv = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg)
     assert torch.equal(out, o) and torch.equal(q.grad, dq) and torch.equal(k.grad, dk) and torch.equal(v.grad, dv)
+
+
+def test_backward_reuses_forward_index():
+    """PHSA_FLAG_REUSE_INDEX: the backward on the forward's workspace equals a backward that rebuilds the index."""
+    wl = small("reuse", 2, 2048, 8, 2, 128, 6, 1, 64)
+    cfg = cfg_of(wl)
+    _, dev = device_inputs(wl, 10, with_grad_out=True)
+    B, Lq, Hq, d = dev["q"].shape
+    p = phsa.make_params(cfg, B, Lq, 2048, Hq, wl.n_heads_kv, d, dev["q"].dtype)
+    need = max(phsa.workspace_size(p, phsa.OP_FORWARD), phsa.workspace_size(p, phsa.OP_ATTN_BWD))
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg, ws)
+    got = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg, ws, reuse_index=True)
+    ref = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg)
+    for a, b in zip(got, ref):
+        assert torch.equal(a, b)
