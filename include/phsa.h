@@ -123,8 +123,9 @@ phsa_status phsa_compress(const phsa_params *p, const void *K, const uint8_t *pu
 
 /* Relevance scoring and block selection (Eq. 8, Algorithm 1 scoring and
  * selection).  Reads Q and K_comp; writes sel [B, Hkv, Lq, Ksel].  Scores
- * are computed in float32 from float32 K_comp.  No workspace is needed
- * (ws may be NULL when phsa_workspace_size(p, PHSA_OP_SELECT) is 0). */
+ * are computed in float32 from float32 K_comp.  The bf16 path needs
+ * phsa_workspace_size(p, PHSA_OP_SELECT) bytes of workspace (split copies of
+ * K_comp); the float32 path needs none (ws may then be NULL). */
 phsa_status phsa_select(const phsa_params *p, const void *Q, const float *K_comp, int32_t *sel,
                         void *ws, size_t ws_bytes, void *stream);
 

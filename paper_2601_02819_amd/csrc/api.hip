@@ -3,6 +3,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <exception>
 #include <vector>
 
@@ -118,7 +119,8 @@ phsa_status validate(const phsa_params *p, int op, Geom *out) {
   const int G = p->n_heads_q / p->n_heads_kv;
   if (ksel > 64 || p->top_k > 32) return PHSA_ERR_UNSUPPORTED;
   if (T > 2048 || p->seqlen_q >= (1 << 25)) return PHSA_ERR_UNSUPPORTED;
-  if (p->batch > 65535 || p->n_heads_q > 65535) return PHSA_ERR_UNSUPPORTED;
+  if (p->batch > 65535 || p->n_heads_q > 65535 || (int64_t)p->batch * p->n_heads_kv > 65535)
+    return PHSA_ERR_UNSUPPORTED;  // grid y/z extents
   if (is_attention_op(op)) {
     if (p->block_size != 64) return PHSA_ERR_UNSUPPORTED;
     if (G != 1 && G != 2 && G != 4 && G != 8) return PHSA_ERR_UNSUPPORTED;
@@ -151,8 +153,10 @@ phsa_status validate(const phsa_params *p, int op, Geom *out) {
 
 size_t workspace_bytes(const Geom &g, int op) {
   switch (op) {
-    case PHSA_OP_ATTN_FWD:
-    case PHSA_OP_FORWARD: return fwd_layout(g, nullptr, nullptr);
+    case PHSA_OP_SELECT: return align_up(select_split_bytes(g));
+    case PHSA_OP_ATTN_FWD: return fwd_layout(g, nullptr, nullptr);
+    // the selection scratch is dead before the attention step reuses the same bytes
+    case PHSA_OP_FORWARD: return std::max(fwd_layout(g, nullptr, nullptr), align_up(select_split_bytes(g)));
     case PHSA_OP_ATTN_BWD: return bwd_layout(g, nullptr, nullptr);
     case PHSA_OP_DECODE: return decode_layout(g);
     default: return 0;
@@ -261,7 +265,7 @@ phsa_status phsa_select(const phsa_params *p, const void *Q, const float *K_comp
     if (st != PHSA_OK) return st;
     if (!Q || !K_comp || !sel) return PHSA_ERR_NULL;
     if ((st = check_ws(g, PHSA_OP_SELECT, ws, ws_bytes)) != PHSA_OK) return st;
-    return from_hip(launch_select(g, Q, K_comp, sel, static_cast<hipStream_t>(stream)));
+    return from_hip(launch_select(g, Q, K_comp, sel, ws, static_cast<hipStream_t>(stream)));
   })
 }
 
@@ -316,7 +320,7 @@ phsa_status phsa_forward(const phsa_params *p, const void *Q, const void *K, con
     if ((st = check_ws(g, PHSA_OP_FORWARD, ws, ws_bytes)) != PHSA_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = launch_compress(g, K, punct, K_comp, s);
-    if (e == hipSuccess) e = launch_select(g, Q, K_comp, sel, s);
+    if (e == hipSuccess) e = launch_select(g, Q, K_comp, sel, ws, s);
     if (e != hipSuccess) return PHSA_ERR_HIP;
     if (g.dtype == PHSA_FP32)
       return from_hip(launch_attn_fwd_fp32(g, static_cast<const float *>(Q), static_cast<const float *>(K),

@@ -42,7 +42,9 @@ void timing_begin(const char *name, hipStream_t s);
 void timing_end(hipStream_t s);
 
 hipError_t launch_compress(const Geom &g, const void *K, const uint8_t *punct, float *Kc, hipStream_t s);
-hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t *sel, hipStream_t s);
+// ws: select_split_bytes(g) bytes (bf16 hi/lo copies of K_comp), unused for float32
+size_t select_split_bytes(const Geom &g);
+hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t *sel, void *ws, hipStream_t s);
 hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &ix, hipStream_t s);
 hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel,
                            void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s);

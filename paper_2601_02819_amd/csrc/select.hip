@@ -164,270 +164,391 @@ __global__ __launch_bounds__(256) void select_kernel(const T *__restrict__ Q, co
   for (; n < gm.ksel; ++n) out[n] = -1;
 }
 
-// bf16 inputs: scoring on the matrix cores.
+// bf16 inputs: scoring on the matrix cores, selection by a bar and a short exact rank.
 //
-// The group's query heads are summed in float32 (sum_h q_h . M = (sum_h q_h) . M),
-// and both that sum and the float32 representative M are split into bf16
-// hi + lo parts.  Three bf16 MFMA chains (hi.hi + hi.lo + lo.hi, float32
+// Scores.  The group's query heads are summed in float32
+// (sum_h q_h . M = (sum_h q_h) . M), and both that sum and the float32
+// representative M are split into bf16 hi + lo parts (M once per call, by
+// select_split_kernel).  Three bf16 MFMA chains (hi.hi + hi.lo + lo.hi, float32
 // accumulate) reproduce the float32 dot product to about 2^-17 relative, far
-// inside the 1e-4 score gap the selection is compared at.  Wave w owns the
-// 16 query rows 16w..16w+15 of the 64-row tile; representatives stream
-// through LDS in chunks of 64 blocks, pre-split into hi/lo tiles.
+// inside the 1e-4 score gap the selection is compared at; these are the
+// scores the selection is made on.  Wave w owns two 16-row tiles (rows
+// 32w..32w+31 of a 128-row workgroup tile), so every representative fragment
+// read from LDS feeds several MFMAs; representatives stream through LDS in
+// chunks of 64 blocks.  In the accumulator layout lane (q4, l16) holds, per
+// tile, the scores of rows 4 q4 + r (r = 0..3) for blocks t0 + 16 nt + l16, so
+// the 16 lanes of a quarter-wave together see every block of their rows, each
+// lane a fixed residue of (t - n_init) mod 16 (its "stripe").
 //
-// Top-k: four threads per row (one in each wave) keep private sorted lists
-// of (score, block) in registers.  Each private list's k-th entry is a lower
-// bound on the row's final k-th score, so the strongest of the four is the
-// bar a new score must beat.  Scores that pass are appended to the row's LDS
-// buffer, and the row's four threads insert every fourth of them into their
-// lists (compare/select only, no memory traffic).  After the last chunk the
-// four lists are merged.
-template <int D, int G, int KMAX>
-__global__ __launch_bounds__(256) void select_mfma_kernel(const bf16_t *__restrict__ Q, const float *__restrict__ Kc,
-                                                          int32_t *__restrict__ sel, Geom gm) {
-  constexpr int CH = 64;
+// Top-k in two passes:
+//   pass 1: a single hi.hi chain gives approximate scores.  The dropped terms
+//           hi.lo + lo.hi are bounded by 2^-7 (1 + 2^-8)^2 sum |q_c M_c| <=
+//           2^-7 (1 + 2^-8)^2 |q| |M| (each bf16 part is within 2^-8 of its
+//           value; Cauchy-Schwarz), and float32 accumulation of the 3 d terms
+//           adds below 2^-15 of that sum, so s_exact >= s_approx - eps with
+//           eps = 1.024 * 2^-7 |q| |M| scale.  Every lane keeps the best two of these
+//           lower bounds in its stripe for each of its rows.  A row's 32 stripe
+//           tops belong to 32 distinct blocks, so the largest value v with at
+//           least k of them >= v (the bar) lies below the row's k-th best
+//           exact score.
+//   pass 2: the exact scores are computed and those >= bar are appended, in
+//           block order, to the row's LDS list (quarter-wave ballots give the
+//           slots; no atomics).  For random scores about k + 3 pass.  Should a
+//           list near its capacity (40 for k <= 16, else 48), it is cut to its
+//           k best, whose k-th score becomes the bar.
+//   final : the k best of the list (score descending, then block ascending)
+//           are found by counting ranks and written in block order between the
+//           forced init and local blocks.
+
+// float32 K_comp -> bf16 hi, lo (hi + lo = K_comp to about 2^-17 relative) and
+// the Euclidean norm of every representative.  D / 8 consecutive threads hold
+// one representative.
+template <int D>
+__global__ __launch_bounds__(256) void select_split_kernel(const float *__restrict__ Kc, bf16_t *__restrict__ Mh,
+                                                           bf16_t *__restrict__ Ml, float *__restrict__ Mnorm,
+                                                           int64_t n8) {
+  constexpr int TPR = D / 8;
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  float v[8];
+  if (x < n8) {
+    const float4 a = reinterpret_cast<const float4 *>(Kc)[2 * x];
+    const float4 c = reinterpret_cast<const float4 *>(Kc)[2 * x + 1];
+    v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w, v[4] = c.x, v[5] = c.y, v[6] = c.z, v[7] = c.w;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = 0.f;
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ss = fmaf(v[e], v[e], ss);
+#pragma unroll
+  for (int o = 1; o < TPR; o <<= 1) ss += __shfl_xor(ss, o, 64);
+  if (x >= n8) return;
+  bf16_t hi[8], lo[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    hi[e] = f32_to_bf16(v[e]);
+    lo[e] = f32_to_bf16(v[e] - bf16_to_f32(hi[e]));
+  }
+  reinterpret_cast<uint4 *>(Mh)[x] = *reinterpret_cast<const uint4 *>(hi);
+  reinterpret_cast<uint4 *>(Ml)[x] = *reinterpret_cast<const uint4 *>(lo);
+  if (x % TPR == 0) Mnorm[x / TPR] = sqrtf(ss);
+}
+
+template <int D, int G, int CAP>
+__global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
+    const bf16_t *__restrict__ Q, const bf16_t *__restrict__ Mh_g, const bf16_t *__restrict__ Ml_g,
+    const float *__restrict__ Mnorm_g, int32_t *__restrict__ sel, Geom gm) {
+  constexpr int CH = 64;                  // blocks per chunk
+  constexpr int RT = 2;                   // 16-row tiles per wave (B fragments are reused across them)
+  constexpr int ROWS = 4 * 16 * RT;       // query rows per workgroup
+  constexpr int NR = 4 * RT;              // rows per lane in the accumulator layout
   constexpr int MP = D + 8;
   constexpr int KB = D / 32;
-  constexpr int TILE_BYTES = 2 * CH * MP * 2;
-  constexpr int LIST_BYTES = 4 * 64 * KMAX * 8;
-  constexpr int BUF = TILE_BYTES > LIST_BYTES ? TILE_BYTES : LIST_BYTES;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[BUF];
-  // candidate buffers, one row per query row; rows padded by one word so that the
-  // merge threads (lane = row) do not all hit the same LDS bank
-  __shared__ float nb_s[64][CH + 1];
-  __shared__ int nb_t[64][CH + 1];
-  __shared__ int nnew[64];
-  __shared__ float bar_s[4][64];
-  __shared__ int bar_t[4][64];
-  bf16_t *Mh = reinterpret_cast<bf16_t *>(smem);
-  bf16_t *Ml = Mh + CH * MP;
+  constexpr int NL = CH * D / (256 * 8);  // 16-byte loads per thread per tile
+  constexpr int PITCH = CAP + 2;          // 8-byte words; keeps a wave's 4 row groups in distinct banks
+  constexpr int NJ = (CAP + 15) / 16;
+  __shared__ __attribute__((aligned(16))) bf16_t Mh[CH * MP];
+  __shared__ __attribute__((aligned(16))) bf16_t Ml[CH * MP];
+  __shared__ __attribute__((aligned(16))) float2 cand[ROWS][PITCH];  // (score, block as int bits)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
   const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg % gm.Hkv;
-  const int i0 = blockIdx.x * 64;
+  const int i0 = blockIdx.x * ROWS;
+  const int k = gm.top_k;
+  const uint64_t grp_bits = 0xffffull << (16 * q4);
+  const uint64_t below = (1ull << lane) - 1ull;
+  // tile row of accumulator entry (j, r) held by this lane: 32 w + 16 j + 4 q4 + r
+  auto crow = [&](int rr) { return wave * 16 * RT + (rr >> 2) * 16 + q4 * 4 + (rr & 3); };
 
-  // A operand: split query-head sums of row 16w + l16 (all loads issued together)
-  bf16x8 ah[KB], al[KB];
-  {
-    const int ia = i0 + wave * 16 + l16;
-    uint4 raw[G][KB];
+  // A operands: split query-head sums of rows 32w + 16j + l16 (all loads issued
+  // together); the lo parts only for pass 2, the row norms only for pass 1
+  bf16x8 ah[RT][KB], al[RT][KB];
+  float qn[RT];
+  auto load_a = [&](bool pass2) {
 #pragma unroll
-    for (int hh = 0; hh < G; ++hh)
+    for (int j = 0; j < RT; ++j) {
+      const int ia = i0 + wave * 16 * RT + j * 16 + l16;
+      uint4 raw[G][KB];
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-        raw[hh][kb] = ia < gm.Lq ? *reinterpret_cast<const uint4 *>(
-                                       Q + (((int64_t)b * gm.Lq + ia) * gm.Hq + g * G + hh) * D + kb * 32 + kq)
-                                 : make_uint4(0u, 0u, 0u, 0u);
+      for (int hh = 0; hh < G; ++hh)
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      float qs[8];
+        for (int kb = 0; kb < KB; ++kb)
+          raw[hh][kb] = ia < gm.Lq ? *reinterpret_cast<const uint4 *>(
+                                         Q + (((int64_t)b * gm.Lq + ia) * gm.Hq + g * G + hh) * D + kb * 32 + kq)
+                                   : make_uint4(0u, 0u, 0u, 0u);
+      float ss = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qs[e] = 0.f;
+      for (int kb = 0; kb < KB; ++kb) {
+        float qs[8];
 #pragma unroll
-      for (int hh = 0; hh < G; ++hh) {
-        const bf16_t *v = reinterpret_cast<const bf16_t *>(&raw[hh][kb]);
+        for (int e = 0; e < 8; ++e) qs[e] = 0.f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) qs[e] += bf16_to_f32(v[e]);
+        for (int hh = 0; hh < G; ++hh) {
+          const bf16_t *v = reinterpret_cast<const bf16_t *>(&raw[hh][kb]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) qs[e] += bf16_to_f32(v[e]);
+        }
+        bf16_t hi[8], lo[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          ss = fmaf(qs[e], qs[e], ss);
+          hi[e] = f32_to_bf16(qs[e]);
+          lo[e] = f32_to_bf16(qs[e] - bf16_to_f32(hi[e]));
+        }
+        ah[j][kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(hi));
+        if (pass2) al[j][kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(lo));
       }
-      bf16_t hi[8], lo[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        hi[e] = f32_to_bf16(qs[e]);
-        lo[e] = f32_to_bf16(qs[e] - bf16_to_f32(hi[e]));
+      if (!pass2) {
+        ss += __shfl_xor(ss, 16, 64);
+        ss += __shfl_xor(ss, 32, 64);
+        qn[j] = sqrtf(ss);
       }
-      ah[kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(hi));
-      al[kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(lo));
-    }
-  }
-  // private list of thread (row = lane, part = wave)
-  float ls[KMAX];
-  int lt[KMAX];
-#pragma unroll
-  for (int k = 0; k < KMAX; ++k) {
-    ls[k] = -FLT_MAX;
-    lt[k] = 0x7fffffff;
-  }
-  int nl = 0;
-  nnew[lane] = 0;  // (every wave writes the same zero)
-  bar_s[wave][lane] = -FLT_MAX;
-  bar_t[wave][lane] = 0x7fffffff;
-  // first local block of the 4 rows this lane holds in the C layout (no candidates past it)
-  int lo_r[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int i = i0 + wave * 16 + q4 * 4 + r;
-    lo_r[r] = i < gm.Lq ? max(0, (gm.q_pos0 + i) / gm.m - gm.window / gm.m) : 0;
-  }
-  const int last_i = min(i0 + 63, gm.Lq - 1);
-  const int t_end = gm.top_k > 0 ? max(0, (gm.q_pos0 + last_i) / gm.m - gm.window / gm.m) : 0;
-  const float *kc_bg = Kc + (int64_t)bg * gm.T * D;
-
-  // representative chunks: the next chunk's float32 rows are fetched into
-  // registers while the current chunk is scored
-  constexpr int NM = CH * D / (256 * 4);
-  float4 mreg[NM];
-  auto fetch_chunk = [&](int t0) {
-    const int nblk = min(CH, gm.T - t0);
-#pragma unroll
-    for (int k = 0; k < NM; ++k) {
-      const int e = (tid + 256 * k) * 4, row = e / D, c = e % D;
-      mreg[k] = row < nblk ? *reinterpret_cast<const float4 *>(kc_bg + (int64_t)(t0 + row) * D + c)
-                           : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
-  if (gm.n_init < t_end) fetch_chunk(gm.n_init);
+  load_a(false);
+  // per row held in the accumulator layout: first local block (candidates lie
+  // below it) and the pass-1 margin factor 2^-6 |q| scale
+  int lo_r[NR];
+  float eq[NR];
+#pragma unroll
+  for (int rr = 0; rr < NR; ++rr) {
+    const int i = i0 + crow(rr);
+    lo_r[rr] = i < gm.Lq ? max(0, (gm.q_pos0 + i) / gm.m - gm.window / gm.m) : 0;
+    eq[rr] = __shfl(qn[rr >> 2], q4 * 4 + (rr & 3), 64) * gm.scale * 0.008f;
+  }
+  const int last_i = min(i0 + ROWS - 1, gm.Lq - 1);
+  const int t_end = k > 0 ? max(0, (gm.q_pos0 + last_i) / gm.m - gm.window / gm.m) : 0;
+  const bf16_t *mh_bg = Mh_g + (int64_t)bg * gm.T * D;
+  const bf16_t *ml_bg = Ml_g + (int64_t)bg * gm.T * D;
+  const float *mn_bg = Mnorm_g + (int64_t)bg * gm.T;
 
-  for (int t0 = gm.n_init; t0 < t_end; t0 += CH) {
-    __syncthreads();
+  uint4 ph[NL], pl[NL];
+  float mnp[4];  // pass 1: norms of the blocks t0 + 16 nt + l16 of the prefetched chunk
+  auto fetch = [&](int t0, bool pass2) {
+    const int nblk = min(CH, gm.T - t0);
 #pragma unroll
-    for (int k = 0; k < NM; ++k) {
-      const int e = (tid + 256 * k) * 4, row = e / D, c = e % D;
-      const float mv[4] = {mreg[k].x, mreg[k].y, mreg[k].z, mreg[k].w};
-      bf16_t hi[4], lo[4];
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        hi[x] = f32_to_bf16(mv[x]);
-        lo[x] = f32_to_bf16(mv[x] - bf16_to_f32(hi[x]));
-      }
-      *reinterpret_cast<uint2 *>(&Mh[row * MP + c]) = *reinterpret_cast<const uint2 *>(hi);
-      *reinterpret_cast<uint2 *>(&Ml[row * MP + c]) = *reinterpret_cast<const uint2 *>(lo);
+    for (int x = 0; x < NL; ++x) {
+      const int e = (tid + 256 * x) * 8, row = e / D, c = e % D;
+      const int64_t off = (int64_t)(t0 + row) * D + c;
+      ph[x] = row < nblk ? *reinterpret_cast<const uint4 *>(mh_bg + off) : make_uint4(0u, 0u, 0u, 0u);
+      if (pass2)
+        pl[x] = row < nblk ? *reinterpret_cast<const uint4 *>(ml_bg + off) : make_uint4(0u, 0u, 0u, 0u);
     }
-    __syncthreads();
-    if (t0 + CH < t_end) fetch_chunk(t0 + CH);
-
-    f32x4 acc[4];
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const bf16x8 bh = load_bf16x8(&Mh[(nt * 16 + l16) * MP + kb * 32 + kq]);
-        const bf16x8 bl = load_bf16x8(&Ml[(nt * 16 + l16) * MP + kb * 32 + kq]);
-        acc[nt] = mfma16x16x32(ah[kb], bh, acc[nt]);
-        acc[nt] = mfma16x16x32(ah[kb], bl, acc[nt]);
-        acc[nt] = mfma16x16x32(al[kb], bh, acc[nt]);
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = wave * 16 + q4 * 4 + r;
-      float bs = bar_s[0][row];
-      int bt = bar_t[0][row];
-#pragma unroll
-      for (int p = 1; p < 4; ++p) {
-        const float s2 = bar_s[p][row];
-        const int t2 = bar_t[p][row];
-        if (beats(s2, t2, bs, bt)) {
-          bs = s2;
-          bt = t2;
-        }
-      }
+    if (!pass2) {
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
         const int t = t0 + nt * 16 + l16;
-        const float s = acc[nt][r] * gm.scale;
-        if (t < lo_r[r] && beats(s, t, bs, bt)) {
-          const int slot = atomicAdd(&nnew[row], 1);
-          nb_s[row][slot] = s;
-          nb_t[row][slot] = t;
-        }
+        mnp[nt] = t < gm.T ? mn_bg[t] : 0.f;
       }
     }
-    __syncthreads();
-    const int nn = nnew[lane];
-    for (int e = wave; e < nn; e += 4) {
-      float s = nb_s[lane][e];
-      int ct = nb_t[lane][e];
-      if (!beats(s, ct, ls[KMAX - 1], lt[KMAX - 1])) continue;
+  };
+  auto stage = [&](bool pass2) {
 #pragma unroll
-      for (int k = 0; k < KMAX; ++k) {
-        const bool bt = beats(s, ct, ls[k], lt[k]);
-        const float os = ls[k];
-        const int ot = lt[k];
-        ls[k] = bt ? s : os;
-        lt[k] = bt ? ct : ot;
-        s = bt ? os : s;
-        ct = bt ? ot : ct;
+    for (int x = 0; x < NL; ++x) {
+      const int e = (tid + 256 * x) * 8, row = e / D, c = e % D;
+      *reinterpret_cast<uint4 *>(&Mh[row * MP + c]) = ph[x];
+      if (pass2) *reinterpret_cast<uint4 *>(&Ml[row * MP + c]) = pl[x];
+    }
+  };
+
+  // ---- pass 1: best two lower bounds of each lane's stripe, per row
+  float top1[NR], top2[NR];
+#pragma unroll
+  for (int rr = 0; rr < NR; ++rr) top1[rr] = top2[rr] = -INFINITY;
+  if (gm.n_init < t_end) fetch(gm.n_init, false);
+  for (int t0 = gm.n_init; t0 < t_end; t0 += CH) {
+    __syncthreads();
+    stage(false);
+    __syncthreads();
+    float mn[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) mn[nt] = mnp[nt];
+    if (t0 + CH < t_end) fetch(t0 + CH, false);
+    f32x4 acc[RT][4];
+#pragma unroll
+    for (int j = 0; j < RT; ++j)
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) acc[j][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      bf16x8 bh[4];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) bh[nt] = load_bf16x8(&Mh[(nt * 16 + l16) * MP + kb * 32 + kq]);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(ah[j][kb], bh[nt], acc[j][nt]);
+    }
+#pragma unroll
+    for (int rr = 0; rr < NR; ++rr)
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const int t = t0 + nt * 16 + l16;
+        const float lb = fmaf(acc[rr >> 2][nt][rr & 3], gm.scale, -fmaf(eq[rr], mn[nt], 1e-30f));
+        const float v = t < lo_r[rr] ? lb : -INFINITY;
+        const bool c1 = v > top1[rr], c2 = v > top2[rr];
+        top2[rr] = c1 ? top1[rr] : (c2 ? v : top2[rr]);
+        top1[rr] = c1 ? v : top1[rr];
       }
-      ++nl;
-    }
-    if (nl >= gm.top_k) {  // list holds top_k real entries: its k-th is a valid bar
-      float ks = ls[0];
-      int kt = lt[0];
-#pragma unroll
-      for (int k = 0; k < KMAX; ++k)
-        if (k == gm.top_k - 1) {
-          ks = ls[k];
-          kt = lt[k];
-        }
-      bar_s[wave][lane] = ks;
-      bar_t[wave][lane] = kt;
-    }
-    __syncthreads();
-    if (wave == 0) nnew[lane] = 0;
   }
 
-  // merge the four private lists of every row
-  __syncthreads();
-  float *list_s = reinterpret_cast<float *>(smem);
-  int *list_t = reinterpret_cast<int *>(smem) + 4 * 64 * KMAX;
+  // ---- bar of each row: the largest stripe top v with at least k stripe tops >= v
+  float thr[NR];
+  int cnt[NR];
 #pragma unroll
-  for (int k = 0; k < KMAX; ++k) {
-    list_s[(wave * 64 + lane) * KMAX + k] = ls[k];
-    list_t[(wave * 64 + lane) * KMAX + k] = lt[k];
+  for (int rr = 0; rr < NR; ++rr) {
+    float *rowp = reinterpret_cast<float *>(cand[crow(rr)]);
+    rowp[2 * l16] = top1[rr];
+    rowp[2 * l16 + 1] = top2[rr];
   }
-  __syncthreads();
-  const int i = i0 + lane;
-  if (wave != 0 || i >= gm.Lq) return;
-  int head[4] = {0, 0, 0, 0};
-  int picks[KMAX];
-  int npick = 0;
-#pragma unroll 1
-  for (int p = 0; p < gm.top_k; ++p) {
-    int bw = -1;
-    float bs = -FLT_MAX;
-    int bt = 0x7fffffff;
+  wave_lds_sync();
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      if (head[w] < KMAX) {
-        const float s = list_s[(w * 64 + lane) * KMAX + head[w]];
-        const int t = list_t[(w * 64 + lane) * KMAX + head[w]];
-        if (t != 0x7fffffff && beats(s, t, bs, bt)) {
-          bw = w;
-          bs = s;
-          bt = t;
+  for (int rr = 0; rr < NR; ++rr) {
+    const float4 *rowp = reinterpret_cast<const float4 *>(cand[crow(rr)]);
+    int c1 = 0, c2 = 0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float4 v = rowp[u];
+      c1 += (v.x >= top1[rr]) + (v.y >= top1[rr]) + (v.z >= top1[rr]) + (v.w >= top1[rr]);
+      c2 += (v.x >= top2[rr]) + (v.y >= top2[rr]) + (v.z >= top2[rr]) + (v.w >= top2[rr]);
+    }
+    float best = -INFINITY;
+    if (c1 >= k) best = top1[rr];
+    if (c2 >= k) best = fmaxf(best, top2[rr]);
+    thr[rr] = max16(best);
+    cnt[rr] = 0;
+  }
+  wave_lds_sync();
+
+  // cuts the list of row rr to its k best, in block order; the k-th score becomes the bar
+  auto compact = [&](int rr) {
+    float2 *rowp = cand[crow(rr)];
+    const int n = cnt[rr];
+    float ks[NJ];
+    int kt[NJ], rk[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const float2 e = j * 16 + l16 < n ? rowp[j * 16 + l16] : make_float2(-INFINITY, 0.f);
+      ks[j] = e.x;
+      kt[j] = __float_as_int(e.y);
+      rk[j] = 0;
+    }
+    for (int u = 0; u < n; ++u) {
+      const float2 e = rowp[u];
+      const int tu = __float_as_int(e.y);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) rk[j] += beats(e.x, tu, ks[j], kt[j]);
+    }
+    wave_lds_sync();
+    int pos = 0;
+    float kth = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const bool keep = j * 16 + l16 < n && rk[j] < k;
+      const uint64_t m = __ballot(keep) & grp_bits;
+      if (keep) rowp[pos + __popcll(m & below)] = make_float2(ks[j], __int_as_float(kt[j]));
+      if (keep && rk[j] == k - 1) kth = ks[j];
+      pos += __popcll(m);
+    }
+    wave_lds_sync();
+    thr[rr] = max16(kth);
+    cnt[rr] = k;
+  };
+
+  // ---- pass 2: exact scores >= bar go to the row lists in block order
+  if (gm.n_init < t_end) fetch(gm.n_init, true);
+  load_a(true);
+  for (int t0 = gm.n_init; t0 < t_end; t0 += CH) {
+    __syncthreads();
+    stage(true);
+    __syncthreads();
+    if (t0 + CH < t_end) fetch(t0 + CH, true);
+    f32x4 acc[RT][4];
+#pragma unroll
+    for (int j = 0; j < RT; ++j)
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) acc[j][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      bf16x8 bh[4], bl[4];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        bh[nt] = load_bf16x8(&Mh[(nt * 16 + l16) * MP + kb * 32 + kq]);
+        bl[nt] = load_bf16x8(&Ml[(nt * 16 + l16) * MP + kb * 32 + kq]);
+      }
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int j = 0; j < RT; ++j) {
+          acc[j][nt] = mfma16x16x32(ah[j][kb], bh[nt], acc[j][nt]);
+          acc[j][nt] = mfma16x16x32(ah[j][kb], bl[nt], acc[j][nt]);
+          acc[j][nt] = mfma16x16x32(al[j][kb], bh[nt], acc[j][nt]);
         }
+    }
+#pragma unroll
+    for (int rr = 0; rr < NR; ++rr) {
+      float2 *rowp = cand[crow(rr)];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        if (cnt[rr] > CAP - 16) compact(rr);
+        const int t = t0 + nt * 16 + l16;
+        const float sc = acc[rr >> 2][nt][rr & 3] * gm.scale;
+        const bool pass = t < lo_r[rr] && sc >= thr[rr];
+        const uint64_t m = __ballot(pass) & grp_bits;
+        if (pass) rowp[cnt[rr] + __popcll(m & below)] = make_float2(sc, __int_as_float(t));
+        cnt[rr] += __popcll(m);
       }
     }
-    if (bw < 0) break;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) head[w] += (w == bw);
-    // insert bt into the ascending picks (the elements above bt form a suffix)
-    int pos = npick;
-#pragma unroll
-    for (int k = KMAX - 2; k >= 0; --k)
-      if (k < npick && picks[k] > bt) {
-        picks[k + 1] = picks[k];
-        pos = k;
-      }
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k)
-      if (k == pos) picks[k] = bt;
-    ++npick;
   }
-  const int cur = (gm.q_pos0 + i) / gm.m;
-  const int lo = max(0, cur - gm.window / gm.m);
-  int32_t *out = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
-  int n = 0;
-  const int ni = min(gm.n_init, cur + 1);
-  for (int t = 0; t < ni; ++t) out[n++] = t;
+
+  // ---- final: the k best of each list, written in block order
+  wave_lds_sync();
 #pragma unroll
-  for (int k = 0; k < KMAX; ++k)
-    if (k < npick) out[n + k] = picks[k];
-  n += npick;
-  for (int t = max(lo, ni); t <= cur; ++t) out[n++] = t;
-  for (; n < gm.ksel; ++n) out[n] = -1;
+  for (int rr = 0; rr < NR; ++rr) {
+    const int row = crow(rr);
+    const int i = i0 + row;
+    if (i >= gm.Lq) continue;
+    const float2 *rowp = cand[row];
+    const int n = cnt[rr];
+    const int npick = min(n, k);
+    int32_t *out = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
+    float ks[NJ];
+    int kt[NJ], rk[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const float2 e = j * 16 + l16 < n ? rowp[j * 16 + l16] : make_float2(-INFINITY, 0.f);
+      ks[j] = e.x;
+      kt[j] = __float_as_int(e.y);
+      rk[j] = 0;
+    }
+    if (n > k) {
+      for (int u = 0; u < n; ++u) {
+        const float2 e = rowp[u];
+        const int tu = __float_as_int(e.y);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) rk[j] += beats(e.x, tu, ks[j], kt[j]);
+      }
+    }
+    const int cur = (gm.q_pos0 + i) / gm.m;
+    const int ni = min(gm.n_init, cur + 1);
+    int pos = 0;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const bool take = j * 16 + l16 < n && rk[j] < k;
+      const uint64_t m = __ballot(take) & grp_bits;
+      if (take) out[ni + pos + __popcll(m & below)] = kt[j];
+      pos += __popcll(m);
+    }
+    // forced init blocks, local blocks and padding around the picks
+    const int lo1 = max(max(0, cur - gm.window / gm.m), ni);
+    for (int s = l16; s < gm.ksel; s += 16) {
+      if (s >= ni && s < ni + npick) continue;
+      const int x = s - ni - npick;
+      out[s] = s < ni ? s : (lo1 + x <= cur ? lo1 + x : -1);
+    }
+  }
 }
 
 template <typename T, int D>
@@ -445,34 +566,50 @@ static hipError_t launch_select_t(const Geom &g, const void *Q, const float *Kc,
 }
 
 template <int D, int G>
-static hipError_t launch_select_mfma(const Geom &g, const void *Q, const float *Kc, int32_t *sel, hipStream_t s) {
-  dim3 grid((g.Lq + 63) / 64, g.B * g.Hkv);
-  const bf16_t *q = static_cast<const bf16_t *>(Q);
+static hipError_t launch_select_mfma(const Geom &g, const void *Q, const float *Kc, int32_t *sel, char *ws,
+                                     hipStream_t s) {
+  const int64_t n = (int64_t)g.B * g.Hkv * g.T * D;
+  bf16_t *mh = reinterpret_cast<bf16_t *>(ws), *ml = mh + n;
+  float *mnorm = reinterpret_cast<float *>(ml + n);
+  timing_begin("phsa_select_split", s);
+  hipLaunchKernelGGL(select_split_kernel<D>, dim3((unsigned)((n / 8 + 255) / 256)), dim3(256), 0, s, Kc, mh, ml, mnorm,
+                     n / 8);
+  timing_end(s);
+  // list capacity: at least k survivors of a cut plus one 16-key append (40 keeps two workgroups per CU)
+  const dim3 grid((g.Lq + 127) / 128, g.B * g.Hkv);
   timing_begin("phsa_select", s);
-  if (g.top_k <= 8)
-    hipLaunchKernelGGL((select_mfma_kernel<D, G, 8>), grid, dim3(256), 0, s, q, Kc, sel, g);
-  else if (g.top_k <= 16)
-    hipLaunchKernelGGL((select_mfma_kernel<D, G, 16>), grid, dim3(256), 0, s, q, Kc, sel, g);
+  if (g.top_k <= 16)
+    hipLaunchKernelGGL((select_mfma_kernel<D, G, 40>), grid, dim3(256), 0, s, static_cast<const bf16_t *>(Q), mh, ml,
+                       mnorm, sel, g);
   else
-    hipLaunchKernelGGL((select_mfma_kernel<D, G, 32>), grid, dim3(256), 0, s, q, Kc, sel, g);
+    hipLaunchKernelGGL((select_mfma_kernel<D, G, 48>), grid, dim3(256), 0, s, static_cast<const bf16_t *>(Q), mh, ml,
+                       mnorm, sel, g);
   timing_end(s);
   return hipGetLastError();
 }
 
 template <int D>
-static hipError_t launch_select_mfma_d(const Geom &g, const void *Q, const float *Kc, int32_t *sel, hipStream_t s) {
+static hipError_t launch_select_mfma_d(const Geom &g, const void *Q, const float *Kc, int32_t *sel, char *split,
+                                       hipStream_t s) {
   switch (g.G) {
-    case 1: return launch_select_mfma<D, 1>(g, Q, Kc, sel, s);
-    case 2: return launch_select_mfma<D, 2>(g, Q, Kc, sel, s);
-    case 4: return launch_select_mfma<D, 4>(g, Q, Kc, sel, s);
-    case 8: return launch_select_mfma<D, 8>(g, Q, Kc, sel, s);
+    case 1: return launch_select_mfma<D, 1>(g, Q, Kc, sel, split, s);
+    case 2: return launch_select_mfma<D, 2>(g, Q, Kc, sel, split, s);
+    case 4: return launch_select_mfma<D, 4>(g, Q, Kc, sel, split, s);
+    case 8: return launch_select_mfma<D, 8>(g, Q, Kc, sel, split, s);
     default: return launch_select_t<bf16_t, D>(g, Q, Kc, sel, s);
   }
 }
 
-hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t *sel, hipStream_t s) {
+size_t select_split_bytes(const Geom &g) {
+  const size_t nblk = (size_t)g.B * g.Hkv * g.T;
+  return g.dtype == 0 ? nblk * (2 * g.d * sizeof(bf16_t) + sizeof(float)) : 0;
+}
+
+hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t *sel, void *ws, hipStream_t s) {
+  char *split = static_cast<char *>(ws);
   if (g.dtype == 0)
-    return g.d == 128 ? launch_select_mfma_d<128>(g, Q, Kc, sel, s) : launch_select_mfma_d<64>(g, Q, Kc, sel, s);
+    return g.d == 128 ? launch_select_mfma_d<128>(g, Q, Kc, sel, split, s)
+                      : launch_select_mfma_d<64>(g, Q, Kc, sel, split, s);
   return g.d == 128 ? launch_select_t<float, 128>(g, Q, Kc, sel, s) : launch_select_t<float, 64>(g, Q, Kc, sel, s);
 }
 

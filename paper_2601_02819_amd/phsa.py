@@ -147,14 +147,17 @@ def compress(k: torch.Tensor, punct: torch.Tensor, cfg: Config) -> torch.Tensor:
     return kc
 
 
-def select(q: torch.Tensor, kc: torch.Tensor, seqlen_k: int, cfg: Config) -> torch.Tensor:
+def select(q: torch.Tensor, kc: torch.Tensor, seqlen_k: int, cfg: Config,
+           ws: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Q [B, Lq, Hq, d], K_comp [B, Hkv, T, d] -> sel int32 [B, Hkv, Lq, Ksel]."""
     _dev(q, kc)
     B, Lq, Hq, d = q.shape
     Hkv = kc.shape[1]
     p = make_params(cfg, B, Lq, seqlen_k, Hq, Hkv, d, q.dtype)
     sel = torch.empty(B, Hkv, Lq, cfg.ksel, dtype=torch.int32, device=q.device)
-    _check(lib().phsa_select(ctypes.byref(p), _ptr(q), _ptr(kc), _ptr(sel), None, 0, _stream()), "phsa_select")
+    w = _workspace(p, OP_SELECT, ws, q.device)
+    _check(lib().phsa_select(ctypes.byref(p), _ptr(q), _ptr(kc), _ptr(sel), _ptr(w), w.numel() if w is not None else 0,
+                             _stream()), "phsa_select")
     return sel
 
 

@@ -58,6 +58,7 @@ def _p(**kw):
     ({}, 17, phsa.ERR_INVALID_ARG),
     ({"flags": phsa.FLAG_REUSE_INDEX}, phsa.OP_ATTN_BWD, phsa.OK),
     ({"flags": 2}, phsa.OP_ATTN_BWD, phsa.ERR_INVALID_ARG),                 # unknown flag bit
+    ({"batch": 40000, "n_heads_q": 2, "n_heads_kv": 2}, phsa.OP_SELECT, phsa.ERR_UNSUPPORTED),  # B * Hkv > 65535
 ])
 def test_validate(kw, op, code):
     assert phsa.lib().phsa_validate(ctypes.byref(_p(**kw)), op) == code
@@ -68,7 +69,10 @@ def test_ksel_and_workspace():
     p = _p(n_init_blocks=2, window=128, top_k=5)
     assert L.phsa_ksel(ctypes.byref(p)) == 2 + 2 + 1 + 5
     assert phsa.workspace_size(_p(), phsa.OP_COMPRESS) == 0
-    assert phsa.workspace_size(_p(), phsa.OP_SELECT) == 0
+    # bf16 hi/lo copies of K_comp and one norm per block, rounded up to 256 bytes
+    assert phsa.workspace_size(_p(), phsa.OP_SELECT) == -(-16 * (2 * 64 * 2 + 4) // 256) * 256
+    assert phsa.workspace_size(_p(dtype=phsa.FP32), phsa.OP_SELECT) == 0
+    assert phsa.workspace_size(_p(), phsa.OP_FORWARD) >= phsa.workspace_size(_p(), phsa.OP_SELECT)
     fwd = phsa.workspace_size(_p(), phsa.OP_ATTN_FWD)
     assert fwd > 0 and fwd % 256 == 0
     assert phsa.workspace_size(_p(batch=2), phsa.OP_ATTN_FWD) > fwd

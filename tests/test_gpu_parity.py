@@ -191,3 +191,46 @@ def test_backward_reuses_forward_index():
     ref = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg)
     for a, b in zip(got, ref):
         assert torch.equal(a, b)
+
+
+def _structured_select(kind: str, top_k: int, L: int = 32768, n_init: int = 1, seed: int = 11):
+    """Selection on hand-built representatives: every row's scores follow f(t) (times a
+    positive per-row factor), so the right answer is known to be far from rounding."""
+    T, d = L // 64, 128
+    g = torch.Generator().manual_seed(seed)
+    q = torch.zeros(1, L, 2, d)
+    q[..., 0] = 0.5 + torch.rand(1, L, 2, generator=g)
+    q = q.to(torch.bfloat16)
+    t = torch.arange(T, dtype=torch.float64)
+    if kind == "stripe":      # the best blocks all share one residue mod 16
+        f = torch.where((t - n_init) % 16 == 0, 1.0 + t / T, 0.5 * t / T)
+    elif kind == "ascending":
+        f = t / T
+    elif kind == "descending":
+        f = 1.0 - t / T
+    elif kind == "ties":
+        f = torch.zeros(T, dtype=torch.float64)
+    else:
+        raise ValueError(kind)
+    kc = torch.zeros(1, 1, T, d, dtype=torch.float32)
+    kc[..., 0] = f.float()
+    cfg = phsa.Config(block_size=64, top_k=top_k, n_init_blocks=n_init, window=0)
+    sel = phsa.select(q.cuda(), kc.cuda(), L, cfg).cpu().numpy()
+    scale = d ** -0.5
+    qh = q.float().numpy()
+    kch = kc.double().numpy()
+    ref, kth, gap = oracle.select(qh, kch, 64, top_k, n_init, 0, scale, L)
+    return sel, ref, kth, gap, (lambda idx: oracle.score_row(qh, kch, 64, scale, L, idx[0], idx[2], idx[1]))
+
+
+@pytest.mark.parametrize("kind,top_k", [("stripe", 12), ("stripe", 32), ("ascending", 12), ("descending", 20),
+                                        ("ties", 12), ("ties", 32)])
+def test_select_structured_scores(kind, top_k):
+    """Orders that defeat a per-lane filter (all winners in one lane's stripe, forcing the
+    candidate lists to be cut), monotone scores, and exact ties (broken by block index)."""
+    log(f"[parity] structured selection {kind} k={top_k}")
+    sel, ref, kth, gap, score_fn = _structured_select(kind, top_k)
+    if kind == "ties":
+        np.testing.assert_array_equal(sel, ref)
+    else:
+        assert check_sel(sel, ref, kth, gap, score_fn) == 0
