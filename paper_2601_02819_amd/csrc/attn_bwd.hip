@@ -33,8 +33,6 @@
 
 namespace phsa {
 
-__device__ __forceinline__ bool slot_ok_b(int t, int cur, int T) { return t >= 0 && t <= cur && t < T; }
-
 // D = rowsum(dO * O) per (b, i, h), float32, stored [B, Lq, Hq] (workspace
 // layout).  TPR threads cover one row with
 // 16-byte loads (coalesced), then reduce with lane shuffles.
@@ -66,16 +64,22 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     const bf16_t *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dvec, Geom gm, IndexWs ix,
     bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dK, bf16_t *__restrict__ dV, float *__restrict__ dkvpart) {
   constexpr int CT = 64 / G;
-  constexpr int KP = D + 8;          // pitch of row-major [row][d] tiles
+  // Row-major [row][d] tiles.  The pitch decides the banks of the 16-byte
+  // fragment reads (rows 16m + l16, chunk q4): with D + 16 elements (288 bytes)
+  // they are conflict-free, with D + 8 they conflict about 1.6x.  Q and dO, read
+  // that way every chunk, get D + 16; K and V (one row read per wave per chunk)
+  // keep D + 8, which holds the workgroup at 80 KB (two per CU).
+  constexpr int KPQ = D + 16;
+  constexpr int KPK = D + 8;
   constexpr int RP = 64 + 8;         // pitch of the [key][row] dS tile
   constexpr int VPR = D / 8;
   constexpr int NV = 64 * VPR / 256;
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t dOs[64 * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KPK];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KPK];
+  __shared__ __attribute__((aligned(16))) bf16_t Qs[64 * KPQ];
+  __shared__ __attribute__((aligned(16))) bf16_t dOs[64 * KPQ];
   __shared__ __attribute__((aligned(16))) bf16_t dSt[64 * RP];
   __shared__ __attribute__((aligned(16))) float lse_s[64];
   __shared__ __attribute__((aligned(16))) float dd_s[64];
@@ -99,8 +103,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   for (int x = tid; x < 64 * VPR; x += 256) {
     const int kk = x / VPR, c = (x % VPR) * 8;
     const int64_t src = (krow0 + (int64_t)kk * gm.Hkv) * D + c;
-    *reinterpret_cast<uint4 *>(&Ks[kk * KP + c]) = *reinterpret_cast<const uint4 *>(K + src);
-    *reinterpret_cast<uint4 *>(&Vs[kk * KP + c]) = *reinterpret_cast<const uint4 *>(V + src);
+    *reinterpret_cast<uint4 *>(&Ks[kk * KPK + c]) = *reinterpret_cast<const uint4 *>(K + src);
+    *reinterpret_cast<uint4 *>(&Vs[kk * KPK + c]) = *reinterpret_cast<const uint4 *>(V + src);
   }
   // dK^T / dV^T accumulators: lane (q, j) holds feature 16nt + 4q + r of key 16w + j
   f32x4 dkt[NT], dvt[NT];
@@ -162,8 +166,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
-      *reinterpret_cast<uint4 *>(&Qs[r * KP + c]) = pq[k];
-      *reinterpret_cast<uint4 *>(&dOs[r * KP + c]) = pd[k];
+      *reinterpret_cast<uint4 *>(&Qs[r * KPQ + c]) = pq[k];
+      *reinterpret_cast<uint4 *>(&dOs[r * KPQ + c]) = pd[k];
       if (c == 0 && r % G == 0) ent_s[r / G] = pe[k];
     }
     if (tid < 64) {
@@ -183,12 +187,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     for (int mt = 0; mt < 4; ++mt) s[mt] = dp[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      const bf16x8 kf = load_bf16x8(&Ks[(wave * 16 + l16) * KP + kb * 32 + kq]);
-      const bf16x8 vf = load_bf16x8(&Vs[(wave * 16 + l16) * KP + kb * 32 + kq]);
+      const bf16x8 kf = load_bf16x8(&Ks[(wave * 16 + l16) * KPK + kb * 32 + kq]);
+      const bf16x8 vf = load_bf16x8(&Vs[(wave * 16 + l16) * KPK + kb * 32 + kq]);
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
-        s[mt] = mfma16x16x32(load_bf16x8(&Qs[(mt * 16 + l16) * KP + kb * 32 + kq]), kf, s[mt]);
-        dp[mt] = mfma16x16x32(load_bf16x8(&dOs[(mt * 16 + l16) * KP + kb * 32 + kq]), vf, dp[mt]);
+        s[mt] = mfma16x16x32(load_bf16x8(&Qs[(mt * 16 + l16) * KPQ + kb * 32 + kq]), kf, s[mt]);
+        dp[mt] = mfma16x16x32(load_bf16x8(&dOs[(mt * 16 + l16) * KPQ + kb * 32 + kq]), vf, dp[mt]);
       }
     }
     // P and dS; dS also goes to LDS as [key][row] for the dQ product
@@ -218,10 +222,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     // dV^T += dO^T P,  dK^T += Q^T dS   (feature tiles x this wave's keys)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      dvt[nt] = mfma16x16x32(lds_col8(dOs, KP, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, dvt[nt]);
-      dvt[nt] = mfma16x16x32(lds_col8(dOs, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, dvt[nt]);
-      dkt[nt] = mfma16x16x32(lds_col8(Qs, KP, q4 * 4, 16 + q4 * 4, nt * 16, l16), sb0, dkt[nt]);
-      dkt[nt] = mfma16x16x32(lds_col8(Qs, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dkt[nt]);
+      dvt[nt] = mfma16x16x32(lds_col8(dOs, KPQ, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, dvt[nt]);
+      dvt[nt] = mfma16x16x32(lds_col8(dOs, KPQ, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, dvt[nt]);
+      dkt[nt] = mfma16x16x32(lds_col8(Qs, KPQ, q4 * 4, 16 + q4 * 4, nt * 16, l16), sb0, dkt[nt]);
+      dkt[nt] = mfma16x16x32(lds_col8(Qs, KPQ, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dkt[nt]);
     }
     __syncthreads();  // dSt complete
 
@@ -235,7 +239,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       const bf16x8 bs = lds_col8(dSt, RP, kb * 32 + kq, kb * 32 + kq + 4, wave * 16, l16);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
-        dqt[nt] = mfma16x16x32(lds_col8(Ks, KP, kb * 32 + kq, kb * 32 + kq + 4, nt * 16, l16), bs, dqt[nt]);
+        dqt[nt] = mfma16x16x32(lds_col8(Ks, KPK, kb * 32 + kq, kb * 32 + kq + 4, nt * 16, l16), bs, dqt[nt]);
     }
     // The wave's 16 dQ rows (chunk rows 16w..16w+15) are one contiguous run of
     // the list-ordered partial buffer: stage them in this wave's rows of Qs
@@ -244,7 +248,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     for (int nt = 0; nt < NT; ++nt) {
       const bf16_t o4[4] = {f32_to_bf16(dqt[nt][0] * gm.scale), f32_to_bf16(dqt[nt][1] * gm.scale),
                             f32_to_bf16(dqt[nt][2] * gm.scale), f32_to_bf16(dqt[nt][3] * gm.scale)};
-      *reinterpret_cast<uint2 *>(&Qs[row * KP + nt * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(o4);
+      *reinterpret_cast<uint2 *>(&Qs[row * KPQ + nt * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(o4);
     }
     wave_lds_sync();
     {
@@ -255,7 +259,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
         const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
         if (r < nrows)
           *reinterpret_cast<uint4 *>(dqpart + (run0 + r) * D + cc) =
-              *reinterpret_cast<const uint4 *>(&Qs[(wave * 16 + r) * KP + cc]);
+              *reinterpret_cast<const uint4 *>(&Qs[(wave * 16 + r) * KPQ + cc]);
       }
     }
   }
@@ -319,55 +323,39 @@ __global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restri
 // (b, g, query row), 8 features per lane (16-byte loads); the slot loop is
 // unrolled over a prefix of valid slots (the well-formed case), else a bit-walk.
 template <int D, int G>
-__global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restrict__ sel,
-                                                         const int32_t *__restrict__ pmap,
+__global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restrict__ pmap,
                                                          const bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dQ,
                                                          Geom gm) {
-  constexpr int U = 8;
+  constexpr int U = 16;  // slots whose partials are in flight together
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
   const int64_t x = ((int64_t)blockIdx.x * 4 + wave) * 2 + half;
   const bool row_ok = x < (int64_t)gm.B * gm.Hkv * gm.Lq;
   const int64_t xr = row_ok ? x : 0;
   const int bg = (int)(xr / gm.Lq), i = (int)(xr - (int64_t)bg * gm.Lq);
   const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
-  const int cur = (gm.q_pos0 + i) / gm.m;
-  // valid slots of this half's row (Ksel <= 64): lane l32 tests slots l32 and l32 + 32
-  const int ta = (row_ok && l32 < gm.ksel) ? sel[xr * gm.ksel + l32] : -1;
-  const int tb = (row_ok && l32 + 32 < gm.ksel) ? sel[xr * gm.ksel + l32 + 32] : -1;
-  const uint64_t ba = __ballot(slot_ok_b(ta, cur, gm.T)), bb = __ballot(slot_ok_b(tb, cur, gm.T));
-  const uint64_t valid = ((ba >> (32 * half)) & 0xffffffffull) | (((bb >> (32 * half)) & 0xffffffffull) << 32);
-  const int nv = __popcll(valid);
-  const bool prefix = valid == (nv == 64 ? ~0ull : ((1ull << nv) - 1));
-  const int64_t base = xr * gm.ksel;
-  if (!row_ok) return;
+  const RowSlots rs(pmap, xr * gm.ksel, row_ok, gm.ksel, half, l32);
+  const int ns = rs.slots();
   for (int e = l32 * 8; e < G * D; e += 256) {
     const int hh = e / D, c = e - hh * D;
     float a[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) a[k] = 0.f;
-    auto add = [&](const uint4 &raw) {
-      const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
+    for (int s0 = 0; s0 < ns; s0 += U) {
+      uint4 raw[U];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) a[k] += bf16_to_f32(pv[k]);
-    };
-    if (prefix) {
-      for (int k0 = 0; k0 < nv; k0 += U) {
-        int pk[U];
-#pragma unroll
-        for (int k = 0; k < U; ++k) pk[k] = k0 + k < nv ? pmap[base + k0 + k] : 0;
-        uint4 raw[U];
-#pragma unroll
-        for (int k = 0; k < U; ++k)
-          raw[k] = k0 + k < nv ? ld_stream16(dqpart + ((int64_t)pk[k] * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
-#pragma unroll
-        for (int k = 0; k < U; ++k) add(raw[k]);
+      for (int k = 0; k < U; ++k) {
+        const int s = s0 + k;
+        const int p = s < ns ? rs.pos(s, half) : -1;
+        raw[k] = p >= 0 ? ld_stream16(dqpart + ((int64_t)p * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
       }
-    } else {
-      for (uint64_t v = valid; v; v &= v - 1) {
-        const int64_t sl = pmap[base + __ffsll((long long)v) - 1];
-        add(*reinterpret_cast<const uint4 *>(dqpart + (sl * G + hh) * D + c));
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw[k]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) a[j] += bf16_to_f32(pv[j]);
       }
     }
+    if (!row_ok) continue;
     bf16_t outv[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) outv[k] = f32_to_bf16(a[k]);
@@ -392,8 +380,8 @@ static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, cons
   timing_end(s);
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_attn_bwd_dq_combine", s);
-  hipLaunchKernelGGL((dq_combine_kernel<D, G>), dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s, sel,
-                     ix.pmap, static_cast<const bf16_t *>(dqpart), static_cast<bf16_t *>(dQ), g);
+  hipLaunchKernelGGL((dq_combine_kernel<D, G>), dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s, ix.pmap,
+                     static_cast<const bf16_t *>(dqpart), static_cast<bf16_t *>(dQ), g);
   timing_end(s);
   return hipGetLastError();
 }

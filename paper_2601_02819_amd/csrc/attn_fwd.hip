@@ -34,8 +34,6 @@
 
 namespace phsa {
 
-__device__ __forceinline__ bool slot_ok(int t, int cur, int T) { return t >= 0 && t <= cur && t < T; }
-
 template <int D, int G>
 __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *__restrict__ Q,
                                                               const bf16_t *__restrict__ K,
@@ -170,77 +168,49 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
 // slots are a prefix 0..n-1; that case runs with the slot loop unrolled so
 // all partial loads are in flight together.  Other patterns take a bit-walk.
 template <int D, int G>
-__global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__restrict__ sel,
-                                                               const int32_t *__restrict__ pmap,
+__global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__restrict__ pmap,
                                                                const bf16_t *__restrict__ opart,
                                                                const float2 *__restrict__ ml, bf16_t *__restrict__ O,
                                                                float *__restrict__ LSE, Geom gm) {
-  constexpr int U = 8;
+  constexpr int U = 16;  // slots whose partials are in flight together
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
   const int64_t x = ((int64_t)blockIdx.x * 4 + wave) * 2 + half;  // bg * Lq + i
   const bool row_ok = x < (int64_t)gm.B * gm.Hkv * gm.Lq;
   const int64_t xr = row_ok ? x : 0;
   const int bg = (int)(xr / gm.Lq), i = (int)(xr - (int64_t)bg * gm.Lq);
   const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
-  const int cur = (gm.q_pos0 + i) / gm.m;
-  // valid slots of this half's row (Ksel <= 64): lane l32 tests slots l32 and l32 + 32
-  const int ta = (row_ok && l32 < gm.ksel) ? sel[xr * gm.ksel + l32] : -1;
-  const int tb = (row_ok && l32 + 32 < gm.ksel) ? sel[xr * gm.ksel + l32 + 32] : -1;
-  const uint64_t ba = __ballot(slot_ok(ta, cur, gm.T)), bb = __ballot(slot_ok(tb, cur, gm.T));
-  const uint64_t valid = ((ba >> (32 * half)) & 0xffffffffull) | (((bb >> (32 * half)) & 0xffffffffull) << 32);
-  const int nv = __popcll(valid);
-  const bool prefix = valid == (nv == 64 ? ~0ull : ((1ull << nv) - 1));
-  const int64_t base = xr * gm.ksel;
-  if (!row_ok) return;
+  const RowSlots rs(pmap, xr * gm.ksel, row_ok, gm.ksel, half, l32);
+  const int ns = rs.slots();
   for (int e = l32 * 8; e < G * D; e += 256) {
     const int hh = e / D, c = e - hh * D;
+    // online merge in slot order: running max M (log2 units), sum L, sum a
     float M = -INFINITY, L = 0.f, a[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) a[k] = 0.f;
-    auto add = [&](float w, const uint4 &raw) {
-      const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
+    for (int s0 = 0; s0 < ns; s0 += U) {
+      float2 q[U];
+      uint4 raw[U];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) a[k] = fmaf(w, bf16_to_f32(pv[k]), a[k]);
-    };
-    if (prefix) {
-      for (int k0 = 0; k0 < nv; k0 += U) {
-        int pk[U];
-#pragma unroll
-        for (int k = 0; k < U; ++k) pk[k] = k0 + k < nv ? pmap[base + k0 + k] : 0;
-#pragma unroll
-        for (int k = 0; k < U; ++k)
-          if (k0 + k < nv) M = fmaxf(M, ml[(int64_t)pk[k] * G + hh].x);
+      for (int k = 0; k < U; ++k) {
+        const int s = s0 + k;
+        const int p = s < ns ? rs.pos(s, half) : -1;
+        const bool ok = p >= 0;
+        q[k] = ok ? ml[(int64_t)p * G + hh] : make_float2(-INFINITY, 0.f);
+        raw[k] = ok ? ld_stream16(opart + ((int64_t)p * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
       }
-      for (int k0 = 0; k0 < nv; k0 += U) {
-        int pk[U];
 #pragma unroll
-        for (int k = 0; k < U; ++k) pk[k] = k0 + k < nv ? pmap[base + k0 + k] : 0;
-        float2 q[U];
-        uint4 raw[U];
+      for (int k = 0; k < U; ++k) {
+        if (q[k].x == -INFINITY) continue;
+        const float mn = fmaxf(M, q[k].x);
+        const float sc = exp2f(M - mn), w = exp2f(q[k].x - mn);
+        L = fmaf(w, q[k].y, L * sc);
+        const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw[k]);
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
-          const bool ok = k0 + k < nv;
-          q[k] = ok ? ml[(int64_t)pk[k] * G + hh] : make_float2(-INFINITY, 0.f);
-          raw[k] = ok ? ld_stream16(opart + ((int64_t)pk[k] * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
-        }
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-          const float w = exp2f(q[k].x - M);
-          L = fmaf(w, q[k].y, L);
-          add(w, raw[k]);
-        }
-      }
-    } else {
-      for (uint64_t v = valid; v; v &= v - 1)
-        M = fmaxf(M, ml[(int64_t)pmap[base + __ffsll((long long)v) - 1] * G + hh].x);
-      for (uint64_t v = valid; v; v &= v - 1) {
-        const int64_t sl = pmap[base + __ffsll((long long)v) - 1];
-        const float2 q = ml[sl * G + hh];
-        const float w = exp2f(q.x - M);
-        L = fmaf(w, q.y, L);
-        add(w, *reinterpret_cast<const uint4 *>(opart + (sl * G + hh) * D + c));
+        for (int j = 0; j < 8; ++j) a[j] = fmaf(w, bf16_to_f32(pv[j]), a[j] * sc);
+        M = mn;
       }
     }
+    if (!row_ok) continue;
     const float inv = L > 0.f ? 1.f / L : 0.f;
     bf16_t outv[8];
 #pragma unroll
@@ -261,8 +231,8 @@ static hipError_t launch_fwd_t(const Geom &g, const void *Q, const void *K, cons
   timing_end(s);
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_attn_fwd_combine", s);
-  hipLaunchKernelGGL((attn_fwd_combine_kernel<D, G>), dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s, sel,
-                     ix.pmap, static_cast<const bf16_t *>(opart), ml, static_cast<bf16_t *>(O), LSE, g);
+  hipLaunchKernelGGL((attn_fwd_combine_kernel<D, G>), dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s, ix.pmap,
+                     static_cast<const bf16_t *>(opart), ml, static_cast<bf16_t *>(O), LSE, g);
   timing_end(s);
   return hipGetLastError();
 }

@@ -99,6 +99,30 @@ __device__ __forceinline__ bf16x8 lds_col8(const bf16_t *X, int pitch, int r0, i
   return __builtin_bit_cast(bf16x8, c);
 }
 
+// The partials of one (b, g, query row) for the per-row merges.  Half a wave
+// owns a row: lane l32 reads the list positions of slots l32 and l32 + 32
+// (-1 marks a slot without a partial).  slots() is a wave-uniform bound on the
+// highest used slot of either half, and pos(s) gives each lane its own half's
+// position of slot s (every lane must call it, s uniform).
+struct RowSlots {
+  int pa, pb;
+  uint64_t valid;  // this half's slots that hold a partial
+  uint32_t lo, hi; // slots < 32 / >= 32 used by either half
+  __device__ __forceinline__ RowSlots(const int32_t *pmap, int64_t base, bool row_ok, int ksel, int half, int l32) {
+    pa = (row_ok && l32 < ksel) ? pmap[base + l32] : -1;
+    pb = (row_ok && l32 + 32 < ksel) ? pmap[base + l32 + 32] : -1;
+    const uint64_t ba = __ballot(pa >= 0), bb = __ballot(pb >= 0);
+    valid = ((ba >> (32 * half)) & 0xffffffffull) | (((bb >> (32 * half)) & 0xffffffffull) << 32);
+    lo = (uint32_t)ba | (uint32_t)(ba >> 32);
+    hi = (uint32_t)bb | (uint32_t)(bb >> 32);
+  }
+  __device__ __forceinline__ int slots() const { return hi ? 64 - __clz(hi) : 32 - __clz(lo); }
+  __device__ __forceinline__ int pos(int s, int half) const {
+    const int src = half * 32 + (s & 31);
+    return s < 32 ? __shfl(pa, src, 64) : __shfl(pb, src, 64);
+  }
+};
+
 // Orders a wave's LDS writes before its following LDS reads of other lanes'
 // data.  A wave's LDS instructions execute in order, so this only has to stop
 // the compiler from moving the accesses across it.
