@@ -33,10 +33,12 @@ METRIC = "PHSA fwd+bwd ms & selected-block TFLOP/s at L=32k, 97.3% sparsity; % M
 CSRC = os.path.join(ROOT, "paper_2601_02819_amd", "csrc")
 # kernel name in the timing hooks -> its source file (the traffic record is void once that changes)
 KERNEL_SOURCE = {"phsa_attn_bwd_sparse": "attn_bwd.hip", "phsa_attn_fwd_sparse": "attn_fwd.hip",
-                 "phsa_select": "select.hip", "phsa_compress": "compress.hip"}
+                 "phsa_select": "select.hip", "phsa_compress": "compress.hip",
+                 "phsa_attn_fwd_combine": "attn_fwd.hip", "phsa_attn_bwd_dq_combine": "attn_bwd.hip"}
 # rocprofv3 kernel-name fragment of each timed kernel
 KERNEL_SYMBOL = {"phsa_attn_bwd_sparse": "attn_bwd_sparse_kernel", "phsa_attn_fwd_sparse": "attn_fwd_sparse_kernel",
-                 "phsa_select": "select_mfma_kernel", "phsa_compress": "compress_kernel"}
+                 "phsa_select": "select_mfma_kernel", "phsa_compress": "compress_kernel",
+                 "phsa_attn_fwd_combine": "attn_fwd_combine_kernel", "phsa_attn_bwd_dq_combine": "dq_combine_kernel"}
 
 
 def source_hash(kernel: str) -> str:
@@ -146,6 +148,16 @@ def bench_train(steps: int, warmup: int, seed: int):
 
     fwd_flop = 4.0 * d * m * nsel * G
     bwd_flop = 2.5 * fwd_flop
+    # Bytes the key-block-major kernels must move per launch: every (row, block)
+    # pair gathers its query rows (and dO rows) and leaves a bf16 partial (plus
+    # the forward's (m, l)); every work unit loads its K/V block once.  This is
+    # the schedule's own traffic floor, above the method's algorithmic minimum.
+    unit_tokens = 64 * (64 // G)
+    units = B * Hkv * T + nsel // unit_tokens
+    kv_bytes = units * 64 * d * 2 * 2
+    pair_row = G * d * 2
+    design_bytes = {"phsa_attn_fwd_sparse": nsel * (2 * pair_row + G * 8 + 4) + kv_bytes,
+                    "phsa_attn_bwd_sparse": nsel * (3 * pair_row + G * 8 + 4) + kv_bytes + B * L * Hkv * d * 2 * 2}
     bytes_compress = B * L * Hkv * d * 2 + B * L + B * Hkv * T * d * 4
     bytes_select = B * L * Hq * d * 2 + B * Hkv * T * d * 4 + B * Hkv * L * wl.ksel * 4
     work = {"phsa_attn_fwd_sparse": ("TFLOP/s", fwd_flop / 1e12), "phsa_attn_bwd_sparse": ("TFLOP/s", bwd_flop / 1e12),
@@ -155,6 +167,14 @@ def bench_train(steps: int, warmup: int, seed: int):
             rate = amount / (ks[n]["avg_ms"] / 1e3)
             peak = PEAK_BF16_TFLOPS if unit == "TFLOP/s" else PEAK_HBM_GBS
             ks[n].update(rate=rate, unit=unit, frac=rate / peak)
+            if n in design_bytes:
+                # attainable = min(MFMA peak, intensity x HBM peak) for this schedule's traffic
+                flop = fwd_flop if "fwd" in n else bwd_flop
+                t_min = max(flop / (PEAK_BF16_TFLOPS * 1e12), design_bytes[n] / (PEAK_HBM_GBS * 1e9))
+                att = flop / 1e12 / t_min
+                ks[n].update(schedule_bytes=design_bytes[n],
+                             schedule_GB_per_s=design_bytes[n] / 1e9 / (ks[n]["avg_ms"] / 1e3),
+                             attainable_tflops=att, frac_of_attainable=rate / att)
     dom = max(ks, key=lambda n: ks[n]["total_ms"])
     return {
         "ms_per_step": ms_step,
@@ -277,6 +297,9 @@ def main():
                 "achieved": dk.get("rate"), "peak": PEAK_BF16_TFLOPS if dk.get("unit") == "TFLOP/s" else PEAK_HBM_GBS,
                 "unit": dk.get("unit"), "frac": dk.get("frac"), "traffic": traffic,
                 "avg_ms": dk["avg_ms"]}
+    for key in ("schedule_bytes", "attainable_tflops", "frac_of_attainable"):
+        if key in dk:
+            roofline[key] = dk[key]
     result = {
         "metric": METRIC, "value": tr["value"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": tr["ms_per_step"], "higher_is_better": True, "scaling": "weak",

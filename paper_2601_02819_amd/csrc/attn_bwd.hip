@@ -320,8 +320,9 @@ __global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restri
 }
 
 // dQ = sum over a row's valid slots of the partials.  Half a wave per
-// (b, g, query row), 8 features per lane (16-byte loads); the slot loop is
-// unrolled over a prefix of valid slots (the well-formed case), else a bit-walk.
+// (b, g, query row), 8 features per lane (16-byte loads); the row's list
+// positions come in one load (RowSlots), then up to 16 partials are loaded
+// together and summed in slot order.
 template <int D, int G>
 __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restrict__ pmap,
                                                          const bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dQ,

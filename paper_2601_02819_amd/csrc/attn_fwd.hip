@@ -26,7 +26,8 @@
 // writes one contiguous run: the unnormalised partial O (bf16) and (m, l) in
 // log2 units.  A second kernel merges the at most Ksel partials of each row:
 //   M = max_s m_s,  w_s = 2^(m_s - M),  O = sum_s w_s O_s / sum_s w_s l_s,
-//   LSE = (M + log2 sum_s w_s l_s) ln 2.
+//   LSE = (M + log2 sum_s w_s l_s) ln 2
+// (computed with a running maximum in slot order).
 #include <math.h>
 
 #include "common.h"
@@ -40,13 +41,14 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
                                                               const bf16_t *__restrict__ V, Geom gm, IndexWs ix,
                                                               bf16_t *__restrict__ opart, float2 *__restrict__ ml) {
   constexpr int TW = 16 / G;         // query tokens per wave chunk
-  constexpr int KP = D + 8;          // LDS row pitch (elements)
+  constexpr int KP = D + 16;         // K pitch: 16-byte row reads of 16 rows are conflict-free at D + 16
+  constexpr int VP = D + 8;          // V pitch (transposing reads only)
   constexpr int VPR = D / 8;         // 16-byte vectors per row
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
   constexpr int SP = D + 8;          // pitch of the per-wave output staging rows
   __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * VP];
   __shared__ __attribute__((aligned(16))) bf16_t Os[4][16 * SP];  // per-wave partial rows
 
   const int u = blockIdx.x;
@@ -64,7 +66,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
     const int kk = x / VPR, c = (x % VPR) * 8;
     const int64_t grow = ((int64_t)b * gm.Lk + (int64_t)t * 64 + kk) * gm.Hkv + g;
     *reinterpret_cast<uint4 *>(&Ks[kk * KP + c]) = *reinterpret_cast<const uint4 *>(K + grow * D + c);
-    *reinterpret_cast<uint4 *>(&Vs[kk * KP + c]) = *reinterpret_cast<const uint4 *>(V + grow * D + c);
+    *reinterpret_cast<uint4 *>(&Vs[kk * VP + c]) = *reinterpret_cast<const uint4 *>(V + grow * D + c);
   }
   __syncthreads();
 
@@ -132,8 +134,8 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       ot[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      ot[nt] = mfma16x16x32(lds_col8(Vs, KP, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, ot[nt]);
-      ot[nt] = mfma16x16x32(lds_col8(Vs, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, ot[nt]);
+      ot[nt] = mfma16x16x32(lds_col8(Vs, VP, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, ot[nt]);
+      ot[nt] = mfma16x16x32(lds_col8(Vs, VP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, ot[nt]);
     }
     // The chunk's 16 partial rows are one contiguous run of the list-ordered
     // partial buffer (entries c*TW.., heads inner): stage them in LDS and write
@@ -164,9 +166,10 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
 }
 
 // Merge of a row's per-slot partials.  Half a wave per (b, g, query row), 8
-// features per lane (16-byte loads).  For a well-formed selection the valid
-// slots are a prefix 0..n-1; that case runs with the slot loop unrolled so
-// all partial loads are in flight together.  Other patterns take a bit-walk.
+// features per lane (16-byte loads).  The row's list positions come in one
+// load spread over the lanes (RowSlots); the partials and their (m, l) of up
+// to 16 slots are then loaded together and folded in slot order with a
+// running maximum, so a row costs two dependent global loads.
 template <int D, int G>
 __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__restrict__ pmap,
                                                                const bf16_t *__restrict__ opart,
