@@ -88,9 +88,7 @@ size_t bwd_layout(const Geom &g, char *base, BwdWs *ws) {
   return off;
 }
 
-size_t decode_layout(const Geom &g) {
-  return align_up(sizeof(float) * (size_t)g.B * g.Hkv * g.ksel * g.G * (g.d + 2));
-}
+size_t decode_layout(const Geom &) { return 0; }  // the decode kernels need no scratch
 
 bool is_attention_op(int op) {
   return op == PHSA_OP_ATTN_FWD || op == PHSA_OP_ATTN_BWD || op == PHSA_OP_FORWARD || op == PHSA_OP_DECODE;
@@ -340,8 +338,7 @@ phsa_status phsa_decode(const phsa_params *p, const void *Q, const void *K_cache
     if (st != PHSA_OK) return st;
     if (!Q || !K_cache || !V_cache || !K_comp || !sel || !O || !LSE) return PHSA_ERR_NULL;
     if ((st = check_ws(g, PHSA_OP_DECODE, ws, ws_bytes)) != PHSA_OK) return st;
-    return from_hip(launch_decode(g, Q, K_cache, V_cache, K_comp, sel, O, LSE, static_cast<float *>(ws),
-                                  static_cast<hipStream_t>(stream)));
+    return from_hip(launch_decode(g, Q, K_cache, V_cache, K_comp, sel, O, LSE, static_cast<hipStream_t>(stream)));
   })
 }
 

@@ -5,16 +5,14 @@
 // memory-bound: the representatives and the selected K/V blocks are each
 // read once.
 //
-//   decode_select  : one workgroup per (b, g).  Waves score blocks with
-//                    coalesced 512-byte reads of K_comp rows and a wave sum;
-//                    wave 0 then takes the top-k by successive maxima of the
-//                    strict order (score desc, block asc), each round looking
-//                    only below the previous winner.
-//   decode_attn    : one workgroup per (slot, b, g): the block's K/V tile is
-//                    staged in LDS as float32, each wave does one head's
-//                    softmax over the 64 keys, and the partial (o / l, m, l)
-//                    goes to the workspace.
-//   decode_combine : one wave per (b, g) merges the partials.
+//   decode_select : one workgroup of 8 waves per (b, g).  Lanes read K_comp
+//                   rows as float4 (D / 4 lanes per row, 8 loads in flight
+//                   each) and reduce a row's dot product by shuffles; the
+//                   top-k (score desc, block asc) comes from per-wave bitonic
+//                   sorts of 64-candidate chunks merged pairwise in LDS.
+//   decode_attn   : one workgroup per (b, g) streams its selected K/V blocks
+//                   with coalesced 16-byte loads, keeps a running softmax per
+//                   wave and merges the waves in LDS: O and LSE directly.
 #include <float.h>
 #include <math.h>
 
@@ -27,60 +25,107 @@ __device__ __forceinline__ bool beats_d(float s1, int t1, float s2, int t2) {
   return s1 > s2 || (s1 == s2 && t1 < t2);
 }
 
+// One (score, block) pair per lane, sorted across the wave best first
+// (higher score, then lower block) by a bitonic network over shuffles.
+__device__ __forceinline__ void wave_sort_best_first(float &s, int &t, int lane) {
+#pragma unroll
+  for (int size = 2; size <= 64; size <<= 1)
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      const float os = __shfl_xor(s, stride, 64);
+      const int ot = __shfl_xor(t, stride, 64);
+      const bool want_better = ((lane & size) == 0) == ((lane & stride) == 0);
+      if (beats_d(os, ot, s, t) == want_better && !(os == s && ot == t)) {
+        s = os;
+        t = ot;
+      }
+    }
+}
+
+// r := the best 64 of r and v, best first (both best-first sorted across the wave).
+__device__ __forceinline__ void wave_merge_best_first(float &rs, int &rt, float vs, int vt, int lane) {
+  const float ws = __shfl(vs, 63 - lane, 64);
+  const int wt = __shfl(vt, 63 - lane, 64);
+  if (beats_d(ws, wt, rs, rt)) {
+    rs = ws;
+    rt = wt;
+  }
+  // r is now bitonic; finish with the merge stages of a best-first sort
+#pragma unroll
+  for (int stride = 32; stride > 0; stride >>= 1) {
+    const float os = __shfl_xor(rs, stride, 64);
+    const int ot = __shfl_xor(rt, stride, 64);
+    const bool want_better = (lane & stride) == 0;
+    if (beats_d(os, ot, rs, rt) == want_better && !(os == rs && ot == rt)) {
+      rs = os;
+      rt = ot;
+    }
+  }
+}
+
 template <typename T, int D>
-__global__ __launch_bounds__(256) void decode_select_kernel(const T *__restrict__ Q, const float *__restrict__ Kc,
+__global__ __launch_bounds__(512) void decode_select_kernel(const T *__restrict__ Q, const float *__restrict__ Kc,
                                                             int32_t *__restrict__ sel, Geom gm) {
-  extern __shared__ float sc[];  // [T]
-  __shared__ float qsum[D];
+  constexpr int LPR = D / 4;      // lanes per representative row (one float4 each)
+  constexpr int RPW = 64 / LPR;   // rows per wave load instruction
+  constexpr int U = 8;            // load instructions in flight per lane
+  extern __shared__ float sc[];   // [T]
+  __shared__ float mbuf_s[4][64];
+  __shared__ int mbuf_t[4][64];
   const int bg = blockIdx.x, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int c = tid; c < D; c += 256) {
-    float a = 0.f;
-    for (int hh = 0; hh < gm.G; ++hh) a += to_f32<T>(Q[((int64_t)b * gm.Hq + g * gm.G + hh) * D + c]);
-    qsum[c] = a;
+  const int sub = lane / LPR, c4 = (lane % LPR) * 4;
+  float q[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int hh = 0; hh < gm.G; ++hh) {
+    const T *src = Q + ((int64_t)b * gm.Hq + g * gm.G + hh) * D + c4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) q[e] += to_f32<T>(src[e]);
   }
-  __syncthreads();
   const int cur = gm.T - 1;
   const int lo = max(0, cur - gm.window / gm.m);
   const float *kc = Kc + (int64_t)bg * gm.T * D;
-  for (int t = gm.n_init + wave; t < lo; t += 4) {
-    float a = 0.f;
+  for (int t0 = gm.n_init + wave * RPW * U; t0 < lo; t0 += 8 * RPW * U) {
+    float4 v[U];
 #pragma unroll
-    for (int c = lane; c < D; c += 64) a = fmaf(qsum[c], kc[(int64_t)t * D + c], a);
-    a = wave_sum(a);
-    if (lane == 0) sc[t] = a * gm.scale;
+    for (int u = 0; u < U; ++u) {
+      const int t = t0 + u * RPW + sub;
+      v[u] = t < lo ? *reinterpret_cast<const float4 *>(kc + (int64_t)t * D + c4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float a = fmaf(q[0], v[u].x, fmaf(q[1], v[u].y, fmaf(q[2], v[u].z, q[3] * v[u].w)));
+#pragma unroll
+      for (int o = 1; o < LPR; o <<= 1) a += __shfl_xor(a, o, 64);
+      const int t = t0 + u * RPW + sub;
+      if (lane % LPR == 0 && t < lo) sc[t] = a * gm.scale;
+    }
   }
   __syncthreads();
-  if (wave != 0) return;
 
+  // Top-k: every wave sorts its 64-candidate chunks best-first across its
+  // lanes (bitonic network over shuffles) and keeps the best 64 seen; the
+  // eight sorted lists are then merged pairwise through LDS.
   const int nc = max(0, lo - gm.n_init);
-  const int npick = min(gm.top_k, nc);
-  float ps = FLT_MAX;  // previous winner (strictly better than everything left)
-  int pt = -1;
-  int mine = 0x7fffffff;
-  for (int p = 0; p < npick; ++p) {
-    float bs = -FLT_MAX;
-    int bt = 0x7fffffff;
-    for (int t = gm.n_init + lane; t < lo; t += 64) {
-      const float s = sc[t];
-      if (beats_d(ps, pt, s, t) && beats_d(s, t, bs, bt)) {
-        bs = s;
-        bt = t;
-      }
-    }
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const float os = __shfl_xor(bs, o, 64);
-      const int ot = __shfl_xor(bt, o, 64);
-      if (beats_d(os, ot, bs, bt)) {
-        bs = os;
-        bt = ot;
-      }
-    }
-    if (lane == p) mine = bt;
-    ps = bs;
-    pt = bt;
+  float rs = -INFINITY;
+  int rt = 0x7fffffff;
+  for (int c0 = wave * 64; c0 < nc; c0 += 8 * 64) {
+    float vs = c0 + lane < nc ? sc[gm.n_init + c0 + lane] : -INFINITY;
+    int vt = c0 + lane < nc ? gm.n_init + c0 + lane : 0x7fffffff;
+    wave_sort_best_first(vs, vt, lane);
+    wave_merge_best_first(rs, rt, vs, vt, lane);
   }
+  for (int half = 4; half >= 1; half >>= 1) {
+    if (wave >= half && wave < 2 * half) {
+      mbuf_s[wave - half][lane] = rs;
+      mbuf_t[wave - half][lane] = rt;
+    }
+    __syncthreads();
+    if (wave < half) wave_merge_best_first(rs, rt, mbuf_s[wave][lane], mbuf_t[wave][lane], lane);
+    __syncthreads();
+  }
+  if (wave != 0) return;
+  const int npick = min(gm.top_k, nc);
+  const int mine = rt;  // lanes 0..npick-1 hold the picks, best first
   // ascending order of the picks: rank = number of smaller picks
   int rank = 0;
   for (int j = 0; j < npick; ++j) rank += (__shfl(mine, j, 64) < mine);
@@ -94,121 +139,160 @@ __global__ __launch_bounds__(256) void decode_select_kernel(const T *__restrict_
   for (int x = ni + npick + nlocal + lane; x < gm.ksel; x += 64) out[x] = -1;
 }
 
-template <typename T, int D>
-__global__ __launch_bounds__(256) void decode_attn_kernel(const T *__restrict__ Q, const T *__restrict__ K,
+// Attention of one decode query over its selected blocks, one workgroup per
+// (b, g); wave w takes slots w, w + 4, ....  A block's K and V rows arrive
+// with coalesced 16-byte loads, NI per lane (lane = one 16-byte chunk of a key
+// row, KPI key rows per load); the CPR lanes of a row reduce its dot products
+// by shuffles.  Each wave keeps a running (m, l, o) per head (log2 units);
+// the four are merged through LDS and O, LSE written directly.
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256, 2) void decode_attn_kernel(const T *__restrict__ Q, const T *__restrict__ K,
                                                           const T *__restrict__ V, const int32_t *__restrict__ sel,
-                                                          float *__restrict__ part, Geom gm) {
-  __shared__ float Kf[64][D + 1];
-  __shared__ float Vf[64][D];
-  __shared__ float ps[8][64];
-  __shared__ float qf[8][D];
-  __shared__ float mls[8][2];
-  const int slot = blockIdx.x, bg = blockIdx.y, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
+                                                          T *__restrict__ O, float *__restrict__ LSE, Geom gm) {
+  constexpr int VEC = 16 / sizeof(T);   // elements per 16-byte chunk
+  constexpr int CPR = D / VEC;          // chunks (lanes) per key row
+  constexpr int KPI = 64 / CPR;         // key rows per load instruction
+  constexpr int NI = (8 * KPI > 64 ? 64 : 8 * KPI) / KPI;    // loads per tensor per key group
+  constexpr int KG = NI * KPI;          // keys per group
+  __shared__ float wm[4][G], wl[4][G];
+  __shared__ float wo[4][G][D];
+  const int bg = blockIdx.x, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int cur = gm.T - 1, pos = gm.Lk - 1;
-  const int t = sel[(int64_t)bg * gm.ksel + slot];
-  if (t < 0 || t > cur || t >= gm.T) return;
-  constexpr int VEC = 16 / sizeof(T);
-  for (int x = tid; x < 64 * D / VEC; x += 256) {
-    const int kk = x / (D / VEC), c = (x % (D / VEC)) * VEC;
-    const int64_t src = (((int64_t)b * gm.Lk + (int64_t)t * 64 + kk) * gm.Hkv + g) * D + c;
-    const uint4 rk = *reinterpret_cast<const uint4 *>(K + src);
-    const uint4 rv = *reinterpret_cast<const uint4 *>(V + src);
-    const T *pk = reinterpret_cast<const T *>(&rk);
-    const T *pv = reinterpret_cast<const T *>(&rv);
+  const int ch = lane % CPR, sub = lane / CPR;
+  const float sl2 = gm.scale * kLog2e;
+  float qv[G][VEC];
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      Kf[kk][c + e] = to_f32<T>(pk[e]);
-      Vf[kk][c + e] = to_f32<T>(pv[e]);
+  for (int h = 0; h < G; ++h) {
+    const uint4 raw = *reinterpret_cast<const uint4 *>(Q + ((int64_t)b * gm.Hq + g * G + h) * D + ch * VEC);
+    const T *pv = reinterpret_cast<const T *>(&raw);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) qv[h][e] = to_f32<T>(pv[e]) * sl2;
+  }
+  float mrun[G], lrun[G], o[G][VEC];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    mrun[h] = -INFINITY;
+    lrun[h] = 0.f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[h][e] = 0.f;
+  }
+  const int cur = gm.T - 1, pos = gm.Lk - 1;
+  for (int s = wave; s < gm.ksel; s += 4) {
+    const int t = sel[(int64_t)bg * gm.ksel + s];
+    if (t < 0 || t > cur || t >= gm.T) continue;  // wave-uniform
+    for (int k0 = 0; k0 < 64; k0 += KG) {
+      uint4 kr[NI], vr[NI];
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int key = k0 + i * KPI + sub;
+        const int64_t src = (((int64_t)b * gm.Lk + (int64_t)t * 64 + key) * gm.Hkv + g) * D + ch * VEC;
+        kr[i] = *reinterpret_cast<const uint4 *>(K + src);
+        vr[i] = *reinterpret_cast<const uint4 *>(V + src);
+      }
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float sc[NI];
+        float bm = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const T *pk = reinterpret_cast<const T *>(&kr[i]);
+          float a = 0.f;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) a = fmaf(qv[h][e], to_f32<T>(pk[e]), a);
+#pragma unroll
+          for (int x = 1; x < CPR; x <<= 1) a += __shfl_xor(a, x, 64);
+          sc[i] = (t * 64 + k0 + i * KPI + sub) <= pos ? a : -INFINITY;
+          bm = fmaxf(bm, sc[i]);
+        }
+#pragma unroll
+        for (int x = CPR; x < 64; x <<= 1) bm = fmaxf(bm, __shfl_xor(bm, x, 64));
+        const float mn = fmaxf(mrun[h], bm);
+        const float f = exp2f(mrun[h] - mn);
+        float ls = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) o[h][e] *= f;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const float p = exp2f(sc[i] - mn);
+          ls += p;
+          const T *pv = reinterpret_cast<const T *>(&vr[i]);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) o[h][e] = fmaf(p, to_f32<T>(pv[e]), o[h][e]);
+        }
+        // ls counts this lane's keys; the CPR lanes of a key row hold the same keys
+        lrun[h] = lrun[h] * f + ls;
+        mrun[h] = mn;
+      }
     }
   }
-  for (int x = tid; x < gm.G * D; x += 256) qf[x / D][x % D] = to_f32<T>(Q[((int64_t)b * gm.Hq + g * gm.G) * D + x]);
-  __syncthreads();
-  for (int hh = wave; hh < gm.G; hh += 4) {
-    float a = 0.f;
-#pragma unroll 8
-    for (int c = 0; c < D; ++c) a = fmaf(qf[hh][c], Kf[lane][c], a);
-    const float s = (t * 64 + lane) <= pos ? a * gm.scale : -INFINITY;
-    const float m = wave_max(s);
-    const float p = expf(s - m);
-    const float l = wave_sum(p);
-    ps[hh][lane] = p;
+  // reduce over the key-row groups of the wave (lanes with the same chunk)
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+#pragma unroll
+    for (int x = CPR; x < 64; x <<= 1) {
+      lrun[h] += __shfl_xor(lrun[h], x, 64);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) o[h][e] += __shfl_xor(o[h][e], x, 64);
+    }
     if (lane == 0) {
-      mls[hh][0] = m;
-      mls[hh][1] = l;
+      wm[wave][h] = mrun[h];
+      wl[wave][h] = lrun[h];
+    }
+    if (sub == 0) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) wo[wave][h][ch * VEC + e] = o[h][e];
     }
   }
   __syncthreads();
-  for (int x = tid; x < gm.G * D; x += 256) {
-    const int hh = x / D, c = x - hh * D;
-    float o = 0.f;
-#pragma unroll 8
-    for (int k = 0; k < 64; ++k) o = fmaf(ps[hh][k], Vf[k][c], o);
-    float *dst = part + (((int64_t)bg * gm.ksel + slot) * gm.G + hh) * (D + 2);
-    dst[c] = o / mls[hh][1];
-    if (c == 0) {
-      dst[D] = mls[hh][0];
-      dst[D + 1] = mls[hh][1];
-    }
-  }
-}
-
-template <typename T, int D>
-__global__ __launch_bounds__(256) void decode_combine_kernel(const int32_t *__restrict__ sel,
-                                                             const float *__restrict__ part, T *__restrict__ O,
-                                                             float *__restrict__ LSE, Geom gm) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int bg = blockIdx.x * 4 + wave;
-  if (bg >= gm.B * gm.Hkv) return;
-  const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
-  const int cur = gm.T - 1;
-  const int tl = lane < gm.ksel ? sel[(int64_t)bg * gm.ksel + lane] : -1;
-  const uint64_t valid = __ballot(tl >= 0 && tl <= cur && tl < gm.T);
-  for (int e = lane; e < gm.G * D; e += 64) {
-    const int hh = e / D, c = e - hh * D;
+  for (int x = tid; x < G * D; x += 256) {
+    const int h = x / D, c = x - h * D;
     float M = -INFINITY;
-    for (uint64_t v = valid; v; v &= v - 1) {
-      const int s = __ffsll((long long)v) - 1;
-      M = fmaxf(M, part[(((int64_t)bg * gm.ksel + s) * gm.G + hh) * (D + 2) + D]);
-    }
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, wm[w][h]);
     float L = 0.f, acc = 0.f;
-    for (uint64_t v = valid; v; v &= v - 1) {
-      const int s = __ffsll((long long)v) - 1;
-      const float *p = part + (((int64_t)bg * gm.ksel + s) * gm.G + hh) * (D + 2);
-      const float w = p[D + 1] * expf(p[D] - M);
-      L += w;
-      acc = fmaf(w, p[c], acc);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float f = wm[w][h] == -INFINITY ? 0.f : exp2f(wm[w][h] - M);
+      L = fmaf(f, wl[w][h], L);
+      acc = fmaf(f, wo[w][h][c], acc);
     }
-    O[((int64_t)b * gm.Hq + g * gm.G + hh) * D + c] = from_f32<T>(L > 0.f ? acc / L : 0.f);
-    if (c == 0) LSE[(int64_t)b * gm.Hq + g * gm.G + hh] = L > 0.f ? M + logf(L) : -INFINITY;
+    O[((int64_t)b * gm.Hq + g * G + h) * D + c] = from_f32<T>(L > 0.f ? acc / L : 0.f);
+    if (c == 0) LSE[(int64_t)b * gm.Hq + g * G + h] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
   }
 }
 
-template <typename T, int D>
-static hipError_t launch_decode_t(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc,
-                                  int32_t *sel, void *O, float *LSE, float *part, hipStream_t s) {
+template <typename T, int D, int G>
+static hipError_t launch_decode_g(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc,
+                                  int32_t *sel, void *O, float *LSE, hipStream_t s) {
   timing_begin("phsa_decode_select", s);
-  hipLaunchKernelGGL((decode_select_kernel<T, D>), dim3(g.B * g.Hkv), dim3(256), (size_t)g.T * sizeof(float), s,
+  hipLaunchKernelGGL((decode_select_kernel<T, D>), dim3(g.B * g.Hkv), dim3(512), (size_t)g.T * sizeof(float), s,
                      static_cast<const T *>(Q), Kc, sel, g);
   timing_end(s);
   timing_begin("phsa_decode_attn", s);
-  hipLaunchKernelGGL((decode_attn_kernel<T, D>), dim3(g.ksel, g.B * g.Hkv), dim3(256), 0, s,
-                     static_cast<const T *>(Q), static_cast<const T *>(K), static_cast<const T *>(V), sel, part, g);
-  timing_end(s);
-  timing_begin("phsa_decode_combine", s);
-  hipLaunchKernelGGL((decode_combine_kernel<T, D>), dim3((g.B * g.Hkv + 3) / 4), dim3(256), 0, s, sel, part,
-                     static_cast<T *>(O), LSE, g);
+  hipLaunchKernelGGL((decode_attn_kernel<T, D, G>), dim3(g.B * g.Hkv), dim3(256), 0, s, static_cast<const T *>(Q),
+                     static_cast<const T *>(K), static_cast<const T *>(V), sel, static_cast<T *>(O), LSE, g);
   timing_end(s);
   return hipGetLastError();
 }
 
+template <typename T, int D>
+static hipError_t launch_decode_t(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc,
+                                  int32_t *sel, void *O, float *LSE, hipStream_t s) {
+  switch (g.G) {
+    case 1: return launch_decode_g<T, D, 1>(g, Q, K, V, Kc, sel, O, LSE, s);
+    case 2: return launch_decode_g<T, D, 2>(g, Q, K, V, Kc, sel, O, LSE, s);
+    case 4: return launch_decode_g<T, D, 4>(g, Q, K, V, Kc, sel, O, LSE, s);
+    default: return launch_decode_g<T, D, 8>(g, Q, K, V, Kc, sel, O, LSE, s);
+  }
+}
+
 hipError_t launch_decode(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc, int32_t *sel,
-                         void *O, float *LSE, float *part, hipStream_t s) {
+                         void *O, float *LSE, hipStream_t s) {
   if (g.dtype == 0)
-    return g.d == 128 ? launch_decode_t<bf16_t, 128>(g, Q, K, V, Kc, sel, O, LSE, part, s)
-                      : launch_decode_t<bf16_t, 64>(g, Q, K, V, Kc, sel, O, LSE, part, s);
-  return g.d == 128 ? launch_decode_t<float, 128>(g, Q, K, V, Kc, sel, O, LSE, part, s)
-                    : launch_decode_t<float, 64>(g, Q, K, V, Kc, sel, O, LSE, part, s);
+    return g.d == 128 ? launch_decode_t<bf16_t, 128>(g, Q, K, V, Kc, sel, O, LSE, s)
+                      : launch_decode_t<bf16_t, 64>(g, Q, K, V, Kc, sel, O, LSE, s);
+  return g.d == 128 ? launch_decode_t<float, 128>(g, Q, K, V, Kc, sel, O, LSE, s)
+                    : launch_decode_t<float, 64>(g, Q, K, V, Kc, sel, O, LSE, s);
 }
 
 }  // namespace phsa

@@ -58,7 +58,7 @@ hipError_t launch_attn_fwd_fp32(const Geom &g, const float *Q, const float *K, c
 hipError_t launch_attn_bwd_fp32(const Geom &g, const float *Q, const float *K, const float *V,
                                 const float *O, const float *dO, const float *LSE, const int32_t *sel,
                                 float *dQ, float *dK, float *dV, float *Dvec, hipStream_t s);
-hipError_t launch_decode(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc,
-                         int32_t *sel, void *O, float *LSE, float *part, hipStream_t s);
+hipError_t launch_decode(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc, int32_t *sel,
+                         void *O, float *LSE, hipStream_t s);
 
 }  // namespace phsa

@@ -77,7 +77,7 @@ def test_ksel_and_workspace():
     assert fwd > 0 and fwd % 256 == 0
     assert phsa.workspace_size(_p(batch=2), phsa.OP_ATTN_FWD) > fwd
     assert phsa.workspace_size(_p(dtype=phsa.FP32), phsa.OP_ATTN_FWD) == 0
-    assert phsa.workspace_size(_p(seqlen_q=1), phsa.OP_DECODE) > 0
+    assert phsa.workspace_size(_p(seqlen_q=1), phsa.OP_DECODE) == 0          # decode needs no scratch
     assert phsa.workspace_size(_p(head_dim=96), phsa.OP_ATTN_FWD) == 0     # invalid -> 0
     assert L.phsa_validate(None, phsa.OP_SELECT) == phsa.ERR_NULL
 

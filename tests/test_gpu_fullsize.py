@@ -142,3 +142,35 @@ def test_decode_variants(L, window, n_init, top_k):
     o_r, lse_r = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, wl.block_size, scale)
     np.testing.assert_allclose(to_np(o), o_r, atol=O_TOL[wl.dtype], rtol=0)
     np.testing.assert_allclose(to_np(lse), lse_r, atol=O_TOL[wl.dtype], rtol=0)
+
+
+@pytest.mark.parametrize("kind,top_k,L", [("ties", 12, 32768), ("ties", 32, 131072), ("stripe", 20, 32768),
+                                          ("descending", 12, 65536)])
+def test_decode_select_structured(kind, top_k, L):
+    """Decode selection on hand-built representatives: exact ties (decided by block index),
+    winners concentrated in one residue class, monotone scores; up to T = 2048 blocks."""
+    log(f"[fullsize] decode selection {kind} k={top_k} L={L}")
+    B, Hq, Hkv, d, m = 4, 4, 2, 128, 64
+    T = L // m
+    g = torch.Generator().manual_seed(13)
+    q = torch.zeros(B, 1, Hq, d)
+    q[..., 0] = 0.5 + torch.rand(B, 1, Hq, generator=g)
+    q = q.to(torch.bfloat16)
+    t = torch.arange(T, dtype=torch.float64)
+    f = {"ties": torch.zeros(T, dtype=torch.float64),
+         "stripe": torch.where((t - 1) % 16 == 0, 1.0 + t / T, 0.5 * t / T),
+         "descending": 1.0 - t / T}[kind]
+    kc = torch.zeros(B, Hkv, T, d, dtype=torch.float32)
+    kc[..., 0] = f.float()
+    kv = torch.zeros(B, L, Hkv, d, dtype=torch.bfloat16)
+    cfg = phsa.Config(block_size=m, top_k=top_k, n_init_blocks=1, window=0)
+    sel, o, lse = phsa.decode(q.cuda(), kv.cuda(), kv.cuda(), kc.cuda(), cfg)
+    sel = sel.cpu().numpy()
+    scale = d ** -0.5
+    qh, kch = q.float().numpy(), kc.double().numpy()
+    ref, kth, gap = oracle.select(qh, kch, m, top_k, 1, 0, scale, L)
+    if kind == "ties":
+        np.testing.assert_array_equal(sel, ref)
+    else:
+        assert check_sel(sel, ref, kth, gap,
+                         lambda idx: oracle.score_row(qh, kch, m, scale, L, idx[0], idx[2], idx[1])) == 0
