@@ -62,7 +62,9 @@ size_t fwd_layout(const Geom &g, char *base, FwdWs *ws) {
   if (g.dtype == PHSA_FP32) return 0;
   FwdWs w{};
   size_t off = index_layout(g, base, &w.ix);
-  const int64_t slots = w.ix.nnz_max * g.G;  // partials in list order, one per (entry, head)
+  // partials in list order, one per (entry, head), plus one discard row that
+  // absorbs the stores of rows past the end of a chunk
+  const int64_t slots = w.ix.nnz_max * g.G + 1;
   w.opart = base ? base + off : nullptr;
   off += align_up(slots * g.d * elem_bytes(g));
   w.ml = base ? reinterpret_cast<float2 *>(base + off) : nullptr;
@@ -78,7 +80,7 @@ size_t bwd_layout(const Geom &g, char *base, BwdWs *ws) {
   w.Dvec = base ? reinterpret_cast<float *>(base + off) : nullptr;
   off += align_up(sizeof(float) * (size_t)g.B * g.Hq * g.Lq);
   if (g.dtype == PHSA_BF16) {
-    const int64_t slots = w.ix.nnz_max * g.G;
+    const int64_t slots = w.ix.nnz_max * g.G + 1;  // + the discard row
     w.dqpart = base ? base + off : nullptr;
     off += align_up(slots * g.d * elem_bytes(g));
     w.dkvpart = base ? reinterpret_cast<float *>(base + off) : nullptr;

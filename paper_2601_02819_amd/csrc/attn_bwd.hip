@@ -97,7 +97,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
-  const int32_t *list = ix.tok + ix.off[bgt] + e0;
+  // list position of the unit's first entry, read once (a load inside the chunk loop
+  // would make the wait for it also wait for the prefetched rows)
+  const int64_t list0 = (int64_t)ix.off[bgt] + e0;
+  const int32_t *list = ix.tok + list0;
   const int64_t krow0 = ((int64_t)b * gm.Lk + (int64_t)t * 64) * gm.Hkv + g;  // global row of key 0
 
   for (int x = tid; x < 64 * VPR; x += 256) {
@@ -144,7 +147,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       if (nrow >= 0) {
         const int i = nrow >> 6;
         const int h = g * G + tid % G;
-        plse = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + i] * kLog2e;
+        plse = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + i];  // scaled when staged, so nothing waits here
         pdd = Dvec[((int64_t)b * gm.Lq + i) * gm.Hq + h];
         ppos = gm.q_pos0 + i;
       } else {
@@ -171,7 +174,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       if (c == 0 && r % G == 0) ent_s[r / G] = pe[k];
     }
     if (tid < 64) {
-      lse_s[tid] = plse;
+      lse_s[tid] = plse * kLog2e;
       dd_s[tid] = pdd;
       pos_s[tid] = ppos;
     }
@@ -252,14 +255,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     }
     wave_lds_sync();
     {
-      const int64_t run0 = ((int64_t)ix.off[bgt] + e0 + c0) * G + wave * 16;  // first row of this wave
+      const int64_t run0 = (list0 + c0) * G + wave * 16;  // first row of this wave
       const int nrows = min(CT, n_ent - c0) * G - wave * 16;                // valid rows of this wave
+      // every lane stores (rows past the chunk's end go to the discard row), so the
+      // number of stores per chunk is fixed and the waits for the prefetched rows
+      // need not wait for them
+      const int64_t discard = (int64_t)ix.nnz_max * G;
 #pragma unroll
       for (int k = 0; k < 16 * VPR / 64; ++k) {
         const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
-        if (r < nrows)
-          *reinterpret_cast<uint4 *>(dqpart + (run0 + r) * D + cc) =
-              *reinterpret_cast<const uint4 *>(&Qs[(wave * 16 + r) * KPQ + cc]);
+        const int64_t row = r < nrows ? run0 + r : discard;
+        *reinterpret_cast<uint4 *>(dqpart + row * D + cc) =
+            *reinterpret_cast<const uint4 *>(&Qs[(wave * 16 + r) * KPQ + cc]);
       }
     }
   }

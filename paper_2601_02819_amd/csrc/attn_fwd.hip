@@ -60,7 +60,10 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
   const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
-  const int32_t *list = ix.tok + ix.off[bgt] + e0;
+  // list position of the unit's first entry, read once (a load inside the chunk loop
+  // would make the wait for it also wait for the prefetched rows)
+  const int64_t list0 = (int64_t)ix.off[bgt] + e0;
+  const int32_t *list = ix.tok + list0;
 
   for (int x = tid; x < 64 * VPR; x += 256) {
     const int kk = x / VPR, c = (x % VPR) * 8;
@@ -73,28 +76,28 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
   // lane (q, j) works on row j = l16 of the wave chunk: token j / G, head j % G
   const int hh = l16 % G;
   const int nch = (n_ent + TW - 1) / TW;
+  // Loads are issued unconditionally (rows past the list read its last entry,
+  // or query row 0): their results are masked, and a fixed number of loads per
+  // chunk lets the compiler wait for exactly the ones a chunk needs.
   auto entry = [&](int c) {
     const int tk = c * TW + l16 / G;
-    return (c < nch && tk < n_ent) ? list[tk] : -1;
+    const int v = list[min(tk, n_ent - 1)];
+    return tk < n_ent ? v : -1;
   };
   auto fetch = [&](int e, bf16x8 (&qf)[KB]) {
+    const int64_t row = e >= 0 ? (e >> 6) : 0;  // an empty chunk row is masked to zero weight
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
-      qf[kb] = e >= 0 ? load_bf16x8(Q + (((int64_t)b * gm.Lq + (e >> 6)) * gm.Hq + g * G + hh) * D + kb * 32 + kq)
-                      : __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+      qf[kb] = load_bf16x8(Q + (((int64_t)b * gm.Lq + row) * gm.Hq + g * G + hh) * D + kb * 32 + kq);
   };
 
   const float sl2 = gm.scale * kLog2e;
   const int key0 = t * 64;
-  int e_cur = entry(wave), e_nxt = entry(wave + 4);
-  bf16x8 qf[KB], qn[KB];
-  fetch(e_cur, qf);
+  // rows of discarded stores (past a chunk's end): one spare partial row
+  const int64_t discard = (int64_t)ix.nnz_max * G;
 
-  for (int c = wave; c < nch; c += 4) {
-    // next chunk's rows (and the entries of the one after) are in flight during this one
-    const int e_nn = entry(c + 8);
-    fetch(e_nxt, qn);
-
+  // one wave chunk: rows of list entry e (-1: none) with query fragments q
+  auto chunk = [&](int c, int e, const bf16x8 (&q)[KB]) {
     f32x4 st[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) st[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -102,8 +105,8 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
-        st[kt] = mfma16x16x32(load_bf16x8(&Ks[(kt * 16 + l16) * KP + kb * 32 + kq]), qf[kb], st[kt]);
-    const int pos = e_cur >= 0 ? gm.q_pos0 + (e_cur >> 6) : -1;
+        st[kt] = mfma16x16x32(load_bf16x8(&Ks[(kt * 16 + l16) * KP + kb * 32 + kq]), q[kb], st[kt]);
+    const int pos = e >= 0 ? gm.q_pos0 + (e >> 6) : -1;
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
@@ -139,9 +142,11 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
     }
     // The chunk's 16 partial rows are one contiguous run of the list-ordered
     // partial buffer (entries c*TW.., heads inner): stage them in LDS and write
-    // full 16-byte lanes.
-    const int64_t run0 = (int64_t)ix.off[bgt] + e0 + c * TW;  // list position of the chunk's first entry
-    if (e_cur >= 0 && q4 == 0) ml[(run0 + l16 / G) * G + hh] = make_float2(mx, l);
+    // full 16-byte lanes.  Every lane stores (unused lanes to the discard row),
+    // so a chunk issues a fixed number of stores and the waits for the
+    // prefetched rows need not wait for them.
+    const int64_t run0 = list0 + c * TW;  // list position of the chunk's first entry
+    ml[e >= 0 && q4 == 0 ? (run0 + l16 / G) * G + hh : discard] = make_float2(mx, l);
     bf16_t *os = Os[wave];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -154,14 +159,27 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
 #pragma unroll
     for (int k = 0; k < 16 * D / 8 / 64; ++k) {
       const int v = lane + 64 * k, r = v / (D / 8), cc = (v % (D / 8)) * 8;
-      if (r < nrows)
-        *reinterpret_cast<uint4 *>(opart + (run0 * G + r) * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
+      const int64_t row = r < nrows ? run0 * G + r : discard;
+      *reinterpret_cast<uint4 *>(opart + row * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
     }
     wave_lds_sync();
-    e_cur = e_nxt;
-    e_nxt = e_nn;
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) qf[kb] = qn[kb];
+  };
+
+  // Two register sets alternate: while one chunk computes, the next one's rows
+  // are in flight in the other set and the entries of the one after that too.
+  int e_a = entry(wave), e_b = entry(wave + 4);
+  bf16x8 qa[KB], qb[KB];
+  fetch(e_a, qa);
+  for (int c = wave; c < nch; c += 8) {
+    int e_n = entry(c + 8);
+    fetch(e_b, qb);
+    chunk(c, e_a, qa);
+    if (c + 4 >= nch) break;
+    e_a = e_n;
+    e_n = entry(c + 12);
+    fetch(e_a, qa);
+    chunk(c + 4, e_b, qb);
+    e_b = e_n;
   }
 }
 
