@@ -10,6 +10,8 @@ arithmetic inside the C library is IEEE double.  Citations refer to the paper
 "Punctuation-aware Hybrid Trainable Sparse Attention for Large Language
 Models" (arXiv 2601.02819):
 
+* ``punct_mask`` - the indicator I(x_i in P) of Eq. 7 (token id in the
+  punctuation set).
 * ``compress``  - Eq. 3 (blocks), Eq. 6 (global mean), Eq. 7 (punctuation
   mean and its no-punctuation fallback), Eq. 8 (gated fusion).
 * ``select``    - Eq. 8 relevance logits and Algorithm 1's block selection
@@ -49,11 +51,13 @@ def _load():
         _lib = ctypes.CDLL(_LIB_PATH)
         I, D, L, P = ctypes.c_int, ctypes.c_double, ctypes.c_int64, ctypes.c_void_p
         _lib.oracle_compress.argtypes = [I, I, I, I, I, D, P, P, P]
+        _lib.oracle_punct_mask.argtypes = [L, P, ctypes.c_int32, P, P]
         _lib.oracle_select.argtypes = [I] * 11 + [D, P, P, L, P, P, P, P]
         _lib.oracle_score_row.argtypes = [I] * 7 + [D, P, P, I, I, I, P]
         _lib.oracle_attn_fwd.argtypes = [I] * 9 + [D, P, P, P, P, L, P, P, P]
         _lib.oracle_attn_bwd.argtypes = [I] * 9 + [D, P, P, P, P, P, L, P, P, L, P, P, P]
-        for f in ("oracle_compress", "oracle_select", "oracle_score_row", "oracle_attn_fwd", "oracle_attn_bwd"):
+        for f in ("oracle_compress", "oracle_select", "oracle_score_row", "oracle_attn_fwd", "oracle_attn_bwd",
+                  "oracle_punct_mask"):
             getattr(_lib, f).restype = None
     return _lib
 
@@ -79,6 +83,15 @@ def _rows_arg(rows, total):
 def ksel(block_size: int, top_k: int, n_init: int, window: int) -> int:
     """Number of index slots per row: init + local (w/m + 1) + top-k."""
     return n_init + window // block_size + 1 + top_k
+
+
+def punct_mask(ids, punct_ids) -> np.ndarray:
+    """Token ids (any shape, int32) and the punctuation id set -> uint8 mask of the same shape."""
+    ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int32))
+    pid = np.ascontiguousarray(np.asarray(punct_ids, dtype=np.int32).reshape(-1))
+    out = np.empty(ids.shape, dtype=np.uint8)
+    _load().oracle_punct_mask(ids.size, _ptr(ids), int(pid.size), _ptr(pid), _ptr(out))
+    return out
 
 
 def compress(K, punct, block_size: int, lam: float) -> np.ndarray:

@@ -28,6 +28,20 @@
 #define IDX4(a, b, c, d_, B_, C_, D_) ((((int64_t)(a) * (B_) + (b)) * (C_) + (c)) * (D_) + (d_))
 
 /* ------------------------------------------------------------------------ */
+/* Punctuation indicator of Eq. 7 (Section 3.2, Punctuation Token Selection):
+ * mask[i] = I(x_i in P), the token id x_i compared with every id of the set
+ * P in turn.  ids [n], punct_ids [n_punct] in any order.                    */
+void oracle_punct_mask(int64_t n, const int32_t *ids, int32_t n_punct, const int32_t *punct_ids,
+                       uint8_t *mask) {
+  for (int64_t i = 0; i < n; ++i) {
+    uint8_t hit = 0;
+    for (int32_t j = 0; j < n_punct; ++j)
+      if (ids[i] == punct_ids[j]) hit = 1;
+    mask[i] = hit;
+  }
+}
+
+/* ------------------------------------------------------------------------ */
 /* Block representatives: global mean (Eq. 6), punctuation mean (Eq. 7),
  * gated fusion (Eq. 8), with the no-punctuation fallback M = M0 of Eq. 7 and
  * the "else" branch of Algorithm 1's representative-token step.            */
