@@ -115,6 +115,18 @@ size_t phsa_workspace_size(const phsa_params *p, int32_t op);
 /* Static, human-readable name of a status code. */
 const char *phsa_status_string(phsa_status s);
 
+/* Punctuation mask from token ids: mask[i] = 1 if ids[i] is one of the
+ * punctuation ids, else 0 (the indicator I(x_i in P) of Eq. 7, Section 3.2
+ * "Punctuation Token Selection").  ids and mask hold n_tokens entries of any
+ * shape (e.g. [B, Lk], the layout phsa_compress reads); punct_ids holds the
+ * set P and must be sorted ascending (duplicates are allowed).  All device
+ * pointers.  n_punct may be 0 (no token is punctuation) and at most
+ * PHSA_MAX_PUNCT_IDS (PHSA_ERR_UNSUPPORTED beyond).  Building P from a
+ * tokenizer's vocabulary is the caller's part. */
+#define PHSA_MAX_PUNCT_IDS 16384
+phsa_status phsa_punct_mask(const int32_t *ids, int64_t n_tokens, const int32_t *punct_ids, int32_t n_punct,
+                            uint8_t *mask, void *stream);
+
 /* Block representatives (Eq. 6-8, Algorithm 1 representative-token step).
  * Reads K [B, Lk, Hkv, d] and punct [B, Lk]; writes K_comp [B, Hkv, T, d]
  * (float32, sums accumulated in float32).  Uses seqlen_k, not seqlen_q. */

@@ -257,6 +257,17 @@ phsa_status phsa_compress(const phsa_params *p, const void *K, const uint8_t *pu
   })
 }
 
+phsa_status phsa_punct_mask(const int32_t *ids, int64_t n_tokens, const int32_t *punct_ids, int32_t n_punct,
+                            uint8_t *mask, void *stream) {
+  PHSA_GUARD({
+    if (n_tokens < 0 || n_punct < 0) return PHSA_ERR_INVALID_ARG;
+    if (n_punct > PHSA_MAX_PUNCT_IDS) return PHSA_ERR_UNSUPPORTED;
+    if (n_tokens > 0 && (!ids || !mask)) return PHSA_ERR_NULL;
+    if (n_punct > 0 && !punct_ids) return PHSA_ERR_NULL;
+    return from_hip(launch_punct_mask(ids, n_tokens, punct_ids, n_punct, mask, static_cast<hipStream_t>(stream)));
+  })
+}
+
 phsa_status phsa_select(const phsa_params *p, const void *Q, const float *K_comp, int32_t *sel, void *ws,
                         size_t ws_bytes, void *stream) {
   PHSA_GUARD({

@@ -41,6 +41,8 @@ constexpr int kIndexTile = 256;  // query rows per index-building workgroup
 void timing_begin(const char *name, hipStream_t s);
 void timing_end(hipStream_t s);
 
+hipError_t launch_punct_mask(const int32_t *ids, int64_t n, const int32_t *pset, int n_punct, uint8_t *mask,
+                             hipStream_t s);
 hipError_t launch_compress(const Geom &g, const void *K, const uint8_t *punct, float *Kc, hipStream_t s);
 // ws: select_split_bytes(g) bytes (bf16 hi/lo copies of K_comp), unused for float32
 size_t select_split_bytes(const Geom &g);

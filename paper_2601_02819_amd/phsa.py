@@ -21,8 +21,10 @@ BF16, FP32 = 0, 1
 OP_COMPRESS, OP_SELECT, OP_ATTN_FWD, OP_ATTN_BWD, OP_FORWARD, OP_DECODE = range(6)
 FLAG_REUSE_INDEX = 1
 
+MAX_PUNCT_IDS = 16384
+
 EXPORTS = (
-    "phsa_ksel", "phsa_validate", "phsa_workspace_size", "phsa_status_string", "phsa_compress",
+    "phsa_ksel", "phsa_validate", "phsa_workspace_size", "phsa_status_string", "phsa_punct_mask", "phsa_compress",
     "phsa_select", "phsa_attn_fwd", "phsa_attn_bwd", "phsa_forward", "phsa_decode",
     "phsa_timing_enable", "phsa_timing_collect", "phsa_timing_reset",
 )
@@ -60,6 +62,7 @@ def lib():
             "phsa_validate": (ctypes.c_int, [P, ctypes.c_int32]),
             "phsa_workspace_size": (ctypes.c_size_t, [P, ctypes.c_int32]),
             "phsa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+            "phsa_punct_mask": (ctypes.c_int, [PP, ctypes.c_int64, PP, ctypes.c_int32, PP, PP]),
             "phsa_compress": (ctypes.c_int, [P, PP, PP, PP, PP]),
             "phsa_select": (ctypes.c_int, [P, PP, PP, PP, PP, ctypes.c_size_t, PP]),
             "phsa_attn_fwd": (ctypes.c_int, [P, PP, PP, PP, PP, PP, PP, PP, ctypes.c_size_t, PP]),
@@ -135,6 +138,31 @@ def _workspace(p: Params, op: int, ws: Optional[torch.Tensor], device) -> Option
     if ws is not None and ws.numel() >= need:
         return ws
     return torch.empty(need, dtype=torch.uint8, device=device)
+
+
+def punct_mask(ids: torch.Tensor, punct_ids) -> torch.Tensor:
+    """Token ids (int32 device tensor, any shape) -> uint8 punctuation mask of the same shape.
+
+    punct_ids: the punctuation id set, as a host sequence (sorted and uploaded
+    here) or an int32 device tensor already sorted ascending."""
+    _dev(ids)
+    if ids.dtype != torch.int32:
+        raise ValueError("ids must be int32")
+    if isinstance(punct_ids, torch.Tensor) and punct_ids.is_cuda:
+        pset = punct_ids.contiguous()
+        if pset.dtype != torch.int32:
+            raise ValueError("punct_ids must be int32")
+    else:
+        import numpy as np
+        host = np.unique(np.asarray(list(punct_ids) if not isinstance(punct_ids, torch.Tensor) else punct_ids.numpy(),
+                                    dtype=np.int64))
+        if host.size and (host[0] < -2**31 or host[-1] >= 2**31):
+            raise ValueError("punctuation ids must fit int32")
+        pset = torch.from_numpy(host.astype(np.int32)).to(ids.device)
+    mask = torch.empty(ids.shape, dtype=torch.uint8, device=ids.device)
+    _check(lib().phsa_punct_mask(_ptr(ids), ids.numel(), _ptr(pset) if pset.numel() else None, pset.numel(),
+                                 _ptr(mask), _stream()), "phsa_punct_mask")
+    return mask
 
 
 def compress(k: torch.Tensor, punct: torch.Tensor, cfg: Config) -> torch.Tensor:

@@ -100,6 +100,17 @@ def test_entry_points_reject_before_launch():
     assert L.phsa_decode(ctypes.byref(good), *([bogus] * 7), None, 0, None) == phsa.ERR_SHAPE  # Lq != 1
 
 
+def test_punct_mask_rejects_before_launch():
+    L = phsa.lib()
+    bogus = ctypes.c_void_p(0x1000)
+    assert L.phsa_punct_mask(bogus, -1, bogus, 1, bogus, None) == phsa.ERR_INVALID_ARG
+    assert L.phsa_punct_mask(bogus, 10, bogus, -3, bogus, None) == phsa.ERR_INVALID_ARG
+    assert L.phsa_punct_mask(bogus, 10, bogus, phsa.MAX_PUNCT_IDS + 1, bogus, None) == phsa.ERR_UNSUPPORTED
+    assert L.phsa_punct_mask(None, 10, bogus, 1, bogus, None) == phsa.ERR_NULL
+    assert L.phsa_punct_mask(bogus, 10, None, 1, bogus, None) == phsa.ERR_NULL
+    assert L.phsa_punct_mask(None, 0, None, 0, None, None) == phsa.OK     # nothing to do, nothing launched
+
+
 def test_status_strings():
     for s in range(8):
         assert isinstance(phsa.status_string(s), str) and phsa.status_string(s)

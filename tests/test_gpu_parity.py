@@ -234,3 +234,39 @@ def test_select_structured_scores(kind, top_k):
         np.testing.assert_array_equal(sel, ref)
     else:
         assert check_sel(sel, ref, kth, gap, score_fn) == 0
+
+
+def test_punct_mask_matches_oracle():
+    """Token ids -> punctuation mask (the indicator of Eq. 7) against the oracle, then into compress."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "worked_example.json")))
+    ids = torch.tensor(g["token_ids"], dtype=torch.int32, device="cuda")
+    assert phsa.punct_mask(ids, g["punctuation_ids"]).cpu().tolist() == g["expected_mask"]
+
+    gen = torch.Generator().manual_seed(21)
+    vocab = 151936
+    ids = torch.randint(0, vocab, (4, 32768), generator=gen, dtype=torch.int32)
+    pset = torch.randperm(vocab, generator=gen)[:60].to(torch.int32)
+    ids[0, ::7] = pset[torch.randint(0, 60, (ids[0, ::7].numel(),), generator=gen)]   # plenty of hits
+    want = oracle.punct_mask(ids.numpy(), pset.numpy())
+    got = phsa.punct_mask(ids.cuda(), pset.tolist())
+    assert np.array_equal(got.cpu().numpy(), want)
+    # device set (sorted), ragged and misaligned views, empty set
+    dset = torch.sort(pset).values.cuda()
+    flat = ids.reshape(-1).cuda()
+    for view in (flat[1:], flat[:1001], flat[3:3 + 4097]):
+        v = view.contiguous() if view.storage_offset() % 4 == 0 else view
+        got = phsa.punct_mask(v, dset)
+        assert np.array_equal(got.cpu().numpy(), oracle.punct_mask(v.cpu().numpy(), pset.numpy()))
+    assert int(phsa.punct_mask(flat, []).sum()) == 0
+    # the mask feeds compress exactly like a stored one
+    wl = small("punct_ids", 1, 1024, 4, 2, 128, 3, 1, 0)
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 3, with_grad_out=False)
+    tok = torch.randint(0, vocab, (1, 1024), generator=gen, dtype=torch.int32)
+    mask = phsa.punct_mask(tok.cuda(), pset.tolist())
+    kc = phsa.compress(dev["k"], mask, cfg)
+    torch.cuda.synchronize()
+    kc_ref = oracle.compress(host["k"].float().numpy(), oracle.punct_mask(tok.numpy(), pset.numpy()), 64, wl.lam)
+    np.testing.assert_allclose(to_np(kc), kc_ref, atol=1e-5, rtol=1e-5)
