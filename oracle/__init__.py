@@ -106,8 +106,10 @@ def compress(K, punct, block_size: int, lam: float) -> np.ndarray:
 
 
 def select(Q, Kc, block_size: int, top_k: int, n_init: int, window: int, scale: float,
-           seqlen_k: int, rows=None):
-    """Q [B, Lq, Hq, d], Kc [B, Hkv, T, d] float64.
+           seqlen_k: int, rows=None, q_pos0=None):
+    """Q [B, Lq, Hq, d], Kc [B, Hkv, T, d] float64.  Query row i sits at position
+    q_pos0 + i (default seqlen_k - Lq); seqlen_k must cover whole blocks up to
+    the last query's own block.
 
     Returns (sel, kth, gap).  With rows=None: sel [B, Hkv, Lq, Ksel] and
     kth/gap [B, Hkv, Lq].  With rows (flat b*Lq + i): sel [n, Hkv, Ksel],
@@ -122,8 +124,9 @@ def select(Q, Kc, block_size: int, top_k: int, n_init: int, window: int, scale: 
     sel = np.empty((n, Hkv, ks), dtype=np.int32)
     kth = np.empty((n, Hkv), dtype=np.float64)
     gap = np.empty((n, Hkv), dtype=np.float64)
+    pos0 = seqlen_k - Lq if q_pos0 is None else int(q_pos0)
     _load().oracle_select(B, Lq, seqlen_k, Hq, Hkv, d, block_size, top_k, n_init, window,
-                          seqlen_k - Lq, float(scale), _ptr(Q), _ptr(Kc), n, _ptr(r), _ptr(sel),
+                          pos0, float(scale), _ptr(Q), _ptr(Kc), n, _ptr(r), _ptr(sel),
                           _ptr(kth), _ptr(gap))
     if rows is None:
         sel = sel.reshape(B, Lq, Hkv, ks).transpose(0, 2, 1, 3).copy()
@@ -144,11 +147,12 @@ def score_row(Q, Kc, block_size: int, scale: float, seqlen_k: int, b: int, i: in
     return out
 
 
-def attn_fwd(Q, K, V, sel, block_size: int, scale: float, rows=None):
+def attn_fwd(Q, K, V, sel, block_size: int, scale: float, rows=None, q_pos0=None):
     """Sparse attention forward.  sel [B, Hkv, Lq, Ksel] int32.
 
     Returns (O, LSE): with rows=None O [B, Lq, Hq, d], LSE [B, Hq, Lq];
-    with rows (flat b*Lq + i) O [n, Hq, d], LSE [n, Hq].
+    with rows (flat b*Lq + i) O [n, Hq, d], LSE [n, Hq].  Query row i sits at
+    position q_pos0 + i (default Lk - Lq); keys past it are never read.
     """
     Q, K, V = _f32(Q), _f32(K), _f32(V)
     sel = np.ascontiguousarray(np.asarray(sel, dtype=np.int32))
@@ -158,7 +162,8 @@ def attn_fwd(Q, K, V, sel, block_size: int, scale: float, rows=None):
     n, r = _rows_arg(rows, B * Lq)
     O = np.empty((n, Hq, d), dtype=np.float64)
     LSE = np.empty((n, Hq), dtype=np.float64)
-    _load().oracle_attn_fwd(B, Lq, Lk, Hq, Hkv, d, block_size, ks, Lk - Lq, float(scale), _ptr(Q), _ptr(K),
+    pos0 = Lk - Lq if q_pos0 is None else int(q_pos0)
+    _load().oracle_attn_fwd(B, Lq, Lk, Hq, Hkv, d, block_size, ks, pos0, float(scale), _ptr(Q), _ptr(K),
                             _ptr(V), _ptr(sel), n, _ptr(r), _ptr(O), _ptr(LSE))
     if rows is None:
         O = O.reshape(B, Lq, Hq, d)
