@@ -222,6 +222,59 @@ def bench_decode(iters: int, seed: int):
             "timing": f"{iters} steps rotating {R} query sets and {R} copies of the representatives"}
 
 
+def bench_generation(iters: int, seed: int):
+    """One generation step with per-sequence cache lengths: append a token to every
+    sequence's block cache (maintaining the representative of a block it completes),
+    then decode it.  64 sequences, 32k capacity, lengths 30000-32700."""
+    wl = WORKLOADS["decode_32k"]
+    cfg = cfg_of(wl)
+    B, cap, Hq, Hkv, d = wl.batch, wl.seqlen_k, wl.n_heads_q, wl.n_heads_kv, wl.head_dim
+    host = make_inputs(wl, seed, with_grad_out=False)
+    k, v, punct = host["k"].cuda(), host["v"].cuda(), host["punct"].cuda()
+    kc = phsa.compress(k, punct, cfg)
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(seed + 2)
+    clen = torch.randint(30000, 32700, (B,), generator=gen, dtype=torch.int32).cuda()
+    R = 4
+    qs = [torch.randn(B, 1, Hq, d, generator=gen).to(torch.bfloat16).cuda() for _ in range(R)]
+    kn = [torch.randn(B, Hkv, d, generator=gen).to(torch.bfloat16).cuda() for _ in range(R)]
+    vn = [torch.randn(B, Hkv, d, generator=gen).to(torch.bfloat16).cuda() for _ in range(R)]
+    pn = [(torch.rand(B, generator=gen) < 0.08).to(torch.uint8).cuda() for _ in range(R)]
+    for r in range(R):
+        phsa.cache_append(kn[r], vn[r], pn[r], k, v, punct, clen, kc, cfg)
+        phsa.decode_varlen(qs[r], k, v, kc, clen, cfg)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for i in range(iters):
+        phsa.cache_append(kn[i % R], vn[i % R], pn[i % R], k, v, punct, clen, kc, cfg)
+        phsa.decode_varlen(qs[i % R], k, v, kc, clen, cfg)
+    ev1.record()
+    torch.cuda.synchronize()
+    return {"workload": "64 sequences, 32k-token block caches at lengths 30000-32700: append one token "
+                        "(block representative maintained) + decode it", "ms_per_step": ev0.elapsed_time(ev1) / iters}
+
+
+def bench_punct(seed: int):
+    """Token ids -> punctuation mask for the 4 x 32768 training batch (60 punctuation ids)."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(seed + 3)
+    ids = torch.randint(0, 151936, (4, 32768), generator=gen, dtype=torch.int32).cuda()
+    pset = torch.sort(torch.randperm(151936, generator=gen)[:60].to(torch.int32)).values.cuda()
+    for _ in range(3):
+        phsa.punct_mask(ids, pset)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(50):
+        phsa.punct_mask(ids, pset)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / 50
+    nbytes = ids.numel() * 5
+    return {"workload": "4 x 32768 token ids, 60 punctuation ids", "ms": ms, "GB_per_s": nbytes / 1e9 / (ms / 1e3)}
+
+
 def cpu_baseline(host, wl, prefix: int):
     """The fp64 oracle on a causal prefix of batch 0 (all heads): a complete PHSA
     sub-problem, timed end to end (compress, select, forward, backward)."""
@@ -325,6 +378,8 @@ def main():
     }
     if not args.no_decode:
         result["decode"] = bench_decode(40, args.seed)
+        result["generation_step"] = bench_generation(40, args.seed)
+        result["punct_mask"] = bench_punct(args.seed)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(tr["host"], WORKLOADS["train_32k"], args.cpu_prefix)
     print(json.dumps(result))

@@ -172,6 +172,34 @@ phsa_status phsa_decode(const phsa_params *p, const void *Q, const void *K_cache
                         const void *V_cache, const float *K_comp, int32_t *sel, void *O,
                         float *LSE, void *ws, size_t ws_bytes, void *stream);
 
+/* Generation with per-sequence cache lengths.  The caches have capacity
+ * Lk = p->seqlen_k tokens (a multiple of block_size): K_cache, V_cache
+ * [B, Lk, Hkv, d], punct_cache [B, Lk], K_comp [B, Hkv, Lk / m, d];
+ * cache_len [B] (device int32) holds the number of valid tokens of each
+ * sequence.  Validation is that of phsa_decode (seqlen_q must be 1).
+ *
+ * phsa_cache_append: one new token per sequence, K_new and V_new [B, Hkv, d],
+ * punct_new [B], is written at position cache_len[b], and cache_len[b] grows
+ * by one.  When the token completes block t = cache_len[b] / m (old length),
+ * the block's representative (Eq. 6-8, as phsa_compress computes it) is
+ * written to K_comp[b, :, t]; no other block is touched ("block-level
+ * key-value caching", Section 3.2 "Block Segmentation").  A sequence whose
+ * cache is full (cache_len[b] >= Lk) is left unchanged.
+ *
+ * phsa_decode_varlen: as phsa_decode, but sequence b's query sits at position
+ * cache_len[b] - 1 (lengths are clamped to [1, Lk]).  Its own block may be
+ * partly written: it is always selected (forced), and keys past the query are
+ * masked without their values being read.  Only complete blocks are scored,
+ * so K_comp must hold the representatives of every complete block below the
+ * query's own (phsa_compress on the prefilled prefix, then phsa_cache_append). */
+phsa_status phsa_decode_varlen(const phsa_params *p, const void *Q, const void *K_cache,
+                               const void *V_cache, const float *K_comp, const int32_t *cache_len,
+                               int32_t *sel, void *O, float *LSE, void *ws, size_t ws_bytes,
+                               void *stream);
+phsa_status phsa_cache_append(const phsa_params *p, const void *K_new, const void *V_new,
+                              const uint8_t *punct_new, void *K_cache, void *V_cache,
+                              uint8_t *punct_cache, int32_t *cache_len, float *K_comp, void *stream);
+
 /* Profiling aid (off by default, not thread-safe): while enabled, every
  * kernel launch is bracketed by a pair of HIP events on its stream.
  * phsa_timing_collect synchronises those events and returns, for the kernel

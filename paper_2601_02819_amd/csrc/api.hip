@@ -351,7 +351,36 @@ phsa_status phsa_decode(const phsa_params *p, const void *Q, const void *K_cache
     if (st != PHSA_OK) return st;
     if (!Q || !K_cache || !V_cache || !K_comp || !sel || !O || !LSE) return PHSA_ERR_NULL;
     if ((st = check_ws(g, PHSA_OP_DECODE, ws, ws_bytes)) != PHSA_OK) return st;
-    return from_hip(launch_decode(g, Q, K_cache, V_cache, K_comp, sel, O, LSE, static_cast<hipStream_t>(stream)));
+    return from_hip(
+        launch_decode(g, Q, K_cache, V_cache, K_comp, nullptr, sel, O, LSE, static_cast<hipStream_t>(stream)));
+  })
+}
+
+phsa_status phsa_decode_varlen(const phsa_params *p, const void *Q, const void *K_cache, const void *V_cache,
+                               const float *K_comp, const int32_t *cache_len, int32_t *sel, void *O, float *LSE,
+                               void *ws, size_t ws_bytes, void *stream) {
+  PHSA_GUARD({
+    Geom g;
+    phsa_status st = validate(p, PHSA_OP_DECODE, &g);
+    if (st != PHSA_OK) return st;
+    if (!Q || !K_cache || !V_cache || !K_comp || !cache_len || !sel || !O || !LSE) return PHSA_ERR_NULL;
+    if ((st = check_ws(g, PHSA_OP_DECODE, ws, ws_bytes)) != PHSA_OK) return st;
+    return from_hip(
+        launch_decode(g, Q, K_cache, V_cache, K_comp, cache_len, sel, O, LSE, static_cast<hipStream_t>(stream)));
+  })
+}
+
+phsa_status phsa_cache_append(const phsa_params *p, const void *K_new, const void *V_new, const uint8_t *punct_new,
+                              void *K_cache, void *V_cache, uint8_t *punct_cache, int32_t *cache_len, float *K_comp,
+                              void *stream) {
+  PHSA_GUARD({
+    Geom g;
+    phsa_status st = validate(p, PHSA_OP_DECODE, &g);
+    if (st != PHSA_OK) return st;
+    if (!K_new || !V_new || !punct_new || !K_cache || !V_cache || !punct_cache || !cache_len || !K_comp)
+      return PHSA_ERR_NULL;
+    return from_hip(launch_cache_append(g, K_new, V_new, punct_new, K_cache, V_cache, punct_cache, cache_len, K_comp,
+                                        static_cast<hipStream_t>(stream)));
   })
 }
 

@@ -13,6 +13,10 @@
 //   decode_attn   : one workgroup per (b, g) streams its selected K/V blocks
 //                   with coalesced 16-byte loads, keeps a running softmax per
 //                   wave and merges the waves in LDS: O and LSE directly.
+// With per-sequence cache lengths (phsa_decode_varlen) sequence b's query sits
+// at position len[b] - 1; its own block may be partly written, and keys past
+// the query are masked without reading their values.  cache_append adds one
+// token per sequence and maintains the block representatives.
 #include <float.h>
 #include <math.h>
 
@@ -63,8 +67,15 @@ __device__ __forceinline__ void wave_merge_best_first(float &rs, int &rt, float 
   }
 }
 
+// Cache length of sequence b: clen[b] clamped to [1, capacity], or the
+// uniform Lk when no length array is given.
+__device__ __forceinline__ int seq_len(const int32_t *clen, int b, const Geom &gm) {
+  return clen ? min(max(clen[b], 1), gm.Lk) : gm.Lk;
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(512) void decode_select_kernel(const T *__restrict__ Q, const float *__restrict__ Kc,
+                                                            const int32_t *__restrict__ clen,
                                                             int32_t *__restrict__ sel, Geom gm) {
   constexpr int LPR = D / 4;      // lanes per representative row (one float4 each)
   constexpr int RPW = 64 / LPR;   // rows per wave load instruction
@@ -81,7 +92,7 @@ __global__ __launch_bounds__(512) void decode_select_kernel(const T *__restrict_
 #pragma unroll
     for (int e = 0; e < 4; ++e) q[e] += to_f32<T>(src[e]);
   }
-  const int cur = gm.T - 1;
+  const int cur = (seq_len(clen, b, gm) - 1) / gm.m;  // the query's own block
   const int lo = max(0, cur - gm.window / gm.m);
   const float *kc = Kc + (int64_t)bg * gm.T * D;
   for (int t0 = gm.n_init + wave * RPW * U; t0 < lo; t0 += 8 * RPW * U) {
@@ -147,8 +158,9 @@ __global__ __launch_bounds__(512) void decode_select_kernel(const T *__restrict_
 // the four are merged through LDS and O, LSE written directly.
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256, 2) void decode_attn_kernel(const T *__restrict__ Q, const T *__restrict__ K,
-                                                          const T *__restrict__ V, const int32_t *__restrict__ sel,
-                                                          T *__restrict__ O, float *__restrict__ LSE, Geom gm) {
+                                                          const T *__restrict__ V, const int32_t *__restrict__ clen,
+                                                          const int32_t *__restrict__ sel, T *__restrict__ O,
+                                                          float *__restrict__ LSE, Geom gm) {
   constexpr int VEC = 16 / sizeof(T);   // elements per 16-byte chunk
   constexpr int CPR = D / VEC;          // chunks (lanes) per key row
   constexpr int KPI = 64 / CPR;         // key rows per load instruction
@@ -176,7 +188,7 @@ __global__ __launch_bounds__(256, 2) void decode_attn_kernel(const T *__restrict
 #pragma unroll
     for (int e = 0; e < VEC; ++e) o[h][e] = 0.f;
   }
-  const int cur = gm.T - 1, pos = gm.Lk - 1;
+  const int pos = seq_len(clen, b, gm) - 1, cur = pos / gm.m;
   for (int s = wave; s < gm.ksel; s += 4) {
     const int t = sel[(int64_t)bg * gm.ksel + s];
     if (t < 0 || t > cur || t >= gm.T) continue;  // wave-uniform
@@ -207,17 +219,22 @@ __global__ __launch_bounds__(256, 2) void decode_attn_kernel(const T *__restrict
 #pragma unroll
         for (int x = CPR; x < 64; x <<= 1) bm = fmaxf(bm, __shfl_xor(bm, x, 64));
         const float mn = fmaxf(mrun[h], bm);
-        const float f = exp2f(mrun[h] - mn);
+        // mn stays -inf only while every key so far was past the query (a partly
+        // written own block): nothing has been accumulated yet
+        const float f = mn == -INFINITY ? 1.f : exp2f(mrun[h] - mn);
         float ls = 0.f;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) o[h][e] *= f;
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
-          const float p = exp2f(sc[i] - mn);
+          // keys past the query (the unwritten tail of its own block) add nothing,
+          // whatever their V slots hold
+          const bool valid = (t * 64 + k0 + i * KPI + sub) <= pos;
+          const float p = valid ? exp2f(sc[i] - mn) : 0.f;
           ls += p;
           const T *pv = reinterpret_cast<const T *>(&vr[i]);
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) o[h][e] = fmaf(p, to_f32<T>(pv[e]), o[h][e]);
+          for (int e = 0; e < VEC; ++e) o[h][e] = valid ? fmaf(p, to_f32<T>(pv[e]), o[h][e]) : o[h][e];
         }
         // ls counts this lane's keys; the CPR lanes of a key row hold the same keys
         lrun[h] = lrun[h] * f + ls;
@@ -263,36 +280,146 @@ __global__ __launch_bounds__(256, 2) void decode_attn_kernel(const T *__restrict
 
 template <typename T, int D, int G>
 static hipError_t launch_decode_g(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc,
-                                  int32_t *sel, void *O, float *LSE, hipStream_t s) {
+                                  const int32_t *clen, int32_t *sel, void *O, float *LSE, hipStream_t s) {
   timing_begin("phsa_decode_select", s);
   hipLaunchKernelGGL((decode_select_kernel<T, D>), dim3(g.B * g.Hkv), dim3(512), (size_t)g.T * sizeof(float), s,
-                     static_cast<const T *>(Q), Kc, sel, g);
+                     static_cast<const T *>(Q), Kc, clen, sel, g);
   timing_end(s);
   timing_begin("phsa_decode_attn", s);
   hipLaunchKernelGGL((decode_attn_kernel<T, D, G>), dim3(g.B * g.Hkv), dim3(256), 0, s, static_cast<const T *>(Q),
-                     static_cast<const T *>(K), static_cast<const T *>(V), sel, static_cast<T *>(O), LSE, g);
+                     static_cast<const T *>(K), static_cast<const T *>(V), clen, sel, static_cast<T *>(O), LSE, g);
   timing_end(s);
   return hipGetLastError();
 }
 
 template <typename T, int D>
 static hipError_t launch_decode_t(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc,
-                                  int32_t *sel, void *O, float *LSE, hipStream_t s) {
+                                  const int32_t *clen, int32_t *sel, void *O, float *LSE, hipStream_t s) {
   switch (g.G) {
-    case 1: return launch_decode_g<T, D, 1>(g, Q, K, V, Kc, sel, O, LSE, s);
-    case 2: return launch_decode_g<T, D, 2>(g, Q, K, V, Kc, sel, O, LSE, s);
-    case 4: return launch_decode_g<T, D, 4>(g, Q, K, V, Kc, sel, O, LSE, s);
-    default: return launch_decode_g<T, D, 8>(g, Q, K, V, Kc, sel, O, LSE, s);
+    case 1: return launch_decode_g<T, D, 1>(g, Q, K, V, Kc, clen, sel, O, LSE, s);
+    case 2: return launch_decode_g<T, D, 2>(g, Q, K, V, Kc, clen, sel, O, LSE, s);
+    case 4: return launch_decode_g<T, D, 4>(g, Q, K, V, Kc, clen, sel, O, LSE, s);
+    default: return launch_decode_g<T, D, 8>(g, Q, K, V, Kc, clen, sel, O, LSE, s);
   }
 }
 
-hipError_t launch_decode(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc, int32_t *sel,
-                         void *O, float *LSE, hipStream_t s) {
+// ---------------------------------------------------------------- cache append
+// One token per sequence joins the cache at position len[b]; the length grows
+// by one.  When the token completes block t, that block's representative is
+// computed from the cache (Eq. 6-8, the same pooling as phsa_compress) and
+// written to K_comp[b, :, t].  One workgroup per sequence; a sequence whose
+// cache is full is left unchanged.  Rows move in 16-byte chunks; for the
+// pooling, the Hkv*d elements are split into 16-byte chunks and the block's m
+// keys into 256 / #chunks slices, whose partial sums meet in LDS.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void cache_append_kernel(const T *__restrict__ Kn, const T *__restrict__ Vn,
+                                                           const uint8_t *__restrict__ pn, T *__restrict__ Kcache,
+                                                           T *__restrict__ Vcache, uint8_t *__restrict__ pcache,
+                                                           int32_t *__restrict__ clen, float *__restrict__ Kc,
+                                                           Geom gm) {
+  constexpr int VEC = 16 / sizeof(T);
+  __shared__ float red[2][256][VEC];
+  __shared__ int npun;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int pos = clen[b];
+  if (pos < 0 || pos >= gm.Lk) return;  // full (or invalid): nothing changes
+  const int HD = gm.Hkv * D, NCH = HD / VEC;
+  for (int x = tid; x < NCH; x += 256) {
+    const int64_t dst = ((int64_t)b * gm.Lk + pos) * HD + x * VEC;
+    *reinterpret_cast<uint4 *>(Kcache + dst) = *reinterpret_cast<const uint4 *>(Kn + (int64_t)b * HD + x * VEC);
+    *reinterpret_cast<uint4 *>(Vcache + dst) = *reinterpret_cast<const uint4 *>(Vn + (int64_t)b * HD + x * VEC);
+  }
+  if (tid == 0) pcache[(int64_t)b * gm.Lk + pos] = pn[b];
+  if ((pos + 1) % gm.m == 0) {
+    // the block is complete: pool its m keys (the newest one from the input,
+    // the others from the cache, which this launch does not write)
+    const int t = pos / gm.m, j0 = t * gm.m;
+    if (tid == 0) {
+      int c = 0;
+      for (int j = j0; j < j0 + gm.m; ++j) c += (j == pos ? pn[b] : pcache[(int64_t)b * gm.Lk + j]) != 0;
+      npun = c;
+    }
+    for (int x0 = 0; x0 < NCH; x0 += 256) {
+      const int nch = min(256, NCH - x0);       // chunks handled in this pass
+      const int slices = 256 / nch;             // key slices
+      const int ch = tid % nch, sl = tid / nch;
+      float sum[VEC], psum[VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) sum[e] = psum[e] = 0.f;
+      if (sl < slices) {
+        for (int j = j0 + sl; j < j0 + gm.m; j += slices) {
+          const bool newest = j == pos;
+          const uint4 raw = newest ? *reinterpret_cast<const uint4 *>(Kn + (int64_t)b * HD + (x0 + ch) * VEC)
+                                   : *reinterpret_cast<const uint4 *>(Kcache + ((int64_t)b * gm.Lk + j) * HD +
+                                                                      (x0 + ch) * VEC);
+          const bool pj = (newest ? pn[b] : pcache[(int64_t)b * gm.Lk + j]) != 0;
+          const T *pv = reinterpret_cast<const T *>(&raw);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            const float k = to_f32<T>(pv[e]);
+            sum[e] += k;
+            psum[e] += pj ? k : 0.f;
+          }
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        red[0][tid][e] = sum[e];
+        red[1][tid][e] = psum[e];
+      }
+      __syncthreads();
+      if (tid < nch) {
+        const int np = npun;
+        float rep[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          float s0 = 0.f, s1 = 0.f;
+          for (int q = 0; q < slices; ++q) {
+            s0 += red[0][q * nch + tid][e];
+            s1 += red[1][q * nch + tid][e];
+          }
+          const float m0 = s0 / (float)gm.m;
+          rep[e] = np > 0 ? gm.lambda * m0 + (1.f - gm.lambda) * (s1 / (float)np) : m0;
+        }
+        const int x = (x0 + tid) * VEC, g = x / D, c = x - g * D;
+        float *dst = Kc + (((int64_t)b * gm.Hkv + g) * gm.T + t) * D + c;
+#pragma unroll
+        for (int e = 0; e < VEC; e += 4) *reinterpret_cast<float4 *>(dst + e) = make_float4(rep[e], rep[e + 1], rep[e + 2], rep[e + 3]);
+      }
+      __syncthreads();
+    }
+  }
+  __syncthreads();
+  if (tid == 0) clen[b] = pos + 1;
+}
+
+template <typename T, int D>
+static hipError_t launch_cache_append_t(const Geom &g, const void *Kn, const void *Vn, const uint8_t *pn, void *Kcache,
+                                        void *Vcache, uint8_t *pcache, int32_t *clen, float *Kc, hipStream_t s) {
+  timing_begin("phsa_cache_append", s);
+  hipLaunchKernelGGL((cache_append_kernel<T, D>), dim3(g.B), dim3(256), 0, s, static_cast<const T *>(Kn),
+                     static_cast<const T *>(Vn), pn, static_cast<T *>(Kcache), static_cast<T *>(Vcache), pcache, clen,
+                     Kc, g);
+  timing_end(s);
+  return hipGetLastError();
+}
+
+hipError_t launch_cache_append(const Geom &g, const void *Kn, const void *Vn, const uint8_t *pn, void *Kcache,
+                               void *Vcache, uint8_t *pcache, int32_t *clen, float *Kc, hipStream_t s) {
   if (g.dtype == 0)
-    return g.d == 128 ? launch_decode_t<bf16_t, 128>(g, Q, K, V, Kc, sel, O, LSE, s)
-                      : launch_decode_t<bf16_t, 64>(g, Q, K, V, Kc, sel, O, LSE, s);
-  return g.d == 128 ? launch_decode_t<float, 128>(g, Q, K, V, Kc, sel, O, LSE, s)
-                    : launch_decode_t<float, 64>(g, Q, K, V, Kc, sel, O, LSE, s);
+    return g.d == 128 ? launch_cache_append_t<bf16_t, 128>(g, Kn, Vn, pn, Kcache, Vcache, pcache, clen, Kc, s)
+                      : launch_cache_append_t<bf16_t, 64>(g, Kn, Vn, pn, Kcache, Vcache, pcache, clen, Kc, s);
+  return g.d == 128 ? launch_cache_append_t<float, 128>(g, Kn, Vn, pn, Kcache, Vcache, pcache, clen, Kc, s)
+                    : launch_cache_append_t<float, 64>(g, Kn, Vn, pn, Kcache, Vcache, pcache, clen, Kc, s);
+}
+
+hipError_t launch_decode(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc,
+                         const int32_t *clen, int32_t *sel, void *O, float *LSE, hipStream_t s) {
+  if (g.dtype == 0)
+    return g.d == 128 ? launch_decode_t<bf16_t, 128>(g, Q, K, V, Kc, clen, sel, O, LSE, s)
+                      : launch_decode_t<bf16_t, 64>(g, Q, K, V, Kc, clen, sel, O, LSE, s);
+  return g.d == 128 ? launch_decode_t<float, 128>(g, Q, K, V, Kc, clen, sel, O, LSE, s)
+                    : launch_decode_t<float, 64>(g, Q, K, V, Kc, clen, sel, O, LSE, s);
 }
 
 }  // namespace phsa

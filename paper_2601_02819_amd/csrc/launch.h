@@ -60,7 +60,9 @@ hipError_t launch_attn_fwd_fp32(const Geom &g, const float *Q, const float *K, c
 hipError_t launch_attn_bwd_fp32(const Geom &g, const float *Q, const float *K, const float *V,
                                 const float *O, const float *dO, const float *LSE, const int32_t *sel,
                                 float *dQ, float *dK, float *dV, float *Dvec, hipStream_t s);
-hipError_t launch_decode(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc, int32_t *sel,
-                         void *O, float *LSE, hipStream_t s);
+hipError_t launch_decode(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc,
+                         const int32_t *clen, int32_t *sel, void *O, float *LSE, hipStream_t s);
+hipError_t launch_cache_append(const Geom &g, const void *Kn, const void *Vn, const uint8_t *pn, void *Kcache,
+                               void *Vcache, uint8_t *pcache, int32_t *clen, float *Kc, hipStream_t s);
 
 }  // namespace phsa

@@ -25,7 +25,8 @@ MAX_PUNCT_IDS = 16384
 
 EXPORTS = (
     "phsa_ksel", "phsa_validate", "phsa_workspace_size", "phsa_status_string", "phsa_punct_mask", "phsa_compress",
-    "phsa_select", "phsa_attn_fwd", "phsa_attn_bwd", "phsa_forward", "phsa_decode",
+    "phsa_select", "phsa_attn_fwd", "phsa_attn_bwd", "phsa_forward", "phsa_decode", "phsa_decode_varlen",
+    "phsa_cache_append",
     "phsa_timing_enable", "phsa_timing_collect", "phsa_timing_reset",
 )
 
@@ -69,6 +70,8 @@ def lib():
             "phsa_attn_bwd": (ctypes.c_int, [P] + [PP] * 11 + [ctypes.c_size_t, PP]),
             "phsa_forward": (ctypes.c_int, [P] + [PP] * 9 + [ctypes.c_size_t, PP]),
             "phsa_decode": (ctypes.c_int, [P] + [PP] * 8 + [ctypes.c_size_t, PP]),
+            "phsa_decode_varlen": (ctypes.c_int, [P] + [PP] * 9 + [ctypes.c_size_t, PP]),
+            "phsa_cache_append": (ctypes.c_int, [P] + [PP] * 8 + [PP]),
             "phsa_timing_enable": (ctypes.c_int, [ctypes.c_int32]),
             "phsa_timing_collect": (ctypes.c_int32, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
                                                      ctypes.POINTER(ctypes.c_int64)]),
@@ -251,6 +254,34 @@ def decode(q, k_cache, v_cache, kc, cfg: Config, ws: Optional[torch.Tensor] = No
     _check(lib().phsa_decode(ctypes.byref(p), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kc), _ptr(sel), _ptr(o),
                              _ptr(lse), _ptr(w), w.numel() if w is not None else 0, _stream()), "phsa_decode")
     return sel, o, lse
+
+
+def decode_varlen(q, k_cache, v_cache, kc, cache_len, cfg: Config):
+    """Decode step with per-sequence cache lengths: q [B, 1, Hq, d], caches [B, Lk, Hkv, d]
+    (capacity Lk), kc [B, Hkv, Lk/m, d], cache_len int32 [B] -> (sel, O, LSE)."""
+    _dev(q, k_cache, v_cache, kc, cache_len)
+    B, Lq, Hq, d = q.shape
+    Lk, Hkv = k_cache.shape[1], k_cache.shape[2]
+    p = make_params(cfg, B, Lq, Lk, Hq, Hkv, d, q.dtype)
+    sel = torch.empty(B, Hkv, Lq, cfg.ksel, dtype=torch.int32, device=q.device)
+    o = torch.empty_like(q)
+    lse = torch.empty(B, Hq, Lq, dtype=torch.float32, device=q.device)
+    w = _workspace(p, OP_DECODE, None, q.device)
+    _check(lib().phsa_decode_varlen(ctypes.byref(p), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(kc), _ptr(cache_len),
+                                    _ptr(sel), _ptr(o), _ptr(lse), _ptr(w), w.numel() if w is not None else 0,
+                                    _stream()), "phsa_decode_varlen")
+    return sel, o, lse
+
+
+def cache_append(k_new, v_new, punct_new, k_cache, v_cache, punct_cache, cache_len, kc, cfg: Config) -> None:
+    """Appends one token per sequence (k_new, v_new [B, Hkv, d], punct_new uint8 [B]) to the caches
+    in place, growing cache_len and writing the representative of every block it completes."""
+    _dev(k_new, v_new, punct_new, k_cache, v_cache, punct_cache, cache_len, kc)
+    B, Lk, Hkv, d = k_cache.shape
+    p = make_params(cfg, B, 1, Lk, Hkv, Hkv, d, k_cache.dtype)
+    _check(lib().phsa_cache_append(ctypes.byref(p), _ptr(k_new), _ptr(v_new), _ptr(punct_new), _ptr(k_cache),
+                                   _ptr(v_cache), _ptr(punct_cache), _ptr(cache_len), _ptr(kc), _stream()),
+           "phsa_cache_append")
 
 
 class SparseAttention(torch.autograd.Function):
