@@ -52,8 +52,8 @@ def _load():
         I, D, L, P = ctypes.c_int, ctypes.c_double, ctypes.c_int64, ctypes.c_void_p
         _lib.oracle_compress.argtypes = [I, I, I, I, I, D, P, P, P]
         _lib.oracle_punct_mask.argtypes = [L, P, ctypes.c_int32, P, P]
-        _lib.oracle_select.argtypes = [I] * 11 + [D, P, P, L, P, P, P, P]
-        _lib.oracle_score_row.argtypes = [I] * 7 + [D, P, P, I, I, I, P]
+        _lib.oracle_select.argtypes = [I] * 12 + [D, P, P, L, P, P, P, P]
+        _lib.oracle_score_row.argtypes = [I] * 7 + [D, P, P, I, I, I, I, I, P]
         _lib.oracle_attn_fwd.argtypes = [I] * 9 + [D, P, P, P, P, L, P, P, P]
         _lib.oracle_attn_bwd.argtypes = [I] * 9 + [D, P, P, P, P, P, L, P, P, L, P, P, P]
         for f in ("oracle_compress", "oracle_select", "oracle_score_row", "oracle_attn_fwd", "oracle_attn_bwd",
@@ -105,11 +105,16 @@ def compress(K, punct, block_size: int, lam: float) -> np.ndarray:
     return out
 
 
+SUM_LOGITS, SOFTMAX_SUM = 0, 1   # group aggregation of the per-head Eq. 8 scores
+
+
 def select(Q, Kc, block_size: int, top_k: int, n_init: int, window: int, scale: float,
-           seqlen_k: int, rows=None, q_pos0=None):
+           seqlen_k: int, rows=None, q_pos0=None, mode: int = SUM_LOGITS):
     """Q [B, Lq, Hq, d], Kc [B, Hkv, T, d] float64.  Query row i sits at position
     q_pos0 + i (default seqlen_k - Lq); seqlen_k must cover whole blocks up to
-    the last query's own block.
+    the last query's own block.  mode SUM_LOGITS ranks blocks on the group's
+    summed scaled logits; SOFTMAX_SUM on log sum_h softmax_h(t), each head's
+    softmax taken over the complete causal blocks 0 .. cur-1.
 
     Returns (sel, kth, gap).  With rows=None: sel [B, Hkv, Lq, Ksel] and
     kth/gap [B, Hkv, Lq].  With rows (flat b*Lq + i): sel [n, Hkv, Ksel],
@@ -125,8 +130,9 @@ def select(Q, Kc, block_size: int, top_k: int, n_init: int, window: int, scale: 
     kth = np.empty((n, Hkv), dtype=np.float64)
     gap = np.empty((n, Hkv), dtype=np.float64)
     pos0 = seqlen_k - Lq if q_pos0 is None else int(q_pos0)
+    assert mode in (SUM_LOGITS, SOFTMAX_SUM) and Hq // Hkv <= 64
     _load().oracle_select(B, Lq, seqlen_k, Hq, Hkv, d, block_size, top_k, n_init, window,
-                          pos0, float(scale), _ptr(Q), _ptr(Kc), n, _ptr(r), _ptr(sel),
+                          pos0, int(mode), float(scale), _ptr(Q), _ptr(Kc), n, _ptr(r), _ptr(sel),
                           _ptr(kth), _ptr(gap))
     if rows is None:
         sel = sel.reshape(B, Lq, Hkv, ks).transpose(0, 2, 1, 3).copy()
@@ -135,15 +141,19 @@ def select(Q, Kc, block_size: int, top_k: int, n_init: int, window: int, scale: 
     return sel, kth, gap
 
 
-def score_row(Q, Kc, block_size: int, scale: float, seqlen_k: int, b: int, i: int, g: int) -> np.ndarray:
-    """Group relevance logits of every block for one (b, i, g): float64 [T]."""
+def score_row(Q, Kc, block_size: int, scale: float, seqlen_k: int, b: int, i: int, g: int,
+              q_pos0=None, mode: int = SUM_LOGITS) -> np.ndarray:
+    """Group relevance scores of every block for one (b, i, g) in the given
+    mode: float64 [T] (SOFTMAX_SUM gives -inf outside blocks 0 .. cur-1)."""
     Q = _f32(Q)
     Kc = np.ascontiguousarray(np.asarray(Kc, dtype=np.float64))
     B, Lq, Hq, d = Q.shape
     Hkv, T = Kc.shape[1], Kc.shape[2]
     out = np.empty(T, dtype=np.float64)
+    pos0 = seqlen_k - Lq if q_pos0 is None else int(q_pos0)
+    assert mode in (SUM_LOGITS, SOFTMAX_SUM) and Hq // Hkv <= 64
     _load().oracle_score_row(B, Lq, seqlen_k, Hq, Hkv, d, block_size, float(scale), _ptr(Q), _ptr(Kc),
-                             b, i, g, _ptr(out))
+                             b, i, g, pos0, int(mode), _ptr(out))
     return out
 
 

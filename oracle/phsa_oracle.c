@@ -92,10 +92,65 @@ static double group_score(const float *Q, const double *Kc, int b, int i, int g,
   return s;
 }
 
+/* Scaled logit q_h^T M(B_t) / sqrt(d_k) of one query head h (Eq. 8). */
+static double head_logit(const float *Q, const double *Kc, int b, int i, int h, int g, int t,
+                         int Lq, int Hq, int Hkv, int T, int d, double scale) {
+  double dot = 0.0;
+  for (int c = 0; c < d; ++c) dot += (double)Q[IDX4(b, i, h, c, Lq, Hq, d)] * Kc[IDX4(b, g, t, c, Hkv, T, d)];
+  return scale * dot;
+}
+
+/* Selection mode SOFTMAX_SUM: Eq. 8 taken literally per query head, i.e. the
+ * softmax of the head's block logits, and the group's heads combined by
+ * adding their probabilities.  The softmax runs over the complete blocks in
+ * the query's causal past, 0 .. cur-1: the query's own block is left out
+ * because it holds keys past the query (in prefill) or is still being filled
+ * (in generation).  lse[hh] = log sum_{t < cur} exp(logit_h(t)) for the G
+ * heads of group g; -inf when cur = 0.                                      */
+static void head_log_normalisers(const float *Q, const double *Kc, int b, int i, int g, int cur,
+                                 int Lq, int Hq, int Hkv, int T, int d, double scale, double *lse) {
+  const int G = Hq / Hkv;
+  for (int hh = 0; hh < G; ++hh) {
+    const int h = g * G + hh;
+    double mx = -INFINITY;
+    for (int t = 0; t < cur; ++t) {
+      const double x = head_logit(Q, Kc, b, i, h, g, t, Lq, Hq, Hkv, T, d, scale);
+      if (x > mx) mx = x;
+    }
+    double sum = 0.0;
+    for (int t = 0; t < cur; ++t) sum += exp(head_logit(Q, Kc, b, i, h, g, t, Lq, Hq, Hkv, T, d, scale) - mx);
+    lse[hh] = cur > 0 ? mx + log(sum) : -INFINITY;
+  }
+}
+
+/* Group score of block t in mode SOFTMAX_SUM, in log units:
+ * log sum_h softmax_h(t), which ranks blocks exactly as the summed
+ * probabilities do.                                                         */
+static double group_softmax_score(const float *Q, const double *Kc, int b, int i, int g, int t,
+                                  int Lq, int Hq, int Hkv, int T, int d, double scale, const double *lse) {
+  const int G = Hq / Hkv;
+  double p = 0.0;
+  for (int hh = 0; hh < G; ++hh)
+    p += exp(head_logit(Q, Kc, b, i, g * G + hh, g, t, Lq, Hq, Hkv, T, d, scale) - lse[hh]);
+  return log(p);
+}
+
+/* Scores of every block for one (b, i, g) in the given mode (0 = summed
+ * logits, 1 = summed per-head softmax); query row i sits at q_pos0 + i.
+ * In mode 1 blocks outside 0 .. cur-1 get -inf.                              */
 void oracle_score_row(int B, int Lq, int Lk, int Hq, int Hkv, int d, int m, double scale,
-                      const float *Q, const double *Kc, int b, int i, int g, double *scores_T) {
+                      const float *Q, const double *Kc, int b, int i, int g, int q_pos0, int mode,
+                      double *scores_T) {
   (void)B;
   const int T = Lk / m;
+  if (mode == 1) {
+    const int cur = (q_pos0 + i) / m;
+    double lse[64];
+    head_log_normalisers(Q, Kc, b, i, g, cur, Lq, Hq, Hkv, T, d, scale, lse);
+    for (int t = 0; t < T; ++t)
+      scores_T[t] = t < cur ? group_softmax_score(Q, Kc, b, i, g, t, Lq, Hq, Hkv, T, d, scale, lse) : -INFINITY;
+    return;
+  }
   for (int t = 0; t < T; ++t)
     scores_T[t] = group_score(Q, Kc, b, i, g, t, Lq, Hq, Hkv, T, d, scale);
 }
@@ -124,9 +179,11 @@ static int int_cmp(const void *a, const void *b) {
  * Rows: list of b*Lq + i (NULL = all rows, in order).  Outputs are compact:
  *   sel_out [n_rows, Hkv, Ksel], kth_out/gap_out [n_rows, Hkv].
  * kth_out = score of the k-th pick (NaN if no pick), gap_out = k-th minus
- * (k+1)-th score (+inf when there is no (k+1)-th candidate).               */
+ * (k+1)-th score (+inf when there is no (k+1)-th candidate).
+ * mode 0 ranks on the group's summed logits, mode 1 on log sum_h softmax_h
+ * (SOFTMAX_SUM above); kth/gap are in the mode's own units.                */
 void oracle_select(int B, int Lq, int Lk, int Hq, int Hkv, int d, int m, int top_k, int n_init,
-                   int window, int q_pos0, double scale, const float *Q, const double *Kc,
+                   int window, int q_pos0, int mode, double scale, const float *Q, const double *Kc,
                    int64_t n_rows, const int64_t *rows, int32_t *sel_out, double *kth_out,
                    double *gap_out) {
   (void)B;
@@ -149,11 +206,14 @@ void oracle_select(int B, int Lq, int Lk, int Hq, int Hkv, int d, int m, int top
         int lo = cur - window / m;
         if (lo < 0) lo = 0;
         for (int t = lo; t <= cur; ++t) forced[t] = 1; /* local window incl. own block */
+        double lse[64];
+        if (mode == 1) head_log_normalisers(Q, Kc, b, i, g, cur, Lq, Hq, Hkv, T, d, scale, lse);
         int nc = 0;
         for (int t = 0; t <= cur; ++t) /* causal: only blocks <= cur */
           if (!forced[t]) {
             cand[nc].t = t;
-            cand[nc].s = group_score(Q, Kc, b, i, g, t, Lq, Hq, Hkv, T, d, scale);
+            cand[nc].s = mode == 1 ? group_softmax_score(Q, Kc, b, i, g, t, Lq, Hq, Hkv, T, d, scale, lse)
+                                   : group_score(Q, Kc, b, i, g, t, Lq, Hq, Hkv, T, d, scale);
             ++nc;
           }
         qsort(cand, (size_t)nc, sizeof(cand_t), cand_cmp);

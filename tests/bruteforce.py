@@ -46,11 +46,35 @@ def group_scores(Q, Kc, scale):
     return out
 
 
-def select(Q, Kc, m, top_k, n_init, window, scale, Lk):
+def group_softmax_scores(Q, Kc, scale, m, Lk):
+    """[B, Hkv, Lq, T] log of the summed per-head softmax probabilities, each
+    head's softmax taken (with scipy) over the blocks strictly before the
+    query's own block; -inf elsewhere."""
+    from scipy.special import softmax
+    Q = np.asarray(Q, dtype=np.float64)
+    B, Lq, Hq, d = Q.shape
+    H, T = Kc.shape[1], Kc.shape[2]
+    G = Hq // H
+    cur = (Lk - Lq + np.arange(Lq)) // m
+    past = np.arange(T)[None, :] < cur[:, None]                     # [Lq, T]
+    per_head = np.einsum("bihd,bgtd->bhgit", Q, Kc) * scale
+    out = np.full((B, H, Lq, T), -np.inf)
+    with np.errstate(divide="ignore"):
+        for g in range(H):
+            prob = np.zeros((B, Lq, T))
+            for hh in range(G):
+                logits = np.where(past[None], per_head[:, g * G + hh, g], -np.inf)
+                rows = past.any(axis=1)
+                prob[:, rows] += softmax(logits[:, rows], axis=-1)
+            out[:, g] = np.where(past[None], np.log(prob), -np.inf)
+    return out
+
+
+def select(Q, Kc, m, top_k, n_init, window, scale, Lk, softmax_sum=False):
     """Algorithm 1 block selection by full lexsort of every row's score vector."""
     B, Lq = Q.shape[0], Q.shape[1]
     H, T = Kc.shape[1], Kc.shape[2]
-    S = group_scores(Q, Kc, scale)
+    S = group_softmax_scores(Q, Kc, scale, m, Lk) if softmax_sum else group_scores(Q, Kc, scale)
     ksel = n_init + window // m + 1 + top_k
     out = -np.ones((B, H, Lq, ksel), dtype=np.int32)
     t_all = np.arange(T)
