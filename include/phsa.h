@@ -100,7 +100,15 @@ typedef enum {
    * (the first part of the workspace) is reused instead of rebuilt; the rest of
    * the workspace is overwritten.  ws_bytes must still cover
    * phsa_workspace_size(p, PHSA_OP_ATTN_BWD). */
-  PHSA_FLAG_REUSE_INDEX = 1
+  PHSA_FLAG_REUSE_INDEX = 1,
+  /* phsa_select, phsa_forward, phsa_decode, phsa_decode_varlen: rank blocks
+   * by Eq. 8's softmax taken per query head and summed over the heads that
+   * share a KV head (the grouped-query aggregation of NSA) instead of by the
+   * summed logits.  Each head's softmax runs over the complete blocks before
+   * the query's own block (0 .. cur-1): the own block holds keys past the
+   * query in prefill and is still filling in generation.  For one head per
+   * group both modes select the same blocks.  Forced blocks are unchanged. */
+  PHSA_FLAG_SELECT_SOFTMAX_SUM = 2
 } phsa_flag;
 
 /* Number of index slots per (query row, KV head): n_init + w/m + 1 + top_k. */

@@ -109,7 +109,7 @@ phsa_status validate(const phsa_params *p, int op, Geom *out) {
   if (op == PHSA_OP_DECODE && p->seqlen_q != 1) return PHSA_ERR_SHAPE;
   if (p->top_k < 0 || p->n_init_blocks < 0 || p->window < 0 || p->window % p->block_size != 0)
     return PHSA_ERR_INVALID_ARG;
-  if ((p->flags & ~PHSA_FLAG_REUSE_INDEX) != 0) return PHSA_ERR_INVALID_ARG;
+  if ((p->flags & ~(PHSA_FLAG_REUSE_INDEX | PHSA_FLAG_SELECT_SOFTMAX_SUM)) != 0) return PHSA_ERR_INVALID_ARG;
   if (!(p->lambda >= 0.f && p->lambda <= 1.f)) return PHSA_ERR_INVALID_ARG;
   if (!isfinite(p->softmax_scale)) return PHSA_ERR_INVALID_ARG;
   // What the kernels implement.
@@ -121,6 +121,8 @@ phsa_status validate(const phsa_params *p, int op, Geom *out) {
   if (T > 2048 || p->seqlen_q >= (1 << 25)) return PHSA_ERR_UNSUPPORTED;
   if (p->batch > 65535 || p->n_heads_q > 65535 || (int64_t)p->batch * p->n_heads_kv > 65535)
     return PHSA_ERR_UNSUPPORTED;  // grid y/z extents
+  // the softmax-sum kernels give each lane one (row, head) pair, at most 8 heads in decode
+  if ((p->flags & PHSA_FLAG_SELECT_SOFTMAX_SUM) && (G > 64 || 64 % G != 0)) return PHSA_ERR_UNSUPPORTED;
   if (is_attention_op(op)) {
     if (p->block_size != 64) return PHSA_ERR_UNSUPPORTED;
     if (G != 1 && G != 2 && G != 4 && G != 8) return PHSA_ERR_UNSUPPORTED;
@@ -146,6 +148,7 @@ phsa_status validate(const phsa_params *p, int op, Geom *out) {
     g.lambda = p->lambda;
     g.scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.f / sqrtf((float)p->head_dim);
     g.dtype = p->dtype;
+    g.sel_mode = (p->flags & PHSA_FLAG_SELECT_SOFTMAX_SUM) ? 1 : 0;
     *out = g;
   }
   return PHSA_OK;

@@ -73,45 +73,126 @@ __device__ __forceinline__ int seq_len(const int32_t *clen, int b, const Geom &g
   return clen ? min(max(clen[b], 1), gm.Lk) : gm.Lk;
 }
 
-template <typename T, int D>
+// MODE 0 ranks on the summed logits of the group's heads.  MODE 1
+// (PHSA_FLAG_SELECT_SOFTMAX_SUM) keeps every head's log2 logits of the
+// complete blocks 0..cur-1 in LDS, reduces each head's log2 normaliser over
+// the workgroup, and scores a candidate by log2 sum_h 2^(x_h - lse_h).
+template <typename T, int D, int MODE>
 __global__ __launch_bounds__(512) void decode_select_kernel(const T *__restrict__ Q, const float *__restrict__ Kc,
                                                             const int32_t *__restrict__ clen,
                                                             int32_t *__restrict__ sel, Geom gm) {
   constexpr int LPR = D / 4;      // lanes per representative row (one float4 each)
   constexpr int RPW = 64 / LPR;   // rows per wave load instruction
   constexpr int U = 8;            // load instructions in flight per lane
-  extern __shared__ float sc[];   // [T]
+  constexpr int GM = MODE == 1 ? 8 : 1;   // heads kept apart (the group size is at most 8)
+  extern __shared__ float sc[];   // MODE 0: [T] scores; MODE 1: [G][T] head logits, then scores in row 0
   __shared__ float mbuf_s[4][64];
   __shared__ int mbuf_t[4][64];
+  __shared__ float red_m[8][8], red_l[8][8];
   const int bg = blockIdx.x, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane / LPR, c4 = (lane % LPR) * 4;
-  float q[4] = {0.f, 0.f, 0.f, 0.f};
+  const int NH = MODE == 1 ? gm.G : 1;
+  float q[GM][4];
+#pragma unroll
+  for (int h = 0; h < GM; ++h)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) q[h][e] = 0.f;
   for (int hh = 0; hh < gm.G; ++hh) {
     const T *src = Q + ((int64_t)b * gm.Hq + g * gm.G + hh) * D + c4;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) q[e] += to_f32<T>(src[e]);
+    for (int h = 0; h < GM; ++h)
+      if (MODE == 0 || h == hh) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) q[h][e] += to_f32<T>(src[e]) * (MODE == 1 ? gm.scale * kLog2e : 1.f);
+      }
   }
   const int cur = (seq_len(clen, b, gm) - 1) / gm.m;  // the query's own block
   const int lo = max(0, cur - gm.window / gm.m);
+  // MODE 0 scores the candidates n_init <= t < lo; MODE 1 every complete block t < cur
+  const int s0 = MODE == 1 ? 0 : gm.n_init, s1 = MODE == 1 ? cur : lo;
   const float *kc = Kc + (int64_t)bg * gm.T * D;
-  for (int t0 = gm.n_init + wave * RPW * U; t0 < lo; t0 += 8 * RPW * U) {
+  for (int t0 = s0 + wave * RPW * U; t0 < s1; t0 += 8 * RPW * U) {
     float4 v[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int t = t0 + u * RPW + sub;
-      v[u] = t < lo ? *reinterpret_cast<const float4 *>(kc + (int64_t)t * D + c4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      v[u] = t < s1 ? *reinterpret_cast<const float4 *>(kc + (int64_t)t * D + c4) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      float a = fmaf(q[0], v[u].x, fmaf(q[1], v[u].y, fmaf(q[2], v[u].z, q[3] * v[u].w)));
-#pragma unroll
-      for (int o = 1; o < LPR; o <<= 1) a += __shfl_xor(a, o, 64);
       const int t = t0 + u * RPW + sub;
-      if (lane % LPR == 0 && t < lo) sc[t] = a * gm.scale;
+#pragma unroll
+      for (int h = 0; h < GM; ++h) {
+        if (h >= NH) break;
+        float a = fmaf(q[h][0], v[u].x, fmaf(q[h][1], v[u].y, fmaf(q[h][2], v[u].z, q[h][3] * v[u].w)));
+#pragma unroll
+        for (int o = 1; o < LPR; o <<= 1) a += __shfl_xor(a, o, 64);
+        if (lane % LPR == 0 && t < s1) sc[h * gm.T + t] = MODE == 1 ? a : a * gm.scale;
+      }
     }
   }
   __syncthreads();
+  if (MODE == 1) {
+    // per-head log2 normaliser over t < cur: thread-local running (max, sum),
+    // merged across the wave by shuffles and across the waves through LDS
+    float lse[GM];
+#pragma unroll
+    for (int h = 0; h < GM; ++h) {
+      if (h >= NH) break;
+      float mx = -INFINITY, sm = 0.f;
+      for (int t = tid; t < cur; t += 512) {
+        const float x = sc[h * gm.T + t];
+        if (x > mx) {
+          sm = sm * exp2f(mx - x) + 1.f;
+          mx = x;
+        } else {
+          sm += exp2f(x - mx);
+        }
+      }
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const float om = __shfl_xor(mx, o, 64), os = __shfl_xor(sm, o, 64);
+        const float nm = fmaxf(mx, om);
+        sm = (sm > 0.f ? sm * exp2f(mx - nm) : 0.f) + (os > 0.f ? os * exp2f(om - nm) : 0.f);
+        mx = nm;
+      }
+      if (lane == 0) {
+        red_m[wave][h] = mx;
+        red_l[wave][h] = sm;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < GM; ++h) {
+      if (h >= NH) break;
+      float M = -INFINITY, L = 0.f;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) M = fmaxf(M, red_m[w][h]);
+#pragma unroll
+      for (int w = 0; w < 8; ++w)
+        if (red_l[w][h] > 0.f) L += red_l[w][h] * exp2f(red_m[w][h] - M);
+      lse[h] = L > 0.f ? M + log2f(L) : 0.f;  // cur = 0 leaves no candidate
+    }
+    // candidates: the group score replaces head 0's logit in place (one thread per block)
+    for (int t = gm.n_init + tid; t < lo; t += 512) {
+      float y[GM], ym = -INFINITY;
+#pragma unroll
+      for (int h = 0; h < GM; ++h) {
+        if (h >= NH) break;
+        y[h] = sc[h * gm.T + t] - lse[h];
+        ym = fmaxf(ym, y[h]);
+      }
+      float e = 0.f;
+#pragma unroll
+      for (int h = 0; h < GM; ++h) {
+        if (h >= NH) break;
+        e += exp2f(y[h] - ym);
+      }
+      sc[t] = ym + log2f(e);
+    }
+    __syncthreads();
+  }
 
   // Top-k: every wave sorts its 64-candidate chunks best-first across its
   // lanes (bitonic network over shuffles) and keeps the best 64 seen; the
@@ -282,8 +363,12 @@ template <typename T, int D, int G>
 static hipError_t launch_decode_g(const Geom &g, const void *Q, const void *K, const void *V, const float *Kc,
                                   const int32_t *clen, int32_t *sel, void *O, float *LSE, hipStream_t s) {
   timing_begin("phsa_decode_select", s);
-  hipLaunchKernelGGL((decode_select_kernel<T, D>), dim3(g.B * g.Hkv), dim3(512), (size_t)g.T * sizeof(float), s,
-                     static_cast<const T *>(Q), Kc, clen, sel, g);
+  if (g.sel_mode == 1)
+    hipLaunchKernelGGL((decode_select_kernel<T, D, 1>), dim3(g.B * g.Hkv), dim3(512),
+                       (size_t)g.G * g.T * sizeof(float), s, static_cast<const T *>(Q), Kc, clen, sel, g);
+  else
+    hipLaunchKernelGGL((decode_select_kernel<T, D, 0>), dim3(g.B * g.Hkv), dim3(512), (size_t)g.T * sizeof(float), s,
+                       static_cast<const T *>(Q), Kc, clen, sel, g);
   timing_end(s);
   timing_begin("phsa_decode_attn", s);
   hipLaunchKernelGGL((decode_attn_kernel<T, D, G>), dim3(g.B * g.Hkv), dim3(256), 0, s, static_cast<const T *>(Q),

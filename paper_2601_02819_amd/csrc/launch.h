@@ -16,6 +16,7 @@ struct Geom {
   float lambda;
   float scale;        // softmax scale
   int dtype;          // 0 bf16, 1 fp32
+  int sel_mode;       // group aggregation of block scores: 0 summed logits, 1 summed per-head softmax
 };
 
 // Index (inverted selection) workspace, carved out of the caller's buffer.

@@ -25,6 +25,69 @@ __device__ __forceinline__ bool beats(float s1, int t1, float s2, int t2) {
   return s1 > s2 || (s1 == s2 && t1 < t2);
 }
 
+// Merge the four waves' sorted (score, block) lists of each row through LDS,
+// take the k best (score descending, block ascending) and write the row:
+// forced init blocks, the picks and the local blocks in ascending order,
+// padded with -1.  Every thread of the workgroup calls this (it holds a
+// barrier); lanes with `active` set write their row.  smem must hold the four
+// lists (4 * 64 * KMAX (score, block) pairs).
+template <int KMAX>
+__device__ __forceinline__ void finish_rows(const float (&ls)[KMAX], const int (&lt)[KMAX], unsigned char *smem,
+                                            int (*picks)[KMAX], bool active, int i, int cur, int lo, int bg,
+                                            int32_t *__restrict__ sel, const Geom &gm) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __syncthreads();
+  float *list_s = reinterpret_cast<float *>(smem);
+  int *list_t = reinterpret_cast<int *>(smem) + 4 * 64 * KMAX;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    list_s[(wave * 64 + lane) * KMAX + k] = ls[k];
+    list_t[(wave * 64 + lane) * KMAX + k] = lt[k];
+  }
+  __syncthreads();
+  if (!active) return;
+  int head[4] = {0, 0, 0, 0};
+  int npick = 0;
+  for (int p = 0; p < gm.top_k && p < KMAX; ++p) {
+    int bw = -1;
+    float bs = -FLT_MAX;
+    int bt = 0x7fffffff;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (head[w] < KMAX) {
+        const float s = list_s[(w * 64 + lane) * KMAX + head[w]];
+        const int t = list_t[(w * 64 + lane) * KMAX + head[w]];
+        if (t != 0x7fffffff && beats(s, t, bs, bt)) {
+          bw = w;
+          bs = s;
+          bt = t;
+        }
+      }
+    }
+    if (bw < 0) break;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) head[w] += (w == bw);
+    picks[lane][npick++] = bt;
+  }
+  // ascending block order of the picks (insertion sort, at most KMAX items)
+  for (int a = 1; a < npick; ++a) {
+    const int x = picks[lane][a];
+    int c = a - 1;
+    while (c >= 0 && picks[lane][c] > x) {
+      picks[lane][c + 1] = picks[lane][c];
+      --c;
+    }
+    picks[lane][c + 1] = x;
+  }
+  int32_t *out = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
+  int n = 0;
+  const int ni = min(gm.n_init, cur + 1);
+  for (int t = 0; t < ni; ++t) out[n++] = t;
+  for (int a = 0; a < npick; ++a) out[n++] = picks[lane][a];
+  for (int t = max(lo, ni); t <= cur; ++t) out[n++] = t;
+  for (; n < gm.ksel; ++n) out[n] = -1;
+}
+
 template <typename T, int D, int KMAX>
 __global__ __launch_bounds__(256) void select_kernel(const T *__restrict__ Q, const float *__restrict__ Kc,
                                                      int32_t *__restrict__ sel, Geom gm) {
@@ -110,58 +173,153 @@ __global__ __launch_bounds__(256) void select_kernel(const T *__restrict__ Q, co
     }
   }
 
-  // Merge the four wave lists.
-  __syncthreads();
-  float *list_s = reinterpret_cast<float *>(smem);
-  int *list_t = reinterpret_cast<int *>(smem) + 4 * 64 * KMAX;
+  finish_rows<KMAX>(ls, lt, smem, picks, wave == 0 && row_ok, i, cur, lo, bg, sel, gm);
+}
+
+// Softmax-sum selection (PHSA_FLAG_SELECT_SOFTMAX_SUM): Eq. 8's softmax is
+// taken per query head over the complete blocks 0..cur-1 of the row's causal
+// past, and a block's group score is the sum of its G head probabilities,
+// ranked as s = log2 sum_h 2^(x_h - lse_h) with x_h the head's logit in log2
+// units and lse_h the head's log2 normaliser.
+//
+// A lane owns one (query row, head) pair: 64 / G rows per workgroup, lane l
+// holding row l / G and head l % G, whose query (scaled by scale * log2 e)
+// stays in registers.  Representatives stream through LDS in chunks of 64
+// blocks as in select_kernel, wave w scoring blocks 16w..16w+15 of a chunk.
+//   pass 1: every lane keeps a running (max, sum) of 2^x over t < cur; the
+//           four waves' states are merged through LDS into lse_h.
+//   pass 2: the candidate blocks are scored again, the G lanes of a row
+//           combine their terms by shuffles (shifted by their maximum, so no
+//           term underflows), and every lane inserts the row's score into
+//           its sorted list (the G lanes of a row hold identical lists).
+// Costs two d-long dot products per (row, head, block), 2G times those of the
+// summed-logit kernel.
+template <typename T, int D, int KMAX>
+__global__ __launch_bounds__(256) void select_softmax_kernel(const T *__restrict__ Q, const float *__restrict__ Kc,
+                                                             int32_t *__restrict__ sel, Geom gm) {
+  constexpr int CH = 64;
+  constexpr int LIST_BYTES = 4 * 64 * KMAX * 8;
+  constexpr int CHUNK_BYTES = CH * D * 4;
+  constexpr int BUF = LIST_BYTES > CHUNK_BYTES ? LIST_BYTES : CHUNK_BYTES;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[BUF];
+  __shared__ int picks[64][KMAX];
+  __shared__ float wmax[4][64], wsum[4][64];
+  float *kc_s = reinterpret_cast<float *>(smem);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int G = gm.G, R = 64 / G;                      // rows per workgroup
+  const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg % gm.Hkv;
+  const int hh = lane % G;
+  const int i = blockIdx.x * R + lane / G;
+  const bool row_ok = i < gm.Lq;
+  const int pos = gm.q_pos0 + (row_ok ? i : gm.Lq - 1);
+  const int cur = pos / gm.m;
+  const int lo = max(0, cur - gm.window / gm.m);
+  const int last_i = min(blockIdx.x * R + R - 1, gm.Lq - 1);
+  const int cur_max = (gm.q_pos0 + last_i) / gm.m;     // normaliser blocks: t < cur
+  const int t_end = max(0, cur_max - gm.window / gm.m);  // candidates: n_init <= t < lo
+
+  float q[D];
+  {
+    const float f = gm.scale * kLog2e;
+    const T *src = Q + (((int64_t)b * gm.Lq + (row_ok ? i : gm.Lq - 1)) * gm.Hq + g * G + hh) * D;
+#pragma unroll
+    for (int c = 0; c < D; c += 16 / sizeof(T)) {
+      const uint4 raw = *reinterpret_cast<const uint4 *>(src + c);
+      const T *v = reinterpret_cast<const T *>(&raw);
+#pragma unroll
+      for (int e = 0; e < 16 / (int)sizeof(T); ++e) q[c + e] = to_f32<T>(v[e]) * f;
+    }
+  }
+  const float *kc_bg = Kc + (int64_t)bg * gm.T * D;
+  auto load_chunk = [&](int t0, int nblk) {
+    __syncthreads();
+    for (int e = tid * 4; e < nblk * D; e += 256 * 4)
+      *reinterpret_cast<float4 *>(kc_s + e) = *reinterpret_cast<const float4 *>(kc_bg + (int64_t)t0 * D + e);
+    __syncthreads();
+  };
+  auto dot = [&](int tt) {
+    const float *kr = kc_s + tt * D;
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+    for (int c = 0; c < D; c += 4) {
+      const float4 kv = *reinterpret_cast<const float4 *>(kr + c);
+      a0 = fmaf(q[c], kv.x, a0);
+      a1 = fmaf(q[c + 1], kv.y, a1);
+      a2 = fmaf(q[c + 2], kv.z, a2);
+      a3 = fmaf(q[c + 3], kv.w, a3);
+    }
+    return (a0 + a1) + (a2 + a3);
+  };
+
+  float ls[KMAX];
+  int lt[KMAX];
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) {
-    list_s[(wave * 64 + lane) * KMAX + k] = ls[k];
-    list_t[(wave * 64 + lane) * KMAX + k] = lt[k];
+    ls[k] = -FLT_MAX;
+    lt[k] = 0x7fffffff;
   }
-  __syncthreads();
-  if (wave != 0 || !row_ok) return;
 
-  int head[4] = {0, 0, 0, 0};
-  int npick = 0;
-  for (int p = 0; p < gm.top_k && p < KMAX; ++p) {
-    int bw = -1;
-    float bs = -FLT_MAX;
-    int bt = 0x7fffffff;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      if (head[w] < KMAX) {
-        const float s = list_s[(w * 64 + lane) * KMAX + head[w]];
-        const int t = list_t[(w * 64 + lane) * KMAX + head[w]];
-        if (t != 0x7fffffff && beats(s, t, bs, bt)) {
-          bw = w;
-          bs = s;
-          bt = t;
+  if (gm.top_k > 0 && t_end > gm.n_init) {
+    // pass 1: per-head log2 normaliser over blocks 0..cur-1
+    float mx = -INFINITY, sm = 0.f;
+    for (int t0 = 0; t0 < cur_max; t0 += CH) {
+      load_chunk(t0, min(CH, gm.T - t0));
+      for (int tt = wave * 16; tt < wave * 16 + 16; ++tt) {
+        const int t = t0 + tt;
+        if (t >= cur_max) break;
+        const float x = dot(tt);
+        if (t < cur) {
+          if (x > mx) {
+            sm = sm * exp2f(mx - x) + 1.f;
+            mx = x;
+          } else {
+            sm += exp2f(x - mx);
+          }
         }
       }
     }
-    if (bw < 0) break;
+    wmax[wave][lane] = mx;
+    wsum[wave][lane] = sm;
+    __syncthreads();
+    float gmx = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) head[w] += (w == bw);
-    picks[lane][npick++] = bt;
-  }
-  // ascending block order of the picks (insertion sort, at most KMAX items)
-  for (int a = 1; a < npick; ++a) {
-    const int x = picks[lane][a];
-    int c = a - 1;
-    while (c >= 0 && picks[lane][c] > x) {
-      picks[lane][c + 1] = picks[lane][c];
-      --c;
+    for (int w = 0; w < 4; ++w) gmx = fmaxf(gmx, wmax[w][lane]);
+    float gsum = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      if (wsum[w][lane] > 0.f) gsum += wsum[w][lane] * exp2f(wmax[w][lane] - gmx);
+    const float lse = gsum > 0.f ? gmx + log2f(gsum) : 0.f;  // rows with cur = 0 have no candidates
+
+    // pass 2: group scores of the candidates and the running top-k
+    for (int t0 = gm.n_init; t0 < t_end; t0 += CH) {
+      load_chunk(t0, min(CH, gm.T - t0));
+      for (int tt = wave * 16; tt < wave * 16 + 16; ++tt) {
+        const int t = t0 + tt;
+        if (t >= t_end) break;
+        const float y = dot(tt) - lse;
+        float ymax = y;
+        for (int o = 1; o < G; o <<= 1) ymax = fmaxf(ymax, __shfl_xor(ymax, o, 64));
+        float e = exp2f(y - ymax);
+        for (int o = 1; o < G; o <<= 1) e += __shfl_xor(e, o, 64);
+        float sc = ymax + log2f(e);
+        int ct = t;
+        if (row_ok && t < lo && beats(sc, ct, ls[KMAX - 1], lt[KMAX - 1])) {
+#pragma unroll
+          for (int k = 0; k < KMAX; ++k) {
+            const bool bt = beats(sc, ct, ls[k], lt[k]);
+            const float os = ls[k];
+            const int ot = lt[k];
+            ls[k] = bt ? sc : os;
+            lt[k] = bt ? ct : ot;
+            sc = bt ? os : sc;
+            ct = bt ? ot : ct;
+          }
+        }
+      }
     }
-    picks[lane][c + 1] = x;
   }
-  int32_t *out = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
-  int n = 0;
-  const int ni = min(gm.n_init, cur + 1);
-  for (int t = 0; t < ni; ++t) out[n++] = t;
-  for (int a = 0; a < npick; ++a) out[n++] = picks[lane][a];
-  for (int t = max(lo, ni); t <= cur; ++t) out[n++] = t;
-  for (; n < gm.ksel; ++n) out[n] = -1;
+  finish_rows<KMAX>(ls, lt, smem, picks, wave == 0 && row_ok && hh == 0, i, cur, lo, bg, sel, gm);
 }
 
 // bf16 inputs: scoring on the matrix cores, selection by a bar and a short exact rank.
@@ -565,6 +723,20 @@ static hipError_t launch_select_t(const Geom &g, const void *Q, const float *Kc,
   return hipGetLastError();
 }
 
+template <typename T, int D>
+static hipError_t launch_select_softmax(const Geom &g, const void *Q, const float *Kc, int32_t *sel, hipStream_t s) {
+  dim3 grid((g.Lq + 64 / g.G - 1) / (64 / g.G), g.B * g.Hkv);
+  timing_begin("phsa_select_softmax", s);
+  if (g.top_k <= 8)
+    hipLaunchKernelGGL((select_softmax_kernel<T, D, 8>), grid, dim3(256), 0, s, static_cast<const T *>(Q), Kc, sel, g);
+  else if (g.top_k <= 16)
+    hipLaunchKernelGGL((select_softmax_kernel<T, D, 16>), grid, dim3(256), 0, s, static_cast<const T *>(Q), Kc, sel, g);
+  else
+    hipLaunchKernelGGL((select_softmax_kernel<T, D, 32>), grid, dim3(256), 0, s, static_cast<const T *>(Q), Kc, sel, g);
+  timing_end(s);
+  return hipGetLastError();
+}
+
 template <int D, int G>
 static hipError_t launch_select_mfma(const Geom &g, const void *Q, const float *Kc, int32_t *sel, char *ws,
                                      hipStream_t s) {
@@ -602,11 +774,18 @@ static hipError_t launch_select_mfma_d(const Geom &g, const void *Q, const float
 
 size_t select_split_bytes(const Geom &g) {
   const size_t nblk = (size_t)g.B * g.Hkv * g.T;
-  return g.dtype == 0 ? nblk * (2 * g.d * sizeof(bf16_t) + sizeof(float)) : 0;
+  return g.dtype == 0 && g.sel_mode == 0 ? nblk * (2 * g.d * sizeof(bf16_t) + sizeof(float)) : 0;
 }
 
 hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t *sel, void *ws, hipStream_t s) {
   char *split = static_cast<char *>(ws);
+  if (g.sel_mode == 1) {
+    if (g.dtype == 0)
+      return g.d == 128 ? launch_select_softmax<bf16_t, 128>(g, Q, Kc, sel, s)
+                        : launch_select_softmax<bf16_t, 64>(g, Q, Kc, sel, s);
+    return g.d == 128 ? launch_select_softmax<float, 128>(g, Q, Kc, sel, s)
+                      : launch_select_softmax<float, 64>(g, Q, Kc, sel, s);
+  }
   if (g.dtype == 0)
     return g.d == 128 ? launch_select_mfma_d<128>(g, Q, Kc, sel, split, s)
                       : launch_select_mfma_d<64>(g, Q, Kc, sel, split, s);

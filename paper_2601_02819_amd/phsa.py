@@ -20,6 +20,7 @@ OK, ERR_INVALID_ARG, ERR_SHAPE, ERR_DTYPE, ERR_NULL, ERR_WORKSPACE, ERR_UNSUPPOR
 BF16, FP32 = 0, 1
 OP_COMPRESS, OP_SELECT, OP_ATTN_FWD, OP_ATTN_BWD, OP_FORWARD, OP_DECODE = range(6)
 FLAG_REUSE_INDEX = 1
+FLAG_SELECT_SOFTMAX_SUM = 2
 
 MAX_PUNCT_IDS = 16384
 
@@ -98,6 +99,7 @@ class Config:
     window: int = 0
     lam: float = 0.5
     softmax_scale: float = 0.0   # <= 0: 1 / sqrt(head_dim)
+    softmax_sum: bool = False    # rank blocks by summed per-head softmax (else by summed logits)
 
     @property
     def ksel(self) -> int:
@@ -108,7 +110,8 @@ def make_params(cfg: Config, batch: int, seqlen_q: int, seqlen_k: int, n_heads_q
                 head_dim: int, dtype, flags: int = 0) -> Params:
     code = BF16 if dtype in (torch.bfloat16, BF16) else FP32 if dtype in (torch.float32, FP32) else 99
     return Params(batch, seqlen_q, seqlen_k, n_heads_q, n_heads_kv, head_dim, cfg.block_size, cfg.top_k,
-                  cfg.n_init_blocks, cfg.window, cfg.lam, cfg.softmax_scale, code, flags)
+                  cfg.n_init_blocks, cfg.window, cfg.lam, cfg.softmax_scale, code,
+                  flags | (FLAG_SELECT_SOFTMAX_SUM if cfg.softmax_sum else 0))
 
 
 def workspace_size(p: Params, op: int) -> int:

@@ -57,7 +57,12 @@ def _p(**kw):
     ({"seqlen_q": 1}, phsa.OP_DECODE, phsa.OK),
     ({}, 17, phsa.ERR_INVALID_ARG),
     ({"flags": phsa.FLAG_REUSE_INDEX}, phsa.OP_ATTN_BWD, phsa.OK),
-    ({"flags": 2}, phsa.OP_ATTN_BWD, phsa.ERR_INVALID_ARG),                 # unknown flag bit
+    ({"flags": 4}, phsa.OP_ATTN_BWD, phsa.ERR_INVALID_ARG),                 # unknown flag bit
+    ({"flags": phsa.FLAG_SELECT_SOFTMAX_SUM}, phsa.OP_SELECT, phsa.OK),
+    ({"flags": phsa.FLAG_SELECT_SOFTMAX_SUM}, phsa.OP_DECODE, phsa.ERR_SHAPE),   # still needs Lq = 1
+    ({"n_heads_q": 6, "n_heads_kv": 2}, phsa.OP_SELECT, phsa.OK),                # G = 3, summed logits
+    ({"n_heads_q": 6, "n_heads_kv": 2, "flags": phsa.FLAG_SELECT_SOFTMAX_SUM}, phsa.OP_SELECT,
+     phsa.ERR_UNSUPPORTED),                                                      # G = 3, softmax sum
     ({"batch": 40000, "n_heads_q": 2, "n_heads_kv": 2}, phsa.OP_SELECT, phsa.ERR_UNSUPPORTED),  # B * Hkv > 65535
 ])
 def test_validate(kw, op, code):
@@ -72,6 +77,7 @@ def test_ksel_and_workspace():
     # bf16 hi/lo copies of K_comp and one norm per block, rounded up to 256 bytes
     assert phsa.workspace_size(_p(), phsa.OP_SELECT) == -(-16 * (2 * 64 * 2 + 4) // 256) * 256
     assert phsa.workspace_size(_p(dtype=phsa.FP32), phsa.OP_SELECT) == 0
+    assert phsa.workspace_size(_p(flags=phsa.FLAG_SELECT_SOFTMAX_SUM), phsa.OP_SELECT) == 0
     assert phsa.workspace_size(_p(), phsa.OP_FORWARD) >= phsa.workspace_size(_p(), phsa.OP_SELECT)
     fwd = phsa.workspace_size(_p(), phsa.OP_ATTN_FWD)
     assert fwd > 0 and fwd % 256 == 0

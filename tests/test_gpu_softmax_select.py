@@ -1,0 +1,167 @@
+"""GPU parity of the softmax-sum selection mode (PHSA_FLAG_SELECT_SOFTMAX_SUM):
+each head's Eq. 8 softmax over the complete causal blocks, summed over the
+group's heads.  Selections are compared with the oracle in the same mode (exact
+except rows whose oracle k-th / (k+1)-th gap, in log-probability units, is
+below 1e-4); attention outputs on the GPU's own selection."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2601_02819_amd import phsa
+from paper_2601_02819_amd.inputs import WORKLOADS, Workload
+from tests.gpu_common import O_TOL, cfg_of, check_sel, device_inputs, log, oracle_inputs, to_np
+
+pytestmark = pytest.mark.gpu
+SM = oracle.SOFTMAX_SUM
+
+
+def _cfg(wl):
+    return dataclasses.replace(cfg_of(wl), softmax_sum=True)
+
+
+def small(name, B, L, Hq, Hkv, d, top_k, n_init, window, dtype="bf16", Lq=None):
+    return Workload(name, B, Lq or L, L, Hq, Hkv, d, 64, top_k, n_init, window, dtype)
+
+
+CASES = [
+    small("ragged320_g2", 1, 320, 2, 1, 64, 2, 1, 0),
+    small("g2_win", 2, 1024, 4, 2, 128, 3, 1, 64),
+    small("g8_init2", 1, 1024, 8, 1, 128, 5, 2, 128),
+    small("g1_d64", 1, 768, 4, 4, 64, 4, 1, 0),
+    small("g4_k14", 1, 2048, 16, 4, 128, 14, 1, 0),
+    small("k32_init3", 1, 4096, 2, 1, 128, 32, 3, 192),
+    small("k7_tail_rows", 1, 2048, 4, 2, 128, 7, 1, 0, Lq=700),     # query rows at the end of the keys
+    small("fp32_g2", 1, 1024, 4, 2, 128, 3, 1, 64, dtype="fp32"),
+    small("fp32_g4_d64", 2, 640, 8, 2, 64, 9, 1, 0, dtype="fp32"),
+]
+
+
+@pytest.mark.parametrize("wl", CASES, ids=[w.name for w in CASES])
+def test_select_and_forward(wl):
+    log(f"[softmax-sum] {wl.name}")
+    cfg = _cfg(wl)
+    host, dev = device_inputs(wl, 3, with_grad_out=False)
+    h = oracle_inputs(host)
+    scale = wl.head_dim ** -0.5
+    Lk = wl.seqlen_k
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    sel = phsa.select(dev["q"], kc, Lk, cfg)
+    o, lse = phsa.attn_fwd(dev["q"], dev["k"], dev["v"], sel, cfg)
+    torch.cuda.synchronize()
+    kc_ref = oracle.compress(h["k"], h["punct"], wl.block_size, wl.lam)
+    sel_ref, kth, gap = oracle.select(h["q"], kc_ref, wl.block_size, wl.top_k, wl.n_init_blocks, wl.window, scale,
+                                      Lk, mode=SM)
+    sel_g = sel.cpu().numpy()
+    exempt = check_sel(sel_g, sel_ref, kth, gap,
+                       lambda idx: oracle.score_row(h["q"], kc_ref, wl.block_size, scale, Lk, idx[0], idx[2], idx[1],
+                                                    mode=SM))
+    o_ref, lse_ref = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, wl.block_size, scale)
+    tol = O_TOL[wl.dtype]
+    np.testing.assert_allclose(to_np(o), o_ref, atol=tol, rtol=0)
+    np.testing.assert_allclose(to_np(lse), lse_ref, atol=tol, rtol=0)
+    # the two modes rank differently once a group has several heads
+    logit_sel, _, _ = oracle.select(h["q"], kc_ref, wl.block_size, wl.top_k, wl.n_init_blocks, wl.window, scale, Lk)
+    differ = int((logit_sel != sel_ref).any(-1).sum())
+    log(f"[softmax-sum] {wl.name}: {exempt} exempt rows; {differ} rows differ from summed-logit selection")
+    if wl.n_heads_q == wl.n_heads_kv:
+        assert differ == 0
+
+
+def test_forward_entry_point_uses_mode():
+    wl = CASES[1]
+    cfg = _cfg(wl)
+    host, dev = device_inputs(wl, 4, with_grad_out=False)
+    kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg)
+    sel2 = phsa.select(dev["q"], kc, wl.seqlen_k, cfg)
+    torch.cuda.synchronize()
+    assert torch.equal(sel, sel2)
+
+
+def test_prefill_8k_sampled():
+    wl = WORKLOADS["prefill_8k"]
+    log(f"[softmax-sum] {wl.name}")
+    cfg = _cfg(wl)
+    host, dev = device_inputs(wl, 0, with_grad_out=False)
+    kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg)
+    torch.cuda.synchronize()
+    h = oracle_inputs(host)
+    scale = wl.head_dim ** -0.5
+    L = wl.seqlen_q
+    kc_ref = oracle.compress(h["k"], h["punct"], wl.block_size, wl.lam)
+    rng = np.random.default_rng(8)
+    rows = np.array(sorted(set([0, 63, 64, 65, 200, L // 2, L - 65, L - 64, L - 1]
+                               + rng.integers(0, L, 400).tolist())), dtype=np.int64)
+    sel_r, kth, gap = oracle.select(h["q"], kc_ref, wl.block_size, wl.top_k, wl.n_init_blocks, wl.window, scale,
+                                    wl.seqlen_k, rows=rows, mode=SM)
+    sel_g = sel.cpu().numpy()
+    exempt = check_sel(sel_g[0][:, rows].transpose(1, 0, 2),
+                       sel_r, kth, gap,
+                       lambda idx: oracle.score_row(h["q"], kc_ref, wl.block_size, scale, wl.seqlen_k, 0,
+                                                    int(rows[idx[0]]), idx[1], mode=SM))
+    o_r, lse_r = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, wl.block_size, scale, rows=rows)
+    np.testing.assert_allclose(to_np(o)[0, rows], o_r, atol=O_TOL["bf16"], rtol=0)
+    np.testing.assert_allclose(to_np(lse)[0][:, rows].T, lse_r, atol=O_TOL["bf16"], rtol=0)
+    log(f"[softmax-sum] {wl.name}: {rows.size} rows checked, {exempt} exempt")
+
+
+@pytest.mark.parametrize("L,window,n_init,top_k,B", [(32768, 0, 1, 12, 64), (4096, 128, 2, 5, 8), (192, 0, 1, 12, 8)])
+def test_decode(L, window, n_init, top_k, B):
+    wl = WORKLOADS["decode_32k"].replace(batch=B, seqlen_k=L, window=window, n_init_blocks=n_init, top_k=top_k)
+    log(f"[softmax-sum] decode B={B} L={L} w={window} init={n_init} k={top_k}")
+    cfg = _cfg(wl)
+    host, dev = device_inputs(wl, 5, with_grad_out=False)
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    sel, o, lse = phsa.decode(dev["q"], dev["k"], dev["v"], kc, cfg)
+    torch.cuda.synchronize()
+    h = oracle_inputs(host)
+    scale = wl.head_dim ** -0.5
+    kc_ref = oracle.compress(h["k"], h["punct"], wl.block_size, wl.lam)
+    sel_ref, kth, gap = oracle.select(h["q"], kc_ref, wl.block_size, top_k, n_init, window, scale, L, mode=SM)
+    sel_g = sel.cpu().numpy()
+    exempt = check_sel(sel_g, sel_ref, kth, gap,
+                       lambda idx: oracle.score_row(h["q"], kc_ref, wl.block_size, scale, L, idx[0], idx[2], idx[1],
+                                                    mode=SM))
+    o_r, lse_r = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, wl.block_size, scale)
+    np.testing.assert_allclose(to_np(o), o_r, atol=O_TOL["bf16"], rtol=0)
+    np.testing.assert_allclose(to_np(lse), lse_r, atol=O_TOL["bf16"], rtol=0)
+    log(f"[softmax-sum] decode L={L}: {sel_g.shape[0] * sel_g.shape[1]} rows, {exempt} exempt")
+
+
+def test_decode_varlen():
+    """Per-sequence lengths: each query's softmax covers its own complete blocks only;
+    cache slots past a sequence's length hold NaN."""
+    B, cap, Hq, Hkv, d, m = 6, 4096, 8, 2, 128, 64
+    lens = [1, 64, 65, 130, 2500, cap]
+    cfg = phsa.Config(block_size=m, top_k=5, n_init_blocks=1, window=64, softmax_sum=True)
+    g = torch.Generator().manual_seed(17)
+    k = torch.randn(B, cap, Hkv, d, generator=g)
+    v = torch.randn(B, cap, Hkv, d, generator=g)
+    punct = (torch.rand(B, cap, generator=g) < 0.1).to(torch.uint8)
+    q = torch.randn(B, 1, Hq, d, generator=g).to(torch.bfloat16)
+    k, v = k.to(torch.bfloat16), v.to(torch.bfloat16)
+    kc = phsa.compress(k.cuda(), punct.cuda(), cfg)        # every block pooled; partial blocks are never scored
+    kn, vn = k.clone(), v.clone()
+    for b, n in enumerate(lens):
+        kn[b, n:] = float("nan")
+        vn[b, n:] = float("nan")
+    clen = torch.tensor(lens, dtype=torch.int32).cuda()
+    sel, o, lse = phsa.decode_varlen(q.cuda(), kn.cuda(), vn.cuda(), kc, clen, cfg)
+    torch.cuda.synchronize()
+    scale = d ** -0.5
+    qh, kh, vh = q.float().numpy(), k.float().numpy(), v.float().numpy()
+    kc_ref = oracle.compress(kh, punct.numpy(), m, cfg.lam)
+    sel_g, o_g, lse_g = sel.cpu().numpy(), to_np(o), lse.cpu().numpy()
+    for b, n in enumerate(lens):
+        pad = -(-n // m) * m
+        ref, kth, gap = oracle.select(qh[b:b + 1], kc_ref[b:b + 1, :, :pad // m], m, cfg.top_k, cfg.n_init_blocks,
+                                      cfg.window, scale, pad, q_pos0=n - 1, mode=SM)
+        check_sel(sel_g[b:b + 1], ref, kth, gap,
+                  lambda idx: oracle.score_row(qh[b:b + 1], kc_ref[b:b + 1, :, :pad // m], m, scale, pad, 0, 0,
+                                               idx[1], q_pos0=n - 1, mode=SM))
+        o_r, lse_r = oracle.attn_fwd(qh[b:b + 1], kh[b:b + 1, :pad], vh[b:b + 1, :pad], sel_g[b:b + 1], m, scale,
+                                     q_pos0=n - 1)
+        np.testing.assert_allclose(o_g[b:b + 1], o_r, atol=O_TOL["bf16"], rtol=0)
+        np.testing.assert_allclose(lse_g[b:b + 1], lse_r, atol=O_TOL["bf16"], rtol=0)
