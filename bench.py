@@ -15,6 +15,7 @@ CPU oracle timed on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -275,6 +276,43 @@ def bench_punct(seed: int):
     return {"workload": "4 x 32768 token ids, 60 punctuation ids", "ms": ms, "GB_per_s": nbytes / 1e9 / (ms / 1e3)}
 
 
+def bench_select_modes(seed: int):
+    """Block selection alone on the 4 x 32768 training batch in both group
+    aggregation modes: summed logits (the training step's mode) and summed
+    per-head softmax.  The softmax mode computes, per (row, head), a logit for
+    every complete causal block (normaliser) and again for every candidate."""
+    wl = WORKLOADS["train_32k"]
+    B, L, Hq, Hkv, d, m = wl.batch, wl.seqlen_k, wl.n_heads_q, wl.n_heads_kv, wl.head_dim, wl.block_size
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(seed + 5)
+    q = torch.randn(B, L, Hq, d, generator=gen).to(torch.bfloat16).cuda()
+    k = torch.randn(B, L, Hkv, d, generator=gen).to(torch.bfloat16).cuda()
+    punct = (torch.rand(B, L, generator=gen) < 0.08).to(torch.uint8).cuda()
+    out = {"workload": "train_32k selection: 4 x 32768 queries, 16/8 heads, d 128, 512 blocks, 12 free picks"}
+    cur = np.arange(L) // m
+    G = Hq // Hkv
+    cand = np.maximum(cur - wl.n_init_blocks - wl.window // m, 0).sum()
+    for name, sm in (("summed_logits", False), ("softmax_sum", True)):
+        cfg = dataclasses.replace(cfg_of(wl), softmax_sum=sm)
+        kc = phsa.compress(k, punct, cfg)
+        for _ in range(2):
+            phsa.select(q, kc, L, cfg)
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(5):
+            phsa.select(q, kc, L, cfg)
+        ev1.record()
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / 5
+        if sm:
+            flop = 2.0 * d * B * Hkv * G * (cur.sum() + cand)   # fp32 FMAs on the vector units
+        else:
+            flop = 2.0 * d * B * Hkv * cand                     # one dot per (row, group, candidate)
+        out[name] = {"ms": ms, "score_tflop": flop / 1e12, "TFLOP_per_s": flop / 1e12 / (ms / 1e3)}
+    return out
+
+
 def cpu_baseline(host, wl, prefix: int):
     """The fp64 oracle on a causal prefix of batch 0 (all heads): a complete PHSA
     sub-problem, timed end to end (compress, select, forward, backward)."""
@@ -380,6 +418,7 @@ def main():
         result["decode"] = bench_decode(40, args.seed)
         result["generation_step"] = bench_generation(40, args.seed)
         result["punct_mask"] = bench_punct(args.seed)
+        result["select_modes"] = bench_select_modes(args.seed)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(tr["host"], WORKLOADS["train_32k"], args.cpu_prefix)
     print(json.dumps(result))
