@@ -81,7 +81,9 @@ typedef struct {
   int32_t n_heads_q;     /* Hq, a multiple of n_heads_kv */
   int32_t n_heads_kv;    /* Hkv >= 1 */
   int32_t head_dim;      /* d; the kernels implement 64 and 128 */
-  int32_t block_size;    /* m, tokens per key block (Eq. 3); the kernels implement 64 */
+  int32_t block_size;    /* m, tokens per key block (Eq. 3).  compress/select take any m;
+                            attention takes 16, 32 and 64 (bf16 forward/backward with
+                            m < 64 also need seqlen_k to be a multiple of 64) */
   int32_t top_k;         /* k, free picks after the forced blocks are excluded */
   int32_t n_init_blocks; /* n_init, blocks 0..n_init-1 always kept (clipped to causal) */
   int32_t window;        /* w, local window in tokens, a multiple of block_size;

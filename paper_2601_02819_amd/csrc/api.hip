@@ -44,12 +44,57 @@ size_t index_layout(const Geom &g, char *base, IndexWs *ix) {
   return off;
 }
 
+// bf16 attention with blocks of m = 16 or 32 tokens runs on 64-key tiles:
+// the selection is regrouped per tile with a mask of its 16-key quarters.
+bool tiles_coarsened(const Geom &g) { return g.dtype == PHSA_BF16 && g.m != 64; }
+
+// Tile geometry: m = 64, T = Lk / 64, and ksel = a bound on the distinct tiles
+// of a row: the init blocks cover ceil(n_init m / 64) tiles, the local blocks
+// (w + m tokens starting on an m boundary) at most ceil(w / 64) + 1, and each
+// free pick one.
+Geom tile_geom(const Geom &g) {
+  if (!tiles_coarsened(g)) return g;
+  Geom t = g;
+  t.m = 64;
+  t.T = g.Lk / 64;
+  const int bound = (g.n_init * g.m + 63) / 64 + (g.window + 63) / 64 + 1 + g.top_k;
+  t.ksel = std::min(g.ksel, bound);
+  t.n_init = (g.n_init * g.m + 63) / 64;
+  t.window = 0;
+  return t;
+}
+
+struct Coarse {
+  Geom gc;            // tile geometry (== g when not coarsened)
+  int32_t *csel;      // [B, Hkv, Lq, gc.ksel] tiles per row, NULL when not coarsened
+  uint8_t *cq;        // [B, Hkv, Lq, gc.ksel] quarter masks
+};
+
+// The coarsened selection sits at the start of the forward and backward
+// workspaces, followed by the index, so a backward that reuses the forward's
+// index finds it at the same place.
+size_t coarse_layout(const Geom &g, char *base, Coarse *c) {
+  Coarse w{tile_geom(g), nullptr, nullptr};
+  size_t off = 0;
+  if (tiles_coarsened(g)) {
+    const size_t n = (size_t)g.B * g.Hkv * g.Lq * w.gc.ksel;
+    w.csel = base ? reinterpret_cast<int32_t *>(base) : nullptr;
+    off += align_up(n * sizeof(int32_t));
+    w.cq = base ? reinterpret_cast<uint8_t *>(base + off) : nullptr;
+    off += align_up(n);
+  }
+  if (c) *c = w;
+  return off;
+}
+
 struct FwdWs {
+  Coarse co;
   IndexWs ix;
   void *opart;
   float2 *ml;
 };
 struct BwdWs {
+  Coarse co;
   IndexWs ix;
   float *Dvec;
   void *dqpart;
@@ -58,10 +103,12 @@ struct BwdWs {
 
 size_t elem_bytes(const Geom &g) { return g.dtype == PHSA_BF16 ? 2 : 4; }
 
-size_t fwd_layout(const Geom &g, char *base, FwdWs *ws) {
-  if (g.dtype == PHSA_FP32) return 0;
+size_t fwd_layout(const Geom &g0, char *base, FwdWs *ws) {
+  if (g0.dtype == PHSA_FP32) return 0;
   FwdWs w{};
-  size_t off = index_layout(g, base, &w.ix);
+  size_t off = coarse_layout(g0, base, &w.co);
+  const Geom &g = w.co.gc;
+  off += index_layout(g, base ? base + off : nullptr, &w.ix);
   // partials in list order, one per (entry, head), plus one discard row that
   // absorbs the stores of rows past the end of a chunk
   const int64_t slots = w.ix.nnz_max * g.G + 1;
@@ -73,10 +120,15 @@ size_t fwd_layout(const Geom &g, char *base, FwdWs *ws) {
   return off;
 }
 
-size_t bwd_layout(const Geom &g, char *base, BwdWs *ws) {
+size_t bwd_layout(const Geom &g0, char *base, BwdWs *ws) {
   BwdWs w{};
+  w.co = Coarse{tile_geom(g0), nullptr, nullptr};
+  const Geom g = w.co.gc;
   size_t off = 0;
-  if (g.dtype == PHSA_BF16) off = index_layout(g, base, &w.ix);
+  if (g.dtype == PHSA_BF16) {
+    off = coarse_layout(g0, base, &w.co);
+    off += index_layout(g, base ? base + off : nullptr, &w.ix);
+  }
   w.Dvec = base ? reinterpret_cast<float *>(base + off) : nullptr;
   off += align_up(sizeof(float) * (size_t)g.B * g.Hq * g.Lq);
   if (g.dtype == PHSA_BF16) {
@@ -119,14 +171,23 @@ phsa_status validate(const phsa_params *p, int op, Geom *out) {
   const int G = p->n_heads_q / p->n_heads_kv;
   if (ksel > 64 || p->top_k > 32) return PHSA_ERR_UNSUPPORTED;
   if (T > 2048 || p->seqlen_q >= (1 << 25)) return PHSA_ERR_UNSUPPORTED;
+  // bf16 attention on blocks below 64 tokens runs on 64-key tiles (quarter masks)
+  const bool coarse = p->dtype == PHSA_BF16 && p->block_size != 64;
+  const int64_t ksel_tiles =
+      coarse ? std::min<int64_t>(ksel, ((int64_t)p->n_init_blocks * p->block_size + 63) / 64 + (p->window + 63) / 64 +
+                                           1 + p->top_k)
+             : ksel;
   if (p->batch > 65535 || p->n_heads_q > 65535 || (int64_t)p->batch * p->n_heads_kv > 65535)
     return PHSA_ERR_UNSUPPORTED;  // grid y/z extents
   // the softmax-sum kernels give each lane one (row, head) pair, at most 8 heads in decode
   if ((p->flags & PHSA_FLAG_SELECT_SOFTMAX_SUM) && (G > 64 || 64 % G != 0)) return PHSA_ERR_UNSUPPORTED;
   if (is_attention_op(op)) {
-    if (p->block_size != 64) return PHSA_ERR_UNSUPPORTED;
+    if (p->block_size != 64 && p->block_size != 32 && p->block_size != 16) return PHSA_ERR_UNSUPPORTED;
     if (G != 1 && G != 2 && G != 4 && G != 8) return PHSA_ERR_UNSUPPORTED;
-    const int64_t nnz = (int64_t)p->batch * p->n_heads_kv * p->seqlen_q * ksel;
+    if (p->seqlen_q >= (1 << 21)) return PHSA_ERR_UNSUPPORTED;  // index entries hold the row in 21 bits
+    // the 64-key tiles of m-token blocks must not run past the keys
+    if (coarse && op != PHSA_OP_DECODE && p->seqlen_k % 64 != 0) return PHSA_ERR_UNSUPPORTED;
+    const int64_t nnz = (int64_t)p->batch * p->n_heads_kv * p->seqlen_q * ksel_tiles;
     if (nnz >= ((int64_t)1 << 31) / 2) return PHSA_ERR_UNSUPPORTED;
   }
   if (out) {
@@ -175,6 +236,21 @@ phsa_status check_ws(const Geom &g, int op, const void *ws, size_t ws_bytes) {
 }
 
 phsa_status from_hip(hipError_t e) { return e == hipSuccess ? PHSA_OK : PHSA_ERR_HIP; }
+
+// bf16 forward attention over sel: regroup m-token blocks into 64-key tiles
+// when m < 64, then index, sparse kernel and merge.
+hipError_t attn_fwd_bf16(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel, void *O,
+                         float *LSE, void *ws, hipStream_t s) {
+  FwdWs w;
+  fwd_layout(g, static_cast<char *>(ws), &w);
+  const int32_t *tsel = sel;
+  if (w.co.csel) {
+    const hipError_t e = launch_coarsen(g, w.co.gc, sel, w.co.csel, w.co.cq, s);
+    if (e != hipSuccess) return e;
+    tsel = w.co.csel;
+  }
+  return launch_attn_fwd(w.co.gc, Q, K, V, tsel, w.co.cq, O, LSE, w.ix, w.opart, w.ml, s);
+}
 
 // ---------------------------------------------------------------- timing
 struct TimingRec {
@@ -295,9 +371,7 @@ phsa_status phsa_attn_fwd(const phsa_params *p, const void *Q, const void *K, co
     if (g.dtype == PHSA_FP32)
       return from_hip(launch_attn_fwd_fp32(g, static_cast<const float *>(Q), static_cast<const float *>(K),
                                            static_cast<const float *>(V), sel, static_cast<float *>(O), LSE, s));
-    FwdWs w;
-    fwd_layout(g, static_cast<char *>(ws), &w);
-    return from_hip(launch_attn_fwd(g, Q, K, V, sel, O, LSE, w.ix, w.opart, w.ml, s));
+    return from_hip(attn_fwd_bf16(g, Q, K, V, sel, O, LSE, ws, s));
   })
 }
 
@@ -319,8 +393,16 @@ phsa_status phsa_attn_bwd(const phsa_params *p, const void *Q, const void *K, co
                                            static_cast<const float *>(dO), LSE, sel, static_cast<float *>(dQ),
                                            static_cast<float *>(dK), static_cast<float *>(dV), w.Dvec, s));
     const bool reuse = (p->flags & PHSA_FLAG_REUSE_INDEX) != 0;
-    return from_hip(
-        launch_attn_bwd(g, Q, K, V, O, dO, LSE, sel, dQ, dK, dV, w.ix, w.Dvec, w.dqpart, w.dkvpart, reuse, s));
+    const int32_t *tsel = sel;
+    if (w.co.csel) {  // tiles of the m-token blocks (already there when the index is reused)
+      if (!reuse) {
+        const hipError_t e = launch_coarsen(g, w.co.gc, sel, w.co.csel, w.co.cq, s);
+        if (e != hipSuccess) return PHSA_ERR_HIP;
+      }
+      tsel = w.co.csel;
+    }
+    return from_hip(launch_attn_bwd(w.co.gc, Q, K, V, O, dO, LSE, tsel, w.co.cq, dQ, dK, dV, w.ix, w.Dvec, w.dqpart,
+                                    w.dkvpart, reuse, s));
   })
 }
 
@@ -339,9 +421,7 @@ phsa_status phsa_forward(const phsa_params *p, const void *Q, const void *K, con
     if (g.dtype == PHSA_FP32)
       return from_hip(launch_attn_fwd_fp32(g, static_cast<const float *>(Q), static_cast<const float *>(K),
                                            static_cast<const float *>(V), sel, static_cast<float *>(O), LSE, s));
-    FwdWs w;
-    fwd_layout(g, static_cast<char *>(ws), &w);
-    return from_hip(launch_attn_fwd(g, Q, K, V, sel, O, LSE, w.ix, w.opart, w.ml, s));
+    return from_hip(attn_fwd_bf16(g, Q, K, V, sel, O, LSE, ws, s));
   })
 }
 

@@ -6,7 +6,9 @@
 //   dQ_i = scale * sum_j dS_ij k_j
 //   dK_j = scale * sum_i dS_ij q_i
 // where i ranges over the query rows (all heads of the group) that selected
-// the block of key j and are causally allowed to see j.
+// the block of key j and are causally allowed to see j.  With blocks of 16 or
+// 32 tokens a 64-key tile holds several blocks; a list entry's quarter mask
+// says which 16-key quarters its row selected (wave w's keys are quarter w).
 //
 // Like the forward, the main kernel is key-block-major over the inverted
 // index.  A work unit keeps K_t and V_t in LDS (wave w owns keys
@@ -120,7 +122,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   uint4 pq[NV], pd[NV];
   int pe[NV];
   float plse = 0.f, pdd = 0.f;
-  int ppos = -1;
+  int ppos = 0;
   auto load_entries = [&](int c0) {
     const int ntok = min(CT, n_ent - c0);
 #pragma unroll
@@ -138,22 +140,22 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       pe[k] = ne[k];
       pq[k] = pd[k] = make_uint4(0u, 0u, 0u, 0u);
       if (pe[k] >= 0) {
-        const int64_t src = (((int64_t)b * gm.Lq + (pe[k] >> 6)) * gm.Hq + g * G + r % G) * D + c;
+        const int64_t src = (((int64_t)b * gm.Lq + (pe[k] >> 10)) * gm.Hq + g * G + r % G) * D + c;
         pq[k] = *reinterpret_cast<const uint4 *>(Q + src);
         pd[k] = *reinterpret_cast<const uint4 *>(dO + src);
       }
     }
     if (tid < 64) {
       if (nrow >= 0) {
-        const int i = nrow >> 6;
+        const int i = nrow >> 10;
         const int h = g * G + tid % G;
         plse = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + i];  // scaled when staged, so nothing waits here
         pdd = Dvec[((int64_t)b * gm.Lq + i) * gm.Hq + h];
-        ppos = gm.q_pos0 + i;
+        ppos = (gm.q_pos0 + i) | (((nrow >> 6) & 15) << 27);  // position, and the quarters the row attends to
       } else {
         plse = 0.f;
         pdd = 0.f;
-        ppos = -1;
+        ppos = 0;  // no quarter: nothing allowed
       }
     }
   };
@@ -211,7 +213,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       bf16_t dsq[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = key <= posv[r] ? exp2f(s[mt][r] * sl2 - lsev[r]) : 0.f;
+        // the wave's 16 keys are quarter `wave` of the block
+        const bool ok = ((posv[r] >> (27 + wave)) & 1) && key <= (posv[r] & 0x7ffffff);
+        const float p = ok ? exp2f(s[mt][r] * sl2 - lsev[r]) : 0.f;
         const float ds = p * (dp[mt][r] - ddv[r]);
         s[mt][r] = p;
         dp[mt][r] = ds;
@@ -427,13 +431,13 @@ hipError_t launch_bwd_pre(const Geom &g, const void *O, const void *dO, float *D
 }
 
 hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
-                           const void *dO, const float *LSE, const int32_t *sel, void *dQ, void *dK, void *dV,
-                           const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart, bool reuse_index,
-                           hipStream_t s) {
+                           const void *dO, const float *LSE, const int32_t *sel, const uint8_t *quarters, void *dQ,
+                           void *dK, void *dV, const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart,
+                           bool reuse_index, hipStream_t s) {
   hipError_t e = launch_bwd_pre(g, O, dO, Dvec, s);
   if (e != hipSuccess) return e;
   if (!reuse_index) {
-    e = launch_build_index(g, sel, ix, s);
+    e = launch_build_index(g, sel, quarters, ix, s);
     if (e != hipSuccess) return e;
   }
   return g.d == 128 ? launch_bwd_d<128>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, s)

@@ -22,6 +22,10 @@
 // key set, so P never goes through LDS.  O^T leaves each lane with 4
 // consecutive features of one row (8-byte stores).
 //
+// Blocks of 16 or 32 tokens run on the same 64-key tiles: each list entry
+// carries the mask of the 16-key quarters its row selected, and keys of the
+// other quarters get zero weight (key tile kt of S^T is quarter kt).
+//
 // Output per list entry (row, slot), stored in list order so that a unit
 // writes one contiguous run: the unnormalised partial O (bf16) and (m, l) in
 // log2 units.  A second kernel merges the at most Ksel partials of each row:
@@ -85,7 +89,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
     return tk < n_ent ? v : -1;
   };
   auto fetch = [&](int e, bf16x8 (&qf)[KB]) {
-    const int64_t row = e >= 0 ? (e >> 6) : 0;  // an empty chunk row is masked to zero weight
+    const int64_t row = e >= 0 ? (e >> 10) : 0;  // an empty chunk row is masked to zero weight
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
       qf[kb] = load_bf16x8(Q + (((int64_t)b * gm.Lq + row) * gm.Hq + g * G + hh) * D + kb * 32 + kq);
@@ -106,13 +110,16 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
         st[kt] = mfma16x16x32(load_bf16x8(&Ks[(kt * 16 + l16) * KP + kb * 32 + kq]), q[kb], st[kt]);
-    const int pos = e >= 0 ? gm.q_pos0 + (e >> 6) : -1;
+    // key tile kt is quarter kt of the block: allowed if the row selected it
+    const int pos = e >= 0 ? gm.q_pos0 + (e >> 10) : -1;
+    const int qm = e >= 0 ? (e >> 6) & 15 : 0;
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float v = (key0 + kt * 16 + q4 * 4 + r) <= pos ? st[kt][r] * sl2 : -INFINITY;
+        const bool ok = ((qm >> kt) & 1) && (key0 + kt * 16 + q4 * 4 + r) <= pos;
+        const float v = ok ? st[kt][r] * sl2 : -INFINITY;
         st[kt][r] = v;
         mx = fmaxf(mx, v);
       }
@@ -270,8 +277,9 @@ static hipError_t launch_fwd_d(const Geom &g, const void *Q, const void *K, cons
 }
 
 hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel,
-                           void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s) {
-  hipError_t e = launch_build_index(g, sel, ix, s);
+                           const uint8_t *quarters, void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml,
+                           hipStream_t s) {
+  hipError_t e = launch_build_index(g, sel, quarters, ix, s);
   if (e != hipSuccess) return e;
   return g.d == 128 ? launch_fwd_d<128>(g, Q, K, V, sel, O, LSE, ix, opart, ml, s)
                     : launch_fwd_d<64>(g, Q, K, V, sel, O, LSE, ix, opart, ml, s);

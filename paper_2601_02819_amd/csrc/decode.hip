@@ -273,12 +273,12 @@ __global__ __launch_bounds__(256, 2) void decode_attn_kernel(const T *__restrict
   for (int s = wave; s < gm.ksel; s += 4) {
     const int t = sel[(int64_t)bg * gm.ksel + s];
     if (t < 0 || t > cur || t >= gm.T) continue;  // wave-uniform
-    for (int k0 = 0; k0 < 64; k0 += KG) {
+    for (int k0 = 0; k0 < gm.m; k0 += KG) {
       uint4 kr[NI], vr[NI];
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
-        const int key = k0 + i * KPI + sub;
-        const int64_t src = (((int64_t)b * gm.Lk + (int64_t)t * 64 + key) * gm.Hkv + g) * D + ch * VEC;
+        const int key = min(k0 + i * KPI + sub, gm.m - 1);  // rows past a short block are masked below
+        const int64_t src = (((int64_t)b * gm.Lk + (int64_t)t * gm.m + key) * gm.Hkv + g) * D + ch * VEC;
         kr[i] = *reinterpret_cast<const uint4 *>(K + src);
         vr[i] = *reinterpret_cast<const uint4 *>(V + src);
       }
@@ -294,7 +294,8 @@ __global__ __launch_bounds__(256, 2) void decode_attn_kernel(const T *__restrict
           for (int e = 0; e < VEC; ++e) a = fmaf(qv[h][e], to_f32<T>(pk[e]), a);
 #pragma unroll
           for (int x = 1; x < CPR; x <<= 1) a += __shfl_xor(a, x, 64);
-          sc[i] = (t * 64 + k0 + i * KPI + sub) <= pos ? a : -INFINITY;
+          const int kb = k0 + i * KPI + sub;
+          sc[i] = kb < gm.m && t * gm.m + kb <= pos ? a : -INFINITY;
           bm = fmaxf(bm, sc[i]);
         }
 #pragma unroll
@@ -310,7 +311,8 @@ __global__ __launch_bounds__(256, 2) void decode_attn_kernel(const T *__restrict
         for (int i = 0; i < NI; ++i) {
           // keys past the query (the unwritten tail of its own block) add nothing,
           // whatever their V slots hold
-          const bool valid = (t * 64 + k0 + i * KPI + sub) <= pos;
+          const int kb = k0 + i * KPI + sub;
+          const bool valid = kb < gm.m && t * gm.m + kb <= pos;
           const float p = valid ? exp2f(sc[i] - mn) : 0.f;
           ls += p;
           const T *pv = reinterpret_cast<const T *>(&vr[i]);

@@ -4,10 +4,12 @@
 // its list).  This lets the attention kernels run key-block-major: one K/V
 // tile is loaded once and meets every query row that selected it.
 //
-// Entries are (row << 6) | slot, where slot is the position of t in the row's
-// sel vector.  The attention kernels store per-entry partial results in list
-// order (contiguous per work unit); pmap[(row, slot)] = list position lets the
-// per-row merges find them.
+// Entries are (row << 10) | (quarters << 6) | slot, where slot is the
+// position of t in the row's sel vector and quarters is a 4-bit mask of the
+// 16-key quarters of block t the row attends to (all four for 64-token
+// blocks; see coarsen_kernel for smaller ones).  The attention kernels store
+// per-entry partial results in list order (contiguous per work unit);
+// pmap[(row, slot)] = list position lets the per-row merges find them.
 //
 // Four integer-only passes, all deterministic (no order depends on timing):
 //   count : per 256-row tile, an LDS bitmap [T][256 bits] of who selected
@@ -110,7 +112,8 @@ __global__ __launch_bounds__(1024) void index_scan_lists_kernel(Geom gm, IndexWs
   }
 }
 
-__global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restrict__ sel, Geom gm, IndexWs ix) {
+__global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restrict__ sel,
+                                                         const uint8_t *__restrict__ quarters, Geom gm, IndexWs ix) {
   extern __shared__ uint32_t bm[];
   int32_t *pm = reinterpret_cast<int32_t *>(bm + gm.T * 8);  // [kIndexTile][ksel] staged position map
   const int w = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x;
@@ -129,7 +132,8 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
         int rank = __popc(bm[t * 8 + word] & below);
         for (int k = 0; k < word; ++k) rank += __popc(bm[t * 8 + k]);
         pos = ix.off[bg * gm.T + t] + tile_off[t] + rank;
-        ix.tok[pos] = (i << 6) | s;
+        const int qm = quarters ? quarters[((int64_t)bg * gm.Lq + i) * gm.ksel + s] & 15 : 15;
+        ix.tok[pos] = (i << 10) | (qm << 6) | s;
       }
       pm[tid * gm.ksel + s] = pos;
     }
@@ -141,7 +145,71 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
   for (int x = tid; x < nrow * gm.ksel; x += 256) dst[x] = pm[x];
 }
 
-hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &ix, hipStream_t s) {
+// Blocks of m = 16 or 32 tokens run on the 64-key attention tiles: the
+// m-token blocks a row selected are grouped by the 64-token tile that holds
+// them (tile = block / (64 / m)), and each tile gets the mask of the 16-key
+// quarters its selected blocks cover.  The input rows are ascending, so a
+// row's blocks in one tile are adjacent.  gc is the tile geometry (m = 64,
+// T = Lk / 64, ksel = a bound on the tiles per row).  The rows of a 128-row
+// group are staged through LDS so that the reads are coalesced.
+constexpr int kCoarsenRows = 128;
+__global__ __launch_bounds__(kCoarsenRows) void coarsen_kernel(const int32_t *__restrict__ sel, Geom g, Geom gc,
+                                                               int32_t *__restrict__ csel,
+                                                               uint8_t *__restrict__ cq) {
+  extern __shared__ int32_t rows_s[];  // [kCoarsenRows][g.ksel]
+  const int64_t nrows = (int64_t)g.B * g.Hkv * g.Lq;
+  const int64_t x0 = (int64_t)blockIdx.x * kCoarsenRows;
+  const int nr = (int)min((int64_t)kCoarsenRows, nrows - x0);
+  for (int v = threadIdx.x; v < nr * g.ksel; v += kCoarsenRows) rows_s[v] = sel[x0 * g.ksel + v];
+  __syncthreads();
+  const int r = threadIdx.x;
+  if (r >= nr) return;
+  const int64_t x = x0 + r;
+  const int i = (int)(x % g.Lq);
+  const int cur = (g.q_pos0 + i) / g.m;
+  const int per = 64 / g.m, qpb = g.m / 16;  // blocks per tile, quarters per block
+  int32_t *out = csel + x * gc.ksel;
+  uint8_t *oq = cq + x * gc.ksel;
+  int n = 0, last = -1;
+  unsigned msk = 0u;
+  for (int s = 0; s < g.ksel; ++s) {
+    const int t = rows_s[r * g.ksel + s];
+    if (t < 0 || t > cur || t >= g.T) continue;
+    const int tc = t / per;
+    if (tc != last) {
+      if (last >= 0 && n < gc.ksel) {
+        out[n] = last;
+        oq[n] = (uint8_t)msk;
+        ++n;
+      }
+      last = tc;
+      msk = 0u;
+    }
+    msk |= ((1u << qpb) - 1u) << ((t % per) * qpb);
+  }
+  if (last >= 0 && n < gc.ksel) {
+    out[n] = last;
+    oq[n] = (uint8_t)msk;
+    ++n;
+  }
+  for (; n < gc.ksel; ++n) {
+    out[n] = -1;
+    oq[n] = 0;
+  }
+}
+
+hipError_t launch_coarsen(const Geom &g, const Geom &gc, const int32_t *sel, int32_t *csel, uint8_t *cq,
+                          hipStream_t s) {
+  const int64_t nrows = (int64_t)g.B * g.Hkv * g.Lq;
+  timing_begin("phsa_coarsen", s);
+  hipLaunchKernelGGL(coarsen_kernel, dim3((unsigned)((nrows + kCoarsenRows - 1) / kCoarsenRows)),
+                     dim3(kCoarsenRows), (size_t)kCoarsenRows * g.ksel * sizeof(int32_t), s, sel, g, gc, csel, cq);
+  timing_end(s);
+  return hipGetLastError();
+}
+
+hipError_t launch_build_index(const Geom &g, const int32_t *sel, const uint8_t *quarters, const IndexWs &ix,
+                              hipStream_t s) {
   const int nbgt = g.B * g.Hkv * g.T;
   const size_t lds = (size_t)g.T * 8 * sizeof(uint32_t);
   timing_begin("phsa_index_count", s);
@@ -155,7 +223,7 @@ hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &
   timing_end(s);
   timing_begin("phsa_index_fill", s);
   hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds + (size_t)kIndexTile * g.ksel * 4,
-                     s, sel, g, ix);
+                     s, sel, quarters, g, ix);
   timing_end(s);
   return hipGetLastError();
 }

@@ -30,7 +30,7 @@ struct IndexWs {
   int32_t *off;       // [B*Hkv*T + 1]  list start per (b, g, t)
   int32_t *uoff;      // [B*Hkv*T + 1]  first work unit per (b, g, t)
   int32_t *totals;    // [4]            nnz, n_units
-  int32_t *tok;       // [nnz_max]      (query row << 6) | slot, ascending row per list
+  int32_t *tok;       // [nnz_max]      (query row << 10) | (quarter mask << 6) | slot, ascending row per list
   int32_t *pmap;      // [B*Hkv*Lq*Ksel] list position of each valid (row, slot); partials are
                       //                 stored in list order and the merges gather through this map
   int2 *units;        // [units_max]    (b*Hkv*T + g*T + t, first list entry)
@@ -48,13 +48,20 @@ hipError_t launch_compress(const Geom &g, const void *K, const uint8_t *punct, f
 // ws: select_split_bytes(g) bytes (bf16 hi/lo copies of K_comp), unused for float32
 size_t select_split_bytes(const Geom &g);
 hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t *sel, void *ws, hipStream_t s);
-hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &ix, hipStream_t s);
+// quarters: per (row, slot) mask of the 16-key quarters of the block the row
+// attends to, NULL = all four (64-token blocks)
+hipError_t launch_build_index(const Geom &g, const int32_t *sel, const uint8_t *quarters, const IndexWs &ix,
+                              hipStream_t s);
+// m-token blocks (m = 16, 32) -> 64-key tiles with quarter masks; gc = tile geometry
+hipError_t launch_coarsen(const Geom &g, const Geom &gc, const int32_t *sel, int32_t *csel, uint8_t *cq,
+                          hipStream_t s);
 hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel,
-                           void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s);
-hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
-                           const void *dO, const float *LSE, const int32_t *sel, void *dQ, void *dK, void *dV,
-                           const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart, bool reuse_index,
+                           const uint8_t *quarters, void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml,
                            hipStream_t s);
+hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
+                           const void *dO, const float *LSE, const int32_t *sel, const uint8_t *quarters, void *dQ,
+                           void *dK, void *dV, const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart,
+                           bool reuse_index, hipStream_t s);
 hipError_t launch_bwd_pre(const Geom &g, const void *O, const void *dO, float *Dvec, hipStream_t s);
 hipError_t launch_attn_fwd_fp32(const Geom &g, const float *Q, const float *K, const float *V,
                                 const int32_t *sel, float *O, float *LSE, hipStream_t s);

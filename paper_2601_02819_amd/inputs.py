@@ -75,6 +75,12 @@ WORKLOADS: Dict[str, Workload] = {
     "prefill_32k": Workload("prefill_32k", 1, 32768, 32768, 16, 8, 128, 64, 12, 1, 0, "bf16"),
     "decode_32k": Workload("decode_32k", 64, 1, 32768, 16, 8, 128, 64, 12, 1, 0, "bf16"),
     "train_32k": Workload("train_32k", 4, 32768, 32768, 16, 8, 128, 64, 12, 1, 0, "bf16", backward=True),
+    # the paper's own 32k training setting (Section 4.1, model configuration, and
+    # Top-K = 16 in Section 4.2): 16-token blocks, 128 init tokens (8 blocks), a
+    # 512-token local window (32 blocks + the query's own) and 16 free picks:
+    # 57 blocks = 912 tokens per query
+    "train_32k_paper": Workload("train_32k_paper", 4, 32768, 32768, 16, 8, 128, 16, 16, 8, 512, "bf16",
+                                backward=True),
 }
 
 

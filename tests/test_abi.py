@@ -50,7 +50,12 @@ def _p(**kw):
     ({"softmax_scale": float("inf")}, phsa.OP_SELECT, phsa.ERR_INVALID_ARG),
     ({"head_dim": 96}, phsa.OP_SELECT, phsa.ERR_UNSUPPORTED),
     ({"top_k": 40}, phsa.OP_SELECT, phsa.ERR_UNSUPPORTED),
-    ({"block_size": 32}, phsa.OP_ATTN_FWD, phsa.ERR_UNSUPPORTED),
+    ({"block_size": 8}, phsa.OP_ATTN_FWD, phsa.ERR_UNSUPPORTED),
+    ({"block_size": 32}, phsa.OP_ATTN_FWD, phsa.OK),
+    ({"block_size": 16, "n_init_blocks": 8, "window": 512, "top_k": 16}, phsa.OP_ATTN_BWD, phsa.OK),
+    ({"block_size": 16, "seqlen_k": 1040, "seqlen_q": 1040}, phsa.OP_ATTN_FWD, phsa.ERR_UNSUPPORTED),  # Lk % 64
+    ({"block_size": 16, "seqlen_k": 1040, "seqlen_q": 1040, "dtype": phsa.FP32}, phsa.OP_ATTN_FWD, phsa.OK),
+    ({"block_size": 16, "seqlen_k": 1040, "seqlen_q": 1}, phsa.OP_DECODE, phsa.OK),
     ({"block_size": 32}, phsa.OP_SELECT, phsa.OK),
     ({"n_heads_q": 6, "n_heads_kv": 2}, phsa.OP_ATTN_FWD, phsa.ERR_UNSUPPORTED),   # G = 3
     ({"seqlen_q": 2}, phsa.OP_DECODE, phsa.ERR_SHAPE),
@@ -85,6 +90,13 @@ def test_ksel_and_workspace():
     assert phsa.workspace_size(_p(dtype=phsa.FP32), phsa.OP_ATTN_FWD) == 0
     assert phsa.workspace_size(_p(seqlen_q=1), phsa.OP_DECODE) == 0          # decode needs no scratch
     assert phsa.workspace_size(_p(head_dim=96), phsa.OP_ATTN_FWD) == 0     # invalid -> 0
+    # 16-token blocks: the workspace adds the regrouped tile selection (int32 + mask byte per slot)
+    # and the index/partials are sized by the tiles per row, bounded by 2 + 9 + 16 = 27 < Ksel = 57
+    paper = dict(block_size=16, n_init_blocks=8, window=512, top_k=16)
+    w16 = phsa.workspace_size(_p(**paper), phsa.OP_ATTN_FWD)
+    w64 = phsa.workspace_size(_p(top_k=25), phsa.OP_ATTN_FWD)    # 27 slots per row at m = 64
+    rows = 1 * 1 * 1024
+    assert w16 - w64 == -(-rows * 27 * 4 // 256) * 256 + -(-rows * 27 // 256) * 256
     assert L.phsa_validate(None, phsa.OP_SELECT) == phsa.ERR_NULL
 
 

@@ -1,0 +1,167 @@
+"""GPU parity with blocks of 16 and 32 tokens (the paper's 32k geometry uses
+m = 16, 8 init blocks, a 512-token window and 16 free picks).  The bf16
+attention kernels run such blocks on 64-key tiles with per-row quarter masks;
+the oracle works on the m-token blocks directly."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2601_02819_amd import phsa
+from paper_2601_02819_amd.inputs import WORKLOADS, Workload
+from tests.gpu_common import (GRAD_REL_L2, O_TOL, cfg_of, check_sel, device_inputs, log, oracle_inputs, rel_l2,
+                              to_np)
+
+pytestmark = pytest.mark.gpu
+
+
+def wl_(name, B, L, Hq, Hkv, d, m, top_k, n_init, window, dtype="bf16", Lq=None):
+    return Workload(name, B, Lq or L, L, Hq, Hkv, d, m, top_k, n_init, window, dtype)
+
+
+CASES = [
+    wl_("m16_small", 1, 1024, 4, 2, 128, 16, 5, 2, 64),
+    wl_("m16_paper_2k", 1, 2048, 4, 2, 128, 16, 16, 8, 512),
+    wl_("m16_g8_d64", 1, 1024, 8, 1, 64, 16, 9, 1, 0),
+    wl_("m16_g1", 2, 768, 2, 2, 128, 16, 12, 3, 128),
+    wl_("m32_win", 1, 1024, 4, 2, 128, 32, 6, 1, 64),
+    wl_("m16_tail_rows", 1, 2048, 4, 2, 128, 16, 10, 8, 256, Lq=333),
+    wl_("m16_fp32", 1, 1040, 4, 2, 128, 16, 5, 2, 64, dtype="fp32"),
+    wl_("m32_fp32_g4", 1, 640, 8, 2, 64, 32, 4, 1, 32, dtype="fp32"),
+]
+
+
+@pytest.mark.parametrize("wl", CASES, ids=[w.name for w in CASES])
+def test_forward_backward(wl):
+    log(f"[block16] {wl.name}")
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 11, with_grad_out=True)
+    h = oracle_inputs(host)
+    scale = wl.head_dim ** -0.5
+    Lk, m = wl.seqlen_k, wl.block_size
+    kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg)
+    dq, dk, dv = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg)
+    torch.cuda.synchronize()
+    kc_ref = oracle.compress(h["k"], h["punct"], m, wl.lam)
+    np.testing.assert_allclose(to_np(kc), kc_ref, atol=1e-5, rtol=1e-5)
+    sel_ref, kth, gap = oracle.select(h["q"], kc_ref, m, wl.top_k, wl.n_init_blocks, wl.window, scale, Lk)
+    sel_g = sel.cpu().numpy()
+    exempt = check_sel(sel_g, sel_ref, kth, gap,
+                       lambda idx: oracle.score_row(h["q"], kc_ref, m, scale, Lk, idx[0], idx[2], idx[1]))
+    o_ref, lse_ref = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, m, scale)
+    tol = O_TOL[wl.dtype]
+    np.testing.assert_allclose(to_np(o), o_ref, atol=tol, rtol=0)
+    np.testing.assert_allclose(to_np(lse), lse_ref, atol=tol, rtol=0)
+    dq_r, dk_r, dv_r = oracle.attn_bwd(h["q"], h["k"], h["v"], h["do"], sel_g, m, scale)
+    errs = (rel_l2(to_np(dq), dq_r), rel_l2(to_np(dk), dk_r), rel_l2(to_np(dv), dv_r))
+    log(f"[block16] {wl.name}: {exempt} exempt rows; grad rel-L2 {errs}")
+    assert max(errs) < GRAD_REL_L2[wl.dtype], errs
+
+
+def test_attn_on_given_selection_with_shared_tiles():
+    """Hand-made selections where several 16-token blocks of a row share a
+    64-key tile, rows select every quarter pattern, and the local blocks cross
+    tile boundaries (the forward and backward entry points on a given sel)."""
+    B, L, Hq, Hkv, d, m = 1, 1024, 2, 1, 128, 16
+    T = L // m
+    g = torch.Generator().manual_seed(23)
+    q = torch.randn(B, L, Hq, d, generator=g).to(torch.bfloat16)
+    k = torch.randn(B, L, Hkv, d, generator=g).to(torch.bfloat16)
+    v = torch.randn(B, L, Hkv, d, generator=g).to(torch.bfloat16)
+    do = torch.randn(B, L, Hq, d, generator=g).to(torch.bfloat16)
+    cfg = phsa.Config(block_size=m, top_k=8, n_init_blocks=1, window=32)
+    ks = cfg.ksel
+    rng = np.random.default_rng(3)
+    sel = -np.ones((B, Hkv, L, ks), np.int32)
+    for i in range(L):
+        cur = i // m
+        forced = set(range(min(1, cur + 1))) | set(range(max(0, cur - 2), cur + 1))
+        cand = [t for t in range(cur + 1) if t not in forced]
+        if cand:
+            # a random subset of quarters of a few tiles (pattern i % 16 on the first tile)
+            tile = rng.integers(0, max(1, cur // 4 + 1))
+            picks = [4 * tile + j for j in range(4) if (i % 16) >> j & 1]
+            picks += list(rng.choice(cand, size=min(len(cand), 8), replace=False))
+            picks = [t for t in dict.fromkeys(picks) if t in cand][:8]
+        else:
+            picks = []
+        row = sorted(forced | set(picks))
+        sel[0, 0, i, :len(row)] = row
+    assert (sel.max() < T)
+    sel_t = torch.from_numpy(sel).cuda()
+    o, lse = phsa.attn_fwd(q.cuda(), k.cuda(), v.cuda(), sel_t, cfg)
+    dq, dk, dv = phsa.attn_bwd(q.cuda(), k.cuda(), v.cuda(), o, do.cuda(), lse, sel_t, cfg)
+    torch.cuda.synchronize()
+    qh, kh, vh, doh = (x.float().numpy() for x in (q, k, v, do))
+    scale = d ** -0.5
+    o_r, lse_r = oracle.attn_fwd(qh, kh, vh, sel, m, scale)
+    np.testing.assert_allclose(to_np(o), o_r, atol=O_TOL["bf16"], rtol=0)
+    np.testing.assert_allclose(to_np(lse), lse_r, atol=O_TOL["bf16"], rtol=0)
+    dq_r, dk_r, dv_r = oracle.attn_bwd(qh, kh, vh, doh, sel, m, scale)
+    errs = (rel_l2(to_np(dq), dq_r), rel_l2(to_np(dk), dk_r), rel_l2(to_np(dv), dv_r))
+    assert max(errs) < GRAD_REL_L2["bf16"], errs
+
+
+def test_decode_block16():
+    wl = WORKLOADS["decode_32k"].replace(batch=8, seqlen_k=8192, block_size=16, top_k=16, n_init_blocks=8,
+                                         window=512)
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 6, with_grad_out=False)
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    sel, o, lse = phsa.decode(dev["q"], dev["k"], dev["v"], kc, cfg)
+    torch.cuda.synchronize()
+    h = oracle_inputs(host)
+    scale = wl.head_dim ** -0.5
+    kc_ref = oracle.compress(h["k"], h["punct"], 16, wl.lam)
+    sel_ref, kth, gap = oracle.select(h["q"], kc_ref, 16, 16, 8, 512, scale, wl.seqlen_k)
+    sel_g = sel.cpu().numpy()
+    check_sel(sel_g, sel_ref, kth, gap,
+              lambda idx: oracle.score_row(h["q"], kc_ref, 16, scale, wl.seqlen_k, idx[0], idx[2], idx[1]))
+    o_r, lse_r = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, 16, scale)
+    np.testing.assert_allclose(to_np(o), o_r, atol=O_TOL["bf16"], rtol=0)
+    np.testing.assert_allclose(to_np(lse), lse_r, atol=O_TOL["bf16"], rtol=0)
+
+
+def test_paper_geometry_32k_sampled():
+    """One 32k sequence in the paper's geometry (57 blocks of 16 tokens per query):
+    forward and backward on the GPU, the oracle on sampled rows and key blocks."""
+    wl = WORKLOADS["train_32k_paper"].replace(batch=1)
+    log(f"[block16] {wl.name} batch 1: generating inputs")
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 0, with_grad_out=True)
+    kc, sel, o, lse = phsa.forward(dev["q"], dev["k"], dev["v"], dev["punct"], cfg)
+    dq, dk, dv = phsa.attn_bwd(dev["q"], dev["k"], dev["v"], o, dev["do"], lse, sel, cfg)
+    torch.cuda.synchronize()
+    h = oracle_inputs(host)
+    del host
+    L, m, T = wl.seqlen_q, wl.block_size, wl.n_blocks
+    scale = wl.head_dim ** -0.5
+    kc_ref = oracle.compress(h["k"], h["punct"], m, wl.lam)
+    np.testing.assert_allclose(to_np(kc), kc_ref, atol=1e-5, rtol=1e-5)
+    sel_g = sel.cpu().numpy()
+    cur = np.arange(L) // m
+    valid = sel_g >= 0
+    assert (np.where(valid, sel_g, -1).max(-1) == cur).all()
+    assert (valid.sum(-1) == np.minimum(cur + 1, wl.ksel)).all()
+    rng = np.random.default_rng(2)
+    rows = np.array(sorted(set([0, 15, 16, 130, 527, 528, 529, 600, L // 2, L - 17, L - 16, L - 1]
+                               + rng.integers(0, L, 100).tolist())), dtype=np.int64)
+    sel_r, kth, gap = oracle.select(h["q"], kc_ref, m, wl.top_k, wl.n_init_blocks, wl.window, scale, L, rows=rows)
+    exempt = check_sel(sel_g[0][:, rows].transpose(1, 0, 2), sel_r, kth, gap,
+                       lambda idx: oracle.score_row(h["q"], kc_ref, m, scale, L, 0, int(rows[idx[0]]), idx[1]))
+    o_r, lse_r = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, m, scale, rows=rows)
+    np.testing.assert_allclose(to_np(o)[0, rows], o_r, atol=O_TOL["bf16"], rtol=0)
+    np.testing.assert_allclose(to_np(lse)[0][:, rows].T, lse_r, atol=O_TOL["bf16"], rtol=0)
+    dq_r, _, _ = oracle.attn_bwd(h["q"], h["k"], h["v"], h["do"], sel_g, m, scale, rows=rows, want_dkv=False)
+    e_dq = rel_l2(to_np(dq)[0, rows], dq_r)
+    Hkv = wl.n_heads_kv
+    picks = [(0, T - 1), (3, T - 40), (5, 1000), (7, 3), (6, T - 2)]   # (g, t); block 3 is an init block
+    blocks = np.array([g * T + t for g, t in picks], dtype=np.int64)
+    _, dk_r, dv_r = oracle.attn_bwd(h["q"], h["k"], h["v"], h["do"], sel_g, m, scale, blocks=blocks, want_dq=False)
+    dk_c, dv_c = to_np(dk), to_np(dv)
+    dk_g = np.stack([dk_c[0, t * m:(t + 1) * m, g] for g, t in picks])
+    dv_g = np.stack([dv_c[0, t * m:(t + 1) * m, g] for g, t in picks])
+    e_dk, e_dv = rel_l2(dk_g, dk_r), rel_l2(dv_g, dv_r)
+    log(f"[block16] paper geometry: {rows.size} rows, {exempt} exempt; grad rel-L2 dQ {e_dq:.2e} dK {e_dk:.2e} "
+        f"dV {e_dv:.2e}")
+    assert max(e_dq, e_dk, e_dv) < GRAD_REL_L2["bf16"]
