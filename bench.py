@@ -87,6 +87,15 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 
 
+TRAIN_TEXT = {
+    "train_32k": "train_32k: PHSA fwd+bwd, batch 4 x 32768 tokens, 16 query / 8 KV heads, head dim 128, "
+                 "block 64, 1 init + 1 local + 12 top-k blocks (97.3% sparse)",
+    "train_32k_paper": "train_32k_paper: PHSA fwd+bwd, batch 4 x 32768 tokens, 16 query / 8 KV heads, head dim 128, "
+                       "16-token blocks, 8 init blocks, 512-token window, 16 top-k blocks (57 blocks = 912 tokens "
+                       "per query, 97.2% sparse)",
+}
+
+
 def cfg_of(wl):
     return phsa.Config(block_size=wl.block_size, top_k=wl.top_k, n_init_blocks=wl.n_init_blocks, window=wl.window,
                        lam=wl.lam)
@@ -108,13 +117,25 @@ def kernel_stats(names):
     return out
 
 
-KERNELS = ["phsa_compress", "phsa_select_split", "phsa_select", "phsa_index_count", "phsa_index_scan_tiles", "phsa_index_scan_lists",
+KERNELS = ["phsa_compress", "phsa_select_split", "phsa_select", "phsa_coarsen", "phsa_index_count", "phsa_index_scan_tiles", "phsa_index_scan_lists",
            "phsa_index_fill", "phsa_attn_fwd_sparse", "phsa_attn_fwd_combine", "phsa_attn_bwd_pre",
            "phsa_attn_bwd_sparse", "phsa_attn_bwd_dkv_finalize", "phsa_attn_bwd_dq_combine"]
 
 
-def bench_train(steps: int, warmup: int, seed: int):
-    wl = WORKLOADS["train_32k"]
+def selected_tiles(sel: torch.Tensor, seqlen_k: int, block: int) -> int:
+    """Sum over (b, g, query row) of the distinct 64-key tiles holding the row's
+    valid selected blocks (the attention kernels' work items; = selected_blocks
+    for 64-token blocks)."""
+    Lq = sel.shape[2]
+    cur = ((seqlen_k - Lq + torch.arange(Lq, device=sel.device)) // block).view(1, 1, Lq, 1)
+    valid = (sel >= 0) & (sel <= cur)
+    tc = torch.div(sel, 64 // block, rounding_mode="floor")
+    same = (tc[..., 1:] == tc[..., :-1]) & valid[..., 1:] & valid[..., :-1]
+    return int(valid.sum().item() - same.sum().item())
+
+
+def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
+    wl = WORKLOADS[name]
     cfg = cfg_of(wl)
     host = make_inputs(wl, seed, with_grad_out=True)
     dev = {k: v.cuda() for k, v in host.items()}
@@ -134,6 +155,7 @@ def bench_train(steps: int, warmup: int, seed: int):
         sel = step()
     torch.cuda.synchronize()
     nsel = selected_blocks(sel, L, m)
+    ntile = selected_tiles(sel, L, m)
     phsa.timing_reset()
     phsa.timing_enable(True)
     torch.cuda.synchronize()
@@ -149,16 +171,20 @@ def bench_train(steps: int, warmup: int, seed: int):
 
     fwd_flop = 4.0 * d * m * nsel * G
     bwd_flop = 2.5 * fwd_flop
-    # Bytes the key-block-major kernels must move per launch: every (row, block)
+    # MFMA work the kernels execute: whole 64-key tiles (blocks below 64 tokens
+    # share tiles, the unselected quarters of a tile are masked)
+    tile_fwd_flop = 4.0 * d * 64 * ntile * G
+    # Bytes the key-block-major kernels must move per launch: every (row, tile)
     # pair gathers its query rows (and dO rows) and leaves a bf16 partial (plus
-    # the forward's (m, l)); every work unit loads its K/V block once.  This is
+    # the forward's (m, l)); every work unit loads its K/V tile once.  This is
     # the schedule's own traffic floor, above the method's algorithmic minimum.
     unit_tokens = 64 * (64 // G)
-    units = B * Hkv * T + nsel // unit_tokens
+    T64 = L // 64
+    units = B * Hkv * T64 + ntile // unit_tokens
     kv_bytes = units * 64 * d * 2 * 2
     pair_row = G * d * 2
-    design_bytes = {"phsa_attn_fwd_sparse": nsel * (2 * pair_row + G * 8 + 4) + kv_bytes,
-                    "phsa_attn_bwd_sparse": nsel * (3 * pair_row + G * 8 + 4) + kv_bytes + B * L * Hkv * d * 2 * 2}
+    design_bytes = {"phsa_attn_fwd_sparse": ntile * (2 * pair_row + G * 8 + 4) + kv_bytes,
+                    "phsa_attn_bwd_sparse": ntile * (3 * pair_row + G * 8 + 4) + kv_bytes + B * L * Hkv * d * 2 * 2}
     bytes_compress = B * L * Hkv * d * 2 + B * L + B * Hkv * T * d * 4
     bytes_select = B * L * Hq * d * 2 + B * Hkv * T * d * 4 + B * Hkv * L * wl.ksel * 4
     work = {"phsa_attn_fwd_sparse": ("TFLOP/s", fwd_flop / 1e12), "phsa_attn_bwd_sparse": ("TFLOP/s", bwd_flop / 1e12),
@@ -169,9 +195,11 @@ def bench_train(steps: int, warmup: int, seed: int):
             peak = PEAK_BF16_TFLOPS if unit == "TFLOP/s" else PEAK_HBM_GBS
             ks[n].update(rate=rate, unit=unit, frac=rate / peak)
             if n in design_bytes:
-                # attainable = min(MFMA peak, intensity x HBM peak) for this schedule's traffic
+                # attainable = min(MFMA peak, intensity x HBM peak) for this schedule's
+                # traffic and executed tile work, in selected-block FLOP/s
                 flop = fwd_flop if "fwd" in n else bwd_flop
-                t_min = max(flop / (PEAK_BF16_TFLOPS * 1e12), design_bytes[n] / (PEAK_HBM_GBS * 1e9))
+                exec_flop = tile_fwd_flop * (1.0 if "fwd" in n else 2.5)
+                t_min = max(exec_flop / (PEAK_BF16_TFLOPS * 1e12), design_bytes[n] / (PEAK_HBM_GBS * 1e9))
                 att = flop / 1e12 / t_min
                 ks[n].update(schedule_bytes=design_bytes[n],
                              schedule_GB_per_s=design_bytes[n] / 1e9 / (ks[n]["avg_ms"] / 1e3),
@@ -180,7 +208,8 @@ def bench_train(steps: int, warmup: int, seed: int):
     return {
         "ms_per_step": ms_step,
         "value": (fwd_flop + bwd_flop) / 1e12 / (ms_step / 1e3),
-        "fwd_flop": fwd_flop, "bwd_flop": bwd_flop, "selected_blocks": nsel,
+        "fwd_flop": fwd_flop, "bwd_flop": bwd_flop, "selected_blocks": nsel, "selected_tiles": ntile,
+        "tile_fwd_flop": tile_fwd_flop,
         # the paper's convention: active tokens of the last query over the sequence length
         "sparsity_last_query": 1.0 - wl.ksel * m / L,
         "sparsity_causal_mean": 1.0 - nsel * m / (B * Hkv * L * (L + 1) / 2),
@@ -353,6 +382,9 @@ def main():
     ap.add_argument("--cpu-prefix", type=int, default=8192)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-paper-geometry", action="store_true")
+    ap.add_argument("--train-workload", default="train_32k", choices=sorted(TRAIN_TEXT),
+                    help="training workload of the headline line (train_32k_paper: for profiling that geometry)")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="run one device-to-device copy of this many MiB first (a known-size kernel for "
                          "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -373,6 +405,7 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
     phsa.lib()
+    wl0 = WORKLOADS[args.train_workload]
     if args.calib_copy_mb > 0:
         # plain elementwise copy (reads N bytes, writes N bytes) for counter calibration
         n = args.calib_copy_mb * (1 << 20) // 4
@@ -382,7 +415,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    tr = bench_train(args.steps, args.warmup, args.seed)
+    tr = bench_train(args.steps, args.warmup, args.seed, args.train_workload)
     dom = tr["dominant"]
     dk = tr["kernels"][dom]
     traffic = None
@@ -404,23 +437,31 @@ def main():
         "metric": METRIC, "value": tr["value"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": tr["ms_per_step"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": "train_32k: PHSA fwd+bwd, batch 4 x 32768 tokens, 16 query / 8 KV heads, head dim 128, "
-                               "block 64, 1 init + 1 local + 12 top-k blocks (97.3% sparse)",
-                   "batch": 4, "seq_len": 32768, "heads_q": 16, "heads_kv": 8, "head_dim": 128, "block": 64,
-                   "blocks_per_query": 14, "sparsity_last_query": tr["sparsity_last_query"],
+        "config": {"workload": TRAIN_TEXT[args.train_workload],
+                   "batch": wl0.batch, "seq_len": wl0.seqlen_k, "heads_q": wl0.n_heads_q, "heads_kv": wl0.n_heads_kv,
+                   "head_dim": wl0.head_dim, "block": wl0.block_size,
+                   "blocks_per_query": wl0.ksel, "sparsity_last_query": tr["sparsity_last_query"],
                    "sparsity_causal_mean": tr["sparsity_causal_mean"]},
         "selected_block_gflop": {"fwd": tr["fwd_flop"] / 1e9, "bwd": tr["bwd_flop"] / 1e9},
         "frac_mfma_peak_step": tr["value"] / PEAK_BF16_TFLOPS,
         "roofline": roofline,
         "kernels": tr["kernels"],
     }
+    host0 = tr.pop("host")
+    if not args.no_paper_geometry and args.train_workload != "train_32k_paper":
+        pg = bench_train(max(2, args.steps // 2), max(1, args.warmup), args.seed, "train_32k_paper")
+        del pg["host"]
+        pg.pop("dominant")
+        pg["value_unit"] = "TFLOP/s (selected-block)"
+        pg["workload"] = TRAIN_TEXT["train_32k_paper"]
+        result["train_32k_paper_geometry"] = pg
     if not args.no_decode:
         result["decode"] = bench_decode(40, args.seed)
         result["generation_step"] = bench_generation(40, args.seed)
         result["punct_mask"] = bench_punct(args.seed)
         result["select_modes"] = bench_select_modes(args.seed)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(tr["host"], WORKLOADS["train_32k"], args.cpu_prefix)
+        result["cpu_baseline"] = cpu_baseline(host0, wl0, args.cpu_prefix)
     print(json.dumps(result))
 
 
