@@ -25,6 +25,27 @@ __device__ __forceinline__ bool beats(float s1, int t1, float s2, int t2) {
   return s1 > s2 || (s1 == s2 && t1 < t2);
 }
 
+// Writes one row of sel: the forced init blocks, the npick picks (sorted here
+// into ascending order, in place) and the local blocks, padded with -1.
+__device__ __forceinline__ void emit_row(int32_t *__restrict__ out, int *pk, int npick, int cur, const Geom &gm) {
+  for (int a = 1; a < npick; ++a) {  // insertion sort, at most top_k items
+    const int x = pk[a];
+    int c = a - 1;
+    while (c >= 0 && pk[c] > x) {
+      pk[c + 1] = pk[c];
+      --c;
+    }
+    pk[c + 1] = x;
+  }
+  const int lo = max(0, cur - gm.window / gm.m);
+  const int ni = min(gm.n_init, cur + 1);
+  int n = 0;
+  for (int t = 0; t < ni; ++t) out[n++] = t;
+  for (int a = 0; a < npick; ++a) out[n++] = pk[a];
+  for (int t = max(lo, ni); t <= cur; ++t) out[n++] = t;
+  for (; n < gm.ksel; ++n) out[n] = -1;
+}
+
 // Merge the four waves' sorted (score, block) lists of each row through LDS,
 // take the k best (score descending, block ascending) and write the row:
 // forced init blocks, the picks and the local blocks in ascending order,
@@ -69,23 +90,7 @@ __device__ __forceinline__ void finish_rows(const float (&ls)[KMAX], const int (
     for (int w = 0; w < 4; ++w) head[w] += (w == bw);
     picks[lane][npick++] = bt;
   }
-  // ascending block order of the picks (insertion sort, at most KMAX items)
-  for (int a = 1; a < npick; ++a) {
-    const int x = picks[lane][a];
-    int c = a - 1;
-    while (c >= 0 && picks[lane][c] > x) {
-      picks[lane][c + 1] = picks[lane][c];
-      --c;
-    }
-    picks[lane][c + 1] = x;
-  }
-  int32_t *out = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
-  int n = 0;
-  const int ni = min(gm.n_init, cur + 1);
-  for (int t = 0; t < ni; ++t) out[n++] = t;
-  for (int a = 0; a < npick; ++a) out[n++] = picks[lane][a];
-  for (int t = max(lo, ni); t <= cur; ++t) out[n++] = t;
-  for (; n < gm.ksel; ++n) out[n] = -1;
+  emit_row(sel + ((int64_t)bg * gm.Lq + i) * gm.ksel, picks[lane], npick, cur, gm);
 }
 
 template <typename T, int D, int KMAX>
@@ -320,6 +325,325 @@ __global__ __launch_bounds__(256) void select_softmax_kernel(const T *__restrict
     }
   }
   finish_rows<KMAX>(ls, lt, smem, picks, wave == 0 && row_ok && hh == 0, i, cur, lo, bg, sel, gm);
+}
+
+// Softmax-sum selection on the matrix cores (bf16 inputs; mode of
+// select_softmax_kernel).  A workgroup holds 64 (query token, head) pairs,
+// 64 / G tokens with their heads inner; wave w owns pairs 16w..16w+15 as one
+// 16-row MFMA tile.  A pair's query is scaled to log2 units and split into
+// bf16 hi + lo like the representatives (select_split_kernel), and the three
+// chains hi.hi + hi.lo + lo.hi give its logits to about 2^-17 relative.  In
+// the accumulator layout lane (q4, l16) holds pairs 4 q4 + r of its tile for
+// blocks t0 + 16 nt + l16: the G heads of a token sit in the same lane (G <= 4)
+// or in lanes q4 and q4 ^ 1 (G = 8), so a token's group score
+// log2 sum_h 2^(x_h - lse_h) is formed without LDS, and the 16 lanes of a
+// quarter-wave see all blocks of their tokens, each a fixed residue mod 16.
+//   pass 1: the complete causal blocks t < cur: a running (max, sum) of 2^x per
+//           lane and pair, merged over the 16 lanes: the log2 normaliser lse.
+//   pass 2: the candidates' group scores; each lane keeps the best two of its
+//           stripe per token.  A token's 32 stripe tops are 32 distinct
+//           blocks, so the largest v with at least k of them >= v (the bar)
+//           lies at or below the token's k-th best score.
+//   pass 3: the group scores again; those >= bar are appended to the token's
+//           LDS list (slots from an LDS counter: about k + 3 per token on
+//           random inputs).  A list that could overflow with the next chunk
+//           (many equal scores) is cut to its k best first.
+//   final:  the k best of each list (score descending, block ascending) by
+//           counting ranks, so the order of arrival does not matter.
+// Scores of passes 2 and 3 come from identical instruction sequences on the
+// same data, so they are bitwise equal and the bar never drops a winner.
+template <int D, int G, int KMAX>
+__global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *__restrict__ Q,
+                                                                  const bf16_t *__restrict__ Mh_g,
+                                                                  const bf16_t *__restrict__ Ml_g,
+                                                                  int32_t *__restrict__ sel, Geom gm) {
+  constexpr int CH = 64;
+  constexpr int NTOK = 64 / G;            // tokens per workgroup
+  constexpr int GL = G < 4 ? G : 4;       // heads of a token within one lane
+  constexpr int TPL = 4 / GL;             // tokens per lane (lanes q4 even only when G = 8)
+  constexpr int LPT = 256 / NTOK;         // threads per token when ranking
+  constexpr int CAP = KMAX + CH;          // list slots per token: k best + one chunk
+  constexpr int MP = D + 16;              // 16-byte fragment reads of 16 rows are conflict-free
+  constexpr int KB = D / 32;
+  constexpr int NL = CH * D / (256 * 8);
+  constexpr int BUF = 2 * CH * MP * 2;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[BUF];
+  __shared__ float2 cand[NTOK][CAP];      // (score, block as int bits), unordered
+  __shared__ int ccnt[NTOK];
+  __shared__ int picks[NTOK][KMAX];
+  __shared__ float bar_s[NTOK];
+  bf16_t *Mh = reinterpret_cast<bf16_t *>(smem);
+  bf16_t *Ml = Mh + CH * MP;
+  float *tops = reinterpret_cast<float *>(smem);   // bar and cuts: [NTOK][32] / [NTOK][2 KMAX]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
+  const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg % gm.Hkv;
+  const int i0 = blockIdx.x * NTOK;
+  const int last_i = min(i0 + NTOK - 1, gm.Lq - 1);
+  const int cur_max = (gm.q_pos0 + last_i) / gm.m;
+  const int t_end = max(0, cur_max - gm.window / gm.m);
+  const int k = gm.top_k;
+
+  // A operand: pair 16 w + l16 (token (16 w + l16) / G, head l16 % G)
+  bf16x8 ah[KB], al[KB];
+  {
+    const float f = gm.scale * kLog2e;
+    const int p = wave * 16 + l16;
+    const int i = min(i0 + p / G, gm.Lq - 1);
+    const bf16_t *src = Q + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + p % G) * D;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const uint4 raw = *reinterpret_cast<const uint4 *>(src + kb * 32 + kq);
+      const bf16_t *v = reinterpret_cast<const bf16_t *>(&raw);
+      bf16_t hi[8], lo[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = bf16_to_f32(v[e]) * f;
+        hi[e] = f32_to_bf16(x);
+        lo[e] = f32_to_bf16(x - bf16_to_f32(hi[e]));
+      }
+      ah[kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(hi));
+      al[kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(lo));
+    }
+  }
+  // accumulator row r of this lane: pair 16 w + 4 q4 + r; its token and bounds
+  const int tok0 = (wave * 16 + q4 * 4) / G;   // first token of this lane's rows
+  int cur_r[4], lo_t[TPL];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int i = i0 + (wave * 16 + q4 * 4 + r) / G;
+    cur_r[r] = i < gm.Lq ? (gm.q_pos0 + i) / gm.m : 0;
+  }
+#pragma unroll
+  for (int u = 0; u < TPL; ++u) {
+    const int i = i0 + tok0 + u;
+    lo_t[u] = i < gm.Lq ? max(0, (gm.q_pos0 + i) / gm.m - gm.window / gm.m) : 0;
+  }
+
+  const bf16_t *mh_bg = Mh_g + (int64_t)bg * gm.T * D;
+  const bf16_t *ml_bg = Ml_g + (int64_t)bg * gm.T * D;
+  uint4 ph[NL], pl[NL];
+  auto fetch = [&](int t0) {
+    const int nblk = min(CH, gm.T - t0);
+#pragma unroll
+    for (int x = 0; x < NL; ++x) {
+      const int e = (tid + 256 * x) * 8, row = e / D, c = e % D;
+      const int64_t off = (int64_t)(t0 + row) * D + c;
+      ph[x] = row < nblk ? *reinterpret_cast<const uint4 *>(mh_bg + off) : make_uint4(0u, 0u, 0u, 0u);
+      pl[x] = row < nblk ? *reinterpret_cast<const uint4 *>(ml_bg + off) : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto stage = [&]() {
+#pragma unroll
+    for (int x = 0; x < NL; ++x) {
+      const int e = (tid + 256 * x) * 8, row = e / D, c = e % D;
+      *reinterpret_cast<uint4 *>(&Mh[row * MP + c]) = ph[x];
+      *reinterpret_cast<uint4 *>(&Ml[row * MP + c]) = pl[x];
+    }
+  };
+  // exact logits of the staged chunk: acc[nt][r] = x(pair 16 w + 4 q4 + r, block t0 + 16 nt + l16)
+  auto scores = [&](f32x4 (&acc)[4]) {
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      bf16x8 bh[4], bl[4];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        bh[nt] = load_bf16x8(&Mh[(nt * 16 + l16) * MP + kb * 32 + kq]);
+        bl[nt] = load_bf16x8(&Ml[(nt * 16 + l16) * MP + kb * 32 + kq]);
+      }
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        acc[nt] = mfma16x16x32(ah[kb], bh[nt], acc[nt]);
+        acc[nt] = mfma16x16x32(ah[kb], bl[nt], acc[nt]);
+        acc[nt] = mfma16x16x32(al[kb], bh[nt], acc[nt]);
+      }
+    }
+  };
+  // one pass over the chunks of [ta, tb): body(t0, acc) after the scores
+  auto sweep = [&](int ta, int tb, auto body) {
+    fetch(ta);
+    for (int t0 = ta; t0 < tb; t0 += CH) {
+      __syncthreads();
+      stage();
+      __syncthreads();
+      if (t0 + CH < tb) fetch(t0 + CH);
+      f32x4 acc[4];
+      scores(acc);
+      body(t0, acc);
+    }
+  };
+  float lse[4];
+  // group score of token u of this lane for block t0 + 16 nt + l16 (all lanes call this)
+  auto group = [&](const f32x4 &a, int u) {
+    float m = a[u * GL] - lse[u * GL];
+#pragma unroll
+    for (int r = 1; r < GL; ++r) m = fmaxf(m, a[u * GL + r] - lse[u * GL + r]);
+    if (G == 8) m = fmaxf(m, __shfl_xor(m, 16, 64));
+    float e = 0.f;
+#pragma unroll
+    for (int r = 0; r < GL; ++r) e += __builtin_amdgcn_exp2f(a[u * GL + r] - lse[u * GL + r] - m);
+    if (G == 8) e += __shfl_xor(e, 16, 64);
+    return m + __builtin_amdgcn_logf(e);   // e in [1, G]
+  };
+  const bool lane_tok = G < 8 || (q4 & 1) == 0;   // lanes that hold whole tokens
+
+  if (tid < NTOK) ccnt[tid] = 0;
+  if (k > 0 && t_end > gm.n_init) {
+    // ---- pass 1: log2 normaliser of every pair over blocks 0 .. cur - 1
+    float mx[4], sm[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      mx[r] = -INFINITY;
+      sm[r] = 0.f;
+    }
+    sweep(0, cur_max, [&](int t0, f32x4 (&acc)[4]) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float cm = -INFINITY;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+          if (t0 + nt * 16 + l16 < cur_r[r]) cm = fmaxf(cm, acc[nt][r]);
+        const float nm = fmaxf(mx[r], cm);
+        if (nm == -INFINITY) continue;
+        float add = 0.f;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+          if (t0 + nt * 16 + l16 < cur_r[r]) add += __builtin_amdgcn_exp2f(acc[nt][r] - nm);
+        sm[r] = sm[r] * __builtin_amdgcn_exp2f(mx[r] - nm) + add;  // 2^-inf = 0 on the first block
+        mx[r] = nm;
+      }
+    });
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float m = mx[r], l = sm[r];
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        const float om = __shfl_xor(m, o, 64), ol = __shfl_xor(l, o, 64);
+        const float nm = fmaxf(m, om);
+        l = (l > 0.f ? l * __builtin_amdgcn_exp2f(m - nm) : 0.f) + (ol > 0.f ? ol * __builtin_amdgcn_exp2f(om - nm) : 0.f);
+        m = nm;
+      }
+      lse[r] = l > 0.f ? m + __builtin_amdgcn_logf(l) : 0.f;  // cur = 0: no candidate uses it
+    }
+
+    // ---- pass 2: best two group scores of each lane's stripe, per token
+    float top1[TPL], top2[TPL];
+#pragma unroll
+    for (int u = 0; u < TPL; ++u) top1[u] = top2[u] = -INFINITY;
+    sweep(gm.n_init, t_end, [&](int t0, f32x4 (&acc)[4]) {
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const int t = t0 + nt * 16 + l16;
+#pragma unroll
+        for (int u = 0; u < TPL; ++u) {
+          const float sv = group(acc[nt], u);
+          const float v = t < lo_t[u] ? sv : -INFINITY;
+          const bool c1 = v > top1[u], c2 = v > top2[u];
+          top2[u] = c1 ? top1[u] : (c2 ? v : top2[u]);
+          top1[u] = c1 ? v : top1[u];
+        }
+      }
+    });
+    // ---- bar of each token: the largest stripe top v with at least k stripe tops >= v
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < TPL; ++u)
+      if (lane_tok) {
+        tops[(tok0 + u) * 32 + 2 * l16] = top1[u];
+        tops[(tok0 + u) * 32 + 2 * l16 + 1] = top2[u];
+      }
+    wave_lds_sync();
+#pragma unroll
+    for (int u = 0; u < TPL; ++u) {
+      const float4 *rowp = reinterpret_cast<const float4 *>(tops + (tok0 + u) * 32);
+      int c1 = 0, c2 = 0;
+#pragma unroll
+      for (int x = 0; x < 8; ++x) {
+        const float4 v = rowp[x];
+        c1 += (v.x >= top1[u]) + (v.y >= top1[u]) + (v.z >= top1[u]) + (v.w >= top1[u]);
+        c2 += (v.x >= top2[u]) + (v.y >= top2[u]) + (v.z >= top2[u]) + (v.w >= top2[u]);
+      }
+      float best = -INFINITY;
+      if (c1 >= k) best = top1[u];
+      if (c2 >= k) best = fmaxf(best, top2[u]);
+      best = max16(best);
+      if (lane_tok && l16 == 0) bar_s[tok0 + u] = best;
+    }
+    __syncthreads();
+    float bar[TPL];
+#pragma unroll
+    for (int u = 0; u < TPL; ++u) bar[u] = bar_s[tok0 + u];
+
+    // ---- pass 3: scores >= bar join their token's list
+    const int own_tok = tid / LPT, own_str = tid % LPT;
+    sweep(gm.n_init, t_end, [&](int t0, f32x4 (&acc)[4]) {
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const int t = t0 + nt * 16 + l16;
+#pragma unroll
+        for (int u = 0; u < TPL; ++u) {
+          const float sv = group(acc[nt], u);
+          if (lane_tok && t < lo_t[u] && sv >= bar[u])
+            cand[tok0 + u][atomicAdd(&ccnt[tok0 + u], 1)] = make_float2(sv, __int_as_float(t));
+        }
+      }
+      __syncthreads();
+      // a list that the next chunk could overflow keeps its k best (the staging
+      // buffer is free until the next chunk is staged) and raises its bar
+      const int n_own = ccnt[own_tok];
+      const bool cut = n_own > CAP - CH;
+      if (cut)
+        for (int e = own_str; e < n_own; e += LPT) {
+          const float2 me = cand[own_tok][e];
+          int rk = 0;
+          for (int f = 0; f < n_own; ++f) {
+            const float2 o = cand[own_tok][f];
+            rk += beats(o.x, __float_as_int(o.y), me.x, __float_as_int(me.y));
+          }
+          if (rk < k) {
+            tops[own_tok * 2 * KMAX + 2 * rk] = me.x;
+            tops[own_tok * 2 * KMAX + 2 * rk + 1] = me.y;
+          }
+        }
+      __syncthreads();
+      if (cut) {
+        for (int r = own_str; r < k; r += LPT)
+          cand[own_tok][r] = make_float2(tops[own_tok * 2 * KMAX + 2 * r], tops[own_tok * 2 * KMAX + 2 * r + 1]);
+        if (own_str == 0) {
+          ccnt[own_tok] = k;
+          bar_s[own_tok] = tops[own_tok * 2 * KMAX + 2 * (k - 1)];
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < TPL; ++u) bar[u] = bar_s[tok0 + u];
+    });
+  }
+
+  // ---- the k best of each token's list, then its row
+  __syncthreads();
+  {
+    const int own_tok = tid / LPT, own_str = tid % LPT;
+    const int n = ccnt[own_tok];
+    for (int e = own_str; e < n; e += LPT) {
+      const float2 me = cand[own_tok][e];
+      int rk = 0;
+      for (int f = 0; f < n; ++f) {
+        const float2 o = cand[own_tok][f];
+        rk += beats(o.x, __float_as_int(o.y), me.x, __float_as_int(me.y));
+      }
+      if (rk < k) picks[own_tok][rk] = __float_as_int(me.y);
+    }
+  }
+  __syncthreads();
+  if (tid >= NTOK) return;
+  const int i = i0 + tid;
+  if (i >= gm.Lq) return;
+  const int cur = (gm.q_pos0 + i) / gm.m;
+  emit_row(sel + ((int64_t)bg * gm.Lq + i) * gm.ksel, picks[tid], min(k, ccnt[tid]), cur, gm);
 }
 
 // bf16 inputs: scoring on the matrix cores, selection by a bar and a short exact rank.
@@ -774,12 +1098,49 @@ static hipError_t launch_select_mfma_d(const Geom &g, const void *Q, const float
 
 size_t select_split_bytes(const Geom &g) {
   const size_t nblk = (size_t)g.B * g.Hkv * g.T;
-  return g.dtype == 0 && g.sel_mode == 0 ? nblk * (2 * g.d * sizeof(bf16_t) + sizeof(float)) : 0;
+  return g.dtype == 0 ? nblk * (2 * g.d * sizeof(bf16_t) + sizeof(float)) : 0;
+}
+
+template <int D, int G>
+static hipError_t launch_select_softmax_mfma(const Geom &g, const void *Q, const float *Kc, int32_t *sel, char *ws,
+                                             hipStream_t s) {
+  const int64_t n = (int64_t)g.B * g.Hkv * g.T * D;
+  bf16_t *mh = reinterpret_cast<bf16_t *>(ws), *ml = mh + n;
+  float *mnorm = reinterpret_cast<float *>(ml + n);
+  timing_begin("phsa_select_split", s);
+  hipLaunchKernelGGL(select_split_kernel<D>, dim3((unsigned)((n / 8 + 255) / 256)), dim3(256), 0, s, Kc, mh, ml, mnorm,
+                     n / 8);
+  timing_end(s);
+  constexpr int NTOK = 64 / G;
+  const dim3 grid((g.Lq + NTOK - 1) / NTOK, g.B * g.Hkv);
+  timing_begin("phsa_select_softmax", s);
+  if (g.top_k <= 16)
+    hipLaunchKernelGGL((select_softmax_mfma_kernel<D, G, 16>), grid, dim3(256), 0, s,
+                       static_cast<const bf16_t *>(Q), mh, ml, sel, g);
+  else
+    hipLaunchKernelGGL((select_softmax_mfma_kernel<D, G, 32>), grid, dim3(256), 0, s,
+                       static_cast<const bf16_t *>(Q), mh, ml, sel, g);
+  timing_end(s);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_select_softmax_mfma_d(const Geom &g, const void *Q, const float *Kc, int32_t *sel,
+                                               char *split, hipStream_t s) {
+  switch (g.G) {
+    case 1: return launch_select_softmax_mfma<D, 1>(g, Q, Kc, sel, split, s);
+    case 2: return launch_select_softmax_mfma<D, 2>(g, Q, Kc, sel, split, s);
+    case 4: return launch_select_softmax_mfma<D, 4>(g, Q, Kc, sel, split, s);
+    default: return launch_select_softmax_mfma<D, 8>(g, Q, Kc, sel, split, s);
+  }
 }
 
 hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t *sel, void *ws, hipStream_t s) {
   char *split = static_cast<char *>(ws);
   if (g.sel_mode == 1) {
+    if (g.dtype == 0 && g.G <= 8)
+      return g.d == 128 ? launch_select_softmax_mfma_d<128>(g, Q, Kc, sel, split, s)
+                        : launch_select_softmax_mfma_d<64>(g, Q, Kc, sel, split, s);
     if (g.dtype == 0)
       return g.d == 128 ? launch_select_softmax<bf16_t, 128>(g, Q, Kc, sel, s)
                         : launch_select_softmax<bf16_t, 64>(g, Q, Kc, sel, s);

@@ -82,7 +82,9 @@ def test_ksel_and_workspace():
     # bf16 hi/lo copies of K_comp and one norm per block, rounded up to 256 bytes
     assert phsa.workspace_size(_p(), phsa.OP_SELECT) == -(-16 * (2 * 64 * 2 + 4) // 256) * 256
     assert phsa.workspace_size(_p(dtype=phsa.FP32), phsa.OP_SELECT) == 0
-    assert phsa.workspace_size(_p(flags=phsa.FLAG_SELECT_SOFTMAX_SUM), phsa.OP_SELECT) == 0
+    # the softmax-sum mode scores with the same split copies
+    assert phsa.workspace_size(_p(flags=phsa.FLAG_SELECT_SOFTMAX_SUM), phsa.OP_SELECT) == \
+        phsa.workspace_size(_p(), phsa.OP_SELECT)
     assert phsa.workspace_size(_p(), phsa.OP_FORWARD) >= phsa.workspace_size(_p(), phsa.OP_SELECT)
     fwd = phsa.workspace_size(_p(), phsa.OP_ATTN_FWD)
     assert fwd > 0 and fwd % 256 == 0
