@@ -26,16 +26,19 @@ namespace phsa {
 
 __device__ __forceinline__ bool slot_valid(int t, int cur, int T) { return t >= 0 && t <= cur && t < T; }
 
-__device__ void build_tile_bitmap(uint32_t *bm, const int32_t *sel, const Geom &gm, int bg, int w) {
+// The tile's sel rows are one contiguous run: staged into rows_s
+// ([kIndexTile][ksel]) with coalesced loads, then row tid is read from LDS.
+__device__ void build_tile_bitmap(uint32_t *bm, int32_t *rows_s, const int32_t *sel, const Geom &gm, int bg, int w) {
   const int tid = threadIdx.x;
   for (int x = tid; x < gm.T * 8; x += 256) bm[x] = 0u;
+  const int nrow = min(kIndexTile, gm.Lq - w * kIndexTile);
+  const int32_t *src = sel + ((int64_t)bg * gm.Lq + (int64_t)w * kIndexTile) * gm.ksel;
+  for (int x = tid; x < nrow * gm.ksel; x += 256) rows_s[x] = src[x];
   __syncthreads();
-  const int i = w * kIndexTile + tid;
-  if (i < gm.Lq) {
-    const int cur = (gm.q_pos0 + i) / gm.m;
-    const int32_t *row = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
+  if (tid < nrow) {
+    const int cur = (gm.q_pos0 + w * kIndexTile + tid) / gm.m;
     for (int s = 0; s < gm.ksel; ++s) {
-      const int t = row[s];
+      const int t = rows_s[tid * gm.ksel + s];
       if (slot_valid(t, cur, gm.T)) atomicOr(&bm[t * 8 + (tid >> 5)], 1u << (tid & 31));
     }
   }
@@ -45,7 +48,7 @@ __device__ void build_tile_bitmap(uint32_t *bm, const int32_t *sel, const Geom &
 __global__ __launch_bounds__(256) void index_count_kernel(const int32_t *__restrict__ sel, Geom gm, IndexWs ix) {
   extern __shared__ uint32_t bm[];
   const int w = blockIdx.x, bg = blockIdx.y;
-  build_tile_bitmap(bm, sel, gm, bg, w);
+  build_tile_bitmap(bm, reinterpret_cast<int32_t *>(bm + gm.T * 8), sel, gm, bg, w);
   int32_t *dst = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
   for (int t = threadIdx.x; t < gm.T; t += 256) {
     int c = 0;
@@ -115,18 +118,18 @@ __global__ __launch_bounds__(1024) void index_scan_lists_kernel(Geom gm, IndexWs
 __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restrict__ sel,
                                                          const uint8_t *__restrict__ quarters, Geom gm, IndexWs ix) {
   extern __shared__ uint32_t bm[];
-  int32_t *pm = reinterpret_cast<int32_t *>(bm + gm.T * 8);  // [kIndexTile][ksel] staged position map
+  // [kIndexTile][ksel]: the staged sel rows, each entry replaced in place by its list position
+  int32_t *pm = reinterpret_cast<int32_t *>(bm + gm.T * 8);
   const int w = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x;
-  build_tile_bitmap(bm, sel, gm, bg, w);
+  build_tile_bitmap(bm, pm, sel, gm, bg, w);
   const int i = w * kIndexTile + tid;
   if (i < gm.Lq) {
     const int cur = (gm.q_pos0 + i) / gm.m;
-    const int32_t *row = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
     const int32_t *tile_off = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
     const int word = tid >> 5;
     const uint32_t below = (1u << (tid & 31)) - 1u;
     for (int s = 0; s < gm.ksel; ++s) {
-      const int t = row[s];
+      const int t = pm[tid * gm.ksel + s];
       int32_t pos = -1;
       if (slot_valid(t, cur, gm.T)) {
         int rank = __popc(bm[t * 8 + word] & below);
@@ -212,8 +215,9 @@ hipError_t launch_build_index(const Geom &g, const int32_t *sel, const uint8_t *
                               hipStream_t s) {
   const int nbgt = g.B * g.Hkv * g.T;
   const size_t lds = (size_t)g.T * 8 * sizeof(uint32_t);
+  const size_t rows_lds = (size_t)kIndexTile * g.ksel * sizeof(int32_t);
   timing_begin("phsa_index_count", s);
-  hipLaunchKernelGGL(index_count_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds, s, sel, g, ix);
+  hipLaunchKernelGGL(index_count_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds + rows_lds, s, sel, g, ix);
   timing_end(s);
   timing_begin("phsa_index_scan_tiles", s);
   hipLaunchKernelGGL(index_scan_tiles_kernel, dim3((nbgt + 255) / 256), dim3(256), 0, s, g, ix, nbgt);
@@ -222,8 +226,7 @@ hipError_t launch_build_index(const Geom &g, const int32_t *sel, const uint8_t *
   hipLaunchKernelGGL(index_scan_lists_kernel, dim3(1), dim3(1024), 0, s, g, ix, nbgt);
   timing_end(s);
   timing_begin("phsa_index_fill", s);
-  hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds + (size_t)kIndexTile * g.ksel * 4,
-                     s, sel, quarters, g, ix);
+  hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds + rows_lds, s, sel, quarters, g, ix);
   timing_end(s);
   return hipGetLastError();
 }
