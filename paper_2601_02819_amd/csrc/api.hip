@@ -48,17 +48,17 @@ size_t index_layout(const Geom &g, char *base, IndexWs *ix) {
 // the selection is regrouped per tile with a mask of its 16-key quarters.
 bool tiles_coarsened(const Geom &g) { return g.dtype == PHSA_BF16 && g.m != 64; }
 
-// Tile geometry: m = 64, T = Lk / 64, and ksel = a bound on the distinct tiles
-// of a row: the init blocks cover ceil(n_init m / 64) tiles, the local blocks
-// (w + m tokens starting on an m boundary) at most ceil(w / 64) + 1, and each
-// free pick one.
+// Tile geometry: m = 64, T = Lk / 64, and ksel = the most distinct tiles a
+// row can hold, min(Ksel, T).  (A selection made by phsa_select needs fewer:
+// ceil(n_init m / 64) init tiles, at most ceil(w / 64) + 1 local ones and one
+// per pick, 27 against Ksel = 57 in the paper's geometry; but sel may be any
+// ascending causal block list.)
 Geom tile_geom(const Geom &g) {
   if (!tiles_coarsened(g)) return g;
   Geom t = g;
   t.m = 64;
   t.T = g.Lk / 64;
-  const int bound = (g.n_init * g.m + 63) / 64 + (g.window + 63) / 64 + 1 + g.top_k;
-  t.ksel = std::min(g.ksel, bound);
+  t.ksel = std::min(g.ksel, t.T);
   t.n_init = (g.n_init * g.m + 63) / 64;
   t.window = 0;
   return t;
@@ -173,10 +173,7 @@ phsa_status validate(const phsa_params *p, int op, Geom *out) {
   if (T > 2048 || p->seqlen_q >= (1 << 25)) return PHSA_ERR_UNSUPPORTED;
   // bf16 attention on blocks below 64 tokens runs on 64-key tiles (quarter masks)
   const bool coarse = p->dtype == PHSA_BF16 && p->block_size != 64;
-  const int64_t ksel_tiles =
-      coarse ? std::min<int64_t>(ksel, ((int64_t)p->n_init_blocks * p->block_size + 63) / 64 + (p->window + 63) / 64 +
-                                           1 + p->top_k)
-             : ksel;
+  const int64_t ksel_tiles = coarse ? std::min<int64_t>(ksel, p->seqlen_k / 64) : ksel;
   if (p->batch > 65535 || p->n_heads_q > 65535 || (int64_t)p->batch * p->n_heads_kv > 65535)
     return PHSA_ERR_UNSUPPORTED;  // grid y/z extents
   // the softmax-sum kernels give each lane one (row, head) pair, at most 8 heads in decode

@@ -37,9 +37,11 @@ __device__ void build_tile_bitmap(uint32_t *bm, int32_t *rows_s, const int32_t *
   __syncthreads();
   if (tid < nrow) {
     const int cur = (gm.q_pos0 + w * kIndexTile + tid) / gm.m;
+    // a row's valid slots are a prefix (ascending blocks, then -1 or blocks past cur)
     for (int s = 0; s < gm.ksel; ++s) {
       const int t = rows_s[tid * gm.ksel + s];
-      if (slot_valid(t, cur, gm.T)) atomicOr(&bm[t * 8 + (tid >> 5)], 1u << (tid & 31));
+      if (!slot_valid(t, cur, gm.T)) break;
+      atomicOr(&bm[t * 8 + (tid >> 5)], 1u << (tid & 31));
     }
   }
   __syncthreads();
@@ -128,18 +130,18 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
     const int32_t *tile_off = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
     const int word = tid >> 5;
     const uint32_t below = (1u << (tid & 31)) - 1u;
-    for (int s = 0; s < gm.ksel; ++s) {
+    int s = 0;
+    for (; s < gm.ksel; ++s) {  // the valid prefix
       const int t = pm[tid * gm.ksel + s];
-      int32_t pos = -1;
-      if (slot_valid(t, cur, gm.T)) {
-        int rank = __popc(bm[t * 8 + word] & below);
-        for (int k = 0; k < word; ++k) rank += __popc(bm[t * 8 + k]);
-        pos = ix.off[bg * gm.T + t] + tile_off[t] + rank;
-        const int qm = quarters ? quarters[((int64_t)bg * gm.Lq + i) * gm.ksel + s] & 15 : 15;
-        ix.tok[pos] = (i << 10) | (qm << 6) | s;
-      }
+      if (!slot_valid(t, cur, gm.T)) break;
+      int rank = __popc(bm[t * 8 + word] & below);
+      for (int k = 0; k < word; ++k) rank += __popc(bm[t * 8 + k]);
+      const int32_t pos = ix.off[bg * gm.T + t] + tile_off[t] + rank;
+      const int qm = quarters ? quarters[((int64_t)bg * gm.Lq + i) * gm.ksel + s] & 15 : 15;
+      ix.tok[pos] = (i << 10) | (qm << 6) | s;
       pm[tid * gm.ksel + s] = pos;
     }
+    for (; s < gm.ksel; ++s) pm[tid * gm.ksel + s] = -1;
   }
   __syncthreads();
   // the tile's rows are consecutive, so their position-map rows form one contiguous run
@@ -151,53 +153,44 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
 // Blocks of m = 16 or 32 tokens run on the 64-key attention tiles: the
 // m-token blocks a row selected are grouped by the 64-token tile that holds
 // them (tile = block / (64 / m)), and each tile gets the mask of the 16-key
-// quarters its selected blocks cover.  The input rows are ascending, so a
-// row's blocks in one tile are adjacent.  gc is the tile geometry (m = 64,
-// T = Lk / 64, ksel = a bound on the tiles per row).  The rows of a 128-row
-// group are staged through LDS so that the reads are coalesced.
-constexpr int kCoarsenRows = 128;
-__global__ __launch_bounds__(kCoarsenRows) void coarsen_kernel(const int32_t *__restrict__ sel, Geom g, Geom gc,
-                                                               int32_t *__restrict__ csel,
-                                                               uint8_t *__restrict__ cq) {
-  extern __shared__ int32_t rows_s[];  // [kCoarsenRows][g.ksel]
-  const int64_t nrows = (int64_t)g.B * g.Hkv * g.Lq;
-  const int64_t x0 = (int64_t)blockIdx.x * kCoarsenRows;
-  const int nr = (int)min((int64_t)kCoarsenRows, nrows - x0);
-  for (int v = threadIdx.x; v < nr * g.ksel; v += kCoarsenRows) rows_s[v] = sel[x0 * g.ksel + v];
-  __syncthreads();
-  const int r = threadIdx.x;
-  if (r >= nr) return;
-  const int64_t x = x0 + r;
+// quarters its selected blocks cover.  gc is the tile geometry (m = 64,
+// T = Lk / 64, ksel = min(Ksel, T): no row holds more tiles than that).
+// One wave per row, lane s holding slot s (Ksel <= 64): the rows are ascending,
+// so a tile's blocks sit in adjacent lanes; a tile's first lane finds its
+// output slot by a ballot prefix count and ORs the quarters of the (at most
+// 64 / m) lanes of its group.  Reads and writes are contiguous per row.
+__global__ __launch_bounds__(256) void coarsen_kernel(const int32_t *__restrict__ sel, Geom g, Geom gc,
+                                                      int32_t *__restrict__ csel, uint8_t *__restrict__ cq) {
+  const int lane = threadIdx.x & 63;
+  const int64_t x = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // row (b, g, i)
+  if (x >= (int64_t)g.B * g.Hkv * g.Lq) return;                    // whole wave
   const int i = (int)(x % g.Lq);
   const int cur = (g.q_pos0 + i) / g.m;
-  const int per = 64 / g.m, qpb = g.m / 16;  // blocks per tile, quarters per block
+  const int per = 64 / g.m, qpb = g.m / 16;
+  const int t = lane < g.ksel ? sel[x * g.ksel + lane] : -1;
+  const bool valid = t >= 0 && t <= cur && t < g.T;
+  const int tc = valid ? t / per : -1;
+  const unsigned qb = valid ? ((1u << qpb) - 1u) << ((t % per) * qpb) : 0u;
+  const int prev = __shfl_up(tc, 1, 64);
+  const bool first = valid && (lane == 0 || prev != tc);
+  const uint64_t heads = __ballot(first);
+  const int pos = __popcll(heads & ((1ull << lane) - 1ull));
+  const int n = __popcll(heads);
+  unsigned acc = qb;
+  for (int dd = 1; dd < per; ++dd) {
+    const unsigned o = __shfl_down(qb, dd, 64);
+    const int otc = __shfl_down(tc, dd, 64);
+    if (lane + dd < 64 && otc == tc) acc |= o;
+  }
   int32_t *out = csel + x * gc.ksel;
   uint8_t *oq = cq + x * gc.ksel;
-  int n = 0, last = -1;
-  unsigned msk = 0u;
-  for (int s = 0; s < g.ksel; ++s) {
-    const int t = rows_s[r * g.ksel + s];
-    if (t < 0 || t > cur || t >= g.T) continue;
-    const int tc = t / per;
-    if (tc != last) {
-      if (last >= 0 && n < gc.ksel) {
-        out[n] = last;
-        oq[n] = (uint8_t)msk;
-        ++n;
-      }
-      last = tc;
-      msk = 0u;
-    }
-    msk |= ((1u << qpb) - 1u) << ((t % per) * qpb);
+  if (first && pos < gc.ksel) {
+    out[pos] = tc;
+    oq[pos] = (uint8_t)acc;
   }
-  if (last >= 0 && n < gc.ksel) {
-    out[n] = last;
-    oq[n] = (uint8_t)msk;
-    ++n;
-  }
-  for (; n < gc.ksel; ++n) {
-    out[n] = -1;
-    oq[n] = 0;
+  if (lane >= n && lane < gc.ksel) {
+    out[lane] = -1;
+    oq[lane] = 0;
   }
 }
 
@@ -205,8 +198,7 @@ hipError_t launch_coarsen(const Geom &g, const Geom &gc, const int32_t *sel, int
                           hipStream_t s) {
   const int64_t nrows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_coarsen", s);
-  hipLaunchKernelGGL(coarsen_kernel, dim3((unsigned)((nrows + kCoarsenRows - 1) / kCoarsenRows)),
-                     dim3(kCoarsenRows), (size_t)kCoarsenRows * g.ksel * sizeof(int32_t), s, sel, g, gc, csel, cq);
+  hipLaunchKernelGGL(coarsen_kernel, dim3((unsigned)((nrows + 3) / 4)), dim3(256), 0, s, sel, g, gc, csel, cq);
   timing_end(s);
   return hipGetLastError();
 }

@@ -165,3 +165,39 @@ def test_paper_geometry_32k_sampled():
     log(f"[block16] paper geometry: {rows.size} rows, {exempt} exempt; grad rel-L2 dQ {e_dq:.2e} dK {e_dk:.2e} "
         f"dV {e_dv:.2e}")
     assert max(e_dq, e_dk, e_dv) < GRAD_REL_L2["bf16"]
+
+
+def test_scattered_selection_many_tiles():
+    """A given selection of 57 blocks of 16 tokens spread one per 64-key tile
+    (more tiles than phsa_select could produce in this geometry): every tile
+    must reach the attention kernels."""
+    B, L, Hq, Hkv, d, m = 1, 4096, 2, 1, 128, 16
+    cfg = phsa.Config(block_size=m, top_k=16, n_init_blocks=8, window=512)
+    ks = cfg.ksel
+    assert ks == 57
+    g = torch.Generator().manual_seed(29)
+    q = torch.randn(B, L, Hq, d, generator=g).to(torch.bfloat16)
+    k = torch.randn(B, L, Hkv, d, generator=g).to(torch.bfloat16)
+    v = torch.randn(B, L, Hkv, d, generator=g).to(torch.bfloat16)
+    do = torch.randn(B, L, Hq, d, generator=g).to(torch.bfloat16)
+    sel = -np.ones((B, Hkv, L, ks), np.int32)
+    rng = np.random.default_rng(4)
+    for i in range(L):
+        cur = i // m
+        tiles = np.arange(cur // 4 + 1)
+        pick = np.sort(rng.choice(tiles, size=min(ks - 1, tiles.size), replace=False))
+        row = sorted(set((4 * pick + rng.integers(0, 4, pick.size)).clip(max=cur).tolist()) | {cur})
+        sel[0, 0, i, :len(row)] = row[:ks]
+    assert (np.unique(sel[0, 0, -1] // 4).size - 1) > 27       # more tiles than the select-made bound
+    sel_t = torch.from_numpy(sel).cuda()
+    o, lse = phsa.attn_fwd(q.cuda(), k.cuda(), v.cuda(), sel_t, cfg)
+    dq, dk, dv = phsa.attn_bwd(q.cuda(), k.cuda(), v.cuda(), o, do.cuda(), lse, sel_t, cfg)
+    torch.cuda.synchronize()
+    qh, kh, vh, doh = (x.float().numpy() for x in (q, k, v, do))
+    scale = d ** -0.5
+    o_r, lse_r = oracle.attn_fwd(qh, kh, vh, sel, m, scale)
+    np.testing.assert_allclose(to_np(o), o_r, atol=O_TOL["bf16"], rtol=0)
+    np.testing.assert_allclose(to_np(lse), lse_r, atol=O_TOL["bf16"], rtol=0)
+    dq_r, dk_r, dv_r = oracle.attn_bwd(qh, kh, vh, doh, sel, m, scale)
+    errs = (rel_l2(to_np(dq), dq_r), rel_l2(to_np(dk), dk_r), rel_l2(to_np(dv), dv_r))
+    assert max(errs) < GRAD_REL_L2["bf16"], errs
