@@ -118,8 +118,9 @@ def kernel_stats(names):
 
 
 KERNELS = ["phsa_compress", "phsa_select_split", "phsa_select", "phsa_coarsen", "phsa_index_count", "phsa_index_scan_tiles", "phsa_index_scan_lists",
-           "phsa_index_fill", "phsa_attn_fwd_sparse", "phsa_attn_fwd_combine", "phsa_attn_bwd_pre",
-           "phsa_attn_bwd_sparse", "phsa_attn_bwd_dkv_finalize", "phsa_attn_bwd_dq_combine"]
+           "phsa_index_fill", "phsa_attn_fwd_sparse", "phsa_attn_fwd_band", "phsa_attn_fwd_combine",
+           "phsa_attn_bwd_pre", "phsa_attn_bwd_band_dkv", "phsa_attn_bwd_band_dq", "phsa_attn_bwd_sparse",
+           "phsa_attn_bwd_dkv_finalize", "phsa_attn_bwd_dq_combine"]
 
 
 def selected_tiles(sel: torch.Tensor, seqlen_k: int, block: int) -> int:

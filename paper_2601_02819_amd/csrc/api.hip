@@ -24,7 +24,9 @@ size_t index_layout(const Geom &g, char *base, IndexWs *ix) {
   const int64_t nbgt = R * g.T;
   w.W = (g.Lq + kIndexTile - 1) / kIndexTile;
   w.unit_tokens = 64 * (64 / g.G);  // 64 chunks of 64 MFMA rows
-  w.nnz_max = R * g.Lq * g.ksel;
+  w.nnz_max = R * g.Lq * (g.ksel - g.band);  // a band geometry's last slot is the band partial
+  w.band_base = w.nnz_max;
+  w.discard = (w.nnz_max + (g.band ? R * g.Lq : 0)) * g.G;
   w.units_max = nbgt + (w.nnz_max + w.unit_tokens - 1) / w.unit_tokens;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -38,29 +40,36 @@ size_t index_layout(const Geom &g, char *base, IndexWs *ix) {
   w.uoff = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (nbgt + 1)));
   w.totals = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * 4));
   w.tok = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * w.nnz_max));
-  w.pmap = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * w.nnz_max));
+  w.pmap = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * R * g.Lq * g.ksel));  // every slot, band slot too
   w.units = reinterpret_cast<int2 *>(take(sizeof(int2) * w.units_max));
   if (ix) *ix = w;
   return off;
 }
 
-// bf16 attention with blocks of m = 16 or 32 tokens runs on 64-key tiles:
-// the selection is regrouped per tile with a mask of its 16-key quarters.
-bool tiles_coarsened(const Geom &g) { return g.dtype == PHSA_BF16 && g.m != 64; }
+// bf16 attention with a local window of at least one 64-key tile attends to
+// the windows with the band kernels (dense, query-major for O and dQ,
+// key-major for dK/dV) and to the other selected blocks with the sparse ones.
+bool band_on(const Geom &g) {
+  return g.dtype == PHSA_BF16 && g.window >= 64 && std::min(g.ksel, g.Lk / 64) <= 63;
+}
+
+// bf16 attention with blocks of m = 16 or 32 tokens, or with the band, runs
+// on a regrouped selection: 64-key tiles with a mask of their 16-key quarters.
+bool tiles_coarsened(const Geom &g) { return g.dtype == PHSA_BF16 && (g.m != 64 || band_on(g)); }
 
 // Tile geometry: m = 64, T = Lk / 64, and ksel = the most distinct tiles a
-// row can hold, min(Ksel, T).  (A selection made by phsa_select needs fewer:
-// ceil(n_init m / 64) init tiles, at most ceil(w / 64) + 1 local ones and one
-// per pick, 27 against Ksel = 57 in the paper's geometry; but sel may be any
-// ascending causal block list.)
+// row can hold, min(Ksel, T), plus the band slot.  (A selection made by
+// phsa_select needs fewer: ceil(n_init m / 64) init tiles, at most
+// ceil(w / 64) + 1 local ones and one per pick, 27 against Ksel = 57 in the
+// paper's geometry; but sel may be any ascending causal block list.)  n_init
+// and window stay in units of the selection's blocks (sm).
 Geom tile_geom(const Geom &g) {
   if (!tiles_coarsened(g)) return g;
   Geom t = g;
+  t.band = band_on(g) ? 1 : 0;
   t.m = 64;
   t.T = g.Lk / 64;
-  t.ksel = std::min(g.ksel, t.T);
-  t.n_init = (g.n_init * g.m + 63) / 64;
-  t.window = 0;
+  t.ksel = std::min(g.ksel, t.T) + t.band;
   return t;
 }
 
@@ -68,13 +77,14 @@ struct Coarse {
   Geom gc;            // tile geometry (== g when not coarsened)
   int32_t *csel;      // [B, Hkv, Lq, gc.ksel] tiles per row, NULL when not coarsened
   uint8_t *cq;        // [B, Hkv, Lq, gc.ksel] quarter masks
+  uint8_t *bflag;     // [B, Hkv, Lq] rows whose local window is in the band (band geometry only)
 };
 
 // The coarsened selection sits at the start of the forward and backward
 // workspaces, followed by the index, so a backward that reuses the forward's
 // index finds it at the same place.
 size_t coarse_layout(const Geom &g, char *base, Coarse *c) {
-  Coarse w{tile_geom(g), nullptr, nullptr};
+  Coarse w{tile_geom(g), nullptr, nullptr, nullptr};
   size_t off = 0;
   if (tiles_coarsened(g)) {
     const size_t n = (size_t)g.B * g.Hkv * g.Lq * w.gc.ksel;
@@ -82,6 +92,10 @@ size_t coarse_layout(const Geom &g, char *base, Coarse *c) {
     off += align_up(n * sizeof(int32_t));
     w.cq = base ? reinterpret_cast<uint8_t *>(base + off) : nullptr;
     off += align_up(n);
+    if (w.gc.band) {
+      w.bflag = base ? reinterpret_cast<uint8_t *>(base + off) : nullptr;
+      off += align_up((size_t)g.B * g.Hkv * g.Lq);
+    }
   }
   if (c) *c = w;
   return off;
@@ -99,6 +113,7 @@ struct BwdWs {
   float *Dvec;
   void *dqpart;
   float *dkvpart;
+  float *bkv;         // band geometry: the band's dK/dV per 64-key tile, float32 [B*Hkv*T][2][64][d]
 };
 
 size_t elem_bytes(const Geom &g) { return g.dtype == PHSA_BF16 ? 2 : 4; }
@@ -109,9 +124,11 @@ size_t fwd_layout(const Geom &g0, char *base, FwdWs *ws) {
   size_t off = coarse_layout(g0, base, &w.co);
   const Geom &g = w.co.gc;
   off += index_layout(g, base ? base + off : nullptr, &w.ix);
-  // partials in list order, one per (entry, head), plus one discard row that
-  // absorbs the stores of rows past the end of a chunk
-  const int64_t slots = w.ix.nnz_max * g.G + 1;
+  w.ix.bflag = w.co.bflag;
+  // partials in list order, one per (entry, head), then the band partials (a
+  // band geometry), then one discard row that absorbs the stores of rows past
+  // the end of a chunk
+  const int64_t slots = w.ix.discard + 1;
   w.opart = base ? base + off : nullptr;
   off += align_up(slots * g.d * elem_bytes(g));
   w.ml = base ? reinterpret_cast<float2 *>(base + off) : nullptr;
@@ -122,21 +139,26 @@ size_t fwd_layout(const Geom &g0, char *base, FwdWs *ws) {
 
 size_t bwd_layout(const Geom &g0, char *base, BwdWs *ws) {
   BwdWs w{};
-  w.co = Coarse{tile_geom(g0), nullptr, nullptr};
+  w.co = Coarse{tile_geom(g0), nullptr, nullptr, nullptr};
   const Geom g = w.co.gc;
   size_t off = 0;
   if (g.dtype == PHSA_BF16) {
     off = coarse_layout(g0, base, &w.co);
     off += index_layout(g, base ? base + off : nullptr, &w.ix);
+    w.ix.bflag = w.co.bflag;
   }
   w.Dvec = base ? reinterpret_cast<float *>(base + off) : nullptr;
   off += align_up(sizeof(float) * (size_t)g.B * g.Hq * g.Lq);
   if (g.dtype == PHSA_BF16) {
-    const int64_t slots = w.ix.nnz_max * g.G + 1;  // + the discard row
+    const int64_t slots = w.ix.discard + 1;  // list and band partials + the discard row
     w.dqpart = base ? base + off : nullptr;
     off += align_up(slots * g.d * elem_bytes(g));
     w.dkvpart = base ? reinterpret_cast<float *>(base + off) : nullptr;
     off += align_up(sizeof(float) * (size_t)w.ix.units_max * 2 * 64 * g.d);
+    if (g.band) {
+      w.bkv = base ? reinterpret_cast<float *>(base + off) : nullptr;
+      off += align_up(sizeof(float) * (size_t)g.B * g.Hkv * g.T * 2 * 64 * g.d);
+    }
   }
   if (ws) *ws = w;
   return off;
@@ -207,6 +229,8 @@ phsa_status validate(const phsa_params *p, int op, Geom *out) {
     g.scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.f / sqrtf((float)p->head_dim);
     g.dtype = p->dtype;
     g.sel_mode = (p->flags & PHSA_FLAG_SELECT_SOFTMAX_SUM) ? 1 : 0;
+    g.sm = g.m;
+    g.band = 0;
     *out = g;
   }
   return PHSA_OK;
@@ -242,7 +266,7 @@ hipError_t attn_fwd_bf16(const Geom &g, const void *Q, const void *K, const void
   fwd_layout(g, static_cast<char *>(ws), &w);
   const int32_t *tsel = sel;
   if (w.co.csel) {
-    const hipError_t e = launch_coarsen(g, w.co.gc, sel, w.co.csel, w.co.cq, s);
+    const hipError_t e = launch_coarsen(g, w.co.gc, sel, w.co.csel, w.co.cq, w.co.bflag, s);
     if (e != hipSuccess) return e;
     tsel = w.co.csel;
   }
@@ -393,13 +417,13 @@ phsa_status phsa_attn_bwd(const phsa_params *p, const void *Q, const void *K, co
     const int32_t *tsel = sel;
     if (w.co.csel) {  // tiles of the m-token blocks (already there when the index is reused)
       if (!reuse) {
-        const hipError_t e = launch_coarsen(g, w.co.gc, sel, w.co.csel, w.co.cq, s);
+        const hipError_t e = launch_coarsen(g, w.co.gc, sel, w.co.csel, w.co.cq, w.co.bflag, s);
         if (e != hipSuccess) return PHSA_ERR_HIP;
       }
       tsel = w.co.csel;
     }
     return from_hip(launch_attn_bwd(w.co.gc, Q, K, V, O, dO, LSE, tsel, w.co.cq, dQ, dK, dV, w.ix, w.Dvec, w.dqpart,
-                                    w.dkvpart, reuse, s));
+                                    w.dkvpart, w.bkv, reuse, s));
   })
 }
 

@@ -1,0 +1,534 @@
+// Local windows as dense attention (the "band"), bf16.
+//
+// Algorithm 1 always keeps the local window: blocks max(0, cur - w/m) .. cur
+// of every query row, i.e. the keys [A(i), pos(i)] with
+//   A(i) = max(cur - w/m, min(n_init, cur + 1)) * m
+// (the init blocks below it stay with the sparse kernels).  These key ranges
+// slide with the row, so consecutive rows share almost all of them.  In the
+// key-block-major sparse kernels each (row, window tile) pair would gather
+// the row and leave a partial; here the window is attended densely instead:
+//   forward, dQ : query-major.  A workgroup holds 128 (token, head) MFMA rows
+//                 (128 / G consecutive tokens) in registers and streams the
+//                 64-key tiles covering their windows through LDS, with an
+//                 online softmax (forward) or the dQ accumulation (backward).
+//                 A row leaves one partial in the same format and buffer as
+//                 the sparse partials, at list position band_base + row; the
+//                 per-row merges find it through the row's last index slot.
+//   dK, dV      : key-major.  A workgroup holds one 64-key tile (wave w owns
+//                 keys 16w..16w+15, accumulators in registers) and streams the
+//                 contiguous rows whose windows reach into it; it writes the
+//                 tile's float32 dK/dV to bkv, which the sparse backward's
+//                 epilogue and the dK/dV finalize add to the sparse part.
+// Only rows that hold their whole window (bflag, set when the selection is
+// regrouped) take part; other rows keep every block in the sparse kernels.
+// Operand layouts and the transposing LDS reads are those of the sparse
+// kernels (attn_fwd.hip, attn_bwd.hip).
+#include <math.h>
+
+#include "common.h"
+#include "launch.h"
+
+namespace phsa {
+
+// First key of the band of the query at position pos (selection blocks of gm.sm tokens).
+__device__ __forceinline__ int band_first_key(const Geom &gm, int pos) {
+  const int cur = pos / gm.sm;
+  return max(max(0, cur - gm.window / gm.sm), min(gm.n_init, cur + 1)) * gm.sm;
+}
+
+// ---------------------------------------------------------------- forward
+template <int D, int G>
+__global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__restrict__ Q,
+                                                               const bf16_t *__restrict__ K,
+                                                               const bf16_t *__restrict__ V, Geom gm, IndexWs ix,
+                                                               bf16_t *__restrict__ opart, float2 *__restrict__ ml) {
+  constexpr int RT = 2;                  // 16-row chunks per wave
+  constexpr int TOK = 4 * RT * 16 / G;   // tokens per workgroup
+  constexpr int KP = D + 16, VP = D + 8, SP = D + 8;
+  constexpr int VPR = D / 8, KB = D / 32, NT = D / 16;
+  constexpr int NV = 64 * VPR / 256;     // 16-byte loads per thread per tensor per tile
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * VP];
+  __shared__ __attribute__((aligned(16))) bf16_t Os[4][16 * SP];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
+  const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
+  const int i0 = blockIdx.x * TOK, i1 = min(i0 + TOK, gm.Lq) - 1;
+  const uint8_t *bf = ix.bflag + (int64_t)bg * gm.Lq;
+
+  // the rows of this lane: chunk c, MFMA row (wave RT + c) 16 + l16
+  int pos[RT], a0[RT], tokc[RT];
+  bool ok[RT];
+  bf16x8 qf[RT][KB];
+#pragma unroll
+  for (int c = 0; c < RT; ++c) {
+    const int r = (wave * RT + c) * 16 + l16;
+    const int tok = i0 + r / G, h = r % G;
+    const int ti = min(tok, i1);
+    tokc[c] = tok;
+    ok[c] = tok <= i1 && bf[ti] != 0;
+    pos[c] = gm.q_pos0 + ti;
+    a0[c] = band_first_key(gm, pos[c]);
+    const bf16_t *src = Q + (((int64_t)b * gm.Lq + ti) * gm.Hq + g * G + h) * D;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) qf[c][kb] = load_bf16x8(src + kb * 32 + kq);
+  }
+  if (!__syncthreads_or(ok[0] || ok[RT - 1])) return;
+  const int kt_lo = band_first_key(gm, gm.q_pos0 + i0) / 64, kt_hi = (gm.q_pos0 + i1) / 64;
+
+  const float sl2 = gm.scale * kLog2e;
+  float mrun[RT], lrun[RT];
+  f32x4 o[RT][NT];
+#pragma unroll
+  for (int c = 0; c < RT; ++c) {
+    mrun[c] = -INFINITY;
+    lrun[c] = 0.f;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) o[c][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  // each tile's loads are issued before the barrier that waits for the previous
+  // tile's use; the other workgroup on the CU covers the rest of their latency
+  for (int kt = kt_lo; kt <= kt_hi; ++kt) {
+    u32x4 kr[NV], vr[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int x = tid + 256 * v, kk = x / VPR, c8 = (x % VPR) * 8;
+      const int64_t src = (((int64_t)b * gm.Lk + (int64_t)kt * 64 + kk) * gm.Hkv + g) * D + c8;
+      kr[v] = *reinterpret_cast<const u32x4 *>(K + src);
+      vr[v] = *reinterpret_cast<const u32x4 *>(V + src);
+    }
+    lds_barrier();
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int x = tid + 256 * v, kk = x / VPR, c8 = (x % VPR) * 8;
+      *reinterpret_cast<u32x4 *>(&Ks[kk * KP + c8]) = kr[v];
+      *reinterpret_cast<u32x4 *>(&Vs[kk * VP + c8]) = vr[v];
+    }
+    lds_barrier();
+    const int key0 = kt * 64;
+    // S^T = K Q^T for both chunks (every K fragment read from LDS feeds both)
+    f32x4 sa[RT][4];
+#pragma unroll
+    for (int c = 0; c < RT; ++c)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sa[c][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bf16x8 kfr = load_bf16x8(&Ks[(j * 16 + l16) * KP + kb * 32 + kq]);
+#pragma unroll
+        for (int c = 0; c < RT; ++c) sa[c][j] = mfma16x16x32(kfr, qf[c][kb], sa[c][j]);
+      }
+    bf16x8 pb[RT][2];
+    float fs[RT];
+#pragma unroll
+    for (int c = 0; c < RT; ++c) {
+      f32x4 (&st)[4] = sa[c];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = key0 + j * 16 + q4 * 4 + r;
+          const float v = (ok[c] && key >= a0[c] && key <= pos[c]) ? st[j][r] * sl2 : -INFINITY;
+          st[j][r] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mn = fmaxf(mrun[c], mx);
+      const float mref = mn == -INFINITY ? 0.f : mn;    // no key of the row yet: every weight is 0
+      const float f = exp2f(mrun[c] - mref);            // 0 while the running sum is still empty
+      float l = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = exp2f(st[j][r] - mref);
+          st[j][r] = p;
+          l += p;
+        }
+      l += __shfl_xor(l, 16, 64);
+      l += __shfl_xor(l, 32, 64);
+      lrun[c] = lrun[c] * f + l;
+      mrun[c] = mn;
+      fs[c] = f;
+      pb[c][0] = pack_bf16x8(st[0], st[1]);
+      pb[c][1] = pack_bf16x8(st[2], st[3]);
+    }
+    // O^T = O^T f + V^T P^T for both chunks (every V^T fragment feeds both)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const bf16x8 v0 = lds_col8(Vs, VP, q4 * 4, 16 + q4 * 4, nt * 16, l16);
+      const bf16x8 v1 = lds_col8(Vs, VP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16);
+#pragma unroll
+      for (int c = 0; c < RT; ++c) {
+        o[c][nt] *= fs[c];
+        o[c][nt] = mfma16x16x32(v0, pb[c][0], o[c][nt]);
+        o[c][nt] = mfma16x16x32(v1, pb[c][1], o[c][nt]);
+      }
+    }
+  }
+
+  // partials: row (token, head) at list position band_base + (b, g, token); rows
+  // outside the band go to the discard row
+  auto dest = [&](int r) {
+    const int tok = i0 + r / G;
+    const bool v = tok <= i1 && bf[min(tok, i1)] != 0;
+    return v ? (ix.band_base + (int64_t)bg * gm.Lq + tok) * G + r % G : ix.discard;
+  };
+#pragma unroll
+  for (int c = 0; c < RT; ++c) {
+    const int r0 = (wave * RT + c) * 16;
+    ml[q4 == 0 ? dest(r0 + l16) : ix.discard] = make_float2(mrun[c], lrun[c]);
+    bf16_t *os = Os[wave];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const bf16_t o4[4] = {f32_to_bf16(o[c][nt][0]), f32_to_bf16(o[c][nt][1]), f32_to_bf16(o[c][nt][2]),
+                            f32_to_bf16(o[c][nt][3])};
+      *reinterpret_cast<uint2 *>(&os[l16 * SP + nt * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(o4);
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int k = 0; k < 16 * VPR / 64; ++k) {
+      const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
+      *reinterpret_cast<uint4 *>(opart + dest(r0 + r) * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
+    }
+    wave_lds_sync();
+  }
+  (void)tokc;
+}
+
+// ---------------------------------------------------------------- backward: dQ
+template <int D, int G>
+__global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
+    const bf16_t *__restrict__ Q, const bf16_t *__restrict__ K, const bf16_t *__restrict__ V,
+    const bf16_t *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dvec, Geom gm, IndexWs ix,
+    bf16_t *__restrict__ dqpart) {
+  constexpr int RT = 1;                  // one 16-row chunk per wave (registers)
+  constexpr int TOK = 4 * RT * 16 / G;
+  constexpr int KP = D + 16, SP = D + 8;  // K and V: 16-byte row reads and transposing reads
+  constexpr int VPR = D / 8, KB = D / 32, NT = D / 16;
+  constexpr int NV = 64 * VPR / 256;
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Os[4][16 * SP];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
+  const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
+  const int i0 = blockIdx.x * TOK, i1 = min(i0 + TOK, gm.Lq) - 1;
+  const uint8_t *bf = ix.bflag + (int64_t)bg * gm.Lq;
+
+  int pos[RT], a0[RT];
+  bool ok[RT];
+  float lse2[RT], dd[RT];
+  bf16x8 qf[RT][KB], df[RT][KB];
+#pragma unroll
+  for (int c = 0; c < RT; ++c) {
+    const int r = (wave * RT + c) * 16 + l16;
+    const int tok = i0 + r / G, h = g * G + r % G;
+    const int ti = min(tok, i1);
+    ok[c] = tok <= i1 && bf[ti] != 0;
+    pos[c] = gm.q_pos0 + ti;
+    a0[c] = band_first_key(gm, pos[c]);
+    lse2[c] = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + ti] * kLog2e;
+    dd[c] = Dvec[((int64_t)b * gm.Lq + ti) * gm.Hq + h];
+    const int64_t src = (((int64_t)b * gm.Lq + ti) * gm.Hq + h) * D;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      qf[c][kb] = load_bf16x8(Q + src + kb * 32 + kq);
+      df[c][kb] = load_bf16x8(dO + src + kb * 32 + kq);
+    }
+  }
+  if (!__syncthreads_or(ok[0])) return;
+  const int kt_lo = band_first_key(gm, gm.q_pos0 + i0) / 64, kt_hi = (gm.q_pos0 + i1) / 64;
+
+  const float sl2 = gm.scale * kLog2e;
+  f32x4 dq[RT][NT];
+#pragma unroll
+  for (int c = 0; c < RT; ++c)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) dq[c][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // each tile's loads are issued before the barrier that waits for the previous
+  // tile's use; the other workgroup on the CU covers the rest of their latency
+  for (int kt = kt_lo; kt <= kt_hi; ++kt) {
+    u32x4 kr[NV], vr[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int x = tid + 256 * v, kk = x / VPR, c8 = (x % VPR) * 8;
+      const int64_t src = (((int64_t)b * gm.Lk + (int64_t)kt * 64 + kk) * gm.Hkv + g) * D + c8;
+      kr[v] = *reinterpret_cast<const u32x4 *>(K + src);
+      vr[v] = *reinterpret_cast<const u32x4 *>(V + src);
+    }
+    lds_barrier();
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int x = tid + 256 * v, kk = x / VPR, c8 = (x % VPR) * 8;
+      *reinterpret_cast<u32x4 *>(&Ks[kk * KP + c8]) = kr[v];
+      *reinterpret_cast<u32x4 *>(&Vs[kk * KP + c8]) = vr[v];
+    }
+    lds_barrier();
+    const int key0 = kt * 64;
+#pragma unroll
+    for (int c = 0; c < RT; ++c) {
+      // S^T = K Q^T and dP^T = V dO^T: lane (q, j) holds keys 16 jt + 4 q + r of row j
+      f32x4 st[4], dp[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) st[j] = dp[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          st[j] = mfma16x16x32(load_bf16x8(&Ks[(j * 16 + l16) * KP + kb * 32 + kq]), qf[c][kb], st[j]);
+          dp[j] = mfma16x16x32(load_bf16x8(&Vs[(j * 16 + l16) * KP + kb * 32 + kq]), df[c][kb], dp[j]);
+        }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = key0 + j * 16 + q4 * 4 + r;
+          const float p = (ok[c] && key >= a0[c] && key <= pos[c]) ? exp2f(st[j][r] * sl2 - lse2[c]) : 0.f;
+          dp[j][r] = p * (dp[j][r] - dd[c]);
+        }
+      // dQ^T += K^T dS^T
+      const bf16x8 sb0 = pack_bf16x8(dp[0], dp[1]), sb1 = pack_bf16x8(dp[2], dp[3]);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        dq[c][nt] = mfma16x16x32(lds_col8(Ks, KP, q4 * 4, 16 + q4 * 4, nt * 16, l16), sb0, dq[c][nt]);
+        dq[c][nt] = mfma16x16x32(lds_col8(Ks, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dq[c][nt]);
+      }
+    }
+  }
+
+  auto dest = [&](int r) {
+    const int tok = i0 + r / G;
+    const bool v = tok <= i1 && bf[min(tok, i1)] != 0;
+    return v ? (ix.band_base + (int64_t)bg * gm.Lq + tok) * G + r % G : ix.discard;
+  };
+#pragma unroll
+  for (int c = 0; c < RT; ++c) {
+    const int r0 = (wave * RT + c) * 16;
+    bf16_t *os = Os[wave];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const bf16_t o4[4] = {f32_to_bf16(dq[c][nt][0] * gm.scale), f32_to_bf16(dq[c][nt][1] * gm.scale),
+                            f32_to_bf16(dq[c][nt][2] * gm.scale), f32_to_bf16(dq[c][nt][3] * gm.scale)};
+      *reinterpret_cast<uint2 *>(&os[l16 * SP + nt * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(o4);
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int k = 0; k < 16 * VPR / 64; ++k) {
+      const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
+      *reinterpret_cast<uint4 *>(dqpart + dest(r0 + r) * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
+    }
+    wave_lds_sync();
+  }
+}
+
+// ---------------------------------------------------------------- backward: dK, dV
+// One workgroup per (b, g, 64-key tile kt).  The rows whose band reaches into
+// the tile are tokens kt 64 - q_pos0 .. (the last token with A(i) <= kt 64 + 63);
+// they stream through in chunks of 64 MFMA rows (64 / G tokens, heads inner).
+template <int D, int G>
+__global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
+    const bf16_t *__restrict__ Q, const bf16_t *__restrict__ K, const bf16_t *__restrict__ V,
+    const bf16_t *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dvec, Geom gm, IndexWs ix,
+    float *__restrict__ bkv) {
+  constexpr int CT = 64 / G;             // tokens per chunk
+  constexpr int KPQ = D + 16;
+  constexpr int VPR = D / 8, KB = D / 32, NT = D / 16;
+  constexpr int NV = 64 * VPR / 256;     // 16-byte loads per thread per tensor per chunk
+  constexpr int KPK = D + 8;
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KPK];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KPK];
+  __shared__ __attribute__((aligned(16))) bf16_t Qs[64 * KPQ];
+  __shared__ __attribute__((aligned(16))) bf16_t dOs[64 * KPQ];
+  __shared__ __attribute__((aligned(16))) float lse_s[64];
+  __shared__ __attribute__((aligned(16))) float dd_s[64];
+  __shared__ __attribute__((aligned(16))) int pos_s[64];
+  __shared__ __attribute__((aligned(16))) int a_s[64];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
+  const int kt = blockIdx.x, bg = blockIdx.y, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
+  const uint8_t *bf = ix.bflag + (int64_t)bg * gm.Lq;
+  const int key0 = kt * 64;
+  // rows: from the first token that sees key0 to the last whose band starts by key0 + 63
+  const int r_lo = max(0, key0 - gm.q_pos0);
+  const int cmax = (key0 + 63) / gm.sm + gm.window / gm.sm;
+  const int r_hi = min(gm.Lq - 1, (cmax + 1) * gm.sm - 1 - gm.q_pos0);
+
+  // the tile's keys and values (wave w reads its keys 16w..16w+15 as B operands)
+  for (int x = tid; x < 64 * VPR; x += 256) {
+    const int kk = x / VPR, c8 = (x % VPR) * 8;
+    const int64_t src = (((int64_t)b * gm.Lk + key0 + kk) * gm.Hkv + g) * D + c8;
+    *reinterpret_cast<uint4 *>(&Ks[kk * KPK + c8]) = *reinterpret_cast<const uint4 *>(K + src);
+    *reinterpret_cast<uint4 *>(&Vs[kk * KPK + c8]) = *reinterpret_cast<const uint4 *>(V + src);
+  }
+  f32x4 dkt[NT], dvt[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) dkt[n] = dvt[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const float sl2 = gm.scale * kLog2e;
+  const int key = key0 + wave * 16 + l16;  // the key whose S column this lane holds
+  for (int c0 = r_lo; c0 <= r_hi; c0 += CT) {
+    // the chunk's rows (token c0 + r / G, head r % G; tokens past r_hi repeat the
+    // last one and are masked) and, for thread r < 64, that row's LSE, D,
+    // position (-1: not in the band) and band start; loaded before the barrier
+    u32x4 pq[NV], pd[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int x = tid + 256 * v, r = x / VPR, c8 = (x % VPR) * 8;
+      const int tok = min(c0 + r / G, r_hi);
+      const int64_t src = (((int64_t)b * gm.Lq + tok) * gm.Hq + g * G + r % G) * D + c8;
+      pq[v] = *reinterpret_cast<const u32x4 *>(Q + src);
+      pd[v] = *reinterpret_cast<const u32x4 *>(dO + src);
+    }
+    float plse = 0.f, pdd = 0.f;
+    int ppos = -1, pa = 0;
+    if (tid < 64) {
+      const int tok = c0 + tid / G, h = g * G + tid % G;
+      const int ti = min(tok, r_hi);
+      plse = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + ti];
+      pdd = Dvec[((int64_t)b * gm.Lq + ti) * gm.Hq + h];
+      ppos = (tok <= r_hi && bf[ti] != 0) ? gm.q_pos0 + ti : -1;
+      pa = band_first_key(gm, gm.q_pos0 + ti);
+    }
+    lds_barrier();
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int x = tid + 256 * v, r = x / VPR, c8 = (x % VPR) * 8;
+      *reinterpret_cast<u32x4 *>(&Qs[r * KPQ + c8]) = pq[v];
+      *reinterpret_cast<u32x4 *>(&dOs[r * KPQ + c8]) = pd[v];
+    }
+    if (tid < 64) {
+      lse_s[tid] = plse * kLog2e;
+      dd_s[tid] = pdd;
+      pos_s[tid] = ppos;
+      a_s[tid] = pa;
+    }
+    lds_barrier();
+
+    // S and dP: 64 rows (4 tiles) x this wave's 16 keys; lane (q, j) holds rows 16 mt + 4 q + r of key j
+    f32x4 s[4], dp[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) s[mt] = dp[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const bf16x8 kf = load_bf16x8(&Ks[(wave * 16 + l16) * KPK + kb * 32 + kq]);
+      const bf16x8 vf = load_bf16x8(&Vs[(wave * 16 + l16) * KPK + kb * 32 + kq]);
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        s[mt] = mfma16x16x32(load_bf16x8(&Qs[(mt * 16 + l16) * KPQ + kb * 32 + kq]), kf, s[mt]);
+        dp[mt] = mfma16x16x32(load_bf16x8(&dOs[(mt * 16 + l16) * KPQ + kb * 32 + kq]), vf, dp[mt]);
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const int r0 = mt * 16 + q4 * 4;
+      const float4 lse4 = *reinterpret_cast<const float4 *>(&lse_s[r0]);
+      const float4 dd4 = *reinterpret_cast<const float4 *>(&dd_s[r0]);
+      const int4 pos4 = *reinterpret_cast<const int4 *>(&pos_s[r0]);
+      const int4 a4 = *reinterpret_cast<const int4 *>(&a_s[r0]);
+      const float lsev[4] = {lse4.x, lse4.y, lse4.z, lse4.w};
+      const float ddv[4] = {dd4.x, dd4.y, dd4.z, dd4.w};
+      const int posv[4] = {pos4.x, pos4.y, pos4.z, pos4.w};
+      const int av[4] = {a4.x, a4.y, a4.z, a4.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = (key <= posv[r] && key >= av[r]) ? exp2f(s[mt][r] * sl2 - lsev[r]) : 0.f;
+        s[mt][r] = p;
+        dp[mt][r] = p * (dp[mt][r] - ddv[r]);
+      }
+    }
+    const bf16x8 pb0 = pack_bf16x8(s[0], s[1]), pb1 = pack_bf16x8(s[2], s[3]);
+    const bf16x8 sb0 = pack_bf16x8(dp[0], dp[1]), sb1 = pack_bf16x8(dp[2], dp[3]);
+    // dV^T += dO^T P,  dK^T += Q^T dS   (feature tiles x this wave's keys)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      dvt[nt] = mfma16x16x32(lds_col8(dOs, KPQ, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, dvt[nt]);
+      dvt[nt] = mfma16x16x32(lds_col8(dOs, KPQ, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, dvt[nt]);
+      dkt[nt] = mfma16x16x32(lds_col8(Qs, KPQ, q4 * 4, 16 + q4 * 4, nt * 16, l16), sb0, dkt[nt]);
+      dkt[nt] = mfma16x16x32(lds_col8(Qs, KPQ, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dkt[nt]);
+    }
+  }
+  // the tile's dK (scaled) and dV: lane (q, j) holds features 16 nt + 4 q .. +3 of key 16 w + j
+  float *pk = bkv + ((int64_t)bg * gm.T + kt) * 2 * 64 * D + (wave * 16 + l16) * D + q4 * 4;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    *reinterpret_cast<float4 *>(pk + nt * 16) =
+        make_float4(dkt[nt][0] * gm.scale, dkt[nt][1] * gm.scale, dkt[nt][2] * gm.scale, dkt[nt][3] * gm.scale);
+    *reinterpret_cast<float4 *>(pk + 64 * D + nt * 16) = make_float4(dvt[nt][0], dvt[nt][1], dvt[nt][2], dvt[nt][3]);
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+template <int D, int G>
+static hipError_t fwd_band_t(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
+                             void *opart, float2 *ml, hipStream_t s) {
+  constexpr int TOK = 128 / G;
+  timing_begin("phsa_attn_fwd_band", s);
+  hipLaunchKernelGGL((attn_fwd_band_kernel<D, G>), dim3((g.Lq + TOK - 1) / TOK, g.B * g.Hkv), dim3(256), 0, s,
+                     static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
+                     g, ix, static_cast<bf16_t *>(opart), ml);
+  timing_end(s);
+  return hipGetLastError();
+}
+
+template <int D, int G>
+static hipError_t bwd_band_t(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                             const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
+                             hipStream_t s) {
+  timing_begin("phsa_attn_bwd_band_dkv", s);
+  hipLaunchKernelGGL((attn_bwd_band_dkv_kernel<D, G>), dim3(g.T, g.B * g.Hkv), dim3(256), 0, s,
+                     static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
+                     static_cast<const bf16_t *>(dO), LSE, Dvec, g, ix, bkv);
+  timing_end(s);
+  constexpr int TOKQ = 64 / G;
+  timing_begin("phsa_attn_bwd_band_dq", s);
+  hipLaunchKernelGGL((attn_bwd_band_dq_kernel<D, G>), dim3((g.Lq + TOKQ - 1) / TOKQ, g.B * g.Hkv), dim3(256), 0, s,
+                     static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
+                     static_cast<const bf16_t *>(dO), LSE, Dvec, g, ix, static_cast<bf16_t *>(dqpart));
+  timing_end(s);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t fwd_band_d(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
+                             void *opart, float2 *ml, hipStream_t s) {
+  switch (g.G) {
+    case 1: return fwd_band_t<D, 1>(g, Q, K, V, ix, opart, ml, s);
+    case 2: return fwd_band_t<D, 2>(g, Q, K, V, ix, opart, ml, s);
+    case 4: return fwd_band_t<D, 4>(g, Q, K, V, ix, opart, ml, s);
+    default: return fwd_band_t<D, 8>(g, Q, K, V, ix, opart, ml, s);
+  }
+}
+
+template <int D>
+static hipError_t bwd_band_d(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                             const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
+                             hipStream_t s) {
+  switch (g.G) {
+    case 1: return bwd_band_t<D, 1>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
+    case 2: return bwd_band_t<D, 2>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
+    case 4: return bwd_band_t<D, 4>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
+    default: return bwd_band_t<D, 8>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
+  }
+}
+
+hipError_t launch_fwd_band(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
+                           void *opart, float2 *ml, hipStream_t s) {
+  return g.d == 128 ? fwd_band_d<128>(g, Q, K, V, ix, opart, ml, s) : fwd_band_d<64>(g, Q, K, V, ix, opart, ml, s);
+}
+
+hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                           const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
+                           hipStream_t s) {
+  return g.d == 128 ? bwd_band_d<128>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s)
+                    : bwd_band_d<64>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
+}
+
+}  // namespace phsa

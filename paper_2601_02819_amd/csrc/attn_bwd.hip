@@ -64,7 +64,8 @@ template <int D, int G>
 __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     const bf16_t *__restrict__ Q, const bf16_t *__restrict__ K, const bf16_t *__restrict__ V,
     const bf16_t *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dvec, Geom gm, IndexWs ix,
-    bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dK, bf16_t *__restrict__ dV, float *__restrict__ dkvpart) {
+    bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dK, bf16_t *__restrict__ dV, float *__restrict__ dkvpart,
+    const float *__restrict__ bkv) {
   constexpr int CT = 64 / G;
   // Row-major [row][d] tiles.  The pitch decides the banks of the 16-byte
   // fragment reads (rows 16m + l16, chunk q4): with D + 16 elements (288 bytes)
@@ -264,7 +265,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       // every lane stores (rows past the chunk's end go to the discard row), so the
       // number of stores per chunk is fixed and the waits for the prefetched rows
       // need not wait for them
-      const int64_t discard = (int64_t)ix.nnz_max * G;
+      const int64_t discard = ix.discard;
 #pragma unroll
       for (int k = 0; k < 16 * VPR / 64; ++k) {
         const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
@@ -279,12 +280,19 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   const int kk = wave * 16 + l16;
   if (whole_block) {
     const int64_t dst = (krow0 + (int64_t)kk * gm.Hkv) * D + q4 * 4;
+    // the band's contribution to these keys (a band geometry), already scaled
+    const float *bk = bkv ? bkv + (int64_t)bgt * 2 * 64 * D + kk * D + q4 * 4 : nullptr;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const bf16_t k4[4] = {f32_to_bf16(dkt[nt][0] * gm.scale), f32_to_bf16(dkt[nt][1] * gm.scale),
-                            f32_to_bf16(dkt[nt][2] * gm.scale), f32_to_bf16(dkt[nt][3] * gm.scale)};
-      const bf16_t v4[4] = {f32_to_bf16(dvt[nt][0]), f32_to_bf16(dvt[nt][1]), f32_to_bf16(dvt[nt][2]),
-                            f32_to_bf16(dvt[nt][3])};
+      float4 ak = make_float4(0.f, 0.f, 0.f, 0.f), av = ak;
+      if (bk) {
+        ak = *reinterpret_cast<const float4 *>(bk + nt * 16);
+        av = *reinterpret_cast<const float4 *>(bk + 64 * D + nt * 16);
+      }
+      const bf16_t k4[4] = {f32_to_bf16(fmaf(dkt[nt][0], gm.scale, ak.x)), f32_to_bf16(fmaf(dkt[nt][1], gm.scale, ak.y)),
+                            f32_to_bf16(fmaf(dkt[nt][2], gm.scale, ak.z)), f32_to_bf16(fmaf(dkt[nt][3], gm.scale, ak.w))};
+      const bf16_t v4[4] = {f32_to_bf16(dvt[nt][0] + av.x), f32_to_bf16(dvt[nt][1] + av.y),
+                            f32_to_bf16(dvt[nt][2] + av.z), f32_to_bf16(dvt[nt][3] + av.w)};
       *reinterpret_cast<uint2 *>(dK + dst + nt * 16) = *reinterpret_cast<const uint2 *>(k4);
       *reinterpret_cast<uint2 *>(dV + dst + nt * 16) = *reinterpret_cast<const uint2 *>(v4);
     }
@@ -301,11 +309,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
 }
 
 // Per (b, g, t): sum float32 partials of multi-unit blocks; zero unselected
-// blocks.  Each block's 2 x 64 x d outputs are split over kFinSplit
-// workgroups; each thread owns 4 consecutive features (16-byte loads).
+// blocks.  A band geometry adds the band's float32 dK/dV of the tile (bkv).
+// Each block's 2 x 64 x d outputs are split over kFinSplit workgroups; each
+// thread owns 4 consecutive features (16-byte loads).
 constexpr int kFinSplit = 16;
 template <int D>
-__global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restrict__ dkvpart, bf16_t *__restrict__ dK,
+__global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restrict__ dkvpart,
+                                                           const float *__restrict__ bkv, bf16_t *__restrict__ dK,
                                                            bf16_t *__restrict__ dV, Geom gm, IndexWs ix) {
   const int bgt = blockIdx.x;
   const int u0 = ix.uoff[bgt], u1 = ix.uoff[bgt + 1];
@@ -316,6 +326,10 @@ __global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restri
   for (int x = blockIdx.y * PER + threadIdx.x * 4; x < (blockIdx.y + 1) * PER; x += 256 * 4) {
     const int kk = x / D, c = x - kk * D;
     float4 sk = make_float4(0.f, 0.f, 0.f, 0.f), sv = sk;
+    if (bkv) {
+      sk = *reinterpret_cast<const float4 *>(bkv + (int64_t)bgt * 2 * 64 * D + x);
+      sv = *reinterpret_cast<const float4 *>(bkv + (int64_t)bgt * 2 * 64 * D + 64 * D + x);
+    }
     for (int u = u0; u < u1; ++u) {
       const float4 a = *reinterpret_cast<const float4 *>(dkvpart + (int64_t)u * 2 * 64 * D + x);
       const float4 v = *reinterpret_cast<const float4 *>(dkvpart + (int64_t)u * 2 * 64 * D + 64 * D + x);
@@ -379,15 +393,20 @@ __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restri
 template <int D, int G>
 static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
                                const float *LSE, const int32_t *sel, void *dQ, void *dK, void *dV, const IndexWs &ix,
-                               const float *Dvec, void *dqpart, float *dkvpart, hipStream_t s) {
+                               const float *Dvec, void *dqpart, float *dkvpart, float *bkv, hipStream_t s) {
+  if (g.band) {  // the band's dQ partials and dK/dV tiles first: the sparse epilogue adds the latter
+    const hipError_t e = launch_bwd_band(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
+    if (e != hipSuccess) return e;
+  }
+  const float *bk = g.band ? bkv : nullptr;
   timing_begin("phsa_attn_bwd_sparse", s);
   hipLaunchKernelGGL((attn_bwd_sparse_kernel<D, G>), dim3((unsigned)ix.units_max), dim3(256), 0, s,
                      static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
                      static_cast<const bf16_t *>(dO), LSE, Dvec, g, ix, static_cast<bf16_t *>(dqpart),
-                     static_cast<bf16_t *>(dK), static_cast<bf16_t *>(dV), dkvpart);
+                     static_cast<bf16_t *>(dK), static_cast<bf16_t *>(dV), dkvpart, bk);
   timing_end(s);
   timing_begin("phsa_attn_bwd_dkv_finalize", s);
-  hipLaunchKernelGGL((dkv_finalize_kernel<D>), dim3(g.B * g.Hkv * g.T, kFinSplit), dim3(256), 0, s, dkvpart,
+  hipLaunchKernelGGL((dkv_finalize_kernel<D>), dim3(g.B * g.Hkv * g.T, kFinSplit), dim3(256), 0, s, dkvpart, bk,
                      static_cast<bf16_t *>(dK), static_cast<bf16_t *>(dV), g, ix);
   timing_end(s);
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;
@@ -401,12 +420,12 @@ static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, cons
 template <int D>
 static hipError_t launch_bwd_d(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
                                const float *LSE, const int32_t *sel, void *dQ, void *dK, void *dV, const IndexWs &ix,
-                               const float *Dvec, void *dqpart, float *dkvpart, hipStream_t s) {
+                               const float *Dvec, void *dqpart, float *dkvpart, float *bkv, hipStream_t s) {
   switch (g.G) {
-    case 1: return launch_bwd_t<D, 1>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, s);
-    case 2: return launch_bwd_t<D, 2>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, s);
-    case 4: return launch_bwd_t<D, 4>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, s);
-    default: return launch_bwd_t<D, 8>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, s);
+    case 1: return launch_bwd_t<D, 1>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    case 2: return launch_bwd_t<D, 2>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    case 4: return launch_bwd_t<D, 4>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    default: return launch_bwd_t<D, 8>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
   }
 }
 
@@ -433,15 +452,15 @@ hipError_t launch_bwd_pre(const Geom &g, const void *O, const void *dO, float *D
 hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
                            const void *dO, const float *LSE, const int32_t *sel, const uint8_t *quarters, void *dQ,
                            void *dK, void *dV, const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart,
-                           bool reuse_index, hipStream_t s) {
+                           float *bkv, bool reuse_index, hipStream_t s) {
   hipError_t e = launch_bwd_pre(g, O, dO, Dvec, s);
   if (e != hipSuccess) return e;
   if (!reuse_index) {
     e = launch_build_index(g, sel, quarters, ix, s);
     if (e != hipSuccess) return e;
   }
-  return g.d == 128 ? launch_bwd_d<128>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, s)
-                    : launch_bwd_d<64>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, s);
+  return g.d == 128 ? launch_bwd_d<128>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s)
+                    : launch_bwd_d<64>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
 }
 
 }  // namespace phsa

@@ -98,7 +98,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
   const float sl2 = gm.scale * kLog2e;
   const int key0 = t * 64;
   // rows of discarded stores (past a chunk's end): one spare partial row
-  const int64_t discard = (int64_t)ix.nnz_max * G;
+  const int64_t discard = ix.discard;
 
   // one wave chunk: rows of list entry e (-1: none) with query fragments q
   auto chunk = [&](int c, int e, const bf16x8 (&q)[KB]) {
@@ -257,6 +257,10 @@ static hipError_t launch_fwd_t(const Geom &g, const void *Q, const void *K, cons
                      static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
                      g, ix, static_cast<bf16_t *>(opart), ml);
   timing_end(s);
+  if (g.band) {
+    const hipError_t e = launch_fwd_band(g, Q, K, V, ix, opart, ml, s);
+    if (e != hipSuccess) return e;
+  }
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_attn_fwd_combine", s);
   hipLaunchKernelGGL((attn_fwd_combine_kernel<D, G>), dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s, ix.pmap,

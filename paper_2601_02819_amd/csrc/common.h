@@ -9,6 +9,9 @@ namespace phsa {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t bf16_t;  // storage type of bfloat16 values
+// 16 raw bytes as a native vector: loads and stores of it are single values
+// (a uint4 struct copy can be lowered to a memcpy through scratch memory)
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -122,6 +125,16 @@ struct RowSlots {
     return s < 32 ? __shfl(pa, src, 64) : __shfl(pb, src, 64);
   }
 };
+
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// fences global and private memory, and values held in registers across it
+// (loads issued before the barrier, stored to LDS after it) can then be sent
+// through scratch memory; this barrier leaves them in registers.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
 // Orders a wave's LDS writes before its following LDS reads of other lanes'
 // data.  A wave's LDS instructions execute in order, so this only has to stop

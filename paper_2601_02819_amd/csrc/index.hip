@@ -141,7 +141,10 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
       ix.tok[pos] = (i << 10) | (qm << 6) | s;
       pm[tid * gm.ksel + s] = pos;
     }
+    // the last slot of a band geometry marks (-2) a row whose local window is in the band
+    const bool in_band = ix.bflag && pm[tid * gm.ksel + gm.ksel - 1] == -2;
     for (; s < gm.ksel; ++s) pm[tid * gm.ksel + s] = -1;
+    if (in_band) pm[tid * gm.ksel + gm.ksel - 1] = (int32_t)(ix.band_base + (int64_t)bg * gm.Lq + i);
   }
   __syncthreads();
   // the tile's rows are consecutive, so their position-map rows form one contiguous run
@@ -159,8 +162,12 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
 // so a tile's blocks sit in adjacent lanes; a tile's first lane finds its
 // output slot by a ballot prefix count and ORs the quarters of the (at most
 // 64 / m) lanes of its group.  Reads and writes are contiguous per row.
+// With gc.band, a row that holds every local block outside the init blocks
+// (a_blk .. cur) leaves them to the band kernels: they are not regrouped, the
+// row's last slot holds -2 and bflag = 1.  Other rows keep all their blocks.
 __global__ __launch_bounds__(256) void coarsen_kernel(const int32_t *__restrict__ sel, Geom g, Geom gc,
-                                                      int32_t *__restrict__ csel, uint8_t *__restrict__ cq) {
+                                                      int32_t *__restrict__ csel, uint8_t *__restrict__ cq,
+                                                      uint8_t *__restrict__ bflag) {
   const int lane = threadIdx.x & 63;
   const int64_t x = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // row (b, g, i)
   if (x >= (int64_t)g.B * g.Hkv * g.Lq) return;                    // whole wave
@@ -168,7 +175,15 @@ __global__ __launch_bounds__(256) void coarsen_kernel(const int32_t *__restrict_
   const int cur = (g.q_pos0 + i) / g.m;
   const int per = 64 / g.m, qpb = g.m / 16;
   const int t = lane < g.ksel ? sel[x * g.ksel + lane] : -1;
-  const bool valid = t >= 0 && t <= cur && t < g.T;
+  const bool in_range = t >= 0 && t <= cur && t < g.T;
+  bool band_ok = false;
+  int a_blk = cur + 1;
+  if (gc.band) {
+    a_blk = max(max(0, cur - g.window / g.m), min(g.n_init, cur + 1));
+    const int have = __popcll(__ballot(in_range && t >= a_blk));
+    band_ok = a_blk <= cur && have == cur - a_blk + 1;
+  }
+  const bool valid = in_range && !(band_ok && t >= a_blk);
   const int tc = valid ? t / per : -1;
   const unsigned qb = valid ? ((1u << qpb) - 1u) << ((t % per) * qpb) : 0u;
   const int prev = __shfl_up(tc, 1, 64);
@@ -184,21 +199,22 @@ __global__ __launch_bounds__(256) void coarsen_kernel(const int32_t *__restrict_
   }
   int32_t *out = csel + x * gc.ksel;
   uint8_t *oq = cq + x * gc.ksel;
-  if (first && pos < gc.ksel) {
+  if (first && pos < gc.ksel - gc.band) {
     out[pos] = tc;
     oq[pos] = (uint8_t)acc;
   }
   if (lane >= n && lane < gc.ksel) {
-    out[lane] = -1;
+    out[lane] = (gc.band && band_ok && lane == gc.ksel - 1) ? -2 : -1;
     oq[lane] = 0;
   }
+  if (gc.band && lane == 0) bflag[x] = band_ok ? 1 : 0;
 }
 
 hipError_t launch_coarsen(const Geom &g, const Geom &gc, const int32_t *sel, int32_t *csel, uint8_t *cq,
-                          hipStream_t s) {
+                          uint8_t *bflag, hipStream_t s) {
   const int64_t nrows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_coarsen", s);
-  hipLaunchKernelGGL(coarsen_kernel, dim3((unsigned)((nrows + 3) / 4)), dim3(256), 0, s, sel, g, gc, csel, cq);
+  hipLaunchKernelGGL(coarsen_kernel, dim3((unsigned)((nrows + 3) / 4)), dim3(256), 0, s, sel, g, gc, csel, cq, bflag);
   timing_end(s);
   return hipGetLastError();
 }

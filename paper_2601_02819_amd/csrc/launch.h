@@ -17,6 +17,8 @@ struct Geom {
   float scale;        // softmax scale
   int dtype;          // 0 bf16, 1 fp32
   int sel_mode;       // group aggregation of block scores: 0 summed logits, 1 summed per-head softmax
+  int sm;             // block size of the selection (m of a tile geometry is 64; n_init, window keep sm units)
+  int band;           // 1: the local window of every row holding it whole is attended by the band kernels
 };
 
 // Index (inverted selection) workspace, carved out of the caller's buffer.
@@ -34,6 +36,9 @@ struct IndexWs {
   int32_t *pmap;      // [B*Hkv*Lq*Ksel] list position of each valid (row, slot); partials are
                       //                 stored in list order and the merges gather through this map
   int2 *units;        // [units_max]    (b*Hkv*T + g*T + t, first list entry)
+  int64_t band_base;  // list position of the band partial of row (b, g, i): band_base + (b*Hkv + g)*Lq + i
+  int64_t discard;    // partial row that absorbs stores past a chunk's end (after the list and band rows)
+  const uint8_t *bflag;  // [B*Hkv*Lq] 1: the row's local window is in the band (NULL: no band)
 };
 
 constexpr int kIndexTile = 256;  // query rows per index-building workgroup
@@ -52,16 +57,24 @@ hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t 
 // attends to, NULL = all four (64-token blocks)
 hipError_t launch_build_index(const Geom &g, const int32_t *sel, const uint8_t *quarters, const IndexWs &ix,
                               hipStream_t s);
-// m-token blocks (m = 16, 32) -> 64-key tiles with quarter masks; gc = tile geometry
+// m-token blocks -> 64-key tiles with quarter masks; gc = tile geometry.  With
+// gc.band the local windows of rows that hold them whole are left out (bflag = 1)
 hipError_t launch_coarsen(const Geom &g, const Geom &gc, const int32_t *sel, int32_t *csel, uint8_t *cq,
-                          hipStream_t s);
+                          uint8_t *bflag, hipStream_t s);
 hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel,
                            const uint8_t *quarters, void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml,
                            hipStream_t s);
+// bkv: with g.band, float32 [B*Hkv*T][2][64][d] for the band's dK, dV per 64-key tile
 hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
                            const void *dO, const float *LSE, const int32_t *sel, const uint8_t *quarters, void *dQ,
                            void *dK, void *dV, const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart,
-                           bool reuse_index, hipStream_t s);
+                           float *bkv, bool reuse_index, hipStream_t s);
+// band kernels (attn_band.hip): local windows as dense query-major / key-major attention
+hipError_t launch_fwd_band(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
+                           void *opart, float2 *ml, hipStream_t s);
+hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                           const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
+                           hipStream_t s);
 hipError_t launch_bwd_pre(const Geom &g, const void *O, const void *dO, float *Dvec, hipStream_t s);
 hipError_t launch_attn_fwd_fp32(const Geom &g, const float *Q, const float *K, const float *V,
                                 const int32_t *sel, float *O, float *LSE, hipStream_t s);
