@@ -53,8 +53,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
-  const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
-  const int i0 = blockIdx.x * TOK, i1 = min(i0 + TOK, gm.Lq) - 1;
+  // query tiles of one XCD are consecutive (they share most key tiles)
+  const int item = xcd_item(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
+  const int qt = item % gridDim.x, bg = item / gridDim.x, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
+  const int i0 = qt * TOK, i1 = min(i0 + TOK, gm.Lq) - 1;
   const uint8_t *bf = ix.bflag + (int64_t)bg * gm.Lq;
 
   // the rows of this lane: chunk c, MFMA row (wave RT + c) 16 + l16
@@ -76,6 +78,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
   }
   if (!__syncthreads_or(ok[0] || ok[RT - 1])) return;
   const int kt_lo = band_first_key(gm, gm.q_pos0 + i0) / 64, kt_hi = (gm.q_pos0 + i1) / 64;
+  const int a_last = band_first_key(gm, gm.q_pos0 + i1), pos_first = gm.q_pos0 + i0;
 
   const float sl2 = gm.scale * kLog2e;
   float mrun[RT], lrun[RT];
@@ -89,8 +92,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
   }
   // each tile's loads are issued before the barrier that waits for the previous
   // tile's use; the other workgroup on the CU covers the rest of their latency
-  for (int kt = kt_lo; kt <= kt_hi; ++kt) {
-    u32x4 kr[NV], vr[NV];
+  // tile kt + 1 is loaded into registers while tile kt is used (the last tile
+  // is loaded twice: a fixed load sequence per iteration)
+  u32x4 kr[NV], vr[NV];
+  auto load_tile = [&](int kt) {
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int x = tid + 256 * v, kk = x / VPR, c8 = (x % VPR) * 8;
@@ -98,6 +103,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
       kr[v] = *reinterpret_cast<const u32x4 *>(K + src);
       vr[v] = *reinterpret_cast<const u32x4 *>(V + src);
     }
+  };
+  load_tile(kt_lo);
+  for (int kt = kt_lo; kt <= kt_hi; ++kt) {
     lds_barrier();
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
@@ -106,6 +114,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
       *reinterpret_cast<u32x4 *>(&Vs[kk * VP + c8]) = vr[v];
     }
     lds_barrier();
+    load_tile(min(kt + 1, kt_hi));
     const int key0 = kt * 64;
     // S^T = K Q^T for both chunks (every K fragment read from LDS feeds both)
     f32x4 sa[RT][4];
@@ -121,43 +130,56 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 #pragma unroll
         for (int c = 0; c < RT; ++c) sa[c][j] = mfma16x16x32(kfr, qf[c][kb], sa[c][j]);
       }
+    // Tiles inside every row's band (all but the first and last one or two)
+    // need no mask: rows outside the band compute values that are discarded.
+    const bool interior = key0 >= a_last && key0 + 63 <= pos_first;
     bf16x8 pb[RT][2];
     float fs[RT];
 #pragma unroll
     for (int c = 0; c < RT; ++c) {
       f32x4 (&st)[4] = sa[c];
+      if (!interior) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = key0 + j * 16 + q4 * 4 + r;
+            st[j][r] = (ok[c] && key >= a0[c] && key <= pos[c]) ? st[j][r] : -INFINITY;
+          }
+      }
       float mx = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int key = key0 + j * 16 + q4 * 4 + r;
-          const float v = (ok[c] && key >= a0[c] && key <= pos[c]) ? st[j][r] * sl2 : -INFINITY;
-          st[j][r] = v;
-          mx = fmaxf(mx, v);
-        }
+      for (int j = 0; j < 4; ++j) mx = fmaxf(fmaxf(mx, fmaxf(st[j][0], st[j][1])), fmaxf(st[j][2], st[j][3]));
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = fmaxf(mrun[c], mx);
-      const float mref = mn == -INFINITY ? 0.f : mn;    // no key of the row yet: every weight is 0
-      const float f = exp2f(mrun[c] - mref);            // 0 while the running sum is still empty
+      mx *= sl2;
+      // The reference maximum moves only when some row's maximum rises by more
+      // than 2^8 (or is first set): weights stay below 2^8, far inside bf16
+      // and float32, and most tiles skip the rescaling of O and l.
+      float f = 1.f;
+      if (__any(mx > mrun[c] + 8.f)) {
+        const float mn = fmaxf(mrun[c], mx);
+        f = mn == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(mrun[c] - mn);  // 0 when the row had no key yet
+        mrun[c] = mn;
+      }
+      const float mref = mrun[c] == -INFINITY ? 0.f : mrun[c];  // no key of the row yet: every weight is 0
       float l = 0.f;
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = exp2f(st[j][r] - mref);
+          const float p = __builtin_amdgcn_exp2f(fmaf(st[j][r], sl2, -mref));
           st[j][r] = p;
           l += p;
         }
       l += __shfl_xor(l, 16, 64);
       l += __shfl_xor(l, 32, 64);
       lrun[c] = lrun[c] * f + l;
-      mrun[c] = mn;
       fs[c] = f;
       pb[c][0] = pack_bf16x8(st[0], st[1]);
       pb[c][1] = pack_bf16x8(st[2], st[3]);
     }
+    const bool rescale = __any(fs[0] != 1.f || fs[RT - 1] != 1.f);
     // O^T = O^T f + V^T P^T for both chunks (every V^T fragment feeds both)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -165,7 +187,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
       const bf16x8 v1 = lds_col8(Vs, VP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16);
 #pragma unroll
       for (int c = 0; c < RT; ++c) {
-        o[c][nt] *= fs[c];
+        if (rescale) o[c][nt] *= fs[c];
         o[c][nt] = mfma16x16x32(v0, pb[c][0], o[c][nt]);
         o[c][nt] = mfma16x16x32(v1, pb[c][1], o[c][nt]);
       }
@@ -218,8 +240,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
-  const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
-  const int i0 = blockIdx.x * TOK, i1 = min(i0 + TOK, gm.Lq) - 1;
+  // query tiles of one XCD are consecutive (they share most key tiles)
+  const int item = xcd_item(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
+  const int qt = item % gridDim.x, bg = item / gridDim.x, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
+  const int i0 = qt * TOK, i1 = min(i0 + TOK, gm.Lq) - 1;
   const uint8_t *bf = ix.bflag + (int64_t)bg * gm.Lq;
 
   int pos[RT], a0[RT];
@@ -245,6 +269,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
   }
   if (!__syncthreads_or(ok[0])) return;
   const int kt_lo = band_first_key(gm, gm.q_pos0 + i0) / 64, kt_hi = (gm.q_pos0 + i1) / 64;
+  const int a_last = band_first_key(gm, gm.q_pos0 + i1), pos_first = gm.q_pos0 + i0;
 
   const float sl2 = gm.scale * kLog2e;
   f32x4 dq[RT][NT];
@@ -254,8 +279,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
     for (int nt = 0; nt < NT; ++nt) dq[c][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   // each tile's loads are issued before the barrier that waits for the previous
   // tile's use; the other workgroup on the CU covers the rest of their latency
-  for (int kt = kt_lo; kt <= kt_hi; ++kt) {
-    u32x4 kr[NV], vr[NV];
+  // tile kt + 1 is loaded into registers while tile kt is used (the last tile
+  // is loaded twice: a fixed load sequence per iteration)
+  u32x4 kr[NV], vr[NV];
+  auto load_tile = [&](int kt) {
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int x = tid + 256 * v, kk = x / VPR, c8 = (x % VPR) * 8;
@@ -263,6 +290,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
       kr[v] = *reinterpret_cast<const u32x4 *>(K + src);
       vr[v] = *reinterpret_cast<const u32x4 *>(V + src);
     }
+  };
+  load_tile(kt_lo);
+  for (int kt = kt_lo; kt <= kt_hi; ++kt) {
     lds_barrier();
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
@@ -271,7 +301,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
       *reinterpret_cast<u32x4 *>(&Vs[kk * KP + c8]) = vr[v];
     }
     lds_barrier();
+    load_tile(min(kt + 1, kt_hi));
     const int key0 = kt * 64;
+    const bool interior = key0 >= a_last && key0 + 63 <= pos_first;
 #pragma unroll
     for (int c = 0; c < RT; ++c) {
       // S^T = K Q^T and dP^T = V dO^T: lane (q, j) holds keys 16 jt + 4 q + r of row j
@@ -285,12 +317,15 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
           st[j] = mfma16x16x32(load_bf16x8(&Ks[(j * 16 + l16) * KP + kb * 32 + kq]), qf[c][kb], st[j]);
           dp[j] = mfma16x16x32(load_bf16x8(&Vs[(j * 16 + l16) * KP + kb * 32 + kq]), df[c][kb], dp[j]);
         }
+      // interior tiles (inside every row's band) need no mask: rows outside
+      // the band compute values that are discarded
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int key = key0 + j * 16 + q4 * 4 + r;
-          const float p = (ok[c] && key >= a0[c] && key <= pos[c]) ? exp2f(st[j][r] * sl2 - lse2[c]) : 0.f;
+          const bool in = interior || (ok[c] && key >= a0[c] && key <= pos[c]);
+          const float p = in ? __builtin_amdgcn_exp2f(fmaf(st[j][r], sl2, -lse2[c])) : 0.f;
           dp[j][r] = p * (dp[j][r] - dd[c]);
         }
       // dQ^T += K^T dS^T
@@ -353,7 +388,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
-  const int kt = blockIdx.x, bg = blockIdx.y, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
+  // key tiles of one XCD are consecutive (they share most rows)
+  const int item = xcd_item(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
+  const int kt = item % gridDim.x, bg = item / gridDim.x, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   const uint8_t *bf = ix.bflag + (int64_t)bg * gm.Lq;
   const int key0 = kt * 64;
   // rows: from the first token that sees key0 to the last whose band starts by key0 + 63
@@ -374,11 +411,14 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
 
   const float sl2 = gm.scale * kLog2e;
   const int key = key0 + wave * 16 + l16;  // the key whose S column this lane holds
-  for (int c0 = r_lo; c0 <= r_hi; c0 += CT) {
-    // the chunk's rows (token c0 + r / G, head r % G; tokens past r_hi repeat the
-    // last one and are masked) and, for thread r < 64, that row's LSE, D,
-    // position (-1: not in the band) and band start; loaded before the barrier
-    u32x4 pq[NV], pd[NV];
+  // the chunk's rows (token c0 + r / G, head r % G; tokens past r_hi repeat the
+  // last one and are masked) and, for thread r < 64, that row's LSE, D,
+  // position (-1: not in the band) and band start.  Chunk c0 + CT is loaded
+  // into registers while chunk c0 is used.
+  u32x4 pq[NV], pd[NV];
+  float plse = 0.f, pdd = 0.f;
+  int ppos = -1, pa = 0;
+  auto load_rows = [&](int c0) {
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int x = tid + 256 * v, r = x / VPR, c8 = (x % VPR) * 8;
@@ -387,8 +427,6 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       pq[v] = *reinterpret_cast<const u32x4 *>(Q + src);
       pd[v] = *reinterpret_cast<const u32x4 *>(dO + src);
     }
-    float plse = 0.f, pdd = 0.f;
-    int ppos = -1, pa = 0;
     if (tid < 64) {
       const int tok = c0 + tid / G, h = g * G + tid % G;
       const int ti = min(tok, r_hi);
@@ -397,6 +435,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       ppos = (tok <= r_hi && bf[ti] != 0) ? gm.q_pos0 + ti : -1;
       pa = band_first_key(gm, gm.q_pos0 + ti);
     }
+  };
+  if (r_lo <= r_hi) load_rows(r_lo);
+  for (int c0 = r_lo; c0 <= r_hi; c0 += CT) {
     lds_barrier();
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
@@ -411,6 +452,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       a_s[tid] = pa;
     }
     lds_barrier();
+    load_rows(min(c0 + CT, r_hi));
 
     // S and dP: 64 rows (4 tiles) x this wave's 16 keys; lane (q, j) holds rows 16 mt + 4 q + r of key j
     f32x4 s[4], dp[4];
@@ -439,7 +481,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       const int av[4] = {a4.x, a4.y, a4.z, a4.w};
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = (key <= posv[r] && key >= av[r]) ? exp2f(s[mt][r] * sl2 - lsev[r]) : 0.f;
+        const float p = (key <= posv[r] && key >= av[r]) ? __builtin_amdgcn_exp2f(fmaf(s[mt][r], sl2, -lsev[r])) : 0.f;
         s[mt][r] = p;
         dp[mt][r] = p * (dp[mt][r] - ddv[r]);
       }

@@ -21,12 +21,8 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t x) {
   return __uint_as_float(static_cast<uint32_t>(x) << 16);
 }
 
-// float -> bfloat16, round to nearest even (inputs here are finite).
-__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return static_cast<bf16_t>(u >> 16);
-}
+// float -> bfloat16, round to nearest even (the gfx950 conversion instruction).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
 template <typename T> __device__ __forceinline__ float to_f32(T x);
 template <> __device__ __forceinline__ float to_f32<float>(float x) { return x; }
@@ -126,6 +122,17 @@ struct RowSlots {
   }
 };
 
+// The dispatcher hands workgroups to the 8 XCDs (each with its own L2) in
+// turn by linear id.  Returns the work item of linear id `lin` (of n) such that
+// each XCD takes one contiguous run of items: neighbouring items, which read
+// the same tiles, then share an L2.  A bijection of 0..n-1.
+__device__ __forceinline__ int xcd_item(int lin, int n) {
+  const int x = lin & 7, j = lin >> 3;
+  int off = 0;
+  for (int y = 0; y < x; ++y) off += (n - y + 7) >> 3;  // items of the XCDs before
+  return off + j;
+}
+
 // Workgroup barrier that orders LDS accesses only.  __syncthreads() also
 // fences global and private memory, and values held in registers across it
 // (loads issued before the barrier, stored to LDS after it) can then be sent
@@ -145,12 +152,12 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Packs two 4-element float groups into a bf16 MFMA operand (elements 0..3, then 4..7).
+// Packs two 4-element float groups into a bf16 MFMA operand (elements 0..3,
+// then 4..7), rounding to nearest even with the packed conversion instruction.
+typedef float f32x8 __attribute__((ext_vector_type(8)));
 __device__ __forceinline__ bf16x8 pack_bf16x8(const f32x4 &a, const f32x4 &b) {
-  const v8i16 c = {(short)f32_to_bf16(a[0]), (short)f32_to_bf16(a[1]), (short)f32_to_bf16(a[2]),
-                   (short)f32_to_bf16(a[3]), (short)f32_to_bf16(b[0]), (short)f32_to_bf16(b[1]),
-                   (short)f32_to_bf16(b[2]), (short)f32_to_bf16(b[3])};
-  return __builtin_bit_cast(bf16x8, c);
+  const f32x8 c = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return __builtin_convertvector(c, bf16x8);
 }
 
 }  // namespace phsa
