@@ -216,7 +216,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       for (int r = 0; r < 4; ++r) {
         // the wave's 16 keys are quarter `wave` of the block
         const bool ok = ((posv[r] >> (27 + wave)) & 1) && key <= (posv[r] & 0x7ffffff);
-        const float p = ok ? exp2f(s[mt][r] * sl2 - lsev[r]) : 0.f;
+        const float p = ok ? __builtin_amdgcn_exp2f(fmaf(s[mt][r], sl2, -lsev[r])) : 0.f;
         const float ds = p * (dp[mt][r] - ddv[r]);
         s[mt][r] = p;
         dp[mt][r] = ds;

@@ -131,7 +131,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = exp2f(st[kt][r] - mx);
+        const float p = __builtin_amdgcn_exp2f(st[kt][r] - mx);
         st[kt][r] = p;
         l += p;
       }
@@ -230,7 +230,7 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
       for (int k = 0; k < U; ++k) {
         if (q[k].x == -INFINITY) continue;
         const float mn = fmaxf(M, q[k].x);
-        const float sc = exp2f(M - mn), w = exp2f(q[k].x - mn);
+        const float sc = __builtin_amdgcn_exp2f(M - mn), w = __builtin_amdgcn_exp2f(q[k].x - mn);
         L = fmaf(w, q[k].y, L * sc);
         const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw[k]);
 #pragma unroll

@@ -133,6 +133,10 @@ __device__ __forceinline__ int xcd_item(int lin, int n) {
   return off + j;
 }
 
+// The exponentials of the softmax weights use the hardware 2^x instruction
+// (__builtin_amdgcn_exp2f): its arguments are <= 0 or a bounded offset, and it
+// flushes results below 2^-126, which are negligible against a sum >= 1.
+
 // Workgroup barrier that orders LDS accesses only.  __syncthreads() also
 // fences global and private memory, and values held in registers across it
 // (loads issued before the barrier, stored to LDS after it) can then be sent
