@@ -238,7 +238,7 @@ __global__ __launch_bounds__(512) void decode_select_kernel(const T *__restrict_
 // by shuffles.  Each wave keeps a running (m, l, o) per head (log2 units);
 // the four are merged through LDS and O, LSE written directly.
 template <typename T, int D, int G>
-__global__ __launch_bounds__(256, 2) void decode_attn_kernel(const T *__restrict__ Q, const T *__restrict__ K,
+__global__ __launch_bounds__(256, G >= 8 ? 1 : 2) void decode_attn_kernel(const T *__restrict__ Q, const T *__restrict__ K,
                                                           const T *__restrict__ V, const int32_t *__restrict__ clen,
                                                           const int32_t *__restrict__ sel, T *__restrict__ O,
                                                           float *__restrict__ LSE, Geom gm) {
@@ -274,13 +274,13 @@ __global__ __launch_bounds__(256, 2) void decode_attn_kernel(const T *__restrict
     const int t = sel[(int64_t)bg * gm.ksel + s];
     if (t < 0 || t > cur || t >= gm.T) continue;  // wave-uniform
     for (int k0 = 0; k0 < gm.m; k0 += KG) {
-      uint4 kr[NI], vr[NI];
+      u32x4 kr[NI], vr[NI];  // native vectors: uint4 arrays here would live in scratch
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int key = min(k0 + i * KPI + sub, gm.m - 1);  // rows past a short block are masked below
         const int64_t src = (((int64_t)b * gm.Lk + (int64_t)t * gm.m + key) * gm.Hkv + g) * D + ch * VEC;
-        kr[i] = *reinterpret_cast<const uint4 *>(K + src);
-        vr[i] = *reinterpret_cast<const uint4 *>(V + src);
+        kr[i] = *reinterpret_cast<const u32x4 *>(K + src);
+        vr[i] = *reinterpret_cast<const u32x4 *>(V + src);
       }
 #pragma unroll
       for (int h = 0; h < G; ++h) {

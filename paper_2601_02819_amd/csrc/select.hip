@@ -752,25 +752,29 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
 #pragma unroll
     for (int j = 0; j < RT; ++j) {
       const int ia = i0 + wave * 16 * RT + j * 16 + l16;
-      uint4 raw[G][KB];
-#pragma unroll
-      for (int hh = 0; hh < G; ++hh)
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-          raw[hh][kb] = ia < gm.Lq ? *reinterpret_cast<const uint4 *>(
-                                         Q + (((int64_t)b * gm.Lq + ia) * gm.Hq + g * G + hh) * D + kb * 32 + kq)
-                                   : make_uint4(0u, 0u, 0u, 0u);
       float ss = 0.f;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
+        // this feature slice summed over the G heads, HU heads' loads in flight at
+        // a time (all of them at once would not fit in registers for G = 8)
+        constexpr int HU = G < 4 ? G : 4;
         float qs[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) qs[e] = 0.f;
+#pragma unroll 1
+        for (int h0 = 0; h0 < G; h0 += HU) {
+          u32x4 raw[HU];
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh) {
-          const bf16_t *v = reinterpret_cast<const bf16_t *>(&raw[hh][kb]);
+          for (int hh = 0; hh < HU; ++hh)
+            raw[hh] = ia < gm.Lq ? *reinterpret_cast<const u32x4 *>(
+                                       Q + (((int64_t)b * gm.Lq + ia) * gm.Hq + g * G + h0 + hh) * D + kb * 32 + kq)
+                                 : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-          for (int e = 0; e < 8; ++e) qs[e] += bf16_to_f32(v[e]);
+          for (int hh = 0; hh < HU; ++hh) {
+            const bf16_t *v = reinterpret_cast<const bf16_t *>(&raw[hh]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) qs[e] += bf16_to_f32(v[e]);
+          }
         }
         bf16_t hi[8], lo[8];
 #pragma unroll
