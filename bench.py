@@ -135,6 +135,22 @@ def selected_tiles(sel: torch.Tensor, seqlen_k: int, block: int) -> int:
     return int(valid.sum().item() - same.sum().item())
 
 
+def band_blocks(sel: torch.Tensor, seqlen_k: int, block: int, n_init: int, window: int):
+    """Per (b, g, query row): how many of its selected blocks the band kernels
+    take (bf16 attention with a window of at least 64 keys).  A row whose
+    selection holds every local block outside the init blocks, A .. cur with
+    A = max(cur - window / block, min(n_init, cur + 1)), leaves those blocks to
+    the band; other rows keep all their blocks in the sparse kernels.  Returns
+    the counts and A per row."""
+    Lq = sel.shape[2]
+    cur = ((seqlen_k - Lq + torch.arange(Lq, device=sel.device)) // block).view(1, 1, Lq)
+    a = torch.maximum((cur - window // block).clamp(min=0), torch.clamp(cur + 1, max=n_init))
+    valid = (sel >= 0) & (sel <= cur.unsqueeze(-1))
+    have = (valid & (sel >= a.unsqueeze(-1))).sum(-1)
+    ok = (a <= cur) & (have == cur - a + 1)
+    return torch.where(ok, cur - a + 1, torch.zeros_like(cur)), a
+
+
 def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
     wl = WORKLOADS[name]
     cfg = cfg_of(wl)
@@ -156,7 +172,15 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
         sel = step()
     torch.cuda.synchronize()
     nsel = selected_blocks(sel, L, m)
-    ntile = selected_tiles(sel, L, m)
+    band = wl.window >= 64 and min(wl.ksel, L // 64) <= 63  # the library's rule for bf16 attention
+    if band:
+        nb, a = band_blocks(sel, L, m, wl.n_init_blocks, wl.window)
+        # the band rows' local blocks are the top of their ascending lists
+        sparse_sel = torch.where((nb > 0).unsqueeze(-1) & (sel >= a.unsqueeze(-1)), torch.full_like(sel, -1), sel)
+        nband = int(nb.sum().item())
+    else:
+        sparse_sel, nband = sel, 0
+    ntile = selected_tiles(sparse_sel, L, m)  # the sparse kernels' tiles
     phsa.timing_reset()
     phsa.timing_enable(True)
     torch.cuda.synchronize()
@@ -172,6 +196,9 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
 
     fwd_flop = 4.0 * d * m * nsel * G
     bwd_flop = 2.5 * fwd_flop
+    # the local windows' share, attended by the band kernels (same convention)
+    band_fwd_flop = 4.0 * d * m * nband * G
+    sparse_fwd_flop = fwd_flop - band_fwd_flop
     # MFMA work the kernels execute: whole 64-key tiles (blocks below 64 tokens
     # share tiles, the unselected quarters of a tile are masked)
     tile_fwd_flop = 4.0 * d * 64 * ntile * G
@@ -188,8 +215,15 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
                     "phsa_attn_bwd_sparse": ntile * (3 * pair_row + G * 8 + 4) + kv_bytes + B * L * Hkv * d * 2 * 2}
     bytes_compress = B * L * Hkv * d * 2 + B * L + B * Hkv * T * d * 4
     bytes_select = B * L * Hq * d * 2 + B * Hkv * T * d * 4 + B * Hkv * L * wl.ksel * 4
-    work = {"phsa_attn_fwd_sparse": ("TFLOP/s", fwd_flop / 1e12), "phsa_attn_bwd_sparse": ("TFLOP/s", bwd_flop / 1e12),
+    # each attention kernel is credited with the selected-block FLOPs it covers;
+    # the band's backward is split as executed: dK/dV 8 d, dQ 6 d per (row, head, key)
+    work = {"phsa_attn_fwd_sparse": ("TFLOP/s", sparse_fwd_flop / 1e12),
+            "phsa_attn_bwd_sparse": ("TFLOP/s", 2.5 * sparse_fwd_flop / 1e12),
             "phsa_compress": ("GB/s", bytes_compress / 1e9), "phsa_select": ("GB/s", bytes_select / 1e9)}
+    if nband:
+        work.update({"phsa_attn_fwd_band": ("TFLOP/s", band_fwd_flop / 1e12),
+                     "phsa_attn_bwd_band_dkv": ("TFLOP/s", 2.0 * band_fwd_flop / 1e12),
+                     "phsa_attn_bwd_band_dq": ("TFLOP/s", 1.5 * band_fwd_flop / 1e12)})
     for n, (unit, amount) in work.items():
         if n in ks:
             rate = amount / (ks[n]["avg_ms"] / 1e3)
@@ -198,7 +232,7 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
             if n in design_bytes:
                 # attainable = min(MFMA peak, intensity x HBM peak) for this schedule's
                 # traffic and executed tile work, in selected-block FLOP/s
-                flop = fwd_flop if "fwd" in n else bwd_flop
+                flop = work[n][1] * 1e12
                 exec_flop = tile_fwd_flop * (1.0 if "fwd" in n else 2.5)
                 t_min = max(exec_flop / (PEAK_BF16_TFLOPS * 1e12), design_bytes[n] / (PEAK_HBM_GBS * 1e9))
                 att = flop / 1e12 / t_min
@@ -209,7 +243,8 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
     return {
         "ms_per_step": ms_step,
         "value": (fwd_flop + bwd_flop) / 1e12 / (ms_step / 1e3),
-        "fwd_flop": fwd_flop, "bwd_flop": bwd_flop, "selected_blocks": nsel, "selected_tiles": ntile,
+        "fwd_flop": fwd_flop, "bwd_flop": bwd_flop, "selected_blocks": nsel, "band_blocks": nband,
+        "sparse_tiles": ntile,
         "tile_fwd_flop": tile_fwd_flop,
         # the paper's convention: active tokens of the last query over the sequence length
         "sparsity_last_query": 1.0 - wl.ksel * m / L,

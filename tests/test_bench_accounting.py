@@ -1,0 +1,49 @@
+"""The benchmark's split of selected blocks between the band and sparse kernels."""
+import os
+import sys
+
+import torch
+
+sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+import bench  # noqa: E402
+
+
+def _sel(rows, ksel):
+    out = torch.full((1, 1, len(rows), ksel), -1, dtype=torch.int32)
+    for i, r in enumerate(rows):
+        out[0, 0, i, :len(r)] = torch.tensor(sorted(r), dtype=torch.int32)
+    return out
+
+
+def test_band_blocks_whole_and_holed_windows():
+    # m = 16, 2 init blocks, 64-token window (4 blocks); each row is the last
+    # query of a sequence of pos + 1 keys
+    m, n_init, w = 16, 2, 64
+    rows = [
+        [0],                    # pos 0: cur 0, A = max(0 - 4, min(2, 1)) = 1 > cur: no band
+        [0, 1],                 # pos 16 (cur 1): A = min(2, 2) = 2 > cur: no band
+        [0, 1, 2, 3, 4, 5, 6],  # pos 100 (cur 6): A = max(2, 2) = 2, local 2..6 whole: 5 band blocks
+        [0, 1, 2, 4, 5, 6],     # hole at 3: no band
+        [0, 1, 2, 3, 4, 5, 6, 9],  # block 9 past cur is not valid; local whole: 5
+    ]
+    pos = [0, 16, 100, 100, 100]
+    want = [0, 0, 5, 0, 5]
+    for r, p, wv in zip(rows, pos, want):
+        nb, a = bench.band_blocks(_sel([r], 8), p + 1, m, n_init, w)
+        assert int(nb.item()) == wv, (r, p)
+        cur = p // m
+        assert int(a.item()) == max(max(0, cur - w // m), min(n_init, cur + 1))
+
+
+def test_sparse_tiles_exclude_band_blocks():
+    # m = 16: four blocks per 64-key tile
+    m, n_init, w = 16, 1, 64
+    row = [0, 5, 6, 7, 8, 9, 10]  # pos 170 (cur 10): A = 6, local 6..10 whole
+    sel = _sel([row], 8)
+    Lk = 171
+    nb, a = bench.band_blocks(sel, Lk, m, n_init, w)
+    assert int(nb.item()) == 5
+    sparse = torch.where((nb > 0).unsqueeze(-1) & (sel >= a.unsqueeze(-1)), torch.full_like(sel, -1), sel)
+    # blocks 0 and 5 remain: tiles 0 and 1
+    assert bench.selected_tiles(sparse, Lk, m) == 2
+    assert bench.selected_tiles(sel, Lk, m) == 3  # tiles 0, 1, 2 with the window
