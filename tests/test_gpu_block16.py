@@ -201,3 +201,50 @@ def test_scattered_selection_many_tiles():
     dq_r, dk_r, dv_r = oracle.attn_bwd(qh, kh, vh, doh, sel, m, scale)
     errs = (rel_l2(to_np(dq), dq_r), rel_l2(to_np(dk), dk_r), rel_l2(to_np(dv), dv_r))
     assert max(errs) < GRAD_REL_L2["bf16"], errs
+
+
+@pytest.mark.parametrize("m,n_init,window,top_k", [(16, 8, 512, 16), (64, 1, 128, 8)])
+def test_band_rows_mixed_with_holed_windows(m, n_init, window, top_k):
+    """A given selection where most rows hold their whole local window (the
+    band kernels take it) and every third row misses one local block (all its
+    blocks stay in the sparse kernels), in one call."""
+    B, L, Hq, Hkv, d = 1, 2048, 4, 2, 128
+    cfg = phsa.Config(block_size=m, top_k=top_k, n_init_blocks=n_init, window=window)
+    ks = cfg.ksel
+    log(f"[block16] band/holed rows m={m} init={n_init} w={window} k={top_k}")
+    g = torch.Generator().manual_seed(31)
+    q = torch.randn(B, L, Hq, d, generator=g).to(torch.bfloat16)
+    k = torch.randn(B, L, Hkv, d, generator=g).to(torch.bfloat16)
+    v = torch.randn(B, L, Hkv, d, generator=g).to(torch.bfloat16)
+    do = torch.randn(B, L, Hq, d, generator=g).to(torch.bfloat16)
+    sel = -np.ones((B, Hkv, L, ks), np.int32)
+    rng = np.random.default_rng(6)
+    holed = 0
+    for gg in range(Hkv):
+        for i in range(L):
+            cur = i // m
+            a = max(cur - window // m, min(n_init, cur + 1))
+            row = set(range(min(n_init, cur + 1))) | set(range(a, cur + 1))
+            free = np.arange(n_init, a)
+            if free.size and i % 5 != 2:
+                row |= set(rng.choice(free, size=min(top_k, free.size), replace=False).tolist())
+            if i % 3 == 1 and cur - a >= 1:
+                row.discard(int(rng.integers(a, cur + 1)))
+                holed += 1
+            row = sorted(row)
+            assert len(row) <= ks
+            sel[0, gg, i, :len(row)] = row
+    assert holed > L // 4
+    sel_t = torch.from_numpy(sel).cuda()
+    o, lse = phsa.attn_fwd(q.cuda(), k.cuda(), v.cuda(), sel_t, cfg)
+    dq, dk, dv = phsa.attn_bwd(q.cuda(), k.cuda(), v.cuda(), o, do.cuda(), lse, sel_t, cfg)
+    torch.cuda.synchronize()
+    qh, kh, vh, doh = (x.float().numpy() for x in (q, k, v, do))
+    scale = d ** -0.5
+    o_r, lse_r = oracle.attn_fwd(qh, kh, vh, sel, m, scale)
+    np.testing.assert_allclose(to_np(o), o_r, atol=O_TOL["bf16"], rtol=0)
+    np.testing.assert_allclose(to_np(lse), lse_r, atol=O_TOL["bf16"], rtol=0)
+    dq_r, dk_r, dv_r = oracle.attn_bwd(qh, kh, vh, doh, sel, m, scale)
+    errs = (rel_l2(to_np(dq), dq_r), rel_l2(to_np(dk), dk_r), rel_l2(to_np(dv), dv_r))
+    log(f"[block16] band/holed rows m={m}: grad rel-L2 {errs}")
+    assert max(errs) < GRAD_REL_L2["bf16"], errs
