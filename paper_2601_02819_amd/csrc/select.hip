@@ -454,12 +454,14 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
         bh[nt] = load_bf16x8(&Mh[(nt * 16 + l16) * MP + kb * 32 + kq]);
         bl[nt] = load_bf16x8(&Ml[(nt * 16 + l16) * MP + kb * 32 + kq]);
       }
+      // each chain over the 4 accumulators in turn (consecutive MFMAs independent;
+      // every accumulator still takes hi.hi, hi.lo, lo.hi of each kb in that order)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        acc[nt] = mfma16x16x32(ah[kb], bh[nt], acc[nt]);
-        acc[nt] = mfma16x16x32(ah[kb], bl[nt], acc[nt]);
-        acc[nt] = mfma16x16x32(al[kb], bh[nt], acc[nt]);
-      }
+      for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma16x16x32(ah[kb], bh[nt], acc[nt]);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma16x16x32(ah[kb], bl[nt], acc[nt]);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) acc[nt] = mfma16x16x32(al[kb], bh[nt], acc[nt]);
     }
   };
   // one pass over the chunks of [ta, tb): body(t0, acc) after the scores
@@ -653,8 +655,9 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
 // representative M are split into bf16 hi + lo parts (M once per call, by
 // select_split_kernel).  Three bf16 MFMA chains (hi.hi + hi.lo + lo.hi, float32
 // accumulate) reproduce the float32 dot product to about 2^-17 relative, far
-// inside the 1e-4 score gap the selection is compared at; these are the
-// scores the selection is made on.  Wave w owns two 16-row tiles (rows
+// inside the 1e-4 score gap the selection is compared at.  The selection is
+// made on these sums before the (positive) softmax scale, which orders the
+// blocks the same way.  Wave w owns two 16-row tiles (rows
 // 32w..32w+31 of a 128-row workgroup tile), so every representative fragment
 // read from LDS feeds several MFMAs; representatives stream through LDS in
 // chunks of 64 blocks.  In the accumulator layout lane (q4, l16) holds, per
@@ -668,11 +671,13 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
 //           2^-7 (1 + 2^-8)^2 |q| |M| (each bf16 part is within 2^-8 of its
 //           value; Cauchy-Schwarz), and float32 accumulation of the 3 d terms
 //           adds below 2^-15 of that sum, so s_exact >= s_approx - eps with
-//           eps = 1.024 * 2^-7 |q| |M| scale.  Every lane keeps the best two of these
-//           lower bounds in its stripe for each of its rows.  A row's 32 stripe
-//           tops belong to 32 distinct blocks, so the largest value v with at
-//           least k of them >= v (the bar) lies below the row's k-th best
-//           exact score.
+//           eps = 1.024 * 2^-7 |q| |M|.  One margin per row and chunk of 64
+//           blocks, taken with the largest |M| of the chunk, bounds every
+//           block of the chunk, and every lane keeps the best two of these
+//           lower bounds in its stripe for each of its rows.  A row's 32
+//           stripe tops belong to 32 distinct blocks, so the largest value v
+//           with at least k of them >= v (the bar) lies below the row's k-th
+//           best exact score.
 //   pass 2: the exact scores are computed and those >= bar are appended, in
 //           block order, to the row's LDS list (quarter-wave ballots give the
 //           slots; no atomics).  For random scores about k + 3 pass.  Should a
@@ -730,6 +735,7 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
   constexpr int NL = CH * D / (256 * 8);  // 16-byte loads per thread per tile
   constexpr int PITCH = CAP + 2;          // 8-byte words; keeps a wave's 4 row groups in distinct banks
   constexpr int NJ = (CAP + 15) / 16;
+  static_assert(NJ <= 3, "the final rank count handles at most three 16-entry fragments");
   __shared__ __attribute__((aligned(16))) bf16_t Mh[CH * MP];
   __shared__ __attribute__((aligned(16))) bf16_t Ml[CH * MP];
   __shared__ __attribute__((aligned(16))) float2 cand[ROWS][PITCH];  // (score, block as int bits)
@@ -795,17 +801,19 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
   };
   load_a(false);
   // per row held in the accumulator layout: first local block (candidates lie
-  // below it) and the pass-1 margin factor 2^-6 |q| scale
+  // below it) and the pass-1 margin factor 1.024 * 2^-7 |q|
   int lo_r[NR];
   float eq[NR];
 #pragma unroll
   for (int rr = 0; rr < NR; ++rr) {
     const int i = i0 + crow(rr);
     lo_r[rr] = i < gm.Lq ? max(0, (gm.q_pos0 + i) / gm.m - gm.window / gm.m) : 0;
-    eq[rr] = __shfl(qn[rr >> 2], q4 * 4 + (rr & 3), 64) * gm.scale * 0.008f;
+    eq[rr] = __shfl(qn[rr >> 2], q4 * 4 + (rr & 3), 64) * 0.008f;
   }
   const int last_i = min(i0 + ROWS - 1, gm.Lq - 1);
   const int t_end = k > 0 ? max(0, (gm.q_pos0 + last_i) / gm.m - gm.window / gm.m) : 0;
+  // chunks ending at or below the first row's first local block hold candidates of every row
+  const int lo_first = max(0, (gm.q_pos0 + i0) / gm.m - gm.window / gm.m);
   const bf16_t *mh_bg = Mh_g + (int64_t)bg * gm.T * D;
   const bf16_t *ml_bg = Ml_g + (int64_t)bg * gm.T * D;
   const float *mn_bg = Mnorm_g + (int64_t)bg * gm.T;
@@ -839,7 +847,7 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
     }
   };
 
-  // ---- pass 1: best two lower bounds of each lane's stripe, per row
+  // ---- pass 1: best two approximate scores of each lane's stripe, per row
   float top1[NR], top2[NR];
 #pragma unroll
   for (int rr = 0; rr < NR; ++rr) top1[rr] = top2[rr] = -INFINITY;
@@ -848,9 +856,8 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
     __syncthreads();
     stage(false);
     __syncthreads();
-    float mn[4];
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt) mn[nt] = mnp[nt];
+    // the chunk's largest representative norm, then each row's margin
+    const float mx = max16(fmaxf(fmaxf(mnp[0], mnp[1]), fmaxf(mnp[2], mnp[3])));
     if (t0 + CH < t_end) fetch(t0 + CH, false);
     f32x4 acc[RT][4];
 #pragma unroll
@@ -867,17 +874,25 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
 #pragma unroll
         for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(ah[j][kb], bh[nt], acc[j][nt]);
     }
+    float mg[NR];
 #pragma unroll
-    for (int rr = 0; rr < NR; ++rr)
+    for (int rr = 0; rr < NR; ++rr) mg[rr] = fmaf(eq[rr], mx, 1e-30f);
+    auto keep2 = [&](int rr, float v) {  // best two of the stripe (top1 >= top2)
+      top2[rr] = __builtin_amdgcn_fmed3f(top1[rr], top2[rr], v);  // the middle of the three
+      top1[rr] = fmaxf(top1[rr], v);
+    };
+    if (t0 + CH <= lo_first) {
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const int t = t0 + nt * 16 + l16;
-        const float lb = fmaf(acc[rr >> 2][nt][rr & 3], gm.scale, -fmaf(eq[rr], mn[nt], 1e-30f));
-        const float v = t < lo_r[rr] ? lb : -INFINITY;
-        const bool c1 = v > top1[rr], c2 = v > top2[rr];
-        top2[rr] = c1 ? top1[rr] : (c2 ? v : top2[rr]);
-        top1[rr] = c1 ? v : top1[rr];
-      }
+      for (int rr = 0; rr < NR; ++rr)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) keep2(rr, acc[rr >> 2][nt][rr & 3] - mg[rr]);
+    } else {
+#pragma unroll
+      for (int rr = 0; rr < NR; ++rr)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+          keep2(rr, t0 + nt * 16 + l16 < lo_r[rr] ? acc[rr >> 2][nt][rr & 3] - mg[rr] : -INFINITY);
+    }
   }
 
   // ---- bar of each row: the largest stripe top v with at least k stripe tops >= v
@@ -951,6 +966,7 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
     stage(true);
     __syncthreads();
     if (t0 + CH < t_end) fetch(t0 + CH, true);
+    const bool inner = t0 + CH <= lo_first;
     f32x4 acc[RT][4];
 #pragma unroll
     for (int j = 0; j < RT; ++j)
@@ -964,27 +980,42 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
         bh[nt] = load_bf16x8(&Mh[(nt * 16 + l16) * MP + kb * 32 + kq]);
         bl[nt] = load_bf16x8(&Ml[(nt * 16 + l16) * MP + kb * 32 + kq]);
       }
+      // each chain over all RT x 4 accumulators in turn, so that consecutive
+      // MFMAs are independent; every accumulator still takes hi.hi, hi.lo,
+      // lo.hi of each kb in that order
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-        for (int j = 0; j < RT; ++j) {
-          acc[j][nt] = mfma16x16x32(ah[j][kb], bh[nt], acc[j][nt]);
-          acc[j][nt] = mfma16x16x32(ah[j][kb], bl[nt], acc[j][nt]);
-          acc[j][nt] = mfma16x16x32(al[j][kb], bh[nt], acc[j][nt]);
-        }
+        for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(ah[j][kb], bh[nt], acc[j][nt]);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(ah[j][kb], bl[nt], acc[j][nt]);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(al[j][kb], bh[nt], acc[j][nt]);
     }
+    // appends block t with score sc to row rr's list if it passes; the
+    // quarter-wave's passing lanes take consecutive slots in lane order
+    auto append = [&](int rr, int t, float sc, bool pass_sc, bool pass_t) {
+      const bool pass = pass_sc && pass_t;
+      // ballots of the two compares (lane masks as they are), combined on the scalar unit
+      const uint64_t m = __builtin_amdgcn_ballot_w64(pass_sc) & __builtin_amdgcn_ballot_w64(pass_t) & grp_bits;
+      const int below_m = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+      if (pass) cand[crow(rr)][cnt[rr] + below_m] = make_float2(sc, __int_as_float(t));
+      cnt[rr] += __popcll(m);
+    };
 #pragma unroll
     for (int rr = 0; rr < NR; ++rr) {
-      float2 *rowp = cand[crow(rr)];
+      // in an inner chunk every block is a candidate of every row
+      const int lim = inner ? 0x7fffffff : lo_r[rr];
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
         if (cnt[rr] > CAP - 16) compact(rr);
         const int t = t0 + nt * 16 + l16;
-        const float sc = acc[rr >> 2][nt][rr & 3] * gm.scale;
-        const bool pass = t < lo_r[rr] && sc >= thr[rr];
-        const uint64_t m = __ballot(pass) & grp_bits;
-        if (pass) rowp[cnt[rr] + __popcll(m & below)] = make_float2(sc, __int_as_float(t));
-        cnt[rr] += __popcll(m);
+        const float sc = acc[rr >> 2][nt][rr & 3];
+        append(rr, t, sc, sc >= thr[rr], t < lim);
       }
     }
   }
@@ -1010,11 +1041,15 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
       rk[j] = 0;
     }
     if (n > k) {
+      // fragments j that hold entries in some row of the wave (usually one)
+      const bool two = __ballot(n > 16) != 0, three = __ballot(n > 32) != 0;
       for (int u = 0; u < n; ++u) {
         const float2 e = rowp[u];
         const int tu = __float_as_int(e.y);
+        rk[0] += beats(e.x, tu, ks[0], kt[0]);
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) rk[j] += beats(e.x, tu, ks[j], kt[j]);
+        for (int j = 1; j < NJ; ++j)
+          if (j == 1 ? two : three) rk[j] += beats(e.x, tu, ks[j], kt[j]);
       }
     }
     const int cur = (gm.q_pos0 + i) / gm.m;

@@ -193,10 +193,11 @@ def test_backward_reuses_forward_index():
         assert torch.equal(a, b)
 
 
-def _structured_select(kind: str, top_k: int, L: int = 32768, n_init: int = 1, seed: int = 11):
+def _structured_select(kind: str, top_k: int, L: int = 32768, n_init: int = 1, seed: int = 11, m: int = 64,
+                       window: int = 0):
     """Selection on hand-built representatives: every row's scores follow f(t) (times a
     positive per-row factor), so the right answer is known to be far from rounding."""
-    T, d = L // 64, 128
+    T, d = L // m, 128
     g = torch.Generator().manual_seed(seed)
     q = torch.zeros(1, L, 2, d)
     q[..., 0] = 0.5 + torch.rand(1, L, 2, generator=g)
@@ -214,13 +215,13 @@ def _structured_select(kind: str, top_k: int, L: int = 32768, n_init: int = 1, s
         raise ValueError(kind)
     kc = torch.zeros(1, 1, T, d, dtype=torch.float32)
     kc[..., 0] = f.float()
-    cfg = phsa.Config(block_size=64, top_k=top_k, n_init_blocks=n_init, window=0)
+    cfg = phsa.Config(block_size=m, top_k=top_k, n_init_blocks=n_init, window=window)
     sel = phsa.select(q.cuda(), kc.cuda(), L, cfg).cpu().numpy()
     scale = d ** -0.5
     qh = q.float().numpy()
     kch = kc.double().numpy()
-    ref, kth, gap = oracle.select(qh, kch, 64, top_k, n_init, 0, scale, L)
-    return sel, ref, kth, gap, (lambda idx: oracle.score_row(qh, kch, 64, scale, L, idx[0], idx[2], idx[1]))
+    ref, kth, gap = oracle.select(qh, kch, m, top_k, n_init, window, scale, L)
+    return sel, ref, kth, gap, (lambda idx: oracle.score_row(qh, kch, m, scale, L, idx[0], idx[2], idx[1]))
 
 
 @pytest.mark.parametrize("kind,top_k", [("stripe", 12), ("stripe", 32), ("ascending", 12), ("descending", 20),
@@ -230,6 +231,18 @@ def test_select_structured_scores(kind, top_k):
     candidate lists to be cut), monotone scores, and exact ties (broken by block index)."""
     log(f"[parity] structured selection {kind} k={top_k}")
     sel, ref, kth, gap, score_fn = _structured_select(kind, top_k)
+    if kind == "ties":
+        np.testing.assert_array_equal(sel, ref)
+    else:
+        assert check_sel(sel, ref, kth, gap, score_fn) == 0
+
+
+@pytest.mark.parametrize("kind", ["stripe", "ascending", "ties"])
+def test_select_structured_scores_paper_geometry(kind):
+    """The same orders with 16-token blocks, 8 init blocks, a 512-token window and 16
+    picks over up to T = 2048 blocks (the paper's 32k geometry)."""
+    log(f"[parity] structured selection {kind}, paper geometry")
+    sel, ref, kth, gap, score_fn = _structured_select(kind, 16, n_init=8, m=16, window=512)
     if kind == "ties":
         np.testing.assert_array_equal(sel, ref)
     else:
