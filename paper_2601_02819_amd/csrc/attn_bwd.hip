@@ -270,8 +270,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       for (int k = 0; k < 16 * VPR / 64; ++k) {
         const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
         const int64_t row = r < nrows ? run0 + r : discard;
-        *reinterpret_cast<uint4 *>(dqpart + row * D + cc) =
-            *reinterpret_cast<const uint4 *>(&Qs[(wave * 16 + r) * KPQ + cc]);
+        st_stream16(dqpart + row * D + cc, &Qs[(wave * 16 + r) * KPQ + cc]);
       }
     }
   }

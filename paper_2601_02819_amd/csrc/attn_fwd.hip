@@ -153,7 +153,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
     // so a chunk issues a fixed number of stores and the waits for the
     // prefetched rows need not wait for them.
     const int64_t run0 = list0 + c * TW;  // list position of the chunk's first entry
-    ml[e >= 0 && q4 == 0 ? (run0 + l16 / G) * G + hh : discard] = make_float2(mx, l);
+    st_stream_f2(&ml[e >= 0 && q4 == 0 ? (run0 + l16 / G) * G + hh : discard], mx, l);
     bf16_t *os = Os[wave];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -167,7 +167,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
     for (int k = 0; k < 16 * D / 8 / 64; ++k) {
       const int v = lane + 64 * k, r = v / (D / 8), cc = (v % (D / 8)) * 8;
       const int64_t row = r < nrows ? run0 * G + r : discard;
-      *reinterpret_cast<uint4 *>(opart + row * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
+      st_stream16(opart + row * D + cc, &os[r * SP + cc]);
     }
     wave_lds_sync();
   };

@@ -49,6 +49,17 @@ __device__ __forceinline__ uint4 ld_stream16(const bf16_t *p) {
                     __builtin_nontemporal_load(q + 2), __builtin_nontemporal_load(q + 3));
 }
 
+// Stores of partial results that only a later merge kernel reads: non-temporal,
+// so that they do not displace the gathered rows and key tiles that the
+// writing kernel reuses (16-byte aligned).
+__device__ __forceinline__ void st_stream16(bf16_t *dst, const bf16_t *src_lds) {
+  __builtin_nontemporal_store(*reinterpret_cast<const u32x4 *>(src_lds), reinterpret_cast<u32x4 *>(dst));
+}
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void st_stream_f2(float2 *dst, float a, float b) {  // one 8-byte store
+  __builtin_nontemporal_store(f32x2{a, b}, reinterpret_cast<f32x2 *>(dst));
+}
+
 __device__ __forceinline__ bf16x8 load_bf16x8(const bf16_t *p) {  // 16-byte aligned
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(p));
 }
