@@ -87,7 +87,6 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   __shared__ __attribute__((aligned(16))) float lse_s[64];
   __shared__ __attribute__((aligned(16))) float dd_s[64];
   __shared__ __attribute__((aligned(16))) int pos_s[64];
-  __shared__ int ent_s[64];
 
   const int u = blockIdx.x;
   if (u >= ix.totals[1]) return;
@@ -121,7 +120,6 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   // while the rows of chunk c + 1 are fetched, which is while chunk c computes.
   int ne[NV], nrow = -1;               // list entries of the next chunk to fetch
   uint4 pq[NV], pd[NV];
-  int pe[NV];
   float plse = 0.f, pdd = 0.f;
   int ppos = 0;
   auto load_entries = [&](int c0) {
@@ -138,10 +136,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
-      pe[k] = ne[k];
       pq[k] = pd[k] = make_uint4(0u, 0u, 0u, 0u);
-      if (pe[k] >= 0) {
-        const int64_t src = (((int64_t)b * gm.Lq + (pe[k] >> 10)) * gm.Hq + g * G + r % G) * D + c;
+      if (ne[k] >= 0) {
+        const int64_t src = (((int64_t)b * gm.Lq + (ne[k] >> 10)) * gm.Hq + g * G + r % G) * D + c;
         pq[k] = *reinterpret_cast<const uint4 *>(Q + src);
         pd[k] = *reinterpret_cast<const uint4 *>(dO + src);
       }
@@ -174,7 +171,6 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
       *reinterpret_cast<uint4 *>(&Qs[r * KPQ + c]) = pq[k];
       *reinterpret_cast<uint4 *>(&dOs[r * KPQ + c]) = pd[k];
-      if (c == 0 && r % G == 0) ent_s[r / G] = pe[k];
     }
     if (tid < 64) {
       lse_s[tid] = plse * kLog2e;
