@@ -435,7 +435,7 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the PHSA path shards by (batch, KV head) with no exchange, "
-              "and multi-GPU runs are not part of this build.", file=sys.stderr)
+              "and the library has no multi-GPU mode.", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
