@@ -42,11 +42,21 @@ KERNEL_SYMBOL = {"phsa_attn_bwd_sparse": "attn_bwd_sparse_kernel", "phsa_attn_fw
                  "phsa_attn_fwd_combine": "attn_fwd_combine_kernel", "phsa_attn_bwd_dq_combine": "dq_combine_kernel"}
 
 
+def code_text(src: str) -> str:
+    """Source text without // comments and blank lines (what the compiler sees
+    of a kernel file, up to comment edits)."""
+    import re
+    lines = (re.sub(r"\s*//.*$", "", ln).rstrip() for ln in src.splitlines())
+    return "\n".join(ln for ln in lines if ln)
+
+
 def source_hash(kernel: str) -> str:
+    """Hash of the code a kernel is built from; measured traffic is reported only
+    while it matches the hash stored with the measurement."""
     import hashlib
     h = hashlib.sha256()
     for f in (KERNEL_SOURCE[kernel], "common.h", "launch.h"):
-        h.update(open(os.path.join(CSRC, f), "rb").read())
+        h.update(code_text(open(os.path.join(CSRC, f)).read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -24,7 +24,8 @@
 // come from the row-major tiles through transposing LDS loads, and dS
 // reaches the other waves through one [key][row] LDS tile.  dQ leaves as one
 // bf16 partial per list entry, stored in list order (a unit writes one
-// contiguous run), and a per-row kernel sums a row's partials.  dK/dV leave
+// contiguous run, non-temporal: only the merge reads it), and a per-row
+// kernel sums a row's partials.  dK/dV leave
 // directly (bf16) when the unit covers its whole block, else as float32
 // partials that a per-block kernel sums; blocks nobody selected get zeros
 // from that kernel too.

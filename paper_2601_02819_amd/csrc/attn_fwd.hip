@@ -20,7 +20,9 @@
 // as the P^T operand of the second product, pairing key tiles {4q..4q+3} and
 // {16+4q..16+4q+3}; V_t^T is read with transposing LDS loads over the same
 // key set, so P never goes through LDS.  O^T leaves each lane with 4
-// consecutive features of one row (8-byte stores).
+// consecutive features of one row; a wave stages its 16 rows in LDS and
+// stores them as full 16-byte lanes, with non-temporal stores (only the merge
+// reads them, so they should not displace the rows and tiles the kernel reuses).
 //
 // Blocks of 16 or 32 tokens run on the same 64-key tiles: each list entry
 // carries the mask of the 16-key quarters its row selected, and keys of the
