@@ -124,7 +124,8 @@ def test_decode_block16():
 
 def test_paper_geometry_32k_sampled():
     """One 32k sequence in the paper's geometry (57 blocks of 16 tokens per query):
-    forward and backward on the GPU, the oracle on sampled rows and key blocks."""
+    forward and backward on the GPU; the oracle's selection on every row, its
+    attention on sampled rows and key blocks."""
     wl = WORKLOADS["train_32k_paper"].replace(batch=1)
     log(f"[block16] {wl.name} batch 1: generating inputs")
     cfg = cfg_of(wl)
@@ -146,9 +147,10 @@ def test_paper_geometry_32k_sampled():
     rng = np.random.default_rng(2)
     rows = np.array(sorted(set([0, 15, 16, 130, 527, 528, 529, 600, L // 2, L - 17, L - 16, L - 1]
                                + rng.integers(0, L, 100).tolist())), dtype=np.int64)
-    sel_r, kth, gap = oracle.select(h["q"], kc_ref, m, wl.top_k, wl.n_init_blocks, wl.window, scale, L, rows=rows)
-    exempt = check_sel(sel_g[0][:, rows].transpose(1, 0, 2), sel_r, kth, gap,
-                       lambda idx: oracle.score_row(h["q"], kc_ref, m, scale, L, 0, int(rows[idx[0]]), idx[1]))
+    # every row's selection (T = 2048 blocks per row at the end)
+    sel_r, kth, gap = oracle.select(h["q"], kc_ref, m, wl.top_k, wl.n_init_blocks, wl.window, scale, L)
+    exempt = check_sel(sel_g, sel_r, kth, gap,
+                       lambda idx: oracle.score_row(h["q"], kc_ref, m, scale, L, idx[0], idx[2], idx[1]))
     o_r, lse_r = oracle.attn_fwd(h["q"], h["k"], h["v"], sel_g, m, scale, rows=rows)
     np.testing.assert_allclose(to_np(o)[0, rows], o_r, atol=O_TOL["bf16"], rtol=0)
     np.testing.assert_allclose(to_np(lse)[0][:, rows].T, lse_r, atol=O_TOL["bf16"], rtol=0)
@@ -162,7 +164,7 @@ def test_paper_geometry_32k_sampled():
     dk_g = np.stack([dk_c[0, t * m:(t + 1) * m, g] for g, t in picks])
     dv_g = np.stack([dv_c[0, t * m:(t + 1) * m, g] for g, t in picks])
     e_dk, e_dv = rel_l2(dk_g, dk_r), rel_l2(dv_g, dv_r)
-    log(f"[block16] paper geometry: {rows.size} rows, {exempt} exempt; grad rel-L2 dQ {e_dq:.2e} dK {e_dk:.2e} "
+    log(f"[block16] paper geometry: all selections ({exempt} exempt), {rows.size} rows; grad rel-L2 dQ {e_dq:.2e} dK {e_dk:.2e} "
         f"dV {e_dv:.2e}")
     assert max(e_dq, e_dk, e_dv) < GRAD_REL_L2["bf16"]
 

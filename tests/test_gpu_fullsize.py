@@ -1,6 +1,6 @@
 """GPU parity at the full workload sizes, in the launch configuration the
-benchmark times, on outputs the oracle computes one by one: sampled query rows
-(selection, O, LSE, dQ) and sampled key blocks (dK, dV)."""
+benchmark times: every row's selection, and the outputs the oracle computes
+one by one on sampled query rows (O, LSE, dQ) and sampled key blocks (dK, dV)."""
 import numpy as np
 import pytest
 import torch
@@ -41,6 +41,18 @@ def check_rows(wl, h, kc_ref, sel_g, o, lse, rows):
     log(f"[fullsize] {wl.name}: {rows.size} rows x {Hkv} groups checked, {exempt} exempt")
 
 
+def check_all_selections(wl, h, kc_ref, sel_g):
+    """Every row's selection against the oracle's (index parity with the gap rule)."""
+    scale = wl.head_dim ** -0.5
+    sel_r, kth, gap = oracle.select(h["q"], kc_ref, wl.block_size, wl.top_k, wl.n_init_blocks, wl.window, scale,
+                                    wl.seqlen_k)
+    exempt = check_sel(sel_g, sel_r, kth, gap,
+                       lambda idx: oracle.score_row(h["q"], kc_ref, wl.block_size, scale, wl.seqlen_k, idx[0], idx[2],
+                                                    idx[1]))
+    log(f"[fullsize] {wl.name}: all {sel_g.shape[0] * sel_g.shape[1] * sel_g.shape[2]} selections checked, "
+        f"{exempt} exempt")
+
+
 def test_prefill_32k_sampled():
     wl = WORKLOADS["prefill_32k"]
     log(f"[fullsize] {wl.name}: generating inputs")
@@ -60,6 +72,7 @@ def test_prefill_32k_sampled():
     assert (np.where(valid, sel_g, -1).max(-1) == cur).all()
     assert (np.diff(np.where(valid, sel_g, (1 << 30) + np.arange(wl.ksel)), axis=-1) > 0).all()
     assert (valid.sum(-1) == np.minimum(cur + 1, wl.ksel)).all()
+    check_all_selections(wl, h, kc_ref, sel_g)
     check_rows(wl, h, kc_ref, sel_g, o, lse, sample_rows(1, L, m, 150, 0))
 
 
@@ -79,6 +92,7 @@ def test_train_32k_sampled():
     kc_ref = oracle.compress(h["k"], h["punct"], wl.block_size, wl.lam)
     sel_g = sel.cpu().numpy()
     B, L, m, T = wl.batch, wl.seqlen_q, wl.block_size, wl.n_blocks
+    check_all_selections(wl, h, kc_ref, sel_g)
     rows = sample_rows(B, L, m, 24, 1)
     check_rows(wl, h, kc_ref, sel_g, o, lse, rows)
     scale = wl.head_dim ** -0.5
