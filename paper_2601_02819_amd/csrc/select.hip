@@ -25,6 +25,18 @@ __device__ __forceinline__ bool beats(float s1, int t1, float s2, int t2) {
   return s1 > s2 || (s1 == s2 && t1 < t2);
 }
 
+// The query tile and (b, g) of a workgroup of a (query tiles, B * Hkv) grid,
+// longest first: a tile's causal blocks grow with its index, so the last tiles
+// are dispatched first and the short ones fill in behind them.
+struct TileOrder {
+  int tile, bg;
+  __device__ __forceinline__ TileOrder() {
+    const int lin = blockIdx.x + blockIdx.y * gridDim.x;
+    bg = lin % gridDim.y;
+    tile = gridDim.x - 1 - lin / gridDim.y;
+  }
+};
+
 // Writes one row of sel: the forced init blocks, the npick picks (sorted here
 // into ascending order, in place) and the local blocks, padded with -1.
 __device__ __forceinline__ void emit_row(int32_t *__restrict__ out, int *pk, int npick, int cur, const Geom &gm) {
@@ -105,14 +117,15 @@ __global__ __launch_bounds__(256) void select_kernel(const T *__restrict__ Q, co
   float *kc_s = reinterpret_cast<float *>(smem);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg % gm.Hkv;
-  const int i = blockIdx.x * 64 + lane;
+  const TileOrder wo;
+  const int bg = wo.bg, b = bg / gm.Hkv, g = bg % gm.Hkv;
+  const int i = wo.tile * 64 + lane;
   const bool row_ok = i < gm.Lq;
   const int pos = gm.q_pos0 + (row_ok ? i : gm.Lq - 1);
   const int cur = pos / gm.m;
   const int lo = max(0, cur - gm.window / gm.m);       // first local block
   // candidate blocks of this row: n_init <= t < lo
-  const int last_i = min(blockIdx.x * 64 + 63, gm.Lq - 1);
+  const int last_i = min(wo.tile * 64 + 63, gm.Lq - 1);
   const int t_end = max(0, (gm.q_pos0 + last_i) / gm.m - gm.window / gm.m);  // max lo over the tile
 
   float q[D];
@@ -213,14 +226,15 @@ __global__ __launch_bounds__(256) void select_softmax_kernel(const T *__restrict
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = gm.G, R = 64 / G;                      // rows per workgroup
-  const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg % gm.Hkv;
+  const TileOrder wo;
+  const int bg = wo.bg, b = bg / gm.Hkv, g = bg % gm.Hkv;
   const int hh = lane % G;
-  const int i = blockIdx.x * R + lane / G;
+  const int i = wo.tile * R + lane / G;
   const bool row_ok = i < gm.Lq;
   const int pos = gm.q_pos0 + (row_ok ? i : gm.Lq - 1);
   const int cur = pos / gm.m;
   const int lo = max(0, cur - gm.window / gm.m);
-  const int last_i = min(blockIdx.x * R + R - 1, gm.Lq - 1);
+  const int last_i = min(wo.tile * R + R - 1, gm.Lq - 1);
   const int cur_max = (gm.q_pos0 + last_i) / gm.m;     // normaliser blocks: t < cur
   const int t_end = max(0, cur_max - gm.window / gm.m);  // candidates: n_init <= t < lo
 
@@ -378,8 +392,9 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
-  const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg % gm.Hkv;
-  const int i0 = blockIdx.x * NTOK;
+  const TileOrder wo;
+  const int bg = wo.bg, b = bg / gm.Hkv, g = bg % gm.Hkv;
+  const int i0 = wo.tile * NTOK;
   const int last_i = min(i0 + NTOK - 1, gm.Lq - 1);
   const int cur_max = (gm.q_pos0 + last_i) / gm.m;
   const int t_end = max(0, cur_max - gm.window / gm.m);
@@ -742,8 +757,9 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
-  const int bg = blockIdx.y, b = bg / gm.Hkv, g = bg % gm.Hkv;
-  const int i0 = blockIdx.x * ROWS;
+  const TileOrder wo;
+  const int bg = wo.bg, b = bg / gm.Hkv, g = bg % gm.Hkv;
+  const int i0 = wo.tile * ROWS;
   const int k = gm.top_k;
   const uint64_t grp_bits = 0xffffull << (16 * q4);
   const uint64_t below = (1ull << lane) - 1ull;
