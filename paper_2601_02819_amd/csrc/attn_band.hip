@@ -147,11 +147,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
             st[j][r] = (ok[c] && key >= a0[c] && key <= pos[c]) ? st[j][r] : -INFINITY;
           }
       }
+      // IEEE maximum (v_maximum3_f32): no quieting pass over the accumulators
+      // first; the scores are finite or -inf
       float mx = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) mx = fmaxf(fmaxf(mx, fmaxf(st[j][0], st[j][1])), fmaxf(st[j][2], st[j][3]));
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      for (int j = 0; j < 4; ++j)
+        mx = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mx, st[j][0]),
+                                           __builtin_elementwise_maximum(st[j][1], __builtin_elementwise_maximum(st[j][2], st[j][3])));
+      mx = __builtin_elementwise_maximum(mx, __shfl_xor(mx, 16, 64));
+      mx = __builtin_elementwise_maximum(mx, __shfl_xor(mx, 32, 64));
       mx *= sl2;
       // The reference maximum moves only when some row's maximum rises by more
       // than 2^8 (or is first set): weights stay below 2^8, far inside bf16
