@@ -127,7 +127,7 @@ def kernel_stats(names):
     return out
 
 
-KERNELS = ["phsa_compress", "phsa_select_split", "phsa_select", "phsa_coarsen", "phsa_index_count", "phsa_index_scan_tiles", "phsa_index_scan_lists",
+KERNELS = ["phsa_compress", "phsa_select_split", "phsa_select", "phsa_index_count", "phsa_index_scan_tiles", "phsa_index_scan_lists",
            "phsa_index_fill", "phsa_attn_fwd_sparse", "phsa_attn_fwd_band", "phsa_attn_fwd_combine",
            "phsa_attn_bwd_pre", "phsa_attn_bwd_band_dkv", "phsa_attn_bwd_band_dq", "phsa_attn_bwd_sparse",
            "phsa_attn_bwd_dkv_finalize", "phsa_attn_bwd_dq_combine"]

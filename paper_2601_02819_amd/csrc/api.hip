@@ -75,27 +75,19 @@ Geom tile_geom(const Geom &g) {
 
 struct Coarse {
   Geom gc;            // tile geometry (== g when not coarsened)
-  int32_t *csel;      // [B, Hkv, Lq, gc.ksel] tiles per row, NULL when not coarsened
-  uint8_t *cq;        // [B, Hkv, Lq, gc.ksel] quarter masks
   uint8_t *bflag;     // [B, Hkv, Lq] rows whose local window is in the band (band geometry only)
 };
 
-// The coarsened selection sits at the start of the forward and backward
-// workspaces, followed by the index, so a backward that reuses the forward's
-// index finds it at the same place.
+// The band flags sit at the start of the forward and backward workspaces,
+// followed by the index, so a backward that reuses the forward's index finds
+// them at the same place.  The index builder regroups sel into tiles as it
+// reads it; no regrouped copy is stored.
 size_t coarse_layout(const Geom &g, char *base, Coarse *c) {
-  Coarse w{tile_geom(g), nullptr, nullptr, nullptr};
+  Coarse w{tile_geom(g), nullptr};
   size_t off = 0;
-  if (tiles_coarsened(g)) {
-    const size_t n = (size_t)g.B * g.Hkv * g.Lq * w.gc.ksel;
-    w.csel = base ? reinterpret_cast<int32_t *>(base) : nullptr;
-    off += align_up(n * sizeof(int32_t));
-    w.cq = base ? reinterpret_cast<uint8_t *>(base + off) : nullptr;
-    off += align_up(n);
-    if (w.gc.band) {
-      w.bflag = base ? reinterpret_cast<uint8_t *>(base + off) : nullptr;
-      off += align_up((size_t)g.B * g.Hkv * g.Lq);
-    }
+  if (w.gc.band) {
+    w.bflag = base ? reinterpret_cast<uint8_t *>(base) : nullptr;
+    off += align_up((size_t)g.B * g.Hkv * g.Lq);
   }
   if (c) *c = w;
   return off;
@@ -139,7 +131,7 @@ size_t fwd_layout(const Geom &g0, char *base, FwdWs *ws) {
 
 size_t bwd_layout(const Geom &g0, char *base, BwdWs *ws) {
   BwdWs w{};
-  w.co = Coarse{tile_geom(g0), nullptr, nullptr, nullptr};
+  w.co = Coarse{tile_geom(g0), nullptr};
   const Geom g = w.co.gc;
   size_t off = 0;
   if (g.dtype == PHSA_BF16) {
@@ -258,19 +250,13 @@ phsa_status check_ws(const Geom &g, int op, const void *ws, size_t ws_bytes) {
 
 phsa_status from_hip(hipError_t e) { return e == hipSuccess ? PHSA_OK : PHSA_ERR_HIP; }
 
-// bf16 forward attention over sel: regroup m-token blocks into 64-key tiles
-// when m < 64, then index, sparse kernel and merge.
+// bf16 forward attention over sel: index (on 64-key tiles when m < 64 or with
+// the band), sparse kernel, band kernel and merge.
 hipError_t attn_fwd_bf16(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel, void *O,
                          float *LSE, void *ws, hipStream_t s) {
   FwdWs w;
   fwd_layout(g, static_cast<char *>(ws), &w);
-  const int32_t *tsel = sel;
-  if (w.co.csel) {
-    const hipError_t e = launch_coarsen(g, w.co.gc, sel, w.co.csel, w.co.cq, w.co.bflag, s);
-    if (e != hipSuccess) return e;
-    tsel = w.co.csel;
-  }
-  return launch_attn_fwd(w.co.gc, Q, K, V, tsel, w.co.cq, O, LSE, w.ix, w.opart, w.ml, s);
+  return launch_attn_fwd(w.co.gc, Q, K, V, sel, O, LSE, w.ix, w.opart, w.ml, s);
 }
 
 // ---------------------------------------------------------------- timing
@@ -414,16 +400,8 @@ phsa_status phsa_attn_bwd(const phsa_params *p, const void *Q, const void *K, co
                                            static_cast<const float *>(dO), LSE, sel, static_cast<float *>(dQ),
                                            static_cast<float *>(dK), static_cast<float *>(dV), w.Dvec, s));
     const bool reuse = (p->flags & PHSA_FLAG_REUSE_INDEX) != 0;
-    const int32_t *tsel = sel;
-    if (w.co.csel) {  // tiles of the m-token blocks (already there when the index is reused)
-      if (!reuse) {
-        const hipError_t e = launch_coarsen(g, w.co.gc, sel, w.co.csel, w.co.cq, w.co.bflag, s);
-        if (e != hipSuccess) return PHSA_ERR_HIP;
-      }
-      tsel = w.co.csel;
-    }
-    return from_hip(launch_attn_bwd(w.co.gc, Q, K, V, O, dO, LSE, tsel, w.co.cq, dQ, dK, dV, w.ix, w.Dvec, w.dqpart,
-                                    w.dkvpart, w.bkv, reuse, s));
+    return from_hip(launch_attn_bwd(w.co.gc, Q, K, V, O, dO, LSE, sel, dQ, dK, dV, w.ix, w.Dvec, w.dqpart, w.dkvpart,
+                                    w.bkv, reuse, s));
   })
 }
 

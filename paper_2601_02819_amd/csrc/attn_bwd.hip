@@ -446,13 +446,13 @@ hipError_t launch_bwd_pre(const Geom &g, const void *O, const void *dO, float *D
 }
 
 hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
-                           const void *dO, const float *LSE, const int32_t *sel, const uint8_t *quarters, void *dQ,
+                           const void *dO, const float *LSE, const int32_t *sel, void *dQ,
                            void *dK, void *dV, const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart,
                            float *bkv, bool reuse_index, hipStream_t s) {
   hipError_t e = launch_bwd_pre(g, O, dO, Dvec, s);
   if (e != hipSuccess) return e;
   if (!reuse_index) {
-    e = launch_build_index(g, sel, quarters, ix, s);
+    e = launch_build_index(g, sel, ix, s);
     if (e != hipSuccess) return e;
   }
   return g.d == 128 ? launch_bwd_d<128>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s)

@@ -282,10 +282,9 @@ static hipError_t launch_fwd_d(const Geom &g, const void *Q, const void *K, cons
   }
 }
 
-hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel,
-                           const uint8_t *quarters, void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml,
-                           hipStream_t s) {
-  hipError_t e = launch_build_index(g, sel, quarters, ix, s);
+hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel, void *O,
+                           float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s) {
+  hipError_t e = launch_build_index(g, sel, ix, s);
   if (e != hipSuccess) return e;
   return g.d == 128 ? launch_fwd_d<128>(g, Q, K, V, sel, O, LSE, ix, opart, ml, s)
                     : launch_fwd_d<64>(g, Q, K, V, sel, O, LSE, ix, opart, ml, s);

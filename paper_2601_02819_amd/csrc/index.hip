@@ -5,14 +5,22 @@
 // tile is loaded once and meets every query row that selected it.
 //
 // Entries are (row << 10) | (quarters << 6) | slot, where slot is the
-// position of t in the row's sel vector and quarters is a 4-bit mask of the
-// 16-key quarters of block t the row attends to (all four for 64-token
-// blocks; see coarsen_kernel for smaller ones).  The attention kernels store
-// per-entry partial results in list order (contiguous per work unit);
-// pmap[(row, slot)] = list position lets the per-row merges find them.
+// position of t among the row's entries (its sel vector, for 64-token blocks)
+// and quarters is a 4-bit mask of the 16-key quarters of t the row attends
+// to (all four for 64-token blocks).  The attention kernels store per-entry
+// partial results in list order (contiguous per work unit); pmap[(row, slot)]
+// = list position lets the per-row merges find them.
+//
+// Selections of m = 16 or 32 tokens, and rows whose local window goes to the
+// band kernels, are indexed on 64-key tiles: the m-token blocks a row selected
+// are grouped by the tile that holds them (tile = block / (64 / m)), and each
+// tile entry carries the mask of the 16-key quarters its blocks cover.  The
+// regrouping happens as the rows are read (row_entries), so the index is
+// keyed by the tile geometry gm (m = 64, T = Lk / 64, ksel = min(Ksel, T) plus
+// the band slot) while sel keeps its own width (the selection's Ksel).
 //
 // Four integer-only passes, all deterministic (no order depends on timing):
-//   count : per 256-row tile, an LDS bitmap [T][256 bits] of who selected
+//   count : per 256-row tile, an LDS bitmap [8 words][T] of who selected
 //           what; popcounts give per-tile counts cntw[bg][w][t].
 //   scan1 : per (bg, t), exclusive prefix over tiles -> cntw, total -> cnt.
 //   scan2 : one workgroup scans cnt into list offsets and unit offsets and
@@ -26,36 +34,130 @@ namespace phsa {
 
 __device__ __forceinline__ bool slot_valid(int t, int cur, int T) { return t >= 0 && t <= cur && t < T; }
 
-// The tile's sel rows are one contiguous run: staged into rows_s
-// ([kIndexTile][ksel]) with coalesced loads, then row tid is read from LDS.
-__device__ void build_tile_bitmap(uint32_t *bm, int32_t *rows_s, const int32_t *sel, const Geom &gm, int bg, int w) {
-  const int tid = threadIdx.x;
-  for (int x = tid; x < gm.T * 8; x += 256) bm[x] = 0u;
+// Width of a sel row: the selection's own Ksel (in its block units).
+__device__ __forceinline__ int sel_width(const Geom &gm) { return gm.n_init + gm.window / gm.sm + 1 + gm.top_k; }
+
+// Plain selections (64-token blocks, no band) are indexed as they are, one
+// thread per row: a row's entries are the valid prefix of its sel row
+// (ascending causal blocks, ended by -1 or a block past the query's own).
+__device__ __forceinline__ bool plain_rows(const Geom &gm) { return gm.sm == gm.m && !gm.band; }
+
+// The regrouped entries of one row, one wave per row with lane s holding slot
+// s of sel (t = that slot's block, -1 past the row's width).  A row's blocks
+// are ascending, so a tile's blocks sit in adjacent lanes; a tile's first lane
+// takes its slot by a ballot prefix count and ORs the quarters of the (at most
+// 64 / m) lanes of its group.  With gm.band, a row holding every local block
+// outside the init blocks (a_blk .. cur) leaves them to the band kernels
+// (band_ok); other rows keep all their blocks.  A lane with `mine` set holds
+// entry `pos` of the row: tile `tile` with quarter mask `qm`; n entries in all.
+struct RowEntries {
+  int tile;
+  unsigned qm;
+  int pos;
+  int n;
+  bool mine;
+  bool band_ok;
+};
+
+__device__ __forceinline__ RowEntries row_entries(int t, int i, const Geom &gm) {
+  const int lane = threadIdx.x & 63;
+  RowEntries e;
+  e.band_ok = false;
+  const int cur = (gm.q_pos0 + i) / gm.sm;
+  const int per = 64 / gm.sm, qpb = gm.sm / 16;
+  const bool in_range = t >= 0 && t <= cur && t < gm.Lk / gm.sm;
+  int a_blk = cur + 1;
+  if (gm.band) {
+    a_blk = max(max(0, cur - gm.window / gm.sm), min(gm.n_init, cur + 1));
+    const int have = __popcll(__ballot(in_range && t >= a_blk));
+    e.band_ok = a_blk <= cur && have == cur - a_blk + 1;
+  }
+  const bool valid = in_range && !(e.band_ok && t >= a_blk);
+  const int tc = valid ? t / per : -1;
+  const unsigned qb = valid ? ((1u << qpb) - 1u) << ((t % per) * qpb) : 0u;
+  const int prev = __shfl_up(tc, 1, 64);
+  const bool first = valid && (lane == 0 || prev != tc);
+  const uint64_t heads = __ballot(first);
+  e.pos = __popcll(heads & ((1ull << lane) - 1ull));
+  e.n = __popcll(heads);
+  unsigned acc = qb;
+  for (int dd = 1; dd < per; ++dd) {
+    const unsigned o = __shfl_down(qb, dd, 64);
+    const int otc = __shfl_down(tc, dd, 64);
+    if (lane + dd < 64 && otc == tc) acc |= o;
+  }
+  e.mine = first && e.pos < gm.ksel - gm.band;
+  e.tile = tc;
+  e.qm = acc;
+  return e;
+}
+
+constexpr int kRowBatch = 8;  // sel rows a wave has in flight (regrouped rows)
+
+// The bitmap bm [8][T] of the 256-row tile w of (b, g) = bg: bit r % 32 of
+// bm[r / 32][t] is set when row r has an entry for t.  Plain rows: the tile's
+// sel rows, one contiguous run, are staged into rows_s ([kIndexTile][Ksel])
+// with coalesced loads and each thread walks its row.  Regrouped rows: wave v
+// takes rows 64v .. 64v + 63, one row per pass with its slots across the
+// lanes (word-major bm, so a row's lanes, each on another t, hit different
+// banks).  Every thread calls this (it holds barriers).
+__device__ void build_tile_bitmap(uint32_t *bm, int32_t *rows_s, const int32_t *__restrict__ sel, const Geom &gm,
+                                  int bg, int w) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ks = sel_width(gm);
   const int nrow = min(kIndexTile, gm.Lq - w * kIndexTile);
-  const int32_t *src = sel + ((int64_t)bg * gm.Lq + (int64_t)w * kIndexTile) * gm.ksel;
-  for (int x = tid; x < nrow * gm.ksel; x += 256) rows_s[x] = src[x];
+  const int64_t row0 = (int64_t)bg * gm.Lq + (int64_t)w * kIndexTile;
+  for (int x = tid; x < gm.T * 8; x += 256) bm[x] = 0u;
+  if (plain_rows(gm)) {
+    const int32_t *src = sel + row0 * ks;
+    for (int x = tid; x < nrow * ks; x += 256) rows_s[x] = src[x];
+    __syncthreads();
+    if (tid < nrow) {
+      const int cur = (gm.q_pos0 + w * kIndexTile + tid) / gm.m;
+      for (int s = 0; s < ks; ++s) {
+        const int t = rows_s[tid * ks + s];
+        if (!slot_valid(t, cur, gm.T)) break;
+        atomicOr(&bm[(tid >> 5) * gm.T + t], 1u << (tid & 31));
+      }
+    }
+    __syncthreads();
+    return;
+  }
   __syncthreads();
-  if (tid < nrow) {
-    const int cur = (gm.q_pos0 + w * kIndexTile + tid) / gm.m;
-    // a row's valid slots are a prefix (ascending blocks, then -1 or blocks past cur)
-    for (int s = 0; s < gm.ksel; ++s) {
-      const int t = rows_s[tid * gm.ksel + s];
-      if (!slot_valid(t, cur, gm.T)) break;
-      atomicOr(&bm[t * 8 + (tid >> 5)], 1u << (tid & 31));
+  for (int j0 = 0; j0 < 64; j0 += kRowBatch) {
+    int t[kRowBatch];
+#pragma unroll
+    for (int u = 0; u < kRowBatch; ++u) {
+      const int r = wave * 64 + j0 + u;
+      t[u] = (r < nrow && lane < ks) ? sel[(row0 + r) * ks + lane] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kRowBatch; ++u) {
+      const int r = wave * 64 + j0 + u;
+      if (r < nrow) {  // wave-uniform
+        const RowEntries e = row_entries(t[u], w * kIndexTile + r, gm);
+        if (e.mine) atomicOr(&bm[(r >> 5) * gm.T + e.tile], 1u << (r & 31));
+      }
     }
   }
   __syncthreads();
 }
 
+// LDS of the count kernel (the fill kernel adds one list position per t).
+inline size_t index_lds_bytes(const Geom &g) {
+  const bool plain = g.sm == g.m && !g.band;
+  return (size_t)g.T * 8 * sizeof(uint32_t) + (plain ? (size_t)kIndexTile * g.ksel * sizeof(int32_t) : 0);
+}
+
 __global__ __launch_bounds__(256) void index_count_kernel(const int32_t *__restrict__ sel, Geom gm, IndexWs ix) {
   extern __shared__ uint32_t bm[];
   const int w = blockIdx.x, bg = blockIdx.y;
-  build_tile_bitmap(bm, reinterpret_cast<int32_t *>(bm + gm.T * 8), sel, gm, bg, w);
+  build_tile_bitmap(bm, reinterpret_cast<int32_t *>(bm + 8 * gm.T), sel, gm, bg, w);
   int32_t *dst = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
   for (int t = threadIdx.x; t < gm.T; t += 256) {
     int c = 0;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) c += __popc(bm[t * 8 + k]);
+    for (int k = 0; k < 8; ++k) c += __popc(bm[k * gm.T + t]);
     dst[t] = c;
   }
 }
@@ -117,115 +219,88 @@ __global__ __launch_bounds__(1024) void index_scan_lists_kernel(Geom gm, IndexWs
   }
 }
 
-__global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restrict__ sel,
-                                                         const uint8_t *__restrict__ quarters, Geom gm, IndexWs ix) {
+// Writes each row's entries into their lists, its position-map row (list
+// position per slot, -1 for empty slots, the band partial in the last slot of
+// a band row) and, with the band, its band flag.  The tile's first list
+// position for each t (list offset + tile offset) is staged in LDS beside the
+// bitmap; an entry's position adds the lower rows of the tile that chose t.
+__global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restrict__ sel, Geom gm, IndexWs ix) {
   extern __shared__ uint32_t bm[];
-  // [kIndexTile][ksel]: the staged sel rows, each entry replaced in place by its list position
-  int32_t *pm = reinterpret_cast<int32_t *>(bm + gm.T * 8);
-  const int w = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x;
-  build_tile_bitmap(bm, pm, sel, gm, bg, w);
-  const int i = w * kIndexTile + tid;
-  if (i < gm.Lq) {
-    const int cur = (gm.q_pos0 + i) / gm.m;
-    const int32_t *tile_off = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
-    const int word = tid >> 5;
-    const uint32_t below = (1u << (tid & 31)) - 1u;
-    int s = 0;
-    for (; s < gm.ksel; ++s) {  // the valid prefix
-      const int t = pm[tid * gm.ksel + s];
-      if (!slot_valid(t, cur, gm.T)) break;
-      int rank = __popc(bm[t * 8 + word] & below);
-      for (int k = 0; k < word; ++k) rank += __popc(bm[t * 8 + k]);
-      const int32_t pos = ix.off[bg * gm.T + t] + tile_off[t] + rank;
-      const int qm = quarters ? quarters[((int64_t)bg * gm.Lq + i) * gm.ksel + s] & 15 : 15;
-      ix.tok[pos] = (i << 10) | (qm << 6) | s;
-      pm[tid * gm.ksel + s] = pos;
-    }
-    // the last slot of a band geometry marks (-2) a row whose local window is in the band
-    const bool in_band = ix.bflag && pm[tid * gm.ksel + gm.ksel - 1] == -2;
-    for (; s < gm.ksel; ++s) pm[tid * gm.ksel + s] = -1;
-    if (in_band) pm[tid * gm.ksel + gm.ksel - 1] = (int32_t)(ix.band_base + (int64_t)bg * gm.Lq + i);
-  }
-  __syncthreads();
-  // the tile's rows are consecutive, so their position-map rows form one contiguous run
+  int32_t *base_s = reinterpret_cast<int32_t *>(bm + 8 * gm.T);
+  int32_t *rows_s = base_s + gm.T;  // plain rows: staged sel rows, then their list positions
+  const int w = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int32_t *tile_off = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
+  const int32_t *list_off = ix.off + (int64_t)bg * gm.T;
+  for (int t = tid; t < gm.T; t += 256) base_s[t] = list_off[t] + tile_off[t];
+  build_tile_bitmap(bm, rows_s, sel, gm, bg, w);  // its barriers also publish base_s
+  const int ks = sel_width(gm);
   const int nrow = min(kIndexTile, gm.Lq - w * kIndexTile);
-  int32_t *dst = ix.pmap + ((int64_t)bg * gm.Lq + (int64_t)w * kIndexTile) * gm.ksel;
-  for (int x = tid; x < nrow * gm.ksel; x += 256) dst[x] = pm[x];
+  const int64_t row0 = (int64_t)bg * gm.Lq + (int64_t)w * kIndexTile;
+  if (plain_rows(gm)) {  // gm.ksel == ks
+    const int i = w * kIndexTile + tid;
+    if (tid < nrow) {
+      const int cur = (gm.q_pos0 + i) / gm.m;
+      const int word = tid >> 5;
+      const uint32_t below = (1u << (tid & 31)) - 1u;
+      int s = 0;
+      for (; s < ks; ++s) {  // the valid prefix
+        const int t = rows_s[tid * ks + s];
+        if (!slot_valid(t, cur, gm.T)) break;
+        int rank = __popc(bm[word * gm.T + t] & below);
+        for (int k = 0; k < word; ++k) rank += __popc(bm[k * gm.T + t]);
+        const int32_t p = base_s[t] + rank;
+        ix.tok[p] = (i << 10) | (15 << 6) | s;
+        rows_s[tid * ks + s] = p;
+      }
+      for (; s < ks; ++s) rows_s[tid * ks + s] = -1;
+    }
+    __syncthreads();
+    // the tile's rows are consecutive, so their position-map rows form one contiguous run
+    int32_t *dst = ix.pmap + row0 * ks;
+    for (int x = tid; x < nrow * ks; x += 256) dst[x] = rows_s[x];
+    return;
+  }
+  unsigned flag = 0;  // band flag of row 64 * wave + lane
+  for (int j0 = 0; j0 < 64; j0 += kRowBatch) {
+    int t[kRowBatch];
+#pragma unroll
+    for (int u = 0; u < kRowBatch; ++u) {
+      const int r = wave * 64 + j0 + u;
+      t[u] = (r < nrow && lane < ks) ? sel[(row0 + r) * ks + lane] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kRowBatch; ++u) {
+      const int r = wave * 64 + j0 + u;
+      if (r >= nrow) continue;  // wave-uniform
+      const int i = w * kIndexTile + r;
+      const int64_t x = row0 + r;
+      const RowEntries e = row_entries(t[u], i, gm);
+      int32_t p = -1;
+      if (e.mine) {
+        const int word = r >> 5;
+        int rank = __popc(bm[word * gm.T + e.tile] & ((1u << (r & 31)) - 1u));
+        for (int k = 0; k < word; ++k) rank += __popc(bm[k * gm.T + e.tile]);
+        p = base_s[e.tile] + rank;
+        ix.tok[p] = (i << 10) | ((int)(e.qm & 15u) << 6) | e.pos;
+      }
+      // entry pos's list position moves to lane pos (a lane below n has exactly
+      // one sender; the others send to lane 63, which is below n only when all
+      // 64 lanes are entries), so the row's position-map row is one store
+      const int moved = __builtin_amdgcn_ds_permute((e.mine ? e.pos : 63) << 2, p);
+      if (lane < gm.ksel)
+        ix.pmap[x * gm.ksel + lane] =
+            lane < e.n ? moved : (gm.band && e.band_ok && lane == gm.ksel - 1) ? (int32_t)(ix.band_base + x) : -1;
+      if (lane == j0 + u) flag = e.band_ok ? 1u : 0u;
+    }
+  }
+  if (gm.band && wave * 64 + lane < nrow) ix.bflag[row0 + wave * 64 + lane] = (uint8_t)flag;
 }
 
-// Blocks of m = 16 or 32 tokens run on the 64-key attention tiles: the
-// m-token blocks a row selected are grouped by the 64-token tile that holds
-// them (tile = block / (64 / m)), and each tile gets the mask of the 16-key
-// quarters its selected blocks cover.  gc is the tile geometry (m = 64,
-// T = Lk / 64, ksel = min(Ksel, T): no row holds more tiles than that).
-// One wave per row, lane s holding slot s (Ksel <= 64): the rows are ascending,
-// so a tile's blocks sit in adjacent lanes; a tile's first lane finds its
-// output slot by a ballot prefix count and ORs the quarters of the (at most
-// 64 / m) lanes of its group.  Reads and writes are contiguous per row.
-// With gc.band, a row that holds every local block outside the init blocks
-// (a_blk .. cur) leaves them to the band kernels: they are not regrouped, the
-// row's last slot holds -2 and bflag = 1.  Other rows keep all their blocks.
-__global__ __launch_bounds__(256) void coarsen_kernel(const int32_t *__restrict__ sel, Geom g, Geom gc,
-                                                      int32_t *__restrict__ csel, uint8_t *__restrict__ cq,
-                                                      uint8_t *__restrict__ bflag) {
-  const int lane = threadIdx.x & 63;
-  const int64_t x = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // row (b, g, i)
-  if (x >= (int64_t)g.B * g.Hkv * g.Lq) return;                    // whole wave
-  const int i = (int)(x % g.Lq);
-  const int cur = (g.q_pos0 + i) / g.m;
-  const int per = 64 / g.m, qpb = g.m / 16;
-  const int t = lane < g.ksel ? sel[x * g.ksel + lane] : -1;
-  const bool in_range = t >= 0 && t <= cur && t < g.T;
-  bool band_ok = false;
-  int a_blk = cur + 1;
-  if (gc.band) {
-    a_blk = max(max(0, cur - g.window / g.m), min(g.n_init, cur + 1));
-    const int have = __popcll(__ballot(in_range && t >= a_blk));
-    band_ok = a_blk <= cur && have == cur - a_blk + 1;
-  }
-  const bool valid = in_range && !(band_ok && t >= a_blk);
-  const int tc = valid ? t / per : -1;
-  const unsigned qb = valid ? ((1u << qpb) - 1u) << ((t % per) * qpb) : 0u;
-  const int prev = __shfl_up(tc, 1, 64);
-  const bool first = valid && (lane == 0 || prev != tc);
-  const uint64_t heads = __ballot(first);
-  const int pos = __popcll(heads & ((1ull << lane) - 1ull));
-  const int n = __popcll(heads);
-  unsigned acc = qb;
-  for (int dd = 1; dd < per; ++dd) {
-    const unsigned o = __shfl_down(qb, dd, 64);
-    const int otc = __shfl_down(tc, dd, 64);
-    if (lane + dd < 64 && otc == tc) acc |= o;
-  }
-  int32_t *out = csel + x * gc.ksel;
-  uint8_t *oq = cq + x * gc.ksel;
-  if (first && pos < gc.ksel - gc.band) {
-    out[pos] = tc;
-    oq[pos] = (uint8_t)acc;
-  }
-  if (lane >= n && lane < gc.ksel) {
-    out[lane] = (gc.band && band_ok && lane == gc.ksel - 1) ? -2 : -1;
-    oq[lane] = 0;
-  }
-  if (gc.band && lane == 0) bflag[x] = band_ok ? 1 : 0;
-}
-
-hipError_t launch_coarsen(const Geom &g, const Geom &gc, const int32_t *sel, int32_t *csel, uint8_t *cq,
-                          uint8_t *bflag, hipStream_t s) {
-  const int64_t nrows = (int64_t)g.B * g.Hkv * g.Lq;
-  timing_begin("phsa_coarsen", s);
-  hipLaunchKernelGGL(coarsen_kernel, dim3((unsigned)((nrows + 3) / 4)), dim3(256), 0, s, sel, g, gc, csel, cq, bflag);
-  timing_end(s);
-  return hipGetLastError();
-}
-
-hipError_t launch_build_index(const Geom &g, const int32_t *sel, const uint8_t *quarters, const IndexWs &ix,
-                              hipStream_t s) {
+hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &ix, hipStream_t s) {
   const int nbgt = g.B * g.Hkv * g.T;
-  const size_t lds = (size_t)g.T * 8 * sizeof(uint32_t);
-  const size_t rows_lds = (size_t)kIndexTile * g.ksel * sizeof(int32_t);
+  const size_t lds = index_lds_bytes(g);
   timing_begin("phsa_index_count", s);
-  hipLaunchKernelGGL(index_count_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds + rows_lds, s, sel, g, ix);
+  hipLaunchKernelGGL(index_count_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds, s, sel, g, ix);
   timing_end(s);
   timing_begin("phsa_index_scan_tiles", s);
   hipLaunchKernelGGL(index_scan_tiles_kernel, dim3((nbgt + 255) / 256), dim3(256), 0, s, g, ix, nbgt);
@@ -234,7 +309,8 @@ hipError_t launch_build_index(const Geom &g, const int32_t *sel, const uint8_t *
   hipLaunchKernelGGL(index_scan_lists_kernel, dim3(1), dim3(1024), 0, s, g, ix, nbgt);
   timing_end(s);
   timing_begin("phsa_index_fill", s);
-  hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds + rows_lds, s, sel, quarters, g, ix);
+  hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds + (size_t)g.T * sizeof(int32_t), s, sel,
+                     g, ix);
   timing_end(s);
   return hipGetLastError();
 }

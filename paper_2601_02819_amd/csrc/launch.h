@@ -38,7 +38,7 @@ struct IndexWs {
   int2 *units;        // [units_max]    (b*Hkv*T + g*T + t, first list entry)
   int64_t band_base;  // list position of the band partial of row (b, g, i): band_base + (b*Hkv + g)*Lq + i
   int64_t discard;    // partial row that absorbs stores past a chunk's end (after the list and band rows)
-  const uint8_t *bflag;  // [B*Hkv*Lq] 1: the row's local window is in the band (NULL: no band)
+  uint8_t *bflag;     // [B*Hkv*Lq] 1: the row's local window is in the band (NULL: no band)
 };
 
 constexpr int kIndexTile = 256;  // query rows per index-building workgroup
@@ -53,20 +53,14 @@ hipError_t launch_compress(const Geom &g, const void *K, const uint8_t *punct, f
 // ws: select_split_bytes(g) bytes (bf16 hi/lo copies of K_comp), unused for float32
 size_t select_split_bytes(const Geom &g);
 hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t *sel, void *ws, hipStream_t s);
-// quarters: per (row, slot) mask of the 16-key quarters of the block the row
-// attends to, NULL = all four (64-token blocks)
-hipError_t launch_build_index(const Geom &g, const int32_t *sel, const uint8_t *quarters, const IndexWs &ix,
-                              hipStream_t s);
-// m-token blocks -> 64-key tiles with quarter masks; gc = tile geometry.  With
-// gc.band the local windows of rows that hold them whole are left out (bflag = 1)
-hipError_t launch_coarsen(const Geom &g, const Geom &gc, const int32_t *sel, int32_t *csel, uint8_t *cq,
-                          uint8_t *bflag, hipStream_t s);
-hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel,
-                           const uint8_t *quarters, void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml,
-                           hipStream_t s);
+// g: the index's geometry (the tile geometry of m-token blocks); sel is the
+// selection as phsa_select writes it (its own block size and Ksel)
+hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &ix, hipStream_t s);
+hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel, void *O,
+                           float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s);
 // bkv: with g.band, float32 [B*Hkv*T][2][64][d] for the band's dK, dV per 64-key tile
 hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
-                           const void *dO, const float *LSE, const int32_t *sel, const uint8_t *quarters, void *dQ,
+                           const void *dO, const float *LSE, const int32_t *sel, void *dQ,
                            void *dK, void *dV, const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart,
                            float *bkv, bool reuse_index, hipStream_t s);
 // band kernels (attn_band.hip): local windows as dense query-major / key-major attention
