@@ -26,6 +26,10 @@ CASES = [
     wl_("m16_g1", 2, 768, 2, 2, 128, 16, 12, 3, 128),
     wl_("m32_win", 1, 1024, 4, 2, 128, 32, 6, 1, 64),
     wl_("m16_tail_rows", 1, 2048, 4, 2, 128, 16, 10, 8, 256, Lq=333),
+    # fewer query rows than one wave of the index kernels (band on), and one row
+    # alone in the last 256-row index tile (no window)
+    wl_("m16_37_rows", 1, 2048, 4, 2, 128, 16, 12, 8, 256, Lq=37),
+    wl_("m32_257_rows", 1, 2048, 4, 2, 128, 32, 9, 2, 0, Lq=257),
     wl_("m16_fp32", 1, 1040, 4, 2, 128, 16, 5, 2, 64, dtype="fp32"),
     wl_("m32_fp32_g4", 1, 640, 8, 2, 64, 32, 4, 1, 32, dtype="fp32"),
 ]
