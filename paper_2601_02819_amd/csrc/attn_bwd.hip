@@ -319,7 +319,7 @@ __global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restri
   const int bg = bgt / gm.T, t = bgt - bg * gm.T;
   const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   constexpr int PER = 64 * D / kFinSplit;  // elements of dK (and of dV) per workgroup
-  for (int x = blockIdx.y * PER + threadIdx.x * 4; x < (blockIdx.y + 1) * PER; x += 256 * 4) {
+  for (int x = blockIdx.y * PER + threadIdx.x * 4; x < (int)(blockIdx.y + 1) * PER; x += 256 * 4) {
     const int kk = x / D, c = x - kk * D;
     float4 sk = make_float4(0.f, 0.f, 0.f, 0.f), sv = sk;
     if (bkv) {
@@ -388,7 +388,7 @@ __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restri
 
 template <int D, int G>
 static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
-                               const float *LSE, const int32_t *sel, void *dQ, void *dK, void *dV, const IndexWs &ix,
+                               const float *LSE, void *dQ, void *dK, void *dV, const IndexWs &ix,
                                const float *Dvec, void *dqpart, float *dkvpart, float *bkv, hipStream_t s) {
   if (g.band) {  // the band's dQ partials and dK/dV tiles first: the sparse epilogue adds the latter
     const hipError_t e = launch_bwd_band(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
@@ -415,13 +415,13 @@ static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, cons
 
 template <int D>
 static hipError_t launch_bwd_d(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
-                               const float *LSE, const int32_t *sel, void *dQ, void *dK, void *dV, const IndexWs &ix,
+                               const float *LSE, void *dQ, void *dK, void *dV, const IndexWs &ix,
                                const float *Dvec, void *dqpart, float *dkvpart, float *bkv, hipStream_t s) {
   switch (g.G) {
-    case 1: return launch_bwd_t<D, 1>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
-    case 2: return launch_bwd_t<D, 2>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
-    case 4: return launch_bwd_t<D, 4>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
-    default: return launch_bwd_t<D, 8>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    case 1: return launch_bwd_t<D, 1>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    case 2: return launch_bwd_t<D, 2>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    case 4: return launch_bwd_t<D, 4>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    default: return launch_bwd_t<D, 8>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
   }
 }
 
@@ -455,8 +455,8 @@ hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const vo
     e = launch_build_index(g, sel, ix, s);
     if (e != hipSuccess) return e;
   }
-  return g.d == 128 ? launch_bwd_d<128>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s)
-                    : launch_bwd_d<64>(g, Q, K, V, dO, LSE, sel, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+  return g.d == 128 ? launch_bwd_d<128>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s)
+                    : launch_bwd_d<64>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
 }
 
 }  // namespace phsa

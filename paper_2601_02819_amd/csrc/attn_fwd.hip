@@ -252,8 +252,8 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
 }
 
 template <int D, int G>
-static hipError_t launch_fwd_t(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel,
-                               void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s) {
+static hipError_t launch_fwd_t(const Geom &g, const void *Q, const void *K, const void *V, void *O, float *LSE,
+                               const IndexWs &ix, void *opart, float2 *ml, hipStream_t s) {
   timing_begin("phsa_attn_fwd_sparse", s);
   hipLaunchKernelGGL((attn_fwd_sparse_kernel<D, G>), dim3((unsigned)ix.units_max), dim3(256), 0, s,
                      static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
@@ -272,13 +272,13 @@ static hipError_t launch_fwd_t(const Geom &g, const void *Q, const void *K, cons
 }
 
 template <int D>
-static hipError_t launch_fwd_d(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel,
-                               void *O, float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s) {
+static hipError_t launch_fwd_d(const Geom &g, const void *Q, const void *K, const void *V, void *O, float *LSE,
+                               const IndexWs &ix, void *opart, float2 *ml, hipStream_t s) {
   switch (g.G) {
-    case 1: return launch_fwd_t<D, 1>(g, Q, K, V, sel, O, LSE, ix, opart, ml, s);
-    case 2: return launch_fwd_t<D, 2>(g, Q, K, V, sel, O, LSE, ix, opart, ml, s);
-    case 4: return launch_fwd_t<D, 4>(g, Q, K, V, sel, O, LSE, ix, opart, ml, s);
-    default: return launch_fwd_t<D, 8>(g, Q, K, V, sel, O, LSE, ix, opart, ml, s);
+    case 1: return launch_fwd_t<D, 1>(g, Q, K, V, O, LSE, ix, opart, ml, s);
+    case 2: return launch_fwd_t<D, 2>(g, Q, K, V, O, LSE, ix, opart, ml, s);
+    case 4: return launch_fwd_t<D, 4>(g, Q, K, V, O, LSE, ix, opart, ml, s);
+    default: return launch_fwd_t<D, 8>(g, Q, K, V, O, LSE, ix, opart, ml, s);
   }
 }
 
@@ -286,8 +286,8 @@ hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const vo
                            float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s) {
   hipError_t e = launch_build_index(g, sel, ix, s);
   if (e != hipSuccess) return e;
-  return g.d == 128 ? launch_fwd_d<128>(g, Q, K, V, sel, O, LSE, ix, opart, ml, s)
-                    : launch_fwd_d<64>(g, Q, K, V, sel, O, LSE, ix, opart, ml, s);
+  return g.d == 128 ? launch_fwd_d<128>(g, Q, K, V, O, LSE, ix, opart, ml, s)
+                    : launch_fwd_d<64>(g, Q, K, V, O, LSE, ix, opart, ml, s);
 }
 
 }  // namespace phsa

@@ -178,7 +178,7 @@ __global__ __launch_bounds__(256) void index_scan_tiles_kernel(Geom gm, IndexWs 
 
 // Single workgroup of 1024 threads: exclusive scans of list lengths and of
 // units per list, then the unit table.
-__global__ __launch_bounds__(1024) void index_scan_lists_kernel(Geom gm, IndexWs ix, int nbgt) {
+__global__ __launch_bounds__(1024) void index_scan_lists_kernel(IndexWs ix, int nbgt) {
   __shared__ int s_a[1024], s_b[1024];
   const int tid = threadIdx.x;
   const int per = (nbgt + 1023) / 1024;
@@ -306,7 +306,7 @@ hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &
   hipLaunchKernelGGL(index_scan_tiles_kernel, dim3((nbgt + 255) / 256), dim3(256), 0, s, g, ix, nbgt);
   timing_end(s);
   timing_begin("phsa_index_scan_lists", s);
-  hipLaunchKernelGGL(index_scan_lists_kernel, dim3(1), dim3(1024), 0, s, g, ix, nbgt);
+  hipLaunchKernelGGL(index_scan_lists_kernel, dim3(1), dim3(1024), 0, s, ix, nbgt);
   timing_end(s);
   timing_begin("phsa_index_fill", s);
   hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds + (size_t)g.T * sizeof(int32_t), s, sel,

@@ -66,7 +66,7 @@ __device__ __forceinline__ void emit_row(int32_t *__restrict__ out, int *pk, int
 // lists (4 * 64 * KMAX (score, block) pairs).
 template <int KMAX>
 __device__ __forceinline__ void finish_rows(const float (&ls)[KMAX], const int (&lt)[KMAX], unsigned char *smem,
-                                            int (*picks)[KMAX], bool active, int i, int cur, int lo, int bg,
+                                            int (*picks)[KMAX], bool active, int i, int cur, int bg,
                                             int32_t *__restrict__ sel, const Geom &gm) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   __syncthreads();
@@ -191,7 +191,7 @@ __global__ __launch_bounds__(256) void select_kernel(const T *__restrict__ Q, co
     }
   }
 
-  finish_rows<KMAX>(ls, lt, smem, picks, wave == 0 && row_ok, i, cur, lo, bg, sel, gm);
+  finish_rows<KMAX>(ls, lt, smem, picks, wave == 0 && row_ok, i, cur, bg, sel, gm);
 }
 
 // Softmax-sum selection (PHSA_FLAG_SELECT_SOFTMAX_SUM): Eq. 8's softmax is
@@ -338,7 +338,7 @@ __global__ __launch_bounds__(256) void select_softmax_kernel(const T *__restrict
       }
     }
   }
-  finish_rows<KMAX>(ls, lt, smem, picks, wave == 0 && row_ok && hh == 0, i, cur, lo, bg, sel, gm);
+  finish_rows<KMAX>(ls, lt, smem, picks, wave == 0 && row_ok && hh == 0, i, cur, bg, sel, gm);
 }
 
 // Softmax-sum selection on the matrix cores (bf16 inputs; mode of
