@@ -73,6 +73,27 @@ __device__ __forceinline__ int seq_len(const int32_t *clen, int b, const Geom &g
   return clen ? min(max(clen[b], 1), gm.Lk) : gm.Lk;
 }
 
+// Sum over the CPR consecutive lanes that share a key row (CPR = 8, 16 or 32),
+// every lane getting the total.  Within a 16-lane row DPP moves do it: lane ^ 1
+// and lane ^ 2 (quad permutations), then the mirrored half row and the
+// mirrored row, which pair the quad sums as lane ^ 4 and lane ^ 8 would (the
+// same additions, so the same result as a shuffle butterfly).  Rows are paired
+// by a shuffle.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float a) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), CTRL, 0xF, 0xF, true));
+}
+template <int CPR>
+__device__ __forceinline__ float key_row_sum(float a) {
+  static_assert(CPR == 8 || CPR == 16 || CPR == 32, "key rows span 8, 16 or 32 lanes");
+  a += dpp_move<0xB1>(a);   // quad_perm [1, 0, 3, 2]
+  a += dpp_move<0x4E>(a);   // quad_perm [2, 3, 0, 1]
+  a += dpp_move<0x141>(a);  // row_half_mirror
+  if constexpr (CPR >= 16) a += dpp_move<0x140>(a);  // row_mirror
+  if constexpr (CPR >= 32) a += __shfl_xor(a, 16, 64);
+  return a;
+}
+
 // MODE 0 ranks on the summed logits of the group's heads.  MODE 1
 // (PHSA_FLAG_SELECT_SOFTMAX_SUM) keeps every head's log2 logits of the
 // complete blocks 0..cur-1 in LDS, reduces each head's log2 normaliser over
@@ -126,8 +147,7 @@ __global__ __launch_bounds__(512) void decode_select_kernel(const T *__restrict_
       for (int h = 0; h < GM; ++h) {
         if (h >= NH) break;
         float a = fmaf(q[h][0], v[u].x, fmaf(q[h][1], v[u].y, fmaf(q[h][2], v[u].z, q[h][3] * v[u].w)));
-#pragma unroll
-        for (int o = 1; o < LPR; o <<= 1) a += __shfl_xor(a, o, 64);
+        a = key_row_sum<LPR>(a);
         if (lane % LPR == 0 && t < s1) sc[h * gm.T + t] = MODE == 1 ? a : a * gm.scale;
       }
     }
@@ -235,7 +255,7 @@ __global__ __launch_bounds__(512) void decode_select_kernel(const T *__restrict_
 // (b, g); wave w takes slots w, w + 4, ....  A block's K and V rows arrive
 // with coalesced 16-byte loads, NI per lane (lane = one 16-byte chunk of a key
 // row, KPI key rows per load); the CPR lanes of a row reduce its dot products
-// by shuffles.  Each wave keeps a running (m, l, o) per head (log2 units);
+// (key_row_sum).  Each wave keeps a running (m, l, o) per head (log2 units);
 // the four are merged through LDS and O, LSE written directly.
 template <typename T, int D, int G>
 __global__ __launch_bounds__(256, G >= 8 ? 1 : 2) void decode_attn_kernel(const T *__restrict__ Q, const T *__restrict__ K,
@@ -270,59 +290,68 @@ __global__ __launch_bounds__(256, G >= 8 ? 1 : 2) void decode_attn_kernel(const 
     for (int e = 0; e < VEC; ++e) o[h][e] = 0.f;
   }
   const int pos = seq_len(clen, b, gm) - 1, cur = pos / gm.m;
-  for (int s = wave; s < gm.ksel; s += 4) {
-    const int t = sel[(int64_t)bg * gm.ksel + s];
-    if (t < 0 || t > cur || t >= gm.T) continue;  // wave-uniform
-    for (int k0 = 0; k0 < gm.m; k0 += KG) {
-      u32x4 kr[NI], vr[NI];  // native vectors: uint4 arrays here would live in scratch
+  // this wave's slots w, w + 4, ...: lane j holds slot w + 4j (Ksel <= 64), and
+  // the valid ones are taken in slot order from a wave-uniform bit mask
+  const int sj = wave + 4 * lane;
+  const int tl = sj < gm.ksel ? sel[(int64_t)bg * gm.ksel + sj] : -1;
+  uint64_t todo = __ballot(tl >= 0 && tl <= cur && tl < gm.T);
+  auto load_group = [&](int t, int k0, u32x4 (&kr)[NI], u32x4 (&vr)[NI]) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int key = min(k0 + i * KPI + sub, gm.m - 1);  // rows past a short block are masked below
+      const int64_t src = (((int64_t)b * gm.Lk + (int64_t)t * gm.m + key) * gm.Hkv + g) * D + ch * VEC;
+      kr[i] = *reinterpret_cast<const u32x4 *>(K + src);
+      vr[i] = *reinterpret_cast<const u32x4 *>(V + src);
+    }
+  };
+  auto attend = [&](int t, int k0, const u32x4 (&kr)[NI], const u32x4 (&vr)[NI]) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float sc[NI];
+      float bm = -INFINITY;
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
-        const int key = min(k0 + i * KPI + sub, gm.m - 1);  // rows past a short block are masked below
-        const int64_t src = (((int64_t)b * gm.Lk + (int64_t)t * gm.m + key) * gm.Hkv + g) * D + ch * VEC;
-        kr[i] = *reinterpret_cast<const u32x4 *>(K + src);
-        vr[i] = *reinterpret_cast<const u32x4 *>(V + src);
+        const T *pk = reinterpret_cast<const T *>(&kr[i]);
+        float a = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) a = fmaf(qv[h][e], to_f32<T>(pk[e]), a);
+        a = key_row_sum<CPR>(a);
+        const int kb = k0 + i * KPI + sub;
+        sc[i] = kb < gm.m && t * gm.m + kb <= pos ? a : -INFINITY;
+        bm = fmaxf(bm, sc[i]);
       }
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        float sc[NI];
-        float bm = -INFINITY;
+      for (int x = CPR; x < 64; x <<= 1) bm = fmaxf(bm, __shfl_xor(bm, x, 64));
+      const float mn = fmaxf(mrun[h], bm);
+      // mn stays -inf only while every key so far was past the query (a partly
+      // written own block): nothing has been accumulated yet
+      const float f = mn == -INFINITY ? 1.f : exp2f(mrun[h] - mn);
+      float ls = 0.f;
 #pragma unroll
-        for (int i = 0; i < NI; ++i) {
-          const T *pk = reinterpret_cast<const T *>(&kr[i]);
-          float a = 0.f;
+      for (int e = 0; e < VEC; ++e) o[h][e] *= f;
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) a = fmaf(qv[h][e], to_f32<T>(pk[e]), a);
+      for (int i = 0; i < NI; ++i) {
+        // keys past the query (the unwritten tail of its own block) add nothing,
+        // whatever their V slots hold
+        const int kb = k0 + i * KPI + sub;
+        const bool valid = kb < gm.m && t * gm.m + kb <= pos;
+        const float p = valid ? exp2f(sc[i] - mn) : 0.f;
+        ls += p;
+        const T *pv = reinterpret_cast<const T *>(&vr[i]);
 #pragma unroll
-          for (int x = 1; x < CPR; x <<= 1) a += __shfl_xor(a, x, 64);
-          const int kb = k0 + i * KPI + sub;
-          sc[i] = kb < gm.m && t * gm.m + kb <= pos ? a : -INFINITY;
-          bm = fmaxf(bm, sc[i]);
-        }
-#pragma unroll
-        for (int x = CPR; x < 64; x <<= 1) bm = fmaxf(bm, __shfl_xor(bm, x, 64));
-        const float mn = fmaxf(mrun[h], bm);
-        // mn stays -inf only while every key so far was past the query (a partly
-        // written own block): nothing has been accumulated yet
-        const float f = mn == -INFINITY ? 1.f : exp2f(mrun[h] - mn);
-        float ls = 0.f;
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) o[h][e] *= f;
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-          // keys past the query (the unwritten tail of its own block) add nothing,
-          // whatever their V slots hold
-          const int kb = k0 + i * KPI + sub;
-          const bool valid = kb < gm.m && t * gm.m + kb <= pos;
-          const float p = valid ? exp2f(sc[i] - mn) : 0.f;
-          ls += p;
-          const T *pv = reinterpret_cast<const T *>(&vr[i]);
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) o[h][e] = valid ? fmaf(p, to_f32<T>(pv[e]), o[h][e]) : o[h][e];
-        }
-        // ls counts this lane's keys; the CPR lanes of a key row hold the same keys
-        lrun[h] = lrun[h] * f + ls;
-        mrun[h] = mn;
+        for (int e = 0; e < VEC; ++e) o[h][e] = valid ? fmaf(p, to_f32<T>(pv[e]), o[h][e]) : o[h][e];
       }
+      // ls counts this lane's keys; the CPR lanes of a key row hold the same keys
+      lrun[h] = lrun[h] * f + ls;
+      mrun[h] = mn;
+    }
+  };
+  for (; todo; todo &= todo - 1) {
+    const int t = __builtin_amdgcn_readlane(tl, __builtin_ctzll(todo));
+    for (int k0 = 0; k0 < gm.m; k0 += KG) {
+      u32x4 kr[NI], vr[NI];  // native vectors: uint4 arrays here would live in scratch
+      load_group(t, k0, kr, vr);
+      attend(t, k0, kr, vr);
     }
   }
   // reduce over the key-row groups of the wave (lanes with the same chunk)
