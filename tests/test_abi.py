@@ -5,6 +5,7 @@ import os
 import re
 
 import pytest
+import torch
 
 from paper_2601_02819_amd import phsa
 
@@ -140,3 +141,17 @@ def test_status_strings():
     for s in range(8):
         assert isinstance(phsa.status_string(s), str) and phsa.status_string(s)
     assert phsa.status_string(99) == "unknown status"
+
+
+def test_missing_library_raises(monkeypatch):
+    """No fallback: without the built library the binding raises instead of computing."""
+    monkeypatch.setattr(phsa, "_lib", None)
+    monkeypatch.setattr(phsa, "LIB_PATH", os.path.join(ROOT, "no_such_dir", "libphsa.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        phsa.lib()
+    with pytest.raises(RuntimeError, match="missing"):
+        phsa.workspace_size(_p(), phsa.OP_ATTN_FWD)
+    # CPU tensors are refused before any library call
+    k = torch.zeros(1, 64, 1, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        phsa.compress(k, torch.zeros(1, 64, dtype=torch.uint8), phsa.Config())
