@@ -59,6 +59,15 @@ struct RowEntries {
   bool band_ok;
 };
 
+// Whole-wave DPP shifts by one lane: lane i reads lane i - 1 (wave_shr:1) or
+// lane i + 1 (wave_shl:1); a lane whose source is outside the wave reads 0.
+__device__ __forceinline__ int from_lane_below(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, 0x138, 0xF, 0xF, true);
+}
+__device__ __forceinline__ int from_lane_above(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, 0x130, 0xF, 0xF, true);
+}
+
 __device__ __forceinline__ RowEntries row_entries(int t, int i, const Geom &gm) {
   const int lane = threadIdx.x & 63;
   RowEntries e;
@@ -75,16 +84,17 @@ __device__ __forceinline__ RowEntries row_entries(int t, int i, const Geom &gm) 
   const bool valid = in_range && !(e.band_ok && t >= a_blk);
   const int tc = valid ? t / per : -1;
   const unsigned qb = valid ? ((1u << qpb) - 1u) << ((t % per) * qpb) : 0u;
-  const int prev = __shfl_up(tc, 1, 64);
+  const int prev = from_lane_below(tc);
   const bool first = valid && (lane == 0 || prev != tc);
   const uint64_t heads = __ballot(first);
   e.pos = __popcll(heads & ((1ull << lane) - 1ull));
   e.n = __popcll(heads);
   unsigned acc = qb;
+  int oq = (int)qb, otc = tc;  // the values of lane + dd
   for (int dd = 1; dd < per; ++dd) {
-    const unsigned o = __shfl_down(qb, dd, 64);
-    const int otc = __shfl_down(tc, dd, 64);
-    if (lane + dd < 64 && otc == tc) acc |= o;
+    oq = from_lane_above(oq);
+    otc = from_lane_above(otc);
+    if (lane + dd < 64 && otc == tc) acc |= (unsigned)oq;
   }
   e.mine = first && e.pos < gm.ksel - gm.band;
   e.tile = tc;
