@@ -21,6 +21,19 @@
 
 namespace phsa {
 
+// Maximum over the 16 lanes of a row, every lane getting it: DPP moves inside
+// the row (lane ^ 1, lane ^ 2, then the mirrored half row and row), no LDS.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float a) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float row_max16(float v) {
+  v = fmaxf(v, dpp_move<0xB1>(v));   // quad_perm [1, 0, 3, 2]
+  v = fmaxf(v, dpp_move<0x4E>(v));   // quad_perm [2, 3, 0, 1]
+  v = fmaxf(v, dpp_move<0x141>(v));  // row_half_mirror
+  return fmaxf(v, dpp_move<0x140>(v));  // row_mirror
+}
+
 __device__ __forceinline__ bool beats(float s1, int t1, float s2, int t2) {
   return s1 > s2 || (s1 == s2 && t1 < t2);
 }
@@ -586,7 +599,7 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
       float best = -INFINITY;
       if (c1 >= k) best = top1[u];
       if (c2 >= k) best = fmaxf(best, top2[u]);
-      best = max16(best);
+      best = row_max16(best);
       if (lane_tok && l16 == 0) bar_s[tok0 + u] = best;
     }
     __syncthreads();
@@ -873,7 +886,7 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
     stage(false);
     __syncthreads();
     // the chunk's largest representative norm, then each row's margin
-    const float mx = max16(fmaxf(fmaxf(mnp[0], mnp[1]), fmaxf(mnp[2], mnp[3])));
+    const float mx = row_max16(fmaxf(fmaxf(mnp[0], mnp[1]), fmaxf(mnp[2], mnp[3])));
     if (t0 + CH < t_end) fetch(t0 + CH, false);
     f32x4 acc[RT][4];
 #pragma unroll
@@ -934,7 +947,7 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
     float best = -INFINITY;
     if (c1 >= k) best = top1[rr];
     if (c2 >= k) best = fmaxf(best, top2[rr]);
-    thr[rr] = max16(best);
+    thr[rr] = row_max16(best);
     cnt[rr] = 0;
   }
   wave_lds_sync();
@@ -970,7 +983,7 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
       pos += __popcll(m);
     }
     wave_lds_sync();
-    thr[rr] = max16(kth);
+    thr[rr] = row_max16(kth);
     cnt[rr] = k;
   };
 
