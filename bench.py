@@ -7,15 +7,18 @@ top-k selection, the inverted index, sparse attention forward and backward.
 Inputs are seeded synthetic tensors already resident in HBM.
 
 The JSON line reports whole-step selected-block TFLOP/s (4*d*m FLOPs per
-(query row, head, selected block) forward, 2.5x that backward), per-kernel
-times from HIP events recorded on the launch stream inside the timed region,
-the roofline of the dominant kernel, a decode-step measurement, and the fp64
-CPU oracle timed on a bounded sample of the same workload.
+(query row, head, selected block) forward, 2.5x that backward) from the timed
+steps (HIP events around each step give its median and p90), the GPU clocks
+sampled while they run, per-kernel durations from a second timed pass through
+the profiling build of the library (HIP events around every launch on its
+stream), the roofline of the dominant kernel, a decode-step measurement, and
+the fp64 CPU oracle timed on one (batch, KV head) slice of the same workload.
 """
 from __future__ import annotations
 
 import argparse
 import dataclasses
+import glob
 import json
 import os
 import sys
@@ -118,13 +121,42 @@ def selected_blocks(sel: torch.Tensor, seqlen_k: int, block: int) -> int:
     return int(((sel >= 0) & (sel <= cur)).sum().item())
 
 
-def kernel_stats(names):
+def dist(xs):
+    """avg / median / p90 of a list of durations (ms)."""
+    a = np.asarray(xs, dtype=np.float64)
+    return {"avg_ms": float(a.mean()), "median_ms": float(np.median(a)), "p90_ms": float(np.percentile(a, 90)),
+            "launches": int(a.size)}
+
+
+def kernel_stats(times, names, steps):
     out = {}
     for n in names:
-        ms, cnt = phsa.timing_collect(n)
-        if cnt:
-            out[n] = {"total_ms": ms, "launches": cnt, "avg_ms": ms / cnt}
+        d = times.durations(n)
+        if d:
+            out[n] = dist(d)
+            out[n]["total_ms"] = float(np.sum(d))
+            out[n]["per_step"] = len(d) / steps
     return out
+
+
+def gpu_clocks():
+    """Current shader (sclk) and memory (mclk) clock levels of the GPU, read from
+    the amdgpu driver's sysfs files (no process is started: reading a file is
+    safe once the GPU is in use)."""
+    try:
+        pr = torch.cuda.get_device_properties(0)
+        dev = "/sys/bus/pci/devices/%04x:%02x:%02x.0" % (pr.pci_domain_id, pr.pci_bus_id, pr.pci_device_id)
+        if not os.path.isdir(dev):
+            cands = glob.glob("/sys/class/drm/card*/device")
+            dev = cands[0] if len(cands) == 1 else dev
+        out = {"sysfs": dev}
+        for key in ("pp_dpm_sclk", "pp_dpm_mclk"):
+            with open(os.path.join(dev, key)) as f:
+                cur = [ln.split(":", 1)[1].replace("*", "").strip() for ln in f if ln.rstrip().endswith("*")]
+            out[key[-4:]] = cur[0] if cur else None
+        return out
+    except Exception as e:  # no GPU, no sysfs files, another driver
+        return {"unavailable": type(e).__name__}
 
 
 KERNELS = ["phsa_compress", "phsa_select_split", "phsa_select", "phsa_index_count", "phsa_index_scan_tiles", "phsa_index_scan_lists",
@@ -191,18 +223,28 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
     else:
         sparse_sel, nband = sel, 0
     ntile = selected_tiles(sparse_sel, L, m)  # the sparse kernels' tiles
-    phsa.timing_reset()
-    phsa.timing_enable(True)
+    # headline: `steps` steps of the product library, one HIP event between steps
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(steps):
+    evs[0].record()
+    for i in range(steps):
         step()
+        evs[i + 1].record()
+    clocks = gpu_clocks()   # sampled while the enqueued steps run
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    phsa.timing_enable(False)
-    ks = kernel_stats(KERNELS)
-    phsa.timing_reset()
     ms_step = (t1 - t0) * 1e3 / steps
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+    # per-kernel durations: the same steps again through the profiling build,
+    # which records HIP events around every launch on the launch stream
+    prof_steps = max(steps, 50)
+    with phsa.profiling() as times:
+        for _ in range(prof_steps):
+            step()
+        torch.cuda.synchronize()
+        ks = kernel_stats(times, KERNELS, prof_steps)
+        times.reset()
 
     fwd_flop = 4.0 * d * m * nsel * G
     bwd_flop = 2.5 * fwd_flop
@@ -252,6 +294,9 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
     dom = max(ks, key=lambda n: ks[n]["total_ms"])
     return {
         "ms_per_step": ms_step,
+        "step_ms": {k: v for k, v in dist(step_ms).items() if k != "launches"},
+        "gpu_clocks": clocks,
+        "kernel_timing": f"{prof_steps} steps through libphsa_prof.so (HIP events around each launch)",
         "value": (fwd_flop + bwd_flop) / 1e12 / (ms_step / 1e3),
         "fwd_flop": fwd_flop, "bwd_flop": bwd_flop, "selected_blocks": nsel, "band_blocks": nband,
         "sparse_tiles": ntile,
@@ -388,44 +433,49 @@ def bench_select_modes(seed: int):
     return out
 
 
-def cpu_baseline(host, wl, prefix: int):
-    """The fp64 oracle on a causal prefix of batch 0 (all heads): a complete PHSA
-    sub-problem, timed end to end (compress, select, forward, backward)."""
+def cpu_baseline(host, wl, total_blocks: int, b: int = 0, g: int = 0):
+    """The fp64 oracle, end to end (compress, select, forward, backward), on one
+    (batch, KV head) slice of the workload: batch b, KV head g and its G query
+    heads, all query rows.  PHSA is independent per (batch, KV head) and every
+    slice has the same shape, so this is a complete sub-problem; the time of the
+    whole workload is extrapolated by the ratio of selected-block FLOPs
+    (total_blocks: the workload's selected (row, group, block) count)."""
     import oracle
 
     oracle.build()
-    q = host["q"][:1, :prefix].float().numpy()
-    k = host["k"][:1, :prefix].float().numpy()
-    v = host["v"][:1, :prefix].float().numpy()
-    do = host["do"][:1, :prefix].float().numpy()
-    punct = host["punct"][:1, :prefix].numpy()
-    d, m = wl.head_dim, wl.block_size
+    G = wl.n_heads_q // wl.n_heads_kv
+    q = host["q"][b:b + 1, :, g * G:(g + 1) * G].float().numpy()
+    k = host["k"][b:b + 1, :, g:g + 1].float().numpy()
+    v = host["v"][b:b + 1, :, g:g + 1].float().numpy()
+    do = host["do"][b:b + 1, :, g * G:(g + 1) * G].float().numpy()
+    punct = host["punct"][b:b + 1].numpy()
+    d, m, L = wl.head_dim, wl.block_size, wl.seqlen_k
     scale = d ** -0.5
+    threads = oracle.num_threads()
     t0 = time.perf_counter()
     kc = oracle.compress(k, punct, m, wl.lam)
-    sel, _, _ = oracle.select(q, kc, m, wl.top_k, wl.n_init_blocks, wl.window, scale, prefix)
+    sel, _, _ = oracle.select(q, kc, m, wl.top_k, wl.n_init_blocks, wl.window, scale, L)
     oracle.attn_fwd(q, k, v, sel, m, scale)
     oracle.attn_bwd(q, k, v, do, sel, m, scale)
     dt = time.perf_counter() - t0
-    cur = (np.arange(prefix) // m)[None, None, :, None]
+    cur = (np.arange(L) // m)[None, None, :, None]
     nsel = int(((sel >= 0) & (sel <= cur)).sum())
-    G = wl.n_heads_q // wl.n_heads_kv
     flop = 4.0 * d * m * nsel * G * 3.5
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    full = dt * total_blocks / nsel
     return {"value": flop / 1e12 / dt, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "seconds": dt,
-            "sample": f"batch 0, query/key tokens 0..{prefix - 1} (a causal prefix, a complete PHSA sub-problem) "
-                      f"of the 4x32768 training workload, all 16/8 heads; fp64 compress+select+forward+backward; "
-                      f"FLOPs counted with the same selected-block convention"}
+            "seconds": dt, "extrapolated_full_seconds": full,
+            "sample": f"batch {b}, KV head {g} with its {G} query heads, all {L} query rows of the "
+                      f"{wl.batch}x{L} training workload: 1 of its {wl.batch * wl.n_heads_kv} independent "
+                      f"(batch, KV head) slices, fp64 compress+select+forward+backward; the full workload's "
+                      f"time is extrapolated by the selected-block FLOP ratio ({total_blocks / nsel:.2f}x)"}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-prefix", type=int, default=8192)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-paper-geometry", action="store_true")
@@ -475,7 +525,7 @@ def main():
     roofline = {"bound": "mfma" if dk.get("unit") == "TFLOP/s" else "hbm", "kernel": dom,
                 "achieved": dk.get("rate"), "peak": PEAK_BF16_TFLOPS if dk.get("unit") == "TFLOP/s" else PEAK_HBM_GBS,
                 "unit": dk.get("unit"), "frac": dk.get("frac"), "traffic": traffic,
-                "avg_ms": dk["avg_ms"]}
+                "avg_ms": dk["avg_ms"], "median_ms": dk["median_ms"], "p90_ms": dk["p90_ms"]}
     for key in ("schedule_bytes", "attainable_tflops", "frac_of_attainable"):
         if key in dk:
             roofline[key] = dk[key]
@@ -483,6 +533,7 @@ def main():
         "metric": METRIC, "value": tr["value"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": tr["ms_per_step"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "step_ms": tr["step_ms"], "gpu_clocks": tr["gpu_clocks"],
         "config": {"workload": TRAIN_TEXT[args.train_workload],
                    "batch": wl0.batch, "seq_len": wl0.seqlen_k, "heads_q": wl0.n_heads_q, "heads_kv": wl0.n_heads_kv,
                    "head_dim": wl0.head_dim, "block": wl0.block_size,
@@ -491,6 +542,7 @@ def main():
         "selected_block_gflop": {"fwd": tr["fwd_flop"] / 1e9, "bwd": tr["bwd_flop"] / 1e9},
         "frac_mfma_peak_step": tr["value"] / PEAK_BF16_TFLOPS,
         "roofline": roofline,
+        "kernel_timing": tr["kernel_timing"],
         "kernels": tr["kernels"],
     }
     host0 = tr.pop("host")
@@ -507,7 +559,7 @@ def main():
         result["punct_mask"] = bench_punct(args.seed)
         result["select_modes"] = bench_select_modes(args.seed)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(host0, wl0, args.cpu_prefix)
+        result["cpu_baseline"] = cpu_baseline(host0, wl0, tr["selected_blocks"])
     print(json.dumps(result))
 
 

@@ -39,12 +39,19 @@
  *     failed launch; faults inside kernels surface at the caller's next
  *     synchronisation of the stream.
  *   - No C++ exception crosses this interface.
+ *   - The library keeps no mutable global state: calls are reentrant, and
+ *     calls on different streams with separate workspaces are independent.
  */
 #ifndef PHSA_H
 #define PHSA_H
 
 #include <stddef.h>
 #include <stdint.h>
+
+/* Symbols of the C ABI; the library exports nothing else. */
+#ifndef PHSA_API
+#define PHSA_API __attribute__((visibility("default")))
+#endif
 
 #ifdef __cplusplus
 extern "C" {
@@ -113,17 +120,19 @@ typedef enum {
   PHSA_FLAG_SELECT_SOFTMAX_SUM = 2
 } phsa_flag;
 
-/* Number of index slots per (query row, KV head): n_init + w/m + 1 + top_k. */
-int32_t phsa_ksel(const phsa_params *p);
+/* Number of index slots per (query row, KV head): n_init + w/m + 1 + top_k;
+ * 0 when p is NULL, block_size < 1, a count is negative or the sum exceeds
+ * INT32_MAX. */
+PHSA_API int32_t phsa_ksel(const phsa_params *p);
 
 /* Host-only validation of `p` for operation `op` (no GPU access). */
-phsa_status phsa_validate(const phsa_params *p, int32_t op);
+PHSA_API phsa_status phsa_validate(const phsa_params *p, int32_t op);
 
 /* Workspace bytes `op` needs for `p` (0 if none, or if `p` is invalid). */
-size_t phsa_workspace_size(const phsa_params *p, int32_t op);
+PHSA_API size_t phsa_workspace_size(const phsa_params *p, int32_t op);
 
 /* Static, human-readable name of a status code. */
-const char *phsa_status_string(phsa_status s);
+PHSA_API const char *phsa_status_string(phsa_status s);
 
 /* Punctuation mask from token ids: mask[i] = 1 if ids[i] is one of the
  * punctuation ids, else 0 (the indicator I(x_i in P) of Eq. 7, Section 3.2
@@ -134,13 +143,13 @@ const char *phsa_status_string(phsa_status s);
  * PHSA_MAX_PUNCT_IDS (PHSA_ERR_UNSUPPORTED beyond).  Building P from a
  * tokenizer's vocabulary is the caller's part. */
 #define PHSA_MAX_PUNCT_IDS 16384
-phsa_status phsa_punct_mask(const int32_t *ids, int64_t n_tokens, const int32_t *punct_ids, int32_t n_punct,
+PHSA_API phsa_status phsa_punct_mask(const int32_t *ids, int64_t n_tokens, const int32_t *punct_ids, int32_t n_punct,
                             uint8_t *mask, void *stream);
 
 /* Block representatives (Eq. 6-8, Algorithm 1 representative-token step).
  * Reads K [B, Lk, Hkv, d] and punct [B, Lk]; writes K_comp [B, Hkv, T, d]
  * (float32, sums accumulated in float32).  Uses seqlen_k, not seqlen_q. */
-phsa_status phsa_compress(const phsa_params *p, const void *K, const uint8_t *punct, float *K_comp,
+PHSA_API phsa_status phsa_compress(const phsa_params *p, const void *K, const uint8_t *punct, float *K_comp,
                           void *stream);
 
 /* Relevance scoring and block selection (Eq. 8, Algorithm 1 scoring and
@@ -148,14 +157,14 @@ phsa_status phsa_compress(const phsa_params *p, const void *K, const uint8_t *pu
  * are computed in float32 from float32 K_comp.  The bf16 path needs
  * phsa_workspace_size(p, PHSA_OP_SELECT) bytes of workspace (split copies of
  * K_comp); the float32 path needs none (ws may then be NULL). */
-phsa_status phsa_select(const phsa_params *p, const void *Q, const float *K_comp, int32_t *sel,
+PHSA_API phsa_status phsa_select(const phsa_params *p, const void *Q, const float *K_comp, int32_t *sel,
                         void *ws, size_t ws_bytes, void *stream);
 
 /* Sparse attention forward (Eq. 10-11, Algorithm 1 attention step) over the
  * blocks listed in sel, with the token-level causal mask j <= position(i).
  * Writes O [B, Lq, Hq, d] (dtype) and LSE [B, Hq, Lq].  sel rows must be
  * ascending, duplicate-free, within 0..cur of their row, and -1 padded. */
-phsa_status phsa_attn_fwd(const phsa_params *p, const void *Q, const void *K, const void *V,
+PHSA_API phsa_status phsa_attn_fwd(const phsa_params *p, const void *Q, const void *K, const void *V,
                           const int32_t *sel, void *O, float *LSE, void *ws, size_t ws_bytes,
                           void *stream);
 
@@ -164,13 +173,13 @@ phsa_status phsa_attn_fwd(const phsa_params *p, const void *Q, const void *K, co
  * forward tensors, dO and LSE; writes dQ [B, Lq, Hq, d] and dK, dV
  * [B, Lk, Hkv, d] (dtype; float32 accumulation).  dK/dV sum over the heads
  * of each group; keys that no query selected get zero gradient. */
-phsa_status phsa_attn_bwd(const phsa_params *p, const void *Q, const void *K, const void *V,
+PHSA_API phsa_status phsa_attn_bwd(const phsa_params *p, const void *Q, const void *K, const void *V,
                           const void *O, const void *dO, const float *LSE, const int32_t *sel,
                           void *dQ, void *dK, void *dV, void *ws, size_t ws_bytes, void *stream);
 
 /* Whole forward: phsa_compress, phsa_select, phsa_attn_fwd in one call.
  * Writes K_comp, sel, O and LSE. */
-phsa_status phsa_forward(const phsa_params *p, const void *Q, const void *K, const void *V,
+PHSA_API phsa_status phsa_forward(const phsa_params *p, const void *Q, const void *K, const void *V,
                          const uint8_t *punct, float *K_comp, int32_t *sel, void *O, float *LSE,
                          void *ws, size_t ws_bytes, void *stream);
 
@@ -178,7 +187,7 @@ phsa_status phsa_forward(const phsa_params *p, const void *Q, const void *K, con
  * query sits at position Lk - 1.  K_comp [B, Hkv, T, d] holds the cache's
  * block representatives (from phsa_compress).  Writes sel [B, Hkv, 1, Ksel],
  * O [B, 1, Hq, d] and LSE [B, Hq, 1]. */
-phsa_status phsa_decode(const phsa_params *p, const void *Q, const void *K_cache,
+PHSA_API phsa_status phsa_decode(const phsa_params *p, const void *Q, const void *K_cache,
                         const void *V_cache, const float *K_comp, int32_t *sel, void *O,
                         float *LSE, void *ws, size_t ws_bytes, void *stream);
 
@@ -202,23 +211,13 @@ phsa_status phsa_decode(const phsa_params *p, const void *Q, const void *K_cache
  * masked without their values being read.  Only complete blocks are scored,
  * so K_comp must hold the representatives of every complete block below the
  * query's own (phsa_compress on the prefilled prefix, then phsa_cache_append). */
-phsa_status phsa_decode_varlen(const phsa_params *p, const void *Q, const void *K_cache,
+PHSA_API phsa_status phsa_decode_varlen(const phsa_params *p, const void *Q, const void *K_cache,
                                const void *V_cache, const float *K_comp, const int32_t *cache_len,
                                int32_t *sel, void *O, float *LSE, void *ws, size_t ws_bytes,
                                void *stream);
-phsa_status phsa_cache_append(const phsa_params *p, const void *K_new, const void *V_new,
+PHSA_API phsa_status phsa_cache_append(const phsa_params *p, const void *K_new, const void *V_new,
                               const uint8_t *punct_new, void *K_cache, void *V_cache,
                               uint8_t *punct_cache, int32_t *cache_len, float *K_comp, void *stream);
-
-/* Profiling aid (off by default, not thread-safe): while enabled, every
- * kernel launch is bracketed by a pair of HIP events on its stream.
- * phsa_timing_collect synchronises those events and returns, for the kernel
- * named `name`, the summed duration in milliseconds and the launch count;
- * it returns the number of distinct kernel names recorded.  phsa_timing_reset
- * drops every record.  Event objects are created on first enable. */
-phsa_status phsa_timing_enable(int32_t enable);
-int32_t phsa_timing_collect(const char *name, double *total_ms, int64_t *count);
-void phsa_timing_reset(void);
 
 #ifdef __cplusplus
 }

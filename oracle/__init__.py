@@ -47,8 +47,12 @@ def build(force: bool = False) -> str:
 def _load():
     global _lib
     if _lib is None:
-        build()
-        _lib = ctypes.CDLL(_LIB_PATH)
+        # PHSA_ORACLE_LIB: a prebuilt copy of this library to load instead (the
+        # host-sanitizer test builds one with AddressSanitizer and UBSan)
+        path = os.environ.get("PHSA_ORACLE_LIB")
+        if not path:
+            path = build()
+        _lib = ctypes.CDLL(path)
         I, D, L, P = ctypes.c_int, ctypes.c_double, ctypes.c_int64, ctypes.c_void_p
         _lib.oracle_compress.argtypes = [I, I, I, I, I, D, P, P, P]
         _lib.oracle_punct_mask.argtypes = [L, P, ctypes.c_int32, P, P]
@@ -56,6 +60,8 @@ def _load():
         _lib.oracle_score_row.argtypes = [I] * 7 + [D, P, P, I, I, I, I, I, P]
         _lib.oracle_attn_fwd.argtypes = [I] * 9 + [D, P, P, P, P, L, P, P, P]
         _lib.oracle_attn_bwd.argtypes = [I] * 9 + [D, P, P, P, P, P, L, P, P, L, P, P, P]
+        _lib.oracle_num_threads.argtypes = []
+        _lib.oracle_num_threads.restype = ctypes.c_int
         for f in ("oracle_compress", "oracle_select", "oracle_score_row", "oracle_attn_fwd", "oracle_attn_bwd",
                   "oracle_punct_mask"):
             getattr(_lib, f).restype = None
@@ -78,6 +84,11 @@ def _rows_arg(rows, total):
         return total, None
     r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
     return int(r.size), r
+
+
+def num_threads() -> int:
+    """Threads the oracle's OpenMP loops run on."""
+    return int(_load().oracle_num_threads())
 
 
 def ksel(block_size: int, top_k: int, n_init: int, window: int) -> int:

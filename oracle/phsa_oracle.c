@@ -21,9 +21,22 @@
  * Query head h reads key/value head g = h / (Hq / Hkv).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* Number of threads the oracle's parallel loops run on (as timed by the
+ * benchmark's CPU baseline). */
+int oracle_num_threads(void) {
+  int n = 1;
+#pragma omp parallel
+  {
+#pragma omp single
+    n = omp_get_num_threads();
+  }
+  return n;
+}
 
 #define IDX4(a, b, c, d_, B_, C_, D_) ((((int64_t)(a) * (B_) + (b)) * (C_) + (c)) * (D_) + (d_))
 

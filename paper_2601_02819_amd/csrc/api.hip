@@ -5,7 +5,6 @@
 
 #include <algorithm>
 #include <exception>
-#include <vector>
 
 #include "../../include/phsa.h"
 #include "launch.h"
@@ -158,6 +157,17 @@ size_t bwd_layout(const Geom &g0, char *base, BwdWs *ws) {
 
 size_t decode_layout(const Geom &) { return 0; }  // the decode kernels need no scratch
 
+}  // namespace
+
+// bf16 selection scratch, as launch_select carves it: K_comp split into bf16 hi
+// and lo [B, Hkv, T, d] each, then one float32 norm per block.
+size_t select_split_bytes(const Geom &g) {
+  const size_t nblk = (size_t)g.B * g.Hkv * g.T;
+  return g.dtype == PHSA_BF16 ? nblk * (2 * g.d * sizeof(uint16_t) + sizeof(float)) : 0;
+}
+
+namespace {
+
 bool is_attention_op(int op) {
   return op == PHSA_OP_ATTN_FWD || op == PHSA_OP_ATTN_BWD || op == PHSA_OP_FORWARD || op == PHSA_OP_DECODE;
 }
@@ -259,37 +269,13 @@ hipError_t attn_fwd_bf16(const Geom &g, const void *Q, const void *K, const void
   return launch_attn_fwd(w.co.gc, Q, K, V, sel, O, LSE, w.ix, w.opart, w.ml, s);
 }
 
-// ---------------------------------------------------------------- timing
-struct TimingRec {
-  const char *name;
-  hipEvent_t a, b;
-};
-bool g_timing = false;
-std::vector<TimingRec> g_recs;
-std::vector<std::pair<hipEvent_t, hipEvent_t>> g_pool;
-TimingRec g_open{nullptr, nullptr, nullptr};
-
 }  // namespace
 
-void timing_begin(const char *name, hipStream_t s) {
-  if (!g_timing) return;
-  std::pair<hipEvent_t, hipEvent_t> ev{nullptr, nullptr};
-  if (!g_pool.empty()) {
-    ev = g_pool.back();
-    g_pool.pop_back();
-  } else if (hipEventCreate(&ev.first) != hipSuccess || hipEventCreate(&ev.second) != hipSuccess) {
-    return;
-  }
-  g_open = TimingRec{name, ev.first, ev.second};
-  (void)hipEventRecord(ev.first, s);
-}
-
-void timing_end(hipStream_t s) {
-  if (!g_timing || !g_open.name) return;
-  (void)hipEventRecord(g_open.b, s);
-  g_recs.push_back(g_open);
-  g_open = TimingRec{nullptr, nullptr, nullptr};
-}
+// Launch hooks around every kernel (launch.h).  This library defines them
+// empty and keeps no state; the profiling build (libphsa_prof.so, see
+// include/phsa_prof.h) links definitions that record HIP events instead.
+__attribute__((weak, noinline)) void timing_begin(const char *, hipStream_t) {}
+__attribute__((weak, noinline)) void timing_end(hipStream_t) {}
 
 }  // namespace phsa
 
@@ -307,8 +293,9 @@ using namespace phsa;
 extern "C" {
 
 int32_t phsa_ksel(const phsa_params *p) {
-  if (!p || p->block_size < 1) return 0;
-  return p->n_init_blocks + p->window / p->block_size + 1 + p->top_k;
+  if (!p || p->block_size < 1 || p->n_init_blocks < 0 || p->window < 0 || p->top_k < 0) return 0;
+  const int64_t k = (int64_t)p->n_init_blocks + p->window / p->block_size + 1 + p->top_k;
+  return k > INT32_MAX ? 0 : (int32_t)k;
 }
 
 phsa_status phsa_validate(const phsa_params *p, int32_t op) { return validate(p, op, nullptr); }
@@ -320,7 +307,10 @@ size_t phsa_workspace_size(const phsa_params *p, int32_t op) {
 }
 
 const char *phsa_status_string(phsa_status s) {
-  switch (s) {
+  // a C caller may pass any int: read the bits as one, not as the enum
+  int v;
+  memcpy(&v, &s, sizeof v);
+  switch (v) {
     case PHSA_OK: return "ok";
     case PHSA_ERR_INVALID_ARG: return "invalid argument";
     case PHSA_ERR_SHAPE: return "inconsistent shape";
@@ -350,6 +340,7 @@ phsa_status phsa_punct_mask(const int32_t *ids, int64_t n_tokens, const int32_t 
     if (n_punct > PHSA_MAX_PUNCT_IDS) return PHSA_ERR_UNSUPPORTED;
     if (n_tokens > 0 && (!ids || !mask)) return PHSA_ERR_NULL;
     if (n_punct > 0 && !punct_ids) return PHSA_ERR_NULL;
+    if (n_tokens == 0) return PHSA_OK;  // nothing to do, nothing launched
     return from_hip(launch_punct_mask(ids, n_tokens, punct_ids, n_punct, mask, static_cast<hipStream_t>(stream)));
   })
 }
@@ -464,37 +455,6 @@ phsa_status phsa_cache_append(const phsa_params *p, const void *K_new, const voi
     return from_hip(launch_cache_append(g, K_new, V_new, punct_new, K_cache, V_cache, punct_cache, cache_len, K_comp,
                                         static_cast<hipStream_t>(stream)));
   })
-}
-
-phsa_status phsa_timing_enable(int32_t enable) {
-  g_timing = enable != 0;
-  return PHSA_OK;
-}
-
-int32_t phsa_timing_collect(const char *name, double *total_ms, int64_t *count) {
-  double tot = 0.0;
-  int64_t n = 0;
-  std::vector<const char *> names;
-  for (const TimingRec &r : g_recs) {
-    bool seen = false;
-    for (const char *x : names) seen = seen || strcmp(x, r.name) == 0;
-    if (!seen) names.push_back(r.name);
-    if (name && strcmp(name, r.name) == 0) {
-      float ms = 0.f;
-      if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
-        tot += ms;
-        ++n;
-      }
-    }
-  }
-  if (total_ms) *total_ms = tot;
-  if (count) *count = n;
-  return (int32_t)names.size();
-}
-
-void phsa_timing_reset(void) {
-  for (const TimingRec &r : g_recs) g_pool.emplace_back(r.a, r.b);
-  g_recs.clear();
 }
 
 }  // extern "C"

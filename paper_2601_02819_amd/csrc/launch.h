@@ -43,7 +43,9 @@ struct IndexWs {
 
 constexpr int kIndexTile = 256;  // query rows per index-building workgroup
 
-// Kernel timing hooks (no-ops unless phsa_timing_enable(1)).
+// Hooks around every kernel launch, given the kernel's profiling name.  The
+// library defines them empty (api.hip); the profiling build links definitions
+// that bracket the launch with HIP events on its stream (prof/kernel_timing.hip).
 void timing_begin(const char *name, hipStream_t s);
 void timing_end(hipStream_t s);
 

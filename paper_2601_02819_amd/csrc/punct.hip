@@ -47,7 +47,6 @@ __global__ __launch_bounds__(256) void punct_mask_kernel(const int32_t *__restri
 
 hipError_t launch_punct_mask(const int32_t *ids, int64_t n, const int32_t *pset, int n_punct, uint8_t *mask,
                              hipStream_t s) {
-  if (n == 0) return hipSuccess;
   const int64_t groups = (n + 1023) / 1024;
   const unsigned grid = (unsigned)(groups < 4096 ? groups : 4096);
   timing_begin("phsa_punct_mask", s);

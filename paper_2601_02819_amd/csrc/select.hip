@@ -1164,11 +1164,6 @@ static hipError_t launch_select_mfma_d(const Geom &g, const void *Q, const float
   }
 }
 
-size_t select_split_bytes(const Geom &g) {
-  const size_t nblk = (size_t)g.B * g.Hkv * g.T;
-  return g.dtype == 0 ? nblk * (2 * g.d * sizeof(bf16_t) + sizeof(float)) : 0;
-}
-
 template <int D, int G>
 static hipError_t launch_select_softmax_mfma(const Geom &g, const void *Q, const float *Kc, int32_t *sel, char *ws,
                                              hipStream_t s) {

@@ -6,15 +6,17 @@ If the library has not been built this module raises; there is no fallback.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import dataclasses
 import os
-from typing import Optional, Tuple
+from typing import Dict, List, Optional, Tuple
 
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libphsa.so")
+PROF_LIB_PATH = os.path.join(_HERE, "libphsa_prof.so")   # profiling build (include/phsa_prof.h)
 
 OK, ERR_INVALID_ARG, ERR_SHAPE, ERR_DTYPE, ERR_NULL, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP = range(8)
 BF16, FP32 = 0, 1
@@ -28,8 +30,8 @@ EXPORTS = (
     "phsa_ksel", "phsa_validate", "phsa_workspace_size", "phsa_status_string", "phsa_punct_mask", "phsa_compress",
     "phsa_select", "phsa_attn_fwd", "phsa_attn_bwd", "phsa_forward", "phsa_decode", "phsa_decode_varlen",
     "phsa_cache_append",
-    "phsa_timing_enable", "phsa_timing_collect", "phsa_timing_reset",
 )
+PROF_EXPORTS = ("phsa_prof_enable", "phsa_prof_durations", "phsa_prof_reset")
 
 
 class Params(ctypes.Structure):
@@ -48,16 +50,15 @@ class PHSAError(RuntimeError):
         self.status = status
 
 
-_lib = None
+_libs: Dict[str, ctypes.CDLL] = {}
+_active: Optional[ctypes.CDLL] = None   # the library the calls below go to (libphsa.so unless profiling)
 
 
-def lib():
-    """Load libphsa.so (raises if it has not been built)."""
-    global _lib
-    if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2601_02819_amd.build`")
-        L = ctypes.CDLL(LIB_PATH)
+def _load(path: str) -> ctypes.CDLL:
+    if path not in _libs:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with `python -m paper_2601_02819_amd.build`")
+        L = ctypes.CDLL(path)
         P, PP = ctypes.POINTER(Params), ctypes.c_void_p
         sig = {
             "phsa_ksel": (ctypes.c_int32, [P]),
@@ -73,17 +74,63 @@ def lib():
             "phsa_decode": (ctypes.c_int, [P] + [PP] * 8 + [ctypes.c_size_t, PP]),
             "phsa_decode_varlen": (ctypes.c_int, [P] + [PP] * 9 + [ctypes.c_size_t, PP]),
             "phsa_cache_append": (ctypes.c_int, [P] + [PP] * 8 + [PP]),
-            "phsa_timing_enable": (ctypes.c_int, [ctypes.c_int32]),
-            "phsa_timing_collect": (ctypes.c_int32, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
-                                                     ctypes.POINTER(ctypes.c_int64)]),
-            "phsa_timing_reset": (None, []),
         }
+        if path == PROF_LIB_PATH:
+            sig.update({
+                "phsa_prof_enable": (ctypes.c_int, [ctypes.c_int32]),
+                "phsa_prof_durations": (ctypes.c_int32, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_float),
+                                                         ctypes.c_int32]),
+                "phsa_prof_reset": (None, []),
+            })
         for name, (res, args) in sig.items():
             f = getattr(L, name)
             f.restype = res
             f.argtypes = args
-        _lib = L
-    return _lib
+        _libs[path] = L
+    return _libs[path]
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libphsa.so (raises if it has not been built)."""
+    global _active
+    if _active is None:
+        _active = _load(LIB_PATH)
+    return _active
+
+
+class KernelTimes:
+    """Per-launch kernel durations read from the profiling build."""
+
+    def __init__(self, L: ctypes.CDLL):
+        self._L = L
+
+    def durations(self, name: str) -> List[float]:
+        """Milliseconds of every recorded launch of kernel `name`, in launch order."""
+        n = self._L.phsa_prof_durations(name.encode(), None, 0)
+        buf = (ctypes.c_float * max(n, 1))()
+        n = self._L.phsa_prof_durations(name.encode(), buf, n)
+        return [float(buf[i]) for i in range(n)]
+
+    def reset(self) -> None:
+        self._L.phsa_prof_reset()
+
+
+@contextlib.contextmanager
+def profiling():
+    """Routes the calls of this module to libphsa_prof.so, which records a pair
+    of HIP events around each kernel launch on its stream, and yields a
+    KernelTimes to read them.  The kernels are those of libphsa.so."""
+    global _active
+    prev = lib()
+    L = _load(PROF_LIB_PATH)
+    L.phsa_prof_reset()
+    L.phsa_prof_enable(1)
+    _active = L
+    try:
+        yield KernelTimes(L)
+    finally:
+        L.phsa_prof_enable(0)
+        _active = prev
 
 
 def status_string(status: int) -> str:
@@ -310,17 +357,3 @@ class SparseAttention(torch.autograd.Function):
         dq, dk, dv = attn_bwd(q, k, v, o, do.contiguous(), lse, sel, ctx.cfg, ctx.ws, reuse_index=ctx.ws is not None)
         ctx.ws = None
         return dq, dk, dv, None, None
-
-
-def timing_enable(on: bool = True) -> None:
-    lib().phsa_timing_enable(1 if on else 0)
-
-
-def timing_collect(name: str) -> Tuple[float, int]:
-    ms, n = ctypes.c_double(0.0), ctypes.c_int64(0)
-    lib().phsa_timing_collect(name.encode(), ctypes.byref(ms), ctypes.byref(n))
-    return ms.value, n.value
-
-
-def timing_reset() -> None:
-    lib().phsa_timing_reset()

@@ -60,3 +60,39 @@ def check_sel(gpu, ref, kth, gap, score_fn, tol=SEL_GAP_TOL):
 
 def oracle_inputs(host):
     return {k: (v.float().numpy() if v.dtype != torch.uint8 else v.numpy()) for k, v in host.items()}
+
+
+def shared_workspace(wl, cfg):
+    """One workspace for the forward and the backward, as the benchmark's step
+    uses it: the backward reuses the inverted index the forward built."""
+    p = phsa.make_params(cfg, wl.batch, wl.seqlen_q, wl.seqlen_k, wl.n_heads_q, wl.n_heads_kv, wl.head_dim,
+                         torch.bfloat16)
+    need = max(phsa.workspace_size(p, phsa.OP_FORWARD), phsa.workspace_size(p, phsa.OP_ATTN_BWD))
+    return torch.empty(need, dtype=torch.uint8, device="cuda")
+
+
+def check_grads_sampled(wl, h, sel_g, dq, dk, dv, rows, picks):
+    """dQ on sampled rows and dK/dV on sampled key blocks (b, g, t), each row and
+    each block held to the relative-L2 bar on its own."""
+    scale = wl.head_dim ** -0.5
+    L, m, T, Hkv = wl.seqlen_q, wl.block_size, wl.n_blocks, wl.n_heads_kv
+    bar = GRAD_REL_L2[wl.dtype]
+    dq_r, _, _ = oracle.attn_bwd(h["q"], h["k"], h["v"], h["do"], sel_g, m, scale, rows=rows, want_dkv=False)
+    dq_g = to_np(dq)[rows // L, rows % L]
+    # per row; a row whose exact dQ is (near) zero, such as row 0, which sees only
+    # its own key, is measured against a twentieth of the median row norm instead
+    norms = np.linalg.norm(dq_r.reshape(rows.size, -1), axis=1)
+    floor = 0.05 * float(np.median(norms))
+    e_rows = [float(np.linalg.norm(dq_g[j] - dq_r[j]) / max(norms[j], floor)) for j in range(rows.size)]
+    blocks = np.array([(b * Hkv + g) * T + t for b, g, t in picks], dtype=np.int64)
+    _, dk_r, dv_r = oracle.attn_bwd(h["q"], h["k"], h["v"], h["do"], sel_g, m, scale, blocks=blocks, want_dq=False)
+    dk_c, dv_c = to_np(dk), to_np(dv)
+    for j, (b, g, t) in enumerate(picks):
+        e_k = rel_l2(dk_c[b, t * m:(t + 1) * m, g], dk_r[j])
+        e_v = rel_l2(dv_c[b, t * m:(t + 1) * m, g], dv_r[j])
+        log(f"[grad] {wl.name}: block (b {b}, g {g}, t {t}) dK {e_k:.2e} dV {e_v:.2e}")
+        assert max(e_k, e_v) < bar, (b, g, t, e_k, e_v)
+    worst = int(np.argmax(e_rows))
+    log(f"[grad] {wl.name}: dQ rel-L2 over {rows.size} rows: max {e_rows[worst]:.2e} (row {rows[worst]}), "
+        f"pooled {rel_l2(dq_g, dq_r):.2e}")
+    assert e_rows[worst] < bar, (int(rows[worst]), e_rows[worst])

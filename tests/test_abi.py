@@ -3,6 +3,7 @@ declares, and rejects bad arguments on the host before anything is launched."""
 import ctypes
 import os
 import re
+import subprocess
 
 import pytest
 import torch
@@ -11,22 +12,49 @@ from paper_2601_02819_amd import phsa
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "phsa.h")
+PROF_HEADER = os.path.join(ROOT, "include", "phsa_prof.h")
 
 
-def declared_functions():
-    text = open(HEADER).read()
+def declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(phsa_[a-z_]+)\s*\(", text)))
 
 
+def exported_c_functions(path):
+    """Unmangled function symbols in the dynamic symbol table of a library."""
+    out = subprocess.run(["nm", "-D", "--defined-only", path], capture_output=True, text=True, check=True).stdout
+    return sorted({f[2] for f in (ln.split() for ln in out.splitlines()) if len(f) == 3 and f[1] == "T"
+                   and not f[2].startswith("_")})
+
+
 def test_header_declares_the_binding_exports():
     assert declared_functions() == sorted(phsa.EXPORTS)
+    assert declared_functions(PROF_HEADER) == sorted(phsa.PROF_EXPORTS)
 
 
 def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(phsa.LIB_PATH)
     for name in declared_functions():
         assert hasattr(lib, name), name
+
+
+def test_library_exports_only_the_c_abi():
+    """libphsa.so exports exactly the calls of phsa.h (no profiling or timing
+    calls); the profiling build adds those of phsa_prof.h and nothing else."""
+    assert exported_c_functions(phsa.LIB_PATH) == declared_functions()
+    assert exported_c_functions(phsa.PROF_LIB_PATH) == sorted(declared_functions() + declared_functions(PROF_HEADER))
+
+
+def test_library_keeps_no_mutable_state():
+    """Every writable data symbol of the library's own namespace is a kernel
+    handle that the HIP runtime fills in when it registers the code object:
+    the ABI layer holds no namespace-scope state, so calls are reentrant."""
+    out = subprocess.run(["nm", "-C", phsa.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    data = [ln.split(" ", 2)[2] for ln in out.splitlines() if re.match(r"^[0-9a-f]+ [bBdD] ", ln)]
+    ours = [n for n in data if n.startswith("phsa::")]
+    assert ours, "expected the kernel handles"
+    assert all(re.match(r"phsa::\w+_kernel[<(]", n) for n in ours), [n for n in ours if "_kernel" not in n]
 
 
 def _p(**kw):
@@ -145,7 +173,8 @@ def test_status_strings():
 
 def test_missing_library_raises(monkeypatch):
     """No fallback: without the built library the binding raises instead of computing."""
-    monkeypatch.setattr(phsa, "_lib", None)
+    monkeypatch.setattr(phsa, "_active", None)
+    monkeypatch.setattr(phsa, "_libs", {})
     monkeypatch.setattr(phsa, "LIB_PATH", os.path.join(ROOT, "no_such_dir", "libphsa.so"))
     with pytest.raises(RuntimeError, match="missing"):
         phsa.lib()

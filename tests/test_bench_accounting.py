@@ -47,3 +47,23 @@ def test_sparse_tiles_exclude_band_blocks():
     # blocks 0 and 5 remain: tiles 0 and 1
     assert bench.selected_tiles(sparse, Lk, m) == 2
     assert bench.selected_tiles(sel, Lk, m) == 3  # tiles 0, 1, 2 with the window
+
+
+def test_cpu_baseline_times_one_slice_and_extrapolates():
+    """The CPU baseline runs the oracle on one (batch, KV head) slice, all rows,
+    reports the thread count the oracle ran on, and scales the slice's time to
+    the whole workload by the selected-block ratio."""
+    import oracle
+    from paper_2601_02819_amd.inputs import Workload, make_inputs
+
+    wl = Workload("tiny_train", 2, 512, 512, 4, 2, 64, 64, 3, 1, 0, "bf16", backward=True)
+    host = make_inputs(wl, seed=0, with_grad_out=True)
+    r = bench.cpu_baseline(host, wl, total_blocks=10_000)
+    assert r["kind"] == "oracle" and r["unit"] == "TFLOP/s"
+    assert r["cores"] == oracle.num_threads() >= 1
+    assert r["value"] > 0 and r["seconds"] > 0
+    assert "1 of its 4 independent (batch, KV head) slices" in r["sample"]
+    # the slice holds 512 rows x 1 group x (1 init + 1 local + 3 picks, fewer early)
+    nsel = r["extrapolated_full_seconds"] and 10_000 * r["seconds"] / r["extrapolated_full_seconds"]
+    assert 512 * 2 < nsel <= 512 * 5
+    assert bench.gpu_clocks().get("unavailable")        # no GPU here
