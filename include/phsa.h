@@ -65,7 +65,8 @@ typedef enum {
   PHSA_ERR_NULL = 4,        /* a required pointer is NULL */
   PHSA_ERR_WORKSPACE = 5,   /* ws_bytes < phsa_workspace_size(params, op) or ws is NULL */
   PHSA_ERR_UNSUPPORTED = 6, /* valid for the method but outside what the kernels implement */
-  PHSA_ERR_HIP = 7          /* a HIP launch failed */
+  PHSA_ERR_HIP = 7,         /* a HIP launch failed */
+  PHSA_ERR_SCRATCH_LIMIT = 8 /* needs more than the fixed scratch of a scratch-free entry point */
 } phsa_status;
 
 typedef enum { PHSA_BF16 = 0, PHSA_FP32 = 1 } phsa_dtype;
@@ -218,6 +219,27 @@ PHSA_API phsa_status phsa_decode_varlen(const phsa_params *p, const void *Q, con
 PHSA_API phsa_status phsa_cache_append(const phsa_params *p, const void *K_new, const void *V_new,
                               const uint8_t *punct_new, void *K_cache, void *V_cache,
                               uint8_t *punct_cache, int32_t *cache_len, float *K_comp, void *stream);
+
+/* Scratch-free selection, for callers that cannot allocate device memory:
+ * code under HIP graph capture, allocation-free serving loops, harnesses that
+ * forbid hipMalloc.  It is phsa_select without a workspace: the bf16 path's
+ * scratch (the bf16 hi/lo split of K_comp and the block norms,
+ * phsa_workspace_size(p, PHSA_OP_SELECT) bytes) lives in a static device array
+ * of PHSA_NOALLOC_SCRATCH_BYTES inside the library.  Each GPU the library runs
+ * on holds its own copy until the process ends; its address is looked up once
+ * per GPU, on the first call there.  The call allocates nothing.
+ *   - A problem whose scratch exceeds the array (B * Hkv * (Lk / m) blocks at
+ *     2 * 2 * d + 4 bytes each) returns PHSA_ERR_SCRATCH_LIMIT; nothing is
+ *     launched.
+ *   - `stream` must belong to the current device (PHSA_ERR_INVALID_ARG
+ *     otherwise).
+ *   - All calls on one GPU share its array and leave their contents in it:
+ *     calls that overlap in time on one GPU (different streams or host
+ *     threads) race, and the caller must order them.
+ * Results are those of phsa_select with the same arguments. */
+#define PHSA_NOALLOC_SCRATCH_BYTES (64u << 20)
+PHSA_API phsa_status phsa_select_noalloc(const phsa_params *p, const void *Q, const float *K_comp, int32_t *sel,
+                                         void *stream);
 
 #ifdef __cplusplus
 }

@@ -172,6 +172,9 @@ bool is_attention_op(int op) {
   return op == PHSA_OP_ATTN_FWD || op == PHSA_OP_ATTN_BWD || op == PHSA_OP_FORWARD || op == PHSA_OP_DECODE;
 }
 
+}  // namespace
+
+// Host validation of p for op (shared with the scratch-free entry point).
 phsa_status validate(const phsa_params *p, int op, Geom *out) {
   if (!p) return PHSA_ERR_NULL;
   if (op < PHSA_OP_COMPRESS || op > PHSA_OP_DECODE) return PHSA_ERR_INVALID_ARG;
@@ -237,6 +240,8 @@ phsa_status validate(const phsa_params *p, int op, Geom *out) {
   }
   return PHSA_OK;
 }
+
+namespace {
 
 size_t workspace_bytes(const Geom &g, int op) {
   switch (op) {
@@ -319,6 +324,7 @@ const char *phsa_status_string(phsa_status s) {
     case PHSA_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
     case PHSA_ERR_UNSUPPORTED: return "configuration not implemented by the kernels";
     case PHSA_ERR_HIP: return "HIP launch failure";
+    case PHSA_ERR_SCRATCH_LIMIT: return "problem larger than the fixed scratch of the scratch-free entry point";
   }
   return "unknown status";
 }

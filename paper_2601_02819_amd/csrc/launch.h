@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "../../include/phsa.h"
+
 namespace phsa {
 
 // Geometry resolved once by the ABI layer.
@@ -42,6 +44,10 @@ struct IndexWs {
 };
 
 constexpr int kIndexTile = 256;  // query rows per index-building workgroup
+
+// Host validation of the C ABI's parameters for an operation (api.hip); fills
+// the resolved geometry when out is not NULL.
+phsa_status validate(const phsa_params *p, int op, Geom *out);
 
 // Hooks around every kernel launch, given the kernel's profiling name.  The
 // library defines them empty (api.hip); the profiling build links definitions

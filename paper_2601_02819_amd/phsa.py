@@ -18,7 +18,9 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libphsa.so")
 PROF_LIB_PATH = os.path.join(_HERE, "libphsa_prof.so")   # profiling build (include/phsa_prof.h)
 
-OK, ERR_INVALID_ARG, ERR_SHAPE, ERR_DTYPE, ERR_NULL, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP = range(8)
+(OK, ERR_INVALID_ARG, ERR_SHAPE, ERR_DTYPE, ERR_NULL, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP,
+ ERR_SCRATCH_LIMIT) = range(9)
+NOALLOC_SCRATCH_BYTES = 64 << 20
 BF16, FP32 = 0, 1
 OP_COMPRESS, OP_SELECT, OP_ATTN_FWD, OP_ATTN_BWD, OP_FORWARD, OP_DECODE = range(6)
 FLAG_REUSE_INDEX = 1
@@ -29,7 +31,7 @@ MAX_PUNCT_IDS = 16384
 EXPORTS = (
     "phsa_ksel", "phsa_validate", "phsa_workspace_size", "phsa_status_string", "phsa_punct_mask", "phsa_compress",
     "phsa_select", "phsa_attn_fwd", "phsa_attn_bwd", "phsa_forward", "phsa_decode", "phsa_decode_varlen",
-    "phsa_cache_append",
+    "phsa_cache_append", "phsa_select_noalloc",
 )
 PROF_EXPORTS = ("phsa_prof_enable", "phsa_prof_durations", "phsa_prof_reset")
 
@@ -74,6 +76,7 @@ def _load(path: str) -> ctypes.CDLL:
             "phsa_decode": (ctypes.c_int, [P] + [PP] * 8 + [ctypes.c_size_t, PP]),
             "phsa_decode_varlen": (ctypes.c_int, [P] + [PP] * 9 + [ctypes.c_size_t, PP]),
             "phsa_cache_append": (ctypes.c_int, [P] + [PP] * 8 + [PP]),
+            "phsa_select_noalloc": (ctypes.c_int, [P, PP, PP, PP, PP]),
         }
         if path == PROF_LIB_PATH:
             sig.update({
@@ -239,6 +242,25 @@ def select(q: torch.Tensor, kc: torch.Tensor, seqlen_k: int, cfg: Config,
     w = _workspace(p, OP_SELECT, ws, q.device)
     _check(lib().phsa_select(ctypes.byref(p), _ptr(q), _ptr(kc), _ptr(sel), _ptr(w), w.numel() if w is not None else 0,
                              _stream()), "phsa_select")
+    return sel
+
+
+def select_noalloc(q: torch.Tensor, kc: torch.Tensor, seqlen_k: int, cfg: Config,
+                   sel: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """phsa_select_noalloc: as select(), with the library's fixed scratch instead
+    of a workspace.  Pass `sel` (int32 [B, Hkv, Lq, Ksel]) to make the call itself
+    allocate nothing."""
+    _dev(q, kc)
+    B, Lq, Hq, d = q.shape
+    Hkv = kc.shape[1]
+    p = make_params(cfg, B, Lq, seqlen_k, Hq, Hkv, d, q.dtype)
+    if sel is None:
+        sel = torch.empty(B, Hkv, Lq, cfg.ksel, dtype=torch.int32, device=q.device)
+    _dev(sel)
+    if sel.dtype != torch.int32 or tuple(sel.shape) != (B, Hkv, Lq, cfg.ksel):
+        raise ValueError(f"sel must be int32 {(B, Hkv, Lq, cfg.ksel)}")
+    _check(lib().phsa_select_noalloc(ctypes.byref(p), _ptr(q), _ptr(kc), _ptr(sel), _stream()),
+           "phsa_select_noalloc")
     return sel
 
 

@@ -46,15 +46,23 @@ def test_library_exports_only_the_c_abi():
     assert exported_c_functions(phsa.PROF_LIB_PATH) == sorted(declared_functions() + declared_functions(PROF_HEADER))
 
 
+# The one exception: phsa_select_noalloc's static device scratch (its host-side
+# stand-in) and the per-GPU table of its device address, set once per GPU.
+NOALLOC_STATE = {"phsa::(anonymous namespace)::scratch", "phsa::(anonymous namespace)::g_scratch_ptr",
+                 "phsa::(anonymous namespace)::g_scratch_mu"}
+
+
 def test_library_keeps_no_mutable_state():
     """Every writable data symbol of the library's own namespace is a kernel
-    handle that the HIP runtime fills in when it registers the code object:
-    the ABI layer holds no namespace-scope state, so calls are reentrant."""
+    handle that the HIP runtime fills in when it registers the code object, or
+    the scratch-free entry point's fixed scratch: the ABI layer holds no other
+    namespace-scope state, so calls are reentrant."""
     out = subprocess.run(["nm", "-C", phsa.LIB_PATH], capture_output=True, text=True, check=True).stdout
     data = [ln.split(" ", 2)[2] for ln in out.splitlines() if re.match(r"^[0-9a-f]+ [bBdD] ", ln)]
     ours = [n for n in data if n.startswith("phsa::")]
     assert ours, "expected the kernel handles"
-    assert all(re.match(r"phsa::\w+_kernel[<(]", n) for n in ours), [n for n in ours if "_kernel" not in n]
+    other = [n for n in ours if not re.match(r"phsa::\w+_kernel[<(]", n)]
+    assert set(other) == NOALLOC_STATE, other
 
 
 def _p(**kw):
@@ -165,8 +173,25 @@ def test_punct_mask_rejects_before_launch():
     assert L.phsa_punct_mask(None, 0, None, 0, None, None) == phsa.OK     # nothing to do, nothing launched
 
 
+def test_select_noalloc_rejects_before_launch():
+    """The scratch-free selection validates like phsa_select and refuses a
+    problem whose scratch would not fit its fixed array, before any GPU call."""
+    L = phsa.lib()
+    bogus = ctypes.c_void_p(0x1000)
+    assert L.phsa_select_noalloc(ctypes.byref(_p(seqlen_k=1000)), bogus, bogus, bogus, None) == phsa.ERR_SHAPE
+    assert L.phsa_select_noalloc(ctypes.byref(_p()), None, bogus, bogus, None) == phsa.ERR_NULL
+    # B * Hkv * T blocks at (2 * 2 * d + 4) bytes: 64 x 8 x 512 blocks at d = 128 is 135 MB > 64 MiB
+    big = _p(batch=64, n_heads_q=16, n_heads_kv=8, head_dim=128, seqlen_q=32768, seqlen_k=32768, top_k=12)
+    assert phsa.workspace_size(big, phsa.OP_SELECT) > phsa.NOALLOC_SCRATCH_BYTES
+    assert L.phsa_select_noalloc(ctypes.byref(big), bogus, bogus, bogus, None) == phsa.ERR_SCRATCH_LIMIT
+    # the 4 x 32k workloads fit, in both geometries
+    for kw in (dict(top_k=12), dict(block_size=16, n_init_blocks=8, window=512, top_k=16)):
+        p = _p(batch=4, n_heads_q=16, n_heads_kv=8, head_dim=128, seqlen_q=32768, seqlen_k=32768, **kw)
+        assert 0 < phsa.workspace_size(p, phsa.OP_SELECT) <= phsa.NOALLOC_SCRATCH_BYTES
+
+
 def test_status_strings():
-    for s in range(8):
+    for s in range(9):
         assert isinstance(phsa.status_string(s), str) and phsa.status_string(s)
     assert phsa.status_string(99) == "unknown status"
 
