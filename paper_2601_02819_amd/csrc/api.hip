@@ -6,7 +6,7 @@
 #include <algorithm>
 #include <exception>
 
-#include "../../include/phsa.h"
+#include "phsa.h"
 #include "launch.h"
 
 namespace phsa {
@@ -160,10 +160,10 @@ size_t decode_layout(const Geom &) { return 0; }  // the decode kernels need no 
 }  // namespace
 
 // bf16 selection scratch, as launch_select carves it: K_comp split into bf16 hi
-// and lo [B, Hkv, T, d] each, then one float32 norm per block.
+// and lo [B, Hkv, T, d] each, then the norms of both parts per block (float2).
 size_t select_split_bytes(const Geom &g) {
   const size_t nblk = (size_t)g.B * g.Hkv * g.T;
-  return g.dtype == PHSA_BF16 ? nblk * (2 * g.d * sizeof(uint16_t) + sizeof(float)) : 0;
+  return g.dtype == PHSA_BF16 ? nblk * (2 * g.d * sizeof(uint16_t) + 2 * sizeof(float)) : 0;
 }
 
 namespace {

@@ -6,7 +6,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/phsa.h"
+#include "phsa.h"
 
 namespace phsa {
 

@@ -5,7 +5,7 @@
 #include <atomic>
 #include <mutex>
 
-#include "../../include/phsa.h"
+#include "phsa.h"
 #include "launch.h"
 
 namespace phsa {

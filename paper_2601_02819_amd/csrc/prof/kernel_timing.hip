@@ -7,7 +7,7 @@
 #include <mutex>
 #include <vector>
 
-#include "../../../include/phsa_prof.h"
+#include "phsa_prof.h"
 #include "../launch.h"
 
 namespace phsa {

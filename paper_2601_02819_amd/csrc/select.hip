@@ -16,8 +16,17 @@
 // so every row has one answer).
 #include <float.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
+
+#ifndef PHSA_SEL_NW
+#define PHSA_SEL_NW 8      // waves per selection workgroup (k <= 16)
+#endif
+#ifndef PHSA_SEL_DB
+#define PHSA_SEL_DB true   // double-buffered pass 2 (k <= 16)
+#endif
 
 namespace phsa {
 
@@ -677,6 +686,7 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
 }
 
 // bf16 inputs: scoring on the matrix cores, selection by a bar and a short exact rank.
+// bf16 inputs: scoring on the matrix cores, selection by a bar and a short exact rank.
 //
 // Scores.  The group's query heads are summed in float32
 // (sum_h q_h . M = (sum_h q_h) . M), and both that sum and the float32
@@ -685,15 +695,19 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
 // accumulate) reproduce the float32 dot product to about 2^-17 relative, far
 // inside the 1e-4 score gap the selection is compared at.  The selection is
 // made on these sums before the (positive) softmax scale, which orders the
-// blocks the same way.  Wave w owns two 16-row tiles (rows
-// 32w..32w+31 of a 128-row workgroup tile), so every representative fragment
-// read from LDS feeds several MFMAs; representatives stream through LDS in
-// chunks of 64 blocks.  In the accumulator layout lane (q4, l16) holds, per
-// tile, the scores of rows 4 q4 + r (r = 0..3) for blocks t0 + 16 nt + l16, so
-// the 16 lanes of a quarter-wave together see every block of their rows, each
-// lane a fixed residue of (t - n_init) mod 16 (its "stripe").
+// blocks the same way.
 //
-// Top-k in two passes:
+// Tiling.  A workgroup of 8 waves takes 256 query rows of one (b, g); wave w
+// owns two 16-row tiles (rows 32w..32w+31), so every representative fragment
+// read from LDS feeds two MFMAs, and one staged chunk of 64 representatives
+// serves all 256 rows.  Chunks are staged through LDS from registers that were
+// loaded one chunk ahead, double-buffered so that a chunk costs one barrier.
+// In the accumulator layout lane (q4, l16) holds, per tile, the scores of rows
+// 4 q4 + r (r = 0..3) for blocks t0 + 16 nt + l16: the 16 lanes of a
+// quarter-wave see every block of their rows, each lane a fixed residue of
+// (t - n_init) mod 16 (its "stripe").
+//
+// Top-k in two passes over the candidate blocks:
 //   pass 1: a single hi.hi chain gives approximate scores.  The dropped terms
 //           hi.lo + lo.hi are bounded by 2^-7 (1 + 2^-8)^2 sum |q_c M_c| <=
 //           2^-7 (1 + 2^-8)^2 |q| |M| (each bf16 part is within 2^-8 of its
@@ -703,24 +717,28 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
 //           blocks, taken with the largest |M| of the chunk, bounds every
 //           block of the chunk, and every lane keeps the best two of these
 //           lower bounds in its stripe for each of its rows.  A row's 32
-//           stripe tops belong to 32 distinct blocks, so the largest value v
-//           with at least k of them >= v (the bar) lies below the row's k-th
-//           best exact score.
-//   pass 2: the exact scores are computed and those >= bar are appended, in
-//           block order, to the row's LDS list (quarter-wave ballots give the
-//           slots; no atomics).  For random scores about k + 3 pass.  Should a
-//           list near its capacity (40 for k <= 16, else 48), it is cut to its
-//           k best, whose k-th score becomes the bar.
-//   final : the k best of the list (score descending, then block ascending)
-//           are found by counting ranks and written in block order between the
+//           stripe tops belong to 32 distinct blocks, so the k-th largest of
+//           them (the bar) lies below the row's k-th best exact score.
+//   pass 2: the exact scores are computed and those >= bar are appended to a
+//           list shared by the four rows that one accumulator register holds
+//           across the quarter-waves (rows 4 q4 + r, q4 = 0..3), tagged with
+//           the row's q4.  A ballot gives each passing lane its slot and the
+//           list length grows by a scalar bit count, so an append costs a
+//           compare, a lane count and one LDS store.  A row's entries arrive in
+//           block order.  On random scores about k + 3 per row pass; a list
+//           that could overflow with the next append is cut to each row's k
+//           best (exact rank), whose k-th score becomes that row's bar.
+//   final : each list is split by row (stable), and the k best of a row
+//           (score descending, block ascending) are found by counting ranks
+//           within its quarter-wave and written in block order between the
 //           forced init and local blocks.
 
 // float32 K_comp -> bf16 hi, lo (hi + lo = K_comp to about 2^-17 relative) and
-// the Euclidean norm of every representative.  D / 8 consecutive threads hold
-// one representative.
+// the Euclidean norms of every representative's hi and lo parts (float2).  D / 8
+// consecutive threads hold one representative.
 template <int D>
 __global__ __launch_bounds__(256) void select_split_kernel(const float *__restrict__ Kc, bf16_t *__restrict__ Mh,
-                                                           bf16_t *__restrict__ Ml, float *__restrict__ Mnorm,
+                                                           bf16_t *__restrict__ Ml, float2 *__restrict__ Mnorm,
                                                            int64_t n8) {
   constexpr int TPR = D / 8;
   const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -733,40 +751,117 @@ __global__ __launch_bounds__(256) void select_split_kernel(const float *__restri
 #pragma unroll
     for (int e = 0; e < 8; ++e) v[e] = 0.f;
   }
-  float ss = 0.f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) ss = fmaf(v[e], v[e], ss);
-#pragma unroll
-  for (int o = 1; o < TPR; o <<= 1) ss += __shfl_xor(ss, o, 64);
-  if (x >= n8) return;
   bf16_t hi[8], lo[8];
+  float sh = 0.f, sl = 0.f;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     hi[e] = f32_to_bf16(v[e]);
-    lo[e] = f32_to_bf16(v[e] - bf16_to_f32(hi[e]));
+    const float h = bf16_to_f32(hi[e]);
+    lo[e] = f32_to_bf16(v[e] - h);
+    const float l = bf16_to_f32(lo[e]);
+    sh = fmaf(h, h, sh);
+    sl = fmaf(l, l, sl);
   }
+#pragma unroll
+  for (int o = 1; o < TPR; o <<= 1) {
+    sh += __shfl_xor(sh, o, 64);
+    sl += __shfl_xor(sl, o, 64);
+  }
+  if (x >= n8) return;
   reinterpret_cast<uint4 *>(Mh)[x] = *reinterpret_cast<const uint4 *>(hi);
   reinterpret_cast<uint4 *>(Ml)[x] = *reinterpret_cast<const uint4 *>(lo);
-  if (x % TPR == 0) Mnorm[x / TPR] = sqrtf(ss);
+  if (x % TPR == 0) Mnorm[x / TPR] = make_float2(sqrtf(sh), sqrtf(sl));
 }
 
-template <int D, int G, int CAP>
-__global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
-    const bf16_t *__restrict__ Q, const bf16_t *__restrict__ Mh_g, const bf16_t *__restrict__ Ml_g,
-    const float *__restrict__ Mnorm_g, int32_t *__restrict__ sel, Geom gm) {
+// A candidate list entry is (score, (q4 << 16) | (0xffff - block)): q4 names
+// the entry's row among the four rows that share the list.  For ranking, an
+// entry becomes a 64-bit key: the score's float32 bits mapped to an
+// order-preserving unsigned integer in the high word (-0 counted as +0), the
+// same low word.  For two entries of one row the key order is the selection's
+// order (score descending, then block ascending), so a rank is one 64-bit
+// compare.
+__device__ __forceinline__ uint64_t cand_key(float2 e) {
+  const uint32_t b = __float_as_uint(e.x + 0.f);
+  const uint32_t hi = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return ((uint64_t)hi << 32) | __float_as_uint(e.y);
+}
+__device__ __forceinline__ float2 key_entry(uint64_t key) {
+  const uint32_t hi = (uint32_t)(key >> 32);
+  return make_float2(__uint_as_float((hi & 0x80000000u) ? (hi & 0x7fffffffu) : ~hi), __uint_as_float((uint32_t)key));
+}
+__device__ __forceinline__ int key_row(uint64_t key) { return ((uint32_t)key >> 16) & 3; }
+__device__ __forceinline__ int key_block(uint64_t key) { return 0xffff - ((uint32_t)key & 0xffff); }
+
+// Cuts a 4-row candidate list (n entries in LDS) to the k best entries of each
+// row, keeping their order; ks[q] receives row q's k-th score (-inf for a row
+// with fewer than k entries).  Returns the new length.  Called by a whole wave;
+// rare, so kept out of line.
+template <int C4>
+__device__ __noinline__ int compact_list(float2 *lp, int n, int k, float *ks) {
+  constexpr int U = (C4 + 63) / 64;
+  const int lane = threadIdx.x & 63;
+  const uint64_t below = (1ull << lane) - 1ull;
+  uint64_t *kp = reinterpret_cast<uint64_t *>(lp);  // the same bytes, as keys
+  if (lane < 4) ks[lane] = -INFINITY;
+  uint64_t ent[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int e = lane + 64 * u;
+    ent[u] = e < n ? cand_key(lp[e]) : 0ull;
+  }
+  wave_lds_sync();
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (lane + 64 * u < n) kp[lane + 64 * u] = ent[u];
+  wave_lds_sync();
+  bool keep[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int e = lane + 64 * u;
+    int rk = 0;
+    for (int f = 0; f < n; ++f) {
+      const uint64_t o = kp[f];
+      rk += (((uint32_t)(o ^ ent[u]) & 0x30000u) == 0) & (o > ent[u]);
+    }
+    keep[u] = e < n && rk < k;
+    if (e < n && rk == k - 1) ks[key_row(ent[u])] = key_entry(ent[u]).x;
+  }
+  wave_lds_sync();
+  int pos = 0;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const uint64_t m = __builtin_amdgcn_ballot_w64(keep[u]);
+    if (keep[u]) lp[pos + __popcll(m & below)] = key_entry(ent[u]);
+    pos += __popcll(m);
+  }
+  wave_lds_sync();
+  return pos;
+}
+
+template <int D, int G, int KMAXK, int NW, bool DB>
+__global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__restrict__ Q,
+                                                              const bf16_t *__restrict__ Mh_g,
+                                                              const bf16_t *__restrict__ Ml_g,
+                                                              const float2 *__restrict__ Mnorm_g,
+                                                              int32_t *__restrict__ sel, Geom gm) {
   constexpr int CH = 64;                  // blocks per chunk
   constexpr int RT = 2;                   // 16-row tiles per wave (B fragments are reused across them)
-  constexpr int ROWS = 4 * 16 * RT;       // query rows per workgroup
+  constexpr int ROWS = NW * 16 * RT;      // query rows per workgroup
   constexpr int NR = 4 * RT;              // rows per lane in the accumulator layout
-  constexpr int MP = D + 8;
+  constexpr int MP = D + 8;               // LDS pitch of a staged representative
   constexpr int KB = D / 32;
-  constexpr int NL = CH * D / (256 * 8);  // 16-byte loads per thread per tile
-  constexpr int PITCH = CAP + 2;          // 8-byte words; keeps a wave's 4 row groups in distinct banks
-  constexpr int NJ = (CAP + 15) / 16;
-  static_assert(NJ <= 3, "the final rank count handles at most three 16-entry fragments");
-  __shared__ __attribute__((aligned(16))) bf16_t Mh[CH * MP];
-  __shared__ __attribute__((aligned(16))) bf16_t Ml[CH * MP];
-  __shared__ __attribute__((aligned(16))) float2 cand[ROWS][PITCH];  // (score, block as int bits)
+  constexpr int TILE = CH * MP;           // bf16 elements of one staged hi (or lo) chunk
+  constexpr int NL = CH * D / (NW * 64 * 8);  // 16-byte loads per thread per hi (or lo) chunk
+  constexpr int NBUF = DB ? 2 : 1;        // pass 2 buffers (one: two barriers per chunk)
+  constexpr int C4 = 4 * KMAXK + 112;     // capacity of a 4-row list: 4 k survivors + one 64-entry append + slack
+  constexpr int NGRP = NW * NR;           // lists per workgroup
+  static_assert(NL >= 1 && CH * D == NL * NW * 64 * 8, "chunk staging");
+  static_assert(C4 >= 4 * KMAXK + 64, "list capacity");
+  // staging: pass 1 uses two hi chunks, pass 2 NBUF (hi, lo) pairs; the same bytes
+  __shared__ __attribute__((aligned(16))) bf16_t stg[NBUF * 2 * TILE];
+  __shared__ __attribute__((aligned(16))) float2 lists[NGRP * C4];  // candidate entries; bar scratch first
+  __shared__ float kth_s[NGRP * 4];
+  __shared__ float2 nmax_s[NW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
@@ -778,116 +873,127 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
   const uint64_t below = (1ull << lane) - 1ull;
   // tile row of accumulator entry (j, r) held by this lane: 32 w + 16 j + 4 q4 + r
   auto crow = [&](int rr) { return wave * 16 * RT + (rr >> 2) * 16 + q4 * 4 + (rr & 3); };
+  const bf16_t *mh_bg = Mh_g + (int64_t)bg * gm.T * D;
+  const bf16_t *ml_bg = Ml_g + (int64_t)bg * gm.T * D;
+  const float2 *mn_bg = Mnorm_g + (int64_t)bg * gm.T;
 
-  // A operands: split query-head sums of rows 32w + 16j + l16 (all loads issued
-  // together); the lo parts only for pass 2, the row norms only for pass 1
-  bf16x8 ah[RT][KB], al[RT][KB];
-  float qn[RT];
-  auto load_a = [&](bool pass2) {
-#pragma unroll
-    for (int j = 0; j < RT; ++j) {
-      const int ia = i0 + wave * 16 * RT + j * 16 + l16;
-      float ss = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
-        // this feature slice summed over the G heads, HU heads' loads in flight at
-        // a time (all of them at once would not fit in registers for G = 8)
-        constexpr int HU = G < 4 ? G : 4;
-        float qs[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) qs[e] = 0.f;
-#pragma unroll 1
-        for (int h0 = 0; h0 < G; h0 += HU) {
-          u32x4 raw[HU];
-#pragma unroll
-          for (int hh = 0; hh < HU; ++hh)
-            raw[hh] = ia < gm.Lq ? *reinterpret_cast<const u32x4 *>(
-                                       Q + (((int64_t)b * gm.Lq + ia) * gm.Hq + g * G + h0 + hh) * D + kb * 32 + kq)
-                                 : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-          for (int hh = 0; hh < HU; ++hh) {
-            const bf16_t *v = reinterpret_cast<const bf16_t *>(&raw[hh]);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) qs[e] += bf16_to_f32(v[e]);
-          }
-        }
-        bf16_t hi[8], lo[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          ss = fmaf(qs[e], qs[e], ss);
-          hi[e] = f32_to_bf16(qs[e]);
-          lo[e] = f32_to_bf16(qs[e] - bf16_to_f32(hi[e]));
-        }
-        ah[j][kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(hi));
-        if (pass2) al[j][kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(lo));
-      }
-      if (!pass2) {
-        ss += __shfl_xor(ss, 16, 64);
-        ss += __shfl_xor(ss, 32, 64);
-        qn[j] = sqrtf(ss);
-      }
+  // largest |M_hi| and |M_lo| over the (b, g)'s blocks, for the pass-1 margin
+  {
+    float2 mx = make_float2(0.f, 0.f);
+    for (int t = tid; t < gm.T; t += NW * 64) {
+      const float2 v = mn_bg[t];
+      mx.x = fmaxf(mx.x, v.x);
+      mx.y = fmaxf(mx.y, v.y);
     }
-  };
-  load_a(false);
-  // per row held in the accumulator layout: first local block (candidates lie
-  // below it) and the pass-1 margin factor 1.024 * 2^-7 |q|
-  int lo_r[NR];
-  float eq[NR];
+    mx.x = wave_max(mx.x);
+    mx.y = wave_max(mx.y);
+    if (lane == 0) nmax_s[wave] = mx;
+  }
+
+  // A operands: split query-head sums of rows 32w + 16j + l16, and the norms of their parts
+  bf16x8 ah[RT][KB], al[RT][KB];
+  float qnh[RT], qnl[RT];
 #pragma unroll
-  for (int rr = 0; rr < NR; ++rr) {
-    const int i = i0 + crow(rr);
-    lo_r[rr] = i < gm.Lq ? max(0, (gm.q_pos0 + i) / gm.m - gm.window / gm.m) : 0;
-    eq[rr] = __shfl(qn[rr >> 2], q4 * 4 + (rr & 3), 64) * 0.008f;
+  for (int j = 0; j < RT; ++j) {
+    const int ia = i0 + wave * 16 * RT + j * 16 + l16;
+    float ssh = 0.f, ssl = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      // this feature slice summed over the G heads, HU heads' loads in flight at
+      // a time (all of them at once would not fit in registers for G = 8)
+      constexpr int HU = G < 4 ? G : 4;
+      float qs[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qs[e] = 0.f;
+#pragma unroll 1
+      for (int h0 = 0; h0 < G; h0 += HU) {
+        u32x4 raw[HU];
+#pragma unroll
+        for (int hh = 0; hh < HU; ++hh)
+          raw[hh] = ia < gm.Lq ? *reinterpret_cast<const u32x4 *>(
+                                     Q + (((int64_t)b * gm.Lq + ia) * gm.Hq + g * G + h0 + hh) * D + kb * 32 + kq)
+                               : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int hh = 0; hh < HU; ++hh) {
+          const bf16_t *v = reinterpret_cast<const bf16_t *>(&raw[hh]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) qs[e] += bf16_to_f32(v[e]);
+        }
+      }
+      bf16_t hi[8], lo[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        hi[e] = f32_to_bf16(qs[e]);
+        const float h = bf16_to_f32(hi[e]);
+        lo[e] = f32_to_bf16(qs[e] - h);
+        const float l = bf16_to_f32(lo[e]);
+        ssh = fmaf(h, h, ssh);
+        ssl = fmaf(l, l, ssl);
+      }
+      ah[j][kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(hi));
+      al[j][kb] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(lo));
+    }
+    ssh += __shfl_xor(ssh, 16, 64);
+    ssh += __shfl_xor(ssh, 32, 64);
+    ssl += __shfl_xor(ssl, 16, 64);
+    ssl += __shfl_xor(ssl, 32, 64);
+    qnh[j] = sqrtf(ssh);
+    qnl[j] = sqrtf(ssl);
   }
   const int last_i = min(i0 + ROWS - 1, gm.Lq - 1);
   const int t_end = k > 0 ? max(0, (gm.q_pos0 + last_i) / gm.m - gm.window / gm.m) : 0;
+  const int nch = t_end > gm.n_init ? (t_end - gm.n_init + CH - 1) / CH : 0;
   // chunks ending at or below the first row's first local block hold candidates of every row
   const int lo_first = max(0, (gm.q_pos0 + i0) / gm.m - gm.window / gm.m);
-  const bf16_t *mh_bg = Mh_g + (int64_t)bg * gm.T * D;
-  const bf16_t *ml_bg = Ml_g + (int64_t)bg * gm.T * D;
-  const float *mn_bg = Mnorm_g + (int64_t)bg * gm.T;
 
-  uint4 ph[NL], pl[NL];
-  float mnp[4];  // pass 1: norms of the blocks t0 + 16 nt + l16 of the prefetched chunk
-  auto fetch = [&](int t0, bool pass2) {
-    const int nblk = min(CH, gm.T - t0);
+  // chunk c (blocks n_init + 64 c ..) into registers, then into an LDS buffer.
+  // Rows past the last block repeat it: such blocks are never candidates.
+  u32x4 ph[NL], pl[NL];
+  auto fetch = [&](int c, bool pass2) {
+    const int t0 = gm.n_init + c * CH;
 #pragma unroll
     for (int x = 0; x < NL; ++x) {
-      const int e = (tid + 256 * x) * 8, row = e / D, c = e % D;
-      const int64_t off = (int64_t)(t0 + row) * D + c;
-      ph[x] = row < nblk ? *reinterpret_cast<const uint4 *>(mh_bg + off) : make_uint4(0u, 0u, 0u, 0u);
-      if (pass2)
-        pl[x] = row < nblk ? *reinterpret_cast<const uint4 *>(ml_bg + off) : make_uint4(0u, 0u, 0u, 0u);
-    }
-    if (!pass2) {
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const int t = t0 + nt * 16 + l16;
-        mnp[nt] = t < gm.T ? mn_bg[t] : 0.f;
-      }
+      const int e = (tid + NW * 64 * x) * 8, row = e / D, col = e % D;
+      const int64_t off = (int64_t)min(t0 + row, gm.T - 1) * D + col;
+      ph[x] = *reinterpret_cast<const u32x4 *>(mh_bg + off);
+      if (pass2) pl[x] = *reinterpret_cast<const u32x4 *>(ml_bg + off);
     }
   };
-  auto stage = [&](bool pass2) {
+  auto stage = [&](bf16_t *hb, bf16_t *lb) {
 #pragma unroll
     for (int x = 0; x < NL; ++x) {
-      const int e = (tid + 256 * x) * 8, row = e / D, c = e % D;
-      *reinterpret_cast<uint4 *>(&Mh[row * MP + c]) = ph[x];
-      if (pass2) *reinterpret_cast<uint4 *>(&Ml[row * MP + c]) = pl[x];
+      const int e = (tid + NW * 64 * x) * 8, row = e / D, col = e % D;
+      *reinterpret_cast<u32x4 *>(&hb[row * MP + col]) = ph[x];
+      if (lb) *reinterpret_cast<u32x4 *>(&lb[row * MP + col]) = pl[x];
     }
   };
 
   // ---- pass 1: best two approximate scores of each lane's stripe, per row
+  int lo_r[NR];
   float top1[NR], top2[NR];
 #pragma unroll
-  for (int rr = 0; rr < NR; ++rr) top1[rr] = top2[rr] = -INFINITY;
-  if (gm.n_init < t_end) fetch(gm.n_init, false);
-  for (int t0 = gm.n_init; t0 < t_end; t0 += CH) {
-    __syncthreads();
-    stage(false);
-    __syncthreads();
-    // the chunk's largest representative norm, then each row's margin
-    const float mx = row_max16(fmaxf(fmaxf(mnp[0], mnp[1]), fmaxf(mnp[2], mnp[3])));
-    if (t0 + CH < t_end) fetch(t0 + CH, false);
+  for (int rr = 0; rr < NR; ++rr) {
+    const int i = i0 + crow(rr);
+    lo_r[rr] = i < gm.Lq ? max(0, (gm.q_pos0 + i) / gm.m - gm.window / gm.m) : 0;
+    top1[rr] = top2[rr] = -INFINITY;
+  }
+  if (nch > 0) {
+    fetch(0, false);
+    stage(stg, nullptr);
+    if (nch > 1) fetch(1, false);
+  }
+  lds_barrier();
+  auto keep2 = [&](int rr, float v) {  // best two of the stripe (top1 >= top2)
+    top2[rr] = __builtin_amdgcn_fmed3f(top1[rr], top2[rr], v);  // the middle of the three
+    top1[rr] = fmaxf(top1[rr], v);
+  };
+  for (int c = 0; c < nch; ++c) {
+    const int buf = c & 1;
+    // the other buffer held chunk c - 1, which every wave finished before the last barrier
+    if (c + 1 < nch) stage(stg + (buf ^ 1) * TILE, nullptr);
+    if (c + 2 < nch) fetch(c + 2, false);
+    const bf16_t *hb = stg + buf * TILE;
+    const int t0 = gm.n_init + c * CH;
     f32x4 acc[RT][4];
 #pragma unroll
     for (int j = 0; j < RT; ++j)
@@ -897,105 +1003,87 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
     for (int kb = 0; kb < KB; ++kb) {
       bf16x8 bh[4];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) bh[nt] = load_bf16x8(&Mh[(nt * 16 + l16) * MP + kb * 32 + kq]);
+      for (int nt = 0; nt < 4; ++nt) bh[nt] = load_bf16x8(&hb[(nt * 16 + l16) * MP + kb * 32 + kq]);
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
         for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(ah[j][kb], bh[nt], acc[j][nt]);
     }
-    float mg[NR];
-#pragma unroll
-    for (int rr = 0; rr < NR; ++rr) mg[rr] = fmaf(eq[rr], mx, 1e-30f);
-    auto keep2 = [&](int rr, float v) {  // best two of the stripe (top1 >= top2)
-      top2[rr] = __builtin_amdgcn_fmed3f(top1[rr], top2[rr], v);  // the middle of the three
-      top1[rr] = fmaxf(top1[rr], v);
-    };
     if (t0 + CH <= lo_first) {
 #pragma unroll
       for (int rr = 0; rr < NR; ++rr)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) keep2(rr, acc[rr >> 2][nt][rr & 3] - mg[rr]);
+        for (int nt = 0; nt < 4; ++nt) keep2(rr, acc[rr >> 2][nt][rr & 3]);
     } else {
 #pragma unroll
       for (int rr = 0; rr < NR; ++rr)
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
-          keep2(rr, t0 + nt * 16 + l16 < lo_r[rr] ? acc[rr >> 2][nt][rr & 3] - mg[rr] : -INFINITY);
+          keep2(rr, t0 + nt * 16 + l16 < lo_r[rr] ? acc[rr >> 2][nt][rr & 3] : -INFINITY);
     }
+    lds_barrier();
   }
 
-  // ---- bar of each row: the largest stripe top v with at least k stripe tops >= v
+  // ---- bar of each row: the k-th largest of its 32 stripe lower bounds (the
+  // largest v with at least k of them >= v), k distinct blocks whose exact
+  // scores are at least that.  The margin: |s3 - s1| <= |q_hi| |M_lo| +
+  // |q_lo| |M_hi| for the three-chain score s3 and the hi.hi score s1
+  // (Cauchy-Schwarz on each dropped product), plus the float32 rounding of
+  // both chains, below 2^-15 |q_hi| |M_hi|.  Rows past the end take nothing.
   float thr[NR];
-  int cnt[NR];
+  {
+    float2 nm = nmax_s[0];
 #pragma unroll
-  for (int rr = 0; rr < NR; ++rr) {
-    float *rowp = reinterpret_cast<float *>(cand[crow(rr)]);
-    rowp[2 * l16] = top1[rr];
-    rowp[2 * l16 + 1] = top2[rr];
-  }
-  wave_lds_sync();
-#pragma unroll
-  for (int rr = 0; rr < NR; ++rr) {
-    const float4 *rowp = reinterpret_cast<const float4 *>(cand[crow(rr)]);
-    int c1 = 0, c2 = 0;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const float4 v = rowp[u];
-      c1 += (v.x >= top1[rr]) + (v.y >= top1[rr]) + (v.z >= top1[rr]) + (v.w >= top1[rr]);
-      c2 += (v.x >= top2[rr]) + (v.y >= top2[rr]) + (v.z >= top2[rr]) + (v.w >= top2[rr]);
+    for (int w = 1; w < NW; ++w) {
+      nm.x = fmaxf(nm.x, nmax_s[w].x);
+      nm.y = fmaxf(nm.y, nmax_s[w].y);
     }
-    float best = -INFINITY;
-    if (c1 >= k) best = top1[rr];
-    if (c2 >= k) best = fmaxf(best, top2[rr]);
-    thr[rr] = row_max16(best);
-    cnt[rr] = 0;
+    float *scr = reinterpret_cast<float *>(lists);  // [ROWS][32], free until pass 2
+#pragma unroll
+    for (int rr = 0; rr < NR; ++rr) {
+      const float eh = __shfl(qnh[rr >> 2], q4 * 4 + (rr & 3), 64);
+      const float el = __shfl(qnl[rr >> 2], q4 * 4 + (rr & 3), 64);
+      const float mg = fmaf(eh, fmaf(nm.x, 0x1p-15f, nm.y), el * nm.x) * 1.0001f;
+      top1[rr] -= mg;
+      top2[rr] -= mg;
+      scr[crow(rr) * 32 + 2 * l16] = top1[rr];
+      scr[crow(rr) * 32 + 2 * l16 + 1] = top2[rr];
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int rr = 0; rr < NR; ++rr) {
+      const float4 *rowp = reinterpret_cast<const float4 *>(scr + crow(rr) * 32);
+      int c1 = 0, c2 = 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float4 v = rowp[u];
+        c1 += (v.x >= top1[rr]) + (v.y >= top1[rr]) + (v.z >= top1[rr]) + (v.w >= top1[rr]);
+        c2 += (v.x >= top2[rr]) + (v.y >= top2[rr]) + (v.z >= top2[rr]) + (v.w >= top2[rr]);
+      }
+      float best = -INFINITY;
+      if (c1 >= k) best = top1[rr];
+      if (c2 >= k) best = fmaxf(best, top2[rr]);
+      best = row_max16(best);
+      thr[rr] = i0 + crow(rr) < gm.Lq ? best : INFINITY;
+    }
+    wave_lds_sync();
   }
-  wave_lds_sync();
 
-  // cuts the list of row rr to its k best, in block order; the k-th score becomes the bar
+  // ---- pass 2: exact scores >= bar join the 4-row lists
+  float2 *mylists = lists + wave * NR * C4;  // list rr of this wave at mylists + rr * C4
+  int cnt[NR];                                 // list lengths (wave-uniform)
+#pragma unroll
+  for (int rr = 0; rr < NR; ++rr) cnt[rr] = 0;
+  const uint32_t low_lane = ((uint32_t)q4 << 16) | (uint32_t)(0xffff - l16);
+  // cuts list rr to each row's k best, in order; each row's k-th score becomes its bar
   auto compact = [&](int rr) {
-    float2 *rowp = cand[crow(rr)];
-    const int n = cnt[rr];
-    float ks[NJ];
-    int kt[NJ], rk[NJ];
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const float2 e = j * 16 + l16 < n ? rowp[j * 16 + l16] : make_float2(-INFINITY, 0.f);
-      ks[j] = e.x;
-      kt[j] = __float_as_int(e.y);
-      rk[j] = 0;
-    }
-    for (int u = 0; u < n; ++u) {
-      const float2 e = rowp[u];
-      const int tu = __float_as_int(e.y);
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) rk[j] += beats(e.x, tu, ks[j], kt[j]);
-    }
-    wave_lds_sync();
-    int pos = 0;
-    float kth = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const bool keep = j * 16 + l16 < n && rk[j] < k;
-      const uint64_t m = __ballot(keep) & grp_bits;
-      if (keep) rowp[pos + __popcll(m & below)] = make_float2(ks[j], __int_as_float(kt[j]));
-      if (keep && rk[j] == k - 1) kth = ks[j];
-      pos += __popcll(m);
-    }
-    wave_lds_sync();
-    thr[rr] = row_max16(kth);
-    cnt[rr] = k;
+    float *ks = kth_s + (wave * NR + rr) * 4;
+    cnt[rr] = __builtin_amdgcn_readfirstlane(compact_list<C4>(mylists + rr * C4, cnt[rr], k, ks));
+    thr[rr] = fmaxf(thr[rr], ks[q4]);
   };
-
-  // ---- pass 2: exact scores >= bar go to the row lists in block order
-  if (gm.n_init < t_end) fetch(gm.n_init, true);
-  load_a(true);
-  for (int t0 = gm.n_init; t0 < t_end; t0 += CH) {
-    __syncthreads();
-    stage(true);
-    __syncthreads();
-    if (t0 + CH < t_end) fetch(t0 + CH, true);
-    const bool inner = t0 + CH <= lo_first;
+  // one chunk's exact scores (three chains over hi / lo staged chunks), appended
+  auto pass2_chunk = [&](const bf16_t *hb, const bf16_t *lb, int c) {
+    const int t0 = gm.n_init + c * CH;
     f32x4 acc[RT][4];
 #pragma unroll
     for (int j = 0; j < RT; ++j)
@@ -1006,8 +1094,8 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
       bf16x8 bh[4], bl[4];
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
-        bh[nt] = load_bf16x8(&Mh[(nt * 16 + l16) * MP + kb * 32 + kq]);
-        bl[nt] = load_bf16x8(&Ml[(nt * 16 + l16) * MP + kb * 32 + kq]);
+        bh[nt] = load_bf16x8(&hb[(nt * 16 + l16) * MP + kb * 32 + kq]);
+        bl[nt] = load_bf16x8(&lb[(nt * 16 + l16) * MP + kb * 32 + kq]);
       }
       // each chain over all RT x 4 accumulators in turn, so that consecutive
       // MFMAs are independent; every accumulator still takes hi.hi, hi.lo,
@@ -1025,79 +1113,127 @@ __global__ __launch_bounds__(256, CAP <= 40 ? 2 : 1) void select_mfma_kernel(
 #pragma unroll
         for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(al[j][kb], bh[nt], acc[j][nt]);
     }
-    // appends block t with score sc to row rr's list if it passes; the
-    // quarter-wave's passing lanes take consecutive slots in lane order
-    auto append = [&](int rr, int t, float sc, bool pass_sc, bool pass_t) {
-      const bool pass = pass_sc && pass_t;
-      // ballots of the two compares (lane masks as they are), combined on the scalar unit
-      const uint64_t m = __builtin_amdgcn_ballot_w64(pass_sc) & __builtin_amdgcn_ballot_w64(pass_t) & grp_bits;
-      const int below_m = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
-      if (pass) cand[crow(rr)][cnt[rr] + below_m] = make_float2(sc, __int_as_float(t));
-      cnt[rr] += __popcll(m);
-    };
+    float lowv[4];                           // the entries' low words, per block column
 #pragma unroll
-    for (int rr = 0; rr < NR; ++rr) {
-      // in an inner chunk every block is a candidate of every row
-      const int lim = inner ? 0x7fffffff : lo_r[rr];
+    for (int nt = 0; nt < 4; ++nt) lowv[nt] = __uint_as_float(low_lane - (uint32_t)(t0 + nt * 16));
+    auto appends = [&](auto inner_c) {
+      constexpr bool INNER = decltype(inner_c)::value;  // every block is a candidate of every row
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        if (cnt[rr] > CAP - 16) compact(rr);
-        const int t = t0 + nt * 16 + l16;
-        const float sc = acc[rr >> 2][nt][rr & 3];
-        append(rr, t, sc, sc >= thr[rr], t < lim);
+      for (int rr = 0; rr < NR; ++rr) {
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          if (cnt[rr] > C4 - 64) compact(rr);
+          const float sc = acc[rr >> 2][nt][rr & 3];
+          // wave masks straight from the compares (FCMP_OGE = 3, ICMP_SLT = 40)
+          uint64_t m = __builtin_amdgcn_fcmpf(sc, thr[rr], 3);
+          if (!INNER) m &= __builtin_amdgcn_sicmp(t0 + nt * 16 + l16, lo_r[rr], 40);
+          if (m) {
+            if (__builtin_amdgcn_inverse_ballot_w64(m)) {  // the passing lanes, straight from the mask
+              const int slot = (int)__builtin_amdgcn_mbcnt_hi(
+                  (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, (uint32_t)cnt[rr]));
+              float *ent = reinterpret_cast<float *>(mylists + rr * C4 + slot);
+              ent[0] = sc;
+              ent[1] = lowv[nt];
+            }
+            cnt[rr] = __builtin_amdgcn_readfirstlane(cnt[rr] + (int)__popcll(m));
+          }
+        }
       }
+    };
+    if (t0 + CH <= lo_first) appends(std::true_type{});
+    else appends(std::false_type{});
+  };
+  if (DB) {
+    if (nch > 0) {
+      fetch(0, true);
+      stage(stg, stg + TILE);
+      if (nch > 1) fetch(1, true);
     }
+    lds_barrier();
+    for (int c = 0; c < nch; ++c) {
+      const int buf = c & 1;
+      if (c + 1 < nch) stage(stg + (buf ^ 1) * 2 * TILE, stg + (buf ^ 1) * 2 * TILE + TILE);
+      if (c + 2 < nch) fetch(c + 2, true);
+      pass2_chunk(stg + buf * 2 * TILE, stg + buf * 2 * TILE + TILE, c);
+      lds_barrier();
+    }
+  } else {
+    if (nch > 0) fetch(0, true);
+    for (int c = 0; c < nch; ++c) {
+      lds_barrier();
+      stage(stg, stg + TILE);
+      lds_barrier();
+      if (c + 1 < nch) fetch(c + 1, true);
+      pass2_chunk(stg, stg + TILE, c);
+    }
+    lds_barrier();
   }
 
-  // ---- final: the k best of each list, written in block order
-  wave_lds_sync();
-#pragma unroll
+  // ---- final: per list, split by row into the (now free) staging area, then
+  // each quarter-wave ranks its row's entries and writes the row
+  uint64_t *split = reinterpret_cast<uint64_t *>(stg) + wave * C4;  // this wave's scratch, as keys
+  static_assert(NW * C4 * sizeof(uint64_t) <= NBUF * 2 * TILE * sizeof(bf16_t), "split scratch");
+#pragma unroll 1
   for (int rr = 0; rr < NR; ++rr) {
-    const int row = crow(rr);
-    const int i = i0 + row;
-    if (i >= gm.Lq) continue;
-    const float2 *rowp = cand[row];
+    const float2 *lp = mylists + rr * C4;
     const int n = cnt[rr];
-    const int npick = min(n, k);
-    int32_t *out = sel + ((int64_t)bg * gm.Lq + i) * gm.ksel;
-    float ks[NJ];
-    int kt[NJ], rk[NJ];
+    // row counts, then a stable split into [row 0 | row 1 | row 2 | row 3]
+    int nq[4] = {0, 0, 0, 0};
+    for (int e0 = 0; e0 < n; e0 += 64) {
+      const int e = e0 + lane;
+      const int tg = e < n ? (int)(__float_as_uint(lp[e].y) >> 16) : 4;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const float2 e = j * 16 + l16 < n ? rowp[j * 16 + l16] : make_float2(-INFINITY, 0.f);
-      ks[j] = e.x;
-      kt[j] = __float_as_int(e.y);
-      rk[j] = 0;
+      for (int q = 0; q < 4; ++q) nq[q] += __popcll(__builtin_amdgcn_ballot_w64(tg == q));
     }
-    if (n > k) {
-      // fragments j that hold entries in some row of the wave (usually one)
-      const bool two = __ballot(n > 16) != 0, three = __ballot(n > 32) != 0;
-      for (int u = 0; u < n; ++u) {
-        const float2 e = rowp[u];
-        const int tu = __float_as_int(e.y);
-        rk[0] += beats(e.x, tu, ks[0], kt[0]);
+    int off[4] = {0, nq[0], nq[0] + nq[1], nq[0] + nq[1] + nq[2]};
+    for (int e0 = 0; e0 < n; e0 += 64) {
+      const int e = e0 + lane;
+      const uint64_t ent = e < n ? cand_key(lp[e]) : 0ull;
+      const int tg = e < n ? key_row(ent) : 4;
 #pragma unroll
-        for (int j = 1; j < NJ; ++j)
-          if (j == 1 ? two : three) rk[j] += beats(e.x, tu, ks[j], kt[j]);
+      for (int q = 0; q < 4; ++q) {
+        const uint64_t m = __builtin_amdgcn_ballot_w64(tg == q);
+        if (tg == q) split[off[q] + __popcll(m & below)] = ent;
+        off[q] += __popcll(m);
       }
     }
+    wave_lds_sync();
+    // this quarter-wave's row
+    const int my_n = q4 == 0 ? nq[0] : q4 == 1 ? nq[1] : q4 == 2 ? nq[2] : nq[3];
+    const int my_off = q4 == 0 ? 0 : q4 == 1 ? nq[0] : q4 == 2 ? nq[0] + nq[1] : nq[0] + nq[1] + nq[2];
+    const int max_n = max(max(nq[0], nq[1]), max(nq[2], nq[3]));
+    const uint64_t *rp = split + my_off;
+    const int i = i0 + crow(rr);
+    const bool live = i < gm.Lq;
+    int32_t *out = sel + ((int64_t)bg * gm.Lq + (live ? i : 0)) * gm.ksel;
     const int cur = (gm.q_pos0 + i) / gm.m;
     const int ni = min(gm.n_init, cur + 1);
+    const int npick = min(my_n, k);
+    const bool cut = __builtin_amdgcn_ballot_w64(my_n > k) != 0;  // some row of the list has more than k
     int pos = 0;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const bool take = j * 16 + l16 < n && rk[j] < k;
-      const uint64_t m = __ballot(take) & grp_bits;
-      if (take) out[ni + pos + __popcll(m & below)] = kt[j];
+    for (int j0 = 0; j0 < max_n; j0 += 16) {
+      const int j = j0 + l16;
+      const bool have = j < my_n;
+      const uint64_t me = have ? rp[j] : 0ull;
+      int rk = 0;
+      if (cut) {
+        for (int f = 0; f < max_n; ++f) rk += (f < my_n) & (rp[min(f, max(my_n - 1, 0))] > me);
+      }
+      const bool take = have && rk < k;
+      const uint64_t m = __builtin_amdgcn_ballot_w64(take) & grp_bits;
+      if (take && live) out[ni + pos + __popcll(m & below)] = key_block(me);
       pos += __popcll(m);
     }
     // forced init blocks, local blocks and padding around the picks
-    const int lo1 = max(max(0, cur - gm.window / gm.m), ni);
-    for (int s = l16; s < gm.ksel; s += 16) {
-      if (s >= ni && s < ni + npick) continue;
-      const int x = s - ni - npick;
-      out[s] = s < ni ? s : (lo1 + x <= cur ? lo1 + x : -1);
+    if (live) {
+      const int lo1 = max(max(0, cur - gm.window / gm.m), ni);
+      for (int s = l16; s < gm.ksel; s += 16) {
+        if (s >= ni && s < ni + npick) continue;
+        const int x = s - ni - npick;
+        out[s] = s < ni ? s : (lo1 + x <= cur ? lo1 + x : -1);
+      }
     }
+    wave_lds_sync();
   }
 }
 
@@ -1134,20 +1270,21 @@ static hipError_t launch_select_mfma(const Geom &g, const void *Q, const float *
                                      hipStream_t s) {
   const int64_t n = (int64_t)g.B * g.Hkv * g.T * D;
   bf16_t *mh = reinterpret_cast<bf16_t *>(ws), *ml = mh + n;
-  float *mnorm = reinterpret_cast<float *>(ml + n);
+  float2 *mnorm = reinterpret_cast<float2 *>(ml + n);
   timing_begin("phsa_select_split", s);
   hipLaunchKernelGGL(select_split_kernel<D>, dim3((unsigned)((n / 8 + 255) / 256)), dim3(256), 0, s, Kc, mh, ml, mnorm,
                      n / 8);
   timing_end(s);
-  // list capacity: at least k survivors of a cut plus one 16-key append (40 keeps two workgroups per CU)
-  const dim3 grid((g.Lq + 127) / 128, g.B * g.Hkv);
   timing_begin("phsa_select", s);
-  if (g.top_k <= 16)
-    hipLaunchKernelGGL((select_mfma_kernel<D, G, 40>), grid, dim3(256), 0, s, static_cast<const bf16_t *>(Q), mh, ml,
-                       mnorm, sel, g);
-  else
-    hipLaunchKernelGGL((select_mfma_kernel<D, G, 48>), grid, dim3(256), 0, s, static_cast<const bf16_t *>(Q), mh, ml,
-                       mnorm, sel, g);
+  if (g.top_k <= 16) {
+    const dim3 grid((g.Lq + PHSA_SEL_NW * 32 - 1) / (PHSA_SEL_NW * 32), g.B * g.Hkv);
+    hipLaunchKernelGGL((select_mfma_kernel<D, G, 16, PHSA_SEL_NW, PHSA_SEL_DB>), grid, dim3(PHSA_SEL_NW * 64), 0, s,
+                       static_cast<const bf16_t *>(Q), mh, ml, mnorm, sel, g);
+  } else {
+    const dim3 grid((g.Lq + 255) / 256, g.B * g.Hkv);
+    hipLaunchKernelGGL((select_mfma_kernel<D, G, 32, 8, false>), grid, dim3(512), 0, s,
+                       static_cast<const bf16_t *>(Q), mh, ml, mnorm, sel, g);
+  }
   timing_end(s);
   return hipGetLastError();
 }
@@ -1169,7 +1306,7 @@ static hipError_t launch_select_softmax_mfma(const Geom &g, const void *Q, const
                                              hipStream_t s) {
   const int64_t n = (int64_t)g.B * g.Hkv * g.T * D;
   bf16_t *mh = reinterpret_cast<bf16_t *>(ws), *ml = mh + n;
-  float *mnorm = reinterpret_cast<float *>(ml + n);
+  float2 *mnorm = reinterpret_cast<float2 *>(ml + n);
   timing_begin("phsa_select_split", s);
   hipLaunchKernelGGL(select_split_kernel<D>, dim3((unsigned)((n / 8 + 255) / 256)), dim3(256), 0, s, Kc, mh, ml, mnorm,
                      n / 8);

@@ -8,7 +8,7 @@
 
 #include <vector>
 
-#include "../../include/phsa.h"
+#include "phsa.h"
 
 static int g_fail = 0;
 static long g_checks = 0;

@@ -116,8 +116,8 @@ def test_ksel_and_workspace():
     p = _p(n_init_blocks=2, window=128, top_k=5)
     assert L.phsa_ksel(ctypes.byref(p)) == 2 + 2 + 1 + 5
     assert phsa.workspace_size(_p(), phsa.OP_COMPRESS) == 0
-    # bf16 hi/lo copies of K_comp and one norm per block, rounded up to 256 bytes
-    assert phsa.workspace_size(_p(), phsa.OP_SELECT) == -(-16 * (2 * 64 * 2 + 4) // 256) * 256
+    # bf16 hi/lo copies of K_comp and the norms of both parts per block, rounded up to 256 bytes
+    assert phsa.workspace_size(_p(), phsa.OP_SELECT) == -(-16 * (2 * 64 * 2 + 8) // 256) * 256
     assert phsa.workspace_size(_p(dtype=phsa.FP32), phsa.OP_SELECT) == 0
     # the softmax-sum mode scores with the same split copies
     assert phsa.workspace_size(_p(flags=phsa.FLAG_SELECT_SOFTMAX_SUM), phsa.OP_SELECT) == \
