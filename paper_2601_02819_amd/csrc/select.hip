@@ -27,6 +27,9 @@
 #ifndef PHSA_SEL_DB
 #define PHSA_SEL_DB true   // double-buffered pass 2 (k <= 16)
 #endif
+#ifndef PHSA_SEL_SLACK
+#define PHSA_SEL_SLACK 112 // list capacity beyond 4 k entries
+#endif
 
 namespace phsa {
 
@@ -773,6 +776,25 @@ __global__ __launch_bounds__(256) void select_split_kernel(const float *__restri
   if (x % TPR == 0) Mnorm[x / TPR] = make_float2(sqrtf(sh), sqrtf(sl));
 }
 
+// The value of lane (l16 + r) % 16 of this lane's 16-lane row (DPP row_ror:r).
+template <int R>
+__device__ __forceinline__ uint32_t row_ror32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x120 + R, 0xF, 0xF, true);
+}
+__device__ __forceinline__ uint64_t row_ror64(uint64_t v, int r) {
+  uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  switch (r) {
+#define PHSA_ROR_CASE(R) \
+  case R: lo = row_ror32<R>(lo); hi = row_ror32<R>(hi); break;
+    PHSA_ROR_CASE(1) PHSA_ROR_CASE(2) PHSA_ROR_CASE(3) PHSA_ROR_CASE(4) PHSA_ROR_CASE(5)
+    PHSA_ROR_CASE(6) PHSA_ROR_CASE(7) PHSA_ROR_CASE(8) PHSA_ROR_CASE(9) PHSA_ROR_CASE(10)
+    PHSA_ROR_CASE(11) PHSA_ROR_CASE(12) PHSA_ROR_CASE(13) PHSA_ROR_CASE(14) PHSA_ROR_CASE(15)
+#undef PHSA_ROR_CASE
+    default: break;
+  }
+  return ((uint64_t)hi << 32) | lo;
+}
+
 // A candidate list entry is (score, (q4 << 16) | (0xffff - block)): q4 names
 // the entry's row among the four rows that share the list.  For ranking, an
 // entry becomes a 64-bit key: the score's float32 bits mapped to an
@@ -853,7 +875,7 @@ __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__re
   constexpr int TILE = CH * MP;           // bf16 elements of one staged hi (or lo) chunk
   constexpr int NL = CH * D / (NW * 64 * 8);  // 16-byte loads per thread per hi (or lo) chunk
   constexpr int NBUF = DB ? 2 : 1;        // pass 2 buffers (one: two barriers per chunk)
-  constexpr int C4 = 4 * KMAXK + 112;     // capacity of a 4-row list: 4 k survivors + one 64-entry append + slack
+  constexpr int C4 = 4 * KMAXK + PHSA_SEL_SLACK;  // capacity of a 4-row list: 4 k survivors + one 64-entry append + slack
   constexpr int NGRP = NW * NR;           // lists per workgroup
   static_assert(NL >= 1 && CH * D == NL * NW * 64 * 8, "chunk staging");
   static_assert(C4 >= 4 * KMAXK + 64, "list capacity");
@@ -1038,7 +1060,11 @@ __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__re
       nm.x = fmaxf(nm.x, nmax_s[w].x);
       nm.y = fmaxf(nm.y, nmax_s[w].y);
     }
-    float *scr = reinterpret_cast<float *>(lists);  // [ROWS][32], free until pass 2
+    // [ROWS][36]: the pitch puts the four rows a quarter-wave group reads
+    // together (4 rows apart) in different banks
+    constexpr int SP = 36;
+    static_assert(ROWS * SP * sizeof(float) <= NGRP * C4 * sizeof(float2), "bar scratch");
+    float *scr = reinterpret_cast<float *>(lists);  // free until pass 2
 #pragma unroll
     for (int rr = 0; rr < NR; ++rr) {
       const float eh = __shfl(qnh[rr >> 2], q4 * 4 + (rr & 3), 64);
@@ -1046,13 +1072,12 @@ __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__re
       const float mg = fmaf(eh, fmaf(nm.x, 0x1p-15f, nm.y), el * nm.x) * 1.0001f;
       top1[rr] -= mg;
       top2[rr] -= mg;
-      scr[crow(rr) * 32 + 2 * l16] = top1[rr];
-      scr[crow(rr) * 32 + 2 * l16 + 1] = top2[rr];
+      *reinterpret_cast<float2 *>(&scr[crow(rr) * SP + 2 * l16]) = make_float2(top1[rr], top2[rr]);
     }
     wave_lds_sync();
 #pragma unroll
     for (int rr = 0; rr < NR; ++rr) {
-      const float4 *rowp = reinterpret_cast<const float4 *>(scr + crow(rr) * 32);
+      const float4 *rowp = reinterpret_cast<const float4 *>(scr + crow(rr) * SP);
       int c1 = 0, c2 = 0;
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -1211,18 +1236,41 @@ __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__re
     const int npick = min(my_n, k);
     const bool cut = __builtin_amdgcn_ballot_w64(my_n > k) != 0;  // some row of the list has more than k
     int pos = 0;
-    for (int j0 = 0; j0 < max_n; j0 += 16) {
-      const int j = j0 + l16;
-      const bool have = j < my_n;
-      const uint64_t me = have ? rp[j] : 0ull;
-      int rk = 0;
-      if (cut) {
-        for (int f = 0; f < max_n; ++f) rk += (f < my_n) & (rp[min(f, max(my_n - 1, 0))] > me);
+    if (max_n <= 32) {
+      // up to 32 entries per row: lane l16 holds entries l16 and 16 + l16 as keys
+      // (0 for none, below every entry) and counts the keys above its own with
+      // the 15 rotations of its 16-lane row (DPP, no LDS)
+      const uint64_t k0 = l16 < my_n ? rp[l16] : 0ull, k1 = l16 + 16 < my_n ? rp[16 + l16] : 0ull;
+      int r0 = k1 > k0, r1 = k0 > k1;
+      if (cut && max_n <= 16) {  // one entry per lane
+#pragma unroll
+        for (int r = 1; r < 16; ++r) r0 += row_ror64(k0, r) > k0;
+      } else if (cut) {
+#pragma unroll
+        for (int r = 1; r < 16; ++r) {
+          const uint64_t o0 = row_ror64(k0, r), o1 = row_ror64(k1, r);
+          r0 += (o0 > k0) + (o1 > k0);
+          r1 += (o0 > k1) + (o1 > k1);
+        }
       }
-      const bool take = have && rk < k;
-      const uint64_t m = __builtin_amdgcn_ballot_w64(take) & grp_bits;
-      if (take && live) out[ni + pos + __popcll(m & below)] = key_block(me);
-      pos += __popcll(m);
+      const bool take0 = l16 < my_n && r0 < k, take1 = l16 + 16 < my_n && r1 < k;
+      const uint64_t m0 = __builtin_amdgcn_ballot_w64(take0) & grp_bits;
+      const uint64_t m1 = __builtin_amdgcn_ballot_w64(take1) & grp_bits;
+      if (take0 && live) out[ni + __popcll(m0 & below)] = key_block(k0);
+      if (take1 && live) out[ni + __popcll(m0) + __popcll(m1 & below)] = key_block(k1);
+    } else {
+      // longer lists (many equal scores): rank against every entry through LDS
+      for (int j0 = 0; j0 < max_n; j0 += 16) {
+        const int j = j0 + l16;
+        const bool have = j < my_n;
+        const uint64_t me = have ? rp[j] : 0ull;
+        int rk = 0;
+        for (int f = 0; f < max_n; ++f) rk += (f < my_n) & (rp[min(f, max(my_n - 1, 0))] > me);
+        const bool take = have && rk < k;
+        const uint64_t m = __builtin_amdgcn_ballot_w64(take) & grp_bits;
+        if (take && live) out[ni + pos + __popcll(m & below)] = key_block(me);
+        pos += __popcll(m);
+      }
     }
     // forced init blocks, local blocks and padding around the picks
     if (live) {
