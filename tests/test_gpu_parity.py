@@ -120,6 +120,23 @@ def test_compress_select_block_sizes(m, d, dtype):
               lambda idx: oracle.score_row(h["q"], kc_ref, m, scale, 1024, idx[0], idx[2], idx[1]))
 
 
+@pytest.mark.parametrize("Hkv,d,dtype,m,T", [(16, 128, "bf16", 32, 9), (16, 128, "fp32", 16, 33), (8, 64, "bf16", 16, 7),
+                                            (4, 128, "fp32", 48, 5), (8, 128, "bf16", 5, 67), (2, 128, "bf16", 16, 6),
+                                            (8, 128, "bf16", 64, 5), (8, 64, "bf16", 128, 7)])
+def test_compress_row_layouts(Hkv, d, dtype, m, T):
+    """Compress with every layout of a token's Hkv * d keys: 64 to 512 16-byte
+    vectors with blocks shorter than 64 rows take the all-heads kernel (block
+    lengths below and off the 8 rows in flight, block counts that leave the last
+    workgroup part empty); fewer vectors or longer blocks take the per-head one."""
+    wl = Workload("rows", 2, m * T, m * T, Hkv, Hkv, d, m, 1, 1, 0, dtype, punct="bernoulli", punct_p=0.15)
+    cfg = cfg_of(wl)
+    host, dev = device_inputs(wl, 6, with_grad_out=False)
+    kc = phsa.compress(dev["k"], dev["punct"], cfg)
+    torch.cuda.synchronize()
+    h = oracle_inputs(host)
+    np.testing.assert_allclose(to_np(kc), oracle.compress(h["k"], h["punct"], m, wl.lam), atol=1e-5, rtol=1e-5)
+
+
 def test_forward_entry_point_matches_steps():
     """phsa_forward (one call) equals compress + select + attn_fwd bit for bit."""
     wl = small("fwd1", 2, 1024, 4, 2, 128, 3, 1, 64)
