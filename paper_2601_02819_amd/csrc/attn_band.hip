@@ -44,12 +44,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
                                                                bf16_t *__restrict__ opart, float2 *__restrict__ ml) {
   constexpr int RT = 2;                  // 16-row chunks per wave
   constexpr int TOK = 4 * RT * 16 / G;   // tokens per workgroup
-  constexpr int KP = D + 16, VP = D + 8, SP = D + 8;
+  constexpr int KP = D + 16, VP = D + 16, SP = D + 8;
   constexpr int VPR = D / 8, KB = D / 32, NT = D / 16;
   constexpr int NV = 64 * VPR / 256;     // 16-byte loads per thread per tensor per tile
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * VP];
-  __shared__ __attribute__((aligned(16))) bf16_t Os[4][16 * SP];
+  constexpr int BUF = 64 * (KP + VP);    // one K tile and one V tile
+  static_assert(4 * 16 * SP <= 2 * BUF, "output staging fits the tile buffers");
+  // two tile buffers: tile kt is read from one while tile kt + 1 is stored into
+  // the other; the output staging of the epilogue reuses them
+  __shared__ __attribute__((aligned(16))) bf16_t KV[2 * BUF];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
@@ -81,40 +83,52 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
   const int a_last = band_first_key(gm, gm.q_pos0 + i1), pos_first = gm.q_pos0 + i0;
 
   const float sl2 = gm.scale * kLog2e;
-  float mrun[RT], lrun[RT];
-  f32x4 o[RT][NT];
+  // the row sums l accumulate on the matrix cores: an all-ones A operand
+  // against the same P^T fragments as O, so l sums the bf16 weights that O sums
+  float mrun[RT];
+  f32x4 o[RT][NT], lacc[RT];
+  const bf16x8 ones = __builtin_bit_cast(bf16x8, v8i16{0x3f80, 0x3f80, 0x3f80, 0x3f80, 0x3f80, 0x3f80, 0x3f80, 0x3f80});
 #pragma unroll
   for (int c = 0; c < RT; ++c) {
     mrun[c] = -INFINITY;
-    lrun[c] = 0.f;
+    lacc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) o[c][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  // each tile's loads are issued before the barrier that waits for the previous
-  // tile's use; the other workgroup on the CU covers the rest of their latency
-  // tile kt + 1 is loaded into registers while tile kt is used (the last tile
-  // is loaded twice: a fixed load sequence per iteration)
+  // Tile kt + 1 waits in registers while tile kt is used, and is stored into
+  // the other buffer after that use; one barrier per tile then both publishes
+  // tile kt + 1 and ends every wave's reads of tile kt.  The loads of tile
+  // kt + 2 are issued right after the store, a whole tile ahead of their use.
+  // a tile is one uniform base (key kt 64 of (b, g)) plus per-thread 32-bit offsets
+  const int64_t head0 = (int64_t)b * gm.Lk * gm.Hkv * D + (int64_t)g * D, tile_step = (int64_t)64 * gm.Hkv * D;
+  // thread t moves the 16-byte vectors t + 256 v: key t / VPR + (256 / VPR) v,
+  // so only the first offset is per thread and the others are constants
+  static_assert(256 % VPR == 0, "rows per load pass");
+  const int koff = (tid / VPR) * gm.Hkv * D + (tid % VPR) * 8, soff = (tid / VPR) * KP + (tid % VPR) * 8;
+  const int kstep = (256 / VPR) * gm.Hkv * D;
   u32x4 kr[NV], vr[NV];
   auto load_tile = [&](int kt) {
+    const bf16_t *kp = K + head0 + kt * tile_step, *vp = V + head0 + kt * tile_step;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
-      const int x = tid + 256 * v, kk = x / VPR, c8 = (x % VPR) * 8;
-      const int64_t src = (((int64_t)b * gm.Lk + (int64_t)kt * 64 + kk) * gm.Hkv + g) * D + c8;
-      kr[v] = *reinterpret_cast<const u32x4 *>(K + src);
-      vr[v] = *reinterpret_cast<const u32x4 *>(V + src);
+      kr[v] = *reinterpret_cast<const u32x4 *>(kp + v * kstep + koff);
+      vr[v] = *reinterpret_cast<const u32x4 *>(vp + v * kstep + koff);
+    }
+  };
+  auto store_tile = [&](int buf) {
+    bf16_t *ks = KV + buf * BUF + soff, *vs = ks + 64 * KP;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      *reinterpret_cast<u32x4 *>(ks + v * (256 / VPR) * KP) = kr[v];
+      *reinterpret_cast<u32x4 *>(vs + v * (256 / VPR) * KP) = vr[v];
     }
   };
   load_tile(kt_lo);
-  for (int kt = kt_lo; kt <= kt_hi; ++kt) {
-    lds_barrier();
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      const int x = tid + 256 * v, kk = x / VPR, c8 = (x % VPR) * 8;
-      *reinterpret_cast<u32x4 *>(&Ks[kk * KP + c8]) = kr[v];
-      *reinterpret_cast<u32x4 *>(&Vs[kk * VP + c8]) = vr[v];
-    }
-    lds_barrier();
-    load_tile(min(kt + 1, kt_hi));
+  store_tile(0);
+  if (kt_lo < kt_hi) load_tile(kt_lo + 1);
+  lds_barrier();
+  for (int kt = kt_lo, buf = 0; kt <= kt_hi; ++kt, buf ^= 1) {
+    const bf16_t *Ks = KV + buf * BUF, *Vs = Ks + 64 * KP;
     const int key0 = kt * 64;
     // S^T = K Q^T for both chunks (every K fragment read from LDS feeds both)
     f32x4 sa[RT][4];
@@ -154,8 +168,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
       for (int j = 0; j < 4; ++j)
         mx = __builtin_elementwise_maximum(__builtin_elementwise_maximum(mx, st[j][0]),
                                            __builtin_elementwise_maximum(st[j][1], __builtin_elementwise_maximum(st[j][2], st[j][3])));
-      mx = __builtin_elementwise_maximum(mx, __shfl_xor(mx, 16, 64));
-      mx = __builtin_elementwise_maximum(mx, __shfl_xor(mx, 32, 64));
+      mx = max_xor32(max_xor16(mx));
       mx *= sl2;
       // The reference maximum moves only when some row's maximum rises by more
       // than 2^8 (or is first set): weights stay below 2^8, far inside bf16
@@ -167,35 +180,44 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
         mrun[c] = mn;
       }
       const float mref = mrun[c] == -INFINITY ? 0.f : mrun[c];  // no key of the row yet: every weight is 0
-      float l = 0.f;
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(st[j][r], sl2, -mref));
-          st[j][r] = p;
-          l += p;
-        }
-      l += __shfl_xor(l, 16, 64);
-      l += __shfl_xor(l, 32, 64);
-      lrun[c] = lrun[c] * f + l;
+        for (int r = 0; r < 4; ++r) st[j][r] = __builtin_amdgcn_exp2f(fmaf(st[j][r], sl2, -mref));
       fs[c] = f;
       pb[c][0] = pack_bf16x8(st[0], st[1]);
       pb[c][1] = pack_bf16x8(st[2], st[3]);
     }
-    const bool rescale = __any(fs[0] != 1.f || fs[RT - 1] != 1.f);
-    // O^T = O^T f + V^T P^T for both chunks (every V^T fragment feeds both)
+    // O^T = O^T f (a uniform branch, rarely taken) ...
+    if (__any(fs[0] != 1.f || fs[RT - 1] != 1.f)) {
+#pragma unroll
+      for (int c = 0; c < RT; ++c) {
+        lacc[c] *= fs[c];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) o[c][nt] *= fs[c];
+      }
+    }
+    // ... + V^T P^T for both chunks (every V^T fragment feeds both)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const bf16x8 v0 = lds_col8(Vs, VP, q4 * 4, 16 + q4 * 4, nt * 16, l16);
       const bf16x8 v1 = lds_col8(Vs, VP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16);
 #pragma unroll
       for (int c = 0; c < RT; ++c) {
-        if (rescale) o[c][nt] *= fs[c];
         o[c][nt] = mfma16x16x32(v0, pb[c][0], o[c][nt]);
         o[c][nt] = mfma16x16x32(v1, pb[c][1], o[c][nt]);
       }
     }
+#pragma unroll
+    for (int c = 0; c < RT; ++c) {
+      lacc[c] = mfma16x16x32(ones, pb[c][0], lacc[c]);
+      lacc[c] = mfma16x16x32(ones, pb[c][1], lacc[c]);
+    }
+    if (kt < kt_hi) {
+      store_tile(buf ^ 1);
+      if (kt + 1 < kt_hi) load_tile(kt + 2);
+    }
+    lds_barrier();
   }
 
   // partials: row (token, head) at list position band_base + (b, g, token); rows
@@ -208,8 +230,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 #pragma unroll
   for (int c = 0; c < RT; ++c) {
     const int r0 = (wave * RT + c) * 16;
-    ml[q4 == 0 ? dest(r0 + l16) : ix.discard] = make_float2(mrun[c], lrun[c]);
-    bf16_t *os = Os[wave];
+    ml[q4 == 0 ? dest(r0 + l16) : ix.discard] = make_float2(mrun[c], lacc[c][0]);
+    bf16_t *os = KV + wave * 16 * SP;  // every wave has passed the loop's last barrier
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const bf16_t o4[4] = {f32_to_bf16(o[c][nt][0]), f32_to_bf16(o[c][nt][1]), f32_to_bf16(o[c][nt][2]),
@@ -238,9 +260,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
   constexpr int KP = D + 16, SP = D + 8;  // K and V: 16-byte row reads and transposing reads
   constexpr int VPR = D / 8, KB = D / 32, NT = D / 16;
   constexpr int NV = 64 * VPR / 256;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Os[4][16 * SP];
+  constexpr int BUF = 2 * 64 * KP;        // one K tile and one V tile
+  static_assert(4 * 16 * SP <= 2 * BUF, "output staging fits the tile buffers");
+  // two tile buffers (tile kt read from one, tile kt + 1 stored into the
+  // other); the output staging of the epilogue reuses them
+  __shared__ __attribute__((aligned(16))) bf16_t KV[2 * BUF];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
@@ -281,31 +305,38 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
   for (int c = 0; c < RT; ++c)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) dq[c][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // each tile's loads are issued before the barrier that waits for the previous
-  // tile's use; the other workgroup on the CU covers the rest of their latency
-  // tile kt + 1 is loaded into registers while tile kt is used (the last tile
-  // is loaded twice: a fixed load sequence per iteration)
+  // the staging of the forward kernel: tile kt + 1 waits in registers while
+  // tile kt is used, is stored into the other buffer after that use, and one
+  // barrier per tile publishes it; tile kt + 2 is loaded right after the store
+  const int64_t head0 = (int64_t)b * gm.Lk * gm.Hkv * D + (int64_t)g * D, tile_step = (int64_t)64 * gm.Hkv * D;
+  // thread t moves the 16-byte vectors t + 256 v: key t / VPR + (256 / VPR) v,
+  // so only the first offset is per thread and the others are constants
+  static_assert(256 % VPR == 0, "rows per load pass");
+  const int koff = (tid / VPR) * gm.Hkv * D + (tid % VPR) * 8, soff = (tid / VPR) * KP + (tid % VPR) * 8;
+  const int kstep = (256 / VPR) * gm.Hkv * D;
   u32x4 kr[NV], vr[NV];
   auto load_tile = [&](int kt) {
+    const bf16_t *kp = K + head0 + kt * tile_step, *vp = V + head0 + kt * tile_step;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
-      const int x = tid + 256 * v, kk = x / VPR, c8 = (x % VPR) * 8;
-      const int64_t src = (((int64_t)b * gm.Lk + (int64_t)kt * 64 + kk) * gm.Hkv + g) * D + c8;
-      kr[v] = *reinterpret_cast<const u32x4 *>(K + src);
-      vr[v] = *reinterpret_cast<const u32x4 *>(V + src);
+      kr[v] = *reinterpret_cast<const u32x4 *>(kp + v * kstep + koff);
+      vr[v] = *reinterpret_cast<const u32x4 *>(vp + v * kstep + koff);
+    }
+  };
+  auto store_tile = [&](int buf) {
+    bf16_t *ks = KV + buf * BUF + soff, *vs = ks + 64 * KP;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      *reinterpret_cast<u32x4 *>(ks + v * (256 / VPR) * KP) = kr[v];
+      *reinterpret_cast<u32x4 *>(vs + v * (256 / VPR) * KP) = vr[v];
     }
   };
   load_tile(kt_lo);
-  for (int kt = kt_lo; kt <= kt_hi; ++kt) {
-    lds_barrier();
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      const int x = tid + 256 * v, kk = x / VPR, c8 = (x % VPR) * 8;
-      *reinterpret_cast<u32x4 *>(&Ks[kk * KP + c8]) = kr[v];
-      *reinterpret_cast<u32x4 *>(&Vs[kk * KP + c8]) = vr[v];
-    }
-    lds_barrier();
-    load_tile(min(kt + 1, kt_hi));
+  store_tile(0);
+  if (kt_lo < kt_hi) load_tile(kt_lo + 1);
+  lds_barrier();
+  for (int kt = kt_lo, buf = 0; kt <= kt_hi; ++kt, buf ^= 1) {
+    const bf16_t *Ks = KV + buf * BUF, *Vs = Ks + 64 * KP;
     const int key0 = kt * 64;
     const bool interior = key0 >= a_last && key0 + 63 <= pos_first;
 #pragma unroll
@@ -322,14 +353,22 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
           dp[j] = mfma16x16x32(load_bf16x8(&Vs[(j * 16 + l16) * KP + kb * 32 + kq]), df[c][kb], dp[j]);
         }
       // interior tiles (inside every row's band) need no mask: rows outside
-      // the band compute values that are discarded
+      // the band compute values that are discarded.  A masked score is -inf
+      // and its weight 2^-inf = 0.
+      if (!interior) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = key0 + j * 16 + q4 * 4 + r;
+            st[j][r] = (ok[c] && key >= a0[c] && key <= pos[c]) ? st[j][r] : -INFINITY;
+          }
+      }
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int key = key0 + j * 16 + q4 * 4 + r;
-          const bool in = interior || (ok[c] && key >= a0[c] && key <= pos[c]);
-          const float p = in ? __builtin_amdgcn_exp2f(fmaf(st[j][r], sl2, -lse2[c])) : 0.f;
+          const float p = __builtin_amdgcn_exp2f(fmaf(st[j][r], sl2, -lse2[c]));
           dp[j][r] = p * (dp[j][r] - dd[c]);
         }
       // dQ^T += K^T dS^T
@@ -340,6 +379,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
         dq[c][nt] = mfma16x16x32(lds_col8(Ks, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dq[c][nt]);
       }
     }
+    if (kt < kt_hi) {
+      store_tile(buf ^ 1);
+      if (kt + 1 < kt_hi) load_tile(kt + 2);
+    }
+    lds_barrier();
   }
 
   auto dest = [&](int r) {
@@ -350,7 +394,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
 #pragma unroll
   for (int c = 0; c < RT; ++c) {
     const int r0 = (wave * RT + c) * 16;
-    bf16_t *os = Os[wave];
+    bf16_t *os = KV + wave * 16 * SP;  // every wave has passed the loop's last barrier
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const bf16_t o4[4] = {f32_to_bf16(dq[c][nt][0] * gm.scale), f32_to_bf16(dq[c][nt][1] * gm.scale),
@@ -485,7 +529,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       const int av[4] = {a4.x, a4.y, a4.z, a4.w};
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float p = (key <= posv[r] && key >= av[r]) ? __builtin_amdgcn_exp2f(fmaf(s[mt][r], sl2, -lsev[r])) : 0.f;
+        const bool in = key <= posv[r] && key >= av[r];
+        const float p = __builtin_amdgcn_exp2f(in ? fmaf(s[mt][r], sl2, -lsev[r]) : -INFINITY);
         s[mt][r] = p;
         dp[mt][r] = p * (dp[mt][r] - ddv[r]);
       }

@@ -75,6 +75,22 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Cross-row lane exchange with the gfx950 permlane swaps (VALU, no LDS
+// round trip).  v_permlane16_swap exchanges the odd 16-lane rows of its first
+// operand with the even rows of its second, v_permlane32_swap the upper half of
+// the first with the lower half of the second; with x in both operands every
+// lane ends up holding x of itself and of lane l ^ 16 (resp. l ^ 32), in an
+// order that differs between the two lanes.  Commutative reductions of the
+// pair are therefore equal in both lanes.
+__device__ __forceinline__ float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16_t;
