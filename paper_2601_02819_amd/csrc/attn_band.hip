@@ -44,16 +44,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
                                                                bf16_t *__restrict__ opart, float2 *__restrict__ ml) {
   constexpr int RT = 2;                  // 16-row chunks per wave
   constexpr int TOK = 4 * RT * 16 / G;   // tokens per workgroup
-  constexpr int KP = D + 16, VP = D + 16, SP = D + 8;
+  constexpr int SP = D + 8;
   constexpr int VPR = D / 8, KB = D / 32, NT = D / 16;
-  constexpr int NV = 64 * VPR / 256;     // 16-byte loads per thread per tensor per tile
-  constexpr int BUF = 64 * (KP + VP);    // one K tile and one V tile
-  static_assert(4 * 16 * SP <= 2 * BUF, "output staging fits the tile buffers");
-  // two tile buffers: tile kt is read from one while tile kt + 1 is stored into
-  // the other; the output staging of the epilogue reuses them
-  __shared__ __attribute__((aligned(16))) bf16_t KV[2 * BUF];
+  constexpr int TILE = 64 * D;           // one K or V tile (swizzled rows, no padding)
+  static_assert(4 * 16 * SP <= 2 * TILE, "output staging fits a tile buffer");
+  // two buffers of a K tile and a V tile: tile kt is read from one while tile
+  // kt + 1 is copied into the other; two distinct arrays, so that the
+  // compiler can tell the copies into one from the reads of the other.  The
+  // output staging of the epilogue reuses KV0.
+  __shared__ __attribute__((aligned(16))) bf16_t KV0[2 * TILE];
+  __shared__ __attribute__((aligned(16))) bf16_t KV1[2 * TILE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
   // query tiles of one XCD are consecutive (they share most key tiles)
   const int item = xcd_item(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
@@ -95,40 +97,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) o[c][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  // Tile kt + 1 waits in registers while tile kt is used, and is stored into
-  // the other buffer after that use; one barrier per tile then both publishes
-  // tile kt + 1 and ends every wave's reads of tile kt.  The loads of tile
-  // kt + 2 are issued right after the store, a whole tile ahead of their use.
-  // a tile is one uniform base (key kt 64 of (b, g)) plus per-thread 32-bit offsets
-  const int64_t head0 = (int64_t)b * gm.Lk * gm.Hkv * D + (int64_t)g * D, tile_step = (int64_t)64 * gm.Hkv * D;
-  // thread t moves the 16-byte vectors t + 256 v: key t / VPR + (256 / VPR) v,
-  // so only the first offset is per thread and the others are constants
-  static_assert(256 % VPR == 0, "rows per load pass");
-  const int koff = (tid / VPR) * gm.Hkv * D + (tid % VPR) * 8, soff = (tid / VPR) * KP + (tid % VPR) * 8;
-  const int kstep = (256 / VPR) * gm.Hkv * D;
-  u32x4 kr[NV], vr[NV];
-  auto load_tile = [&](int kt) {
-    const bf16_t *kp = K + head0 + kt * tile_step, *vp = V + head0 + kt * tile_step;
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      kr[v] = *reinterpret_cast<const u32x4 *>(kp + v * kstep + koff);
-      vr[v] = *reinterpret_cast<const u32x4 *>(vp + v * kstep + koff);
-    }
+  // Tile kt + 1 is copied into the other buffer while tile kt is used (issued
+  // before the use, a whole tile ahead); one barrier per tile then publishes
+  // it and ends every wave's reads of tile kt.
+  const int64_t head0 = (int64_t)b * gm.Lk * gm.Hkv * D + (int64_t)g * D;
+  const int kstride = gm.Hkv * D;  // elements between consecutive keys of a head
+  auto key_row = [kstride](int r) { return r * kstride; };
+  auto issue = [&](int kt, bf16_t *buf) {
+    const int64_t t0 = head0 + (int64_t)kt * 64 * kstride;
+    tile_dma<D>(K + t0, key_row, buf, wave, lane);
+    tile_dma<D>(V + t0, key_row, buf + TILE, wave, lane);
   };
-  auto store_tile = [&](int buf) {
-    bf16_t *ks = KV + buf * BUF + soff, *vs = ks + 64 * KP;
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      *reinterpret_cast<u32x4 *>(ks + v * (256 / VPR) * KP) = kr[v];
-      *reinterpret_cast<u32x4 *>(vs + v * (256 / VPR) * KP) = vr[v];
-    }
-  };
-  load_tile(kt_lo);
-  store_tile(0);
-  if (kt_lo < kt_hi) load_tile(kt_lo + 1);
-  lds_barrier();
-  for (int kt = kt_lo, buf = 0; kt <= kt_hi; ++kt, buf ^= 1) {
-    const bf16_t *Ks = KV + buf * BUF, *Vs = Ks + 64 * KP;
+  auto step = [&](int kt, const bf16_t *Ks, bf16_t *nxt) {
+    if (kt < kt_hi) issue(kt + 1, nxt);
+    const bf16_t *Vs = Ks + TILE;
     const int key0 = kt * 64;
     // S^T = K Q^T for both chunks (every K fragment read from LDS feeds both)
     f32x4 sa[RT][4];
@@ -140,7 +122,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const bf16x8 kfr = load_bf16x8(&Ks[(j * 16 + l16) * KP + kb * 32 + kq]);
+        const bf16x8 kfr = load_bf16x8(&Ks[swz<D>(j * 16 + l16, kb * 32 + kq)]);
 #pragma unroll
         for (int c = 0; c < RT; ++c) sa[c][j] = mfma16x16x32(kfr, qf[c][kb], sa[c][j]);
       }
@@ -200,8 +182,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
     // ... + V^T P^T for both chunks (every V^T fragment feeds both)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const bf16x8 v0 = lds_col8(Vs, VP, q4 * 4, 16 + q4 * 4, nt * 16, l16);
-      const bf16x8 v1 = lds_col8(Vs, VP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16);
+      const bf16x8 v0 = lds_col8_sw<D>(Vs, q4 * 4, 16 + q4 * 4, nt * 16, l16);
+      const bf16x8 v1 = lds_col8_sw<D>(Vs, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16);
 #pragma unroll
       for (int c = 0; c < RT; ++c) {
         o[c][nt] = mfma16x16x32(v0, pb[c][0], o[c][nt]);
@@ -213,11 +195,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
       lacc[c] = mfma16x16x32(ones, pb[c][0], lacc[c]);
       lacc[c] = mfma16x16x32(ones, pb[c][1], lacc[c]);
     }
-    if (kt < kt_hi) {
-      store_tile(buf ^ 1);
-      if (kt + 1 < kt_hi) load_tile(kt + 2);
-    }
+    dma_wait();
     lds_barrier();
+  };
+  issue(kt_lo, KV0);
+  dma_wait();
+  lds_barrier();
+  for (int kt = kt_lo; kt <= kt_hi; kt += 2) {
+    step(kt, KV0, KV1);
+    if (kt + 1 <= kt_hi) step(kt + 1, KV1, KV0);
   }
 
   // partials: row (token, head) at list position band_base + (b, g, token); rows
@@ -231,7 +217,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
   for (int c = 0; c < RT; ++c) {
     const int r0 = (wave * RT + c) * 16;
     ml[q4 == 0 ? dest(r0 + l16) : ix.discard] = make_float2(mrun[c], lacc[c][0]);
-    bf16_t *os = KV + wave * 16 * SP;  // every wave has passed the loop's last barrier
+    bf16_t *os = KV0 + wave * 16 * SP;  // every wave has passed the loop's last barrier
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const bf16_t o4[4] = {f32_to_bf16(o[c][nt][0]), f32_to_bf16(o[c][nt][1]), f32_to_bf16(o[c][nt][2]),

@@ -172,6 +172,48 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// 64-row bf16 tiles in LDS without padding.  Row r holds D elements; its
+// 16-byte chunk c sits at chunk position c ^ (r mod D / 8), which spreads the
+// rows that one 16-lane group reads (row reads of MFMA operands and the
+// transposing reads) over the LDS banks.  Element offset of (r, e):
+template <int D>
+__device__ __forceinline__ int swz(int r, int e) {
+  return r * D + ((((e >> 3) ^ r) & (D / 8 - 1)) << 3) + (e & 7);
+}
+
+// 8-element column fragment of a swizzled tile (the layout of lds_col8).
+template <int D>
+__device__ __forceinline__ bf16x8 lds_col8_sw(const bf16_t *X, int r0, int r1, int c0, int l16) {
+  const int e = c0 + 4 * (l16 & 3);
+  const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(X + swz<D>(r0 + (l16 >> 2), e)));
+  const v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(X + swz<D>(r1 + (l16 >> 2), e)));
+  const v8i16 c = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return __builtin_bit_cast(bf16x8, c);
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Copies a 64-row tile from global memory straight into LDS in the swizzled
+// layout (global_load_lds: no registers, no LDS store instructions).  Each of
+// the 4 waves issues D / 32 one-kilobyte copies; lane l of a copy lands at
+// byte 16 l of it and fetches the chunk that belongs there.  Row r starts at
+// element row_off(r) of src.  The copies count in vmcnt: each wave waits for
+// vmcnt(0) and the workgroup then passes a barrier before the tile is read.
+// wave must be wave-uniform (it selects the LDS destination).
+template <int D, typename RowOff>
+__device__ __forceinline__ void tile_dma(const bf16_t *src, RowOff row_off, bf16_t *dst, int wave, int lane) {
+  constexpr int VPR = D / 8, RPI = 64 / VPR, NI = 64 / RPI / 4;
+#pragma unroll
+  for (int v = 0; v < NI; ++v) {
+    const int blk = wave * NI + v, r = blk * RPI + lane / VPR, c = (lane % VPR) ^ (r & (VPR - 1));
+    __builtin_amdgcn_global_load_lds(src + row_off(r) + c * 8, (lds_void_t *)(dst + blk * RPI * D), 16, 0, 0);
+  }
+}
+
+// Waits until this wave's tile_dma copies have landed in LDS (vmcnt(0); the
+// other counters are left alone).
+__device__ __forceinline__ void dma_wait() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+
 // Packs two 4-element float groups into a bf16 MFMA operand (elements 0..3,
 // then 4..7), rounding to nearest even with the packed conversion instruction.
 typedef float f32x8 __attribute__((ext_vector_type(8)));
