@@ -96,6 +96,87 @@ def summarize_traffic(fetch_csv: str, write_csv: str, copy_mb: int, out_json: st
                              "bytes_per_launch": f + w, "source_hash": source_hash(k)}
     json.dump(rec, open(out_json, "w"), indent=1)
     print(json.dumps(rec, indent=1))
+# Three rocprofv3 --pmc passes (at most 8 SQ counters and one GRBM counter each)
+# whose counter_collection.csv files --summarize-counters turns into a table.
+COUNTER_PASSES = (
+    "SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY "
+    "SQ_WAIT_INST_LDS SQ_ACTIVE_INST_ANY SQ_BUSY_CU_CYCLES GRBM_GUI_ACTIVE",
+    "SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_LDS SQ_INSTS_SALU SQ_INSTS_VMEM SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE "
+    "SQ_ACTIVE_INST_LDS GRBM_GUI_ACTIVE",
+    "SQ_INSTS_VALU_TRANS_F32 SQ_LDS_ADDR_CONFLICT SQ_LDS_DATA_FIFO_FULL SQ_LDS_CMD_FIFO_FULL SQ_INSTS_VMEM_RD "
+    "SQ_INSTS_VMEM_WR SQ_INSTS_SMEM SQ_ACTIVE_INST_VALU GRBM_GUI_ACTIVE",
+)
+
+
+def summarize_counters(out_md: str, csvs) -> None:
+    """Per-kernel table from rocprofv3 --pmc counter_collection.csv files (the
+    passes of COUNTER_PASSES, any order).  Values are medians over a kernel's
+    dispatches; the topology (XCCs, SIMDs, CUs) comes from the agent_info.csv
+    written beside each counter file.  Derived columns:
+      MFMA busy   SQ_VALU_MFMA_BUSY_CYCLES / (kernel cycles x SIMDs), kernel
+                  cycles = GRBM_GUI_ACTIVE / XCCs (GRBM counts on every XCC)
+      co-exec     share of MFMA-busy cycles in which a VALU instruction issued
+      VALU/MFMA, LDS/MFMA, exp/MFMA   instruction counts per MFMA instruction
+                  (SQ_INSTS_VALU counts MFMA instructions too)
+      bank confl. SQ_LDS_BANK_CONFLICT / (SQ_LDS_IDX_ACTIVE - SQ_LDS_BANK_CONFLICT)
+      waits       SQ_WAIT_INST_LDS, SQ_WAIT_INST_ANY, SQ_WAIT_ANY as shares of
+                  SQ_WAVE_CYCLES (all in quad-cycles)
+      waves/CU    resident waves per CU on average (4 SQ_WAVE_CYCLES / cycles / CUs)"""
+    import csv
+    import glob
+    import statistics
+
+    per, dur, topo = {}, {}, {}
+    for path in csvs:
+        for ai in glob.glob(os.path.join(os.path.dirname(path), "*agent_info.csv")):
+            for r in csv.DictReader(open(ai)):
+                if r.get("Name", "").startswith("gfx"):
+                    topo = {k: int(r[k]) for k in ("Num_Xcc", "Simd_Count", "Cu_Count")}
+        for r in csv.DictReader(open(path)):
+            sym = r["Kernel_Name"].split("(")[0].replace("void ", "")
+            per.setdefault(sym, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            if r["Counter_Name"] == "GRBM_GUI_ACTIVE":
+                dur.setdefault(sym, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-6)
+    if not topo:
+        raise SystemExit("no gfx agent in the agent_info.csv files beside " + " ".join(csvs))
+
+    def ratio(a, b):
+        return a / b if b else float("nan")
+
+    rows = []
+    for sym, c in per.items():
+        m = {k: statistics.median(v) for k, v in c.items()}
+        need = ("GRBM_GUI_ACTIVE", "SQ_INSTS_MFMA", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_WAVE_CYCLES")
+        if any(k not in m for k in need) or m["SQ_INSTS_MFMA"] == 0 and "phsa::" not in sym:
+            continue
+        cyc = m["GRBM_GUI_ACTIVE"] / topo["Num_Xcc"]
+        ms = statistics.median(dur[sym])
+        wc = m["SQ_WAVE_CYCLES"]
+        rows.append((ms, sym, [
+            f"{ms:.3f}", f"{cyc / ms * 1e-6:.2f}",
+            f"{100 * ratio(m['SQ_VALU_MFMA_BUSY_CYCLES'], cyc * topo['Simd_Count']):.1f}",
+            f"{100 * ratio(m.get('SQ_VALU_MFMA_COEXEC_CYCLES', 0), m['SQ_VALU_MFMA_BUSY_CYCLES']):.0f}",
+            f"{ratio(m.get('SQ_INSTS_VALU', 0), m['SQ_INSTS_MFMA']):.2f}",
+            f"{ratio(m.get('SQ_INSTS_LDS', 0), m['SQ_INSTS_MFMA']):.2f}",
+            f"{ratio(m.get('SQ_INSTS_VALU_TRANS_F32', 0), m['SQ_INSTS_MFMA']):.2f}",
+            f"{100 * ratio(m.get('SQ_LDS_BANK_CONFLICT', 0), m.get('SQ_LDS_IDX_ACTIVE', 0) - m.get('SQ_LDS_BANK_CONFLICT', 0)):.0f}",
+            f"{100 * ratio(m.get('SQ_WAIT_INST_LDS', 0), wc):.0f}",
+            f"{100 * ratio(m.get('SQ_WAIT_INST_ANY', 0), wc):.0f}",
+            f"{100 * ratio(m.get('SQ_WAIT_ANY', 0), wc):.0f}",
+            f"{4 * wc / cyc / topo['Cu_Count']:.1f}",
+            f"{m['SQ_INSTS_MFMA']:.3g}", f"{m.get('SQ_INSTS_VALU', float('nan')):.3g}",
+            f"{m.get('SQ_INSTS_LDS', float('nan')):.3g}"]))
+    rows.sort(reverse=True)
+    head = ["kernel", "ms", "GHz", "MFMA busy %", "co-exec %", "VALU/MFMA", "LDS/MFMA", "exp/MFMA",
+            "bank confl. %", "wait LDS %", "wait inst %", "wait any %", "waves/CU", "MFMA insts", "VALU insts",
+            "LDS insts"]
+    lines = ["| " + " | ".join(head) + " |", "|" + "---|" * len(head)]
+    lines += ["| `" + sym + "` | " + " | ".join(v) + " |" for _, sym, v in rows]
+    text = "\n".join(lines) + "\n"
+    open(out_md, "w").write(text)
+    print(text)
+
+
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 
@@ -486,9 +567,17 @@ def main():
                          "calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM traffic of the dominant kernel (from rocprofv3 counters)")
+    ap.add_argument("--summarize-counters", nargs="+", metavar=("OUT_MD", "CSV"),
+                    help="write a per-kernel counter table (markdown) from rocprofv3 --pmc counter_collection.csv "
+                         "files of the COUNTER_PASSES passes and exit")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write --traffic from two rocprofv3 --pmc counter_collection.csv files and exit")
     args = ap.parse_args()
+    if args.summarize_counters:
+        if len(args.summarize_counters) < 2:
+            ap.error("--summarize-counters OUT_MD CSV [CSV ...]")
+        summarize_counters(args.summarize_counters[0], args.summarize_counters[1:])
+        return
     if args.summarize_traffic:
         summarize_traffic(args.summarize_traffic[0], args.summarize_traffic[1], args.calib_copy_mb or 1024,
                           args.traffic)

@@ -48,13 +48,15 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
                                                               bf16_t *__restrict__ opart, float2 *__restrict__ ml) {
   constexpr int TW = 16 / G;         // query tokens per wave chunk
   constexpr int KP = D + 16;         // K pitch: 16-byte row reads of 16 rows are conflict-free at D + 16
-  constexpr int VP = D + 8;          // V pitch (transposing reads only)
   constexpr int VPR = D / 8;         // 16-byte vectors per row
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
   constexpr int SP = D + 8;          // pitch of the per-wave output staging rows
   __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * VP];
+  // V is read by transposing reads only; it is stored without padding in the
+  // swizzled layout of swz() (with D + 8 padding those reads conflict, and D + 16
+  // would not leave three workgroups per CU)
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * D];
   __shared__ __attribute__((aligned(16))) bf16_t Os[4][16 * SP];  // per-wave partial rows
 
   const int u = blockIdx.x;
@@ -75,7 +77,7 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
     const int kk = x / VPR, c = (x % VPR) * 8;
     const int64_t grow = ((int64_t)b * gm.Lk + (int64_t)t * 64 + kk) * gm.Hkv + g;
     *reinterpret_cast<uint4 *>(&Ks[kk * KP + c]) = *reinterpret_cast<const uint4 *>(K + grow * D + c);
-    *reinterpret_cast<uint4 *>(&Vs[kk * VP + c]) = *reinterpret_cast<const uint4 *>(V + grow * D + c);
+    *reinterpret_cast<uint4 *>(&Vs[swz<D>(kk, c)]) = *reinterpret_cast<const uint4 *>(V + grow * D + c);
   }
   __syncthreads();
 
@@ -146,8 +148,8 @@ __global__ __launch_bounds__(256, 3) void attn_fwd_sparse_kernel(const bf16_t *_
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       ot[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      ot[nt] = mfma16x16x32(lds_col8(Vs, VP, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, ot[nt]);
-      ot[nt] = mfma16x16x32(lds_col8(Vs, VP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, ot[nt]);
+      ot[nt] = mfma16x16x32(lds_col8_sw<D>(Vs, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, ot[nt]);
+      ot[nt] = mfma16x16x32(lds_col8_sw<D>(Vs, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, ot[nt]);
     }
     // The chunk's 16 partial rows are one contiguous run of the list-ordered
     // partial buffer (entries c*TW.., heads inner): stage them in LDS and write
