@@ -242,7 +242,8 @@ def gpu_clocks():
 
 KERNELS = ["phsa_compress", "phsa_select_split", "phsa_select", "phsa_index_count", "phsa_index_scan_tiles", "phsa_index_scan_lists",
            "phsa_index_fill", "phsa_attn_fwd_sparse", "phsa_attn_fwd_band", "phsa_attn_fwd_combine",
-           "phsa_attn_bwd_pre", "phsa_attn_bwd_band_dkv", "phsa_attn_bwd_band_dq", "phsa_attn_bwd_sparse",
+           "phsa_attn_bwd_pre", "phsa_attn_bwd_band_dkv_init", "phsa_attn_bwd_band_init_reduce", "phsa_attn_bwd_band_dkv",
+           "phsa_attn_bwd_band_dq", "phsa_attn_bwd_sparse",
            "phsa_attn_bwd_dkv_finalize", "phsa_attn_bwd_dq_combine"]
 
 
@@ -260,18 +261,28 @@ def selected_tiles(sel: torch.Tensor, seqlen_k: int, block: int) -> int:
 
 def band_blocks(sel: torch.Tensor, seqlen_k: int, block: int, n_init: int, window: int):
     """Per (b, g, query row): how many of its selected blocks the band kernels
-    take (bf16 attention with a window of at least 64 keys).  A row whose
-    selection holds every local block outside the init blocks, A .. cur with
-    A = max(cur - window / block, min(n_init, cur + 1)), leaves those blocks to
+    take (bf16 attention).  A row whose selection holds all its forced blocks,
+    the init blocks 0 .. ninit - 1 (ninit = min(n_init, cur + 1)) and the local
+    window A .. cur with A = max(cur - window / block, ninit), leaves them to
     the band; other rows keep all their blocks in the sparse kernels.  Returns
-    the counts and A per row."""
+    the counts, A, and the counts' init blocks, per row (0 for other rows)."""
     Lq = sel.shape[2]
     cur = ((seqlen_k - Lq + torch.arange(Lq, device=sel.device)) // block).view(1, 1, Lq)
-    a = torch.maximum((cur - window // block).clamp(min=0), torch.clamp(cur + 1, max=n_init))
+    ninit = torch.clamp(cur + 1, max=n_init)
+    a = torch.maximum((cur - window // block).clamp(min=0), ninit)
     valid = (sel >= 0) & (sel <= cur.unsqueeze(-1))
-    have = (valid & (sel >= a.unsqueeze(-1))).sum(-1)
-    ok = (a <= cur) & (have == cur - a + 1)
-    return torch.where(ok, cur - a + 1, torch.zeros_like(cur)), a
+    forced = valid & ((sel < ninit.unsqueeze(-1)) | (sel >= a.unsqueeze(-1)))
+    need = ninit + cur - a + 1
+    ok = forced.sum(-1) == need
+    zero = torch.zeros_like(cur)
+    return torch.where(ok, need, zero), a, torch.where(ok, ninit, zero)
+
+
+def sparse_part(sel: torch.Tensor, nb: torch.Tensor, a: torch.Tensor, ninit: torch.Tensor) -> torch.Tensor:
+    """sel without the blocks that band_blocks gives to the band kernels."""
+    band_row = (nb > 0).unsqueeze(-1)
+    forced = (sel < ninit.unsqueeze(-1)) | (sel >= a.unsqueeze(-1))
+    return torch.where(band_row & forced, torch.full_like(sel, -1), sel)
 
 
 def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
@@ -295,14 +306,13 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
         sel = step()
     torch.cuda.synchronize()
     nsel = selected_blocks(sel, L, m)
-    band = wl.window >= 64 and min(wl.ksel, L // 64) <= 63  # the library's rule for bf16 attention
+    band = wl.window >= 64 and L % 64 == 0 and min(wl.ksel, L // 64) <= 63  # the library's rule for bf16 attention
     if band:
-        nb, a = band_blocks(sel, L, m, wl.n_init_blocks, wl.window)
-        # the band rows' local blocks are the top of their ascending lists
-        sparse_sel = torch.where((nb > 0).unsqueeze(-1) & (sel >= a.unsqueeze(-1)), torch.full_like(sel, -1), sel)
-        nband = int(nb.sum().item())
+        nb, a, ni = band_blocks(sel, L, m, wl.n_init_blocks, wl.window)
+        sparse_sel = sparse_part(sel, nb, a, ni)
+        nband, nband_init = int(nb.sum().item()), int(ni.sum().item())
     else:
-        sparse_sel, nband = sel, 0
+        sparse_sel, nband, nband_init = sel, 0, 0
     ntile = selected_tiles(sparse_sel, L, m)  # the sparse kernels' tiles
     # headline: `steps` steps of the product library, one HIP event between steps
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
@@ -329,8 +339,10 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
 
     fwd_flop = 4.0 * d * m * nsel * G
     bwd_flop = 2.5 * fwd_flop
-    # the local windows' share, attended by the band kernels (same convention)
+    # the forced blocks' share, attended by the band kernels (same convention);
+    # the init tiles' dK/dV run in a launch of their own
     band_fwd_flop = 4.0 * d * m * nband * G
+    band_init_fwd_flop = 4.0 * d * m * nband_init * G
     sparse_fwd_flop = fwd_flop - band_fwd_flop
     # MFMA work the kernels execute: whole 64-key tiles (blocks below 64 tokens
     # share tiles, the unselected quarters of a tile are masked)
@@ -355,7 +367,8 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
             "phsa_compress": ("GB/s", bytes_compress / 1e9), "phsa_select": ("GB/s", bytes_select / 1e9)}
     if nband:
         work.update({"phsa_attn_fwd_band": ("TFLOP/s", band_fwd_flop / 1e12),
-                     "phsa_attn_bwd_band_dkv": ("TFLOP/s", 2.0 * band_fwd_flop / 1e12),
+                     "phsa_attn_bwd_band_dkv": ("TFLOP/s", 2.0 * (band_fwd_flop - band_init_fwd_flop) / 1e12),
+                     "phsa_attn_bwd_band_dkv_init": ("TFLOP/s", 2.0 * band_init_fwd_flop / 1e12),
                      "phsa_attn_bwd_band_dq": ("TFLOP/s", 1.5 * band_fwd_flop / 1e12)})
     for n, (unit, amount) in work.items():
         if n in ks:
@@ -380,6 +393,7 @@ def bench_train(steps: int, warmup: int, seed: int, name: str = "train_32k"):
         "kernel_timing": f"{prof_steps} steps through libphsa_prof.so (HIP events around each launch)",
         "value": (fwd_flop + bwd_flop) / 1e12 / (ms_step / 1e3),
         "fwd_flop": fwd_flop, "bwd_flop": bwd_flop, "selected_blocks": nsel, "band_blocks": nband,
+        "band_init_blocks": nband_init,
         "sparse_tiles": ntile,
         "tile_fwd_flop": tile_fwd_flop,
         # the paper's convention: active tokens of the last query over the sequence length

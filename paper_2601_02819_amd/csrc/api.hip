@@ -46,10 +46,14 @@ size_t index_layout(const Geom &g, char *base, IndexWs *ix) {
 }
 
 // bf16 attention with a local window of at least one 64-key tile attends to
-// the windows with the band kernels (dense, query-major for O and dQ,
-// key-major for dK/dV) and to the other selected blocks with the sparse ones.
+// every row's forced blocks (init blocks and local window, Algorithm 1) with
+// the band kernels (dense, query-major for O and dQ, key-major for dK/dV) and
+// to its other selected blocks with the sparse ones.  Without a window a row
+// has two forced tiles (block 0 and its own), too few for the band kernels'
+// per-workgroup cost: at 4 x 32k with 64-token blocks the band took the step
+// from 11.95 to 12.74 ms, so those forced blocks stay in the sparse kernels.
 bool band_on(const Geom &g) {
-  return g.dtype == PHSA_BF16 && g.window >= 64 && std::min(g.ksel, g.Lk / 64) <= 63;
+  return g.dtype == PHSA_BF16 && g.window >= 64 && g.Lk % 64 == 0 && std::min(g.ksel, g.Lk / 64) <= 63;
 }
 
 // bf16 attention with blocks of m = 16 or 32 tokens, or with the band, runs

@@ -1,29 +1,36 @@
-// Local windows as dense attention (the "band"), bf16.
+// The forced blocks as dense attention (the "band"), bf16.
 //
-// Algorithm 1 always keeps the local window: blocks max(0, cur - w/m) .. cur
-// of every query row, i.e. the keys [A(i), pos(i)] with
+// Algorithm 1 always keeps the init blocks 0 .. n_init - 1 and the local
+// window, blocks max(0, cur - w/m) .. cur, of every query row: the keys
+// [0, n_init m) up to the row and [A(i), pos(i)] with
 //   A(i) = max(cur - w/m, min(n_init, cur + 1)) * m
-// (the init blocks below it stay with the sparse kernels).  These key ranges
-// slide with the row, so consecutive rows share almost all of them.  In the
-// key-block-major sparse kernels each (row, window tile) pair would gather
-// the row and leave a partial; here the window is attended densely instead:
+// (w = 0: the row's own block).  Every row shares the init keys and
+// neighbouring rows share most of their windows.  In the key-block-major
+// sparse kernels each (row, forced tile) pair would gather the row and leave
+// a partial; here the forced keys are attended densely instead:
 //   forward, dQ : query-major.  A workgroup holds 128 (token, head) MFMA rows
 //                 (128 / G consecutive tokens) in registers and streams the
-//                 64-key tiles covering their windows through LDS, with an
-//                 online softmax (forward) or the dQ accumulation (backward).
-//                 A row leaves one partial in the same format and buffer as
-//                 the sparse partials, at list position band_base + row; the
-//                 per-row merges find it through the row's last index slot.
+//                 64-key tiles of their forced keys (the init tiles, then the
+//                 window tiles) through LDS, with an online softmax (forward)
+//                 or the dQ accumulation (backward).  A row leaves one partial
+//                 in the same format and buffer as the sparse partials, at
+//                 list position band_base + row; the per-row merges find it
+//                 through the row's last index slot.
 //   dK, dV      : key-major.  A workgroup holds one 64-key tile (wave w owns
 //                 keys 16w..16w+15, accumulators in registers) and streams the
-//                 contiguous rows whose windows reach into it; it writes the
-//                 tile's float32 dK/dV to bkv, which the sparse backward's
-//                 epilogue and the dK/dV finalize add to the sparse part.
-// Only rows that hold their whole window (bflag, set when the selection is
-// regrouped) take part; other rows keep every block in the sparse kernels.
-// Operand layouts and the transposing LDS reads are those of the sparse
-// kernels (attn_fwd.hip, attn_bwd.hip).
+//                 contiguous rows whose forced keys reach into it; it writes
+//                 the tile's float32 dK/dV to bkv, which the sparse backward's
+//                 epilogue and the dK/dV finalize add to the sparse part.  An
+//                 init tile is reached by every later row: its rows are split
+//                 into segments, one workgroup each, whose float32 sums a
+//                 reduction adds up into bkv in segment order.
+// Only rows that hold all their forced blocks (bflag, set by the index) take
+// part; other rows keep every block in the sparse kernels.  Operand layouts
+// and the transposing LDS reads are those of the sparse kernels (attn_fwd.hip,
+// attn_bwd.hip).
 #include <math.h>
+
+#include <algorithm>
 
 #include "common.h"
 #include "launch.h"
@@ -35,6 +42,26 @@ __device__ __forceinline__ int band_first_key(const Geom &gm, int pos) {
   const int cur = pos / gm.sm;
   return max(max(0, cur - gm.window / gm.sm), min(gm.n_init, cur + 1)) * gm.sm;
 }
+
+// Keys of the init blocks: a band row attends to [0, init_end) up to itself
+// and to its local window [A(i), pos(i)] (A(i) >= init_end once the row is
+// past the init blocks).
+__device__ __forceinline__ int init_end_key(const Geom &gm) { return gm.n_init * gm.sm; }
+__device__ __forceinline__ bool forced_key(int key, int pos, int a, int init_end) {
+  return key <= pos && (key < init_end || key >= a);
+}
+
+// The 64-key tiles a query-major workgroup visits: the init tiles it reaches,
+// then the window tiles past them.  Tile j of ntile is tile_of(j).
+struct TileSeq {
+  int nit, kt_b, ntile;
+  __device__ __forceinline__ TileSeq(int kt_lo, int kt_hi, int init_end) {
+    nit = min((init_end + 63) / 64, kt_hi + 1);
+    kt_b = max(kt_lo, nit);
+    ntile = nit + max(0, kt_hi - kt_b + 1);
+  }
+  __device__ __forceinline__ int tile_of(int j) const { return j < nit ? j : kt_b + (j - nit); }
+};
 
 // ---------------------------------------------------------------- forward
 template <int D, int G>
@@ -83,6 +110,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
   if (!__syncthreads_or(ok[0] || ok[RT - 1])) return;
   const int kt_lo = band_first_key(gm, gm.q_pos0 + i0) / 64, kt_hi = (gm.q_pos0 + i1) / 64;
   const int a_last = band_first_key(gm, gm.q_pos0 + i1), pos_first = gm.q_pos0 + i0;
+  const int init_end = init_end_key(gm);
+  const TileSeq seq(kt_lo, kt_hi, init_end);
 
   const float sl2 = gm.scale * kLog2e;
   // the row sums l accumulate on the matrix cores: an all-ones A operand
@@ -108,10 +137,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
     tile_dma<D>(K + t0, key_row, buf, wave, lane);
     tile_dma<D>(V + t0, key_row, buf + TILE, wave, lane);
   };
-  auto step = [&](int kt, const bf16_t *Ks, bf16_t *nxt) {
-    if (kt < kt_hi) issue(kt + 1, nxt);
+  auto step = [&](int j, const bf16_t *Ks, bf16_t *nxt) {
+    if (j + 1 < seq.ntile) issue(seq.tile_of(j + 1), nxt);
     const bf16_t *Vs = Ks + TILE;
-    const int key0 = kt * 64;
+    const int key0 = seq.tile_of(j) * 64;
     // S^T = K Q^T for both chunks (every K fragment read from LDS feeds both)
     f32x4 sa[RT][4];
 #pragma unroll
@@ -126,9 +155,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 #pragma unroll
         for (int c = 0; c < RT; ++c) sa[c][j] = mfma16x16x32(kfr, qf[c][kb], sa[c][j]);
       }
-    // Tiles inside every row's band (all but the first and last one or two)
-    // need no mask: rows outside the band compute values that are discarded.
-    const bool interior = key0 >= a_last && key0 + 63 <= pos_first;
+    // Tiles inside every row's forced keys (all but the first and last one or
+    // two) need no mask: rows outside the band compute values that are discarded.
+    const bool interior = key0 + 63 <= pos_first && (key0 + 63 < init_end || key0 >= a_last);
     bf16x8 pb[RT][2];
     float fs[RT];
 #pragma unroll
@@ -140,7 +169,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int key = key0 + j * 16 + q4 * 4 + r;
-            st[j][r] = (ok[c] && key >= a0[c] && key <= pos[c]) ? st[j][r] : -INFINITY;
+            st[j][r] = (ok[c] && forced_key(key, pos[c], a0[c], init_end)) ? st[j][r] : -INFINITY;
           }
       }
       // IEEE maximum (v_maximum3_f32): no quieting pass over the accumulators
@@ -198,12 +227,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
     dma_wait();
     lds_barrier();
   };
-  issue(kt_lo, KV0);
+  if (seq.ntile > 0) issue(seq.tile_of(0), KV0);
   dma_wait();
   lds_barrier();
-  for (int kt = kt_lo; kt <= kt_hi; kt += 2) {
-    step(kt, KV0, KV1);
-    if (kt + 1 <= kt_hi) step(kt + 1, KV1, KV0);
+  for (int j = 0; j < seq.ntile; j += 2) {
+    step(j, KV0, KV1);
+    if (j + 1 < seq.ntile) step(j + 1, KV1, KV0);
   }
 
   // partials: row (token, head) at list position band_base + (b, g, token); rows
@@ -284,6 +313,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
   if (!__syncthreads_or(ok[0])) return;
   const int kt_lo = band_first_key(gm, gm.q_pos0 + i0) / 64, kt_hi = (gm.q_pos0 + i1) / 64;
   const int a_last = band_first_key(gm, gm.q_pos0 + i1), pos_first = gm.q_pos0 + i0;
+  const int init_end = init_end_key(gm);
+  const TileSeq seq(kt_lo, kt_hi, init_end);
 
   const float sl2 = gm.scale * kLog2e;
   f32x4 dq[RT][NT];
@@ -317,14 +348,16 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
       *reinterpret_cast<u32x4 *>(vs + v * (256 / VPR) * KP) = vr[v];
     }
   };
-  load_tile(kt_lo);
-  store_tile(0);
-  if (kt_lo < kt_hi) load_tile(kt_lo + 1);
+  if (seq.ntile > 0) {
+    load_tile(seq.tile_of(0));
+    store_tile(0);
+    if (seq.ntile > 1) load_tile(seq.tile_of(1));
+  }
   lds_barrier();
-  for (int kt = kt_lo, buf = 0; kt <= kt_hi; ++kt, buf ^= 1) {
+  for (int jt = 0, buf = 0; jt < seq.ntile; ++jt, buf ^= 1) {
     const bf16_t *Ks = KV + buf * BUF, *Vs = Ks + 64 * KP;
-    const int key0 = kt * 64;
-    const bool interior = key0 >= a_last && key0 + 63 <= pos_first;
+    const int key0 = seq.tile_of(jt) * 64;
+    const bool interior = key0 + 63 <= pos_first && (key0 + 63 < init_end || key0 >= a_last);
 #pragma unroll
     for (int c = 0; c < RT; ++c) {
       // S^T = K Q^T and dP^T = V dO^T: lane (q, j) holds keys 16 jt + 4 q + r of row j
@@ -347,7 +380,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int key = key0 + j * 16 + q4 * 4 + r;
-            st[j][r] = (ok[c] && key >= a0[c] && key <= pos[c]) ? st[j][r] : -INFINITY;
+            st[j][r] = (ok[c] && forced_key(key, pos[c], a0[c], init_end)) ? st[j][r] : -INFINITY;
           }
       }
 #pragma unroll
@@ -365,9 +398,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
         dq[c][nt] = mfma16x16x32(lds_col8(Ks, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dq[c][nt]);
       }
     }
-    if (kt < kt_hi) {
+    if (jt + 1 < seq.ntile) {
       store_tile(buf ^ 1);
-      if (kt + 1 < kt_hi) load_tile(kt + 2);
+      if (jt + 2 < seq.ntile) load_tile(seq.tile_of(jt + 2));
     }
     lds_barrier();
   }
@@ -398,14 +431,18 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
 }
 
 // ---------------------------------------------------------------- backward: dK, dV
-// One workgroup per (b, g, 64-key tile kt).  The rows whose band reaches into
-// the tile are tokens kt 64 - q_pos0 .. (the last token with A(i) <= kt 64 + 63);
-// they stream through in chunks of 64 MFMA rows (64 / G tokens, heads inner).
+// One workgroup per (b, g, 64-key tile kt, row segment).  The rows whose
+// forced keys reach into the tile are tokens kt 64 - q_pos0 .. (the last token
+// with A(i) <= kt 64 + 63), or every later token for an init tile; they stream
+// through in chunks of 64 MFMA rows (64 / G tokens, heads inner).  Work item x
+// of a (b, g) is tile kt0 + x / nseg, segment x % nseg (tokens seg_tok seg ..
+// seg_tok (seg + 1) - 1); the tile's float32 dK, dV go to slot
+// ((b, g) out_tiles + kt) nseg + seg of out.
 template <int D, int G>
 __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
     const bf16_t *__restrict__ Q, const bf16_t *__restrict__ K, const bf16_t *__restrict__ V,
     const bf16_t *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dvec, Geom gm, IndexWs ix,
-    float *__restrict__ bkv) {
+    int kt0, int nseg, int seg_tok, int out_tiles, float *__restrict__ out) {
   constexpr int CT = 64 / G;             // tokens per chunk
   constexpr int KPQ = D + 16;
   constexpr int VPR = D / 8, KB = D / 32, NT = D / 16;
@@ -424,13 +461,22 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
   // key tiles of one XCD are consecutive (they share most rows)
   const int item = xcd_item(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
-  const int kt = item % gridDim.x, bg = item / gridDim.x, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
+  const int xi = item % gridDim.x, bg = item / gridDim.x, b = bg / gm.Hkv, g = bg - b * gm.Hkv;
+  const int kt = kt0 + xi / nseg, seg = xi % nseg;
   const uint8_t *bf = ix.bflag + (int64_t)bg * gm.Lq;
   const int key0 = kt * 64;
-  // rows: from the first token that sees key0 to the last whose band starts by key0 + 63
-  const int r_lo = max(0, key0 - gm.q_pos0);
-  const int cmax = (key0 + 63) / gm.sm + gm.window / gm.sm;
-  const int r_hi = min(gm.Lq - 1, (cmax + 1) * gm.sm - 1 - gm.q_pos0);
+  const int init_end = init_end_key(gm);
+  // rows: from the first token that sees key0 to the last whose window starts
+  // by key0 + 63 (every later token, for a tile holding init keys), within the
+  // segment
+  int r_lo = max(0, key0 - gm.q_pos0);
+  int r_hi = gm.Lq - 1;
+  if (key0 >= init_end) {
+    const int cmax = (key0 + 63) / gm.sm + gm.window / gm.sm;
+    r_hi = min(r_hi, (cmax + 1) * gm.sm - 1 - gm.q_pos0);
+  }
+  r_lo = max(r_lo, seg * seg_tok);
+  r_hi = min(r_hi, seg * seg_tok + seg_tok - 1);
 
   // the tile's keys and values (wave w reads its keys 16w..16w+15 as B operands)
   for (int x = tid; x < 64 * VPR; x += 256) {
@@ -515,7 +561,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       const int av[4] = {a4.x, a4.y, a4.z, a4.w};
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const bool in = key <= posv[r] && key >= av[r];
+        const bool in = forced_key(key, posv[r], av[r], init_end);
         const float p = __builtin_amdgcn_exp2f(in ? fmaf(s[mt][r], sl2, -lsev[r]) : -INFINITY);
         s[mt][r] = p;
         dp[mt][r] = p * (dp[mt][r] - ddv[r]);
@@ -533,13 +579,35 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
     }
   }
   // the tile's dK (scaled) and dV: lane (q, j) holds features 16 nt + 4 q .. +3 of key 16 w + j
-  float *pk = bkv + ((int64_t)bg * gm.T + kt) * 2 * 64 * D + (wave * 16 + l16) * D + q4 * 4;
+  float *pk = out + (((int64_t)bg * out_tiles + kt) * nseg + seg) * 2 * 64 * D + (wave * 16 + l16) * D + q4 * 4;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     *reinterpret_cast<float4 *>(pk + nt * 16) =
         make_float4(dkt[nt][0] * gm.scale, dkt[nt][1] * gm.scale, dkt[nt][2] * gm.scale, dkt[nt][3] * gm.scale);
     *reinterpret_cast<float4 *>(pk + 64 * D + nt * 16) = make_float4(dvt[nt][0], dvt[nt][1], dvt[nt][2], dvt[nt][3]);
   }
+}
+
+// Sums the row segments of each init tile (in segment order) into bkv:
+// workgroup (tile of a (b, g), part) adds 1024 consecutive floats of the
+// tile's 2 x 64 x d.
+template <int D>
+__global__ __launch_bounds__(256) void band_init_reduce_kernel(const float *__restrict__ seg_sums, float *__restrict__ bkv,
+                                                                Geom gm, int nit, int nseg) {
+  constexpr int PER = 2 * 64 * D;
+  const int bgk = blockIdx.x, bg = bgk / nit, kt = bgk - bg * nit;
+  const int x = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (x >= PER) return;
+  const float *src = seg_sums + (int64_t)bgk * nseg * PER + x;
+  float4 acc = *reinterpret_cast<const float4 *>(src);
+  for (int sg = 1; sg < nseg; ++sg) {
+    const float4 v = *reinterpret_cast<const float4 *>(src + (int64_t)sg * PER);
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  *reinterpret_cast<float4 *>(bkv + ((int64_t)bg * gm.T + kt) * PER + x) = acc;
 }
 
 // ---------------------------------------------------------------- launchers
@@ -555,20 +623,47 @@ static hipError_t fwd_band_t(const Geom &g, const void *Q, const void *K, const 
   return hipGetLastError();
 }
 
+// Init tiles that every row reaches are split into segments of about
+// kInitSegTokens tokens, at most T / nit per tile so that their float32 sums
+// fit in the sparse backward's dK/dV partial buffer, which they borrow.
+constexpr int kInitSegTokens = 1024;
+
+int band_init_tiles(const Geom &g) { return std::min((g.n_init * g.sm + 63) / 64, g.T); }
+
+int band_init_segments(const Geom &g) {
+  const int nit = band_init_tiles(g);
+  if (nit == 0) return 0;
+  return std::max(1, std::min((g.Lq + kInitSegTokens - 1) / kInitSegTokens, g.T / nit));
+}
+
 template <int D, int G>
 static hipError_t bwd_band_t(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
                              const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
-                             hipStream_t s) {
-  timing_begin("phsa_attn_bwd_band_dkv", s);
-  hipLaunchKernelGGL((attn_bwd_band_dkv_kernel<D, G>), dim3(g.T, g.B * g.Hkv), dim3(256), 0, s,
-                     static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
-                     static_cast<const bf16_t *>(dO), LSE, Dvec, g, ix, bkv);
-  timing_end(s);
+                             float *seg_sums, hipStream_t s) {
+  const bf16_t *q = static_cast<const bf16_t *>(Q), *k = static_cast<const bf16_t *>(K);
+  const bf16_t *v = static_cast<const bf16_t *>(V), *dout = static_cast<const bf16_t *>(dO);
+  const int nit = band_init_tiles(g), R = g.B * g.Hkv;
+  if (nit > 0) {
+    const int nseg = band_init_segments(g), seg_tok = (g.Lq + nseg - 1) / nseg;
+    timing_begin("phsa_attn_bwd_band_dkv_init", s);
+    hipLaunchKernelGGL((attn_bwd_band_dkv_kernel<D, G>), dim3(nit * nseg, R), dim3(256), 0, s, q, k, v, dout, LSE,
+                       Dvec, g, ix, 0, nseg, seg_tok, nit, seg_sums);
+    timing_end(s);
+    timing_begin("phsa_attn_bwd_band_init_reduce", s);
+    hipLaunchKernelGGL((band_init_reduce_kernel<D>), dim3(R * nit, (2 * 64 * D + 1023) / 1024), dim3(256), 0, s,
+                       static_cast<const float *>(seg_sums), bkv, g, nit, nseg);
+    timing_end(s);
+  }
+  if (g.T > nit) {
+    timing_begin("phsa_attn_bwd_band_dkv", s);
+    hipLaunchKernelGGL((attn_bwd_band_dkv_kernel<D, G>), dim3(g.T - nit, R), dim3(256), 0, s, q, k, v, dout, LSE, Dvec,
+                       g, ix, nit, 1, g.Lq, g.T, bkv);
+    timing_end(s);
+  }
   constexpr int TOKQ = 64 / G;
   timing_begin("phsa_attn_bwd_band_dq", s);
-  hipLaunchKernelGGL((attn_bwd_band_dq_kernel<D, G>), dim3((g.Lq + TOKQ - 1) / TOKQ, g.B * g.Hkv), dim3(256), 0, s,
-                     static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
-                     static_cast<const bf16_t *>(dO), LSE, Dvec, g, ix, static_cast<bf16_t *>(dqpart));
+  hipLaunchKernelGGL((attn_bwd_band_dq_kernel<D, G>), dim3((g.Lq + TOKQ - 1) / TOKQ, R), dim3(256), 0, s, q, k, v,
+                     dout, LSE, Dvec, g, ix, static_cast<bf16_t *>(dqpart));
   timing_end(s);
   return hipGetLastError();
 }
@@ -587,12 +682,12 @@ static hipError_t fwd_band_d(const Geom &g, const void *Q, const void *K, const 
 template <int D>
 static hipError_t bwd_band_d(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
                              const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
-                             hipStream_t s) {
+                             float *seg_sums, hipStream_t s) {
   switch (g.G) {
-    case 1: return bwd_band_t<D, 1>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
-    case 2: return bwd_band_t<D, 2>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
-    case 4: return bwd_band_t<D, 4>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
-    default: return bwd_band_t<D, 8>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
+    case 1: return bwd_band_t<D, 1>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
+    case 2: return bwd_band_t<D, 2>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
+    case 4: return bwd_band_t<D, 4>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
+    default: return bwd_band_t<D, 8>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
   }
 }
 
@@ -603,9 +698,9 @@ hipError_t launch_fwd_band(const Geom &g, const void *Q, const void *K, const vo
 
 hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
                            const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
-                           hipStream_t s) {
-  return g.d == 128 ? bwd_band_d<128>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s)
-                    : bwd_band_d<64>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
+                           float *seg_sums, hipStream_t s) {
+  return g.d == 128 ? bwd_band_d<128>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s)
+                    : bwd_band_d<64>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
 }
 
 }  // namespace phsa

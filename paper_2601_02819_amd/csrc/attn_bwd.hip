@@ -391,7 +391,7 @@ static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, cons
                                const float *LSE, void *dQ, void *dK, void *dV, const IndexWs &ix,
                                const float *Dvec, void *dqpart, float *dkvpart, float *bkv, hipStream_t s) {
   if (g.band) {  // the band's dQ partials and dK/dV tiles first: the sparse epilogue adds the latter
-    const hipError_t e = launch_bwd_band(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, s);
+    const hipError_t e = launch_bwd_band(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, dkvpart, s);
     if (e != hipSuccess) return e;
   }
   const float *bk = g.band ? bkv : nullptr;

@@ -37,10 +37,25 @@ __device__ __forceinline__ bool slot_valid(int t, int cur, int T) { return t >= 
 // Width of a sel row: the selection's own Ksel (in its block units).
 __device__ __forceinline__ int sel_width(const Geom &gm) { return gm.n_init + gm.window / gm.sm + 1 + gm.top_k; }
 
-// Plain selections (64-token blocks, no band) are indexed as they are, one
-// thread per row: a row's entries are the valid prefix of its sel row
-// (ascending causal blocks, ended by -1 or a block past the query's own).
-__device__ __forceinline__ bool plain_rows(const Geom &gm) { return gm.sm == gm.m && !gm.band; }
+// Selections of 64-token blocks are indexed one thread per row: a row's
+// entries are the valid prefix of its sel row (ascending causal blocks, ended
+// by -1 or a block past the query's own), less its forced blocks when the
+// band takes them.
+__device__ __forceinline__ bool plain_rows(const Geom &gm) { return gm.sm == gm.m; }
+
+// The forced blocks of Algorithm 1 for the query in block cur: the init blocks
+// 0 .. ninit - 1 and the local window a_blk .. cur (a_blk >= ninit, so the
+// two ranges are disjoint; both in selection blocks).  With the band, a row
+// that holds all of them leaves them to the band kernels.
+struct Forced {
+  int ninit, a_blk, count;
+  __device__ __forceinline__ Forced(const Geom &gm, int cur) {
+    ninit = min(gm.n_init, cur + 1);
+    a_blk = max(max(0, cur - gm.window / gm.sm), ninit);
+    count = ninit + cur - a_blk + 1;
+  }
+  __device__ __forceinline__ bool has(int t) const { return t < ninit || t >= a_blk; }
+};
 
 // The regrouped entries of one row, one wave per row with lane s holding slot
 // s of sel (t = that slot's block, -1 past the row's width).  A row's blocks
@@ -48,7 +63,7 @@ __device__ __forceinline__ bool plain_rows(const Geom &gm) { return gm.sm == gm.
 // takes its slot by a ballot prefix count and ORs the quarters of the (at most
 // 64 / m) lanes of its group.  With gm.band, a row holding every local block
 // outside the init blocks (a_blk .. cur) leaves them to the band kernels
-// (band_ok); other rows keep all their blocks.  A lane with `mine` set holds
+// (band_ok) together with its init blocks; other rows keep all their blocks.  A lane with `mine` set holds
 // entry `pos` of the row: tile `tile` with quarter mask `qm`; n entries in all.
 struct RowEntries {
   int tile;
@@ -75,13 +90,9 @@ __device__ __forceinline__ RowEntries row_entries(int t, int i, const Geom &gm) 
   const int cur = (gm.q_pos0 + i) / gm.sm;
   const int per = 64 / gm.sm, qpb = gm.sm / 16;
   const bool in_range = t >= 0 && t <= cur && t < gm.Lk / gm.sm;
-  int a_blk = cur + 1;
-  if (gm.band) {
-    a_blk = max(max(0, cur - gm.window / gm.sm), min(gm.n_init, cur + 1));
-    const int have = __popcll(__ballot(in_range && t >= a_blk));
-    e.band_ok = a_blk <= cur && have == cur - a_blk + 1;
-  }
-  const bool valid = in_range && !(e.band_ok && t >= a_blk);
+  const Forced f(gm, cur);
+  if (gm.band) e.band_ok = __popcll(__ballot(in_range && f.has(t))) == f.count;
+  const bool valid = in_range && !(e.band_ok && f.has(t));
   const int tc = valid ? t / per : -1;
   const unsigned qb = valid ? ((1u << qpb) - 1u) << ((t % per) * qpb) : 0u;
   const int prev = from_lane_below(tc);
@@ -104,6 +115,20 @@ __device__ __forceinline__ RowEntries row_entries(int t, int i, const Geom &gm) 
 
 constexpr int kRowBatch = 8;  // sel rows a wave has in flight (regrouped rows)
 
+// A plain row (one thread, its sel row staged at row[0 .. ks)) with the band:
+// does it hold every forced block?
+__device__ __forceinline__ bool plain_band_ok(const int32_t *row, int ks, int cur, const Geom &gm) {
+  if (!gm.band) return false;
+  const Forced f(gm, cur);
+  int have = 0;
+  for (int s = 0; s < ks; ++s) {
+    const int t = row[s];
+    if (!slot_valid(t, cur, gm.T)) break;
+    have += f.has(t);
+  }
+  return have == f.count;
+}
+
 // The bitmap bm [8][T] of the 256-row tile w of (b, g) = bg: bit r % 32 of
 // bm[r / 32][t] is set when row r has an entry for t.  Plain rows: the tile's
 // sel rows, one contiguous run, are staged into rows_s ([kIndexTile][Ksel])
@@ -124,10 +149,12 @@ __device__ void build_tile_bitmap(uint32_t *bm, int32_t *rows_s, const int32_t *
     __syncthreads();
     if (tid < nrow) {
       const int cur = (gm.q_pos0 + w * kIndexTile + tid) / gm.m;
+      const bool bok = plain_band_ok(rows_s + tid * ks, ks, cur, gm);
+      const Forced f(gm, cur);
       for (int s = 0; s < ks; ++s) {
         const int t = rows_s[tid * ks + s];
         if (!slot_valid(t, cur, gm.T)) break;
-        atomicOr(&bm[(tid >> 5) * gm.T + t], 1u << (tid & 31));
+        if (!(bok && f.has(t))) atomicOr(&bm[(tid >> 5) * gm.T + t], 1u << (tid & 31));
       }
     }
     __syncthreads();
@@ -154,9 +181,12 @@ __device__ void build_tile_bitmap(uint32_t *bm, int32_t *rows_s, const int32_t *
 }
 
 // LDS of the count kernel (the fill kernel adds one list position per t).
+// Plain rows stage their sel rows (width Ksel, in selection blocks) and, in
+// the fill kernel, one band flag per row after them.
 inline size_t index_lds_bytes(const Geom &g) {
-  const bool plain = g.sm == g.m && !g.band;
-  return (size_t)g.T * 8 * sizeof(uint32_t) + (plain ? (size_t)kIndexTile * g.ksel * sizeof(int32_t) : 0);
+  const bool plain = g.sm == g.m;
+  const int ks = g.n_init + g.window / g.sm + 1 + g.top_k;
+  return (size_t)g.T * 8 * sizeof(uint32_t) + (plain ? (size_t)kIndexTile * (ks + 1) * sizeof(int32_t) : 0);
 }
 
 __global__ __launch_bounds__(256) void index_count_kernel(const int32_t *__restrict__ sel, Geom gm, IndexWs ix) {
@@ -246,28 +276,41 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
   const int ks = sel_width(gm);
   const int nrow = min(kIndexTile, gm.Lq - w * kIndexTile);
   const int64_t row0 = (int64_t)bg * gm.Lq + (int64_t)w * kIndexTile;
-  if (plain_rows(gm)) {  // gm.ksel == ks
+  if (plain_rows(gm)) {
+    // entries take slots 0 .. n - 1 of the row's position-map row; with the
+    // band its last slot (gm.ksel - 1) holds the band partial of a band row
+    int32_t *flag_s = rows_s + kIndexTile * ks;
     const int i = w * kIndexTile + tid;
     if (tid < nrow) {
       const int cur = (gm.q_pos0 + i) / gm.m;
+      const bool bok = plain_band_ok(rows_s + tid * ks, ks, cur, gm);
+      const Forced f(gm, cur);
       const int word = tid >> 5;
       const uint32_t below = (1u << (tid & 31)) - 1u;
-      int s = 0;
-      for (; s < ks; ++s) {  // the valid prefix
+      int n = 0;
+      for (int s = 0; s < ks; ++s) {  // the valid prefix, less the band's blocks
         const int t = rows_s[tid * ks + s];
         if (!slot_valid(t, cur, gm.T)) break;
+        if (bok && f.has(t)) continue;
         int rank = __popc(bm[word * gm.T + t] & below);
         for (int k = 0; k < word; ++k) rank += __popc(bm[k * gm.T + t]);
         const int32_t p = base_s[t] + rank;
-        ix.tok[p] = (i << 10) | (15 << 6) | s;
-        rows_s[tid * ks + s] = p;
+        ix.tok[p] = (i << 10) | (15 << 6) | n;
+        rows_s[tid * ks + n] = p;  // n <= s: the slots still to be read are above
+        ++n;
       }
-      for (; s < ks; ++s) rows_s[tid * ks + s] = -1;
+      for (int s = n; s < ks; ++s) rows_s[tid * ks + s] = -1;
+      flag_s[tid] = bok;
     }
     __syncthreads();
     // the tile's rows are consecutive, so their position-map rows form one contiguous run
-    int32_t *dst = ix.pmap + row0 * ks;
-    for (int x = tid; x < nrow * ks; x += 256) dst[x] = rows_s[x];
+    const int ksel = gm.ksel, nsp = ksel - gm.band;  // nsp <= ks slots for entries
+    int32_t *dst = ix.pmap + row0 * ksel;
+    for (int x = tid; x < nrow * ksel; x += 256) {
+      const int r = x / ksel, s = x - r * ksel;
+      dst[x] = s < nsp ? rows_s[r * ks + s] : (flag_s[r] ? (int32_t)(ix.band_base + row0 + r) : -1);
+    }
+    if (gm.band && tid < nrow) ix.bflag[row0 + tid] = (uint8_t)flag_s[tid];
     return;
   }
   unsigned flag = 0;  // band flag of row 64 * wave + lane

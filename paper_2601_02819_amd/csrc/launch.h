@@ -66,7 +66,8 @@ hipError_t launch_select(const Geom &g, const void *Q, const float *Kc, int32_t 
 hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &ix, hipStream_t s);
 hipError_t launch_attn_fwd(const Geom &g, const void *Q, const void *K, const void *V, const int32_t *sel, void *O,
                            float *LSE, const IndexWs &ix, void *opart, float2 *ml, hipStream_t s);
-// bkv: with g.band, float32 [B*Hkv*T][2][64][d] for the band's dK, dV per 64-key tile
+// bkv: with g.band, float32 [B*Hkv*T][2][64][d] for the band's dK, dV per 64-key tile;
+// seg_sums: the init tiles' per-segment sums, in the sparse dK/dV partial buffer (dead until the sparse kernel)
 hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
                            const void *dO, const float *LSE, const int32_t *sel, void *dQ,
                            void *dK, void *dV, const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart,
@@ -76,7 +77,7 @@ hipError_t launch_fwd_band(const Geom &g, const void *Q, const void *K, const vo
                            void *opart, float2 *ml, hipStream_t s);
 hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
                            const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
-                           hipStream_t s);
+                           float *seg_sums, hipStream_t s);
 hipError_t launch_bwd_pre(const Geom &g, const void *O, const void *dO, float *Dvec, hipStream_t s);
 hipError_t launch_attn_fwd_fp32(const Geom &g, const float *Q, const float *K, const float *V,
                                 const int32_t *sel, float *O, float *LSE, hipStream_t s);

@@ -17,35 +17,54 @@ def _sel(rows, ksel):
 
 def test_band_blocks_whole_and_holed_windows():
     # m = 16, 2 init blocks, 64-token window (4 blocks); each row is the last
-    # query of a sequence of pos + 1 keys
+    # query of a sequence of pos + 1 keys.  The band takes a row's forced blocks
+    # (init blocks 0 .. min(2, cur + 1) - 1 and local A .. cur) when it holds all.
     m, n_init, w = 16, 2, 64
     rows = [
-        [0],                    # pos 0: cur 0, A = max(0 - 4, min(2, 1)) = 1 > cur: no band
-        [0, 1],                 # pos 16 (cur 1): A = min(2, 2) = 2 > cur: no band
-        [0, 1, 2, 3, 4, 5, 6],  # pos 100 (cur 6): A = max(2, 2) = 2, local 2..6 whole: 5 band blocks
+        [0],                    # pos 0: cur 0, init {0}, A = 1 > cur: 1 band block
+        [0, 1],                 # pos 16 (cur 1): init {0, 1}, A = 2 > cur: 2
+        [0, 1, 2, 3, 4, 5, 6],  # pos 100 (cur 6): init {0, 1}, local 2..6: 7
         [0, 1, 2, 4, 5, 6],     # hole at 3: no band
-        [0, 1, 2, 3, 4, 5, 6, 9],  # block 9 past cur is not valid; local whole: 5
+        [0, 1, 2, 3, 4, 5, 6, 9],  # block 9 past cur is not valid: 7
+        [1, 2, 3, 4, 5, 6],     # init block 0 missing: no band
     ]
-    pos = [0, 16, 100, 100, 100]
-    want = [0, 0, 5, 0, 5]
-    for r, p, wv in zip(rows, pos, want):
-        nb, a = bench.band_blocks(_sel([r], 8), p + 1, m, n_init, w)
+    pos = [0, 16, 100, 100, 100, 100]
+    want = [1, 2, 7, 0, 7, 0]
+    want_init = [1, 2, 2, 0, 2, 0]
+    for r, p, wv, wi in zip(rows, pos, want, want_init):
+        nb, a, ni = bench.band_blocks(_sel([r], 8), p + 1, m, n_init, w)
         assert int(nb.item()) == wv, (r, p)
+        assert int(ni.item()) == wi, (r, p)
         cur = p // m
         assert int(a.item()) == max(max(0, cur - w // m), min(n_init, cur + 1))
+
+
+def test_band_blocks_without_window():
+    # 64-token blocks, window 0, one init block: the forced blocks are block 0
+    # and the row's own block
+    m, n_init, w = 64, 1, 0
+    rows = [[0], [0, 1], [0, 3, 5, 9], [3, 5, 9], [0, 3, 5]]
+    pos = [10, 100, 600, 600, 600]          # cur 0, 1, 9, 9, 9
+    want = [1, 2, 2, 0, 0]                  # row 3 lacks block 0, row 4 its own block
+    for r, p, wv in zip(rows, pos, want):
+        nb, a, ni = bench.band_blocks(_sel([r], 4), p + 1, m, n_init, w)
+        assert int(nb.item()) == wv, (r, p)
+    sel = _sel([[0, 3, 5, 9]], 4)
+    nb, a, ni = bench.band_blocks(sel, 601, m, n_init, w)
+    assert bench.sparse_part(sel, nb, a, ni).tolist() == [[[[-1, 3, 5, -1]]]]
 
 
 def test_sparse_tiles_exclude_band_blocks():
     # m = 16: four blocks per 64-key tile
     m, n_init, w = 16, 1, 64
-    row = [0, 5, 6, 7, 8, 9, 10]  # pos 170 (cur 10): A = 6, local 6..10 whole
+    row = [0, 5, 6, 7, 8, 9, 10]  # pos 170 (cur 10): A = 6, init 0 and local 6..10 whole
     sel = _sel([row], 8)
     Lk = 171
-    nb, a = bench.band_blocks(sel, Lk, m, n_init, w)
-    assert int(nb.item()) == 5
-    sparse = torch.where((nb > 0).unsqueeze(-1) & (sel >= a.unsqueeze(-1)), torch.full_like(sel, -1), sel)
-    # blocks 0 and 5 remain: tiles 0 and 1
-    assert bench.selected_tiles(sparse, Lk, m) == 2
+    nb, a, ni = bench.band_blocks(sel, Lk, m, n_init, w)
+    assert int(nb.item()) == 6  # init block 0 and local 6..10
+    sparse = bench.sparse_part(sel, nb, a, ni)
+    # block 5 remains: tile 1
+    assert bench.selected_tiles(sparse, Lk, m) == 1
     assert bench.selected_tiles(sel, Lk, m) == 3  # tiles 0, 1, 2 with the window
 
 
