@@ -23,7 +23,7 @@ size_t index_layout(const Geom &g, char *base, IndexWs *ix) {
   const int64_t nbgt = R * g.T;
   w.W = (g.Lq + kIndexTile - 1) / kIndexTile;
   w.unit_tokens = 64 * (64 / g.G);  // 64 chunks of 64 MFMA rows
-  w.nnz_max = R * g.Lq * (g.ksel - g.band);  // a band geometry's last slot is the band partial
+  w.nnz_max = R * g.Lq * (g.ksel - g.band);  // a band geometry keeps one slot per row for the band partial
   w.band_base = w.nnz_max;
   w.discard = (w.nnz_max + (g.band ? R * g.Lq : 0)) * g.G;
   w.units_max = nbgt + (w.nnz_max + w.unit_tokens - 1) / w.unit_tokens;

@@ -15,7 +15,7 @@
 //                 or the dQ accumulation (backward).  A row leaves one partial
 //                 in the same format and buffer as the sparse partials, at
 //                 list position band_base + row; the per-row merges find it
-//                 through the row's last index slot.
+//                 through the slot after the row's sparse entries.
 //   dK, dV      : key-major.  A workgroup holds one 64-key tile (wave w owns
 //                 keys 16w..16w+15, accumulators in registers) and streams the
 //                 contiguous rows whose forced keys reach into it; it writes

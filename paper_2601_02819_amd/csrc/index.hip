@@ -260,7 +260,7 @@ __global__ __launch_bounds__(1024) void index_scan_lists_kernel(IndexWs ix, int 
 }
 
 // Writes each row's entries into their lists, its position-map row (list
-// position per slot, -1 for empty slots, the band partial in the last slot of
+// position per slot, -1 for empty slots, the band partial in the slot after the entries of
 // a band row) and, with the band, its band flag.  The tile's first list
 // position for each t (list offset + tile offset) is staged in LDS beside the
 // bitmap; an entry's position adds the lower rows of the tile that chose t.
@@ -277,8 +277,9 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
   const int nrow = min(kIndexTile, gm.Lq - w * kIndexTile);
   const int64_t row0 = (int64_t)bg * gm.Lq + (int64_t)w * kIndexTile;
   if (plain_rows(gm)) {
-    // entries take slots 0 .. n - 1 of the row's position-map row; with the
-    // band its last slot (gm.ksel - 1) holds the band partial of a band row
+    // entries take slots 0 .. n - 1 of the row's position-map row and the band
+    // partial of a band row slot n, so that the merges' slot bound stays at the
+    // row's own partial count; flag_s holds that slot (-1: no band partial)
     int32_t *flag_s = rows_s + kIndexTile * ks;
     const int i = w * kIndexTile + tid;
     if (tid < nrow) {
@@ -300,7 +301,7 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
         ++n;
       }
       for (int s = n; s < ks; ++s) rows_s[tid * ks + s] = -1;
-      flag_s[tid] = bok;
+      flag_s[tid] = bok ? n : -1;
     }
     __syncthreads();
     // the tile's rows are consecutive, so their position-map rows form one contiguous run
@@ -308,9 +309,9 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
     int32_t *dst = ix.pmap + row0 * ksel;
     for (int x = tid; x < nrow * ksel; x += 256) {
       const int r = x / ksel, s = x - r * ksel;
-      dst[x] = s < nsp ? rows_s[r * ks + s] : (flag_s[r] ? (int32_t)(ix.band_base + row0 + r) : -1);
+      dst[x] = s == flag_s[r] ? (int32_t)(ix.band_base + row0 + r) : s < nsp ? rows_s[r * ks + s] : -1;
     }
-    if (gm.band && tid < nrow) ix.bflag[row0 + tid] = (uint8_t)flag_s[tid];
+    if (gm.band && tid < nrow) ix.bflag[row0 + tid] = (uint8_t)(flag_s[tid] >= 0);
     return;
   }
   unsigned flag = 0;  // band flag of row 64 * wave + lane
@@ -342,7 +343,7 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
       const int moved = __builtin_amdgcn_ds_permute((e.mine ? e.pos : 63) << 2, p);
       if (lane < gm.ksel)
         ix.pmap[x * gm.ksel + lane] =
-            lane < e.n ? moved : (gm.band && e.band_ok && lane == gm.ksel - 1) ? (int32_t)(ix.band_base + x) : -1;
+            lane < e.n ? moved : (gm.band && e.band_ok && lane == e.n) ? (int32_t)(ix.band_base + x) : -1;
       if (lane == j0 + u) flag = e.band_ok ? 1u : 0u;
     }
   }
