@@ -31,6 +31,8 @@
 // from that kernel too.
 #include <math.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "launch.h"
 
@@ -304,39 +306,43 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   }
 }
 
-// Per (b, g, t): sum float32 partials of multi-unit blocks; zero unselected
-// blocks.  A band geometry adds the band's float32 dK/dV of the tile (bkv).
+// Per (b, g, t) of the index's compact list (blocks with zero or several work
+// units): sum the float32 partials of its units, or zeros for a block nobody
+// selected; a band geometry adds the band's float32 dK/dV of the tile (bkv).
 // Each block's 2 x 64 x d outputs are split over kFinSplit workgroups; each
-// thread owns 4 consecutive features (16-byte loads).
+// thread owns 4 consecutive features (16-byte loads).  A fixed grid of
+// kFinGrid x kFinSplit workgroups walks the list, kFinGrid blocks apart.
 constexpr int kFinSplit = 16;
+constexpr int kFinGrid = 512;
 template <int D>
 __global__ __launch_bounds__(256) void dkv_finalize_kernel(const float *__restrict__ dkvpart,
                                                            const float *__restrict__ bkv, bf16_t *__restrict__ dK,
                                                            bf16_t *__restrict__ dV, Geom gm, IndexWs ix) {
-  const int bgt = blockIdx.x;
-  const int u0 = ix.uoff[bgt], u1 = ix.uoff[bgt + 1];
-  if (u1 - u0 == 1) return;  // written by the sparse kernel
-  const int bg = bgt / gm.T, t = bgt - bg * gm.T;
-  const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   constexpr int PER = 64 * D / kFinSplit;  // elements of dK (and of dV) per workgroup
-  for (int x = blockIdx.y * PER + threadIdx.x * 4; x < (int)(blockIdx.y + 1) * PER; x += 256 * 4) {
-    const int kk = x / D, c = x - kk * D;
-    float4 sk = make_float4(0.f, 0.f, 0.f, 0.f), sv = sk;
-    if (bkv) {
-      sk = *reinterpret_cast<const float4 *>(bkv + (int64_t)bgt * 2 * 64 * D + x);
-      sv = *reinterpret_cast<const float4 *>(bkv + (int64_t)bgt * 2 * 64 * D + 64 * D + x);
+  for (int j = blockIdx.x; j < ix.totals[2]; j += gridDim.x) {
+    const int bgt = ix.fin[j];
+    const int u0 = ix.uoff[bgt], u1 = ix.uoff[bgt + 1];
+    const int bg = bgt / gm.T, t = bgt - bg * gm.T;
+    const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
+    for (int x = blockIdx.y * PER + threadIdx.x * 4; x < (int)(blockIdx.y + 1) * PER; x += 256 * 4) {
+      const int kk = x / D, c = x - kk * D;
+      float4 sk = make_float4(0.f, 0.f, 0.f, 0.f), sv = sk;
+      if (bkv) {
+        sk = *reinterpret_cast<const float4 *>(bkv + (int64_t)bgt * 2 * 64 * D + x);
+        sv = *reinterpret_cast<const float4 *>(bkv + (int64_t)bgt * 2 * 64 * D + 64 * D + x);
+      }
+      for (int u = u0; u < u1; ++u) {
+        const float4 a = *reinterpret_cast<const float4 *>(dkvpart + (int64_t)u * 2 * 64 * D + x);
+        const float4 v = *reinterpret_cast<const float4 *>(dkvpart + (int64_t)u * 2 * 64 * D + 64 * D + x);
+        sk.x += a.x; sk.y += a.y; sk.z += a.z; sk.w += a.w;
+        sv.x += v.x; sv.y += v.y; sv.z += v.z; sv.w += v.w;
+      }
+      const int64_t dst = (((int64_t)b * gm.Lk + (int64_t)t * 64 + kk) * gm.Hkv + g) * D + c;
+      const bf16_t k4[4] = {f32_to_bf16(sk.x), f32_to_bf16(sk.y), f32_to_bf16(sk.z), f32_to_bf16(sk.w)};
+      const bf16_t v4[4] = {f32_to_bf16(sv.x), f32_to_bf16(sv.y), f32_to_bf16(sv.z), f32_to_bf16(sv.w)};
+      *reinterpret_cast<uint2 *>(dK + dst) = *reinterpret_cast<const uint2 *>(k4);
+      *reinterpret_cast<uint2 *>(dV + dst) = *reinterpret_cast<const uint2 *>(v4);
     }
-    for (int u = u0; u < u1; ++u) {
-      const float4 a = *reinterpret_cast<const float4 *>(dkvpart + (int64_t)u * 2 * 64 * D + x);
-      const float4 v = *reinterpret_cast<const float4 *>(dkvpart + (int64_t)u * 2 * 64 * D + 64 * D + x);
-      sk.x += a.x; sk.y += a.y; sk.z += a.z; sk.w += a.w;
-      sv.x += v.x; sv.y += v.y; sv.z += v.z; sv.w += v.w;
-    }
-    const int64_t dst = (((int64_t)b * gm.Lk + (int64_t)t * 64 + kk) * gm.Hkv + g) * D + c;
-    const bf16_t k4[4] = {f32_to_bf16(sk.x), f32_to_bf16(sk.y), f32_to_bf16(sk.z), f32_to_bf16(sk.w)};
-    const bf16_t v4[4] = {f32_to_bf16(sv.x), f32_to_bf16(sv.y), f32_to_bf16(sv.z), f32_to_bf16(sv.w)};
-    *reinterpret_cast<uint2 *>(dK + dst) = *reinterpret_cast<const uint2 *>(k4);
-    *reinterpret_cast<uint2 *>(dV + dst) = *reinterpret_cast<const uint2 *>(v4);
   }
 }
 
@@ -402,7 +408,8 @@ static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, cons
                      static_cast<bf16_t *>(dK), static_cast<bf16_t *>(dV), dkvpart, bk);
   timing_end(s);
   timing_begin("phsa_attn_bwd_dkv_finalize", s);
-  hipLaunchKernelGGL((dkv_finalize_kernel<D>), dim3(g.B * g.Hkv * g.T, kFinSplit), dim3(256), 0, s, dkvpart, bk,
+  hipLaunchKernelGGL((dkv_finalize_kernel<D>), dim3(std::min(g.B * g.Hkv * g.T, kFinGrid), kFinSplit), dim3(256), 0, s,
+                     dkvpart, bk,
                      static_cast<bf16_t *>(dK), static_cast<bf16_t *>(dV), g, ix);
   timing_end(s);
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;

@@ -216,38 +216,46 @@ __global__ __launch_bounds__(256) void index_scan_tiles_kernel(Geom gm, IndexWs 
   ix.cnt[x] = run;
 }
 
-// Single workgroup of 1024 threads: exclusive scans of list lengths and of
-// units per list, then the unit table.
+// Single workgroup of 1024 threads: exclusive scans of list lengths, of units
+// per list and of the blocks that do not have exactly one unit (their dK/dV
+// is written by the finalize, from partial sums or from nothing), then the
+// unit table and the compact list of those blocks.
 __global__ __launch_bounds__(1024) void index_scan_lists_kernel(IndexWs ix, int nbgt) {
-  __shared__ int s_a[1024], s_b[1024];
+  __shared__ int s_a[1024], s_b[1024], s_c[1024];
   const int tid = threadIdx.x;
   const int per = (nbgt + 1023) / 1024;
   const int lo = min(nbgt, tid * per), hi = min(nbgt, lo + per);
   const int U = ix.unit_tokens;
-  int sa = 0, sb = 0;
+  int sa = 0, sb = 0, sc = 0;
   for (int x = lo; x < hi; ++x) {
     const int c = ix.cnt[x];
+    const int nu = (c + U - 1) / U;
     sa += c;
-    sb += (c + U - 1) / U;
+    sb += nu;
+    sc += nu != 1;
   }
   s_a[tid] = sa;
   s_b[tid] = sb;
+  s_c[tid] = sc;
   __syncthreads();
   for (int o = 1; o < 1024; o <<= 1) {  // inclusive Hillis-Steele scan
     const int va = tid >= o ? s_a[tid - o] : 0;
     const int vb = tid >= o ? s_b[tid - o] : 0;
+    const int vc = tid >= o ? s_c[tid - o] : 0;
     __syncthreads();
     s_a[tid] += va;
     s_b[tid] += vb;
+    s_c[tid] += vc;
     __syncthreads();
   }
-  int ra = s_a[tid] - sa, rb = s_b[tid] - sb;
+  int ra = s_a[tid] - sa, rb = s_b[tid] - sb, rc = s_c[tid] - sc;
   for (int x = lo; x < hi; ++x) {
     const int c = ix.cnt[x];
     const int nu = (c + U - 1) / U;
     ix.off[x] = ra;
     ix.uoff[x] = rb;
     for (int u = 0; u < nu; ++u) ix.units[rb + u] = make_int2(x, u * U);
+    if (nu != 1) ix.fin[rc++] = x;
     ra += c;
     rb += nu;
   }
@@ -256,6 +264,7 @@ __global__ __launch_bounds__(1024) void index_scan_lists_kernel(IndexWs ix, int 
     ix.uoff[nbgt] = s_b[1023];
     ix.totals[0] = s_a[1023];
     ix.totals[1] = s_b[1023];
+    ix.totals[2] = s_c[1023];
   }
 }
 

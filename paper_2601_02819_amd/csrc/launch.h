@@ -33,14 +33,15 @@ struct IndexWs {
   int32_t *cnt;       // [B*Hkv*T]      list length per (b, g, t)
   int32_t *off;       // [B*Hkv*T + 1]  list start per (b, g, t)
   int32_t *uoff;      // [B*Hkv*T + 1]  first work unit per (b, g, t)
-  int32_t *totals;    // [4]            nnz, n_units
+  int32_t *totals;    // [4]            nnz, n_units, blocks in fin
+  int32_t *fin;       // [B*Hkv*T]      the (b, g, t) whose dK/dV the finalize writes (not one work unit)
   int32_t *tok;       // [nnz_max]      (query row << 10) | (quarter mask << 6) | slot, ascending row per list
   int32_t *pmap;      // [B*Hkv*Lq*Ksel] list position of each valid (row, slot); partials are
                       //                 stored in list order and the merges gather through this map
   int2 *units;        // [units_max]    (b*Hkv*T + g*T + t, first list entry)
   int64_t band_base;  // list position of the band partial of row (b, g, i): band_base + (b*Hkv + g)*Lq + i
   int64_t discard;    // partial row that absorbs stores past a chunk's end (after the list and band rows)
-  uint8_t *bflag;     // [B*Hkv*Lq] 1: the row's local window is in the band (NULL: no band)
+  uint8_t *bflag;     // [B*Hkv*Lq] 1: the row's forced blocks are in the band (NULL: no band)
 };
 
 constexpr int kIndexTile = 256;  // query rows per index-building workgroup
