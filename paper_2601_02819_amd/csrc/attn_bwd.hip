@@ -29,6 +29,13 @@
 // directly (bf16) when the unit covers its whole block, else as float32
 // partials that a per-block kernel sums; blocks nobody selected get zeros
 // from that kernel too.
+//
+// The softmax scale rides in the exponent: the kernel computes P' = scale * P
+// (its LSE is lowered by log2(scale)), so dS' = P' (dP - D) = scale * dS is
+// already what dK and dQ need, and dV, summed from P', is divided by the scale
+// once per unit.  A row that did not select a wave's quarter gets LSE = +inf in
+// that wave (its weights are 2^-inf = 0), and the causal test runs only in
+// chunks that reach past the first row's position.
 #include <math.h>
 
 #include <algorithm>
@@ -63,6 +70,25 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const T *__restrict__ O, c
   if (ok && c == 0) Dvec[x] = acc;  // [B, Lq, Hq], the row order of O
 }
 
+// P' and dS' of one 16-row tile (lane (q, j): rows 4q..4q+3, key j); CAUSAL
+// zeroes the weights of keys past a row's position.
+template <bool CAUSAL>
+__device__ __forceinline__ void bwd_p_ds(f32x4 &s, f32x4 &dp, const float4 lse4, const float4 dd4, const int4 pos4,
+                                         int key, float sl2, bf16_t dsq[4]) {
+  const float lsev[4] = {lse4.x, lse4.y, lse4.z, lse4.w};
+  const float ddv[4] = {dd4.x, dd4.y, dd4.z, dd4.w};
+  const int posv[4] = {pos4.x, pos4.y, pos4.z, pos4.w};
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float p = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, -lsev[r]));
+    if (CAUSAL) p = key <= posv[r] ? p : 0.f;
+    const float ds = p * (dp[r] - ddv[r]);
+    s[r] = p;
+    dp[r] = ds;
+    dsq[r] = f32_to_bf16(ds);
+  }
+}
+
 template <int D, int G>
 __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     const bf16_t *__restrict__ Q, const bf16_t *__restrict__ K, const bf16_t *__restrict__ V,
@@ -77,7 +103,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   // keep D + 8, which holds the workgroup at 80 KB (two per CU).
   constexpr int KPQ = D + 16;
   constexpr int KPK = D + 8;
-  constexpr int RP = 64 + 8;         // pitch of the [key][row] dS tile
+  // pitch of the [key][row] dS tile; the 8-element pad of its 64 rows holds the
+  // chunk's per-wave LSE: row 16w + 4mt + q, as 4 floats, those of rows
+  // 16mt + 4q .. +3 in wave w
+  constexpr int RP = 64 + 8;
   constexpr int VPR = D / 8;
   constexpr int NV = 64 * VPR / 256;
   constexpr int KB = D / 32;
@@ -87,7 +116,6 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   __shared__ __attribute__((aligned(16))) bf16_t Qs[64 * KPQ];
   __shared__ __attribute__((aligned(16))) bf16_t dOs[64 * KPQ];
   __shared__ __attribute__((aligned(16))) bf16_t dSt[64 * RP];
-  __shared__ __attribute__((aligned(16))) float lse_s[64];
   __shared__ __attribute__((aligned(16))) float dd_s[64];
   __shared__ __attribute__((aligned(16))) int pos_s[64];
 
@@ -107,6 +135,11 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   const int64_t list0 = (int64_t)ix.off[bgt] + e0;
   const int32_t *list = ix.tok + list0;
   const int64_t krow0 = ((int64_t)b * gm.Lk + (int64_t)t * 64) * gm.Hkv + g;  // global row of key 0
+  // the group's first head of sequence b; a row's head h, query i is at i * Hq * D + (h - gG) * D
+  const int64_t qb0 = ((int64_t)b * gm.Lq * gm.Hq + g * G) * D;
+  const int hqd = gm.Hq * D;
+  const float *lse_b = LSE + ((int64_t)b * gm.Hq + g * G) * gm.Lq;  // [G][Lq] of the group
+  const float *dd_b = Dvec + (int64_t)b * gm.Lq * gm.Hq + g * G;     // [Lq][Hq] from the group's first head
 
   for (int x = tid; x < 64 * VPR; x += 256) {
     const int kk = x / VPR, c = (x % VPR) * 8;
@@ -121,37 +154,34 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
 
   // Row gather, pipelined two deep: the list entries of chunk c + 2 are read
   // while the rows of chunk c + 1 are fetched, which is while chunk c computes.
+  // Rows past the list's end fetch the last entry's row again (finite values
+  // whose weights are zero: their LSE is +inf).
   int ne[NV], nrow = -1;               // list entries of the next chunk to fetch
-  uint4 pq[NV], pd[NV];
+  u32x4 pq[NV], pd[NV];
   float plse = 0.f, pdd = 0.f;
   int ppos = 0;
   auto load_entries = [&](int c0) {
-    const int ntok = min(CT, n_ent - c0);
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       const int tk = ((tid + 256 * k) / VPR) / G;
-      ne[k] = (c0 < n_ent && tk < ntok) ? list[c0 + tk] : -1;
+      ne[k] = list[min(c0 + tk, n_ent - 1)];
     }
     const int tk = tid / G;
-    nrow = (tid < 64 && c0 < n_ent && tk < ntok) ? list[c0 + tk] : -1;
+    nrow = (tid < 64 && c0 + tk < n_ent) ? list[c0 + tk] : -1;
   };
   auto fetch_rows = [&]() {
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
-      pq[k] = pd[k] = make_uint4(0u, 0u, 0u, 0u);
-      if (ne[k] >= 0) {
-        const int64_t src = (((int64_t)b * gm.Lq + (ne[k] >> 10)) * gm.Hq + g * G + r % G) * D + c;
-        pq[k] = *reinterpret_cast<const uint4 *>(Q + src);
-        pd[k] = *reinterpret_cast<const uint4 *>(dO + src);
-      }
+      const int64_t src = qb0 + (int64_t)(ne[k] >> 10) * hqd + ((r % G) * D + c);
+      pq[k] = *reinterpret_cast<const u32x4 *>(Q + src);
+      pd[k] = *reinterpret_cast<const u32x4 *>(dO + src);
     }
     if (tid < 64) {
       if (nrow >= 0) {
         const int i = nrow >> 10;
-        const int h = g * G + tid % G;
-        plse = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + i];  // scaled when staged, so nothing waits here
-        pdd = Dvec[((int64_t)b * gm.Lq + i) * gm.Hq + h];
+        plse = lse_b[(tid % G) * gm.Lq + i];  // scaled when staged, so nothing waits here
+        pdd = dd_b[i * gm.Hq + tid % G];
         ppos = (gm.q_pos0 + i) | (((nrow >> 6) & 15) << 27);  // position, and the quarters the row attends to
       } else {
         plse = 0.f;
@@ -165,6 +195,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   load_entries(CT);
 
   const float sl2 = gm.scale * kLog2e;
+  const float lsc = __log2f(gm.scale);       // P' = scale * P
+  const float inv_scale = 1.f / gm.scale;
   const int key = t * 64 + wave * 16 + l16;  // the key whose S column this lane holds
 
   for (int c0 = 0; c0 < n_ent; c0 += CT) {
@@ -172,13 +204,17 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       const int v = tid + 256 * k, r = v / VPR, c = (v % VPR) * 8;
-      *reinterpret_cast<uint4 *>(&Qs[r * KPQ + c]) = pq[k];
-      *reinterpret_cast<uint4 *>(&dOs[r * KPQ + c]) = pd[k];
+      *reinterpret_cast<u32x4 *>(&Qs[r * KPQ + c]) = pq[k];
+      *reinterpret_cast<u32x4 *>(&dOs[r * KPQ + c]) = pd[k];
     }
     if (tid < 64) {
-      lse_s[tid] = plse * kLog2e;
+      const float l = plse * kLog2e - lsc;
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        reinterpret_cast<float *>(&dSt[(w * 16 + (tid >> 2)) * RP + 64])[tid & 3] =
+            (ppos >> (27 + w)) & 1 ? l : INFINITY;
       dd_s[tid] = pdd;
-      pos_s[tid] = ppos;
+      pos_s[tid] = ppos & 0x7ffffff;
     }
     __syncthreads();
     if (c0 + CT < n_ent) {
@@ -200,27 +236,21 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
         dp[mt] = mfma16x16x32(load_bf16x8(&dOs[(mt * 16 + l16) * KPQ + kb * 32 + kq]), vf, dp[mt]);
       }
     }
-    // P and dS; dS also goes to LDS as [key][row] for the dQ product
+    // P' and dS'; dS' also goes to LDS as [key][row] for the dQ product.  The
+    // chunk's rows ascend: when the first one sees all of the wave's 16 keys,
+    // every row does.
+    const bool causal = __builtin_amdgcn_readfirstlane(pos_s[0]) < t * 64 + wave * 16 + 15;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       const int r0 = mt * 16 + q4 * 4;
-      const float4 lse4 = *reinterpret_cast<const float4 *>(&lse_s[r0]);
+      const float4 lse4 = *reinterpret_cast<const float4 *>(&dSt[(wave * 16 + mt * 4 + q4) * RP + 64]);
       const float4 dd4 = *reinterpret_cast<const float4 *>(&dd_s[r0]);
       const int4 pos4 = *reinterpret_cast<const int4 *>(&pos_s[r0]);
-      const float lsev[4] = {lse4.x, lse4.y, lse4.z, lse4.w};
-      const float ddv[4] = {dd4.x, dd4.y, dd4.z, dd4.w};
-      const int posv[4] = {pos4.x, pos4.y, pos4.z, pos4.w};
       bf16_t dsq[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        // the wave's 16 keys are quarter `wave` of the block
-        const bool ok = ((posv[r] >> (27 + wave)) & 1) && key <= (posv[r] & 0x7ffffff);
-        const float p = ok ? __builtin_amdgcn_exp2f(fmaf(s[mt][r], sl2, -lsev[r])) : 0.f;
-        const float ds = p * (dp[mt][r] - ddv[r]);
-        s[mt][r] = p;
-        dp[mt][r] = ds;
-        dsq[r] = f32_to_bf16(ds);
-      }
+      if (causal)
+        bwd_p_ds<true>(s[mt], dp[mt], lse4, dd4, pos4, key, sl2, dsq);
+      else
+        bwd_p_ds<false>(s[mt], dp[mt], lse4, dd4, pos4, key, sl2, dsq);
       *reinterpret_cast<uint2 *>(&dSt[(wave * 16 + l16) * RP + r0]) = *reinterpret_cast<const uint2 *>(dsq);
     }
     // rows {4q..4q+3} and {16+4q..16+4q+3} (+32) as the K-operand of the row contractions
@@ -253,8 +283,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     // (free after the dK product) and write full 16-byte lanes.
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const bf16_t o4[4] = {f32_to_bf16(dqt[nt][0] * gm.scale), f32_to_bf16(dqt[nt][1] * gm.scale),
-                            f32_to_bf16(dqt[nt][2] * gm.scale), f32_to_bf16(dqt[nt][3] * gm.scale)};
+      const bf16_t o4[4] = {f32_to_bf16(dqt[nt][0]), f32_to_bf16(dqt[nt][1]), f32_to_bf16(dqt[nt][2]),
+                            f32_to_bf16(dqt[nt][3])};
       *reinterpret_cast<uint2 *>(&Qs[row * KPQ + nt * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(o4);
     }
     wave_lds_sync();
@@ -287,10 +317,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
         ak = *reinterpret_cast<const float4 *>(bk + nt * 16);
         av = *reinterpret_cast<const float4 *>(bk + 64 * D + nt * 16);
       }
-      const bf16_t k4[4] = {f32_to_bf16(fmaf(dkt[nt][0], gm.scale, ak.x)), f32_to_bf16(fmaf(dkt[nt][1], gm.scale, ak.y)),
-                            f32_to_bf16(fmaf(dkt[nt][2], gm.scale, ak.z)), f32_to_bf16(fmaf(dkt[nt][3], gm.scale, ak.w))};
-      const bf16_t v4[4] = {f32_to_bf16(dvt[nt][0] + av.x), f32_to_bf16(dvt[nt][1] + av.y),
-                            f32_to_bf16(dvt[nt][2] + av.z), f32_to_bf16(dvt[nt][3] + av.w)};
+      const bf16_t k4[4] = {f32_to_bf16(dkt[nt][0] + ak.x), f32_to_bf16(dkt[nt][1] + ak.y),
+                            f32_to_bf16(dkt[nt][2] + ak.z), f32_to_bf16(dkt[nt][3] + ak.w)};
+      const bf16_t v4[4] = {f32_to_bf16(fmaf(dvt[nt][0], inv_scale, av.x)), f32_to_bf16(fmaf(dvt[nt][1], inv_scale, av.y)),
+                            f32_to_bf16(fmaf(dvt[nt][2], inv_scale, av.z)), f32_to_bf16(fmaf(dvt[nt][3], inv_scale, av.w))};
       *reinterpret_cast<uint2 *>(dK + dst + nt * 16) = *reinterpret_cast<const uint2 *>(k4);
       *reinterpret_cast<uint2 *>(dV + dst + nt * 16) = *reinterpret_cast<const uint2 *>(v4);
     }
@@ -299,9 +329,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     float *pv = pk + 64 * D;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      *reinterpret_cast<float4 *>(pk + nt * 16) =
-          make_float4(dkt[nt][0] * gm.scale, dkt[nt][1] * gm.scale, dkt[nt][2] * gm.scale, dkt[nt][3] * gm.scale);
-      *reinterpret_cast<float4 *>(pv + nt * 16) = make_float4(dvt[nt][0], dvt[nt][1], dvt[nt][2], dvt[nt][3]);
+      *reinterpret_cast<float4 *>(pk + nt * 16) = make_float4(dkt[nt][0], dkt[nt][1], dkt[nt][2], dkt[nt][3]);
+      *reinterpret_cast<float4 *>(pv + nt * 16) =
+          make_float4(dvt[nt][0] * inv_scale, dvt[nt][1] * inv_scale, dvt[nt][2] * inv_scale, dvt[nt][3] * inv_scale);
     }
   }
 }
