@@ -97,12 +97,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     const float *__restrict__ bkv) {
   constexpr int CT = 64 / G;
   // Row-major [row][d] tiles.  The pitch decides the banks of the 16-byte
-  // fragment reads (rows 16m + l16, chunk q4): with D + 16 elements (288 bytes)
-  // they are conflict-free, with D + 8 they conflict about 1.6x.  Q and dO, read
-  // that way every chunk, get D + 16; K and V (one row read per wave per chunk)
-  // keep D + 8, which holds the workgroup at 80 KB (two per CU).
+  // fragment reads (rows 16m + l16, chunk q4) and of the transposing reads: with
+  // D + 16 elements (288 bytes) both are nearly conflict-free, with D + 8 they
+  // conflict.  Q, dO and K (read transposed every chunk) get D + 16; V, read
+  // only as one row fragment per wave per chunk, is unpadded and swizzled
+  // (swz), which holds the workgroup under 80 KB (two per CU).
   constexpr int KPQ = D + 16;
-  constexpr int KPK = D + 8;
   // pitch of the [key][row] dS tile; the 8-element pad of its 64 rows holds the
   // chunk's per-wave LSE: row 16w + 4mt + q, as 4 floats, those of rows
   // 16mt + 4q .. +3 in wave w
@@ -111,8 +111,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   constexpr int NV = 64 * VPR / 256;
   constexpr int KB = D / 32;
   constexpr int NT = D / 16;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KPK];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KPK];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KPQ];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * D];
   __shared__ __attribute__((aligned(16))) bf16_t Qs[64 * KPQ];
   __shared__ __attribute__((aligned(16))) bf16_t dOs[64 * KPQ];
   __shared__ __attribute__((aligned(16))) bf16_t dSt[64 * RP];
@@ -144,8 +144,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   for (int x = tid; x < 64 * VPR; x += 256) {
     const int kk = x / VPR, c = (x % VPR) * 8;
     const int64_t src = (krow0 + (int64_t)kk * gm.Hkv) * D + c;
-    *reinterpret_cast<uint4 *>(&Ks[kk * KPK + c]) = *reinterpret_cast<const uint4 *>(K + src);
-    *reinterpret_cast<uint4 *>(&Vs[kk * KPK + c]) = *reinterpret_cast<const uint4 *>(V + src);
+    *reinterpret_cast<uint4 *>(&Ks[kk * KPQ + c]) = *reinterpret_cast<const uint4 *>(K + src);
+    *reinterpret_cast<uint4 *>(&Vs[swz<D>(kk, c)]) = *reinterpret_cast<const uint4 *>(V + src);
   }
   // dK^T / dV^T accumulators: lane (q, j) holds feature 16nt + 4q + r of key 16w + j
   f32x4 dkt[NT], dvt[NT];
@@ -228,8 +228,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
     for (int mt = 0; mt < 4; ++mt) s[mt] = dp[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      const bf16x8 kf = load_bf16x8(&Ks[(wave * 16 + l16) * KPK + kb * 32 + kq]);
-      const bf16x8 vf = load_bf16x8(&Vs[(wave * 16 + l16) * KPK + kb * 32 + kq]);
+      const bf16x8 kf = load_bf16x8(&Ks[(wave * 16 + l16) * KPQ + kb * 32 + kq]);
+      const bf16x8 vf = load_bf16x8(&Vs[swz<D>(wave * 16 + l16, kb * 32 + kq)]);
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
         s[mt] = mfma16x16x32(load_bf16x8(&Qs[(mt * 16 + l16) * KPQ + kb * 32 + kq]), kf, s[mt]);
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
       const bf16x8 bs = lds_col8(dSt, RP, kb * 32 + kq, kb * 32 + kq + 4, wave * 16, l16);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
-        dqt[nt] = mfma16x16x32(lds_col8(Ks, KPK, kb * 32 + kq, kb * 32 + kq + 4, nt * 16, l16), bs, dqt[nt]);
+        dqt[nt] = mfma16x16x32(lds_col8(Ks, KPQ, kb * 32 + kq, kb * 32 + kq + 4, nt * 16, l16), bs, dqt[nt]);
     }
     // The wave's 16 dQ rows (chunk rows 16w..16w+15) are one contiguous run of
     // the list-ordered partial buffer: stage them in this wave's rows of Qs
