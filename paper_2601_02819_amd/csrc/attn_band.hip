@@ -526,12 +526,19 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       *reinterpret_cast<u32x4 *>(&dOs[r * KPQ + c8]) = pd[v];
     }
     if (tid < 64) {
-      lse_s[tid] = plse * kLog2e;
+      lse_s[tid] = ppos >= 0 ? plse * kLog2e : INFINITY;  // rows outside the band: weight 2^-inf = 0
       dd_s[tid] = pdd;
       pos_s[tid] = ppos;
       a_s[tid] = pa;
     }
     lds_barrier();
+    // the chunk's tokens ascend, and so do their positions and band starts:
+    // when the first token sees the wave's last key and the last token's
+    // window starts by its first key (or the keys are init keys), every key of
+    // the wave is forced for every row of the chunk
+    const int wk0 = key0 + wave * 16;
+    const int pos_first = gm.q_pos0 + c0, a_last = band_first_key(gm, gm.q_pos0 + min(c0 + CT - 1, r_hi));
+    const bool interior = wk0 + 15 <= pos_first && (wk0 + 15 < init_end || wk0 >= a_last);
     load_rows(min(c0 + CT, r_hi));
 
     // S and dP: 64 rows (4 tiles) x this wave's 16 keys; lane (q, j) holds rows 16 mt + 4 q + r of key j
@@ -559,12 +566,21 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       const float ddv[4] = {dd4.x, dd4.y, dd4.z, dd4.w};
       const int posv[4] = {pos4.x, pos4.y, pos4.z, pos4.w};
       const int av[4] = {a4.x, a4.y, a4.z, a4.w};
+      if (interior) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool in = forced_key(key, posv[r], av[r], init_end);
-        const float p = __builtin_amdgcn_exp2f(in ? fmaf(s[mt][r], sl2, -lsev[r]) : -INFINITY);
-        s[mt][r] = p;
-        dp[mt][r] = p * (dp[mt][r] - ddv[r]);
+        for (int r = 0; r < 4; ++r) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s[mt][r], sl2, -lsev[r]));
+          s[mt][r] = p;
+          dp[mt][r] = p * (dp[mt][r] - ddv[r]);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool in = forced_key(key, posv[r], av[r], init_end);
+          const float p = __builtin_amdgcn_exp2f(in ? fmaf(s[mt][r], sl2, -lsev[r]) : -INFINITY);
+          s[mt][r] = p;
+          dp[mt][r] = p * (dp[mt][r] - ddv[r]);
+        }
       }
     }
     const bf16x8 pb0 = pack_bf16x8(s[0], s[1]), pb1 = pack_bf16x8(s[2], s[3]);
