@@ -110,7 +110,8 @@ COUNTER_PASSES = (
 
 def summarize_counters(out_md: str, csvs) -> None:
     """Per-kernel table from rocprofv3 --pmc counter_collection.csv files (the
-    passes of COUNTER_PASSES, any order).  Values are medians over a kernel's
+    passes of COUNTER_PASSES, any order), written after the preamble of an
+    existing out_md.  Values are medians over a kernel's
     dispatches; the topology (XCCs, SIMDs, CUs) comes from the agent_info.csv
     written beside each counter file.  Derived columns:
       MFMA busy   SQ_VALU_MFMA_BUSY_CYCLES / (kernel cycles x SIMDs), kernel
@@ -173,7 +174,12 @@ def summarize_counters(out_md: str, csvs) -> None:
     lines = ["| " + " | ".join(head) + " |", "|" + "---|" * len(head)]
     lines += ["| `" + sym + "` | " + " | ".join(v) + " |" for _, sym, v in rows]
     text = "\n".join(lines) + "\n"
-    open(out_md, "w").write(text)
+    # an existing summary keeps its preamble (title, commands, legend) and gets the new table
+    pre = ""
+    if os.path.exists(out_md):
+        old = open(out_md).read()
+        pre = old[:old.index("| kernel |")] if "| kernel |" in old else old
+    open(out_md, "w").write(pre + text)
     print(text)
 
 
