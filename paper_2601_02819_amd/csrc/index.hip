@@ -272,16 +272,35 @@ __global__ __launch_bounds__(1024) void index_scan_lists_kernel(IndexWs ix, int 
 // position per slot, -1 for empty slots, the band partial in the slot after the entries of
 // a band row) and, with the band, its band flag.  The tile's first list
 // position for each t (list offset + tile offset) is staged in LDS beside the
-// bitmap; an entry's position adds the lower rows of the tile that chose t.
+// bitmap; an entry's position adds the lower rows of the tile that chose t:
+// the set bits of its own bitmap word below it plus those of the lower words,
+// whose counts are staged per t as eight bytes (byte k: words 0 .. k - 1).
 __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restrict__ sel, Geom gm, IndexWs ix) {
   extern __shared__ uint32_t bm[];
-  int32_t *base_s = reinterpret_cast<int32_t *>(bm + 8 * gm.T);
+  uint64_t *pre_s = reinterpret_cast<uint64_t *>(bm + 8 * gm.T);
+  int32_t *base_s = reinterpret_cast<int32_t *>(pre_s + gm.T);
   int32_t *rows_s = base_s + gm.T;  // plain rows: staged sel rows, then their list positions
   const int w = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t *tile_off = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
   const int32_t *list_off = ix.off + (int64_t)bg * gm.T;
   for (int t = tid; t < gm.T; t += 256) base_s[t] = list_off[t] + tile_off[t];
   build_tile_bitmap(bm, rows_s, sel, gm, bg, w);  // its barriers also publish base_s
+  for (int t = tid; t < gm.T; t += 256) {
+    uint64_t pre = 0;
+    int run = 0;  // at most 7 x 32 = 224 rows below the last word
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      pre |= (uint64_t)run << (8 * k);
+      run += __popc(bm[k * gm.T + t]);
+    }
+    pre_s[t] = pre;
+  }
+  __syncthreads();
+  // rows of the tile below row r (word r / 32, bit r % 32) that chose t
+  auto rank_of = [&](int t, int r) {
+    const int word = r >> 5;
+    return (int)((pre_s[t] >> (8 * word)) & 0xffu) + __popc(bm[word * gm.T + t] & ((1u << (r & 31)) - 1u));
+  };
   const int ks = sel_width(gm);
   const int nrow = min(kIndexTile, gm.Lq - w * kIndexTile);
   const int64_t row0 = (int64_t)bg * gm.Lq + (int64_t)w * kIndexTile;
@@ -295,16 +314,12 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
       const int cur = (gm.q_pos0 + i) / gm.m;
       const bool bok = plain_band_ok(rows_s + tid * ks, ks, cur, gm);
       const Forced f(gm, cur);
-      const int word = tid >> 5;
-      const uint32_t below = (1u << (tid & 31)) - 1u;
       int n = 0;
       for (int s = 0; s < ks; ++s) {  // the valid prefix, less the band's blocks
         const int t = rows_s[tid * ks + s];
         if (!slot_valid(t, cur, gm.T)) break;
         if (bok && f.has(t)) continue;
-        int rank = __popc(bm[word * gm.T + t] & below);
-        for (int k = 0; k < word; ++k) rank += __popc(bm[k * gm.T + t]);
-        const int32_t p = base_s[t] + rank;
+        const int32_t p = base_s[t] + rank_of(t, tid);
         ix.tok[p] = (i << 10) | (15 << 6) | n;
         rows_s[tid * ks + n] = p;  // n <= s: the slots still to be read are above
         ++n;
@@ -340,10 +355,7 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
       const RowEntries e = row_entries(t[u], i, gm);
       int32_t p = -1;
       if (e.mine) {
-        const int word = r >> 5;
-        int rank = __popc(bm[word * gm.T + e.tile] & ((1u << (r & 31)) - 1u));
-        for (int k = 0; k < word; ++k) rank += __popc(bm[k * gm.T + e.tile]);
-        p = base_s[e.tile] + rank;
+        p = base_s[e.tile] + rank_of(e.tile, r);
         ix.tok[p] = (i << 10) | ((int)(e.qm & 15u) << 6) | e.pos;
       }
       // entry pos's list position moves to lane pos (a lane below n has exactly
@@ -372,7 +384,8 @@ hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &
   hipLaunchKernelGGL(index_scan_lists_kernel, dim3(1), dim3(1024), 0, s, ix, nbgt);
   timing_end(s);
   timing_begin("phsa_index_fill", s);
-  hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds + (size_t)g.T * sizeof(int32_t), s, sel,
+  hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256),
+                     lds + (size_t)g.T * (sizeof(int32_t) + sizeof(uint64_t)), s, sel,
                      g, ix);
   timing_end(s);
   return hipGetLastError();
