@@ -8,11 +8,13 @@
 // neighbouring rows share most of their windows.  In the key-block-major
 // sparse kernels each (row, forced tile) pair would gather the row and leave
 // a partial; here the forced keys are attended densely instead:
-//   forward, dQ : query-major.  A workgroup holds 128 (token, head) MFMA rows
-//                 (128 / G consecutive tokens) in registers and streams the
-//                 64-key tiles of their forced keys (the init tiles, then the
-//                 window tiles) through LDS, with an online softmax (forward)
-//                 or the dQ accumulation (backward).  A row leaves one partial
+//   forward, dQ : query-major.  A workgroup holds 128 (forward) or 64 (dQ)
+//                 (token, head) MFMA rows of consecutive tokens in registers
+//                 and streams the 64-key tiles of their forced keys (the init
+//                 tiles, then the window tiles) through LDS, each copied from
+//                 global memory straight into LDS while the previous one is
+//                 used, with an online softmax (forward) or the dQ
+//                 accumulation (backward).  A row leaves one partial
 //                 in the same format and buffer as the sparse partials, at
 //                 list position band_base + row; the per-row merges find it
 //                 through the slot after the row's sparse entries.
@@ -272,16 +274,16 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
     bf16_t *__restrict__ dqpart) {
   constexpr int RT = 1;                  // one 16-row chunk per wave (registers)
   constexpr int TOK = 4 * RT * 16 / G;
-  constexpr int KP = D + 16, SP = D + 8;  // K and V: 16-byte row reads and transposing reads
+  constexpr int SP = D + 8;
   constexpr int VPR = D / 8, KB = D / 32, NT = D / 16;
-  constexpr int NV = 64 * VPR / 256;
-  constexpr int BUF = 2 * 64 * KP;        // one K tile and one V tile
-  static_assert(4 * 16 * SP <= 2 * BUF, "output staging fits the tile buffers");
-  // two tile buffers (tile kt read from one, tile kt + 1 stored into the
-  // other); the output staging of the epilogue reuses them
-  __shared__ __attribute__((aligned(16))) bf16_t KV[2 * BUF];
+  constexpr int TILE = 64 * D;           // one K or V tile (swizzled rows, no padding)
+  static_assert(4 * 16 * SP <= 2 * TILE, "output staging fits a tile buffer");
+  // the tile buffers of the forward kernel: tile kt + 1 is copied from global
+  // memory straight into one while tile kt is read from the other
+  __shared__ __attribute__((aligned(16))) bf16_t KV0[2 * TILE];
+  __shared__ __attribute__((aligned(16))) bf16_t KV1[2 * TILE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
   // query tiles of one XCD are consecutive (they share most key tiles)
   const int item = xcd_item(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
@@ -322,40 +324,17 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
   for (int c = 0; c < RT; ++c)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) dq[c][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // the staging of the forward kernel: tile kt + 1 waits in registers while
-  // tile kt is used, is stored into the other buffer after that use, and one
-  // barrier per tile publishes it; tile kt + 2 is loaded right after the store
-  const int64_t head0 = (int64_t)b * gm.Lk * gm.Hkv * D + (int64_t)g * D, tile_step = (int64_t)64 * gm.Hkv * D;
-  // thread t moves the 16-byte vectors t + 256 v: key t / VPR + (256 / VPR) v,
-  // so only the first offset is per thread and the others are constants
-  static_assert(256 % VPR == 0, "rows per load pass");
-  const int koff = (tid / VPR) * gm.Hkv * D + (tid % VPR) * 8, soff = (tid / VPR) * KP + (tid % VPR) * 8;
-  const int kstep = (256 / VPR) * gm.Hkv * D;
-  u32x4 kr[NV], vr[NV];
-  auto load_tile = [&](int kt) {
-    const bf16_t *kp = K + head0 + kt * tile_step, *vp = V + head0 + kt * tile_step;
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      kr[v] = *reinterpret_cast<const u32x4 *>(kp + v * kstep + koff);
-      vr[v] = *reinterpret_cast<const u32x4 *>(vp + v * kstep + koff);
-    }
+  const int64_t head0 = (int64_t)b * gm.Lk * gm.Hkv * D + (int64_t)g * D;
+  const int kstride = gm.Hkv * D;  // elements between consecutive keys of a head
+  auto key_row = [kstride](int r) { return r * kstride; };
+  auto issue = [&](int kt, bf16_t *buf) {
+    const int64_t t0 = head0 + (int64_t)kt * 64 * kstride;
+    tile_dma<D>(K + t0, key_row, buf, wave, lane);
+    tile_dma<D>(V + t0, key_row, buf + TILE, wave, lane);
   };
-  auto store_tile = [&](int buf) {
-    bf16_t *ks = KV + buf * BUF + soff, *vs = ks + 64 * KP;
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      *reinterpret_cast<u32x4 *>(ks + v * (256 / VPR) * KP) = kr[v];
-      *reinterpret_cast<u32x4 *>(vs + v * (256 / VPR) * KP) = vr[v];
-    }
-  };
-  if (seq.ntile > 0) {
-    load_tile(seq.tile_of(0));
-    store_tile(0);
-    if (seq.ntile > 1) load_tile(seq.tile_of(1));
-  }
-  lds_barrier();
-  for (int jt = 0, buf = 0; jt < seq.ntile; ++jt, buf ^= 1) {
-    const bf16_t *Ks = KV + buf * BUF, *Vs = Ks + 64 * KP;
+  auto step = [&](int jt, const bf16_t *Ks, bf16_t *nxt) {
+    if (jt + 1 < seq.ntile) issue(seq.tile_of(jt + 1), nxt);
+    const bf16_t *Vs = Ks + TILE;
     const int key0 = seq.tile_of(jt) * 64;
     const bool interior = key0 + 63 <= pos_first && (key0 + 63 < init_end || key0 >= a_last);
 #pragma unroll
@@ -368,8 +347,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          st[j] = mfma16x16x32(load_bf16x8(&Ks[(j * 16 + l16) * KP + kb * 32 + kq]), qf[c][kb], st[j]);
-          dp[j] = mfma16x16x32(load_bf16x8(&Vs[(j * 16 + l16) * KP + kb * 32 + kq]), df[c][kb], dp[j]);
+          st[j] = mfma16x16x32(load_bf16x8(&Ks[swz<D>(j * 16 + l16, kb * 32 + kq)]), qf[c][kb], st[j]);
+          dp[j] = mfma16x16x32(load_bf16x8(&Vs[swz<D>(j * 16 + l16, kb * 32 + kq)]), df[c][kb], dp[j]);
         }
       // interior tiles (inside every row's band) need no mask: rows outside
       // the band compute values that are discarded.  A masked score is -inf
@@ -394,15 +373,19 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
       const bf16x8 sb0 = pack_bf16x8(dp[0], dp[1]), sb1 = pack_bf16x8(dp[2], dp[3]);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        dq[c][nt] = mfma16x16x32(lds_col8(Ks, KP, q4 * 4, 16 + q4 * 4, nt * 16, l16), sb0, dq[c][nt]);
-        dq[c][nt] = mfma16x16x32(lds_col8(Ks, KP, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dq[c][nt]);
+        dq[c][nt] = mfma16x16x32(lds_col8_sw<D>(Ks, q4 * 4, 16 + q4 * 4, nt * 16, l16), sb0, dq[c][nt]);
+        dq[c][nt] = mfma16x16x32(lds_col8_sw<D>(Ks, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dq[c][nt]);
       }
     }
-    if (jt + 1 < seq.ntile) {
-      store_tile(buf ^ 1);
-      if (jt + 2 < seq.ntile) load_tile(seq.tile_of(jt + 2));
-    }
+    dma_wait();
     lds_barrier();
+  };
+  if (seq.ntile > 0) issue(seq.tile_of(0), KV0);
+  dma_wait();
+  lds_barrier();
+  for (int jt = 0; jt < seq.ntile; jt += 2) {
+    step(jt, KV0, KV1);
+    if (jt + 1 < seq.ntile) step(jt + 1, KV1, KV0);
   }
 
   auto dest = [&](int r) {
@@ -413,7 +396,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
 #pragma unroll
   for (int c = 0; c < RT; ++c) {
     const int r0 = (wave * RT + c) * 16;
-    bf16_t *os = KV + wave * 16 * SP;  // every wave has passed the loop's last barrier
+    bf16_t *os = KV0 + wave * 16 * SP;  // every wave has passed the loop's last barrier
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const bf16_t o4[4] = {f32_to_bf16(dq[c][nt][0] * gm.scale), f32_to_bf16(dq[c][nt][1] * gm.scale),
