@@ -476,11 +476,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
   const int key = key0 + wave * 16 + l16;  // the key whose S column this lane holds
   // the chunk's rows (token c0 + r / G, head r % G; tokens past r_hi repeat the
   // last one and are masked) and, for thread r < 64, that row's LSE, D,
-  // position (-1: not in the band) and band start.  Chunk c0 + CT is loaded
-  // into registers while chunk c0 is used.
+  // token and band flag.  Chunk c0 + CT is loaded into registers while chunk
+  // c0 is used; nothing loaded is looked at before the next chunk's staging
+  // (a test of the flag right after its load would wait for the rows too).
   u32x4 pq[NV], pd[NV];
   float plse = 0.f, pdd = 0.f;
-  int ppos = -1, pa = 0;
+  int ptok = 0, pflag = 0;
   auto load_rows = [&](int c0) {
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
@@ -495,8 +496,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       const int ti = min(tok, r_hi);
       plse = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + ti];
       pdd = Dvec[((int64_t)b * gm.Lq + ti) * gm.Hq + h];
-      ppos = (tok <= r_hi && bf[ti] != 0) ? gm.q_pos0 + ti : -1;
-      pa = band_first_key(gm, gm.q_pos0 + ti);
+      pflag = bf[ti];
+      ptok = tok;
     }
   };
   if (r_lo <= r_hi) load_rows(r_lo);
@@ -509,10 +510,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       *reinterpret_cast<u32x4 *>(&dOs[r * KPQ + c8]) = pd[v];
     }
     if (tid < 64) {
-      lse_s[tid] = ppos >= 0 ? plse * kLog2e : INFINITY;  // rows outside the band: weight 2^-inf = 0
+      const int ti = min(ptok, r_hi);
+      const bool in_band = ptok <= r_hi && pflag != 0;
+      lse_s[tid] = in_band ? plse * kLog2e : INFINITY;  // rows outside the band: weight 2^-inf = 0
       dd_s[tid] = pdd;
-      pos_s[tid] = ppos;
-      a_s[tid] = pa;
+      pos_s[tid] = in_band ? gm.q_pos0 + ti : -1;
+      a_s[tid] = band_first_key(gm, gm.q_pos0 + ti);
     }
     lds_barrier();
     // the chunk's tokens ascend, and so do their positions and band starts:
