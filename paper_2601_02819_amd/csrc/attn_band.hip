@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
   const uint8_t *bf = ix.bflag + (int64_t)bg * gm.Lq;
 
   // the rows of this lane: chunk c, MFMA row (wave RT + c) 16 + l16
-  int pos[RT], a0[RT], tokc[RT];
+  int pos[RT], a0[RT];
   bool ok[RT];
   bf16x8 qf[RT][KB];
 #pragma unroll
@@ -101,7 +101,6 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
     const int r = (wave * RT + c) * 16 + l16;
     const int tok = i0 + r / G, h = r % G;
     const int ti = min(tok, i1);
-    tokc[c] = tok;
     ok[c] = tok <= i1 && bf[ti] != 0;
     pos[c] = gm.q_pos0 + ti;
     a0[c] = band_first_key(gm, pos[c]);
@@ -239,15 +238,17 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 
   // partials: row (token, head) at list position band_base + (b, g, token); rows
   // outside the band go to the discard row
-  auto dest = [&](int r) {
-    const int tok = i0 + r / G;
-    const bool v = tok <= i1 && bf[min(tok, i1)] != 0;
-    return v ? (ix.band_base + (int64_t)bg * gm.Lq + tok) * G + r % G : ix.discard;
+  // a row's band flag is the ok bit of the lanes that hold it (lane j < 16 of
+  // chunk c: row r0 + j), gathered by a ballot instead of loaded again
+  auto dest = [&](uint64_t okm, int r0, int j) {
+    const int r = r0 + j, tok = i0 + r / G;
+    return (okm >> j) & 1 ? (ix.band_base + (int64_t)bg * gm.Lq + tok) * G + r % G : ix.discard;
   };
 #pragma unroll
   for (int c = 0; c < RT; ++c) {
     const int r0 = (wave * RT + c) * 16;
-    ml[q4 == 0 ? dest(r0 + l16) : ix.discard] = make_float2(mrun[c], lacc[c][0]);
+    const uint64_t okm = __ballot(ok[c]);
+    ml[q4 == 0 ? dest(okm, r0, l16) : ix.discard] = make_float2(mrun[c], lacc[c][0]);
     bf16_t *os = KV0 + wave * 16 * SP;  // every wave has passed the loop's last barrier
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -259,11 +260,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 #pragma unroll
     for (int k = 0; k < 16 * VPR / 64; ++k) {
       const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
-      *reinterpret_cast<uint4 *>(opart + dest(r0 + r) * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
+      *reinterpret_cast<uint4 *>(opart + dest(okm, r0, r) * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
     }
     wave_lds_sync();
   }
-  (void)tokc;
 }
 
 // ---------------------------------------------------------------- backward: dQ
@@ -388,14 +388,16 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
     if (jt + 1 < seq.ntile) step(jt + 1, KV1, KV0);
   }
 
-  auto dest = [&](int r) {
-    const int tok = i0 + r / G;
-    const bool v = tok <= i1 && bf[min(tok, i1)] != 0;
-    return v ? (ix.band_base + (int64_t)bg * gm.Lq + tok) * G + r % G : ix.discard;
+  // a row's band flag is the ok bit of the lanes that hold it (lane j < 16 of
+  // chunk c: row r0 + j), gathered by a ballot instead of loaded again
+  auto dest = [&](uint64_t okm, int r0, int j) {
+    const int r = r0 + j, tok = i0 + r / G;
+    return (okm >> j) & 1 ? (ix.band_base + (int64_t)bg * gm.Lq + tok) * G + r % G : ix.discard;
   };
 #pragma unroll
   for (int c = 0; c < RT; ++c) {
     const int r0 = (wave * RT + c) * 16;
+    const uint64_t okm = __ballot(ok[c]);
     bf16_t *os = KV0 + wave * 16 * SP;  // every wave has passed the loop's last barrier
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -407,7 +409,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
 #pragma unroll
     for (int k = 0; k < 16 * VPR / 64; ++k) {
       const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
-      *reinterpret_cast<uint4 *>(dqpart + dest(r0 + r) * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
+      *reinterpret_cast<uint4 *>(dqpart + dest(okm, r0, r) * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
     }
     wave_lds_sync();
   }

@@ -308,19 +308,27 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_sparse_kernel(
   const int kk = wave * 16 + l16;
   if (whole_block) {
     const int64_t dst = (krow0 + (int64_t)kk * gm.Hkv) * D + q4 * 4;
-    // the band's contribution to these keys (a band geometry), already scaled
-    const float *bk = bkv ? bkv + (int64_t)bgt * 2 * 64 * D + kk * D + q4 * 4 : nullptr;
+    // the band's contribution to these keys (a band geometry), already scaled;
+    // all of it is loaded before any is used, so the loads overlap
+    f32x4 ak[NT], av[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) ak[nt] = av[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (bkv) {
+      const float *bk = bkv + (int64_t)bgt * 2 * 64 * D + kk * D + q4 * 4;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        ak[nt] = *reinterpret_cast<const f32x4 *>(bk + nt * 16);
+        av[nt] = *reinterpret_cast<const f32x4 *>(bk + 64 * D + nt * 16);
+      }
+    }
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      float4 ak = make_float4(0.f, 0.f, 0.f, 0.f), av = ak;
-      if (bk) {
-        ak = *reinterpret_cast<const float4 *>(bk + nt * 16);
-        av = *reinterpret_cast<const float4 *>(bk + 64 * D + nt * 16);
-      }
-      const bf16_t k4[4] = {f32_to_bf16(dkt[nt][0] + ak.x), f32_to_bf16(dkt[nt][1] + ak.y),
-                            f32_to_bf16(dkt[nt][2] + ak.z), f32_to_bf16(dkt[nt][3] + ak.w)};
-      const bf16_t v4[4] = {f32_to_bf16(fmaf(dvt[nt][0], inv_scale, av.x)), f32_to_bf16(fmaf(dvt[nt][1], inv_scale, av.y)),
-                            f32_to_bf16(fmaf(dvt[nt][2], inv_scale, av.z)), f32_to_bf16(fmaf(dvt[nt][3], inv_scale, av.w))};
+      const bf16_t k4[4] = {f32_to_bf16(dkt[nt][0] + ak[nt][0]), f32_to_bf16(dkt[nt][1] + ak[nt][1]),
+                            f32_to_bf16(dkt[nt][2] + ak[nt][2]), f32_to_bf16(dkt[nt][3] + ak[nt][3])};
+      const bf16_t v4[4] = {f32_to_bf16(fmaf(dvt[nt][0], inv_scale, av[nt][0])),
+                            f32_to_bf16(fmaf(dvt[nt][1], inv_scale, av[nt][1])),
+                            f32_to_bf16(fmaf(dvt[nt][2], inv_scale, av[nt][2])),
+                            f32_to_bf16(fmaf(dvt[nt][3], inv_scale, av[nt][3]))};
       *reinterpret_cast<uint2 *>(dK + dst + nt * 16) = *reinterpret_cast<const uint2 *>(k4);
       *reinterpret_cast<uint2 *>(dV + dst + nt * 16) = *reinterpret_cast<const uint2 *>(v4);
     }
