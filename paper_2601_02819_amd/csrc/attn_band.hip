@@ -19,8 +19,10 @@
 //                 list position band_base + row; the per-row merges find it
 //                 through the slot after the row's sparse entries.
 //   dK, dV      : key-major.  A workgroup holds one 64-key tile (wave w owns
-//                 keys 16w..16w+15, accumulators in registers) and streams the
-//                 contiguous rows whose forced keys reach into it; it writes
+//                 keys 16w..16w+15: their K and V fragments and the dK, dV
+//                 accumulators in registers) and streams the contiguous rows
+//                 whose forced keys reach into it, each 64-row chunk of Q and
+//                 dO copied straight into LDS while the previous one is used; it writes
 //                 the tile's float32 dK/dV to bkv, which the sparse backward's
 //                 epilogue and the dK/dV finalize add to the sparse part.  An
 //                 init tile is reached by every later row: its rows are split
@@ -429,20 +431,21 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
     const bf16_t *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dvec, Geom gm, IndexWs ix,
     int kt0, int nseg, int seg_tok, int out_tiles, float *__restrict__ out) {
   constexpr int CT = 64 / G;             // tokens per chunk
-  constexpr int KPQ = D + 16;
-  constexpr int VPR = D / 8, KB = D / 32, NT = D / 16;
-  constexpr int NV = 64 * VPR / 256;     // 16-byte loads per thread per tensor per chunk
-  constexpr int KPK = D + 8;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[64 * KPK];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[64 * KPK];
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[64 * KPQ];
-  __shared__ __attribute__((aligned(16))) bf16_t dOs[64 * KPQ];
-  __shared__ __attribute__((aligned(16))) float lse_s[64];
-  __shared__ __attribute__((aligned(16))) float dd_s[64];
-  __shared__ __attribute__((aligned(16))) int pos_s[64];
-  __shared__ __attribute__((aligned(16))) int a_s[64];
+  constexpr int KB = D / 32, NT = D / 16;
+  constexpr int TILE = 64 * D;           // one chunk's Q or dO rows (swizzled, no padding)
+  // two buffers of a chunk's Q and dO rows: chunk c + 1 is copied from global
+  // memory straight into one while chunk c is read from the other (two
+  // distinct arrays, so that the compiler can tell the copies from the reads)
+  __shared__ __attribute__((aligned(16))) bf16_t QD0[2 * TILE];
+  __shared__ __attribute__((aligned(16))) bf16_t QD1[2 * TILE];
+  // per buffer, the chunk's rows: LSE (log2 units; +inf outside the band), D,
+  // position (-1 outside the band) and band start
+  __shared__ __attribute__((aligned(16))) float lse_s[2][64];
+  __shared__ __attribute__((aligned(16))) float dd_s[2][64];
+  __shared__ __attribute__((aligned(16))) int pos_s[2][64];
+  __shared__ __attribute__((aligned(16))) int a_s[2][64];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, q4 = lane >> 4, kq = q4 * 8;
   // key tiles of one XCD are consecutive (they share most rows)
   const int item = xcd_item(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
@@ -463,12 +466,15 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
   r_lo = max(r_lo, seg * seg_tok);
   r_hi = min(r_hi, seg * seg_tok + seg_tok - 1);
 
-  // the tile's keys and values (wave w reads its keys 16w..16w+15 as B operands)
-  for (int x = tid; x < 64 * VPR; x += 256) {
-    const int kk = x / VPR, c8 = (x % VPR) * 8;
-    const int64_t src = (((int64_t)b * gm.Lk + key0 + kk) * gm.Hkv + g) * D + c8;
-    *reinterpret_cast<uint4 *>(&Ks[kk * KPK + c8]) = *reinterpret_cast<const uint4 *>(K + src);
-    *reinterpret_cast<uint4 *>(&Vs[kk * KPK + c8]) = *reinterpret_cast<const uint4 *>(V + src);
+  // the wave's keys 16w..16w+15 of K and V as B operands, in registers for the whole tile
+  bf16x8 kf[KB], vf[KB];
+  {
+    const int64_t src = (((int64_t)b * gm.Lk + key0 + wave * 16 + l16) * gm.Hkv + g) * D + kq;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      kf[kb] = load_bf16x8(K + src + kb * 32);
+      vf[kb] = load_bf16x8(V + src + kb * 32);
+    }
   }
   f32x4 dkt[NT], dvt[NT];
 #pragma unroll
@@ -476,23 +482,20 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
 
   const float sl2 = gm.scale * kLog2e;
   const int key = key0 + wave * 16 + l16;  // the key whose S column this lane holds
-  // the chunk's rows (token c0 + r / G, head r % G; tokens past r_hi repeat the
-  // last one and are masked) and, for thread r < 64, that row's LSE, D,
-  // token and band flag.  Chunk c0 + CT is loaded into registers while chunk
-  // c0 is used; nothing loaded is looked at before the next chunk's staging
-  // (a test of the flag right after its load would wait for the rows too).
-  u32x4 pq[NV], pd[NV];
+  // Chunk c0's rows are tokens c0 + r / G, heads r % G (tokens past r_hi repeat
+  // the last one and are masked).  Q and dO rows of a token's G heads are one
+  // contiguous run.
+  const int64_t head0 = ((int64_t)b * gm.Lq * gm.Hq + g * G) * D;
+  auto issue = [&](int c0, bf16_t *buf) {
+    auto row_off = [&](int r) { return ((int64_t)min(c0 + r / G, r_hi) * gm.Hq + r % G) * D; };
+    tile_dma<D>(Q + head0, row_off, buf, wave, lane);
+    tile_dma<D>(dO + head0, row_off, buf + TILE, wave, lane);
+  };
+  // thread r < 64 loads row r's LSE, D, band flag of a chunk into registers;
+  // they reach LDS after the chunk before it has been computed
   float plse = 0.f, pdd = 0.f;
   int ptok = 0, pflag = 0;
-  auto load_rows = [&](int c0) {
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      const int x = tid + 256 * v, r = x / VPR, c8 = (x % VPR) * 8;
-      const int tok = min(c0 + r / G, r_hi);
-      const int64_t src = (((int64_t)b * gm.Lq + tok) * gm.Hq + g * G + r % G) * D + c8;
-      pq[v] = *reinterpret_cast<const u32x4 *>(Q + src);
-      pd[v] = *reinterpret_cast<const u32x4 *>(dO + src);
-    }
+  auto load_row = [&](int c0) {
     if (tid < 64) {
       const int tok = c0 + tid / G, h = g * G + tid % G;
       const int ti = min(tok, r_hi);
@@ -502,24 +505,24 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
       ptok = tok;
     }
   };
-  if (r_lo <= r_hi) load_rows(r_lo);
-  for (int c0 = r_lo; c0 <= r_hi; c0 += CT) {
-    lds_barrier();
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      const int x = tid + 256 * v, r = x / VPR, c8 = (x % VPR) * 8;
-      *reinterpret_cast<u32x4 *>(&Qs[r * KPQ + c8]) = pq[v];
-      *reinterpret_cast<u32x4 *>(&dOs[r * KPQ + c8]) = pd[v];
-    }
+  auto store_row = [&](int sb) {
     if (tid < 64) {
       const int ti = min(ptok, r_hi);
       const bool in_band = ptok <= r_hi && pflag != 0;
-      lse_s[tid] = in_band ? plse * kLog2e : INFINITY;  // rows outside the band: weight 2^-inf = 0
-      dd_s[tid] = pdd;
-      pos_s[tid] = in_band ? gm.q_pos0 + ti : -1;
-      a_s[tid] = band_first_key(gm, gm.q_pos0 + ti);
+      lse_s[sb][tid] = in_band ? plse * kLog2e : INFINITY;  // rows outside the band: weight 2^-inf = 0
+      dd_s[sb][tid] = pdd;
+      pos_s[sb][tid] = in_band ? gm.q_pos0 + ti : -1;
+      a_s[sb][tid] = band_first_key(gm, gm.q_pos0 + ti);
     }
-    lds_barrier();
+  };
+
+  auto step = [&](int c0, const bf16_t *Qs, bf16_t *nxt, int sb) {
+    const bool more = c0 + CT <= r_hi;
+    if (more) {
+      issue(c0 + CT, nxt);
+      load_row(c0 + CT);
+    }
+    const bf16_t *dOs = Qs + TILE;
     // the chunk's tokens ascend, and so do their positions and band starts:
     // when the first token sees the wave's last key and the last token's
     // window starts by its first key (or the keys are init keys), every key of
@@ -527,33 +530,25 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
     const int wk0 = key0 + wave * 16;
     const int pos_first = gm.q_pos0 + c0, a_last = band_first_key(gm, gm.q_pos0 + min(c0 + CT - 1, r_hi));
     const bool interior = wk0 + 15 <= pos_first && (wk0 + 15 < init_end || wk0 >= a_last);
-    load_rows(min(c0 + CT, r_hi));
 
     // S and dP: 64 rows (4 tiles) x this wave's 16 keys; lane (q, j) holds rows 16 mt + 4 q + r of key j
     f32x4 s[4], dp[4];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) s[mt] = dp[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      const bf16x8 kf = load_bf16x8(&Ks[(wave * 16 + l16) * KPK + kb * 32 + kq]);
-      const bf16x8 vf = load_bf16x8(&Vs[(wave * 16 + l16) * KPK + kb * 32 + kq]);
+    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
-        s[mt] = mfma16x16x32(load_bf16x8(&Qs[(mt * 16 + l16) * KPQ + kb * 32 + kq]), kf, s[mt]);
-        dp[mt] = mfma16x16x32(load_bf16x8(&dOs[(mt * 16 + l16) * KPQ + kb * 32 + kq]), vf, dp[mt]);
+        s[mt] = mfma16x16x32(load_bf16x8(&Qs[swz<D>(mt * 16 + l16, kb * 32 + kq)]), kf[kb], s[mt]);
+        dp[mt] = mfma16x16x32(load_bf16x8(&dOs[swz<D>(mt * 16 + l16, kb * 32 + kq)]), vf[kb], dp[mt]);
       }
-    }
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       const int r0 = mt * 16 + q4 * 4;
-      const float4 lse4 = *reinterpret_cast<const float4 *>(&lse_s[r0]);
-      const float4 dd4 = *reinterpret_cast<const float4 *>(&dd_s[r0]);
-      const int4 pos4 = *reinterpret_cast<const int4 *>(&pos_s[r0]);
-      const int4 a4 = *reinterpret_cast<const int4 *>(&a_s[r0]);
+      const float4 lse4 = *reinterpret_cast<const float4 *>(&lse_s[sb][r0]);
+      const float4 dd4 = *reinterpret_cast<const float4 *>(&dd_s[sb][r0]);
       const float lsev[4] = {lse4.x, lse4.y, lse4.z, lse4.w};
       const float ddv[4] = {dd4.x, dd4.y, dd4.z, dd4.w};
-      const int posv[4] = {pos4.x, pos4.y, pos4.z, pos4.w};
-      const int av[4] = {a4.x, a4.y, a4.z, a4.w};
       if (interior) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -562,6 +557,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
           dp[mt][r] = p * (dp[mt][r] - ddv[r]);
         }
       } else {
+        const int4 pos4 = *reinterpret_cast<const int4 *>(&pos_s[sb][r0]);
+        const int4 a4 = *reinterpret_cast<const int4 *>(&a_s[sb][r0]);
+        const int posv[4] = {pos4.x, pos4.y, pos4.z, pos4.w};
+        const int av[4] = {a4.x, a4.y, a4.z, a4.w};
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const bool in = forced_key(key, posv[r], av[r], init_end);
@@ -576,11 +575,25 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dkv_kernel(
     // dV^T += dO^T P,  dK^T += Q^T dS   (feature tiles x this wave's keys)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      dvt[nt] = mfma16x16x32(lds_col8(dOs, KPQ, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, dvt[nt]);
-      dvt[nt] = mfma16x16x32(lds_col8(dOs, KPQ, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, dvt[nt]);
-      dkt[nt] = mfma16x16x32(lds_col8(Qs, KPQ, q4 * 4, 16 + q4 * 4, nt * 16, l16), sb0, dkt[nt]);
-      dkt[nt] = mfma16x16x32(lds_col8(Qs, KPQ, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dkt[nt]);
+      dvt[nt] = mfma16x16x32(lds_col8_sw<D>(dOs, q4 * 4, 16 + q4 * 4, nt * 16, l16), pb0, dvt[nt]);
+      dvt[nt] = mfma16x16x32(lds_col8_sw<D>(dOs, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), pb1, dvt[nt]);
+      dkt[nt] = mfma16x16x32(lds_col8_sw<D>(Qs, q4 * 4, 16 + q4 * 4, nt * 16, l16), sb0, dkt[nt]);
+      dkt[nt] = mfma16x16x32(lds_col8_sw<D>(Qs, 32 + q4 * 4, 48 + q4 * 4, nt * 16, l16), sb1, dkt[nt]);
     }
+    if (more) store_row(sb ^ 1);  // the other buffer's rows were last read before the previous barrier
+    dma_wait();
+    lds_barrier();
+  };
+  if (r_lo <= r_hi) {
+    issue(r_lo, QD0);
+    load_row(r_lo);
+    store_row(0);
+  }
+  dma_wait();
+  lds_barrier();
+  for (int c0 = r_lo; c0 <= r_hi; c0 += 2 * CT) {
+    step(c0, QD0, QD1, 0);
+    if (c0 + CT <= r_hi) step(c0 + CT, QD1, QD0, 1);
   }
   // the tile's dK (scaled) and dV: lane (q, j) holds features 16 nt + 4 q .. +3 of key 16 w + j
   float *pk = out + (((int64_t)bg * out_tiles + kt) * nseg + seg) * 2 * 64 * D + (wave * 16 + l16) * D + q4 * 4;
