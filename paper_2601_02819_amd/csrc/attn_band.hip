@@ -272,8 +272,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 template <int D, int G>
 __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
     const bf16_t *__restrict__ Q, const bf16_t *__restrict__ K, const bf16_t *__restrict__ V,
-    const bf16_t *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dvec, Geom gm, IndexWs ix,
-    bf16_t *__restrict__ dqpart) {
+    const bf16_t *__restrict__ O, const bf16_t *__restrict__ dO, const float *__restrict__ LSE,
+    float *__restrict__ Dvec, Geom gm, IndexWs ix, bf16_t *__restrict__ dqpart) {
   constexpr int RT = 1;                  // one 16-row chunk per wave (registers)
   constexpr int TOK = 4 * RT * 16 / G;
   constexpr int SP = D + 8;
@@ -306,13 +306,25 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
     pos[c] = gm.q_pos0 + ti;
     a0[c] = band_first_key(gm, pos[c]);
     lse2[c] = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + ti] * kLog2e;
-    dd[c] = Dvec[((int64_t)b * gm.Lq + ti) * gm.Hq + h];
     const int64_t src = (((int64_t)b * gm.Lq + ti) * gm.Hq + h) * D;
+    bf16x8 of[KB];
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
       qf[c][kb] = load_bf16x8(Q + src + kb * 32 + kq);
       df[c][kb] = load_bf16x8(dO + src + kb * 32 + kq);
+      of[kb] = load_bf16x8(O + src + kb * 32 + kq);
     }
+    // D = dO . O of the row (every row of the sequence passes here once, in
+    // the band or not): the four lanes of a row hold 32 features each
+    float part = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const v8i16 o8 = __builtin_bit_cast(v8i16, of[kb]), d8 = __builtin_bit_cast(v8i16, df[c][kb]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part = fmaf(bf16_to_f32((bf16_t)o8[e]), bf16_to_f32((bf16_t)d8[e]), part);
+    }
+    dd[c] = sum_xor32(sum_xor16(part));
+    if (q4 == 0 && tok <= i1) Dvec[((int64_t)b * gm.Lq + ti) * gm.Hq + h] = dd[c];
   }
   if (!__syncthreads_or(ok[0])) return;
   const int kt_lo = band_first_key(gm, gm.q_pos0 + i0) / 64, kt_hi = (gm.q_pos0 + i1) / 64;
@@ -654,12 +666,19 @@ int band_init_segments(const Geom &g) {
 }
 
 template <int D, int G>
-static hipError_t bwd_band_t(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
-                             const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
-                             float *seg_sums, hipStream_t s) {
+static hipError_t bwd_band_t(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
+                             const void *dO, const float *LSE, float *Dvec, const IndexWs &ix, void *dqpart,
+                             float *bkv, float *seg_sums, hipStream_t s) {
   const bf16_t *q = static_cast<const bf16_t *>(Q), *k = static_cast<const bf16_t *>(K);
   const bf16_t *v = static_cast<const bf16_t *>(V), *dout = static_cast<const bf16_t *>(dO);
   const int nit = band_init_tiles(g), R = g.B * g.Hkv;
+  // dQ first: it also writes D of every row, which the dK/dV kernels and the
+  // sparse backward read
+  constexpr int TOKQ = 64 / G;
+  timing_begin("phsa_attn_bwd_band_dq", s);
+  hipLaunchKernelGGL((attn_bwd_band_dq_kernel<D, G>), dim3((g.Lq + TOKQ - 1) / TOKQ, R), dim3(256), 0, s, q, k, v,
+                     static_cast<const bf16_t *>(O), dout, LSE, Dvec, g, ix, static_cast<bf16_t *>(dqpart));
+  timing_end(s);
   if (nit > 0) {
     const int nseg = band_init_segments(g), seg_tok = (g.Lq + nseg - 1) / nseg;
     timing_begin("phsa_attn_bwd_band_dkv_init", s);
@@ -677,11 +696,6 @@ static hipError_t bwd_band_t(const Geom &g, const void *Q, const void *K, const 
                        g, ix, nit, 1, g.Lq, g.T, bkv);
     timing_end(s);
   }
-  constexpr int TOKQ = 64 / G;
-  timing_begin("phsa_attn_bwd_band_dq", s);
-  hipLaunchKernelGGL((attn_bwd_band_dq_kernel<D, G>), dim3((g.Lq + TOKQ - 1) / TOKQ, R), dim3(256), 0, s, q, k, v,
-                     dout, LSE, Dvec, g, ix, static_cast<bf16_t *>(dqpart));
-  timing_end(s);
   return hipGetLastError();
 }
 
@@ -697,14 +711,14 @@ static hipError_t fwd_band_d(const Geom &g, const void *Q, const void *K, const 
 }
 
 template <int D>
-static hipError_t bwd_band_d(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
-                             const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
-                             float *seg_sums, hipStream_t s) {
+static hipError_t bwd_band_d(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
+                             const void *dO, const float *LSE, float *Dvec, const IndexWs &ix, void *dqpart,
+                             float *bkv, float *seg_sums, hipStream_t s) {
   switch (g.G) {
-    case 1: return bwd_band_t<D, 1>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
-    case 2: return bwd_band_t<D, 2>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
-    case 4: return bwd_band_t<D, 4>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
-    default: return bwd_band_t<D, 8>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
+    case 1: return bwd_band_t<D, 1>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
+    case 2: return bwd_band_t<D, 2>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
+    case 4: return bwd_band_t<D, 4>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
+    default: return bwd_band_t<D, 8>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
   }
 }
 
@@ -713,11 +727,11 @@ hipError_t launch_fwd_band(const Geom &g, const void *Q, const void *K, const vo
   return g.d == 128 ? fwd_band_d<128>(g, Q, K, V, ix, opart, ml, s) : fwd_band_d<64>(g, Q, K, V, ix, opart, ml, s);
 }
 
-hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
-                           const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
-                           float *seg_sums, hipStream_t s) {
-  return g.d == 128 ? bwd_band_d<128>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s)
-                    : bwd_band_d<64>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
+hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
+                           const void *dO, const float *LSE, float *Dvec, const IndexWs &ix, void *dqpart,
+                           float *bkv, float *seg_sums, hipStream_t s) {
+  return g.d == 128 ? bwd_band_d<128>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s)
+                    : bwd_band_d<64>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
 }
 
 }  // namespace phsa

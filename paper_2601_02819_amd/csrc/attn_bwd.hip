@@ -431,11 +431,11 @@ __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restri
 }
 
 template <int D, int G>
-static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
-                               const float *LSE, void *dQ, void *dK, void *dV, const IndexWs &ix,
-                               const float *Dvec, void *dqpart, float *dkvpart, float *bkv, hipStream_t s) {
-  if (g.band) {  // the band's dQ partials and dK/dV tiles first: the sparse epilogue adds the latter
-    const hipError_t e = launch_bwd_band(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, bkv, dkvpart, s);
+static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
+                               const void *dO, const float *LSE, void *dQ, void *dK, void *dV, const IndexWs &ix,
+                               float *Dvec, void *dqpart, float *dkvpart, float *bkv, hipStream_t s) {
+  if (g.band) {  // the band's dQ partials (and D) and dK/dV tiles first: the sparse epilogue adds the latter
+    const hipError_t e = launch_bwd_band(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, dkvpart, s);
     if (e != hipSuccess) return e;
   }
   const float *bk = g.band ? bkv : nullptr;
@@ -459,14 +459,14 @@ static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, cons
 }
 
 template <int D>
-static hipError_t launch_bwd_d(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
-                               const float *LSE, void *dQ, void *dK, void *dV, const IndexWs &ix,
-                               const float *Dvec, void *dqpart, float *dkvpart, float *bkv, hipStream_t s) {
+static hipError_t launch_bwd_d(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
+                               const void *dO, const float *LSE, void *dQ, void *dK, void *dV, const IndexWs &ix,
+                               float *Dvec, void *dqpart, float *dkvpart, float *bkv, hipStream_t s) {
   switch (g.G) {
-    case 1: return launch_bwd_t<D, 1>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
-    case 2: return launch_bwd_t<D, 2>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
-    case 4: return launch_bwd_t<D, 4>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
-    default: return launch_bwd_t<D, 8>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    case 1: return launch_bwd_t<D, 1>(g, Q, K, V, O, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    case 2: return launch_bwd_t<D, 2>(g, Q, K, V, O, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    case 4: return launch_bwd_t<D, 4>(g, Q, K, V, O, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+    default: return launch_bwd_t<D, 8>(g, Q, K, V, O, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
   }
 }
 
@@ -494,14 +494,17 @@ hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const vo
                            const void *dO, const float *LSE, const int32_t *sel, void *dQ,
                            void *dK, void *dV, const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart,
                            float *bkv, bool reuse_index, hipStream_t s) {
-  hipError_t e = launch_bwd_pre(g, O, dO, Dvec, s);
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
+  if (!g.band) {  // with the band, its dQ kernel computes D on the way
+    e = launch_bwd_pre(g, O, dO, Dvec, s);
+    if (e != hipSuccess) return e;
+  }
   if (!reuse_index) {
     e = launch_build_index(g, sel, ix, s);
     if (e != hipSuccess) return e;
   }
-  return g.d == 128 ? launch_bwd_d<128>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s)
-                    : launch_bwd_d<64>(g, Q, K, V, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
+  return g.d == 128 ? launch_bwd_d<128>(g, Q, K, V, O, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s)
+                    : launch_bwd_d<64>(g, Q, K, V, O, dO, LSE, dQ, dK, dV, ix, Dvec, dqpart, dkvpart, bkv, s);
 }
 
 }  // namespace phsa

@@ -76,9 +76,10 @@ hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const vo
 // band kernels (attn_band.hip): local windows as dense query-major / key-major attention
 hipError_t launch_fwd_band(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
                            void *opart, float2 *ml, hipStream_t s);
-hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
-                           const float *LSE, const float *Dvec, const IndexWs &ix, void *dqpart, float *bkv,
-                           float *seg_sums, hipStream_t s);
+// the band's dQ kernel runs first and writes D = rowsum(dO * O) of every row into Dvec
+hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
+                           const void *dO, const float *LSE, float *Dvec, const IndexWs &ix, void *dqpart,
+                           float *bkv, float *seg_sums, hipStream_t s);
 hipError_t launch_bwd_pre(const Geom &g, const void *O, const void *dO, float *Dvec, hipStream_t s);
 hipError_t launch_attn_fwd_fp32(const Geom &g, const float *Q, const float *K, const float *V,
                                 const int32_t *sel, float *O, float *LSE, hipStream_t s);
