@@ -72,7 +72,9 @@ template <int D, int G>
 __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__restrict__ Q,
                                                                const bf16_t *__restrict__ K,
                                                                const bf16_t *__restrict__ V, Geom gm, IndexWs ix,
-                                                               bf16_t *__restrict__ opart, float2 *__restrict__ ml) {
+                                                               const bf16_t *__restrict__ opart,
+                                                               const float2 *__restrict__ ml, bf16_t *__restrict__ O,
+                                                               float *__restrict__ LSE) {
   constexpr int RT = 2;                  // 16-row chunks per wave
   constexpr int TOK = 4 * RT * 16 / G;   // tokens per workgroup
   constexpr int SP = D + 8;
@@ -110,11 +112,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) qf[c][kb] = load_bf16x8(src + kb * 32 + kq);
   }
-  if (!__syncthreads_or(ok[0] || ok[RT - 1])) return;
+  // a workgroup without band rows attends to no tile, but still merges its rows
+  const bool any_band = __syncthreads_or(ok[0] || ok[RT - 1]);
   const int kt_lo = band_first_key(gm, gm.q_pos0 + i0) / 64, kt_hi = (gm.q_pos0 + i1) / 64;
   const int a_last = band_first_key(gm, gm.q_pos0 + i1), pos_first = gm.q_pos0 + i0;
   const int init_end = init_end_key(gm);
-  const TileSeq seq(kt_lo, kt_hi, init_end);
+  TileSeq seq(kt_lo, kt_hi, init_end);
+  if (!any_band) seq.ntile = 0;
 
   const float sl2 = gm.scale * kLog2e;
   // the row sums l accumulate on the matrix cores: an all-ones A operand
@@ -238,33 +242,83 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
     if (j + 1 < seq.ntile) step(j + 1, KV1, KV0);
   }
 
-  // partials: row (token, head) at list position band_base + (b, g, token); rows
-  // outside the band go to the discard row
-  // a row's band flag is the ok bit of the lanes that hold it (lane j < 16 of
-  // chunk c: row r0 + j), gathered by a ballot instead of loaded again
-  auto dest = [&](uint64_t okm, int r0, int j) {
-    const int r = r0 + j, tok = i0 + r / G;
-    return (okm >> j) & 1 ? (ix.band_base + (int64_t)bg * gm.Lq + tok) * G + r % G : ix.discard;
+  // The merge of the workgroup's rows (Eq. 10-11 across the row's partials),
+  // fused here: the sparse kernel's partials of a row are folded in slot
+  // order, then this kernel's band partial, whose slot follows them (the order
+  // of the per-row merge kernel).  Every wave has passed the loop's last
+  // barrier, so the tile buffers hold the band results: rows 0..63 in KV0,
+  // 64..127 in KV1, each as a bf16 row of O, then (m, l) and the band flag.
+  auto orow = [&](int r) -> bf16_t * { return (r < 64 ? KV0 : KV1) + (r & 63) * SP; };
+  auto mls = [&](int r) -> float2 * { return reinterpret_cast<float2 *>((r < 64 ? KV0 : KV1) + 64 * SP) + (r & 63); };
+  auto oks = [&](int r) -> int * {
+    return reinterpret_cast<int *>(reinterpret_cast<float2 *>((r < 64 ? KV0 : KV1) + 64 * SP) + 64) + (r & 63);
   };
+  static_assert(64 * SP * sizeof(bf16_t) + 64 * (sizeof(float2) + sizeof(int)) <= 2 * TILE * sizeof(bf16_t),
+                "band results fit a tile buffer");
 #pragma unroll
   for (int c = 0; c < RT; ++c) {
-    const int r0 = (wave * RT + c) * 16;
-    const uint64_t okm = __ballot(ok[c]);
-    ml[q4 == 0 ? dest(okm, r0, l16) : ix.discard] = make_float2(mrun[c], lacc[c][0]);
-    bf16_t *os = KV0 + wave * 16 * SP;  // every wave has passed the loop's last barrier
+    const int r = (wave * RT + c) * 16 + l16;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const bf16_t o4[4] = {f32_to_bf16(o[c][nt][0]), f32_to_bf16(o[c][nt][1]), f32_to_bf16(o[c][nt][2]),
                             f32_to_bf16(o[c][nt][3])};
-      *reinterpret_cast<uint2 *>(&os[l16 * SP + nt * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(o4);
+      *reinterpret_cast<uint2 *>(orow(r) + nt * 16 + q4 * 4) = *reinterpret_cast<const uint2 *>(o4);
     }
-    wave_lds_sync();
+    if (q4 == 0) {
+      *mls(r) = make_float2(mrun[c], lacc[c][0]);
+      *oks(r) = ok[c] ? 1 : 0;
+    }
+  }
+  __syncthreads();
+  // half a wave per token (its G heads), 8 features per lane, as in the merge kernel
+  constexpr int U = 16;  // slots whose partials are in flight together
+  const int half = lane >> 5, l32 = lane & 31;
+  // a token's list positions are loaded while the previous token's partials are
+  auto load_pos = [&](int t, int &pa, int &pb) {
+    const int i = i0 + t;
+    const bool row_ok = i <= i1;
+    const int64_t base = ((int64_t)bg * gm.Lq + (row_ok ? i : i0)) * gm.ksel;
+    pa = (row_ok && l32 < gm.ksel) ? ix.pmap[base + l32] : -1;
+    pb = (row_ok && l32 + 32 < gm.ksel) ? ix.pmap[base + l32 + 32] : -1;
+  };
+  int pa, pb;
+  load_pos(wave * 2 + half, pa, pb);
+  for (int t0 = 0; t0 < TOK; t0 += 8) {
+    const int t = t0 + wave * 2 + half, i = i0 + t;
+    const bool row_ok = i <= i1;
+    const RowSlots rs(pa, pb, half);
+    if (t0 + 8 < TOK) load_pos(t + 8, pa, pb);
+    const int ns = rs.slots();
+    for (int e = l32 * 8; e < G * D; e += 256) {
+      const int hh = e / D, cc = e - hh * D;
+      float M = -INFINITY, L = 0.f, a[8];
 #pragma unroll
-    for (int k = 0; k < 16 * VPR / 64; ++k) {
-      const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
-      *reinterpret_cast<uint4 *>(opart + dest(okm, r0, r) * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
+      for (int k = 0; k < 8; ++k) a[k] = 0.f;
+      for (int s0 = 0; s0 < ns; s0 += U) {
+        float2 q[U];
+        uint4 raw[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          const int s = s0 + k;
+          const int p = s < ns ? rs.pos(s, half) : -1;
+          const bool sp = p >= 0 && p < ix.band_base;  // a sparse partial (not the band slot)
+          q[k] = sp ? ml[(int64_t)p * G + hh] : make_float2(-INFINITY, 0.f);
+          raw[k] = sp ? ld_stream16(opart + ((int64_t)p * G + hh) * D + cc) : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) fold_partial(M, L, a, q[k], raw[k]);
+      }
+      const int r = t * G + hh;
+      if (row_ok && *oks(r)) fold_partial(M, L, a, *mls(r), *reinterpret_cast<const uint4 *>(orow(r) + cc));
+      if (!row_ok) continue;
+      const float inv = L > 0.f ? 1.f / L : 0.f;
+      bf16_t outv[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) outv[k] = f32_to_bf16(a[k] * inv);
+      *reinterpret_cast<uint4 *>(O + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + hh) * D + cc) =
+          *reinterpret_cast<const uint4 *>(outv);
+      if (cc == 0) LSE[((int64_t)b * gm.Hq + g * G + hh) * gm.Lq + i] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
     }
-    wave_lds_sync();
   }
 }
 
@@ -642,12 +696,12 @@ __global__ __launch_bounds__(256) void band_init_reduce_kernel(const float *__re
 // ---------------------------------------------------------------- launchers
 template <int D, int G>
 static hipError_t fwd_band_t(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
-                             void *opart, float2 *ml, hipStream_t s) {
+                             const void *opart, const float2 *ml, void *O, float *LSE, hipStream_t s) {
   constexpr int TOK = 128 / G;
   timing_begin("phsa_attn_fwd_band", s);
   hipLaunchKernelGGL((attn_fwd_band_kernel<D, G>), dim3((g.Lq + TOK - 1) / TOK, g.B * g.Hkv), dim3(256), 0, s,
                      static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
-                     g, ix, static_cast<bf16_t *>(opart), ml);
+                     g, ix, static_cast<const bf16_t *>(opart), ml, static_cast<bf16_t *>(O), LSE);
   timing_end(s);
   return hipGetLastError();
 }
@@ -701,12 +755,12 @@ static hipError_t bwd_band_t(const Geom &g, const void *Q, const void *K, const 
 
 template <int D>
 static hipError_t fwd_band_d(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
-                             void *opart, float2 *ml, hipStream_t s) {
+                             const void *opart, const float2 *ml, void *O, float *LSE, hipStream_t s) {
   switch (g.G) {
-    case 1: return fwd_band_t<D, 1>(g, Q, K, V, ix, opart, ml, s);
-    case 2: return fwd_band_t<D, 2>(g, Q, K, V, ix, opart, ml, s);
-    case 4: return fwd_band_t<D, 4>(g, Q, K, V, ix, opart, ml, s);
-    default: return fwd_band_t<D, 8>(g, Q, K, V, ix, opart, ml, s);
+    case 1: return fwd_band_t<D, 1>(g, Q, K, V, ix, opart, ml, O, LSE, s);
+    case 2: return fwd_band_t<D, 2>(g, Q, K, V, ix, opart, ml, O, LSE, s);
+    case 4: return fwd_band_t<D, 4>(g, Q, K, V, ix, opart, ml, O, LSE, s);
+    default: return fwd_band_t<D, 8>(g, Q, K, V, ix, opart, ml, O, LSE, s);
   }
 }
 
@@ -723,8 +777,9 @@ static hipError_t bwd_band_d(const Geom &g, const void *Q, const void *K, const 
 }
 
 hipError_t launch_fwd_band(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
-                           void *opart, float2 *ml, hipStream_t s) {
-  return g.d == 128 ? fwd_band_d<128>(g, Q, K, V, ix, opart, ml, s) : fwd_band_d<64>(g, Q, K, V, ix, opart, ml, s);
+                           const void *opart, const float2 *ml, void *O, float *LSE, hipStream_t s) {
+  return g.d == 128 ? fwd_band_d<128>(g, Q, K, V, ix, opart, ml, O, LSE, s)
+                    : fwd_band_d<64>(g, Q, K, V, ix, opart, ml, O, LSE, s);
 }
 
 hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *O,

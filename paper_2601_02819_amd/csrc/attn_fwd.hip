@@ -261,9 +261,10 @@ static hipError_t launch_fwd_t(const Geom &g, const void *Q, const void *K, cons
                      static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
                      g, ix, static_cast<bf16_t *>(opart), ml);
   timing_end(s);
-  if (g.band) {
-    const hipError_t e = launch_fwd_band(g, Q, K, V, ix, opart, ml, s);
+  if (g.band) {  // the band kernel runs after the sparse one and merges every row itself
+    const hipError_t e = launch_fwd_band(g, Q, K, V, ix, opart, ml, O, LSE, s);
     if (e != hipSuccess) return e;
+    return hipGetLastError();
   }
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_attn_fwd_combine", s);

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
 
 namespace phsa {
@@ -133,9 +134,11 @@ struct RowSlots {
   int pa, pb;
   uint64_t valid;  // this half's slots that hold a partial
   uint32_t lo, hi; // slots < 32 / >= 32 used by either half
-  __device__ __forceinline__ RowSlots(const int32_t *pmap, int64_t base, bool row_ok, int ksel, int half, int l32) {
-    pa = (row_ok && l32 < ksel) ? pmap[base + l32] : -1;
-    pb = (row_ok && l32 + 32 < ksel) ? pmap[base + l32 + 32] : -1;
+  __device__ __forceinline__ RowSlots(const int32_t *pmap, int64_t base, bool row_ok, int ksel, int half, int l32)
+      : RowSlots((row_ok && l32 < ksel) ? pmap[base + l32] : -1, (row_ok && l32 + 32 < ksel) ? pmap[base + l32 + 32] : -1,
+                 half) {}
+  // from the two positions this lane loaded (-1 for none), e.g. one row ahead
+  __device__ __forceinline__ RowSlots(int pa_, int pb_, int half) : pa(pa_), pb(pb_) {
     const uint64_t ba = __ballot(pa >= 0), bb = __ballot(pb >= 0);
     valid = ((ba >> (32 * half)) & 0xffffffffull) | (((bb >> (32 * half)) & 0xffffffffull) << 32);
     lo = (uint32_t)ba | (uint32_t)(ba >> 32);
@@ -147,6 +150,21 @@ struct RowSlots {
     return s < 32 ? __shfl(pa, src, 64) : __shfl(pb, src, 64);
   }
 };
+
+// Folds one partial of a row into a running merge (M, L, a) of Eq. 10-11:
+// q = (m, l) in log2 units, raw = 8 bf16 features of its unnormalised O.  The
+// maximum moves to the larger m and both sides are rescaled; a partial with
+// m = -inf (no key) is skipped.
+__device__ __forceinline__ void fold_partial(float &M, float &L, float (&a)[8], float2 q, const uint4 &raw) {
+  if (q.x == -INFINITY) return;
+  const float mn = fmaxf(M, q.x);
+  const float sc = __builtin_amdgcn_exp2f(M - mn), w = __builtin_amdgcn_exp2f(q.x - mn);
+  L = fmaf(w, q.y, L * sc);
+  const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) a[j] = fmaf(w, bf16_to_f32(pv[j]), a[j] * sc);
+  M = mn;
+}
 
 // The dispatcher hands workgroups to the 8 XCDs (each with its own L2) in
 // turn by linear id.  Returns the work item of linear id `lin` (of n) such that

@@ -74,8 +74,10 @@ hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const vo
                            void *dK, void *dV, const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart,
                            float *bkv, bool reuse_index, hipStream_t s);
 // band kernels (attn_band.hip): local windows as dense query-major / key-major attention
+// the forward band kernel runs after the sparse forward and merges every row
+// (the sparse partials, then its own band partial) into O and LSE
 hipError_t launch_fwd_band(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
-                           void *opart, float2 *ml, hipStream_t s);
+                           const void *opart, const float2 *ml, void *O, float *LSE, hipStream_t s);
 // the band's dQ kernel runs first and writes D = rowsum(dO * O) of every row into Dvec
 hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
                            const void *dO, const float *LSE, float *Dvec, const IndexWs &ix, void *dqpart,
