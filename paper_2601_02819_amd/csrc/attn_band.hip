@@ -14,10 +14,13 @@
 //                 tiles, then the window tiles) through LDS, each copied from
 //                 global memory straight into LDS while the previous one is
 //                 used, with an online softmax (forward) or the dQ
-//                 accumulation (backward).  A row leaves one partial
-//                 in the same format and buffer as the sparse partials, at
-//                 list position band_base + row; the per-row merges find it
-//                 through the slot after the row's sparse entries.
+//                 accumulation (backward).  The forward runs after the
+//                 sparse forward and merges its rows itself (the row's sparse
+//                 partials, then its band result); dQ leaves one partial per
+//                 row in the same format and buffer as the sparse partials, at
+//                 list position band_base + row, which the dQ merge finds
+//                 through the slot after the row's sparse entries.  The dQ
+//                 kernel runs first in the backward and also writes D.
 //   dK, dV      : key-major.  A workgroup holds one 64-key tile (wave w owns
 //                 keys 16w..16w+15: their K and V fragments and the dK, dV
 //                 accumulators in registers) and streams the contiguous rows
