@@ -52,7 +52,7 @@ size_t index_layout(const Geom &g, char *base, IndexWs *ix) {
 // to its other selected blocks with the sparse ones.  Without a window a row
 // has two forced tiles (block 0 and its own), too few for the band kernels'
 // per-workgroup cost: at 4 x 32k with 64-token blocks the band took the step
-// from 11.95 to 12.74 ms, so those forced blocks stay in the sparse kernels.
+// from 11.47 to 12.02 ms, so those forced blocks stay in the sparse kernels.
 bool band_on(const Geom &g) {
   return g.dtype == PHSA_BF16 && g.window >= 64 && g.Lk % 64 == 0 && std::min(g.ksel, g.Lk / 64) <= 63;
 }
