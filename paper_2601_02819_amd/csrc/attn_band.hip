@@ -273,10 +273,17 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
     }
   }
   __syncthreads();
-  // half a wave per token (its G heads), 8 features per lane, as in the merge kernel
-  constexpr int U = 16;  // slots whose partials are in flight together
+  // half a wave per token (its G heads), 8 features per lane, as in the merge
+  // kernel; each half-wave merges NP tokens at a time (t, t + 8, ...), so that
+  // their partials are in flight together (this kernel holds only 8 waves per
+  // CU: eight tokens with two slots each in flight took the merge of the
+  // paper's geometry from 2.67 to 2.45 ms, one token with sixteen slots was
+  // the slowest)
+  constexpr int U = 2;                           // slots per token whose partials are in flight together
+  constexpr int NP = TOK >= 64 ? 8 : TOK / 8;  // tokens per half-wave at a time
+  static_assert(TOK % (8 * NP) == 0, "token groups");
   const int half = lane >> 5, l32 = lane & 31;
-  // a token's list positions are loaded while the previous token's partials are
+  // a token's list positions are loaded while the previous tokens' partials are
   auto load_pos = [&](int t, int &pa, int &pb) {
     const int i = i0 + t;
     const bool row_ok = i <= i1;
@@ -284,43 +291,65 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
     pa = (row_ok && l32 < gm.ksel) ? ix.pmap[base + l32] : -1;
     pb = (row_ok && l32 + 32 < gm.ksel) ? ix.pmap[base + l32 + 32] : -1;
   };
-  int pa, pb;
-  load_pos(wave * 2 + half, pa, pb);
-  for (int t0 = 0; t0 < TOK; t0 += 8) {
-    const int t = t0 + wave * 2 + half, i = i0 + t;
-    const bool row_ok = i <= i1;
-    const RowSlots rs(pa, pb, half);
-    if (t0 + 8 < TOK) load_pos(t + 8, pa, pb);
-    const int ns = rs.slots();
+  int pa[NP], pb[NP];
+#pragma unroll
+  for (int u = 0; u < NP; ++u) load_pos(wave * 2 + half + 8 * u, pa[u], pb[u]);
+  for (int t0 = 0; t0 < TOK; t0 += 8 * NP) {
+    RowSlots rs[NP];
+    int ns = 0;
+#pragma unroll
+    for (int u = 0; u < NP; ++u) {
+      rs[u] = RowSlots(pa[u], pb[u], half);
+      ns = max(ns, rs[u].slots());
+    }
+    if (t0 + 8 * NP < TOK) {
+#pragma unroll
+      for (int u = 0; u < NP; ++u) load_pos(t0 + 8 * NP + wave * 2 + half + 8 * u, pa[u], pb[u]);
+    }
     for (int e = l32 * 8; e < G * D; e += 256) {
       const int hh = e / D, cc = e - hh * D;
-      float M = -INFINITY, L = 0.f, a[8];
+      float M[NP], L[NP], a[NP][8];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) a[k] = 0.f;
-      for (int s0 = 0; s0 < ns; s0 += U) {
-        float2 q[U];
-        uint4 raw[U];
+      for (int u = 0; u < NP; ++u) {
+        M[u] = -INFINITY;
+        L[u] = 0.f;
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
-          const int s = s0 + k;
-          const int p = s < ns ? rs.pos(s, half) : -1;
-          const bool sp = p >= 0 && p < ix.band_base;  // a sparse partial (not the band slot)
-          q[k] = sp ? ml[(int64_t)p * G + hh] : make_float2(-INFINITY, 0.f);
-          raw[k] = sp ? ld_stream16(opart + ((int64_t)p * G + hh) * D + cc) : make_uint4(0u, 0u, 0u, 0u);
-        }
-#pragma unroll
-        for (int k = 0; k < U; ++k) fold_partial(M, L, a, q[k], raw[k]);
+        for (int k = 0; k < 8; ++k) a[u][k] = 0.f;
       }
-      const int r = t * G + hh;
-      if (row_ok && *oks(r)) fold_partial(M, L, a, *mls(r), *reinterpret_cast<const uint4 *>(orow(r) + cc));
-      if (!row_ok) continue;
-      const float inv = L > 0.f ? 1.f / L : 0.f;
-      bf16_t outv[8];
+      for (int s0 = 0; s0 < ns; s0 += U) {
+        float2 q[NP][U];
+        uint4 raw[NP][U];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) outv[k] = f32_to_bf16(a[k] * inv);
-      *reinterpret_cast<uint4 *>(O + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + hh) * D + cc) =
-          *reinterpret_cast<const uint4 *>(outv);
-      if (cc == 0) LSE[((int64_t)b * gm.Hq + g * G + hh) * gm.Lq + i] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+        for (int k = 0; k < U; ++k)
+#pragma unroll
+          for (int u = 0; u < NP; ++u) {
+            const int s = s0 + k;
+            const int p = s < ns ? rs[u].pos(s, half) : -1;
+            const bool sp = p >= 0 && p < ix.band_base;  // a sparse partial (not the band slot)
+            q[u][k] = sp ? ml[(int64_t)p * G + hh] : make_float2(-INFINITY, 0.f);
+            raw[u][k] = sp ? ld_stream16(opart + ((int64_t)p * G + hh) * D + cc) : make_uint4(0u, 0u, 0u, 0u);
+          }
+#pragma unroll
+        for (int k = 0; k < U; ++k)
+#pragma unroll
+          for (int u = 0; u < NP; ++u) fold_partial(M[u], L[u], a[u], q[u][k], raw[u][k]);
+      }
+#pragma unroll
+      for (int u = 0; u < NP; ++u) {
+        const int t = t0 + wave * 2 + half + 8 * u, i = i0 + t;
+        const bool row_ok = i <= i1;
+        const int r = t * G + hh;
+        if (row_ok && *oks(r)) fold_partial(M[u], L[u], a[u], *mls(r), *reinterpret_cast<const uint4 *>(orow(r) + cc));
+        if (!row_ok) continue;
+        const float inv = L[u] > 0.f ? 1.f / L[u] : 0.f;
+        bf16_t outv[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) outv[k] = f32_to_bf16(a[u][k] * inv);
+        *reinterpret_cast<uint4 *>(O + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + hh) * D + cc) =
+            *reinterpret_cast<const uint4 *>(outv);
+        if (cc == 0)
+          LSE[((int64_t)b * gm.Hq + g * G + hh) * gm.Lq + i] = L[u] > 0.f ? (M[u] + log2f(L[u])) * kLn2 : -INFINITY;
+      }
     }
   }
 }

@@ -137,6 +137,7 @@ struct RowSlots {
   __device__ __forceinline__ RowSlots(const int32_t *pmap, int64_t base, bool row_ok, int ksel, int half, int l32)
       : RowSlots((row_ok && l32 < ksel) ? pmap[base + l32] : -1, (row_ok && l32 + 32 < ksel) ? pmap[base + l32 + 32] : -1,
                  half) {}
+  RowSlots() = default;
   // from the two positions this lane loaded (-1 for none), e.g. one row ahead
   __device__ __forceinline__ RowSlots(int pa_, int pb_, int half) : pa(pa_), pb(pb_) {
     const uint64_t ba = __ballot(pa >= 0), bb = __ballot(pb >= 0);
