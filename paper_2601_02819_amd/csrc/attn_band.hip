@@ -14,13 +14,12 @@
 //                 tiles, then the window tiles) through LDS, each copied from
 //                 global memory straight into LDS while the previous one is
 //                 used, with an online softmax (forward) or the dQ
-//                 accumulation (backward).  The forward runs after the
-//                 sparse forward and merges its rows itself (the row's sparse
-//                 partials, then its band result); dQ leaves one partial per
-//                 row in the same format and buffer as the sparse partials, at
-//                 list position band_base + row, which the dQ merge finds
-//                 through the slot after the row's sparse entries.  The dQ
-//                 kernel runs first in the backward and also writes D.
+//                 accumulation (backward).  Both run after their sparse
+//                 kernel and merge their rows themselves: a row's sparse
+//                 partials in slot order, then its band result, whose slot
+//                 (list position band_base + row) follows the row's sparse
+//                 entries; that is the order of the per-row merge kernels
+//                 used without a band, so the results are the same bits.
 //   dK, dV      : key-major.  A workgroup holds one 64-key tile (wave w owns
 //                 keys 16w..16w+15: their K and V fragments and the dK, dV
 //                 accumulators in registers) and streams the contiguous rows
@@ -358,8 +357,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 template <int D, int G>
 __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
     const bf16_t *__restrict__ Q, const bf16_t *__restrict__ K, const bf16_t *__restrict__ V,
-    const bf16_t *__restrict__ O, const bf16_t *__restrict__ dO, const float *__restrict__ LSE,
-    float *__restrict__ Dvec, Geom gm, IndexWs ix, bf16_t *__restrict__ dqpart) {
+    const bf16_t *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dvec, Geom gm,
+    IndexWs ix, const bf16_t *__restrict__ dqpart, bf16_t *__restrict__ dQ) {
   constexpr int RT = 1;                  // one 16-row chunk per wave (registers)
   constexpr int TOK = 4 * RT * 16 / G;
   constexpr int SP = D + 8;
@@ -392,31 +391,21 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
     pos[c] = gm.q_pos0 + ti;
     a0[c] = band_first_key(gm, pos[c]);
     lse2[c] = LSE[((int64_t)b * gm.Hq + h) * gm.Lq + ti] * kLog2e;
+    dd[c] = Dvec[((int64_t)b * gm.Lq + ti) * gm.Hq + h];
     const int64_t src = (((int64_t)b * gm.Lq + ti) * gm.Hq + h) * D;
-    bf16x8 of[KB];
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
       qf[c][kb] = load_bf16x8(Q + src + kb * 32 + kq);
       df[c][kb] = load_bf16x8(dO + src + kb * 32 + kq);
-      of[kb] = load_bf16x8(O + src + kb * 32 + kq);
     }
-    // D = dO . O of the row (every row of the sequence passes here once, in
-    // the band or not): the four lanes of a row hold 32 features each
-    float part = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      const v8i16 o8 = __builtin_bit_cast(v8i16, of[kb]), d8 = __builtin_bit_cast(v8i16, df[c][kb]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) part = fmaf(bf16_to_f32((bf16_t)o8[e]), bf16_to_f32((bf16_t)d8[e]), part);
-    }
-    dd[c] = sum_xor32(sum_xor16(part));
-    if (q4 == 0 && tok <= i1) Dvec[((int64_t)b * gm.Lq + ti) * gm.Hq + h] = dd[c];
   }
-  if (!__syncthreads_or(ok[0])) return;
+  // a workgroup without band rows attends to no tile, but still merges its rows
+  const bool any_band = __syncthreads_or(ok[0]);
   const int kt_lo = band_first_key(gm, gm.q_pos0 + i0) / 64, kt_hi = (gm.q_pos0 + i1) / 64;
   const int a_last = band_first_key(gm, gm.q_pos0 + i1), pos_first = gm.q_pos0 + i0;
   const int init_end = init_end_key(gm);
-  const TileSeq seq(kt_lo, kt_hi, init_end);
+  TileSeq seq(kt_lo, kt_hi, init_end);
+  if (!any_band) seq.ntile = 0;
 
   const float sl2 = gm.scale * kLog2e;
   f32x4 dq[RT][NT];
@@ -488,30 +477,84 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
     if (jt + 1 < seq.ntile) step(jt + 1, KV1, KV0);
   }
 
-  // a row's band flag is the ok bit of the lanes that hold it (lane j < 16 of
-  // chunk c: row r0 + j), gathered by a ballot instead of loaded again
-  auto dest = [&](uint64_t okm, int r0, int j) {
-    const int r = r0 + j, tok = i0 + r / G;
-    return (okm >> j) & 1 ? (ix.band_base + (int64_t)bg * gm.Lq + tok) * G + r % G : ix.discard;
-  };
+  // The dQ merge of the workgroup's rows, fused here: the sparse kernel's dQ
+  // partials of a row are summed in slot order, then this kernel's band dQ
+  // (rounded to bf16 like a partial), whose slot follows them: the order of
+  // the per-row merge kernel.  Every wave has passed the loop's last barrier,
+  // so KV0 holds the band results: a bf16 row of dQ per MFMA row, then the
+  // band flags.
+  int *oks = reinterpret_cast<int *>(KV0 + 64 * SP);
+  static_assert(64 * SP * sizeof(bf16_t) + 64 * sizeof(int) <= 2 * TILE * sizeof(bf16_t), "band dQ fits a tile buffer");
 #pragma unroll
   for (int c = 0; c < RT; ++c) {
-    const int r0 = (wave * RT + c) * 16;
-    const uint64_t okm = __ballot(ok[c]);
-    bf16_t *os = KV0 + wave * 16 * SP;  // every wave has passed the loop's last barrier
+    const int r = (wave * RT + c) * 16 + l16;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const bf16_t o4[4] = {f32_to_bf16(dq[c][nt][0] * gm.scale), f32_to_bf16(dq[c][nt][1] * gm.scale),
                             f32_to_bf16(dq[c][nt][2] * gm.scale), f32_to_bf16(dq[c][nt][3] * gm.scale)};
-      *reinterpret_cast<uint2 *>(&os[l16 * SP + nt * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(o4);
+      *reinterpret_cast<uint2 *>(&KV0[r * SP + nt * 16 + q4 * 4]) = *reinterpret_cast<const uint2 *>(o4);
     }
-    wave_lds_sync();
+    if (q4 == 0) oks[r] = ok[c] ? 1 : 0;
+  }
+  __syncthreads();
+  // half a wave per token (its G heads), 8 features per lane, all of the
+  // half-wave's tokens at once (t, t + 8, ...), two slots of each in flight
+  constexpr int U = 2;
+  constexpr int NP = TOK / 8;
+  static_assert(TOK % 8 == 0 && NP >= 1, "tokens per half-wave");
+  const int half = lane >> 5, l32 = lane & 31;
+  RowSlots rs[NP];
+  int ns = 0;
 #pragma unroll
-    for (int k = 0; k < 16 * VPR / 64; ++k) {
-      const int v = lane + 64 * k, r = v / VPR, cc = (v % VPR) * 8;
-      *reinterpret_cast<uint4 *>(dqpart + dest(okm, r0, r) * D + cc) = *reinterpret_cast<const uint4 *>(&os[r * SP + cc]);
+  for (int u = 0; u < NP; ++u) {
+    const int i = i0 + wave * 2 + half + 8 * u;
+    const bool row_ok = i <= i1;
+    rs[u] = RowSlots(ix.pmap, ((int64_t)bg * gm.Lq + (row_ok ? i : i0)) * gm.ksel, row_ok, gm.ksel, half, l32);
+    ns = max(ns, rs[u].slots());
+  }
+  for (int e = l32 * 8; e < G * D; e += 256) {
+    const int hh = e / D, cc = e - hh * D;
+    float a[NP][8];
+#pragma unroll
+    for (int u = 0; u < NP; ++u)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) a[u][k] = 0.f;
+    for (int s0 = 0; s0 < ns; s0 += U) {
+      uint4 raw[NP][U];
+#pragma unroll
+      for (int k = 0; k < U; ++k)
+#pragma unroll
+        for (int u = 0; u < NP; ++u) {
+          const int s = s0 + k;
+          const int p = s < ns ? rs[u].pos(s, half) : -1;
+          raw[u][k] = (p >= 0 && p < ix.band_base) ? ld_stream16(dqpart + ((int64_t)p * G + hh) * D + cc)
+                                                    : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+      for (int k = 0; k < U; ++k)
+#pragma unroll
+        for (int u = 0; u < NP; ++u) {
+          const bf16_t *pv = reinterpret_cast<const bf16_t *>(&raw[u][k]);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) a[u][j] += bf16_to_f32(pv[j]);
+        }
     }
-    wave_lds_sync();
+#pragma unroll
+    for (int u = 0; u < NP; ++u) {
+      const int t = wave * 2 + half + 8 * u, i = i0 + t;
+      if (i > i1) continue;
+      const int r = t * G + hh;
+      if (oks[r]) {
+        const bf16_t *pv = &KV0[r * SP + cc];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) a[u][j] += bf16_to_f32(pv[j]);
+      }
+      bf16_t outv[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) outv[k] = f32_to_bf16(a[u][k]);
+      *reinterpret_cast<uint4 *>(dQ + (((int64_t)b * gm.Lq + i) * gm.Hq + g * G + hh) * D + cc) =
+          *reinterpret_cast<const uint4 *>(outv);
+    }
   }
 }
 
@@ -752,19 +795,12 @@ int band_init_segments(const Geom &g) {
 }
 
 template <int D, int G>
-static hipError_t bwd_band_t(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
-                             const void *dO, const float *LSE, float *Dvec, const IndexWs &ix, void *dqpart,
-                             float *bkv, float *seg_sums, hipStream_t s) {
+static hipError_t bwd_band_dkv_t(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                                 const float *LSE, const float *Dvec, const IndexWs &ix, float *bkv, float *seg_sums,
+                                 hipStream_t s) {
   const bf16_t *q = static_cast<const bf16_t *>(Q), *k = static_cast<const bf16_t *>(K);
   const bf16_t *v = static_cast<const bf16_t *>(V), *dout = static_cast<const bf16_t *>(dO);
   const int nit = band_init_tiles(g), R = g.B * g.Hkv;
-  // dQ first: it also writes D of every row, which the dK/dV kernels and the
-  // sparse backward read
-  constexpr int TOKQ = 64 / G;
-  timing_begin("phsa_attn_bwd_band_dq", s);
-  hipLaunchKernelGGL((attn_bwd_band_dq_kernel<D, G>), dim3((g.Lq + TOKQ - 1) / TOKQ, R), dim3(256), 0, s, q, k, v,
-                     static_cast<const bf16_t *>(O), dout, LSE, Dvec, g, ix, static_cast<bf16_t *>(dqpart));
-  timing_end(s);
   if (nit > 0) {
     const int nseg = band_init_segments(g), seg_tok = (g.Lq + nseg - 1) / nseg;
     timing_begin("phsa_attn_bwd_band_dkv_init", s);
@@ -785,6 +821,20 @@ static hipError_t bwd_band_t(const Geom &g, const void *Q, const void *K, const 
   return hipGetLastError();
 }
 
+template <int D, int G>
+static hipError_t bwd_band_dq_t(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                                const float *LSE, const float *Dvec, const IndexWs &ix, const void *dqpart, void *dQ,
+                                hipStream_t s) {
+  constexpr int TOKQ = 64 / G;
+  timing_begin("phsa_attn_bwd_band_dq", s);
+  hipLaunchKernelGGL((attn_bwd_band_dq_kernel<D, G>), dim3((g.Lq + TOKQ - 1) / TOKQ, g.B * g.Hkv), dim3(256), 0, s,
+                     static_cast<const bf16_t *>(Q), static_cast<const bf16_t *>(K), static_cast<const bf16_t *>(V),
+                     static_cast<const bf16_t *>(dO), LSE, Dvec, g, ix, static_cast<const bf16_t *>(dqpart),
+                     static_cast<bf16_t *>(dQ));
+  timing_end(s);
+  return hipGetLastError();
+}
+
 template <int D>
 static hipError_t fwd_band_d(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
                              const void *opart, const float2 *ml, void *O, float *LSE, hipStream_t s) {
@@ -797,14 +847,26 @@ static hipError_t fwd_band_d(const Geom &g, const void *Q, const void *K, const 
 }
 
 template <int D>
-static hipError_t bwd_band_d(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
-                             const void *dO, const float *LSE, float *Dvec, const IndexWs &ix, void *dqpart,
-                             float *bkv, float *seg_sums, hipStream_t s) {
+static hipError_t bwd_band_dkv_d(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                                 const float *LSE, const float *Dvec, const IndexWs &ix, float *bkv, float *seg_sums,
+                                 hipStream_t s) {
   switch (g.G) {
-    case 1: return bwd_band_t<D, 1>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
-    case 2: return bwd_band_t<D, 2>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
-    case 4: return bwd_band_t<D, 4>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
-    default: return bwd_band_t<D, 8>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
+    case 1: return bwd_band_dkv_t<D, 1>(g, Q, K, V, dO, LSE, Dvec, ix, bkv, seg_sums, s);
+    case 2: return bwd_band_dkv_t<D, 2>(g, Q, K, V, dO, LSE, Dvec, ix, bkv, seg_sums, s);
+    case 4: return bwd_band_dkv_t<D, 4>(g, Q, K, V, dO, LSE, Dvec, ix, bkv, seg_sums, s);
+    default: return bwd_band_dkv_t<D, 8>(g, Q, K, V, dO, LSE, Dvec, ix, bkv, seg_sums, s);
+  }
+}
+
+template <int D>
+static hipError_t bwd_band_dq_d(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                                const float *LSE, const float *Dvec, const IndexWs &ix, const void *dqpart, void *dQ,
+                                hipStream_t s) {
+  switch (g.G) {
+    case 1: return bwd_band_dq_t<D, 1>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, dQ, s);
+    case 2: return bwd_band_dq_t<D, 2>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, dQ, s);
+    case 4: return bwd_band_dq_t<D, 4>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, dQ, s);
+    default: return bwd_band_dq_t<D, 8>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, dQ, s);
   }
 }
 
@@ -814,11 +876,18 @@ hipError_t launch_fwd_band(const Geom &g, const void *Q, const void *K, const vo
                     : fwd_band_d<64>(g, Q, K, V, ix, opart, ml, O, LSE, s);
 }
 
-hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
-                           const void *dO, const float *LSE, float *Dvec, const IndexWs &ix, void *dqpart,
-                           float *bkv, float *seg_sums, hipStream_t s) {
-  return g.d == 128 ? bwd_band_d<128>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s)
-                    : bwd_band_d<64>(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, seg_sums, s);
+hipError_t launch_bwd_band_dkv(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                               const float *LSE, const float *Dvec, const IndexWs &ix, float *bkv, float *seg_sums,
+                               hipStream_t s) {
+  return g.d == 128 ? bwd_band_dkv_d<128>(g, Q, K, V, dO, LSE, Dvec, ix, bkv, seg_sums, s)
+                    : bwd_band_dkv_d<64>(g, Q, K, V, dO, LSE, Dvec, ix, bkv, seg_sums, s);
+}
+
+hipError_t launch_bwd_band_dq(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                              const float *LSE, const float *Dvec, const IndexWs &ix, const void *dqpart, void *dQ,
+                              hipStream_t s) {
+  return g.d == 128 ? bwd_band_dq_d<128>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, dQ, s)
+                    : bwd_band_dq_d<64>(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, dQ, s);
 }
 
 }  // namespace phsa

@@ -434,8 +434,8 @@ template <int D, int G>
 static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
                                const void *dO, const float *LSE, void *dQ, void *dK, void *dV, const IndexWs &ix,
                                float *Dvec, void *dqpart, float *dkvpart, float *bkv, hipStream_t s) {
-  if (g.band) {  // the band's dQ partials (and D) and dK/dV tiles first: the sparse epilogue adds the latter
-    const hipError_t e = launch_bwd_band(g, Q, K, V, O, dO, LSE, Dvec, ix, dqpart, bkv, dkvpart, s);
+  if (g.band) {  // the band's dK/dV tiles first: the sparse epilogue adds them
+    const hipError_t e = launch_bwd_band_dkv(g, Q, K, V, dO, LSE, Dvec, ix, bkv, dkvpart, s);
     if (e != hipSuccess) return e;
   }
   const float *bk = g.band ? bkv : nullptr;
@@ -450,6 +450,11 @@ static hipError_t launch_bwd_t(const Geom &g, const void *Q, const void *K, cons
                      dkvpart, bk,
                      static_cast<bf16_t *>(dK), static_cast<bf16_t *>(dV), g, ix);
   timing_end(s);
+  if (g.band) {  // the band's dQ kernel merges every row's dQ itself
+    const hipError_t e = launch_bwd_band_dq(g, Q, K, V, dO, LSE, Dvec, ix, dqpart, dQ, s);
+    if (e != hipSuccess) return e;
+    return hipGetLastError();
+  }
   const int64_t rows = (int64_t)g.B * g.Hkv * g.Lq;
   timing_begin("phsa_attn_bwd_dq_combine", s);
   hipLaunchKernelGGL((dq_combine_kernel<D, G>), dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, s, ix.pmap,
@@ -494,11 +499,8 @@ hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const vo
                            const void *dO, const float *LSE, const int32_t *sel, void *dQ,
                            void *dK, void *dV, const IndexWs &ix, float *Dvec, void *dqpart, float *dkvpart,
                            float *bkv, bool reuse_index, hipStream_t s) {
-  hipError_t e = hipSuccess;
-  if (!g.band) {  // with the band, its dQ kernel computes D on the way
-    e = launch_bwd_pre(g, O, dO, Dvec, s);
-    if (e != hipSuccess) return e;
-  }
+  hipError_t e = launch_bwd_pre(g, O, dO, Dvec, s);
+  if (e != hipSuccess) return e;
   if (!reuse_index) {
     e = launch_build_index(g, sel, ix, s);
     if (e != hipSuccess) return e;

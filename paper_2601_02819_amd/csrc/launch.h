@@ -78,10 +78,15 @@ hipError_t launch_attn_bwd(const Geom &g, const void *Q, const void *K, const vo
 // (the sparse partials, then its own band partial) into O and LSE
 hipError_t launch_fwd_band(const Geom &g, const void *Q, const void *K, const void *V, const IndexWs &ix,
                            const void *opart, const float2 *ml, void *O, float *LSE, hipStream_t s);
-// the band's dQ kernel runs first and writes D = rowsum(dO * O) of every row into Dvec
-hipError_t launch_bwd_band(const Geom &g, const void *Q, const void *K, const void *V, const void *O,
-                           const void *dO, const float *LSE, float *Dvec, const IndexWs &ix, void *dqpart,
-                           float *bkv, float *seg_sums, hipStream_t s);
+// the band's dK/dV tiles (before the sparse backward, whose epilogue adds them)
+hipError_t launch_bwd_band_dkv(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                               const float *LSE, const float *Dvec, const IndexWs &ix, float *bkv, float *seg_sums,
+                               hipStream_t s);
+// the band's dQ (after the sparse backward): merges every row's sparse dQ
+// partials and its band dQ into dQ
+hipError_t launch_bwd_band_dq(const Geom &g, const void *Q, const void *K, const void *V, const void *dO,
+                              const float *LSE, const float *Dvec, const IndexWs &ix, const void *dqpart, void *dQ,
+                              hipStream_t s);
 hipError_t launch_bwd_pre(const Geom &g, const void *O, const void *dO, float *Dvec, hipStream_t s);
 hipError_t launch_attn_fwd_fp32(const Geom &g, const float *Q, const float *K, const float *V,
                                 const int32_t *sel, float *O, float *LSE, hipStream_t s);
