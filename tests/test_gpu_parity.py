@@ -26,6 +26,7 @@ SMALL = [
     small("ragged320", 1, 320, 2, 1, 64, 2, 1, 0),
     small("g2_win", 2, 1024, 4, 2, 128, 3, 1, 64),
     small("g8_init2", 1, 1024, 8, 1, 128, 5, 2, 128),
+    small("g4_d64_win", 1, 1088, 8, 2, 64, 4, 1, 128),   # band kernels at G = 4, head dim 64, ragged last tile
     small("g1_d64", 1, 768, 4, 4, 64, 4, 1, 0),
     small("g4_k14", 1, 2048, 16, 4, 128, 14, 1, 0),
     small("topk0", 1, 512, 2, 1, 128, 0, 1, 0),
