@@ -49,12 +49,28 @@ __device__ __forceinline__ bool plain_rows(const Geom &gm) { return gm.sm == gm.
 // that holds all of them leaves them to the band kernels.
 struct Forced {
   int ninit, a_blk, count;
-  __device__ __forceinline__ Forced(const Geom &gm, int cur) {
+  // wblk: the window in selection blocks (gm.window / gm.sm)
+  __device__ __forceinline__ Forced(const Geom &gm, int cur, int wblk) {
     ninit = min(gm.n_init, cur + 1);
-    a_blk = max(max(0, cur - gm.window / gm.sm), ninit);
+    a_blk = max(max(0, cur - wblk), ninit);
     count = ninit + cur - a_blk + 1;
   }
+  __device__ __forceinline__ Forced(const Geom &gm, int cur) : Forced(gm, cur, gm.window / gm.sm) {}
   __device__ __forceinline__ bool has(int t) const { return t < ninit || t >= a_blk; }
+};
+
+// Selection block sizes of the attention entry points are 16, 32 or 64
+// tokens, so the regrouping divides by shifts: sh = log2(sm), and a 64-key
+// tile holds 64 >> sh blocks.  All fields are wave-uniform.
+struct BlockShift {
+  int sh, per_sh, qpb, wblk, nblk;
+  __device__ __forceinline__ explicit BlockShift(const Geom &gm) {
+    sh = __builtin_ctz((unsigned)gm.sm);
+    per_sh = 6 - sh;
+    qpb = gm.sm >> 4;
+    wblk = gm.window >> sh;
+    nblk = gm.Lk >> sh;
+  }
 };
 
 // The regrouped entries of one row, one wave per row with lane s holding slot
@@ -83,18 +99,19 @@ __device__ __forceinline__ int from_lane_above(int v) {
   return __builtin_amdgcn_update_dpp(0, v, 0x130, 0xF, 0xF, true);
 }
 
-__device__ __forceinline__ RowEntries row_entries(int t, int i, const Geom &gm) {
+// i: the row (wave-uniform).
+__device__ __forceinline__ RowEntries row_entries(int t, int i, const Geom &gm, const BlockShift &bs) {
   const int lane = threadIdx.x & 63;
   RowEntries e;
   e.band_ok = false;
-  const int cur = (gm.q_pos0 + i) / gm.sm;
-  const int per = 64 / gm.sm, qpb = gm.sm / 16;
-  const bool in_range = t >= 0 && t <= cur && t < gm.Lk / gm.sm;
-  const Forced f(gm, cur);
+  const int cur = (gm.q_pos0 + i) >> bs.sh;
+  const int per = 1 << bs.per_sh, qpb = bs.qpb;
+  const bool in_range = t >= 0 && t <= cur && t < bs.nblk;
+  const Forced f(gm, cur, bs.wblk);
   if (gm.band) e.band_ok = __popcll(__ballot(in_range && f.has(t))) == f.count;
   const bool valid = in_range && !(e.band_ok && f.has(t));
-  const int tc = valid ? t / per : -1;
-  const unsigned qb = valid ? ((1u << qpb) - 1u) << ((t % per) * qpb) : 0u;
+  const int tc = valid ? t >> bs.per_sh : -1;
+  const unsigned qb = valid ? ((1u << qpb) - 1u) << ((t & (per - 1)) * qpb) : 0u;
   const int prev = from_lane_below(tc);
   const bool first = valid && (lane == 0 || prev != tc);
   const uint64_t heads = __ballot(first);
@@ -113,7 +130,11 @@ __device__ __forceinline__ RowEntries row_entries(int t, int i, const Geom &gm) 
   return e;
 }
 
-constexpr int kRowBatch = 8;  // sel rows a wave has in flight (regrouped rows)
+// Sel rows a wave loads at once (regrouped rows), waited for together.  The
+// fill stores as it goes, and loads and stores share one wait counter, so a
+// load issued after a store cannot be waited for alone: each batch waits once
+// for the previous batch's stores, not once per row.
+constexpr int kRowBatch = 16;
 
 // A plain row (one thread, its sel row staged at row[0 .. ks)) with the band:
 // does it hold every forced block?
@@ -138,7 +159,7 @@ __device__ __forceinline__ bool plain_band_ok(const int32_t *row, int ks, int cu
 // banks).  Every thread calls this (it holds barriers).
 __device__ void build_tile_bitmap(uint32_t *bm, int32_t *rows_s, const int32_t *__restrict__ sel, const Geom &gm,
                                   int bg, int w) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ks = sel_width(gm);
   const int nrow = min(kIndexTile, gm.Lq - w * kIndexTile);
   const int64_t row0 = (int64_t)bg * gm.Lq + (int64_t)w * kIndexTile;
@@ -161,6 +182,7 @@ __device__ void build_tile_bitmap(uint32_t *bm, int32_t *rows_s, const int32_t *
     return;
   }
   __syncthreads();
+  const BlockShift bs(gm);
   for (int j0 = 0; j0 < 64; j0 += kRowBatch) {
     int t[kRowBatch];
 #pragma unroll
@@ -172,7 +194,7 @@ __device__ void build_tile_bitmap(uint32_t *bm, int32_t *rows_s, const int32_t *
     for (int u = 0; u < kRowBatch; ++u) {
       const int r = wave * 64 + j0 + u;
       if (r < nrow) {  // wave-uniform
-        const RowEntries e = row_entries(t[u], w * kIndexTile + r, gm);
+        const RowEntries e = row_entries(t[u], w * kIndexTile + r, gm, bs);
         if (e.mine) atomicOr(&bm[(r >> 5) * gm.T + e.tile], 1u << (r & 31));
       }
     }
@@ -208,10 +230,18 @@ __global__ __launch_bounds__(256) void index_scan_tiles_kernel(Geom gm, IndexWs 
   const int bg = x / gm.T, t = x % gm.T;
   int32_t *col = ix.cntw + (int64_t)bg * ix.W * gm.T + t;
   int run = 0;
-  for (int w = 0; w < ix.W; ++w) {
-    const int c = col[(int64_t)w * gm.T];
-    col[(int64_t)w * gm.T] = run;
-    run += c;
+  // a batch of tiles' counts is loaded before any of them is overwritten (a
+  // load behind a store waits for the store too: one round trip per batch)
+  constexpr int U = 32;
+  for (int w0 = 0; w0 < ix.W; w0 += U) {
+    int c[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) c[u] = w0 + u < ix.W ? col[(int64_t)(w0 + u) * gm.T] : 0;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (w0 + u < ix.W) col[(int64_t)(w0 + u) * gm.T] = run;
+      run += c[u];
+    }
   }
   ix.cnt[x] = run;
 }
@@ -226,13 +256,20 @@ __global__ __launch_bounds__(1024) void index_scan_lists_kernel(IndexWs ix, int 
   const int per = (nbgt + 1023) / 1024;
   const int lo = min(nbgt, tid * per), hi = min(nbgt, lo + per);
   const int U = ix.unit_tokens;
+  // list lengths are read NB at a time, all loads of a batch in flight together
+  constexpr int NB = 16;
   int sa = 0, sb = 0, sc = 0;
-  for (int x = lo; x < hi; ++x) {
-    const int c = ix.cnt[x];
-    const int nu = (c + U - 1) / U;
-    sa += c;
-    sb += nu;
-    sc += nu != 1;
+  for (int x0 = lo; x0 < hi; x0 += NB) {
+    int cb[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) cb[j] = x0 + j < hi ? ix.cnt[x0 + j] : 0;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int nu = (cb[j] + U - 1) / U;
+      sa += cb[j];
+      sb += nu;
+      sc += x0 + j < hi && nu != 1;
+    }
   }
   s_a[tid] = sa;
   s_b[tid] = sb;
@@ -249,15 +286,26 @@ __global__ __launch_bounds__(1024) void index_scan_lists_kernel(IndexWs ix, int 
     __syncthreads();
   }
   int ra = s_a[tid] - sa, rb = s_b[tid] - sb, rc = s_c[tid] - sc;
-  for (int x = lo; x < hi; ++x) {
-    const int c = ix.cnt[x];
-    const int nu = (c + U - 1) / U;
-    ix.off[x] = ra;
-    ix.uoff[x] = rb;
-    for (int u = 0; u < nu; ++u) ix.units[rb + u] = make_int2(x, u * U);
-    if (nu != 1) ix.fin[rc++] = x;
-    ra += c;
-    rb += nu;
+  // the writes, each batch's lengths loaded before its stores (a load behind
+  // a store waits for the store too)
+  for (int x0 = lo; x0 < hi; x0 += NB) {
+    int cb[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) cb[j] = x0 + j < hi ? ix.cnt[x0 + j] : 0;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int x = x0 + j;
+      if (x < hi) {
+        const int c = cb[j];
+        const int nu = (c + U - 1) / U;
+        ix.off[x] = ra;
+        ix.uoff[x] = rb;
+        for (int u = 0; u < nu; ++u) ix.units[rb + u] = make_int2(x, u * U);
+        if (nu != 1) ix.fin[rc++] = x;
+        ra += c;
+        rb += nu;
+      }
+    }
   }
   if (tid == 1023) {
     ix.off[nbgt] = s_a[1023];
@@ -280,7 +328,15 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
   uint64_t *pre_s = reinterpret_cast<uint64_t *>(bm + 8 * gm.T);
   int32_t *base_s = reinterpret_cast<int32_t *>(pre_s + gm.T);
   int32_t *rows_s = base_s + gm.T;  // plain rows: staged sel rows, then their list positions
-  const int w = blockIdx.x, bg = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // Query tiles w, w + 1 of one (b, g) write adjacent runs of the same lists.
+  // Workgroups are dealt to the 8 XCDs in turn (each XCD its own L2), so the
+  // grid is renumbered to give each XCD one contiguous range of (bg, w): a
+  // list's cache lines are then written through one L2.
+  const int nwg = gridDim.x * gridDim.y, lin = blockIdx.x + blockIdx.y * gridDim.x;
+  const int xcd = lin & 7, q8 = nwg >> 3, r8 = nwg & 7;
+  const int logical = xcd * q8 + min(xcd, r8) + (lin >> 3);
+  const int w = logical % gridDim.x, bg = logical / gridDim.x, tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int32_t *tile_off = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
   const int32_t *list_off = ix.off + (int64_t)bg * gm.T;
   for (int t = tid; t < gm.T; t += 256) base_s[t] = list_off[t] + tile_off[t];
@@ -339,6 +395,7 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
     return;
   }
   unsigned flag = 0;  // band flag of row 64 * wave + lane
+  const BlockShift bs(gm);
   for (int j0 = 0; j0 < 64; j0 += kRowBatch) {
     int t[kRowBatch];
 #pragma unroll
@@ -346,13 +403,17 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
       const int r = wave * 64 + j0 + u;
       t[u] = (r < nrow && lane < ks) ? sel[(row0 + r) * ks + lane] : -1;
     }
+    // one wait for the whole batch here, before any branch: an (empty) use of
+    // every loaded value, so that no row below waits on the stores again
+#pragma unroll
+    for (int u = 0; u < kRowBatch; ++u) asm volatile("" ::"v"(t[u]));
 #pragma unroll
     for (int u = 0; u < kRowBatch; ++u) {
       const int r = wave * 64 + j0 + u;
       if (r >= nrow) continue;  // wave-uniform
       const int i = w * kIndexTile + r;
       const int64_t x = row0 + r;
-      const RowEntries e = row_entries(t[u], i, gm);
+      const RowEntries e = row_entries(t[u], i, gm, bs);
       int32_t p = -1;
       if (e.mine) {
         p = base_s[e.tile] + rank_of(e.tile, r);
