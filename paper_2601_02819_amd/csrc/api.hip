@@ -38,6 +38,7 @@ size_t index_layout(const Geom &g, char *base, IndexWs *ix) {
   w.off = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (nbgt + 1)));
   w.uoff = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (nbgt + 1)));
   w.totals = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * 4));
+  w.wsum = reinterpret_cast<int4 *>(take(sizeof(int4) * ((nbgt + 255) / 256)));
   w.fin = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * nbgt));
   w.tok = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * w.nnz_max));
   w.pmap = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * R * g.Lq * g.ksel));  // every slot, band slot too

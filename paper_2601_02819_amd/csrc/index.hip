@@ -19,12 +19,13 @@
 // keyed by the tile geometry gm (m = 64, T = Lk / 64, ksel = min(Ksel, T) plus
 // the band slot) while sel keeps its own width (the selection's Ksel).
 //
-// Four integer-only passes, all deterministic (no order depends on timing):
+// Integer-only passes, all deterministic (no order depends on timing):
 //   count : per 256-row tile, an LDS bitmap [8 words][T] of who selected
 //           what; popcounts give per-tile counts cntw[bg][w][t].
-//   scan1 : per (bg, t), exclusive prefix over tiles -> cntw, total -> cnt.
-//   scan2 : one workgroup scans cnt into list offsets and unit offsets and
-//           writes the unit table.
+//   scan1 : per (bg, t), exclusive prefix over tiles -> cntw, total -> cnt,
+//           and per 256 (bg, t) the sums of list lengths and units.
+//   scan2 : one workgroup turns those sums into offsets; then per (bg, t)
+//           the list offsets, unit offsets and the unit table.
 //   fill  : rebuilds the tile bitmap; an entry's place in its list is
 //           tile offset + number of lower rows in the tile that chose t.
 #include "common.h"
@@ -224,96 +225,125 @@ __global__ __launch_bounds__(256) void index_count_kernel(const int32_t *__restr
   }
 }
 
-__global__ __launch_bounds__(256) void index_scan_tiles_kernel(Geom gm, IndexWs ix, int nbgt) {
-  const int x = blockIdx.x * 256 + threadIdx.x;
-  if (x >= nbgt) return;
-  const int bg = x / gm.T, t = x % gm.T;
-  int32_t *col = ix.cntw + (int64_t)bg * ix.W * gm.T + t;
-  int run = 0;
-  // a batch of tiles' counts is loaded before any of them is overwritten (a
-  // load behind a store waits for the store too: one round trip per batch)
-  constexpr int U = 32;
-  for (int w0 = 0; w0 < ix.W; w0 += U) {
-    int c[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) c[u] = w0 + u < ix.W ? col[(int64_t)(w0 + u) * gm.T] : 0;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (w0 + u < ix.W) col[(int64_t)(w0 + u) * gm.T] = run;
-      run += c[u];
-    }
-  }
-  ix.cnt[x] = run;
+// The list scans.  For x = (b, g, t) with list length c: nu = ceil(c /
+// unit_tokens) work units, and the flag f = (nu != 1) of the blocks whose
+// dK/dV the finalize writes (from partial sums, or zeros for an empty list).
+// Exclusive prefixes over x of c, nu and f give the list offsets, the unit
+// offsets and the places in the finalize list.  Three passes, each x one
+// thread: per 256 x the sums (with the tile scan), one workgroup's scan of
+// those sums, then per 256 x the offsets and the unit table.
+struct Counts3 {
+  int c, nu, f;
+};
+
+__device__ __forceinline__ Counts3 list_counts(int c, int unit_tokens, bool live) {
+  const int nu = (c + unit_tokens - 1) / unit_tokens;
+  return Counts3{c, nu, live && nu != 1 ? 1 : 0};
 }
 
-// Single workgroup of 1024 threads: exclusive scans of list lengths, of units
-// per list and of the blocks that do not have exactly one unit (their dK/dV
-// is written by the finalize, from partial sums or from nothing), then the
-// unit table and the compact list of those blocks.
-__global__ __launch_bounds__(1024) void index_scan_lists_kernel(IndexWs ix, int nbgt) {
-  __shared__ int s_a[1024], s_b[1024], s_c[1024];
-  const int tid = threadIdx.x;
-  const int per = (nbgt + 1023) / 1024;
-  const int lo = min(nbgt, tid * per), hi = min(nbgt, lo + per);
-  const int U = ix.unit_tokens;
-  // list lengths are read NB at a time, all loads of a batch in flight together
-  constexpr int NB = 16;
-  int sa = 0, sb = 0, sc = 0;
-  for (int x0 = lo; x0 < hi; x0 += NB) {
-    int cb[NB];
+// Exclusive scan of v over a 256-thread workgroup (x, then y, then z
+// independently); tot receives the workgroup's sums.  Holds barriers.
+__device__ __forceinline__ Counts3 block_scan3(Counts3 v, Counts3 &tot) {
+  __shared__ Counts3 wsum_s[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  Counts3 inc = v;
 #pragma unroll
-    for (int j = 0; j < NB; ++j) cb[j] = x0 + j < hi ? ix.cnt[x0 + j] : 0;
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int nu = (cb[j] + U - 1) / U;
-      sa += cb[j];
-      sb += nu;
-      sc += x0 + j < hi && nu != 1;
+  for (int d = 1; d < 64; d <<= 1) {
+    const int a = __shfl_up(inc.c, d, 64), b = __shfl_up(inc.nu, d, 64), f = __shfl_up(inc.f, d, 64);
+    if (lane >= d) {
+      inc.c += a;
+      inc.nu += b;
+      inc.f += f;
     }
   }
-  s_a[tid] = sa;
-  s_b[tid] = sb;
-  s_c[tid] = sc;
+  if (lane == 63) wsum_s[wave] = inc;
   __syncthreads();
-  for (int o = 1; o < 1024; o <<= 1) {  // inclusive Hillis-Steele scan
-    const int va = tid >= o ? s_a[tid - o] : 0;
-    const int vb = tid >= o ? s_b[tid - o] : 0;
-    const int vc = tid >= o ? s_c[tid - o] : 0;
-    __syncthreads();
-    s_a[tid] += va;
-    s_b[tid] += vb;
-    s_c[tid] += vc;
-    __syncthreads();
+  Counts3 pre{0, 0, 0};
+  tot = Counts3{0, 0, 0};
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const Counts3 s = wsum_s[w];
+    if (w < wave) {
+      pre.c += s.c;
+      pre.nu += s.nu;
+      pre.f += s.f;
+    }
+    tot.c += s.c;
+    tot.nu += s.nu;
+    tot.f += s.f;
   }
-  int ra = s_a[tid] - sa, rb = s_b[tid] - sb, rc = s_c[tid] - sc;
-  // the writes, each batch's lengths loaded before its stores (a load behind
-  // a store waits for the store too)
-  for (int x0 = lo; x0 < hi; x0 += NB) {
-    int cb[NB];
+  __syncthreads();  // wsum_s may be reused by the caller's next scan
+  return Counts3{pre.c + inc.c - v.c, pre.nu + inc.nu - v.nu, pre.f + inc.f - v.f};
+}
+
+// Per (b, g, t): the tile counts become tile offsets (exclusive over the
+// query tiles) and their total the list length; then the workgroup's sums.
+__global__ __launch_bounds__(256) void index_scan_tiles_kernel(Geom gm, IndexWs ix, int nbgt) {
+  const int x = blockIdx.x * 256 + threadIdx.x;
+  const bool live = x < nbgt;
+  int run = 0;
+  if (live) {
+    const int bg = x / gm.T, t = x % gm.T;
+    int32_t *col = ix.cntw + (int64_t)bg * ix.W * gm.T + t;
+    // a batch of tiles' counts is loaded before any of them is overwritten (a
+    // load behind a store waits for the store too: one round trip per batch)
+    constexpr int U = 32;
+    for (int w0 = 0; w0 < ix.W; w0 += U) {
+      int c[U];
 #pragma unroll
-    for (int j = 0; j < NB; ++j) cb[j] = x0 + j < hi ? ix.cnt[x0 + j] : 0;
+      for (int u = 0; u < U; ++u) c[u] = w0 + u < ix.W ? col[(int64_t)(w0 + u) * gm.T] : 0;
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int x = x0 + j;
-      if (x < hi) {
-        const int c = cb[j];
-        const int nu = (c + U - 1) / U;
-        ix.off[x] = ra;
-        ix.uoff[x] = rb;
-        for (int u = 0; u < nu; ++u) ix.units[rb + u] = make_int2(x, u * U);
-        if (nu != 1) ix.fin[rc++] = x;
-        ra += c;
-        rb += nu;
+      for (int u = 0; u < U; ++u) {
+        if (w0 + u < ix.W) col[(int64_t)(w0 + u) * gm.T] = run;
+        run += c[u];
       }
     }
+    ix.cnt[x] = run;
   }
-  if (tid == 1023) {
-    ix.off[nbgt] = s_a[1023];
-    ix.uoff[nbgt] = s_b[1023];
-    ix.totals[0] = s_a[1023];
-    ix.totals[1] = s_b[1023];
-    ix.totals[2] = s_c[1023];
+  Counts3 tot;
+  block_scan3(list_counts(run, ix.unit_tokens, live), tot);
+  if (threadIdx.x == 0) ix.wsum[blockIdx.x] = make_int4(tot.c, tot.nu, tot.f, 0);
+}
+
+// One workgroup: the workgroup sums become exclusive offsets (in place), and
+// the totals (entries, units, finalize blocks) are written.
+__global__ __launch_bounds__(256) void index_scan_sums_kernel(IndexWs ix, int nw, int nbgt) {
+  Counts3 carry{0, 0, 0};
+  for (int b0 = 0; b0 < nw; b0 += 256) {
+    const int j = b0 + (int)threadIdx.x;
+    const int4 v = j < nw ? ix.wsum[j] : make_int4(0, 0, 0, 0);
+    Counts3 tot;
+    const Counts3 ex = block_scan3(Counts3{v.x, v.y, v.z}, tot);
+    if (j < nw) ix.wsum[j] = make_int4(carry.c + ex.c, carry.nu + ex.nu, carry.f + ex.f, 0);
+    carry.c += tot.c;
+    carry.nu += tot.nu;
+    carry.f += tot.f;
   }
+  if (threadIdx.x == 0) {
+    ix.off[nbgt] = carry.c;
+    ix.uoff[nbgt] = carry.nu;
+    ix.totals[0] = carry.c;
+    ix.totals[1] = carry.nu;
+    ix.totals[2] = carry.f;
+  }
+}
+
+// Per x: list offset, first unit, the unit table entries (block, first list
+// entry) and, for nu != 1, the place in the finalize list (ascending x).
+__global__ __launch_bounds__(256) void index_write_lists_kernel(IndexWs ix, int nbgt) {
+  const int x = blockIdx.x * 256 + threadIdx.x;
+  const bool live = x < nbgt;
+  const int c = live ? ix.cnt[x] : 0;
+  const int4 base = ix.wsum[blockIdx.x];
+  Counts3 tot;
+  const Counts3 v = list_counts(c, ix.unit_tokens, live);
+  const Counts3 ex = block_scan3(v, tot);
+  if (!live) return;
+  const int rb = base.y + ex.nu;
+  ix.off[x] = base.x + ex.c;
+  ix.uoff[x] = rb;
+  for (int u = 0; u < v.nu; ++u) ix.units[rb + u] = make_int2(x, u * ix.unit_tokens);
+  if (v.f) ix.fin[base.z + ex.f] = x;
 }
 
 // Writes each row's entries into their lists, its position-map row (list
@@ -438,11 +468,13 @@ hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &
   timing_begin("phsa_index_count", s);
   hipLaunchKernelGGL(index_count_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds, s, sel, g, ix);
   timing_end(s);
+  const int nw = (nbgt + 255) / 256;  // list-scan workgroups (ix.wsum entries)
   timing_begin("phsa_index_scan_tiles", s);
-  hipLaunchKernelGGL(index_scan_tiles_kernel, dim3((nbgt + 255) / 256), dim3(256), 0, s, g, ix, nbgt);
+  hipLaunchKernelGGL(index_scan_tiles_kernel, dim3(nw), dim3(256), 0, s, g, ix, nbgt);
   timing_end(s);
   timing_begin("phsa_index_scan_lists", s);
-  hipLaunchKernelGGL(index_scan_lists_kernel, dim3(1), dim3(1024), 0, s, ix, nbgt);
+  hipLaunchKernelGGL(index_scan_sums_kernel, dim3(1), dim3(256), 0, s, ix, nw, nbgt);
+  hipLaunchKernelGGL(index_write_lists_kernel, dim3(nw), dim3(256), 0, s, ix, nbgt);
   timing_end(s);
   timing_begin("phsa_index_fill", s);
   hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256),

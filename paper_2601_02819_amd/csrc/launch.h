@@ -34,6 +34,8 @@ struct IndexWs {
   int32_t *off;       // [B*Hkv*T + 1]  list start per (b, g, t)
   int32_t *uoff;      // [B*Hkv*T + 1]  first work unit per (b, g, t)
   int32_t *totals;    // [4]            nnz, n_units, blocks in fin
+  int4 *wsum;         // [ceil(B*Hkv*T / 256)] per 256 (b, g, t): sums of list lengths, units and
+                      //                 finalize flags, then their exclusive offsets
   int32_t *fin;       // [B*Hkv*T]      the (b, g, t) whose dK/dV the finalize writes (not one work unit)
   int32_t *tok;       // [nnz_max]      (query row << 10) | (quarter mask << 6) | slot, ascending row per list
   int32_t *pmap;      // [B*Hkv*Lq*Ksel] list position of each valid (row, slot); partials are
