@@ -21,14 +21,23 @@
 #include "common.h"
 #include "launch.h"
 
+// Selection workgroups for k <= 16: 4 waves (128 rows) with one (hi, lo)
+// chunk buffer take 80 KB of LDS, so two workgroups share a CU and one's
+// VALU-heavy phases (bar, final rank) overlap the other's MFMA chunks.  (One
+// 8-wave workgroup per CU with double-buffered chunks, 160 KB, keeps all its
+// waves in the same phase: 0.78 -> 0.70 ms at 4 x 32k, 1.78 -> 1.59 ms at
+// T = 2048 with 16-token blocks.)
 #ifndef PHSA_SEL_NW
-#define PHSA_SEL_NW 8      // waves per selection workgroup (k <= 16)
+#define PHSA_SEL_NW 4      // waves per selection workgroup (k <= 16)
 #endif
 #ifndef PHSA_SEL_DB
-#define PHSA_SEL_DB true   // double-buffered pass 2 (k <= 16)
+#define PHSA_SEL_DB false  // double-buffered pass 2 (k <= 16)
 #endif
 #ifndef PHSA_SEL_SLACK
 #define PHSA_SEL_SLACK 112 // list capacity beyond 4 k entries
+#endif
+#ifndef PHSA_SEL_CH
+#define PHSA_SEL_CH 64     // blocks per staged chunk (a multiple of 16)
 #endif
 
 namespace phsa {
@@ -860,24 +869,26 @@ __device__ __noinline__ int compact_list(float2 *lp, int n, int k, float *ks) {
   return pos;
 }
 
-template <int D, int G, int KMAXK, int NW, bool DB>
+template <int D, int G, int KMAXK, int NW, bool DB, int CH>
 __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__restrict__ Q,
                                                               const bf16_t *__restrict__ Mh_g,
                                                               const bf16_t *__restrict__ Ml_g,
                                                               const float2 *__restrict__ Mnorm_g,
                                                               int32_t *__restrict__ sel, Geom gm) {
-  constexpr int CH = 64;                  // blocks per chunk
+  constexpr int NT = CH / 16;             // 16-block columns per chunk of CH blocks
   constexpr int RT = 2;                   // 16-row tiles per wave (B fragments are reused across them)
   constexpr int ROWS = NW * 16 * RT;      // query rows per workgroup
   constexpr int NR = 4 * RT;              // rows per lane in the accumulator layout
-  constexpr int MP = D + 8;               // LDS pitch of a staged representative
+  constexpr int MP = D + 8;               // LDS pitch of a staged representative (sizes the staging area)
   constexpr int KB = D / 32;
-  constexpr int TILE = CH * MP;           // bf16 elements of one staged hi (or lo) chunk
-  constexpr int NL = CH * D / (NW * 64 * 8);  // 16-byte loads per thread per hi (or lo) chunk
+  constexpr int TILE = CH * MP;           // bf16 elements reserved per staged hi (or lo) chunk
+  constexpr int TD = CH * D;              // bf16 elements of a chunk copied in (swizzled [CH][D], no padding)
   constexpr int NBUF = DB ? 2 : 1;        // pass 2 buffers (one: two barriers per chunk)
+  constexpr int P1 = 2 * NBUF;            // pass 1 buffers (hi only): chunks in flight P1 - 1
+  constexpr int VPR = D / 8, RPI = 64 / VPR, NI = CH / RPI / NW;  // 1 KB copies per wave per chunk
   constexpr int C4 = 4 * KMAXK + PHSA_SEL_SLACK;  // capacity of a 4-row list: 4 k survivors + one 64-entry append + slack
   constexpr int NGRP = NW * NR;           // lists per workgroup
-  static_assert(NL >= 1 && CH * D == NL * NW * 64 * 8, "chunk staging");
+  static_assert(NI >= 1 && NI * NW * RPI == CH && TD <= TILE, "chunk copies");
   static_assert(C4 >= 4 * KMAXK + 64, "list capacity");
   // staging: pass 1 uses two hi chunks, pass 2 NBUF (hi, lo) pairs; the same bytes
   __shared__ __attribute__((aligned(16))) bf16_t stg[NBUF * 2 * TILE];
@@ -968,27 +979,30 @@ __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__re
   // chunks ending at or below the first row's first local block hold candidates of every row
   const int lo_first = max(0, (gm.q_pos0 + i0) / gm.m - gm.window / gm.m);
 
-  // chunk c (blocks n_init + 64 c ..) into registers, then into an LDS buffer.
-  // Rows past the last block repeat it: such blocks are never candidates.
-  u32x4 ph[NL], pl[NL];
-  auto fetch = [&](int c, bool pass2) {
+  // chunk c (blocks n_init + CH c ..) of src straight into LDS tile dst, in
+  // the swizzled layout (element e of row r at swz<D>(r, e)): NI one-kilobyte
+  // copies per wave, lane l of a copy landing at byte 16 l of it.  Rows past
+  // the last block repeat it: such blocks are never candidates.  The copies
+  // count in vmcnt; a chunk is read after its copies are waited for and a
+  // barrier.
+  auto dma_chunk = [&](const bf16_t *src, int c, bf16_t *dst) {
     const int t0 = gm.n_init + c * CH;
 #pragma unroll
-    for (int x = 0; x < NL; ++x) {
-      const int e = (tid + NW * 64 * x) * 8, row = e / D, col = e % D;
-      const int64_t off = (int64_t)min(t0 + row, gm.T - 1) * D + col;
-      ph[x] = *reinterpret_cast<const u32x4 *>(mh_bg + off);
-      if (pass2) pl[x] = *reinterpret_cast<const u32x4 *>(ml_bg + off);
+    for (int v = 0; v < NI; ++v) {
+      const int blk = wave * NI + v, r = blk * RPI + lane / VPR, cc = (lane % VPR) ^ (r & (VPR - 1));
+      __builtin_amdgcn_global_load_lds(src + (int64_t)min(t0 + r, gm.T - 1) * D + cc * 8,
+                                       (lds_void_t *)(dst + blk * RPI * D), 16, 0, 0);
     }
   };
-  auto stage = [&](bf16_t *hb, bf16_t *lb) {
-#pragma unroll
-    for (int x = 0; x < NL; ++x) {
-      const int e = (tid + NW * 64 * x) * 8, row = e / D, col = e % D;
-      *reinterpret_cast<u32x4 *>(&hb[row * MP + col]) = ph[x];
-      if (lb) *reinterpret_cast<u32x4 *>(&lb[row * MP + col]) = pl[x];
-    }
+  // waits until at most n of this wave's copies are outstanding (n a multiple of NI, at most 2 NI)
+  auto dma_wait_n = [&](int n) {
+    if (n >= 2 * NI) __builtin_amdgcn_s_waitcnt(0x0f70 | (2 * NI));
+    else if (n >= NI) __builtin_amdgcn_s_waitcnt(0x0f70 | NI);
+    else __builtin_amdgcn_s_waitcnt(0x0f70);
   };
+  static_assert(2 * NI < 16, "vmcnt immediate");
+  // the B fragment of 16 representatives (rows n0 .. n0 + 15) for feature slice kb
+  auto frag = [&](const bf16_t *tile, int n0, int kb) { return load_bf16x8(&tile[swz<D>(n0 + l16, kb * 32 + kq)]); };
 
   // ---- pass 1: best two approximate scores of each lane's stripe, per row
   int lo_r[NR];
@@ -999,35 +1013,31 @@ __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__re
     lo_r[rr] = i < gm.Lq ? max(0, (gm.q_pos0 + i) / gm.m - gm.window / gm.m) : 0;
     top1[rr] = top2[rr] = -INFINITY;
   }
-  if (nch > 0) {
-    fetch(0, false);
-    stage(stg, nullptr);
-    if (nch > 1) fetch(1, false);
-  }
-  lds_barrier();
+  // P1 - 1 chunks in flight ahead of the one in use
+  for (int j = 0; j < P1 - 1 && j < nch; ++j) dma_chunk(mh_bg, j, stg + j * TD);
   auto keep2 = [&](int rr, float v) {  // best two of the stripe (top1 >= top2)
     top2[rr] = __builtin_amdgcn_fmed3f(top1[rr], top2[rr], v);  // the middle of the three
     top1[rr] = fmaxf(top1[rr], v);
   };
   for (int c = 0; c < nch; ++c) {
-    const int buf = c & 1;
-    // the other buffer held chunk c - 1, which every wave finished before the last barrier
-    if (c + 1 < nch) stage(stg + (buf ^ 1) * TILE, nullptr);
-    if (c + 2 < nch) fetch(c + 2, false);
-    const bf16_t *hb = stg + buf * TILE;
+    dma_wait_n(min(P1 - 2, nch - 1 - c) * NI);  // chunk c landed (later chunks may still be in flight)
+    lds_barrier();
+    // buffer (c + P1 - 1) % P1 held chunk c - 1, which every wave finished before this barrier
+    if (c + P1 - 1 < nch) dma_chunk(mh_bg, c + P1 - 1, stg + ((c + P1 - 1) % P1) * TD);
+    const bf16_t *hb = stg + (c % P1) * TD;
     const int t0 = gm.n_init + c * CH;
-    f32x4 acc[RT][4];
+    f32x4 acc[RT][NT];
 #pragma unroll
     for (int j = 0; j < RT; ++j)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) acc[j][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int nt = 0; nt < NT; ++nt) acc[j][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      bf16x8 bh[4];
+      bf16x8 bh[NT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) bh[nt] = load_bf16x8(&hb[(nt * 16 + l16) * MP + kb * 32 + kq]);
+      for (int nt = 0; nt < NT; ++nt) bh[nt] = frag(hb, nt * 16, kb);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
+      for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
         for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(ah[j][kb], bh[nt], acc[j][nt]);
     }
@@ -1035,16 +1045,16 @@ __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__re
 #pragma unroll
       for (int rr = 0; rr < NR; ++rr)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) keep2(rr, acc[rr >> 2][nt][rr & 3]);
+        for (int nt = 0; nt < NT; ++nt) keep2(rr, acc[rr >> 2][nt][rr & 3]);
     } else {
 #pragma unroll
       for (int rr = 0; rr < NR; ++rr)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
+        for (int nt = 0; nt < NT; ++nt)
           keep2(rr, t0 + nt * 16 + l16 < lo_r[rr] ? acc[rr >> 2][nt][rr & 3] : -INFINITY);
     }
-    lds_barrier();
   }
+  lds_barrier();  // pass 2 copies into the same buffers
 
   // ---- bar of each row: the k-th largest of its 32 stripe lower bounds (the
   // largest v with at least k of them >= v), k distinct blocks whose exact
@@ -1109,44 +1119,44 @@ __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__re
   // one chunk's exact scores (three chains over hi / lo staged chunks), appended
   auto pass2_chunk = [&](const bf16_t *hb, const bf16_t *lb, int c) {
     const int t0 = gm.n_init + c * CH;
-    f32x4 acc[RT][4];
+    f32x4 acc[RT][NT];
 #pragma unroll
     for (int j = 0; j < RT; ++j)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) acc[j][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int nt = 0; nt < NT; ++nt) acc[j][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      bf16x8 bh[4], bl[4];
+      bf16x8 bh[NT], bl[NT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        bh[nt] = load_bf16x8(&hb[(nt * 16 + l16) * MP + kb * 32 + kq]);
-        bl[nt] = load_bf16x8(&lb[(nt * 16 + l16) * MP + kb * 32 + kq]);
+      for (int nt = 0; nt < NT; ++nt) {
+        bh[nt] = frag(hb, nt * 16, kb);
+        bl[nt] = frag(lb, nt * 16, kb);
       }
       // each chain over all RT x 4 accumulators in turn, so that consecutive
       // MFMAs are independent; every accumulator still takes hi.hi, hi.lo,
       // lo.hi of each kb in that order
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
+      for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
         for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(ah[j][kb], bh[nt], acc[j][nt]);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
+      for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
         for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(ah[j][kb], bl[nt], acc[j][nt]);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
+      for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
         for (int j = 0; j < RT; ++j) acc[j][nt] = mfma16x16x32(al[j][kb], bh[nt], acc[j][nt]);
     }
-    float lowv[4];                           // the entries' low words, per block column
+    float lowv[NT];                           // the entries' low words, per block column
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) lowv[nt] = __uint_as_float(low_lane - (uint32_t)(t0 + nt * 16));
+    for (int nt = 0; nt < NT; ++nt) lowv[nt] = __uint_as_float(low_lane - (uint32_t)(t0 + nt * 16));
     auto appends = [&](auto inner_c) {
       constexpr bool INNER = decltype(inner_c)::value;  // every block is a candidate of every row
 #pragma unroll
       for (int rr = 0; rr < NR; ++rr) {
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
+        for (int nt = 0; nt < NT; ++nt) {
           if (cnt[rr] > C4 - 64) compact(rr);
           const float sc = acc[rr >> 2][nt][rr & 3];
           // wave masks straight from the compares (FCMP_OGE = 3, ICMP_SLT = 40)
@@ -1168,28 +1178,30 @@ __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__re
     if (t0 + CH <= lo_first) appends(std::true_type{});
     else appends(std::false_type{});
   };
-  if (DB) {
+  if (DB) {  // chunk c + 1 is copied into the other (hi, lo) pair while chunk c is used
     if (nch > 0) {
-      fetch(0, true);
-      stage(stg, stg + TILE);
-      if (nch > 1) fetch(1, true);
+      dma_chunk(mh_bg, 0, stg);
+      dma_chunk(ml_bg, 0, stg + TD);
+    }
+    for (int c = 0; c < nch; ++c) {
+      dma_wait_n(0);
+      lds_barrier();  // chunk c landed; every wave finished chunk c - 1, whose pair is now free
+      bf16_t *cur = stg + (c & 1) * 2 * TD, *nxt = stg + ((c + 1) & 1) * 2 * TD;
+      if (c + 1 < nch) {
+        dma_chunk(mh_bg, c + 1, nxt);
+        dma_chunk(ml_bg, c + 1, nxt + TD);
+      }
+      pass2_chunk(cur, cur + TD, c);
     }
     lds_barrier();
-    for (int c = 0; c < nch; ++c) {
-      const int buf = c & 1;
-      if (c + 1 < nch) stage(stg + (buf ^ 1) * 2 * TILE, stg + (buf ^ 1) * 2 * TILE + TILE);
-      if (c + 2 < nch) fetch(c + 2, true);
-      pass2_chunk(stg + buf * 2 * TILE, stg + buf * 2 * TILE + TILE, c);
-      lds_barrier();
-    }
   } else {
-    if (nch > 0) fetch(0, true);
     for (int c = 0; c < nch; ++c) {
+      lds_barrier();  // every wave finished chunk c - 1
+      dma_chunk(mh_bg, c, stg);
+      dma_chunk(ml_bg, c, stg + TD);
+      dma_wait_n(0);
       lds_barrier();
-      stage(stg, stg + TILE);
-      lds_barrier();
-      if (c + 1 < nch) fetch(c + 1, true);
-      pass2_chunk(stg, stg + TILE, c);
+      pass2_chunk(stg, stg + TD, c);
     }
     lds_barrier();
   }
@@ -1326,11 +1338,11 @@ static hipError_t launch_select_mfma(const Geom &g, const void *Q, const float *
   timing_begin("phsa_select", s);
   if (g.top_k <= 16) {
     const dim3 grid((g.Lq + PHSA_SEL_NW * 32 - 1) / (PHSA_SEL_NW * 32), g.B * g.Hkv);
-    hipLaunchKernelGGL((select_mfma_kernel<D, G, 16, PHSA_SEL_NW, PHSA_SEL_DB>), grid, dim3(PHSA_SEL_NW * 64), 0, s,
+    hipLaunchKernelGGL((select_mfma_kernel<D, G, 16, PHSA_SEL_NW, PHSA_SEL_DB, PHSA_SEL_CH>), grid, dim3(PHSA_SEL_NW * 64), 0, s,
                        static_cast<const bf16_t *>(Q), mh, ml, mnorm, sel, g);
   } else {
     const dim3 grid((g.Lq + 255) / 256, g.B * g.Hkv);
-    hipLaunchKernelGGL((select_mfma_kernel<D, G, 32, 8, false>), grid, dim3(512), 0, s,
+    hipLaunchKernelGGL((select_mfma_kernel<D, G, 32, 8, false, 64>), grid, dim3(512), 0, s,
                        static_cast<const bf16_t *>(Q), mh, ml, mnorm, sel, g);
   }
   timing_end(s);
