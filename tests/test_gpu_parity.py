@@ -33,6 +33,8 @@ SMALL = [
     small("k32_init3", 1, 4096, 2, 1, 128, 32, 3, 192),
     small("one_block", 1, 64, 2, 1, 128, 4, 1, 0),
     small("fp32_g2", 1, 1024, 4, 2, 128, 3, 1, 64, dtype="fp32"),
+    # 3 x 92 = 276 block lists: the list scan spans two workgroups, the second ragged
+    small("scan_ragged", 3, 5888, 2, 1, 64, 4, 1, 64),
     WORKLOADS["tiny_fp32"],
 ]
 
