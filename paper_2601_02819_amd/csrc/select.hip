@@ -698,7 +698,6 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
 }
 
 // bf16 inputs: scoring on the matrix cores, selection by a bar and a short exact rank.
-// bf16 inputs: scoring on the matrix cores, selection by a bar and a short exact rank.
 //
 // Scores.  The group's query heads are summed in float32
 // (sum_h q_h . M = (sum_h q_h) . M), and both that sum and the float32
@@ -709,11 +708,14 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
 // made on these sums before the (positive) softmax scale, which orders the
 // blocks the same way.
 //
-// Tiling.  A workgroup of 8 waves takes 256 query rows of one (b, g); wave w
-// owns two 16-row tiles (rows 32w..32w+31), so every representative fragment
-// read from LDS feeds two MFMAs, and one staged chunk of 64 representatives
-// serves all 256 rows.  Chunks are staged through LDS from registers that were
-// loaded one chunk ahead, double-buffered so that a chunk costs one barrier.
+// Tiling.  A workgroup of NW waves takes 32 NW query rows of one (b, g); wave
+// w owns two 16-row tiles (rows 32w..32w+31), so every representative fragment
+// read from LDS feeds two MFMAs, and one staged chunk of CH representatives
+// serves all rows of the workgroup.  Chunks are copied from global memory
+// straight into swizzled LDS tiles (global_load_lds); pass 1 keeps the next
+// chunk(s) in flight, pass 2 one or two (hi, lo) pairs (DB).  With k <= 16
+// the kernel runs with 4 waves and one pair: 80 KB of LDS, two workgroups per
+// CU, whose phases then overlap.
 // In the accumulator layout lane (q4, l16) holds, per tile, the scores of rows
 // 4 q4 + r (r = 0..3) for blocks t0 + 16 nt + l16: the 16 lanes of a
 // quarter-wave see every block of their rows, each lane a fixed residue of
@@ -721,14 +723,13 @@ __global__ __launch_bounds__(256) void select_softmax_mfma_kernel(const bf16_t *
 //
 // Top-k in two passes over the candidate blocks:
 //   pass 1: a single hi.hi chain gives approximate scores.  The dropped terms
-//           hi.lo + lo.hi are bounded by 2^-7 (1 + 2^-8)^2 sum |q_c M_c| <=
-//           2^-7 (1 + 2^-8)^2 |q| |M| (each bf16 part is within 2^-8 of its
-//           value; Cauchy-Schwarz), and float32 accumulation of the 3 d terms
-//           adds below 2^-15 of that sum, so s_exact >= s_approx - eps with
-//           eps = 1.024 * 2^-7 |q| |M|.  One margin per row and chunk of 64
-//           blocks, taken with the largest |M| of the chunk, bounds every
-//           block of the chunk, and every lane keeps the best two of these
-//           lower bounds in its stripe for each of its rows.  A row's 32
+//           obey |q_hi . M_lo + q_lo . M_hi| <= |q_hi| |M_lo| + |q_lo| |M_hi|
+//           (Cauchy-Schwarz on each), and float32 accumulation of the chains
+//           adds below 2^-15 |q_hi| |M_hi|.  With the largest |M_hi| and |M_lo|
+//           over the (b, g)'s blocks (select_split_kernel stores every
+//           block's), one margin per row bounds every block: s_exact >=
+//           s_approx - margin.  Every lane keeps the best two of these lower
+//           bounds in its stripe for each of its rows.  A row's 32
 //           stripe tops belong to 32 distinct blocks, so the k-th largest of
 //           them (the bar) lies below the row's k-th best exact score.
 //   pass 2: the exact scores are computed and those >= bar are appended to a
@@ -890,7 +891,7 @@ __global__ __launch_bounds__(NW * 64) void select_mfma_kernel(const bf16_t *__re
   constexpr int NGRP = NW * NR;           // lists per workgroup
   static_assert(NI >= 1 && NI * NW * RPI == CH && TD <= TILE, "chunk copies");
   static_assert(C4 >= 4 * KMAXK + 64, "list capacity");
-  // staging: pass 1 uses two hi chunks, pass 2 NBUF (hi, lo) pairs; the same bytes
+  // staging: pass 1 uses P1 hi chunks, pass 2 NBUF (hi, lo) pairs; the same bytes
   __shared__ __attribute__((aligned(16))) bf16_t stg[NBUF * 2 * TILE];
   __shared__ __attribute__((aligned(16))) float2 lists[NGRP * C4];  // candidate entries; bar scratch first
   __shared__ float kth_s[NGRP * 4];
