@@ -241,8 +241,8 @@ __device__ __forceinline__ Counts3 list_counts(int c, int unit_tokens, bool live
   return Counts3{c, nu, live && nu != 1 ? 1 : 0};
 }
 
-// Exclusive scan of v over a 256-thread workgroup (x, then y, then z
-// independently); tot receives the workgroup's sums.  Holds barriers.
+// Exclusive scan of v over a 256-thread workgroup (c, nu and f each on its
+// own); tot receives the workgroup's sums.  Holds barriers.
 __device__ __forceinline__ Counts3 block_scan3(Counts3 v, Counts3 &tot) {
   __shared__ Counts3 wsum_s[4];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -362,9 +362,7 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
   // Workgroups are dealt to the 8 XCDs in turn (each XCD its own L2), so the
   // grid is renumbered to give each XCD one contiguous range of (bg, w): a
   // list's cache lines are then written through one L2.
-  const int nwg = gridDim.x * gridDim.y, lin = blockIdx.x + blockIdx.y * gridDim.x;
-  const int xcd = lin & 7, q8 = nwg >> 3, r8 = nwg & 7;
-  const int logical = xcd * q8 + min(xcd, r8) + (lin >> 3);
+  const int logical = xcd_item(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y);
   const int w = logical % gridDim.x, bg = logical / gridDim.x, tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int32_t *tile_off = ix.cntw + ((int64_t)bg * ix.W + w) * gm.T;
