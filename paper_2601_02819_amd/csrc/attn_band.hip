@@ -305,8 +305,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
 #pragma unroll
       for (int u = 0; u < NP; ++u) load_pos(t0 + 8 * NP + wave * 2 + half + 8 * u, pa[u], pb[u]);
     }
-    for (int e = l32 * 8; e < G * D; e += 256) {
-      const int hh = e / D, cc = e - hh * D;
+    // every lane runs the feature loop: the slot positions are shuffled from
+    // lanes of the half-wave; with G * D < 256 features, lanes past them only
+    // take part in the shuffles
+    for (int e0 = 0; e0 < G * D; e0 += 256) {
+      const int e = e0 + l32 * 8;
+      const bool act = e < G * D;
+      const int hh = act ? e / D : 0, cc = act ? e - hh * D : 0;
       float M[NP], L[NP], a[NP][8];
 #pragma unroll
       for (int u = 0; u < NP; ++u) {
@@ -324,7 +329,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
           for (int u = 0; u < NP; ++u) {
             const int s = s0 + k;
             const int p = s < ns ? rs[u].pos(s, half) : -1;
-            const bool sp = p >= 0 && p < ix.band_base;  // a sparse partial (not the band slot)
+            const bool sp = act && p >= 0 && p < ix.band_base;  // a sparse partial (not the band slot)
             q[u][k] = sp ? ml[(int64_t)p * G + hh] : make_float2(-INFINITY, 0.f);
             raw[u][k] = sp ? ld_stream16(opart + ((int64_t)p * G + hh) * D + cc) : make_uint4(0u, 0u, 0u, 0u);
           }
@@ -338,8 +343,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_band_kernel(const bf16_t *__r
         const int t = t0 + wave * 2 + half + 8 * u, i = i0 + t;
         const bool row_ok = i <= i1;
         const int r = t * G + hh;
-        if (row_ok && *oks(r)) fold_partial(M[u], L[u], a[u], *mls(r), *reinterpret_cast<const uint4 *>(orow(r) + cc));
-        if (!row_ok) continue;
+        if (!row_ok || !act) continue;
+        if (*oks(r)) fold_partial(M[u], L[u], a[u], *mls(r), *reinterpret_cast<const uint4 *>(orow(r) + cc));
         const float inv = L[u] > 0.f ? 1.f / L[u] : 0.f;
         bf16_t outv[8];
 #pragma unroll
@@ -512,8 +517,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
     rs[u] = RowSlots(ix.pmap, ((int64_t)bg * gm.Lq + (row_ok ? i : i0)) * gm.ksel, row_ok, gm.ksel, half, l32);
     ns = max(ns, rs[u].slots());
   }
-  for (int e = l32 * 8; e < G * D; e += 256) {
-    const int hh = e / D, cc = e - hh * D;
+  // every lane runs the feature loop (the slot positions are shuffled from
+  // lanes of the half-wave); with G * D < 256, lanes past the features only shuffle
+  for (int e0 = 0; e0 < G * D; e0 += 256) {
+    const int e = e0 + l32 * 8;
+    const bool act = e < G * D;
+    const int hh = act ? e / D : 0, cc = act ? e - hh * D : 0;
     float a[NP][8];
 #pragma unroll
     for (int u = 0; u < NP; ++u)
@@ -527,8 +536,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
         for (int u = 0; u < NP; ++u) {
           const int s = s0 + k;
           const int p = s < ns ? rs[u].pos(s, half) : -1;
-          raw[u][k] = (p >= 0 && p < ix.band_base) ? ld_stream16(dqpart + ((int64_t)p * G + hh) * D + cc)
-                                                    : make_uint4(0u, 0u, 0u, 0u);
+          raw[u][k] = (act && p >= 0 && p < ix.band_base) ? ld_stream16(dqpart + ((int64_t)p * G + hh) * D + cc)
+                                                           : make_uint4(0u, 0u, 0u, 0u);
         }
 #pragma unroll
       for (int k = 0; k < U; ++k)
@@ -542,7 +551,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_band_dq_kernel(
 #pragma unroll
     for (int u = 0; u < NP; ++u) {
       const int t = wave * 2 + half + 8 * u, i = i0 + t;
-      if (i > i1) continue;
+      if (i > i1 || !act) continue;
       const int r = t * G + hh;
       if (oks[r]) {
         const bf16_t *pv = &KV0[r * SP + cc];

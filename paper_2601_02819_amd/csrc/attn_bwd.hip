@@ -401,8 +401,13 @@ __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restri
   const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   const RowSlots rs(pmap, xr * gm.ksel, row_ok, gm.ksel, half, l32);
   const int ns = rs.slots();
-  for (int e = l32 * 8; e < G * D; e += 256) {
-    const int hh = e / D, c = e - hh * D;
+  // Every lane runs the feature loop: the slot positions are shuffled from
+  // lanes of the half-wave.  With G * D < 256 features, lanes past them only
+  // take part in the shuffles.
+  for (int e0 = 0; e0 < G * D; e0 += 256) {
+    const int e = e0 + l32 * 8;
+    const bool act = e < G * D;
+    const int hh = act ? e / D : 0, c = act ? e - hh * D : 0;
     float a[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) a[k] = 0.f;
@@ -412,7 +417,7 @@ __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restri
       for (int k = 0; k < U; ++k) {
         const int s = s0 + k;
         const int p = s < ns ? rs.pos(s, half) : -1;
-        raw[k] = p >= 0 ? ld_stream16(dqpart + ((int64_t)p * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
+        raw[k] = act && p >= 0 ? ld_stream16(dqpart + ((int64_t)p * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
       }
 #pragma unroll
       for (int k = 0; k < U; ++k) {
@@ -421,7 +426,7 @@ __global__ __launch_bounds__(256) void dq_combine_kernel(const int32_t *__restri
         for (int j = 0; j < 8; ++j) a[j] += bf16_to_f32(pv[j]);
       }
     }
-    if (!row_ok) continue;
+    if (!row_ok || !act) continue;
     bf16_t outv[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) outv[k] = f32_to_bf16(a[k]);

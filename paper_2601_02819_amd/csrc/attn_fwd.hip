@@ -213,8 +213,13 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
   const int b = bg / gm.Hkv, g = bg - b * gm.Hkv;
   const RowSlots rs(pmap, xr * gm.ksel, row_ok, gm.ksel, half, l32);
   const int ns = rs.slots();
-  for (int e = l32 * 8; e < G * D; e += 256) {
-    const int hh = e / D, c = e - hh * D;
+  // Every lane runs the feature loop: the slot positions are shuffled from
+  // lanes of the half-wave.  With G * D < 256 features, lanes past them only
+  // take part in the shuffles.
+  for (int e0 = 0; e0 < G * D; e0 += 256) {
+    const int e = e0 + l32 * 8;
+    const bool act = e < G * D;
+    const int hh = act ? e / D : 0, c = act ? e - hh * D : 0;
     // online merge in slot order: running max M (log2 units), sum L, sum a
     float M = -INFINITY, L = 0.f, a[8];
 #pragma unroll
@@ -226,7 +231,7 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
       for (int k = 0; k < U; ++k) {
         const int s = s0 + k;
         const int p = s < ns ? rs.pos(s, half) : -1;
-        const bool ok = p >= 0;
+        const bool ok = act && p >= 0;
         q[k] = ok ? ml[(int64_t)p * G + hh] : make_float2(-INFINITY, 0.f);
         raw[k] = ok ? ld_stream16(opart + ((int64_t)p * G + hh) * D + c) : make_uint4(0u, 0u, 0u, 0u);
       }
@@ -242,7 +247,7 @@ __global__ __launch_bounds__(256) void attn_fwd_combine_kernel(const int32_t *__
         M = mn;
       }
     }
-    if (!row_ok) continue;
+    if (!row_ok || !act) continue;
     const float inv = L > 0.f ? 1.f / L : 0.f;
     bf16_t outv[8];
 #pragma unroll

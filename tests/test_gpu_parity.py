@@ -35,6 +35,11 @@ SMALL = [
     small("fp32_g2", 1, 1024, 4, 2, 128, 3, 1, 64, dtype="fp32"),
     # 3 x 92 = 276 block lists: the list scan spans two workgroups, the second ragged
     small("scan_ragged", 3, 5888, 2, 1, 64, 4, 1, 64),
+    # the widest selection the entry points accept: Ksel = 15 + 16 + 1 + 32 = 64 slots
+    small("ksel64", 1, 4096, 4, 2, 64, 32, 15, 1024),
+    # G * d = 64 features (fewer than a half-wave's 32 lanes x 8) with up to 26 slots per row:
+    # the merges shuffle slot positions from every lane of the half-wave
+    small("g1_d64_k24", 1, 4096, 2, 2, 64, 24, 1, 0),
     WORKLOADS["tiny_fp32"],
 ]
 
