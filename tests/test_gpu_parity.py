@@ -40,6 +40,9 @@ SMALL = [
     # G * d = 64 features (fewer than a half-wave's 32 lanes x 8) with up to 26 slots per row:
     # the merges shuffle slot positions from every lane of the half-wave
     small("g1_d64_k24", 1, 4096, 2, 2, 64, 24, 1, 0),
+    small("g1_k20", 1, 2048, 2, 2, 128, 20, 1, 0),   # G * d = 128 with up to 22 slots per row
+    # one query row (the last position) against 2048 keys
+    Workload("one_row", 1, 1, 2048, 4, 2, 128, 64, 6, 1, 0, "bf16"),
     WORKLOADS["tiny_fp32"],
 ]
 
