@@ -131,10 +131,14 @@ def test_decode_32k():
     log(f"[fullsize] {wl.name}: all {sel_g.shape[0] * sel_g.shape[1]} rows checked, {exempt} exempt")
 
 
-@pytest.mark.parametrize("L,window,n_init,top_k", [(4096, 0, 1, 12), (2048, 256, 2, 5), (192, 0, 1, 12)])
-def test_decode_variants(L, window, n_init, top_k):
-    """Decode against short caches, local windows, several init blocks, fewer candidates than k."""
-    wl = WORKLOADS["decode_32k"].replace(batch=8, seqlen_k=L, window=window, n_init_blocks=n_init, top_k=top_k)
+@pytest.mark.parametrize("L,window,n_init,top_k,m", [(4096, 0, 1, 12, 64), (2048, 256, 2, 5, 64), (192, 0, 1, 12, 64),
+                                                      (8192, 1024, 15, 32, 64),   # Ksel = 64, the widest accepted
+                                                      (4096, 512, 8, 16, 16)])    # the paper's geometry (57 slots)
+def test_decode_variants(L, window, n_init, top_k, m):
+    """Decode against short caches, local windows, several init blocks, fewer candidates than k,
+    the widest selection, and 16-token blocks."""
+    wl = WORKLOADS["decode_32k"].replace(batch=8, seqlen_k=L, window=window, n_init_blocks=n_init, top_k=top_k,
+                                         block_size=m)
     cfg = cfg_of(wl)
     host, dev = device_inputs(wl, 2, with_grad_out=False)
     kc = phsa.compress(dev["k"], dev["punct"], cfg)
