@@ -33,6 +33,7 @@ CASES = [
     small("g1_d64", 1, 768, 4, 4, 64, 4, 1, 0),
     small("g4_k14", 1, 2048, 16, 4, 128, 14, 1, 0),
     small("k32_init3", 1, 4096, 2, 1, 128, 32, 3, 192),
+    small("ksel64_g2_d64", 1, 4096, 4, 2, 64, 32, 15, 1024),   # Ksel = 64, the widest accepted
     small("k7_tail_rows", 1, 2048, 4, 2, 128, 7, 1, 0, Lq=700),     # query rows at the end of the keys
     small("fp32_g2", 1, 1024, 4, 2, 128, 3, 1, 64, dtype="fp32"),
     small("fp32_g4_d64", 2, 640, 8, 2, 64, 9, 1, 0, dtype="fp32"),
