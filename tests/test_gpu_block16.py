@@ -30,6 +30,7 @@ CASES = [
     wl_("m16_ksel64", 1, 4096, 4, 2, 64, 16, 32, 15, 256),  # Ksel = 15 + 16 + 1 + 32 = 64, the widest accepted
     wl_("m16_d64_k20", 1, 4096, 4, 2, 64, 16, 20, 2, 128),  # band merges at G * d = 128 with up to 21 slots
     wl_("m16_one_row", 1, 2048, 4, 2, 128, 16, 12, 8, 256, Lq=1),  # a single query row (band rows of one token)
+    wl_("m16_g8_d64_win", 1, 1024, 8, 1, 64, 16, 6, 2, 128),  # band kernels at G = 8, head dim 64
     wl_("m16_tail_rows", 1, 2048, 4, 2, 128, 16, 10, 8, 256, Lq=333),
     # fewer query rows than one wave of the index kernels (band on), and one row
     # alone in the last 256-row index tile (no window)

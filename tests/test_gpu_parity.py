@@ -41,6 +41,10 @@ SMALL = [
     # the merges shuffle slot positions from every lane of the half-wave
     small("g1_d64_k24", 1, 4096, 2, 2, 64, 24, 1, 0),
     small("g1_k20", 1, 2048, 2, 2, 128, 20, 1, 0),   # G * d = 128 with up to 22 slots per row
+    # band kernels at group sizes no other case gives them a window at
+    small("g8_win", 1, 2048, 8, 1, 128, 6, 1, 128),
+    small("g4_win_d128", 1, 2048, 8, 2, 128, 6, 1, 128),
+    small("g1_d64_win", 1, 2048, 2, 2, 64, 6, 1, 128),
     # one query row (the last position) against 2048 keys
     Workload("one_row", 1, 1, 2048, 4, 2, 128, 64, 6, 1, 0, "bf16"),
     WORKLOADS["tiny_fp32"],
