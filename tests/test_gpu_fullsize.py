@@ -137,8 +137,21 @@ def test_decode_32k():
 def test_decode_variants(L, window, n_init, top_k, m):
     """Decode against short caches, local windows, several init blocks, fewer candidates than k,
     the widest selection, and 16-token blocks."""
-    wl = WORKLOADS["decode_32k"].replace(batch=8, seqlen_k=L, window=window, n_init_blocks=n_init, top_k=top_k,
-                                         block_size=m)
+    _decode_check(WORKLOADS["decode_32k"].replace(batch=8, seqlen_k=L, window=window, n_init_blocks=n_init,
+                                                  top_k=top_k, block_size=m))
+
+
+@pytest.mark.parametrize("Hq,Hkv,d", [(8, 8, 128), (16, 4, 128), (16, 2, 128), (16, 8, 64), (8, 1, 64)])
+def test_decode_head_layouts(Hq, Hkv, d):
+    """Decode with groups of 1, 4 and 8 query heads per KV head and head dim 64."""
+    _decode_check(WORKLOADS["decode_32k"].replace(batch=4, seqlen_k=4096, n_heads_q=Hq, n_heads_kv=Hkv, head_dim=d,
+                                                  window=256, n_init_blocks=2, top_k=9))
+
+
+def _decode_check(wl):
+    L, top_k, n_init, window = wl.seqlen_k, wl.top_k, wl.n_init_blocks, wl.window
+    log(f"[fullsize] decode {wl.batch} x {L} Hq={wl.n_heads_q} Hkv={wl.n_heads_kv} d={wl.head_dim} m={wl.block_size} "
+        f"k={top_k} init={n_init} w={window}")
     cfg = cfg_of(wl)
     host, dev = device_inputs(wl, 2, with_grad_out=False)
     kc = phsa.compress(dev["k"], dev["punct"], cfg)
