@@ -45,6 +45,9 @@ SMALL = [
     small("g8_win", 1, 2048, 8, 1, 128, 6, 1, 128),
     small("g4_win_d128", 1, 2048, 8, 2, 128, 6, 1, 128),
     small("g1_d64_win", 1, 2048, 2, 2, 64, 6, 1, 128),
+    # selection with more than 16 picks at groups of 8 and 4 heads
+    small("k24_g8", 1, 2048, 8, 1, 128, 24, 1, 0),
+    small("k20_g4_d64", 1, 2048, 8, 2, 64, 20, 1, 0),
     # one query row (the last position) against 2048 keys
     Workload("one_row", 1, 1, 2048, 4, 2, 128, 64, 6, 1, 0, "bf16"),
     WORKLOADS["tiny_fp32"],
