@@ -33,6 +33,9 @@ SMALL = [
     small("k32_init3", 1, 4096, 2, 1, 128, 32, 3, 192),
     small("one_block", 1, 64, 2, 1, 128, 4, 1, 0),
     small("fp32_g2", 1, 1024, 4, 2, 128, 3, 1, 64, dtype="fp32"),
+    small("fp32_g8", 1, 1024, 8, 1, 128, 5, 2, 64, dtype="fp32"),
+    small("fp32_g1_d64", 1, 1024, 2, 2, 64, 6, 1, 0, dtype="fp32"),
+    small("fp32_ksel64", 1, 4096, 4, 2, 64, 32, 15, 1024, dtype="fp32"),   # Ksel = 64 in float32
     # 3 x 92 = 276 block lists: the list scan spans two workgroups, the second ragged
     small("scan_ragged", 3, 5888, 2, 1, 64, 4, 1, 64),
     # the widest selection the entry points accept: Ksel = 15 + 16 + 1 + 32 = 64 slots
