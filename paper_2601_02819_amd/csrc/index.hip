@@ -461,19 +461,26 @@ __global__ __launch_bounds__(256) void index_fill_kernel(const int32_t *__restri
 }
 
 hipError_t launch_build_index(const Geom &g, const int32_t *sel, const IndexWs &ix, hipStream_t s) {
+  // Each launch's status is taken right after it: the attention kernels gather
+  // through these lists, so a failed pass must stop the chain before them.
+  hipError_t e;
   const int nbgt = g.B * g.Hkv * g.T;
   const size_t lds = index_lds_bytes(g);
   timing_begin("phsa_index_count", s);
   hipLaunchKernelGGL(index_count_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256), lds, s, sel, g, ix);
   timing_end(s);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   const int nw = (nbgt + 255) / 256;  // list-scan workgroups (ix.wsum entries)
   timing_begin("phsa_index_scan_tiles", s);
   hipLaunchKernelGGL(index_scan_tiles_kernel, dim3(nw), dim3(256), 0, s, g, ix, nbgt);
   timing_end(s);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   timing_begin("phsa_index_scan_lists", s);
   hipLaunchKernelGGL(index_scan_sums_kernel, dim3(1), dim3(256), 0, s, ix, nw, nbgt);
-  hipLaunchKernelGGL(index_write_lists_kernel, dim3(nw), dim3(256), 0, s, ix, nbgt);
+  if ((e = hipGetLastError()) == hipSuccess)
+    hipLaunchKernelGGL(index_write_lists_kernel, dim3(nw), dim3(256), 0, s, ix, nbgt);
   timing_end(s);
+  if (e != hipSuccess || (e = hipGetLastError()) != hipSuccess) return e;
   timing_begin("phsa_index_fill", s);
   hipLaunchKernelGGL(index_fill_kernel, dim3(ix.W, g.B * g.Hkv), dim3(256),
                      lds + (size_t)g.T * (sizeof(int32_t) + sizeof(uint64_t)), s, sel,
